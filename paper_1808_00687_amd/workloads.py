@@ -1,0 +1,323 @@
+"""Seeded synthetic workloads for the WFST Viterbi / LSD decoder.
+
+This module only draws random inputs (graphs, acoustic log-likelihoods and
+decode options).  It holds none of the decoding arithmetic: the serial CPU
+oracle and the HIP path both receive the same arrays from here and share
+nothing else.
+
+The paper measures on Switchboard / hub5e-swb with trained CTC and hybrid
+acoustic models and n-gram LMs (Sec. 2, Fig. 1; Sec. 3, Fig. 3).  None of
+those assets exist here, so five synthetic workloads of the same structure
+stand in for them:
+
+1. tiny random WFST (2,000 states), 50 frames, beam 12;
+2. medium WFST (200k states, 1M arcs, Zipf-like out-degree), 500 frames,
+   max-active 7,000, lattice beam 8;
+3. LVCSR-scale HCLG-like WFST (10M states, 25M arcs, 6,000 senones,
+   olabels on 10% of arcs), 1,000 frames, max-active 10,000, lattice beam 8;
+4. the graph of (3) shared by 64 utterances of 300-1,500 frames;
+5. a CTC-style graph (5M states, 15M arcs, a blank self-loop on every state)
+   with blank-dominated frames, decoded frame-synchronously and
+   label-synchronously (Sec. 2, Alg. 1).
+
+Recipe (every draw comes from ``numpy.random.default_rng`` seeded with
+``SeedSequence([1808, 687, cfg, purpose, utt])``; purpose 0 = graph,
+1 = log-likelihoods):
+
+* arcs are generated state by state, so ``src`` is sorted; the start state is
+  0; no final weights;
+* an emitting arc has ``dst`` uniform in [0, N) and ``ilabel`` uniform in
+  [1, L] (ilabel i reads log-likelihood column i-1; 0 is epsilon);
+* an epsilon arc has ``dst`` uniform in (s, N), so the epsilon subgraph is
+  acyclic; an epsilon arc drawn on the last state is made emitting;
+* weights are Exp(mean) drawn in float64 and cast to float32;
+* log-likelihoods are ``z - logsumexp(z)`` per row with ``z ~ N(0, sigma)``
+  drawn in float64, cast to float32, row-major [T x L].
+
+The Zipf-like out-degree of configs 2, 3 and 5 is a rank law
+``deg(r) = clip(floor(C * r**-1.2), 1, 200)`` for ranks r = 1..N with C the
+largest constant whose total does not exceed the arc budget; the residual
+arcs go, one each, to randomly chosen degree-1 states, and a seeded random
+permutation maps ranks to states.  (An i.i.d. Zipf(1.2) draw cannot give a
+mean degree of 2.5-5 at a cap of 200, so the rank law is used instead.)
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional
+
+import numpy as np
+
+GRAPH = 0
+LOGLIKES = 1
+
+
+def rng_for(cfg: int, purpose: int, utt: int = 0) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([1808, 687, cfg, purpose, utt]))
+
+
+@dataclasses.dataclass
+class Graph:
+    num_states: int
+    src: np.ndarray      # int32 [E], sorted ascending
+    dst: np.ndarray      # int32 [E]
+    ilabel: np.ndarray   # int32 [E], 0 = epsilon, i >= 1 reads column i-1
+    olabel: np.ndarray   # int32 [E], 0 = no output
+    weight: np.ndarray   # float32 [E]
+    start: int = 0
+    final: Optional[np.ndarray] = None  # float32 [N] or None (all final, cost 0)
+
+    @property
+    def num_arcs(self) -> int:
+        return int(self.src.shape[0])
+
+
+@dataclasses.dataclass
+class DecodeOpts:
+    beam: float
+    max_active: int = 0            # <= 0: unlimited
+    lattice_beam: float = -1.0     # < 0: no lattice
+    blank_threshold: float = 2.0   # > 1: frame synchronous
+    blank_id: int = 0
+
+
+@dataclasses.dataclass
+class Workload:
+    cfg: int
+    name: str
+    graph: Graph
+    num_labels: int
+    loglikes: List[np.ndarray]  # one float32 [T x L] array per utterance
+    opts: DecodeOpts
+
+
+# --------------------------------------------------------------------------
+# graph pieces
+# --------------------------------------------------------------------------
+
+def rank_law_degrees(n: int, total: int, s: float, cap: int,
+                     rng: np.random.Generator) -> np.ndarray:
+    """Out-degree per state from the rank law, permuted onto states."""
+    r = np.arange(1, n + 1, dtype=np.float64)
+    rp = r ** (-s)
+    lo, hi = 1.0, 1e13
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        if np.clip(np.floor(mid * rp), 1, cap).sum() <= total:
+            lo = mid
+        else:
+            hi = mid
+    deg = np.clip(np.floor(lo * rp), 1, cap).astype(np.int64)
+    resid = total - int(deg.sum())
+    assert resid >= 0
+    if resid:
+        ones = np.flatnonzero(deg == 1)
+        pick = rng.choice(ones, size=resid, replace=False)
+        deg[pick] += 1
+    perm = rng.permutation(n)
+    out = np.empty(n, dtype=np.int64)
+    out[perm] = deg
+    return out
+
+
+def arcs_from_degrees(n: int, deg: np.ndarray, eps_frac: float, num_labels: int,
+                      mean_w: float, rng: np.random.Generator,
+                      first_label: int = 1) -> dict:
+    """Arcs state by state; epsilon arcs only to higher-index states."""
+    src = np.repeat(np.arange(n, dtype=np.int64), deg)
+    e = src.shape[0]
+    is_eps = rng.random(e) < eps_frac
+    is_eps &= src < n - 1
+    u = rng.random(e)
+    dst_emit = np.minimum((u * n).astype(np.int64), n - 1)
+    span = n - 1 - src
+    dst_eps = src + 1 + np.minimum((u * span).astype(np.int64), np.maximum(span - 1, 0))
+    dst = np.where(is_eps, dst_eps, dst_emit)
+    il = rng.integers(first_label, num_labels + 1, size=e, dtype=np.int64)
+    il = np.where(is_eps, 0, il)
+    w = rng.exponential(mean_w, size=e).astype(np.float32)
+    return dict(src=src.astype(np.int32), dst=dst.astype(np.int32),
+                ilabel=il.astype(np.int32), weight=w)
+
+
+def graph_cfg1() -> Graph:
+    rng = rng_for(1, GRAPH)
+    n = 2000
+    deg = 1 + rng.poisson(3.0, size=n)
+    a = arcs_from_degrees(n, deg, 0.15, 64, 1.5, rng)
+    return Graph(n, a["src"], a["dst"], a["ilabel"], np.zeros_like(a["src"]), a["weight"])
+
+
+def graph_rank_law(cfg: int, n: int, e: int, eps_frac: float, num_labels: int,
+                   mean_w: float, olabel_frac: float = 0.0, vocab: int = 0) -> Graph:
+    rng = rng_for(cfg, GRAPH)
+    deg = rank_law_degrees(n, e, 1.2, 200, rng)
+    a = arcs_from_degrees(n, deg, eps_frac, num_labels, mean_w, rng)
+    if olabel_frac > 0:
+        has = rng.random(e) < olabel_frac
+        ol = np.where(has, rng.integers(1, vocab + 1, size=e), 0).astype(np.int32)
+    else:
+        ol = np.zeros(e, dtype=np.int32)
+    return Graph(n, a["src"], a["dst"], a["ilabel"], ol, a["weight"])
+
+
+def graph_cfg2() -> Graph:
+    return graph_rank_law(2, 200_000, 1_000_000, 0.12, 2000, 2.0)
+
+
+def graph_cfg3() -> Graph:
+    return graph_rank_law(3, 10_000_000, 25_000_000, 0.20, 6000, 2.5, 0.10, 100_000)
+
+
+def graph_cfg5() -> Graph:
+    """CTC-style: a blank self-loop (ilabel 1 = column 0) on every state,
+    plus 10M rank-law arcs with non-blank labels 2..80, 15% of them epsilon
+    (about 10% of all 15M arcs)."""
+    rng = rng_for(5, GRAPH)
+    n = 5_000_000
+    deg = rank_law_degrees(n, 10_000_000, 1.2, 200, rng)
+    a = arcs_from_degrees(n, deg, 0.15, 80, 2.0, rng, first_label=2)
+    loop_w = rng.exponential(2.0, size=n).astype(np.float32)
+    # interleave: state s owns [self-loop, its rank-law arcs...]
+    tot = n + a["src"].shape[0]
+    rows = np.zeros(n + 1, dtype=np.int64)
+    rows[1:] = np.cumsum(deg + 1)
+    loop_pos = rows[:-1]
+    other_pos = np.ones(tot, dtype=bool)
+    other_pos[loop_pos] = False
+    src = np.empty(tot, np.int32); dst = np.empty(tot, np.int32)
+    il = np.empty(tot, np.int32); w = np.empty(tot, np.float32)
+    src[loop_pos] = np.arange(n, dtype=np.int32); dst[loop_pos] = np.arange(n, dtype=np.int32)
+    il[loop_pos] = 1; w[loop_pos] = loop_w
+    src[other_pos] = a["src"]; dst[other_pos] = a["dst"]
+    il[other_pos] = a["ilabel"]; w[other_pos] = a["weight"]
+    return Graph(n, src, dst, il, np.zeros(tot, np.int32), w)
+
+
+# --------------------------------------------------------------------------
+# log-likelihoods
+# --------------------------------------------------------------------------
+
+def log_softmax_rows(z: np.ndarray) -> np.ndarray:
+    m = z.max(axis=1, keepdims=True)
+    lse = m + np.log(np.exp(z - m).sum(axis=1, keepdims=True))
+    return (z - lse).astype(np.float32)
+
+
+def loglikes_gauss(cfg: int, utt: int, t: int, num_labels: int, sigma: float) -> np.ndarray:
+    rng = rng_for(cfg, LOGLIKES, utt)
+    z = rng.normal(0.0, sigma, size=(t, num_labels))
+    return np.ascontiguousarray(log_softmax_rows(z))
+
+
+def loglikes_ctc(cfg: int, utt: int, t: int, num_labels: int, boost: float = 8.0,
+                 p_blank: float = 0.85) -> np.ndarray:
+    rng = rng_for(cfg, LOGLIKES, utt)
+    z = rng.normal(0.0, 1.0, size=(t, num_labels))
+    m = rng.random(t) < p_blank
+    z[m, 0] += boost
+    return np.ascontiguousarray(log_softmax_rows(z))
+
+
+def batch_lengths(n_utt: int = 64, lo: int = 300, hi: int = 1500) -> np.ndarray:
+    rng = rng_for(4, LOGLIKES, 10_000)
+    return rng.integers(lo, hi + 1, size=n_utt)
+
+
+# --------------------------------------------------------------------------
+# the five workloads
+# --------------------------------------------------------------------------
+
+_graph_cache: dict = {}
+
+
+def graph_for(cfg: int) -> Graph:
+    key = 3 if cfg == 4 else cfg
+    if key not in _graph_cache:
+        _graph_cache[key] = {1: graph_cfg1, 2: graph_cfg2, 3: graph_cfg3, 5: graph_cfg5}[key]()
+    return _graph_cache[key]
+
+
+def workload(cfg: int, n_utt: Optional[int] = None, lsd: bool = True) -> Workload:
+    """Config ``cfg`` (1..5).  For cfg 4, ``n_utt`` limits the number of
+    utterances (default 64); for cfg 5, ``lsd`` selects label-synchronous
+    (threshold 0.95) or frame-synchronous (threshold 2) decoding."""
+    g = graph_for(cfg)
+    if cfg == 1:
+        ll = [loglikes_gauss(1, 0, 50, 64, 2.0)]
+        return Workload(1, "tiny-fsd", g, 64, ll, DecodeOpts(beam=12.0))
+    if cfg == 2:
+        ll = [loglikes_gauss(2, 0, 500, 2000, 3.0)]
+        return Workload(2, "medium-fsd-lattice", g, 2000, ll,
+                        DecodeOpts(beam=13.0, max_active=7000, lattice_beam=8.0))
+    if cfg == 3:
+        ll = [loglikes_gauss(3, 0, 1000, 6000, 3.0)]
+        return Workload(3, "lvcsr-25m", g, 6000, ll,
+                        DecodeOpts(beam=15.0, max_active=10000, lattice_beam=8.0))
+    if cfg == 4:
+        lens = batch_lengths()
+        n = 64 if n_utt is None else n_utt
+        ll = [loglikes_gauss(4, u, int(lens[u]), 6000, 3.0) for u in range(n)]
+        return Workload(4, "lvcsr-25m-batch%d" % n, g, 6000, ll,
+                        DecodeOpts(beam=15.0, max_active=10000, lattice_beam=8.0))
+    if cfg == 5:
+        ll = [loglikes_ctc(5, 0, 2000, 80)]
+        thr = 0.95 if lsd else 2.0
+        return Workload(5, "ctc-lsd" if lsd else "ctc-fsd", g, 80, ll,
+                        DecodeOpts(beam=14.0, max_active=8000, lattice_beam=8.0,
+                                   blank_threshold=thr, blank_id=0))
+    raise ValueError("cfg must be 1..5")
+
+
+# --------------------------------------------------------------------------
+# small graphs for pins, fuzz and tie forcing
+# --------------------------------------------------------------------------
+
+def random_small_graph(seed: int, n: int, mean_deg: float = 2.0, eps_frac: float = 0.2,
+                       num_labels: int = 4, weights: str = "exp",
+                       final: bool = False) -> Graph:
+    """Small random WFST.  ``weights``: "exp" (Exp(1) float32), "int"
+    (integers 0..3, forcing cost ties) or "dyadic" (multiples of 1/16 in
+    [0, 4), exact in float32 sums of modest length)."""
+    rng = np.random.default_rng(np.random.SeedSequence([1808, 687, 99, seed]))
+    deg = rng.poisson(mean_deg, size=n)
+    src = np.repeat(np.arange(n), deg)
+    e = src.shape[0]
+    is_eps = (rng.random(e) < eps_frac) & (src < n - 1)
+    u = rng.random(e)
+    dst = np.where(is_eps, src + 1 + (u * (n - 1 - src)).astype(np.int64),
+                   (u * n).astype(np.int64))
+    dst = np.minimum(dst, n - 1)
+    il = np.where(is_eps, 0, rng.integers(1, num_labels + 1, size=e))
+    if weights == "exp":
+        w = rng.exponential(1.0, size=e).astype(np.float32)
+    elif weights == "int":
+        w = rng.integers(0, 4, size=e).astype(np.float32)
+    elif weights == "dyadic":
+        w = (rng.integers(0, 64, size=e) / 16.0).astype(np.float32)
+    else:
+        raise ValueError(weights)
+    fw = None
+    if final:
+        fw = np.where(rng.random(n) < 0.5, rng.integers(0, 4, size=n).astype(np.float32),
+                      np.float32(np.inf)).astype(np.float32)
+    return Graph(n, src.astype(np.int32), dst.astype(np.int32), il.astype(np.int32),
+                 np.zeros(e, np.int32), w, 0, fw)
+
+
+def random_small_loglikes(seed: int, t: int, num_labels: int, kind: str = "gauss",
+                          blank_boost: float = 0.0) -> np.ndarray:
+    """``kind``: "gauss" (log-softmax of N(0,2)), "int" (negative integers
+    0..-3, forcing ties) or "dyadic" (multiples of -1/16 in (-4, 0])."""
+    rng = np.random.default_rng(np.random.SeedSequence([1808, 687, 98, seed]))
+    if kind == "gauss":
+        z = rng.normal(0.0, 2.0, size=(t, num_labels))
+        if blank_boost:
+            m = rng.random(t) < 0.6
+            z[m, 0] += blank_boost
+        return np.ascontiguousarray(log_softmax_rows(z))
+    if kind == "int":
+        return np.ascontiguousarray(-rng.integers(0, 4, size=(t, num_labels)).astype(np.float32))
+    if kind == "dyadic":
+        return np.ascontiguousarray((-rng.integers(0, 64, size=(t, num_labels)) / 16.0).astype(np.float32))
+    raise ValueError(kind)
