@@ -1,0 +1,227 @@
+/*
+ * wfstdec -- WFST Viterbi beam decoding with exact (state-level) lattices,
+ * frame-synchronous or label-synchronous, on one AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow Z. Chen, "Linguistic Search Optimization for Deep
+ * Learning Based LVCSR" (Interspeech 2018):
+ *   - linguistic search = Viterbi beam decoding over a WFST search graph
+ *     (Sec. 1), by token passing where every state keeps the minimum-cost
+ *     token over its incoming arcs together with its predecessor
+ *     ("token recombination", Sec. 3 and Fig. 2);
+ *   - label-synchronous decoding (Sec. 2, Eq. 2, Alg. 1): frames whose blank
+ *     posterior exceeds a threshold (the set U) are skipped, so the search
+ *     runs on T - |U| frames (Eq. 3);
+ *   - finalTransition then backtrace (Alg. 1);
+ *   - exact lattice generation and lattice pruning (Sec. 1, Sec. 3).
+ *
+ * Conventions used throughout:
+ *   - costs are negative log probabilities in float32 (min over paths
+ *     = arg max of Eq. 1); an emitting arc a = (s -> d, ilabel i, weight w)
+ *     taken at a frame with log-likelihood row ll gives the candidate
+ *     (cost(s) + w) - ll[i - 1], two float32 roundings in that order, no
+ *     fused multiply-add, no flush of subnormals;
+ *   - ilabel 0 marks an epsilon arc (consumes no frame); ilabel i >= 1 reads
+ *     log-likelihood column i - 1; olabel 0 means no output;
+ *   - arcs are identified by their index in the arrays given to wfst_load
+ *     ("user arc index");
+ *   - equal costs are broken towards the lower arc index, the start token
+ *     wins all ties, and the final state with the lowest id wins a tie on the
+ *     final cost; results are therefore deterministic and independent of
+ *     the order in which the GPU processes work.
+ *
+ * All entry points return an int status (WFST_OK = 0 or a negative error)
+ * unless stated otherwise; wfst_last_error() gives a message for the
+ * calling thread's last failure.
+ */
+#ifndef WFSTDEC_H
+#define WFSTDEC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WFST_OK 0
+#define WFST_EINVAL (-1)    /* invalid argument or graph */
+#define WFST_ENOMEM (-2)    /* host or device allocation failed */
+#define WFST_ENOPATH (-3)   /* the token set became empty: no surviving path */
+#define WFST_ECAPACITY (-4) /* a fixed buffer overflowed even after retries; raise capacity_hint */
+#define WFST_EDEVICE (-5)   /* HIP runtime error */
+
+typedef struct wfst_graph wfst_graph;
+typedef struct wfst_result wfst_result;
+
+/*
+ * wfst_load -- validate a WFST given as arc arrays sorted by source state
+ * (CSR order) and lay it out in device memory of the current HIP device.
+ *
+ *   num_states   N >= 1
+ *   num_arcs     E, 0 <= E < 2^31 - 1
+ *   src, dst     [E] host int32, src sorted ascending, both in [0, N)
+ *   ilabel       [E] host int32 >= 0 (0 = epsilon)
+ *   olabel       [E] host int32 >= 0 (0 = none); kept for the caller only
+ *   weight       [E] host float32, finite; epsilon arcs need weight >= 0
+ *   start_state  in [0, N)  (the start node S of Alg. 1)
+ *   final_weight [N] host float32 or NULL; NULL makes every state final with
+ *                cost 0; +inf marks a non-final state; NaN and -inf are
+ *                invalid (the end node E of Alg. 1 as final costs)
+ *   out          receives the graph handle
+ *
+ * The epsilon subgraph must be acyclic.  Input arrays are copied and may be
+ * freed on return.  The handle is immutable and may be shared by concurrent
+ * decodes on different streams of the same device.  Errors: WFST_EINVAL
+ * (any rule above), WFST_ENOMEM, WFST_EDEVICE.
+ */
+int wfst_load(int32_t num_states, int64_t num_arcs, const int32_t *src, const int32_t *dst,
+              const int32_t *ilabel, const int32_t *olabel, const float *weight,
+              int32_t start_state, const float *final_weight, wfst_graph **out);
+
+/* Release a graph (NULL is allowed).  No decode may be running on it. */
+void wfst_graph_free(wfst_graph *g);
+
+typedef struct wfst_graph_info {
+    int32_t num_states;
+    int64_t num_arcs;
+    int64_t num_emitting;     /* arcs with ilabel != 0 */
+    int64_t num_epsilon;      /* arcs with ilabel == 0 */
+    int32_t max_ilabel;       /* decode needs L >= max_ilabel */
+    int32_t epsilon_depth;    /* longest epsilon path (arcs) */
+    int64_t device_bytes;     /* device memory held by the layout */
+} wfst_graph_info;
+
+int wfst_graph_get_info(const wfst_graph *g, wfst_graph_info *info);
+
+/* decode options */
+#define WFST_RECORD_TOKENS 1u  /* keep every token set for wfst_result_tokens */
+#define WFST_LOGLIKES_HOST 2u  /* loglikes pointers are host memory (copied to the device first) */
+#define WFST_PROFILE 4u        /* time the kernel phases with HIP events on the decode stream */
+
+typedef struct wfst_decode_opts {
+    float beam;               /* > 0 (may be +inf): keep tokens with cost <= best + beam */
+    int32_t max_active;       /* <= 0: unlimited; else keep the max_active cheapest tokens
+                                 (all tokens tied with the last one are kept) */
+    float lattice_beam;       /* < 0: no lattice; else keep lattice arcs whose best complete
+                                 path is within lattice_beam of the best path (+inf: all) */
+    float blank_threshold;    /* > 1: frame-synchronous; in (0, 1]: label-synchronous,
+                                 frame t is skipped when ll[t][blank_id] > log(blank_threshold);
+                                 <= 0 or NaN: WFST_EINVAL */
+    int32_t blank_id;         /* log-likelihood column of the blank unit, in [0, L) */
+    uint32_t flags;           /* WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST */
+    int64_t capacity_hint;    /* 0: automatic; else tokens per frame to reserve */
+} wfst_decode_opts;
+
+/* Fill opts with defaults: beam 16, max_active 0, no lattice, FSD, blank 0. */
+void wfst_default_opts(wfst_decode_opts *opts);
+
+/*
+ * wfst_decode -- decode one utterance (Alg. 1 with ViterbiBeamSearch per
+ * decoded frame).
+ *
+ *   loglikes   [T x L] float32 row-major log-likelihoods (device memory of
+ *              the graph's device, or host memory with WFST_LOGLIKES_HOST);
+ *              values must not be NaN or +inf (-inf is allowed); acoustic
+ *              scale and priors are the caller's business
+ *   T >= 0, L >= max_ilabel of the graph, L >= 1
+ *   hip_stream hipStream_t to run on (NULL = default stream); the call is
+ *              blocking: it returns when the result is complete
+ *   out        receives the result (also on WFST_ENOPATH, so the status can
+ *              be read back); free with wfst_result_free
+ *
+ * Loglikes must stay valid until the call returns.  Errors: WFST_EINVAL,
+ * WFST_ENOMEM, WFST_ECAPACITY, WFST_EDEVICE; WFST_ENOPATH when no path
+ * survives.
+ */
+int wfst_decode(const wfst_graph *g, const float *loglikes, int32_t T, int32_t L,
+                const wfst_decode_opts *opts, void *hip_stream, wfst_result **out);
+
+/*
+ * wfst_decode_batch -- decode n_utt independent utterances against one
+ * graph in lock-step on one device (one launch per phase per frame for the
+ * whole batch).
+ *
+ *   loglikes   [n_utt] host array of pointers, each [T[u] x L] float32
+ *   T          [n_utt] host array of frame counts
+ *   out_array  [n_utt] host array receiving one result per utterance
+ *
+ * Returns WFST_OK when the batch ran (each result carries its own status,
+ * e.g. WFST_ENOPATH for one utterance), or an error for the whole call.
+ */
+int wfst_decode_batch(const wfst_graph *g, int32_t n_utt, const float *const *loglikes,
+                      const int32_t *T, int32_t L, const wfst_decode_opts *opts,
+                      void *hip_stream, wfst_result **out_array);
+
+/* Status of the utterance: WFST_OK or WFST_ENOPATH. */
+int wfst_result_status(const wfst_result *r);
+
+/*
+ * Best path: its cost (final cost included), final state, whether a final
+ * state was reached (0 means the all-final fallback was used), and n arcs
+ * in path order with, per arc, the original frame it consumed (-1 for
+ * epsilon arcs).  Pointers stay valid until wfst_result_free.
+ */
+int wfst_result_best(const wfst_result *r, float *cost, int32_t *final_state,
+                     int32_t *reached_final, int32_t *n, const int32_t **arcs,
+                     const int32_t **frames);
+
+/* Frame counts and, for each decoded frame j, the original frame index. */
+int wfst_result_frames(const wfst_result *r, int32_t *num_frames, int32_t *num_decoded,
+                       const int32_t **orig_frame);
+
+/*
+ * Lattice arc: `frame` is the token set j (0..T') holding the arc's source
+ * (an emitting arc goes from token set j to j + 1 and consumed decoded frame
+ * j; an epsilon arc stays inside token set j); `arc` is the user arc index;
+ * `cost` is the best prefix cost through the arc; `extra` is how much the
+ * best complete path through the arc costs above the best path.
+ */
+typedef struct wfst_lat_arc {
+    int32_t frame;
+    int32_t arc;
+    float cost;
+    float extra;
+} wfst_lat_arc;
+
+/* Lattice-beam-pruned lattice, sorted by (frame, arc), copied to host
+ * memory on first call.  n = 0 when the lattice was disabled. */
+int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs);
+
+/* The same lattice in device memory (owned by the result). */
+int wfst_result_lattice_device(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs);
+
+/*
+ * Token set j (0..T') sorted by state: states, float32 costs and
+ * back-pointer arcs (-1 for the start token).  Needs WFST_RECORD_TOKENS.
+ */
+int wfst_result_tokens(const wfst_result *r, int32_t j, int32_t *n, const int32_t **state,
+                       const float **cost, const int32_t **bp_arc);
+
+typedef struct wfst_stats {
+    int32_t frames;            /* T */
+    int32_t frames_decoded;    /* T' = T - |U| */
+    int64_t tokens;            /* sum over token sets of |S_j| */
+    int64_t arcs_expanded;     /* emitting out-arcs of the expanded token sets */
+    int64_t eps_arcs;          /* epsilon out-arcs of all surviving tokens */
+    int64_t lattice_raw;       /* lattice arcs recorded before lattice-beam pruning */
+    int64_t lattice_kept;      /* lattice arcs kept */
+    double decode_ms;          /* wall time of the call that produced this result */
+    /* with WFST_PROFILE (batch-wide, the same in every result of a batch):
+       device time summed over launches, measured with HIP events */
+    double expand_ms;          /* emitting expansion + epsilon closure */
+    double prune_ms;           /* beam / max-active pruning and compaction */
+    double record_ms;          /* back-pointers and lattice recording */
+    double final_ms;           /* final costs, backtrace, lattice pruning and output */
+    int32_t expand_launches;   /* launches of the expansion kernel */
+} wfst_stats;
+
+int wfst_result_stats(const wfst_result *r, wfst_stats *stats);
+
+void wfst_result_free(wfst_result *r);
+
+/* Message for the last error raised on the calling thread ("" if none). */
+const char *wfst_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

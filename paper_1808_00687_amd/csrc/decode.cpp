@@ -1,0 +1,626 @@
+// Decode driver and result objects of the C ABI.
+//
+// One call decodes a batch of utterances in lock-step: classify frames
+// (label-synchronous compaction), produce token set 0 from the start state,
+// then for every decoded frame run expand -> prune (gather, select, compact)
+// -> record -> advance for the whole batch, and finally the final costs,
+// backtrace and lattice pruning.  Counts stay on the device; the host reads
+// back only the decoded-frame counts (to size the loop) and the results.
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <memory>
+#include <mutex>
+#include <new>
+#include <numeric>
+#include <vector>
+
+#include "internal.h"
+
+using namespace wfd;
+
+namespace {
+
+struct DevBuf {
+    void *p = nullptr;
+    int device = 0;
+    DevBuf() = default;
+    DevBuf(const DevBuf &) = delete;
+    DevBuf &operator=(const DevBuf &) = delete;
+    ~DevBuf()
+    {
+        if (!p) return;
+        int cur = 0;
+        hipGetDevice(&cur);
+        if (cur != device) hipSetDevice(device);
+        hipFree(p);
+        if (cur != device) hipSetDevice(cur);
+    }
+};
+
+}  // namespace
+
+struct wfst_result {
+    int status = WFST_OK;
+    float cost = std::numeric_limits<float>::quiet_NaN();
+    int32_t final_state = -1;
+    int32_t reached_final = 0;
+    std::vector<int32_t> path_arcs, path_frames, kept;
+    int32_t T = 0, Tp = 0;
+    std::shared_ptr<DevBuf> lat_dev;
+    int64_t lat_off = 0, lat_n = 0;
+    mutable std::mutex lat_mu;
+    mutable std::vector<wfst_lat_arc> lat_host;
+    mutable bool lat_loaded = false;
+    bool has_tokens = false;
+    std::vector<int64_t> tok_off;
+    std::vector<int32_t> tok_state, tok_arc;
+    std::vector<float> tok_cost;
+    wfst_stats stats{};
+};
+
+namespace {
+
+int fail(int code, const char *msg)
+{
+    set_error("%s", msg);
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    set_error("%s: %s", what, hipGetErrorString(e));
+    return e == hipErrorOutOfMemory ? WFST_ENOMEM : WFST_EDEVICE;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev)
+    {
+        hipGetDevice(&prev);
+        if (prev != dev) hipSetDevice(dev);
+        else prev = -1;
+    }
+    ~DeviceGuard()
+    {
+        if (prev >= 0) hipSetDevice(prev);
+    }
+};
+
+// Stream-ordered workspace allocations, released when the attempt ends.
+struct Workspace {
+    hipStream_t s;
+    std::vector<void *> ptrs;
+    hipError_t err = hipSuccess;
+    explicit Workspace(hipStream_t st) : s(st) {}
+    template <typename T>
+    T *get(int64_t count)
+    {
+        if (err != hipSuccess) return nullptr;
+        size_t bytes = static_cast<size_t>(std::max<int64_t>(count, 1)) * sizeof(T);
+        void *p = nullptr;
+        err = hipMallocAsync(&p, bytes, s);
+        if (err != hipSuccess) return nullptr;
+        ptrs.push_back(p);
+        return static_cast<T *>(p);
+    }
+    ~Workspace()
+    {
+        for (void *p : ptrs) hipFreeAsync(p, s);
+    }
+};
+
+void keep_pool_memory(int device)
+{
+    static std::once_flag once[64];
+    if (device < 0 || device >= 64) return;
+    std::call_once(once[device], [device]() {
+        hipMemPool_t pool;
+        if (hipDeviceGetDefaultMemPool(&pool, device) == hipSuccess) {
+            uint64_t thr = std::numeric_limits<uint64_t>::max();
+            hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+        }
+    });
+}
+
+int test_queue_cap()
+{
+    // test hook: a tiny per-wave epsilon queue forces the overflow path
+    const char *v = getenv("WFSTDEC_TEST_QUEUE_CAP");
+    if (!v) return kQueueCap;
+    int q = atoi(v);
+    int c = 2;
+    while (c * 2 <= q && c * 2 <= kQueueCap) c *= 2;
+    return c;
+}
+
+struct Sizes {
+    int64_t capF;      // tokens per frame
+    int64_t capT;      // reached states per frame
+    int64_t capO;      // overflow epsilon items per frame
+    int64_t lat_mult;  // lattice records per token
+};
+
+struct Timer {
+    bool on = false;
+    hipStream_t s = nullptr;
+    std::vector<hipEvent_t> ev;
+    std::vector<int> kind;   // phase ending at ev[i]
+    void mark(int k)
+    {
+        if (!on) return;
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return;
+        hipEventRecord(e, s);
+        ev.push_back(e);
+        kind.push_back(k);
+    }
+    ~Timer()
+    {
+        for (auto e : ev) hipEventDestroy(e);
+    }
+};
+
+enum { PH_NONE = -1, PH_EXPAND = 0, PH_PRUNE = 1, PH_RECORD = 2, PH_FINAL = 3, PH_OTHER = 4 };
+
+// One attempt at decoding the batch with the given buffer sizes.  Returns
+// WFST_OK, an error, or WFST_ECAPACITY when a buffer overflowed.
+int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, int L,
+              const wfst_decode_opts &o, float thr, hipStream_t s, const Sizes &z,
+              std::vector<wfst_result *> &out, double t_start)
+{
+    const int64_t N = G.d.n;
+    const bool lattice = o.lattice_beam >= 0.0f;
+    const int depth = G.eps_depth;
+    Workspace ws(s);
+    Timer tm;
+    tm.on = (o.flags & WFST_PROFILE) != 0;
+    tm.s = s;
+
+    std::vector<UttLayout> lay(U);
+    int64_t sv = 0, le = 0, lx = 0, fo = 0, kp = 0, pa = 0;
+    for (int u = 0; u < U; u++) {
+        UttLayout &l = lay[u];
+        const int64_t Tu = T[u];
+        l.sv0 = sv;
+        l.svcap = (Tu + 1) * z.capF;
+        sv += l.svcap;
+        l.le0 = le;
+        l.lecap = lattice ? std::max<int64_t>(Tu, 1) * z.capF * z.lat_mult : 0;
+        le += l.lecap;
+        l.lx0 = lx;
+        l.lxcap = lattice ? (Tu + 1) * z.capF * std::max<int64_t>(z.lat_mult / 2, 1) : 0;
+        lx += l.lxcap;
+        l.fo0 = fo;
+        fo += Tu + 2;
+        l.kept0 = kp;
+        kp += std::max<int64_t>(Tu, 1);
+        l.path0 = pa;
+        l.pathcap = (Tu + 1) * (depth + 1) + 1;
+        pa += l.pathcap;
+        l.lo0 = 0;
+    }
+
+    Params p{};
+    p.g = G.d;
+    p.U = U;
+    p.L = L;
+    p.beam = o.beam;
+    p.max_active = o.max_active;
+    p.lattice_beam = o.lattice_beam;
+    p.lattice = lattice ? 1 : 0;
+    p.blank_id = o.blank_id;
+    p.blank_thr = thr;
+    p.qcap = test_queue_cap();
+    p.capT = z.capT;
+    p.capO = z.capO;
+    p.st = ws.get<UttState>(U);
+    UttLayout *d_lay = ws.get<UttLayout>(U);
+    p.lay = d_lay;
+    int32_t *ctl = ws.get<int32_t>(2);
+    p.cur = ctl;
+    p.done = reinterpret_cast<uint32_t *>(ctl + 1);
+    p.tok = ws.get<uint64_t>(U * N);
+    p.pos = ws.get<int32_t>(U * 2 * N);
+    p.touched = ws.get<int32_t>(U * z.capT);
+    p.pk = ws.get<uint64_t>(U * z.capT);
+    p.ovf = ws.get<uint64_t>(U * z.capO);
+    p.hist = ws.get<uint32_t>(static_cast<int64_t>(U) * kHistBins);
+    p.sv_state = ws.get<int32_t>(sv);
+    p.sv_tok = ws.get<uint64_t>(sv);
+    p.sv_prev = ws.get<int32_t>(sv);
+    p.e_key = lattice ? ws.get<uint32_t>(sv) : nullptr;
+    p.lat_e = lattice ? ws.get<int4>(le) : nullptr;
+    p.lat_x = lattice ? ws.get<int4>(lx) : nullptr;
+    p.ex_e = lattice ? ws.get<float>(le) : nullptr;
+    p.ex_x = lattice ? ws.get<float>(lx) : nullptr;
+    int64_t *fo_all = ws.get<int64_t>(4 * fo);
+    p.kept = ws.get<int32_t>(kp);
+    p.path_arc = ws.get<int32_t>(pa);
+    p.path_frame = ws.get<int32_t>(pa);
+    if (ws.err != hipSuccess) return hip_fail(ws.err, "decode: workspace allocation");
+    p.sv_off = fo_all;
+    p.le_off = fo_all + fo;
+    p.lx_off = fo_all + 2 * fo;
+    p.lo_off = fo_all + 3 * fo;
+
+    std::vector<UttState> st(U);
+    for (int u = 0; u < U; u++) {
+        std::memset(&st[u], 0, sizeof(UttState));
+        st[u].ll = ll[u];
+        st[u].T = T[u];
+        st[u].best = kEmptyKey;
+    }
+    hipError_t e = hipSuccess;
+    auto chk = [&](hipError_t r) {
+        if (e == hipSuccess && r != hipSuccess) e = r;
+    };
+    chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
+    chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
+    chk(hipMemsetAsync(ctl, 0, 2 * sizeof(int32_t), s));
+    chk(hipMemsetAsync(fo_all, 0, 4 * fo * sizeof(int64_t), s));
+    chk(hipMemsetAsync(p.hist, 0, static_cast<size_t>(U) * kHistBins * 4, s));
+    chk(launch_fill_u64(p.tok, U * N, kEmptyTok, s));
+    chk(launch_classify(p, s));
+    chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
+    chk(hipStreamSynchronize(s));
+    if (e != hipSuccess) return hip_fail(e, "decode: setup");
+    int Tmax = 0;
+    for (int u = 0; u < U; u++) Tmax = std::max(Tmax, st[u].Tp);
+
+    // grid sizes: one wave per 64 expected tokens (or reached states)
+    const int64_t est = o.max_active > 0 ? std::min<int64_t>(o.max_active, N) : std::min<int64_t>(N, z.capF);
+    auto clampg = [](int64_t g) { return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(g, 8192))); };
+    const int gE = clampg((U * est + 255) / 256);
+    const int gP = clampg((U * std::min<int64_t>(4 * est, z.capT) + 255) / 256);
+
+    for (int k = 0; k <= Tmax && e == hipSuccess; k++) {
+        tm.mark(PH_OTHER);
+        chk(k == 0 ? launch_init(p, s) : launch_expand(p, gE, s));
+        tm.mark(PH_EXPAND);
+        chk(launch_prune_gather(p, gP, s));
+        chk(launch_prune_select(p, s));
+        chk(launch_prune_compact(p, gP, s));
+        tm.mark(PH_PRUNE);
+        chk(launch_record(p, gE, s));
+        chk(launch_advance(p, s));
+        tm.mark(PH_RECORD);
+    }
+    chk(launch_final(p, s));
+    chk(launch_backtrace(p, s));
+    if (lattice) chk(launch_lattice_backward(p, s));
+    chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
+    chk(hipStreamSynchronize(s));
+    if (e != hipSuccess) return hip_fail(e, "decode: search");
+    for (int u = 0; u < U; u++)
+        if (st[u].status == WFST_ECAPACITY) return WFST_ECAPACITY;
+
+    std::shared_ptr<DevBuf> lat_buf;
+    if (lattice) {
+        int64_t tot = 0;
+        for (int u = 0; u < U; u++) {
+            lay[u].lo0 = tot;
+            if (st[u].status == WFST_OK) tot += st[u].lat_kept;
+        }
+        lat_buf = std::make_shared<DevBuf>();
+        hipGetDevice(&lat_buf->device);
+        chk(hipMalloc(&lat_buf->p, static_cast<size_t>(std::max<int64_t>(tot, 1)) * sizeof(int4)));
+        p.lat_out = static_cast<int4 *>(lat_buf->p);
+        chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
+        chk(launch_lattice_emit(p, Tmax, s));
+    }
+    tm.mark(PH_FINAL);
+
+    // gather results
+    std::vector<int64_t> fo_h(static_cast<size_t>(fo));
+    std::vector<int32_t> kept_h(static_cast<size_t>(kp));
+    chk(hipMemcpyAsync(fo_h.data(), p.sv_off, fo * sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    chk(hipMemcpyAsync(kept_h.data(), p.kept, kp * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    for (int u = 0; u < U; u++) {
+        wfst_result *r = out[u];
+        const UttState &x = st[u];
+        r->status = x.status;
+        r->T = T[u];
+        r->Tp = x.Tp;
+        r->stats.frames = T[u];
+        r->stats.frames_decoded = x.Tp;
+        if (x.status != WFST_OK) continue;
+        r->cost = x.final_cost;
+        r->final_state = x.final_state;
+        r->reached_final = x.reached_final;
+        r->path_arcs.resize(x.path_len);
+        r->path_frames.resize(x.path_len);
+        const int64_t end = lay[u].path0 + lay[u].pathcap;
+        if (x.path_len) {
+            chk(hipMemcpyAsync(r->path_arcs.data(), p.path_arc + end - x.path_len, x.path_len * 4, hipMemcpyDeviceToHost, s));
+            chk(hipMemcpyAsync(r->path_frames.data(), p.path_frame + end - x.path_len, x.path_len * 4, hipMemcpyDeviceToHost, s));
+        }
+        r->stats.tokens = x.tokens;
+        r->stats.arcs_expanded = x.arcs_expanded;
+        r->stats.eps_arcs = x.eps_arcs;
+        r->stats.lattice_raw = x.le_cnt + x.lx_cnt;
+        r->stats.lattice_kept = lattice ? x.lat_kept : 0;
+        if (lattice) {
+            r->lat_dev = lat_buf;
+            r->lat_off = lay[u].lo0;
+            r->lat_n = x.lat_kept;
+        }
+    }
+    std::vector<std::vector<int32_t>> tst(U);
+    std::vector<std::vector<uint64_t>> ttk(U);
+    if (o.flags & WFST_RECORD_TOKENS) {
+        chk(hipStreamSynchronize(s));
+        for (int u = 0; u < U; u++) {
+            if (st[u].status != WFST_OK) continue;
+            const int64_t ntok = fo_h[lay[u].fo0 + st[u].Tp + 1];
+            tst[u].resize(static_cast<size_t>(ntok));
+            ttk[u].resize(static_cast<size_t>(ntok));
+            chk(hipMemcpyAsync(tst[u].data(), p.sv_state + lay[u].sv0, ntok * 4, hipMemcpyDeviceToHost, s));
+            chk(hipMemcpyAsync(ttk[u].data(), p.sv_tok + lay[u].sv0, ntok * 8, hipMemcpyDeviceToHost, s));
+        }
+    }
+    chk(hipStreamSynchronize(s));
+    if (e != hipSuccess) return hip_fail(e, "decode: results");
+
+    double ph[5] = {0, 0, 0, 0, 0};
+    int nexp = 0;
+    for (size_t i = 1; i < tm.ev.size(); i++) {
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, tm.ev[i - 1], tm.ev[i]) == hipSuccess && tm.kind[i] >= 0) {
+            ph[tm.kind[i]] += ms;
+            if (tm.kind[i] == PH_EXPAND) nexp++;
+        }
+    }
+    const double wall = std::chrono::duration<double, std::milli>(
+                            std::chrono::steady_clock::now().time_since_epoch()).count() - t_start;
+    for (int u = 0; u < U; u++) {
+        wfst_result *r = out[u];
+        r->kept.assign(kept_h.begin() + lay[u].kept0, kept_h.begin() + lay[u].kept0 + st[u].Tp);
+        r->stats.decode_ms = wall;
+        r->stats.expand_ms = ph[PH_EXPAND];
+        r->stats.prune_ms = ph[PH_PRUNE];
+        r->stats.record_ms = ph[PH_RECORD];
+        r->stats.final_ms = ph[PH_FINAL];
+        r->stats.expand_launches = nexp;
+        if ((o.flags & WFST_RECORD_TOKENS) && r->status == WFST_OK) {
+            // token sets sorted by state for the caller
+            const int Tp = st[u].Tp;
+            r->has_tokens = true;
+            r->tok_off.assign(fo_h.begin() + lay[u].fo0, fo_h.begin() + lay[u].fo0 + Tp + 2);
+            const int64_t ntok = r->tok_off.back();
+            r->tok_state.resize(static_cast<size_t>(ntok));
+            r->tok_cost.resize(static_cast<size_t>(ntok));
+            r->tok_arc.resize(static_cast<size_t>(ntok));
+            std::vector<int64_t> idx;
+            for (int j = 0; j <= Tp; j++) {
+                const int64_t a = r->tok_off[j], b = r->tok_off[j + 1];
+                idx.resize(static_cast<size_t>(b - a));
+                std::iota(idx.begin(), idx.end(), a);
+                std::sort(idx.begin(), idx.end(), [&](int64_t x, int64_t y) { return tst[u][x] < tst[u][y]; });
+                for (int64_t i = a; i < b; i++) {
+                    const int64_t q = idx[i - a];
+                    const uint64_t t = ttk[u][q];
+                    const uint32_t k = static_cast<uint32_t>(t >> 32);
+                    const uint32_t bits = (k >> 31) ? (k & 0x7FFFFFFFu) : ~k;
+                    float c;
+                    std::memcpy(&c, &bits, 4);
+                    r->tok_state[i] = tst[u][q];
+                    r->tok_cost[i] = c;
+                    r->tok_arc[i] = static_cast<int32_t>(static_cast<uint32_t>(t)) - 1;
+                }
+            }
+        }
+    }
+    return WFST_OK;
+}
+
+int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglikes, const int32_t *T,
+                int32_t L, const wfst_decode_opts *opts, void *hip_stream, wfst_result **out_array)
+{
+    clear_error();
+    const double t0 = std::chrono::duration<double, std::milli>(
+                          std::chrono::steady_clock::now().time_since_epoch()).count();
+    if (!gh || !opts || !out_array || !T || !loglikes) return fail(WFST_EINVAL, "decode: NULL argument");
+    if (n_utt < 1) return fail(WFST_EINVAL, "decode: n_utt must be >= 1");
+    for (int u = 0; u < n_utt; u++) out_array[u] = nullptr;
+    const Graph &G = gh->g;
+    const wfst_decode_opts o = *opts;
+    if (!(o.beam > 0.0f)) return fail(WFST_EINVAL, "decode: beam must be > 0");
+    if (std::isnan(o.lattice_beam)) return fail(WFST_EINVAL, "decode: lattice_beam is NaN");
+    if (!(o.blank_threshold > 0.0f)) return fail(WFST_EINVAL, "decode: blank_threshold must be > 0");
+    if (L < 1 || L < G.max_ilabel) return fail(WFST_EINVAL, "decode: L smaller than the largest ilabel");
+    if (o.blank_id < 0 || o.blank_id >= L) return fail(WFST_EINVAL, "decode: blank_id out of range");
+    if (o.capacity_hint < 0) return fail(WFST_EINVAL, "decode: negative capacity_hint");
+    for (int u = 0; u < n_utt; u++) {
+        if (T[u] < 0) return fail(WFST_EINVAL, "decode: negative T");
+        if (T[u] > 0 && !loglikes[u]) return fail(WFST_EINVAL, "decode: NULL loglikes");
+    }
+    const float thr = o.blank_threshold > 1.0f ? std::numeric_limits<float>::infinity()
+                                               : static_cast<float>(std::log(static_cast<double>(o.blank_threshold)));
+
+    DeviceGuard dg(G.device);
+    keep_pool_memory(G.device);
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+
+    std::vector<const float *> ll(loglikes, loglikes + n_utt);
+    std::vector<std::unique_ptr<DevBuf>> host_copies;
+    if (o.flags & WFST_LOGLIKES_HOST) {
+        for (int u = 0; u < n_utt; u++) {
+            auto b = std::make_unique<DevBuf>();
+            b->device = G.device;
+            size_t bytes = static_cast<size_t>(std::max(T[u], 1)) * L * sizeof(float);
+            hipError_t e = hipMalloc(&b->p, bytes);
+            if (e != hipSuccess) return hip_fail(e, "decode: loglikes copy");
+            if (T[u]) {
+                e = hipMemcpy(b->p, loglikes[u], static_cast<size_t>(T[u]) * L * sizeof(float), hipMemcpyHostToDevice);
+                if (e != hipSuccess) return hip_fail(e, "decode: loglikes copy");
+            }
+            ll[u] = static_cast<const float *>(b->p);
+            host_copies.push_back(std::move(b));
+        }
+    }
+
+    std::vector<wfst_result *> res(n_utt);
+    for (int u = 0; u < n_utt; u++) {
+        res[u] = new (std::nothrow) wfst_result();
+        if (!res[u]) {
+            for (int v = 0; v < u; v++) delete res[v];
+            return fail(WFST_ENOMEM, "decode: host allocation");
+        }
+    }
+    const int64_t N = G.d.n;
+    Sizes z;
+    if (o.capacity_hint > 0) z.capF = std::min<int64_t>(o.capacity_hint, N);
+    else if (o.max_active > 0) z.capF = std::min<int64_t>(N, o.max_active + o.max_active / 4 + 256);
+    else z.capF = std::min<int64_t>(N, 65536);
+    z.capT = std::min<int64_t>(N, std::max<int64_t>(16 * z.capF, 4096));
+    z.capO = z.capT;
+    z.lat_mult = 2;
+    int rc = WFST_ECAPACITY;
+    for (int attempt = 0; attempt < 6 && rc == WFST_ECAPACITY; attempt++) {
+        if (attempt) {
+            for (int u = 0; u < n_utt; u++) {
+                delete res[u];
+                res[u] = new (std::nothrow) wfst_result();
+            }
+            z.capF = std::min<int64_t>(N, z.capF * 2);
+            z.capT = std::min<int64_t>(N, z.capT * 2);
+            z.capO = z.capO * 2;
+            z.lat_mult *= 2;
+        }
+        rc = run_batch(G, n_utt, ll.data(), T, L, o, thr, s, z, res, t0);
+    }
+    if (rc != WFST_OK) {
+        for (int u = 0; u < n_utt; u++) delete res[u];
+        if (rc == WFST_ECAPACITY) set_error("decode: buffers overflowed; raise capacity_hint");
+        return rc;
+    }
+    for (int u = 0; u < n_utt; u++) out_array[u] = res[u];
+    return WFST_OK;
+}
+
+}  // namespace
+
+extern "C" void wfst_default_opts(wfst_decode_opts *o)
+{
+    if (!o) return;
+    o->beam = 16.0f;
+    o->max_active = 0;
+    o->lattice_beam = -1.0f;
+    o->blank_threshold = 2.0f;
+    o->blank_id = 0;
+    o->flags = 0;
+    o->capacity_hint = 0;
+}
+
+extern "C" int wfst_decode(const wfst_graph *g, const float *loglikes, int32_t T, int32_t L,
+                           const wfst_decode_opts *opts, void *hip_stream, wfst_result **out)
+{
+    if (!out) {
+        set_error("wfst_decode: out is NULL");
+        return WFST_EINVAL;
+    }
+    *out = nullptr;
+    int rc = decode_impl(g, 1, &loglikes, &T, L, opts, hip_stream, out);
+    if (rc != WFST_OK) return rc;
+    if ((*out)->status == WFST_ENOPATH) set_error("wfst_decode: no surviving path");
+    return (*out)->status;
+}
+
+extern "C" int wfst_decode_batch(const wfst_graph *g, int32_t n_utt, const float *const *loglikes,
+                                 const int32_t *T, int32_t L, const wfst_decode_opts *opts,
+                                 void *hip_stream, wfst_result **out_array)
+{
+    return decode_impl(g, n_utt, loglikes, T, L, opts, hip_stream, out_array);
+}
+
+extern "C" int wfst_result_status(const wfst_result *r)
+{
+    if (!r) return fail(WFST_EINVAL, "wfst_result_status: NULL result");
+    return r->status;
+}
+
+extern "C" int wfst_result_best(const wfst_result *r, float *cost, int32_t *final_state,
+                                int32_t *reached_final, int32_t *n, const int32_t **arcs,
+                                const int32_t **frames)
+{
+    clear_error();
+    if (!r) return fail(WFST_EINVAL, "wfst_result_best: NULL result");
+    if (r->status != WFST_OK) return fail(r->status, "wfst_result_best: utterance has no path");
+    if (cost) *cost = r->cost;
+    if (final_state) *final_state = r->final_state;
+    if (reached_final) *reached_final = r->reached_final;
+    if (n) *n = static_cast<int32_t>(r->path_arcs.size());
+    if (arcs) *arcs = r->path_arcs.data();
+    if (frames) *frames = r->path_frames.data();
+    return WFST_OK;
+}
+
+extern "C" int wfst_result_frames(const wfst_result *r, int32_t *num_frames, int32_t *num_decoded,
+                                  const int32_t **orig_frame)
+{
+    clear_error();
+    if (!r) return fail(WFST_EINVAL, "wfst_result_frames: NULL result");
+    if (num_frames) *num_frames = r->T;
+    if (num_decoded) *num_decoded = r->Tp;
+    if (orig_frame) *orig_frame = r->kept.data();
+    return WFST_OK;
+}
+
+extern "C" int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs)
+{
+    clear_error();
+    if (!r) return fail(WFST_EINVAL, "wfst_result_lattice: NULL result");
+    std::lock_guard<std::mutex> lk(r->lat_mu);
+    if (!r->lat_loaded) {
+        r->lat_host.resize(static_cast<size_t>(r->lat_n));
+        if (r->lat_n) {
+            DeviceGuard dg(r->lat_dev->device);
+            hipError_t e = hipMemcpy(r->lat_host.data(), static_cast<int4 *>(r->lat_dev->p) + r->lat_off,
+                                     r->lat_n * sizeof(wfst_lat_arc), hipMemcpyDeviceToHost);
+            if (e != hipSuccess) return hip_fail(e, "wfst_result_lattice: copy");
+        }
+        r->lat_loaded = true;
+    }
+    if (n) *n = r->lat_n;
+    if (arcs) *arcs = r->lat_host.data();
+    return WFST_OK;
+}
+
+extern "C" int wfst_result_lattice_device(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs)
+{
+    clear_error();
+    if (!r) return fail(WFST_EINVAL, "wfst_result_lattice_device: NULL result");
+    if (n) *n = r->lat_n;
+    if (arcs)
+        *arcs = r->lat_dev ? reinterpret_cast<const wfst_lat_arc *>(static_cast<int4 *>(r->lat_dev->p) + r->lat_off)
+                           : nullptr;
+    return WFST_OK;
+}
+
+extern "C" int wfst_result_tokens(const wfst_result *r, int32_t j, int32_t *n, const int32_t **state,
+                                  const float **cost, const int32_t **bp_arc)
+{
+    clear_error();
+    if (!r) return fail(WFST_EINVAL, "wfst_result_tokens: NULL result");
+    if (!r->has_tokens) return fail(WFST_EINVAL, "wfst_result_tokens: decoded without WFST_RECORD_TOKENS");
+    if (j < 0 || j > r->Tp) return fail(WFST_EINVAL, "wfst_result_tokens: token set out of range");
+    const int64_t a = r->tok_off[j], b = r->tok_off[j + 1];
+    if (n) *n = static_cast<int32_t>(b - a);
+    if (state) *state = r->tok_state.data() + a;
+    if (cost) *cost = r->tok_cost.data() + a;
+    if (bp_arc) *bp_arc = r->tok_arc.data() + a;
+    return WFST_OK;
+}
+
+extern "C" int wfst_result_stats(const wfst_result *r, wfst_stats *stats)
+{
+    clear_error();
+    if (!r || !stats) return fail(WFST_EINVAL, "wfst_result_stats: NULL argument");
+    *stats = r->stats;
+    return WFST_OK;
+}
+
+extern "C" void wfst_result_free(wfst_result *r) { delete r; }

@@ -1,0 +1,183 @@
+// Device helpers shared by the wfstdec kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "internal.h"
+
+namespace wfd {
+
+// Ordered key of a float32: unsigned order of keys equals numeric order,
+// with -0 just below +0.  Costs are compared only through these keys.
+__device__ __forceinline__ uint32_t okey(float x)
+{
+    uint32_t u = __float_as_uint(x);
+    return (u >> 31) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float okey_val(uint32_t k)
+{
+    uint32_t u = (k >> 31) ? (k & 0x7FFFFFFFu) : ~k;
+    return __uint_as_float(u);
+}
+
+// Token = cost key (high word) | user arc + 1 (low word); 0 marks the start
+// token.  The unsigned minimum is the cheapest token, lowest arc on ties.
+__device__ __forceinline__ uint64_t make_tok(uint32_t key, int32_t arc)
+{
+    return (static_cast<uint64_t>(key) << 32) | static_cast<uint32_t>(arc + 1);
+}
+
+__device__ __forceinline__ float tok_cost(uint64_t t) { return okey_val(static_cast<uint32_t>(t >> 32)); }
+__device__ __forceinline__ int32_t tok_arc(uint64_t t) { return static_cast<int32_t>(static_cast<uint32_t>(t)) - 1; }
+
+// Key of the largest cost a token may keep: fl(best + beam), never +inf.
+__device__ __forceinline__ uint32_t beam_limit(uint32_t best_key, float beam)
+{
+    const uint32_t kmax = 0xFF7FFFFFu;   // okey(FLT_MAX)
+    if (best_key == kEmptyKey) return kmax;
+    uint32_t k = okey(okey_val(best_key) + beam);
+    return k < kmax ? k : kmax;
+}
+
+// Early-drop bound during expansion: any candidate above fl(m + beam),
+// m = a candidate cost already seen, can neither survive pruning nor lower a
+// token that survives.
+__device__ __forceinline__ uint32_t drop_bound(uint32_t m_key, float beam)
+{
+    if (m_key == kEmptyKey) return kEmptyKey;
+    return okey(okey_val(m_key) + beam);
+}
+
+__device__ __forceinline__ int lane_id() { return static_cast<int>(__lane_id()); }
+
+__device__ __forceinline__ uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
+
+__device__ __forceinline__ int rank_in(uint64_t mask) { return __popcll(mask & lanemask_lt()); }
+
+__device__ __forceinline__ int wave_incl_scan(int x)
+{
+    const int lane = lane_id();
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        int y = __shfl_up(x, d, kWave);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x)
+{
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+        uint32_t y = __shfl_xor(x, d, kWave);
+        x = y < x ? y : x;
+    }
+    return x;
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x)
+{
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+        uint64_t y = __shfl_xor(x, d, kWave);
+        x = y < x ? y : x;
+    }
+    return x;
+}
+
+__device__ __forceinline__ long long wave_sum_ll(long long x)
+{
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) x += __shfl_xor(x, d, kWave);
+    return x;
+}
+
+// Largest lane l with pre[l] <= k, where pre is the exclusive prefix of
+// per-lane counts (non-decreasing over lanes).  Called by the whole wave.
+__device__ __forceinline__ int owner_lane(int pre, int k)
+{
+    int lo = 0, hi = kWave - 1;
+#pragma unroll
+    for (int it = 0; it < 6; it++) {
+        int mid = (lo + hi + 1) >> 1;
+        int pm = __shfl(pre, mid, kWave);
+        if (pm <= k) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+template <typename T>
+__device__ __forceinline__ T ld_relaxed(T *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void set_status(UttState &st, int code)
+{
+    atomicCAS(&st.status, 0, code);
+}
+
+// Utterance u takes part in producing token set k.
+__device__ __forceinline__ bool live(const UttState &st, int k)
+{
+    return st.status == 0 && k <= st.Tp;
+}
+
+// Flattened chunk space over utterances: utterance u owns ceil(n_u / per)
+// chunks.  For a group of up to 64 utterances starting at grp, each lane
+// holds its utterance's inclusive chunk prefix.
+struct ChunkGroup {
+    int incl;     // inclusive prefix of this lane's utterance
+    int cnt;      // chunks of this lane's utterance
+    int total;    // chunks in the group
+};
+
+__device__ __forceinline__ ChunkGroup chunk_group(int n_u, int per)
+{
+    ChunkGroup g;
+    g.cnt = (n_u + per - 1) / per;
+    g.incl = wave_incl_scan(g.cnt);
+    g.total = __shfl(g.incl, kWave - 1, kWave);
+    return g;
+}
+
+// For chunk c (wave-uniform, < total) of the group: the lane (utterance
+// offset inside the group) that owns it, and the chunk index inside it.
+__device__ __forceinline__ void chunk_locate(const ChunkGroup &g, int c, int &ul, int &ci)
+{
+    uint64_t m = __ballot(g.incl <= c);
+    ul = __popcll(m);
+    int incl = __shfl(g.incl, ul, kWave);
+    int cnt = __shfl(g.cnt, ul, kWave);
+    ci = c - (incl - cnt);
+}
+
+// Block-wide exclusive scan of one int per thread (blockDim.x a multiple of
+// 64, at most 1024).  `sh` needs 17 ints.  Returns the exclusive prefix and
+// stores the block total in *total.
+__device__ __forceinline__ int block_excl_scan(int x, int *sh, int *total)
+{
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int nw = blockDim.x / kWave;
+    int incl = wave_incl_scan(x);
+    if (lane == kWave - 1) sh[w] = incl;
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+        int v = threadIdx.x < nw ? sh[threadIdx.x] : 0;
+        int vi = wave_incl_scan(v);
+        if (threadIdx.x < nw) sh[threadIdx.x] = vi - v;
+        if (threadIdx.x == kWave - 1) sh[16] = vi;
+    }
+    __syncthreads();
+    int res = incl - x + sh[w];
+    *total = sh[16];
+    __syncthreads();
+    return res;
+}
+
+}  // namespace wfd

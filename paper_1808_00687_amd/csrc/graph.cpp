@@ -1,0 +1,221 @@
+// wfst_load: validation and device layout of the search graph.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace wfd {
+
+static thread_local std::string g_err;
+
+void set_error(const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+}
+
+void clear_error() { g_err.clear(); }
+
+const char *last_error() { return g_err.c_str(); }
+
+}  // namespace wfd
+
+using namespace wfd;
+
+extern "C" const char *wfst_last_error(void) { return wfd::last_error(); }
+
+namespace {
+
+int fail(int code, const char *msg)
+{
+    set_error("%s", msg);
+    return code;
+}
+
+}  // namespace
+
+extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t *dst,
+                         const int32_t *ilabel, const int32_t *olabel, const float *weight,
+                         int32_t start, const float *final_weight, wfst_graph **out)
+{
+    clear_error();
+    if (!out) return fail(WFST_EINVAL, "wfst_load: out is NULL");
+    *out = nullptr;
+    if (n < 1) return fail(WFST_EINVAL, "wfst_load: num_states must be >= 1");
+    if (e < 0 || e >= 2147483647LL) return fail(WFST_EINVAL, "wfst_load: num_arcs out of range");
+    if (start < 0 || start >= n) return fail(WFST_EINVAL, "wfst_load: start_state out of range");
+    if (e > 0 && (!src || !dst || !ilabel || !olabel || !weight))
+        return fail(WFST_EINVAL, "wfst_load: NULL arc array");
+
+    int32_t max_il = 0;
+    int64_t n_eps = 0;
+    for (int64_t a = 0; a < e; a++) {
+        if (src[a] < 0 || src[a] >= n) return fail(WFST_EINVAL, "wfst_load: src out of range");
+        if (a && src[a] < src[a - 1]) return fail(WFST_EINVAL, "wfst_load: src not sorted");
+        if (dst[a] < 0 || dst[a] >= n) return fail(WFST_EINVAL, "wfst_load: dst out of range");
+        if (ilabel[a] < 0 || olabel[a] < 0) return fail(WFST_EINVAL, "wfst_load: negative label");
+        if (!std::isfinite(weight[a])) return fail(WFST_EINVAL, "wfst_load: non-finite weight");
+        if (ilabel[a] == 0) {
+            if (weight[a] < 0.0f) return fail(WFST_EINVAL, "wfst_load: negative epsilon weight");
+            n_eps++;
+        }
+        if (ilabel[a] > max_il) max_il = ilabel[a];
+    }
+    if (final_weight) {
+        for (int32_t s = 0; s < n; s++) {
+            float f = final_weight[s];
+            if (std::isnan(f) || (std::isinf(f) && f < 0))
+                return fail(WFST_EINVAL, "wfst_load: final weight NaN or -inf");
+        }
+    }
+    const int64_t n_emit = e - n_eps;
+
+    std::vector<int32_t> eoff, xoff, arc_src;
+    std::vector<int4> earc, xarc;
+    std::vector<uint8_t> has_eps;
+    int32_t depth = 0;
+    try {
+        eoff.assign(static_cast<size_t>(n) + 1, 0);
+        xoff.assign(static_cast<size_t>(n) + 1, 0);
+        for (int64_t a = 0; a < e; a++) {
+            if (ilabel[a]) eoff[src[a] + 1]++;
+            else xoff[src[a] + 1]++;
+        }
+        for (int32_t s = 0; s < n; s++) {
+            eoff[s + 1] += eoff[s];
+            xoff[s + 1] += xoff[s];
+        }
+        has_eps.assign(static_cast<size_t>(n), 0);
+        for (int32_t s = 0; s < n; s++) has_eps[s] = xoff[s + 1] > xoff[s];
+
+        // epsilon subgraph: acyclic (Kahn) and its longest path
+        std::vector<int32_t> indeg(static_cast<size_t>(n), 0), lvl(static_cast<size_t>(n), 0), q;
+        q.reserve(static_cast<size_t>(n));
+        std::vector<int64_t> row(static_cast<size_t>(n) + 1, 0);
+        for (int64_t a = 0; a < e; a++) row[src[a] + 1]++;
+        for (int32_t s = 0; s < n; s++) row[s + 1] += row[s];
+        for (int64_t a = 0; a < e; a++)
+            if (!ilabel[a]) indeg[dst[a]]++;
+        for (int32_t s = 0; s < n; s++)
+            if (!indeg[s]) q.push_back(s);
+        for (size_t h = 0; h < q.size(); h++) {
+            int32_t s = q[h];
+            for (int64_t a = row[s]; a < row[s + 1]; a++) {
+                if (ilabel[a]) continue;
+                int32_t d = dst[a];
+                if (lvl[s] + 1 > lvl[d]) lvl[d] = lvl[s] + 1;
+                if (lvl[d] > depth) depth = lvl[d];
+                if (--indeg[d] == 0) q.push_back(d);
+            }
+        }
+        if (static_cast<int64_t>(q.size()) != n) return fail(WFST_EINVAL, "wfst_load: epsilon cycle");
+
+        earc.resize(static_cast<size_t>(n_emit));
+        xarc.resize(static_cast<size_t>(n_eps));
+        arc_src.resize(static_cast<size_t>(e));
+        std::vector<int32_t> ef(eoff.begin(), eoff.end() - 1), xf(xoff.begin(), xoff.end() - 1);
+        for (int64_t a = 0; a < e; a++) {
+            int32_t s = src[a], d = dst[a];
+            int32_t dflag = d | (has_eps[d] ? static_cast<int32_t>(0x80000000u) : 0);
+            int32_t wb;
+            std::memcpy(&wb, &weight[a], 4);
+            if (ilabel[a]) {
+                earc[ef[s]++] = make_int4(dflag, ilabel[a] - 1, wb, static_cast<int32_t>(a));
+                arc_src[a] = s;
+            } else {
+                xarc[xf[s]++] = make_int4(dflag, wb, static_cast<int32_t>(a), 0);
+                arc_src[a] = s | static_cast<int32_t>(0x80000000u);
+            }
+        }
+    } catch (const std::bad_alloc &) {
+        return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
+    }
+
+    auto align = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
+    const size_t b_eoff = align((static_cast<size_t>(n) + 1) * 4);
+    const size_t b_xoff = b_eoff;
+    const size_t b_earc = align(static_cast<size_t>(n_emit) * 16 + 16);
+    const size_t b_xarc = align(static_cast<size_t>(n_eps) * 16 + 16);
+    const size_t b_src = align(static_cast<size_t>(e) * 4 + 4);
+    const size_t b_fin = final_weight ? align(static_cast<size_t>(n) * 4) : 0;
+    const size_t total = b_eoff + b_xoff + b_earc + b_xarc + b_src + b_fin;
+
+    wfst_graph *h = new (std::nothrow) wfst_graph();
+    if (!h) return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
+    Graph &g = h->g;
+    if (hipGetDevice(&g.device) != hipSuccess) {
+        delete h;
+        return fail(WFST_EDEVICE, "wfst_load: no HIP device");
+    }
+    char *mem = nullptr;
+    hipError_t err = hipMalloc(reinterpret_cast<void **>(&mem), total);
+    if (err != hipSuccess) {
+        delete h;
+        set_error("wfst_load: hipMalloc(%zu) failed: %s", total, hipGetErrorString(err));
+        return err == hipErrorOutOfMemory ? WFST_ENOMEM : WFST_EDEVICE;
+    }
+    size_t off = 0;
+    auto put = [&](const void *hostp, size_t bytes, size_t span) -> void * {
+        void *d = mem + off;
+        off += span;
+        if (bytes && err == hipSuccess) err = hipMemcpy(d, hostp, bytes, hipMemcpyHostToDevice);
+        return d;
+    };
+    g.d.n = n;
+    g.d.e = e;
+    g.d.start = start;
+    g.d.n_emit = n_emit;
+    g.d.n_eps = n_eps;
+    g.d.eoff = static_cast<const int32_t *>(put(eoff.data(), eoff.size() * 4, b_eoff));
+    g.d.xoff = static_cast<const int32_t *>(put(xoff.data(), xoff.size() * 4, b_xoff));
+    g.d.earc = static_cast<const int4 *>(put(earc.data(), earc.size() * 16, b_earc));
+    g.d.xarc = static_cast<const int4 *>(put(xarc.data(), xarc.size() * 16, b_xarc));
+    g.d.arc_src = static_cast<const int32_t *>(put(arc_src.data(), arc_src.size() * 4, b_src));
+    g.d.final_w = final_weight ? static_cast<const float *>(put(final_weight, static_cast<size_t>(n) * 4, b_fin)) : nullptr;
+    if (err != hipSuccess) {
+        hipFree(mem);
+        delete h;
+        set_error("wfst_load: hipMemcpy failed: %s", hipGetErrorString(err));
+        return WFST_EDEVICE;
+    }
+    g.mem = mem;
+    g.max_ilabel = max_il;
+    g.eps_depth = depth;
+    g.device_bytes = static_cast<int64_t>(total);
+    *out = h;
+    return WFST_OK;
+}
+
+extern "C" void wfst_graph_free(wfst_graph *h)
+{
+    if (!h) return;
+    int cur = 0;
+    hipGetDevice(&cur);
+    if (cur != h->g.device) hipSetDevice(h->g.device);
+    hipFree(h->g.mem);
+    if (cur != h->g.device) hipSetDevice(cur);
+    delete h;
+}
+
+extern "C" int wfst_graph_get_info(const wfst_graph *h, wfst_graph_info *info)
+{
+    clear_error();
+    if (!h || !info) return fail(WFST_EINVAL, "wfst_graph_get_info: NULL argument");
+    info->num_states = h->g.d.n;
+    info->num_arcs = h->g.d.e;
+    info->num_emitting = h->g.d.n_emit;
+    info->num_epsilon = h->g.d.n_eps;
+    info->max_ilabel = h->g.max_ilabel;
+    info->epsilon_depth = h->g.eps_depth;
+    info->device_bytes = h->g.device_bytes;
+    return WFST_OK;
+}

@@ -1,0 +1,174 @@
+// Internal structures of the wfstdec HIP library (gfx950).
+//
+// Device layout of a graph (built once by wfst_load):
+//   eoff[N+1]  emitting-arc row offsets; earc[] 16-byte records
+//              {dst | has_eps << 31, column = ilabel - 1, weight bits, user arc}
+//   xoff[N+1]  epsilon-arc row offsets; xarc[] 16-byte records
+//              {dst | has_eps << 31, weight bits, user arc, 0}
+//   arc_src[E] user arc -> src state | is_epsilon << 31 (cold, back-pointers)
+//   final_w[N] final costs or null
+// Each state's arcs keep their user order inside the emitting and the
+// epsilon partition.  has_eps marks a destination with epsilon out-arcs, so a
+// kernel that lowers its token knows without another load whether the
+// epsilon closure has to continue from it.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "wfstdec.h"
+
+namespace wfd {
+
+constexpr uint64_t kEmptyTok = ~0ull;
+constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
+constexpr uint32_t kDstMask = 0x7FFFFFFFu;
+constexpr int kHistBits = 12;               // radix-select digit width
+constexpr int kHistBins = 1 << kHistBits;   // bins per utterance histogram
+constexpr int kWave = 64;                   // gfx950 wavefront
+constexpr int kQueueCap = 256;              // per-wave LDS epsilon queue (items)
+
+struct DevGraph {
+    int32_t n;
+    int32_t start;
+    int64_t e;
+    int64_t n_emit, n_eps;
+    const int32_t *eoff;
+    const int4 *earc;
+    const int32_t *xoff;
+    const int4 *xarc;
+    const int32_t *arc_src;
+    const float *final_w;
+};
+
+// Host-side graph object behind the opaque wfst_graph handle.
+struct Graph {
+    DevGraph d;
+    int device;
+    int32_t max_ilabel;
+    int32_t eps_depth;
+    int64_t device_bytes;
+    void *mem;   // single device allocation holding every array
+};
+
+// Per-utterance decode state in device memory.  Fields marked "frame" are
+// reset by the advance kernel after each produced token set.
+struct UttState {
+    const float *ll;      // [T x L] log-likelihoods (device)
+    int32_t T;
+    int32_t Tp;           // decoded frames (set by the classify kernel)
+    int32_t status;       // WFST_OK, WFST_ENOPATH or WFST_ECAPACITY
+    int32_t pad0;
+    // frame
+    uint32_t best;        // minimum cost key among candidates of the set in production
+    int32_t ntouched;     // states holding a token in the set in production
+    int32_t n_in_beam;    // of those, within the beam
+    uint32_t cut;         // pruning cutoff key of the set in production
+    int32_t n_new;        // survivors appended for the set in production
+    int32_t ovf;          // epsilon items spilled to the overflow list
+    // previous set
+    int32_t n_cur;        // |S_{k-1}|
+    int32_t best_sv;      // survivor index of a cheapest token of S_{k-1}
+    // cumulative
+    int64_t sv_base;      // survivor index where the set in production starts
+    int64_t le_cnt;       // emitting lattice records so far
+    int64_t lx_cnt;       // epsilon lattice records so far
+    int64_t tokens;
+    int64_t arcs_expanded;
+    int64_t eps_arcs;
+    // final
+    int32_t final_sv;
+    int32_t final_state;
+    int32_t reached_final;
+    float final_cost;
+    int32_t path_len;
+    int32_t pad1;
+    int64_t lat_kept;
+};
+
+// Per-utterance regions inside the shared workspace buffers (element offsets).
+struct UttLayout {
+    int64_t sv0, svcap;       // survivors
+    int64_t le0, lecap;       // emitting lattice records
+    int64_t lx0, lxcap;       // epsilon lattice records
+    int64_t fo0;              // per-frame offset arrays, T + 2 entries each
+    int64_t kept0;            // kept-frame list, T entries
+    int64_t path0, pathcap;   // best path (arcs and frames)
+    int64_t lo0;              // lattice output records
+};
+
+// Everything a kernel needs, passed by value.
+struct Params {
+    DevGraph g;
+    int32_t U;
+    int32_t L;
+    float beam;
+    int32_t max_active;
+    float lattice_beam;
+    int32_t lattice;
+    int32_t blank_id;
+    float blank_thr;
+    int32_t qcap;             // effective per-wave queue capacity (<= kQueueCap)
+    int32_t pad;
+    UttState *st;
+    const UttLayout *lay;
+    int32_t *cur;             // index k of the token set in production
+    // dense per-utterance tables, U x N
+    uint64_t *tok;
+    int32_t *pos;             // U x 2 x N: survivor index of each state, by set parity
+    // per-frame scratch, U x capT
+    int32_t *touched;
+    uint64_t *pk;
+    int64_t capT;
+    uint64_t *ovf;            // U x capO overflow epsilon items (state << 32 | cost bits)
+    int64_t capO;
+    uint32_t *hist;           // U x kHistBins
+    uint32_t *done;           // last-block counter of the expansion kernel
+    // survivors (per utterance regions)
+    int32_t *sv_state;
+    uint64_t *sv_tok;
+    int32_t *sv_prev;
+    uint32_t *e_key;          // lattice backward extra cost per survivor (ordered key)
+    // lattice raw records {src survivor, dst survivor, user arc, prefix cost bits}
+    int4 *lat_e;
+    int4 *lat_x;
+    float *ex_e;
+    float *ex_x;
+    int4 *lat_out;            // kept lattice {frame, arc, cost bits, extra bits}
+    // per-frame arrays (fo0 region): sv_off, le_off, lx_off, lat_cnt
+    int64_t *sv_off;
+    int64_t *le_off;
+    int64_t *lx_off;
+    int64_t *lo_off;
+    int32_t *kept;
+    int32_t *path_arc;
+    int32_t *path_frame;
+};
+
+// ---- launchers (search_kernels.hip / final_kernels.hip) ----
+hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);
+hipError_t launch_classify(const Params &p, hipStream_t s);
+hipError_t launch_init(const Params &p, hipStream_t s);
+hipError_t launch_expand(const Params &p, int grid, hipStream_t s);
+hipError_t launch_prune_gather(const Params &p, int grid, hipStream_t s);
+hipError_t launch_prune_select(const Params &p, hipStream_t s);
+hipError_t launch_prune_compact(const Params &p, int grid, hipStream_t s);
+hipError_t launch_record(const Params &p, int grid, hipStream_t s);
+hipError_t launch_advance(const Params &p, hipStream_t s);
+hipError_t launch_final(const Params &p, hipStream_t s);
+hipError_t launch_backtrace(const Params &p, hipStream_t s);
+hipError_t launch_lattice_backward(const Params &p, hipStream_t s);
+hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
+
+// ---- host helpers (errors.cpp) ----
+void set_error(const char *fmt, ...);
+void clear_error();
+
+}  // namespace wfd
+
+// Opaque handle types of the C ABI.
+struct wfst_graph {
+    wfd::Graph g;
+};

@@ -1,0 +1,373 @@
+"""Thin Python binding of libwfstdec.so (the C ABI in include/wfstdec.h).
+
+The functions keep the C names (``wfst_load``, ``wfst_decode``,
+``wfst_decode_batch``, ...) and only marshal arguments: every step of the
+decode runs in the library's HIP kernels.  PyTorch supplies device memory
+and streams; inputs may be torch tensors on the GPU (the normal case) or
+numpy arrays (copied by the library, WFST_LOGLIKES_HOST).
+
+If the library has not been built this module raises on import: there is no
+CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+import os
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libwfstdec.so")
+
+WFST_OK = 0
+WFST_EINVAL = -1
+WFST_ENOMEM = -2
+WFST_ENOPATH = -3
+WFST_ECAPACITY = -4
+WFST_EDEVICE = -5
+
+WFST_RECORD_TOKENS = 1
+WFST_LOGLIKES_HOST = 2
+WFST_PROFILE = 4
+
+
+class WfstError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("wfstdec error %d: %s" % (code, msg))
+        self.code = code
+
+
+class _Opts(C.Structure):
+    _fields_ = [("beam", C.c_float), ("max_active", C.c_int32), ("lattice_beam", C.c_float),
+                ("blank_threshold", C.c_float), ("blank_id", C.c_int32), ("flags", C.c_uint32),
+                ("capacity_hint", C.c_int64)]
+
+
+class _Info(C.Structure):
+    _fields_ = [("num_states", C.c_int32), ("num_arcs", C.c_int64), ("num_emitting", C.c_int64),
+                ("num_epsilon", C.c_int64), ("max_ilabel", C.c_int32), ("epsilon_depth", C.c_int32),
+                ("device_bytes", C.c_int64)]
+
+
+class _Stats(C.Structure):
+    _fields_ = [("frames", C.c_int32), ("frames_decoded", C.c_int32), ("tokens", C.c_int64),
+                ("arcs_expanded", C.c_int64), ("eps_arcs", C.c_int64), ("lattice_raw", C.c_int64),
+                ("lattice_kept", C.c_int64), ("decode_ms", C.c_double), ("expand_ms", C.c_double),
+                ("prune_ms", C.c_double), ("record_ms", C.c_double), ("final_ms", C.c_double),
+                ("expand_launches", C.c_int32)]
+
+
+class _LatArc(C.Structure):
+    _fields_ = [("frame", C.c_int32), ("arc", C.c_int32), ("cost", C.c_float), ("extra", C.c_float)]
+
+
+def _load_lib():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libwfstdec.so is not built (run __graft_entry__.build() or "
+                          "python -m paper_1808_00687_amd.csrc.build)")
+    lib = C.CDLL(LIB_PATH)
+    i32p, f32p, vp = C.POINTER(C.c_int32), C.POINTER(C.c_float), C.c_void_p
+    lib.wfst_load.argtypes = [C.c_int32, C.c_int64, i32p, i32p, i32p, i32p, f32p, C.c_int32, f32p,
+                              C.POINTER(vp)]
+    lib.wfst_load.restype = C.c_int
+    lib.wfst_graph_free.argtypes = [vp]
+    lib.wfst_graph_free.restype = None
+    lib.wfst_graph_get_info.argtypes = [vp, C.POINTER(_Info)]
+    lib.wfst_graph_get_info.restype = C.c_int
+    lib.wfst_default_opts.argtypes = [C.POINTER(_Opts)]
+    lib.wfst_default_opts.restype = None
+    lib.wfst_decode.argtypes = [vp, vp, C.c_int32, C.c_int32, C.POINTER(_Opts), vp, C.POINTER(vp)]
+    lib.wfst_decode.restype = C.c_int
+    lib.wfst_decode_batch.argtypes = [vp, C.c_int32, C.POINTER(vp), i32p, C.c_int32,
+                                      C.POINTER(_Opts), vp, C.POINTER(vp)]
+    lib.wfst_decode_batch.restype = C.c_int
+    lib.wfst_result_status.argtypes = [vp]
+    lib.wfst_result_status.restype = C.c_int
+    lib.wfst_result_best.argtypes = [vp, f32p, i32p, i32p, i32p, C.POINTER(i32p), C.POINTER(i32p)]
+    lib.wfst_result_best.restype = C.c_int
+    lib.wfst_result_frames.argtypes = [vp, i32p, i32p, C.POINTER(i32p)]
+    lib.wfst_result_frames.restype = C.c_int
+    lib.wfst_result_lattice.argtypes = [vp, C.POINTER(C.c_int64), C.POINTER(C.POINTER(_LatArc))]
+    lib.wfst_result_lattice.restype = C.c_int
+    lib.wfst_result_lattice_device.argtypes = [vp, C.POINTER(C.c_int64), C.POINTER(vp)]
+    lib.wfst_result_lattice_device.restype = C.c_int
+    lib.wfst_result_tokens.argtypes = [vp, C.c_int32, i32p, C.POINTER(i32p), C.POINTER(f32p),
+                                       C.POINTER(i32p)]
+    lib.wfst_result_tokens.restype = C.c_int
+    lib.wfst_result_stats.argtypes = [vp, C.POINTER(_Stats)]
+    lib.wfst_result_stats.restype = C.c_int
+    lib.wfst_result_free.argtypes = [vp]
+    lib.wfst_result_free.restype = None
+    lib.wfst_last_error.argtypes = []
+    lib.wfst_last_error.restype = C.c_char_p
+    return lib
+
+
+_lib = _load_lib()
+
+
+def wfst_last_error() -> str:
+    return _lib.wfst_last_error().decode(errors="replace")
+
+
+def _check(rc: int, what: str):
+    if rc != WFST_OK:
+        raise WfstError(rc, "%s: %s" % (what, wfst_last_error()))
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _p(a, ct):
+    return None if a is None else a.ctypes.data_as(C.POINTER(ct))
+
+
+# --------------------------------------------------------------------------
+# graphs
+# --------------------------------------------------------------------------
+
+class WfstGraph:
+    """Owns a wfst_graph handle (device layout of one WFST)."""
+
+    def __init__(self, handle):
+        self._h = handle
+
+    @property
+    def handle(self):
+        return self._h
+
+    def info(self) -> dict:
+        i = _Info()
+        _check(_lib.wfst_graph_get_info(self._h, C.byref(i)), "wfst_graph_get_info")
+        return {f: getattr(i, f) for f, _ in _Info._fields_}
+
+    def free(self):
+        if self._h:
+            _lib.wfst_graph_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def wfst_load(num_states: int, src, dst, ilabel, olabel, weight, start_state: int = 0,
+              final_weight=None) -> WfstGraph:
+    """Validate and upload a WFST (arc arrays sorted by src); see wfst_load in
+    include/wfstdec.h."""
+    src, dst, il, ol = _i32(src), _i32(dst), _i32(ilabel), _i32(olabel)
+    w = np.ascontiguousarray(weight, dtype=np.float32)
+    fw = None if final_weight is None else np.ascontiguousarray(final_weight, dtype=np.float32)
+    e = src.shape[0]
+    if not (dst.shape[0] == il.shape[0] == ol.shape[0] == w.shape[0] == e):
+        raise ValueError("arc arrays differ in length")
+    if fw is not None and fw.shape[0] != num_states:
+        raise ValueError("final_weight must have num_states entries")
+    h = C.c_void_p()
+    rc = _lib.wfst_load(num_states, e, _p(src, C.c_int32), _p(dst, C.c_int32), _p(il, C.c_int32),
+                        _p(ol, C.c_int32), _p(w, C.c_float), start_state, _p(fw, C.c_float),
+                        C.byref(h))
+    _check(rc, "wfst_load")
+    return WfstGraph(h)
+
+
+def load_graph(g) -> WfstGraph:
+    """wfst_load from an object with the fields of workloads.Graph."""
+    return wfst_load(g.num_states, g.src, g.dst, g.ilabel, g.olabel, g.weight, g.start, g.final)
+
+
+# --------------------------------------------------------------------------
+# results
+# --------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class WfstResult:
+    status: int
+    num_frames: int = 0
+    num_decoded: int = 0
+    kept: Optional[np.ndarray] = None
+    cost: float = float("nan")
+    final_state: int = -1
+    reached_final: int = 0
+    path_arcs: Optional[np.ndarray] = None
+    path_frames: Optional[np.ndarray] = None
+    lat_frame: Optional[np.ndarray] = None
+    lat_arc: Optional[np.ndarray] = None
+    lat_cost: Optional[np.ndarray] = None
+    lat_extra: Optional[np.ndarray] = None
+    tok_off: Optional[np.ndarray] = None
+    tok_state: Optional[np.ndarray] = None
+    tok_cost: Optional[np.ndarray] = None
+    tok_arc: Optional[np.ndarray] = None
+    stats: Optional[dict] = None
+
+    def token_set(self, j: int):
+        """(state, cost bits, back-pointer arc) of token set j, sorted by state."""
+        a, b = int(self.tok_off[j]), int(self.tok_off[j + 1])
+        return self.tok_state[a:b], self.tok_cost[a:b].view(np.uint32), self.tok_arc[a:b]
+
+
+def _arr(ptr, n, dt):
+    if n <= 0 or not ptr:
+        return np.zeros(0, dtype=dt)
+    return np.ctypeslib.as_array(ptr, shape=(n,)).astype(dt, copy=True)
+
+
+def _collect(h, lattice: bool, tokens: bool) -> WfstResult:
+    st = _lib.wfst_result_status(h)
+    r = WfstResult(status=st)
+    nf, nd = C.c_int32(), C.c_int32()
+    kp = C.POINTER(C.c_int32)()
+    _check(_lib.wfst_result_frames(h, C.byref(nf), C.byref(nd), C.byref(kp)), "wfst_result_frames")
+    r.num_frames, r.num_decoded = nf.value, nd.value
+    r.kept = _arr(kp, nd.value, np.int32)
+    s = _Stats()
+    _check(_lib.wfst_result_stats(h, C.byref(s)), "wfst_result_stats")
+    r.stats = {f: getattr(s, f) for f, _ in _Stats._fields_}
+    if st != WFST_OK:
+        return r
+    cost, fs, rf, n = C.c_float(), C.c_int32(), C.c_int32(), C.c_int32()
+    pa, pf = C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)()
+    _check(_lib.wfst_result_best(h, C.byref(cost), C.byref(fs), C.byref(rf), C.byref(n),
+                                 C.byref(pa), C.byref(pf)), "wfst_result_best")
+    r.cost, r.final_state, r.reached_final = float(np.float32(cost.value)), fs.value, rf.value
+    r.path_arcs = _arr(pa, n.value, np.int32)
+    r.path_frames = _arr(pf, n.value, np.int32)
+    if lattice:
+        ln = C.c_int64()
+        la = C.POINTER(_LatArc)()
+        _check(_lib.wfst_result_lattice(h, C.byref(ln), C.byref(la)), "wfst_result_lattice")
+        if ln.value:
+            raw = np.ctypeslib.as_array(C.cast(la, C.POINTER(C.c_int32)), shape=(ln.value, 4)).copy()
+        else:
+            raw = np.zeros((0, 4), np.int32)
+        r.lat_frame = raw[:, 0].copy()
+        r.lat_arc = raw[:, 1].copy()
+        r.lat_cost = raw[:, 2].copy().view(np.float32)
+        r.lat_extra = raw[:, 3].copy().view(np.float32)
+    if tokens:
+        offs = [0]
+        states, costs, arcs = [], [], []
+        for j in range(r.num_decoded + 1):
+            tn = C.c_int32()
+            sp, cp, ap = C.POINTER(C.c_int32)(), C.POINTER(C.c_float)(), C.POINTER(C.c_int32)()
+            _check(_lib.wfst_result_tokens(h, j, C.byref(tn), C.byref(sp), C.byref(cp), C.byref(ap)),
+                   "wfst_result_tokens")
+            states.append(_arr(sp, tn.value, np.int32))
+            costs.append(_arr(cp, tn.value, np.float32))
+            arcs.append(_arr(ap, tn.value, np.int32))
+            offs.append(offs[-1] + tn.value)
+        r.tok_off = np.array(offs, np.int64)
+        r.tok_state = np.concatenate(states)
+        r.tok_cost = np.concatenate(costs)
+        r.tok_arc = np.concatenate(arcs)
+    return r
+
+
+# --------------------------------------------------------------------------
+# decode
+# --------------------------------------------------------------------------
+
+def _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint) -> _Opts:
+    o = _Opts()
+    _lib.wfst_default_opts(C.byref(o))
+    o.beam = beam
+    o.max_active = max_active
+    o.lattice_beam = lattice_beam
+    o.blank_threshold = blank_threshold
+    o.blank_id = blank_id
+    o.flags = flags
+    o.capacity_hint = capacity_hint
+    return o
+
+
+def _ll_ptr(x, keep: list):
+    """Device pointer of a CUDA float32 tensor, or host pointer of numpy."""
+    if isinstance(x, np.ndarray):
+        a = np.ascontiguousarray(x, dtype=np.float32)
+        keep.append(a)
+        return a.ctypes.data, a.shape, True
+    import torch
+    if not isinstance(x, torch.Tensor):
+        raise TypeError("loglikes must be a torch tensor or a numpy array")
+    if x.dtype != torch.float32 or x.dim() != 2:
+        raise ValueError("loglikes must be a 2-D float32 tensor [T x L]")
+    if not x.is_contiguous():
+        x = x.contiguous()
+    keep.append(x)
+    return x.data_ptr(), tuple(x.shape), not x.is_cuda
+
+
+def _stream_handle(stream):
+    if stream is None:
+        try:
+            import torch
+            if torch.cuda.is_available():
+                return torch.cuda.current_stream().cuda_stream
+        except Exception:
+            pass
+        return None
+    return getattr(stream, "cuda_stream", stream)
+
+
+def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_active: int = 0,
+                      lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
+                      record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
+                      stream=None) -> List[WfstResult]:
+    """Decode utterances in lock-step (wfst_decode_batch).  ``loglikes`` are
+    [T_u x L] float32 tensors on the graph's device (or numpy arrays)."""
+    keep: list = []
+    ptrs, Ts, L, host = [], [], None, None
+    for x in loglikes:
+        ptr, shape, is_host = _ll_ptr(x, keep)
+        if L is None:
+            L, host = shape[1], is_host
+        if shape[1] != L or is_host != host:
+            raise ValueError("all utterances need the same L and memory kind")
+        ptrs.append(ptr)
+        Ts.append(shape[0])
+    n = len(ptrs)
+    flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
+        (WFST_PROFILE if profile else 0)
+    o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint)
+    parr = (C.c_void_p * n)(*ptrs)
+    tarr = np.array(Ts, np.int32)
+    outs = (C.c_void_p * n)()
+    rc = _lib.wfst_decode_batch(graph.handle, n, parr, _p(tarr, C.c_int32), L, C.byref(o),
+                                _stream_handle(stream), outs)
+    _check(rc, "wfst_decode_batch")
+    res = []
+    try:
+        for h in outs:
+            res.append(_collect(h, lattice_beam >= 0, record_tokens))
+    finally:
+        for h in outs:
+            _lib.wfst_result_free(h)
+    return res
+
+
+def wfst_decode(graph: WfstGraph, loglikes, beam: float, max_active: int = 0,
+                lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
+                record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
+                stream=None) -> WfstResult:
+    """Decode one utterance (wfst_decode).  Returns the result also when the
+    status is WFST_ENOPATH; other errors raise WfstError."""
+    keep: list = []
+    ptr, shape, host = _ll_ptr(loglikes, keep)
+    flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
+        (WFST_PROFILE if profile else 0)
+    o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint)
+    out = C.c_void_p()
+    rc = _lib.wfst_decode(graph.handle, ptr, shape[0], shape[1], C.byref(o), _stream_handle(stream),
+                          C.byref(out))
+    if rc not in (WFST_OK, WFST_ENOPATH) or not out:
+        raise WfstError(rc, "wfst_decode: %s" % wfst_last_error())
+    try:
+        return _collect(out, lattice_beam >= 0, record_tokens)
+    finally:
+        _lib.wfst_result_free(out)

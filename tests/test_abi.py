@@ -1,0 +1,89 @@
+"""The C-ABI library loads, exports every declared entry point, and its graph
+validation agrees with the oracle's (no GPU needed: validation runs on the
+host before any device call)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_1808_00687_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wfstdec.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(wfst_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_api():
+    names = declared_functions()
+    for n in ("wfst_load", "wfst_decode", "wfst_decode_batch", "wfst_result_best",
+              "wfst_result_lattice", "wfst_result_tokens", "wfst_result_free", "wfst_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_1808_00687_amd import wfstdec
+    import ctypes
+    lib = ctypes.CDLL(wfstdec.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def _graph(n, arcs, start=0, final=None):
+    a = np.array(arcs, dtype=np.float64).reshape(-1, 5)
+    return W.Graph(n, a[:, 0].astype(np.int32), a[:, 1].astype(np.int32), a[:, 2].astype(np.int32),
+                   a[:, 3].astype(np.int32), a[:, 4].astype(np.float32), start,
+                   None if final is None else np.asarray(final, np.float32))
+
+
+BASE = [[0, 1, 1, 0, 1.0], [1, 2, 0, 0, 0.5], [2, 0, 2, 0, 0.0]]
+
+
+def _cases():
+    def mod(**kw):
+        g = _graph(3, BASE)
+        for k, v in kw.items():
+            getattr(g, k)[:] = v
+        return g
+    yield "ok", _graph(3, BASE)
+    yield "unsorted", mod(src=[1, 0, 2])
+    yield "dst_range", mod(dst=[0, 3, 0])
+    yield "src_range", mod(src=[0, 1, 3])
+    yield "neg_label", mod(ilabel=[1, 0, -1])
+    yield "neg_olabel", mod(olabel=[0, -2, 0])
+    yield "nan_weight", mod(weight=[np.nan, 0.5, 0.0])
+    yield "inf_weight", mod(weight=[np.inf, 0.5, 0.0])
+    yield "neg_eps_weight", mod(weight=[1.0, -0.5, 0.0])
+    yield "neg_emit_weight_ok", mod(weight=[-1.0, 0.5, 0.0])
+    yield "eps_path_ok", mod(ilabel=[1, 0, 0])
+    yield "eps_cycle", mod(ilabel=[0, 0, 0])
+    yield "eps_selfloop", mod(src=[0, 1, 2], dst=[1, 2, 2], ilabel=[1, 0, 0])
+    yield "start_range", _graph(3, BASE, start=3)
+    yield "final_nan", _graph(3, BASE, final=[0.0, np.nan, 0.0])
+    yield "final_neginf", _graph(3, BASE, final=[0.0, -np.inf, 0.0])
+    yield "final_inf_ok", _graph(3, BASE, final=[0.0, np.inf, 1.0])
+    yield "no_arcs_ok", W.Graph(2, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32),
+                                np.zeros(0, np.int32), np.zeros(0, np.float32))
+
+
+@pytest.mark.parametrize("name,g", list(_cases()))
+def test_validation_agrees_with_oracle(oracle_mod, name, g):
+    from paper_1808_00687_amd import wfstdec
+    want = oracle_mod.validate_graph(g)
+    assert (want == 0) == name.endswith("ok")
+    try:
+        h = wfstdec.load_graph(g)
+        got = 0
+        h.free()
+    except wfstdec.WfstError as e:
+        got = e.code
+    if want == 0:
+        # valid: loads on a GPU, or reaches the device step without one
+        assert got in (0, wfstdec.WFST_EDEVICE)
+    else:
+        assert got == wfstdec.WFST_EINVAL

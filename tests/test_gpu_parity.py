@@ -1,0 +1,270 @@
+"""GPU decoder (HIP, through the C ABI) against the CPU oracle.
+
+Every case compares token sets (states, float32 cost bits, back-pointers),
+best path, cost, counters and lattice (arcs, prefix costs, extra costs)
+exactly.  Sizes span many 64-token wave chunks and ragged tails; the
+workloads include the medium and LVCSR-scale graphs decoded in the same
+launch configuration as the benchmark.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from paper_1808_00687_amd import workloads as W
+import parity
+
+pytestmark = pytest.mark.gpu
+
+INF = float("inf")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dec():
+    import torch
+    assert torch.cuda.is_available(), "no GPU"
+    from paper_1808_00687_amd import wfstdec
+    return wfstdec
+
+
+@pytest.fixture(scope="module")
+def torch_mod():
+    import torch
+    return torch
+
+
+def to_dev(torch_mod, ll):
+    return torch_mod.from_numpy(np.ascontiguousarray(ll)).to("cuda:0")
+
+
+def both(dec, torch_mod, oracle_mod, g, ll, gh=None, tokens=True, **o):
+    ro = oracle_mod.decode(g, ll, o.get("beam", INF), o.get("max_active", 0), o.get("lattice_beam", -1.0),
+                           o.get("blank_threshold", 2.0), o.get("blank_id", 0))
+    own = gh is None
+    if own:
+        gh = dec.load_graph(g)
+    rg = dec.wfst_decode(gh, to_dev(torch_mod, ll), beam=o.get("beam", INF), max_active=o.get("max_active", 0),
+                         lattice_beam=o.get("lattice_beam", -1.0),
+                         blank_threshold=o.get("blank_threshold", 2.0), blank_id=o.get("blank_id", 0),
+                         record_tokens=tokens)
+    if own:
+        gh.free()
+    return ro, rg
+
+
+SMALL = []
+for seed in range(60):
+    kind = ["exp", "int", "dyadic"][seed % 3]
+    SMALL.append((seed, kind))
+
+
+@pytest.mark.parametrize("seed,kind", SMALL)
+def test_small_random_graphs(dec, torch_mod, oracle_mod, seed, kind):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(5, 400))
+    g = W.random_small_graph(700 + seed, n, mean_deg=float(rng.uniform(1.2, 4.0)),
+                             eps_frac=float(rng.uniform(0.0, 0.4)), num_labels=5,
+                             weights=kind, final=bool(seed % 4 == 1))
+    T = int(rng.integers(0, 40))
+    ll = W.random_small_loglikes(700 + seed, T, 5, kind={"exp": "gauss", "int": "int", "dyadic": "dyadic"}[kind])
+    beam = [INF, 3.0, 6.5, 12.0][seed % 4]
+    max_active = [0, 0, 5, 37, 120][seed % 5]
+    lb = [-1.0, 0.0, 2.5, INF][seed % 4]
+    ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=beam, max_active=max_active, lattice_beam=lb)
+    parity.assert_same(ro, rg, lattice=lb >= 0, tag="seed %d" % seed)
+
+
+def test_config1_full(dec, torch_mod, oracle_mod):
+    wl = W.workload(1)
+    o = wl.opts
+    for lb in (-1.0, 8.0):
+        ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0], beam=o.beam,
+                      max_active=o.max_active, lattice_beam=lb)
+        parity.assert_same(ro, rg, lattice=lb >= 0, tag="config 1 lb %g" % lb)
+        say("config 1: cost", rg.cost, "tokens", rg.stats["tokens"], "lattice", rg.stats["lattice_kept"])
+
+
+@pytest.fixture(scope="module")
+def cfg2(dec):
+    wl = W.workload(2)
+    return wl, dec.load_graph(wl.graph)
+
+
+def test_config2_full(dec, torch_mod, oracle_mod, cfg2):
+    wl, gh = cfg2
+    o = wl.opts
+    ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0], gh=gh, beam=o.beam,
+                  max_active=o.max_active, lattice_beam=o.lattice_beam)
+    parity.assert_same(ro, rg, lattice=True, tag="config 2")
+    parity.assert_path_consistent(wl.graph, rg, wl.loglikes[0])
+    say("config 2: cost", rg.cost, "arcs", rg.stats["arcs_expanded"], "lattice raw", rg.stats["lattice_raw"],
+        "kept", rg.stats["lattice_kept"])
+
+
+def test_config2_raw_lattice_and_infinite_beam_prefix(dec, torch_mod, oracle_mod, cfg2):
+    wl, gh = cfg2
+    ll = wl.loglikes[0][:30]
+    ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, ll, gh=gh, beam=13.0, max_active=7000,
+                  lattice_beam=INF)
+    parity.assert_same(ro, rg, lattice=True, tag="config 2 raw lattice")
+    ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, ll[:6], gh=gh, beam=INF, max_active=0,
+                  lattice_beam=4.0, tokens=True)
+    parity.assert_same(ro, rg, lattice=True, tag="config 2 infinite beam")
+
+
+def test_epsilon_queue_overflow_path(dec, torch_mod, oracle_mod, cfg2):
+    # a 2-item per-wave epsilon queue sends most epsilon work through the
+    # overflow list and the last-block closure
+    wl, gh = cfg2
+    os.environ["WFSTDEC_TEST_QUEUE_CAP"] = "2"
+    try:
+        ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:80], gh=gh, beam=13.0,
+                      max_active=7000, lattice_beam=8.0)
+    finally:
+        del os.environ["WFSTDEC_TEST_QUEUE_CAP"]
+    parity.assert_same(ro, rg, lattice=True, tag="overflow queue")
+
+
+def test_determinism(dec, torch_mod, cfg2):
+    wl, gh = cfg2
+    o = wl.opts
+    x = to_dev(torch_mod, wl.loglikes[0][:120])
+    a = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    b = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    for f in ("tok_off", "tok_state", "tok_arc", "path_arcs", "lat_arc", "lat_frame"):
+        np.testing.assert_array_equal(getattr(a, f), getattr(b, f))
+    np.testing.assert_array_equal(parity.bits(a.tok_cost), parity.bits(b.tok_cost))
+    np.testing.assert_array_equal(parity.bits(a.lat_extra), parity.bits(b.lat_extra))
+
+
+def test_batch_matches_single_and_oracle(dec, torch_mod, oracle_mod):
+    g = W.random_small_graph(901, 3000, mean_deg=3.0, eps_frac=0.2, num_labels=20)
+    gh = dec.load_graph(g)
+    lls = [W.random_small_loglikes(910 + u, T, 20) for u, T in enumerate([0, 1, 17, 64, 65, 130, 3])]
+    res = dec.wfst_decode_batch(gh, [to_dev(torch_mod, x) for x in lls], beam=9.0, max_active=150,
+                                lattice_beam=5.0, record_tokens=True)
+    for u, (x, r) in enumerate(zip(lls, res)):
+        ro = oracle_mod.decode(g, x, 9.0, 150, 5.0)
+        parity.assert_same(ro, r, lattice=True, tag="batch utt %d" % u)
+    gh.free()
+
+
+def test_lsd_small_ctc(dec, torch_mod, oracle_mod):
+    g = W.random_small_graph(950, 5000, mean_deg=2.0, eps_frac=0.1, num_labels=30)
+    n = g.num_states
+    src = np.concatenate([np.arange(n), g.src]).astype(np.int32)
+    dst = np.concatenate([np.arange(n), g.dst]).astype(np.int32)
+    il = np.concatenate([np.ones(n), np.where(g.ilabel == 0, 0, np.maximum(g.ilabel, 2))]).astype(np.int32)
+    w = np.concatenate([np.full(n, 0.3), g.weight]).astype(np.float32)
+    o = np.argsort(src, kind="stable")
+    g2 = W.Graph(n, src[o], dst[o], il[o], np.zeros_like(src), w[o])
+    ll = W.random_small_loglikes(951, 300, 30, blank_boost=7.0)
+    for thr in (0.5, 0.95, 2.0):
+        ro, rg = both(dec, torch_mod, oracle_mod, g2, ll, beam=10.0, max_active=400, lattice_beam=6.0,
+                      blank_threshold=thr, blank_id=0)
+        parity.assert_same(ro, rg, lattice=True, tag="lsd thr %g" % thr)
+
+
+def test_edge_cases(dec, torch_mod, oracle_mod):
+    def gr(n, arcs, final=None):
+        a = np.array(arcs, np.float64).reshape(-1, 5)
+        return W.Graph(n, a[:, 0].astype(np.int32), a[:, 1].astype(np.int32), a[:, 2].astype(np.int32),
+                       a[:, 3].astype(np.int32), a[:, 4].astype(np.float32), 0,
+                       None if final is None else np.asarray(final, np.float32))
+    # dead end -> ENOPATH
+    ro, rg = both(dec, torch_mod, oracle_mod, gr(2, [[0, 1, 1, 0, 0.0]]), np.zeros((2, 1), np.float32), beam=5.0)
+    assert ro.status == rg.status == -3
+    # T = 0: the closure of the start state
+    g = gr(3, [[0, 1, 0, 0, 0.5], [0, 0, 1, 0, 0.0], [1, 2, 0, 0, 1.0]])
+    ro, rg = both(dec, torch_mod, oracle_mod, g, np.zeros((0, 1), np.float32), beam=5.0, lattice_beam=INF)
+    parity.assert_same(ro, rg, lattice=True, tag="T=0")
+    # all frames blank
+    ll = np.log(np.array([[0.99, 0.01]] * 7, np.float32))
+    ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=5.0, blank_threshold=0.9)
+    parity.assert_same(ro, rg, lattice=False, tag="all blank")
+    # final weights with no final state reached (fallback)
+    g = gr(2, [[0, 1, 1, 0, 0.5]], final=[0.0, INF])
+    ro, rg = both(dec, torch_mod, oracle_mod, g, np.array([[-0.25]], np.float32), beam=INF, lattice_beam=3.0)
+    parity.assert_same(ro, rg, lattice=True, tag="final fallback")
+    assert rg.reached_final == 0
+
+
+def test_argument_errors(dec, torch_mod):
+    g = W.Graph(2, np.array([0], np.int32), np.array([1], np.int32), np.array([3], np.int32),
+                np.array([0], np.int32), np.array([1.0], np.float32))
+    gh = dec.load_graph(g)
+    x = to_dev(torch_mod, np.zeros((1, 3), np.float32))
+    assert dec.wfst_decode(gh, x, 1.0).status == 0
+    for kw in (dict(beam=0.0), dict(beam=float("nan")), dict(beam=1.0, blank_id=3),
+               dict(beam=1.0, blank_threshold=0.0), dict(beam=1.0, lattice_beam=float("nan"))):
+        with pytest.raises(dec.WfstError) as e:
+            dec.wfst_decode(gh, x, **kw)
+        assert e.value.code == dec.WFST_EINVAL
+    with pytest.raises(dec.WfstError) as e:
+        dec.wfst_decode(gh, to_dev(torch_mod, np.zeros((1, 2), np.float32)), 1.0)
+    assert e.value.code == dec.WFST_EINVAL
+    gh.free()
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def cfg3(dec):
+    say("generating the 25M-arc graph ...")
+    g = W.graph_for(3)
+    say("uploading")
+    return g, dec.load_graph(g)
+
+
+def test_config3_full(dec, torch_mod, oracle_mod, cfg3):
+    g, gh = cfg3
+    wl = W.workload(3)
+    o = wl.opts
+    say("oracle on config 3 ...")
+    ro, rg = both(dec, torch_mod, oracle_mod, g, wl.loglikes[0], gh=gh, beam=o.beam,
+                  max_active=o.max_active, lattice_beam=o.lattice_beam)
+    say("oracle %.1fs; comparing" % ro.seconds)
+    parity.assert_same(ro, rg, lattice=True, tag="config 3")
+    parity.assert_path_consistent(g, rg, wl.loglikes[0])
+
+
+def test_config4_batch_sampled(dec, torch_mod, oracle_mod, cfg3):
+    # the benchmark's batch (64 utterances on the 25M-arc graph); the oracle
+    # checks two utterances in full, every utterance is checked for a
+    # consistent best path
+    g, gh = cfg3
+    wl = W.workload(4)
+    o = wl.opts
+    xs = [to_dev(torch_mod, x) for x in wl.loglikes]
+    say("batch decode of %d utterances" % len(xs))
+    res = dec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, record_tokens=False)
+    for u, r in enumerate(res):
+        assert r.status == 0
+        parity.assert_path_consistent(g, r, wl.loglikes[u])
+        assert r.lat_arc.size >= r.path_arcs.size
+    for u in (int(np.argmin([x.shape[0] for x in wl.loglikes])), 17):
+        say("oracle on utterance", u)
+        ro = oracle_mod.decode(g, wl.loglikes[u], o.beam, o.max_active, o.lattice_beam)
+        parity.assert_same(ro, res[u], lattice=True, tokens=False, tag="config 4 utt %d" % u)
+
+
+def test_config5_lsd_and_fsd(dec, torch_mod, oracle_mod):
+    wl = W.workload(5, lsd=True)
+    g = wl.graph
+    gh = dec.load_graph(g)
+    o = wl.opts
+    for thr in (0.95, 2.0):
+        say("config 5 threshold", thr)
+        ro, rg = both(dec, torch_mod, oracle_mod, g, wl.loglikes[0], gh=gh, beam=o.beam,
+                      max_active=o.max_active, lattice_beam=o.lattice_beam, blank_threshold=thr, blank_id=0)
+        parity.assert_same(ro, rg, lattice=True, tag="config 5 thr %g" % thr)
+        say("decoded", rg.num_decoded, "of", rg.num_frames, "arcs", rg.stats["arcs_expanded"])
+    gh.free()
