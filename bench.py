@@ -1,0 +1,250 @@
+#!/usr/bin/env python3
+"""Benchmark of WFST Viterbi beam decoding with lattice generation on one
+MI355X: decoded frames/s (with RTF, arcs expanded/s and the HBM roofline of
+the arc-expansion kernel) on the 25M-arc LVCSR-scale graph, 64 utterances of
+300-1,500 frames decoded in one batched call.
+
+One step = one wfst_decode_batch call over the whole batch: label-synchronous
+classification, every decoded frame (expansion + epsilon closure, pruning,
+lattice recording), final costs, backtrace, lattice-beam pruning and the
+sorted lattice.  Log-likelihoods are resident in device memory before the
+timed region; graph generation and upload are outside it.
+
+Prints one JSON line.  --gpus N with N > 1 is rejected: the decoder runs on
+one GPU; batches of utterances would shard across GPUs with no per-frame
+communication, which this build does not do.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decoded frames/sec (RTF) + arcs expanded/sec + % HBM peak, 25M-arc graph"
+HBM_PEAK_GBS = 8000.0
+FRAME_SHIFT_S = 0.010
+COUNTERS = os.path.join(ROOT, "profiles", "expand_kernel_lvcsr-25m-batch64_counters.txt")
+KERNEL_SRC = os.path.join(ROOT, "paper_1808_00687_amd", "csrc", "search_kernels.hip")
+
+WORKLOADS = {
+    "cfg1": (1, True), "cfg2": (2, True), "cfg3": (3, True), "cfg4": (4, True),
+    "cfg5": (5, True), "cfg5fsd": (5, False),
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def expand_bytes(stats_list):
+    """Algorithmic bytes moved by the expansion kernel over one decode: 16 B
+    per expanded token (state, cost, two row offsets), 24 B per emitting arc
+    (dst, ilabel, weight, loglike, 8-byte atomic), 16 B per epsilon arc of a
+    surviving token (dst, weight, 8-byte atomic)."""
+    tok = sum(s["tokens"] - s["tokens_last"] for s in stats_list)
+    arcs = sum(s["arcs_expanded"] for s in stats_list)
+    eps = sum(s["eps_arcs"] for s in stats_list)
+    return 16 * tok + 24 * arcs + 16 * eps
+
+
+def read_traffic(expected_launches):
+    """HBM bytes per expansion launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source."""
+    if not os.path.exists(COUNTERS):
+        return None
+    kv = {}
+    for line in open(COUNTERS):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    if kv.get("kernel_source_sha256") != sha:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, max_seconds: float):
+    """The oracle as it stands, on host cores, over a bounded sample of the
+    same workload (whole utterances, one per thread)."""
+    import oracle
+    oracle.build()
+    cores = len(os.sched_getaffinity(0))
+    cores = max(1, min(cores, 16))
+    o = wl.opts
+    g = wl.graph
+    n_utt = len(wl.loglikes)
+    sample = list(range(min(n_utt, cores)))
+    if n_utt == 1:
+        sample = [0]
+    t0 = time.time()
+    with ThreadPoolExecutor(max_workers=cores) as ex:
+        res = list(ex.map(lambda u: oracle.decode(g, wl.loglikes[u], o.beam, o.max_active, o.lattice_beam,
+                                                  o.blank_threshold, o.blank_id), sample))
+    wall = time.time() - t0
+    frames = sum(r.num_decoded for r in res)
+    busy = sum(r.seconds for r in res)
+    threads = min(cores, len(sample))
+    rate = frames / (busy / threads) if busy > 0 else None
+    return {
+        "value": rate,
+        "unit": "frames/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "%d whole utterance(s) (%d decoded frames) of the same workload, one oracle call per "
+                  "thread; rate = frames / (summed decode time / threads); wall %.1fs" % (
+                      len(sample), frames, wall),
+    }
+
+
+def copy_calibration(torch, mib: int):
+    """A plain device copy of known size, for scaling HBM counters."""
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    log("copy calibration: 3 copies of %d MiB" % mib)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="cfg4", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=30.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0)
+    ap.add_argument("--no-profile", action="store_true",
+                    help="do not time kernel phases with HIP events")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this decoder runs on one GPU; --gpus %d is not supported (utterance batches "
+              "would shard across GPUs with no per-frame traffic, which this build does not do)"
+              % max(args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_1808_00687_amd import wfstdec, workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU", file=sys.stderr)
+        sys.exit(1)
+    cfg, lsd = WORKLOADS[args.workload]
+    t = time.time()
+    wl = workloads.workload(cfg, lsd=lsd)
+    log("workload %s generated in %.1fs (%d states, %d arcs, %d utterances)" % (
+        wl.name, time.time() - t, wl.graph.num_states, wl.graph.num_arcs, len(wl.loglikes)))
+    if args.copy_calibration_mib:
+        copy_calibration(torch, args.copy_calibration_mib)
+    t = time.time()
+    gh = wfstdec.load_graph(wl.graph)
+    torch.cuda.synchronize()
+    load_s = time.time() - t
+    xs = [torch.from_numpy(x).to("cuda:0") for x in wl.loglikes]
+    torch.cuda.synchronize()
+    o = wl.opts
+    stream = torch.cuda.current_stream()
+
+    def step(profile):
+        return wfstdec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, o.blank_threshold,
+                                         o.blank_id, profile=profile, stream=stream)
+
+    for i in range(args.warmup):
+        res = step(False)
+        log("warmup %d done" % i)
+    torch.cuda.synchronize()
+    profile = not args.no_profile
+    t0 = time.perf_counter()
+    all_res = []
+    for i in range(args.steps):
+        all_res.append(step(profile))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / max(args.steps, 1)
+    res = all_res[-1]
+    bad = [r.status for r in res if r.status != 0]
+    if bad:
+        log("warning: %d utterances without a path" % len(bad))
+    stats = [r.stats for r in res]
+    frames_dec = sum(s["frames_decoded"] for s in stats)
+    frames = sum(s["frames"] for s in stats)
+    arcs = sum(s["arcs_expanded"] for s in stats)
+    sec = ms_per_step / 1e3
+    out = {
+        "metric": METRIC,
+        "value": frames_dec / sec,
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "graph_states": wl.graph.num_states,
+            "graph_arcs": wl.graph.num_arcs,
+            "utterances": len(wl.loglikes),
+            "frames": frames,
+            "decoded_frames": frames_dec,
+            "labels": wl.num_labels,
+            "beam": o.beam,
+            "max_active": o.max_active,
+            "lattice_beam": o.lattice_beam,
+            "blank_threshold": o.blank_threshold,
+            "parallelism": "utterance batch of %d on 1 GPU" % len(wl.loglikes),
+        },
+        "rtf": sec / (frames * FRAME_SHIFT_S),
+        "original_frames_per_s": frames / sec,
+        "arcs_expanded_per_s": arcs / sec,
+        "tokens_per_decoded_frame": sum(s["tokens"] for s in stats) / max(frames_dec, 1),
+        "lattice_arcs_kept": sum(s["lattice_kept"] for s in stats),
+        "graph_load_s": load_s,
+    }
+    if profile:
+        s0 = stats[0]
+        launches = s0["expand_launches"]
+        exp_ms = s0["expand_ms"]
+        alg = expand_bytes(stats)
+        per_launch = alg / max(launches, 1)
+        dur_s = exp_ms / 1e3 / max(launches, 1)
+        achieved = per_launch / dur_s / 1e9 if dur_s > 0 else None
+        traffic = read_traffic(launches)
+        out["roofline"] = {
+            "kernel": "expand_kernel",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS if achieved else None,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": per_launch,
+            "avg_launch_us": dur_s * 1e6,
+            "launches": launches,
+        }
+        out["kernel_ms"] = {"expand": exp_ms, "prune": s0["prune_ms"], "record": s0["record_ms"],
+                            "final": s0["final_ms"]}
+    if not args.no_cpu_baseline:
+        log("oracle baseline ...")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

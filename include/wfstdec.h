@@ -200,6 +200,7 @@ typedef struct wfst_stats {
     int32_t frames;            /* T */
     int32_t frames_decoded;    /* T' = T - |U| */
     int64_t tokens;            /* sum over token sets of |S_j| */
+    int64_t tokens_last;       /* |S_T'|, the set the final costs are added to */
     int64_t arcs_expanded;     /* emitting out-arcs of the expanded token sets */
     int64_t eps_arcs;          /* epsilon out-arcs of all surviving tokens */
     int64_t lattice_raw;       /* lattice arcs recorded before lattice-beam pruning */

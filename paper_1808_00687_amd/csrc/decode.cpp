@@ -9,6 +9,8 @@
 #include <algorithm>
 #include <chrono>
 #include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
 #include <memory>
@@ -33,10 +35,10 @@ struct DevBuf {
     {
         if (!p) return;
         int cur = 0;
-        hipGetDevice(&cur);
-        if (cur != device) hipSetDevice(device);
-        hipFree(p);
-        if (cur != device) hipSetDevice(cur);
+        (void)hipGetDevice(&cur);
+        if (cur != device) (void)hipSetDevice(device);
+        (void)hipFree(p);
+        if (cur != device) (void)hipSetDevice(cur);
     }
 };
 
@@ -79,13 +81,13 @@ struct DeviceGuard {
     int prev = -1;
     explicit DeviceGuard(int dev)
     {
-        hipGetDevice(&prev);
-        if (prev != dev) hipSetDevice(dev);
+        (void)hipGetDevice(&prev);
+        if (prev != dev) (void)hipSetDevice(dev);
         else prev = -1;
     }
     ~DeviceGuard()
     {
-        if (prev >= 0) hipSetDevice(prev);
+        if (prev >= 0) (void)hipSetDevice(prev);
     }
 };
 
@@ -108,7 +110,7 @@ struct Workspace {
     }
     ~Workspace()
     {
-        for (void *p : ptrs) hipFreeAsync(p, s);
+        for (void *p : ptrs) (void)hipFreeAsync(p, s);
     }
 };
 
@@ -120,7 +122,7 @@ void keep_pool_memory(int device)
         hipMemPool_t pool;
         if (hipDeviceGetDefaultMemPool(&pool, device) == hipSuccess) {
             uint64_t thr = std::numeric_limits<uint64_t>::max();
-            hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+            (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
         }
     });
 }
@@ -143,27 +145,115 @@ struct Sizes {
     int64_t lat_mult;  // lattice records per token
 };
 
-struct Timer {
-    bool on = false;
-    hipStream_t s = nullptr;
-    std::vector<hipEvent_t> ev;
-    std::vector<int> kind;   // phase ending at ev[i]
-    void mark(int k)
+// Events for phase timing, kept for reuse across calls: creating thousands
+// of events per decode would stall the launch loop.
+struct EventPool {
+    std::mutex mu;
+    std::vector<hipEvent_t> free_ev[64];
+    hipEvent_t get(int dev)
     {
-        if (!on) return;
-        hipEvent_t e;
-        if (hipEventCreate(&e) != hipSuccess) return;
-        hipEventRecord(e, s);
-        ev.push_back(e);
-        kind.push_back(k);
+        {
+            std::lock_guard<std::mutex> lk(mu);
+            if (!free_ev[dev].empty()) {
+                hipEvent_t e = free_ev[dev].back();
+                free_ev[dev].pop_back();
+                return e;
+            }
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
     }
-    ~Timer()
+    void put(int dev, hipEvent_t e)
     {
-        for (auto e : ev) hipEventDestroy(e);
+        std::lock_guard<std::mutex> lk(mu);
+        free_ev[dev].push_back(e);
     }
 };
 
-enum { PH_NONE = -1, PH_EXPAND = 0, PH_PRUNE = 1, PH_RECORD = 2, PH_FINAL = 3, PH_OTHER = 4 };
+EventPool &event_pool()
+{
+    static EventPool *pool = new EventPool();
+    return *pool;
+}
+
+// Phase timing with HIP events (WFST_PROFILE): a start/stop pair per phase
+// launch, recorded on the stream the phase runs on.
+struct Timer {
+    bool on = false;
+    int dev = 0;
+    struct Span {
+        hipEvent_t a, b;
+        int kind;
+    };
+    std::vector<Span> spans;
+    hipEvent_t open_ev = nullptr;
+    void start(hipStream_t s)
+    {
+        if (!on) return;
+        open_ev = event_pool().get(dev);
+        if (open_ev) (void)hipEventRecord(open_ev, s);
+    }
+    void stop(int kind, hipStream_t s)
+    {
+        if (!on || !open_ev) return;
+        hipEvent_t e = event_pool().get(dev);
+        if (!e) return;
+        (void)hipEventRecord(e, s);
+        spans.push_back({open_ev, e, kind});
+        open_ev = nullptr;
+    }
+    ~Timer()
+    {
+        for (auto &x : spans) {
+            event_pool().put(dev, x.a);
+            event_pool().put(dev, x.b);
+        }
+        if (open_ev) event_pool().put(dev, open_ev);
+    }
+};
+
+// Events ordering the two streams of the frame loop.
+struct EventRing {
+    std::vector<hipEvent_t> ev;
+    explicit EventRing(int n) : ev(n, nullptr)
+    {
+        for (auto &e : ev) (void)hipEventCreateWithFlags(&e, hipEventDisableTiming);
+    }
+    hipEvent_t operator[](int i) const { return ev[i % ev.size()]; }
+    ~EventRing()
+    {
+        for (auto e : ev)
+            if (e) (void)hipEventDestroy(e);
+    }
+};
+
+struct StreamHolder {
+    hipStream_t s = nullptr;
+    ~StreamHolder()
+    {
+        if (s) (void)hipStreamDestroy(s);
+    }
+};
+
+// Wall-clock breakdown of one decode call on stderr (WFSTDEC_DEBUG_TIMING=1).
+struct WallTrace {
+    bool on = getenv("WFSTDEC_DEBUG_TIMING") != nullptr;
+    double t = now();
+    static double now()
+    {
+        return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now().time_since_epoch()).count();
+    }
+    void mark(const char *what)
+    {
+        if (!on) return;
+        double x = now();
+        fprintf(stderr, "[wfstdec] %-22s %9.3f ms\n", what, x - t);
+        t = x;
+    }
+};
+
+enum { PH_EXPAND = 0, PH_PRUNE = 1, PH_RECORD = 2, PH_FINAL = 3, PH_COUNT = 4 };
 
 // One attempt at decoding the batch with the given buffer sizes.  Returns
 // WFST_OK, an error, or WFST_ECAPACITY when a buffer overflowed.
@@ -176,8 +266,8 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     const int depth = G.eps_depth;
     Workspace ws(s);
     Timer tm;
-    tm.on = (o.flags & WFST_PROFILE) != 0;
-    tm.s = s;
+    tm.on = (o.flags & WFST_PROFILE) != 0 && G.device >= 0 && G.device < 64;
+    tm.dev = G.device;
 
     std::vector<UttLayout> lay(U);
     int64_t sv = 0, le = 0, lx = 0, fo = 0, kp = 0, pa = 0;
@@ -216,31 +306,32 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.qcap = test_queue_cap();
     p.capT = z.capT;
     p.capO = z.capO;
+    WallTrace wt;
     p.st = ws.get<UttState>(U);
     UttLayout *d_lay = ws.get<UttLayout>(U);
     p.lay = d_lay;
-    int32_t *ctl = ws.get<int32_t>(2);
-    p.cur = ctl;
-    p.done = reinterpret_cast<uint32_t *>(ctl + 1);
     p.tok = ws.get<uint64_t>(U * N);
-    p.pos = ws.get<int32_t>(U * 2 * N);
+    p.pos = ws.get<int32_t>(U * 3 * N);
     p.touched = ws.get<int32_t>(U * z.capT);
     p.pk = ws.get<uint64_t>(U * z.capT);
     p.ovf = ws.get<uint64_t>(U * z.capO);
-    p.hist = ws.get<uint32_t>(static_cast<int64_t>(U) * kHistBins);
     p.sv_state = ws.get<int32_t>(sv);
     p.sv_tok = ws.get<uint64_t>(sv);
     p.sv_prev = ws.get<int32_t>(sv);
+    p.sv_ebeg = ws.get<int32_t>(sv);
+    p.sv_epre = ws.get<int32_t>(sv);
     p.e_key = lattice ? ws.get<uint32_t>(sv) : nullptr;
     p.lat_e = lattice ? ws.get<int4>(le) : nullptr;
     p.lat_x = lattice ? ws.get<int4>(lx) : nullptr;
     p.ex_e = lattice ? ws.get<float>(le) : nullptr;
     p.ex_x = lattice ? ws.get<float>(lx) : nullptr;
     int64_t *fo_all = ws.get<int64_t>(4 * fo);
+    p.cut_arr = ws.get<uint32_t>(fo);
     p.kept = ws.get<int32_t>(kp);
     p.path_arc = ws.get<int32_t>(pa);
     p.path_frame = ws.get<int32_t>(pa);
     if (ws.err != hipSuccess) return hip_fail(ws.err, "decode: workspace allocation");
+    wt.mark("allocate");
     p.sv_off = fo_all;
     p.le_off = fo_all + fo;
     p.lx_off = fo_all + 2 * fo;
@@ -252,6 +343,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         st[u].ll = ll[u];
         st[u].T = T[u];
         st[u].best = kEmptyKey;
+        st[u].hint = kEmptyKey;
     }
     hipError_t e = hipSuccess;
     auto chk = [&](hipError_t r) {
@@ -259,9 +351,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     };
     chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
-    chk(hipMemsetAsync(ctl, 0, 2 * sizeof(int32_t), s));
     chk(hipMemsetAsync(fo_all, 0, 4 * fo * sizeof(int64_t), s));
-    chk(hipMemsetAsync(p.hist, 0, static_cast<size_t>(U) * kHistBins * 4, s));
     chk(launch_fill_u64(p.tok, U * N, kEmptyTok, s));
     chk(launch_classify(p, s));
     chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
@@ -269,30 +359,46 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     if (e != hipSuccess) return hip_fail(e, "decode: setup");
     int Tmax = 0;
     for (int u = 0; u < U; u++) Tmax = std::max(Tmax, st[u].Tp);
+    wt.mark("setup+classify");
 
-    // grid sizes: one wave per 64 expected tokens (or reached states)
+    // grid size: one wave per 64 expected tokens
     const int64_t est = o.max_active > 0 ? std::min<int64_t>(o.max_active, N) : std::min<int64_t>(N, z.capF);
     auto clampg = [](int64_t g) { return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(g, 8192))); };
-    const int gE = clampg((U * est + 255) / 256);
-    const int gP = clampg((U * std::min<int64_t>(4 * est, z.capT) + 255) / 256);
+    const int gE = std::min(clampg((U * est + 255) / 256), 1024);
 
+    // Frame loop.  Main stream: expand(k) -> prune(k).  Second stream:
+    // record(k) once prune(k) is done, overlapping expand(k+1)/prune(k+1).
+    // prune(k) overwrites the state->survivor map slot k mod 3 that
+    // record(k-3) and record(k-2) read, so it waits for record(k-2).
+    StreamHolder aux;
+    chk(hipStreamCreateWithFlags(&aux.s, hipStreamNonBlocking));
+    hipStream_t s2 = aux.s;
+    EventRing pruned(4), recorded(4);
     for (int k = 0; k <= Tmax && e == hipSuccess; k++) {
-        tm.mark(PH_OTHER);
-        chk(k == 0 ? launch_init(p, s) : launch_expand(p, gE, s));
-        tm.mark(PH_EXPAND);
-        chk(launch_prune_gather(p, gP, s));
-        chk(launch_prune_select(p, s));
-        chk(launch_prune_compact(p, gP, s));
-        tm.mark(PH_PRUNE);
-        chk(launch_record(p, gE, s));
-        chk(launch_advance(p, s));
-        tm.mark(PH_RECORD);
+        tm.start(s);
+        chk(launch_expand(p, k, gE, s));
+        tm.stop(PH_EXPAND, s);
+        if (k >= 2) chk(hipStreamWaitEvent(s, recorded[k - 2], 0));
+        tm.start(s);
+        chk(launch_prune(p, k, s));
+        tm.stop(PH_PRUNE, s);
+        chk(hipEventRecord(pruned[k], s));
+        chk(hipStreamWaitEvent(s2, pruned[k], 0));
+        tm.start(s2);
+        chk(launch_record(p, k, gE, s2));
+        tm.stop(PH_RECORD, s2);
+        chk(hipEventRecord(recorded[k], s2));
     }
+    chk(hipStreamWaitEvent(s, recorded[Tmax], 0));
+    tm.start(s);
     chk(launch_final(p, s));
     chk(launch_backtrace(p, s));
     if (lattice) chk(launch_lattice_backward(p, s));
+    tm.stop(PH_FINAL, s);
+    wt.mark("enqueue frames");
     chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
     chk(hipStreamSynchronize(s));
+    wt.mark("wait search");
     if (e != hipSuccess) return hip_fail(e, "decode: search");
     for (int u = 0; u < U; u++)
         if (st[u].status == WFST_ECAPACITY) return WFST_ECAPACITY;
@@ -305,14 +411,16 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
             if (st[u].status == WFST_OK) tot += st[u].lat_kept;
         }
         lat_buf = std::make_shared<DevBuf>();
-        hipGetDevice(&lat_buf->device);
+        (void)hipGetDevice(&lat_buf->device);
         chk(hipMalloc(&lat_buf->p, static_cast<size_t>(std::max<int64_t>(tot, 1)) * sizeof(int4)));
         p.lat_out = static_cast<int4 *>(lat_buf->p);
         chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
+        tm.start(s);
         chk(launch_lattice_emit(p, Tmax, s));
+        tm.stop(PH_FINAL, s);
     }
-    tm.mark(PH_FINAL);
 
+    wt.mark("lattice output");
     // gather results
     std::vector<int64_t> fo_h(static_cast<size_t>(fo));
     std::vector<int32_t> kept_h(static_cast<size_t>(kp));
@@ -338,6 +446,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
             chk(hipMemcpyAsync(r->path_frames.data(), p.path_frame + end - x.path_len, x.path_len * 4, hipMemcpyDeviceToHost, s));
         }
         r->stats.tokens = x.tokens;
+        r->stats.tokens_last = x.n_cur;
         r->stats.arcs_expanded = x.arcs_expanded;
         r->stats.eps_arcs = x.eps_arcs;
         r->stats.lattice_raw = x.le_cnt + x.lx_cnt;
@@ -362,16 +471,15 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         }
     }
     chk(hipStreamSynchronize(s));
+    wt.mark("copy results");
     if (e != hipSuccess) return hip_fail(e, "decode: results");
 
-    double ph[5] = {0, 0, 0, 0, 0};
+    double ph[PH_COUNT] = {0, 0, 0, 0};
     int nexp = 0;
-    for (size_t i = 1; i < tm.ev.size(); i++) {
+    for (const auto &x : tm.spans) {
         float ms = 0.0f;
-        if (hipEventElapsedTime(&ms, tm.ev[i - 1], tm.ev[i]) == hipSuccess && tm.kind[i] >= 0) {
-            ph[tm.kind[i]] += ms;
-            if (tm.kind[i] == PH_EXPAND) nexp++;
-        }
+        if (hipEventElapsedTime(&ms, x.a, x.b) == hipSuccess) ph[x.kind] += ms;
+        if (x.kind == PH_EXPAND) nexp++;
     }
     const double wall = std::chrono::duration<double, std::milli>(
                             std::chrono::steady_clock::now().time_since_epoch()).count() - t_start;
@@ -413,6 +521,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
             }
         }
     }
+    wt.mark("finish");
     return WFST_OK;
 }
 

@@ -117,9 +117,32 @@ __global__ __launch_bounds__(1024) void lattice_backward_kernel(Params p)
     const float B = st.final_cost;
     const bool use_final = p.g.final_w != nullptr && st.reached_final;
     uint32_t *e = p.e_key + ly.sv0;
-    const int64_t ntok = p.sv_off[ly.fo0 + Tp + 1];
+    const int64_t *so = p.sv_off + ly.fo0;
+    const int64_t ntok = so[Tp + 1];
     const uint32_t kinf = okey(__int_as_float(0x7F800000));
     for (int64_t i = threadIdx.x; i < ntok; i += blockDim.x) e[i] = kinf;
+    // Records were appended token set by token set, so the records of set j
+    // are those whose source survivor lies in S_j: locate each set's range by
+    // binary search on the source index.
+    const int64_t ne = st.le_cnt, nx = st.lx_cnt;
+    for (int j = threadIdx.x; j <= Tp + 1; j += blockDim.x) {
+        const int64_t lo_sv = so[j];
+        int64_t a = 0, b = ne;
+        while (a < b) {
+            int64_t mid = (a + b) >> 1;
+            if (p.lat_e[ly.le0 + mid].x < lo_sv) a = mid + 1;
+            else b = mid;
+        }
+        p.le_off[ly.fo0 + j] = a;
+        a = 0;
+        b = nx;
+        while (a < b) {
+            int64_t mid = (a + b) >> 1;
+            if (p.lat_x[ly.lx0 + mid].x < lo_sv) a = mid + 1;
+            else b = mid;
+        }
+        p.lx_off[ly.fo0 + j] = a;
+    }
     __syncthreads();
     {
         const int64_t a = p.sv_off[ly.fo0 + Tp], b = p.sv_off[ly.fo0 + Tp + 1];

@@ -182,7 +182,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     g.d.arc_src = static_cast<const int32_t *>(put(arc_src.data(), arc_src.size() * 4, b_src));
     g.d.final_w = final_weight ? static_cast<const float *>(put(final_weight, static_cast<size_t>(n) * 4, b_fin)) : nullptr;
     if (err != hipSuccess) {
-        hipFree(mem);
+        (void)hipFree(mem);
         delete h;
         set_error("wfst_load: hipMemcpy failed: %s", hipGetErrorString(err));
         return WFST_EDEVICE;
@@ -199,10 +199,10 @@ extern "C" void wfst_graph_free(wfst_graph *h)
 {
     if (!h) return;
     int cur = 0;
-    hipGetDevice(&cur);
-    if (cur != h->g.device) hipSetDevice(h->g.device);
-    hipFree(h->g.mem);
-    if (cur != h->g.device) hipSetDevice(cur);
+    (void)hipGetDevice(&cur);
+    if (cur != h->g.device) (void)hipSetDevice(h->g.device);
+    (void)hipFree(h->g.mem);
+    if (cur != h->g.device) (void)hipSetDevice(cur);
     delete h;
 }
 

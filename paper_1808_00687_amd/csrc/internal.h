@@ -63,13 +63,15 @@ struct UttState {
     // frame
     uint32_t best;        // minimum cost key among candidates of the set in production
     int32_t ntouched;     // states holding a token in the set in production
-    int32_t n_in_beam;    // of those, within the beam
+    int32_t pad3;
     uint32_t cut;         // pruning cutoff key of the set in production
     int32_t n_new;        // survivors appended for the set in production
     int32_t ovf;          // epsilon items spilled to the overflow list
     // previous set
     int32_t n_cur;        // |S_{k-1}|
-    int32_t best_sv;      // survivor index of a cheapest token of S_{k-1}
+    int32_t n_arcs;       // emitting out-arcs of S_{k-1} (the next expansion's work)
+    uint32_t hint;        // key of one candidate cost of the next expansion (early-drop seed)
+    int32_t pad2;
     // cumulative
     int64_t sv_base;      // survivor index where the set in production starts
     int64_t le_cnt;       // emitting lattice records so far
@@ -113,22 +115,21 @@ struct Params {
     int32_t pad;
     UttState *st;
     const UttLayout *lay;
-    int32_t *cur;             // index k of the token set in production
     // dense per-utterance tables, U x N
     uint64_t *tok;
-    int32_t *pos;             // U x 2 x N: survivor index of each state, by set parity
+    int32_t *pos;             // U x 3 x N: survivor index of each state of S_k, slot k mod 3
     // per-frame scratch, U x capT
     int32_t *touched;
     uint64_t *pk;
     int64_t capT;
     uint64_t *ovf;            // U x capO overflow epsilon items (state << 32 | cost bits)
     int64_t capO;
-    uint32_t *hist;           // U x kHistBins
-    uint32_t *done;           // last-block counter of the expansion kernel
     // survivors (per utterance regions)
     int32_t *sv_state;
     uint64_t *sv_tok;
     int32_t *sv_prev;
+    int32_t *sv_ebeg;         // first emitting arc record of the survivor's state
+    int32_t *sv_epre;         // exclusive prefix of emitting out-degree within the token set
     uint32_t *e_key;          // lattice backward extra cost per survivor (ordered key)
     // lattice raw records {src survivor, dst survivor, user arc, prefix cost bits}
     int4 *lat_e;
@@ -136,11 +137,12 @@ struct Params {
     float *ex_e;
     float *ex_x;
     int4 *lat_out;            // kept lattice {frame, arc, cost bits, extra bits}
-    // per-frame arrays (fo0 region): sv_off, le_off, lx_off, lat_cnt
+    // per-frame arrays (fo0 region): survivor, lattice-record and output offsets
     int64_t *sv_off;
     int64_t *le_off;
     int64_t *lx_off;
     int64_t *lo_off;
+    uint32_t *cut_arr;        // pruning cutoff key of each token set
     int32_t *kept;
     int32_t *path_arc;
     int32_t *path_frame;
@@ -150,19 +152,15 @@ struct Params {
 hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);
 hipError_t launch_classify(const Params &p, hipStream_t s);
-hipError_t launch_init(const Params &p, hipStream_t s);
-hipError_t launch_expand(const Params &p, int grid, hipStream_t s);
-hipError_t launch_prune_gather(const Params &p, int grid, hipStream_t s);
-hipError_t launch_prune_select(const Params &p, hipStream_t s);
-hipError_t launch_prune_compact(const Params &p, int grid, hipStream_t s);
-hipError_t launch_record(const Params &p, int grid, hipStream_t s);
-hipError_t launch_advance(const Params &p, hipStream_t s);
+hipError_t launch_expand(const Params &p, int k, int grid, hipStream_t s);
+hipError_t launch_prune(const Params &p, int k, hipStream_t s);
+hipError_t launch_record(const Params &p, int k, int grid, hipStream_t s);
 hipError_t launch_final(const Params &p, hipStream_t s);
 hipError_t launch_backtrace(const Params &p, hipStream_t s);
 hipError_t launch_lattice_backward(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
 
-// ---- host helpers (errors.cpp) ----
+// ---- host helpers (graph.cpp) ----
 void set_error(const char *fmt, ...);
 void clear_error();
 

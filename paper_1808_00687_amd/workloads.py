@@ -95,24 +95,34 @@ class Workload:
 # graph pieces
 # --------------------------------------------------------------------------
 
+def _rank_law_total(c: float, n: int, s: float, cap: int, r: np.ndarray) -> int:
+    """sum over ranks 1..n of clip(floor(c * r**-s), 1, cap), evaluating only
+    the ranks strictly between the capped head and the degree-1 tail."""
+    r_cap = int(np.floor((c / cap) ** (1.0 / s)))          # c r^-s >= cap for r <= r_cap
+    r_one = int(np.ceil(c ** (1.0 / s))) + 1               # c r^-s < 1 beyond this
+    lo = max(min(r_cap - 2, n), 0)
+    hi = max(min(r_one, n), lo)
+    mid = np.clip(np.floor(c * r[lo:hi] ** (-s)), 1, cap).sum()
+    return int(lo * cap + mid + (n - hi))
+
+
 def rank_law_degrees(n: int, total: int, s: float, cap: int,
                      rng: np.random.Generator) -> np.ndarray:
     """Out-degree per state from the rank law, permuted onto states."""
     r = np.arange(1, n + 1, dtype=np.float64)
-    rp = r ** (-s)
     lo, hi = 1.0, 1e13
-    for _ in range(200):
-        mid = 0.5 * (lo + hi)
-        if np.clip(np.floor(mid * rp), 1, cap).sum() <= total:
+    for _ in range(80):
+        mid = np.sqrt(lo * hi)
+        if _rank_law_total(mid, n, s, cap, r) <= total:
             lo = mid
         else:
             hi = mid
-    deg = np.clip(np.floor(lo * rp), 1, cap).astype(np.int64)
+    deg = np.clip(np.floor(lo * r ** (-s)), 1, cap).astype(np.int64)
     resid = total - int(deg.sum())
     assert resid >= 0
     if resid:
         ones = np.flatnonzero(deg == 1)
-        pick = rng.choice(ones, size=resid, replace=False)
+        pick = ones[rng.choice(ones.size, size=resid, replace=False)]
         deg[pick] += 1
     perm = rng.permutation(n)
     out = np.empty(n, dtype=np.int64)
@@ -124,20 +134,18 @@ def arcs_from_degrees(n: int, deg: np.ndarray, eps_frac: float, num_labels: int,
                       mean_w: float, rng: np.random.Generator,
                       first_label: int = 1) -> dict:
     """Arcs state by state; epsilon arcs only to higher-index states."""
-    src = np.repeat(np.arange(n, dtype=np.int64), deg)
+    src = np.repeat(np.arange(n, dtype=np.int32), deg)
     e = src.shape[0]
     is_eps = rng.random(e) < eps_frac
     is_eps &= src < n - 1
-    u = rng.random(e)
-    dst_emit = np.minimum((u * n).astype(np.int64), n - 1)
-    span = n - 1 - src
-    dst_eps = src + 1 + np.minimum((u * span).astype(np.int64), np.maximum(span - 1, 0))
-    dst = np.where(is_eps, dst_eps, dst_emit)
-    il = rng.integers(first_label, num_labels + 1, size=e, dtype=np.int64)
-    il = np.where(is_eps, 0, il)
+    eps = np.flatnonzero(is_eps)
+    del is_eps
+    dst = rng.integers(0, n, size=e, dtype=np.int32)
+    dst[eps] = rng.integers(src[eps] + 1, n, dtype=np.int32)
+    il = rng.integers(first_label, num_labels + 1, size=e, dtype=np.int32)
+    il[eps] = 0
     w = rng.exponential(mean_w, size=e).astype(np.float32)
-    return dict(src=src.astype(np.int32), dst=dst.astype(np.int32),
-                ilabel=il.astype(np.int32), weight=w)
+    return dict(src=src, dst=dst, ilabel=il, weight=w)
 
 
 def graph_cfg1() -> Graph:
