@@ -138,10 +138,20 @@ int test_queue_cap()
     return c;
 }
 
+int test_env_int(const char *name, int dflt)
+{
+    // test hooks: small values force the overflow paths of the search
+    const char *v = getenv(name);
+    if (!v) return dflt;
+    const int x = atoi(v);
+    return x >= 1 && x < dflt ? x : dflt;
+}
+
 struct Sizes {
     int64_t capF;      // tokens per frame
     int64_t capT;      // reached states per frame
-    int64_t capO;      // overflow epsilon items per frame
+    int64_t capO;      // overflow epsilon items per frame (per generation)
+    int64_t capC;      // emitting candidates per frame
     int64_t lat_mult;  // lattice records per token
 };
 
@@ -264,6 +274,9 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     const int64_t N = G.d.n;
     const bool lattice = o.lattice_beam >= 0.0f;
     const int depth = G.eps_depth;
+    // the per-frame kernels (expand / prune / record, one launch each per
+    // frame) instead of the whole-utterance kernel
+    const bool frame_kernels = getenv("WFSTDEC_FRAME_KERNELS") != nullptr;
     Workspace ws(s);
     Timer tm;
     tm.on = (o.flags & WFST_PROFILE) != 0 && G.device >= 0 && G.device < 64;
@@ -275,7 +288,8 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         UttLayout &l = lay[u];
         const int64_t Tu = T[u];
         l.sv0 = sv;
-        l.svcap = (Tu + 1) * z.capF;
+        // survivor indices are 32-bit
+        l.svcap = std::min<int64_t>((Tu + 1) * z.capF, std::numeric_limits<int32_t>::max());
         sv += l.svcap;
         l.le0 = le;
         l.lecap = lattice ? std::max<int64_t>(Tu, 1) * z.capF * z.lat_mult : 0;
@@ -304,17 +318,30 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.blank_id = o.blank_id;
     p.blank_thr = thr;
     p.qcap = test_queue_cap();
+    p.lds_fill = test_env_int("WFSTDEC_TEST_LDS_FILL", 1 << 30);
+    p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1024);
     p.capT = z.capT;
     p.capO = z.capO;
     WallTrace wt;
     p.st = ws.get<UttState>(U);
     UttLayout *d_lay = ws.get<UttLayout>(U);
     p.lay = d_lay;
-    p.tok = ws.get<uint64_t>(U * N);
-    p.pos = ws.get<int32_t>(U * 3 * N);
-    p.touched = ws.get<int32_t>(U * z.capT);
-    p.pk = ws.get<uint64_t>(U * z.capT);
-    p.ovf = ws.get<uint64_t>(U * z.capO);
+    if (frame_kernels) {
+        p.tok = ws.get<uint64_t>(U * N);
+        p.pos = ws.get<int32_t>(U * 3 * N);
+        p.touched = ws.get<int32_t>(U * z.capT);
+        p.pk = ws.get<uint64_t>(U * z.capT);
+        p.ovf = ws.get<uint64_t>(U * z.capO);
+    } else {
+        p.capG = 8192;
+        while (p.capG < z.capT) p.capG *= 2;
+        p.gkeys = ws.get<uint32_t>(U * p.capG);
+        p.gvals = ws.get<unsigned long long>(U * p.capG);
+        p.gslots = ws.get<int32_t>(U * p.capG);
+        p.gspill = ws.get<uint2>(U * 2 * z.capO);
+        p.capC = z.capC;
+        p.cand = ws.get<int4>(U * p.capC);
+    }
     p.sv_state = ws.get<int32_t>(sv);
     p.sv_tok = ws.get<uint64_t>(sv);
     p.sv_prev = ws.get<int32_t>(sv);
@@ -352,7 +379,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
     chk(hipMemsetAsync(fo_all, 0, 4 * fo * sizeof(int64_t), s));
-    chk(launch_fill_u64(p.tok, U * N, kEmptyTok, s));
+    if (frame_kernels) chk(launch_fill_u64(p.tok, U * N, kEmptyTok, s));
     chk(launch_classify(p, s));
     chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
     chk(hipStreamSynchronize(s));
@@ -371,9 +398,14 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     // prune(k) overwrites the state->survivor map slot k mod 3 that
     // record(k-3) and record(k-2) read, so it waits for record(k-2).
     StreamHolder aux;
+    EventRing pruned(frame_kernels ? 4 : 0), recorded(frame_kernels ? 4 : 0);
+    if (!frame_kernels) {
+        tm.start(s);
+        chk(launch_utt(p, s));
+        tm.stop(PH_EXPAND, s);
+    } else {
     chk(hipStreamCreateWithFlags(&aux.s, hipStreamNonBlocking));
     hipStream_t s2 = aux.s;
-    EventRing pruned(4), recorded(4);
     for (int k = 0; k <= Tmax && e == hipSuccess; k++) {
         tm.start(s);
         chk(launch_expand(p, k, gE, s));
@@ -390,6 +422,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         chk(hipEventRecord(recorded[k], s2));
     }
     chk(hipStreamWaitEvent(s, recorded[Tmax], 0));
+    }
     tm.start(s);
     chk(launch_final(p, s));
     chk(launch_backtrace(p, s));
@@ -399,6 +432,11 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
     chk(hipStreamSynchronize(s));
     wt.mark("wait search");
+    if (wt.on) {
+        int64_t gf = 0;
+        for (int u = 0; u < U; u++) gf += st[u].gframes;
+        fprintf(stderr, "[wfstdec] frames redone with the device-memory table: %lld\n", static_cast<long long>(gf));
+    }
     if (e != hipSuccess) return hip_fail(e, "decode: search");
     for (int u = 0; u < U; u++)
         if (st[u].status == WFST_ECAPACITY) return WFST_ECAPACITY;
@@ -585,7 +623,11 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
     else if (o.max_active > 0) z.capF = std::min<int64_t>(N, o.max_active + o.max_active / 4 + 256);
     else z.capF = std::min<int64_t>(N, 65536);
     z.capT = std::min<int64_t>(N, std::max<int64_t>(16 * z.capF, 4096));
-    z.capO = z.capT;
+    // a frame offers each emitting arc at most once; epsilon items of one
+    // generation are bounded by the candidates that produce them
+    const int64_t E = G.d.e;
+    z.capC = std::min<int64_t>(G.d.n_emit + 1, std::max<int64_t>(2 * z.capT, 65536));
+    z.capO = std::min<int64_t>(E + 1, std::max<int64_t>(2 * z.capT, 65536));
     z.lat_mult = 2;
     int rc = WFST_ECAPACITY;
     for (int attempt = 0; attempt < 6 && rc == WFST_ECAPACITY; attempt++) {
@@ -596,7 +638,8 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
             }
             z.capF = std::min<int64_t>(N, z.capF * 2);
             z.capT = std::min<int64_t>(N, z.capT * 2);
-            z.capO = z.capO * 2;
+            z.capO = std::min<int64_t>(E + 1, z.capO * 2);
+            z.capC = std::min<int64_t>(G.d.n_emit + 1, z.capC * 2);
             z.lat_mult *= 2;
         }
         rc = run_batch(G, n_utt, ll.data(), T, L, o, thr, s, z, res, t0);

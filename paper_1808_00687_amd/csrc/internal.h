@@ -59,7 +59,7 @@ struct UttState {
     int32_t T;
     int32_t Tp;           // decoded frames (set by the classify kernel)
     int32_t status;       // WFST_OK, WFST_ENOPATH or WFST_ECAPACITY
-    int32_t pad0;
+    int32_t gframes;      // frames whose token table overflowed LDS (redone in device memory)
     // frame
     uint32_t best;        // minimum cost key among candidates of the set in production
     int32_t ntouched;     // states holding a token in the set in production
@@ -146,6 +146,17 @@ struct Params {
     int32_t *kept;
     int32_t *path_arc;
     int32_t *path_frame;
+    // whole-utterance kernel: per-utterance token table in device memory
+    // (frames that overflow LDS), epsilon item spill lists, candidate lists
+    uint32_t *gkeys;          // U x capG
+    unsigned long long *gvals;
+    int32_t *gslots;
+    int64_t capG;             // power of two
+    uint2 *gspill;            // U x 2 x capO
+    int4 *cand;               // U x capC {src survivor, user arc, cost bits, table slot}
+    int64_t capC;
+    int32_t lds_fill;         // states per frame the LDS table takes (<= its fill limit)
+    int32_t gen_lds;          // epsilon items per generation kept in LDS (<= its capacity)
 };
 
 // ---- launchers (search_kernels.hip / final_kernels.hip) ----
@@ -159,6 +170,7 @@ hipError_t launch_final(const Params &p, hipStream_t s);
 hipError_t launch_backtrace(const Params &p, hipStream_t s);
 hipError_t launch_lattice_backward(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
+hipError_t launch_utt(const Params &p, hipStream_t s);
 
 // ---- host helpers (graph.cpp) ----
 void set_error(const char *fmt, ...);

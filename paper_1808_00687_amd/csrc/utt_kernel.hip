@@ -1,0 +1,762 @@
+// Whole-utterance search kernel: one 1024-thread workgroup per utterance
+// loops over every decoded frame of its utterance (token passing, Sec. 3;
+// the per-frame Viterbi beam search of Alg. 1, with the lattice records of
+// exact lattice generation, Sec. 1 and Sec. 3).
+//
+// Frame k (token set S_k) in one workgroup:
+//   1. expansion of the emitting arcs of S_{k-1}, 64 arcs per wave, found by a
+//      64-ary search over the set's emitting-arc prefix; the frame's tokens
+//      live in a hash table in LDS (state -> packed token), recombination is
+//      an LDS 64-bit atomicMin on (cost key, arc + 1), the first touch of a
+//      state appends its slot to a slot list;
+//   2. epsilon closure, generation by generation: every lowered token whose
+//      state has epsilon out-arcs is relaxed again until nothing changes;
+//   3. pruning: beam limit from the frame's best cost key and, when more
+//      tokens lie within it than max_active, the exact max_active-th
+//      smallest key by radix select over an LDS histogram;
+//   4. compaction of the survivors into S_k (device memory) in slot-list
+//      order, with the prefix of their emitting out-degrees;
+//   5. back-pointer survivor indices and lattice records;
+//   6. clearing of the table.
+// A frame that reaches more states than the LDS table holds is redone with
+// the same code on a table in device memory.  Every table is private to its
+// workgroup: no device-scope synchronisation and no per-frame launches.
+#include "device_util.h"
+
+namespace wfd {
+
+namespace {
+
+constexpr int kT = 1024;                  // threads per workgroup
+constexpr int kW = kT / kWave;            // waves per workgroup
+constexpr int kSlotBits = 13;
+constexpr int kSlots = 1 << kSlotBits;    // LDS hash slots
+constexpr int kFill = 6144;               // LDS states per frame before falling back to device memory
+constexpr int kGenCap = 1024;             // LDS epsilon items per generation
+constexpr int kRun = 2;                   // slot-list entries per thread per compaction pass
+constexpr int kOverflow = 1;              // frame result: the table filled up
+
+static_assert(kHistBins * 4 <= 2 * kGenCap * 8, "the select histogram aliases the epsilon buffers");
+
+__device__ __forceinline__ uint32_t hash_state(uint32_t d) { return d * 0x9E3779B1u; }
+
+// Load through a pointer known to address device memory (a global rather
+// than a flat access, which would also wait on LDS traffic).
+template <typename T>
+__device__ __forceinline__ T ldg(const T *ptr)
+{
+    return *(const __attribute__((address_space(1))) T *)ptr;
+}
+
+// Table loads: plain in LDS; in device memory they bypass the CU's L1, since
+// the table's atomics are performed in L2.
+template <bool G, typename T>
+__device__ __forceinline__ T tld(const T *ptr)
+{
+    if constexpr (G)
+        return __hip_atomic_load(const_cast<T *>(ptr), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+        return *ptr;
+}
+
+// Token table of one frame: keys = state (kEmptyKey if free), vals = packed
+// token (kEmptyTok if none).  After compaction a surviving slot's val holds
+// (user arc + 1) << 32 | survivor index, a pruned one kEmptyTok.  `slots`
+// lists the claimed slots in claim order.
+template <bool G>
+struct Tab {
+    uint32_t *keys;
+    unsigned long long *vals;
+    int32_t *slots;
+    uint32_t mask;
+    int fill;
+    int shift;   // 32 - log2(slots)
+};
+
+struct Sh {
+    int nslots;          // claimed slots
+    int overflow;        // more states than the table's fill limit
+    int status;          // sticky error of the utterance
+    uint32_t best;       // smallest cost key among the frame's tokens
+    uint32_t hint;       // key of one real candidate of the next frame
+    int gen_n[2];        // epsilon items per generation (LDS part first)
+    int ncand;           // emitting candidates listed this frame
+    int nlat_e, nlat_x;  // lattice records this frame
+    int bin, before, cnt;
+    int best_pos, best_eb, best_ed;
+    float best_cost;
+    unsigned long long eps_sum;
+    int scan[40];
+};
+
+// Running values of the utterance, identical in every thread (eps aside).
+struct Run {
+    int64_t set0;        // relative survivor index where the next set starts
+    int64_t prev0;       // relative start of S_{k-1}
+    int n_prev;          // |S_{k-1}|
+    int a_prev;          // emitting out-arcs of S_{k-1}
+    int64_t lat_e, lat_x;
+    int64_t tokens, arcs;
+    int gframes;
+    long long eps;       // epsilon out-arcs of survivors (this thread's share)
+};
+
+template <bool G>
+__device__ __forceinline__ int tab_find(const Tab<G> &t, uint32_t d)
+{
+    uint32_t h = hash_state(d) >> t.shift;
+    for (uint32_t probe = 0; probe <= t.mask; probe++) {
+        const uint32_t k = tld<G>(t.keys + h);
+        if (k == d) return static_cast<int>(h);
+        if (k == kEmptyKey) return -1;
+        h = (h + 1) & t.mask;
+    }
+    return -1;
+}
+
+// Slot of state d, claimed if new; -1 (and the overflow flag) if none is free.
+template <bool G>
+__device__ __forceinline__ int tab_claim(const Tab<G> &t, Sh &sh, uint32_t d)
+{
+    uint32_t h = hash_state(d) >> t.shift;
+    for (uint32_t probe = 0; probe <= t.mask; probe++) {
+        uint32_t k = tld<G>(t.keys + h);
+        if (k == kEmptyKey) {
+            k = atomicCAS(t.keys + h, kEmptyKey, d);
+            if (k == kEmptyKey) {
+                const int idx = atomicAdd(&sh.nslots, 1);
+                if (idx < t.fill) t.slots[idx] = static_cast<int32_t>(h);
+                else sh.overflow = 1;
+                return static_cast<int>(h);
+            }
+        }
+        if (k == d) return static_cast<int>(h);
+        h = (h + 1) & t.mask;
+    }
+    sh.overflow = 1;
+    return -1;
+}
+
+// Offer one candidate token per lane (act) to the table; lowered tokens of
+// states with epsilon out-arcs become items of generation `gen`.  Called by
+// the whole wave; returns the lane's slot or -1.
+template <bool G>
+__device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, uint2 *lgen, int glds, uint2 *sgen, int gcap, int gen,
+                                     bool act, uint32_t d, bool d_eps, float cand, uint32_t key, int32_t arc)
+{
+    bool impr = false;
+    int slot = -1;
+    if (act) {
+        slot = tab_claim<G>(t, sh, d);
+        if (slot >= 0) {
+            const unsigned long long v = make_tok(key, arc);
+            impr = v < atomicMin(t.vals + slot, v);
+        }
+    }
+    const uint32_t mk = wave_min_u32(impr ? key : kEmptyKey);
+    if (lane_id() == 0 && mk < sh.best) atomicMin(&sh.best, mk);
+    const bool push = impr && d_eps;
+    const uint64_t m = __ballot(push);
+    if (m) {
+        int b = 0;
+        if (lane_id() == 0) b = atomicAdd(&sh.gen_n[gen], __popcll(m));
+        b = __shfl(b, 0, kWave);
+        if (push) {
+            const int idx = b + rank_in(m);
+            const uint2 it = make_uint2(static_cast<uint32_t>(slot), __float_as_uint(cand));
+            if (idx < glds) lgen[gen * kGenCap + idx] = it;
+            else if (idx - glds < gcap) sgen[static_cast<int64_t>(gen) * gcap + (idx - glds)] = it;
+            else sh.status = WFST_ECAPACITY;
+        }
+    }
+    return slot;
+}
+
+// Largest t in [0, n) with epre[t] <= a (epre non-decreasing, epre[0] <= a).
+__device__ __forceinline__ int search_le(const int32_t *epre, int n, int a)
+{
+    const int lane = lane_id();
+    int lo = 0, end = n;
+    while (end - lo > 1) {
+        const int step = (end - lo + kWave - 1) / kWave;
+        const int idx = lo + lane * step;
+        const int v = idx < end ? epre[idx] : 0x7FFFFFFF;
+        const uint64_t m = __ballot(v <= a);
+        const int l = 63 - __clzll(static_cast<long long>(m));
+        lo += l * step;
+        end = min(lo + step, end);
+    }
+    return lo;
+}
+
+// Two block-wide exclusive scans at once; `sh` needs 34 ints.
+__device__ __forceinline__ int2 block_scan2(int x, int y, int *sh, int2 *total)
+{
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int ix = wave_incl_scan(x), iy = wave_incl_scan(y);
+    if (lane == kWave - 1) {
+        sh[w] = ix;
+        sh[16 + w] = iy;
+    }
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+        const int vx = threadIdx.x < kW ? sh[threadIdx.x] : 0;
+        const int vy = threadIdx.x < kW ? sh[16 + threadIdx.x] : 0;
+        const int sx = wave_incl_scan(vx), sy = wave_incl_scan(vy);
+        if (threadIdx.x < kW) {
+            sh[threadIdx.x] = sx - vx;
+            sh[16 + threadIdx.x] = sy - vy;
+        }
+        if (threadIdx.x == kWave - 1) {
+            sh[32] = sx;
+            sh[33] = sy;
+        }
+    }
+    __syncthreads();
+    const int2 r = make_int2(ix - x + sh[w], iy - y + sh[16 + w]);
+    *total = make_int2(sh[32], sh[33]);
+    __syncthreads();
+    return r;
+}
+
+// Bin holding the rank-th smallest (1-based) of a histogram: sets sh.bin and
+// sh.before (the count in lower bins).
+__device__ __forceinline__ void select_bin(const uint32_t *h, int nbins, int rank, Sh &sh)
+{
+    const int per = (nbins + kT - 1) / kT;
+    const int b0 = threadIdx.x * per;
+    int local = 0;
+    for (int i = 0; i < per; i++)
+        if (b0 + i < nbins) local += static_cast<int>(h[b0 + i]);
+    int total;
+    const int excl = block_excl_scan(local, sh.scan, &total);
+    if (rank > excl && rank <= excl + local) {
+        int cum = excl;
+        for (int i = 0; i < per && b0 + i < nbins; i++) {
+            const int c = static_cast<int>(h[b0 + i]);
+            if (rank <= cum + c) {
+                sh.bin = b0 + i;
+                sh.before = cum;
+                break;
+            }
+            cum += c;
+        }
+    }
+    __syncthreads();
+}
+
+// Shift of the first radix digit so that (lim - kb) >> shift fits the histogram.
+__device__ __forceinline__ int first_shift(uint32_t kb, uint32_t lim)
+{
+    const uint32_t span = lim - kb;
+    const int nb = span ? 32 - __clz(static_cast<int>(span)) : 0;
+    return nb > kHistBits ? nb - kHistBits : 0;
+}
+
+__device__ __forceinline__ void put_record(int4 *buf, int64_t cap, int64_t base, int *cnt, Sh &sh, bool rec,
+                                           const int4 &r)
+{
+    const uint64_t m = __ballot(rec);
+    if (!m) return;
+    int b = 0;
+    if (lane_id() == 0) b = atomicAdd(cnt, __popcll(m));
+    b = __shfl(b, 0, kWave);
+    if (rec) {
+        const int64_t idx = base + b + rank_in(m);
+        if (idx < cap) buf[idx] = r;
+        else sh.status = WFST_ECAPACITY;
+    }
+}
+
+// One frame: produces S_k from S_{k-1} (or from the start state when k = 0).
+// Returns 0, kOverflow (the table filled up; nothing of S_k was written) or
+// a negative WFST error.  Every return is taken by the whole workgroup.
+template <bool G>
+__device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
+                                     const Tab<G> &t, uint2 *aux, uint2 *spill, int gcap, int4 *cand,
+                                     int capC, Run &run, int k)
+{
+    const int tid = threadIdx.x;
+    const int lane = lane_id();
+    const int wid = tid / kWave;
+    const int glds = p.gen_lds;
+
+    if (tid == 0) {
+        sh.nslots = 0;
+        sh.overflow = 0;
+        sh.best = k > 0 ? sh.hint : kEmptyKey;
+        sh.gen_n[0] = sh.gen_n[1] = 0;
+        sh.ncand = 0;
+        sh.nlat_e = sh.nlat_x = 0;
+        sh.cnt = 0;
+        sh.best_pos = -1;
+    }
+    __syncthreads();
+
+    // ---- 1. expansion ----
+    if (k == 0) {
+        if (wid == 0) {
+            const int s = p.g.start;
+            (void)offer<G>(t, sh, aux, glds, spill, gcap, 0, lane == 0, static_cast<uint32_t>(s),
+                           p.g.xoff[s + 1] > p.g.xoff[s], 0.0f, okey(0.0f), -1);
+        }
+    } else {
+        const int n_tok = run.n_prev;
+        const int A = run.a_prev;
+        const int64_t base = ly.sv0 + run.prev0;
+        const int32_t *epre = p.sv_epre + base;
+        const int32_t *ebeg = p.sv_ebeg + base;
+        const uint64_t *tok = p.sv_tok + base;
+        const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k - 1]) * p.L;
+        for (int a0 = wid * kWave; a0 < A; a0 += kT) {
+            const int a_end = min(a0 + kWave, A);
+            int t0 = search_le(epre, n_tok, a0);
+            int done = a0;
+            while (done < a_end) {
+                const int tt = t0 + lane;
+                int pre = 0x7FFFFFFF, eb = 0;
+                float cst = 0.0f;
+                if (tt < n_tok) {
+                    pre = epre[tt];
+                    eb = ebeg[tt];
+                    cst = tok_cost(tok[tt]);
+                }
+                const int win_end = t0 + kWave < n_tok ? epre[t0 + kWave] : A;
+                const int hi = min(a_end, win_end);
+                const int a = done + lane;
+                const int o = owner_lane(pre, a);
+                const int ob = __shfl(eb, o, kWave);
+                const int op = __shfl(pre, o, kWave);
+                const float oc = __shfl(cst, o, kWave);
+                const uint32_t bnd = drop_bound(sh.best, p.beam);
+                bool act = false, d_eps = false;
+                uint32_t d = 0, key = kEmptyKey;
+                int arc = 0;
+                float cnd = 0.0f;
+                if (a < hi && op <= a) {
+                    const int4 r = p.g.earc[ob + (a - op)];
+                    d = static_cast<uint32_t>(r.x) & kDstMask;
+                    d_eps = r.x < 0;
+                    arc = r.w;
+                    const float t1 = oc + __int_as_float(r.z);
+                    cnd = t1 - ldg(row + r.y);
+                    key = okey(cnd);
+                    act = key <= bnd;
+                }
+                const int slot = offer<G>(t, sh, aux, glds, spill, gcap, 0, act, d, d_eps, cnd, key, arc);
+                // every offered candidate is listed: it gives the back-pointer
+                // of its destination when it wins, and an emitting lattice arc
+                const bool keep = act && slot >= 0;
+                const uint64_t m = __ballot(keep);
+                if (m) {
+                    int b = 0;
+                    if (lane == 0) b = atomicAdd(&sh.ncand, __popcll(m));
+                    b = __shfl(b, 0, kWave);
+                    if (keep) {
+                        const int idx = b + rank_in(m);
+                        if (idx < capC)
+                            cand[idx] = make_int4(static_cast<int>(run.prev0) + t0 + o, arc, __float_as_int(cnd), slot);
+                        else
+                            sh.status = WFST_ECAPACITY;
+                    }
+                }
+                done = hi;
+                t0 += kWave;
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- 2. epsilon closure ----
+    int cur = 0;
+    while (true) {
+        const int total = min(sh.gen_n[cur], glds + gcap);
+        if (total == 0 || sh.overflow || sh.status) break;
+        const int nxt = cur ^ 1;
+        if (tid == 0) sh.gen_n[nxt] = 0;
+        __syncthreads();
+        for (int c0 = wid * kWave; c0 < total; c0 += kT) {
+            const int i = c0 + lane;
+            int xb = 0, xd = 0;
+            float cst = 0.0f;
+            if (i < total) {
+                uint2 it;
+                if (i < glds) it = aux[cur * kGenCap + i];
+                else {
+                    const unsigned long long w = ldg(reinterpret_cast<const unsigned long long *>(
+                        spill + static_cast<int64_t>(cur) * gcap + (i - glds)));
+                    it = make_uint2(static_cast<uint32_t>(w), static_cast<uint32_t>(w >> 32));
+                }
+                cst = __uint_as_float(it.y);
+                const uint32_t now = static_cast<uint32_t>(tld<G>(t.vals + it.x) >> 32);
+                if (okey(cst) == now) {   // otherwise a cheaper item of this state follows
+                    const int s = static_cast<int>(tld<G>(t.keys + it.x));
+                    xb = p.g.xoff[s];
+                    xd = p.g.xoff[s + 1] - xb;
+                }
+            }
+            const int incl = wave_incl_scan(xd);
+            const int pre = incl - xd;
+            const int tot = __shfl(incl, kWave - 1, kWave);
+            for (int k0 = 0; k0 < tot; k0 += kWave) {
+                const int kk = k0 + lane;
+                const int o = owner_lane(pre, kk);
+                const int ob = __shfl(xb, o, kWave);
+                const int op = __shfl(pre, o, kWave);
+                const float oc = __shfl(cst, o, kWave);
+                const uint32_t bnd = drop_bound(sh.best, p.beam);
+                bool act = false, d_eps = false;
+                uint32_t d = 0, key = kEmptyKey;
+                int arc = 0;
+                float cnd = 0.0f;
+                if (kk < tot) {
+                    const int4 r = p.g.xarc[ob + (kk - op)];
+                    d = static_cast<uint32_t>(r.x) & kDstMask;
+                    d_eps = r.x < 0;
+                    arc = r.z;
+                    cnd = oc + __int_as_float(r.y);
+                    key = okey(cnd);
+                    act = key <= bnd;
+                }
+                (void)offer<G>(t, sh, aux, glds, spill, gcap, nxt, act, d, d_eps, cnd, key, arc);
+            }
+        }
+        __syncthreads();
+        cur = nxt;
+    }
+    if (sh.overflow) return kOverflow;
+    if (sh.status) return sh.status;
+
+    // ---- 3. pruning ----
+    const int n = sh.nslots;
+    const uint32_t kb = sh.best;
+    const uint32_t lim = beam_limit(kb, p.beam);
+    uint32_t cut = lim;
+    if (p.max_active > 0 && n > p.max_active && kb <= lim) {
+        uint32_t *hist = reinterpret_cast<uint32_t *>(aux);
+        int shf = first_shift(kb, lim);
+        for (int i = tid; i < kHistBins; i += kT) hist[i] = 0u;
+        __syncthreads();
+        int cnt = 0;
+        for (int i = tid; i < n; i += kT) {
+            const uint32_t key = static_cast<uint32_t>(tld<G>(t.vals + tld<G>(t.slots + i)) >> 32);
+            if (key <= lim) {
+                cnt++;
+                atomicAdd(&hist[(key - kb) >> shf], 1u);
+            }
+        }
+        if (cnt) atomicAdd(&sh.cnt, cnt);
+        __syncthreads();
+        if (sh.cnt > p.max_active) {
+            int rank = p.max_active;
+            select_bin(hist, kHistBins, rank, sh);
+            uint32_t prefix = static_cast<uint32_t>(sh.bin) << shf;
+            rank -= sh.before;
+            while (shf > 0) {
+                const int nsh = shf > kHistBits ? shf - kHistBits : 0;
+                const int nb = 1 << (shf - nsh);
+                __syncthreads();
+                for (int i = tid; i < nb; i += kT) hist[i] = 0u;
+                __syncthreads();
+                for (int i = tid; i < n; i += kT) {
+                    const uint32_t key = static_cast<uint32_t>(tld<G>(t.vals + tld<G>(t.slots + i)) >> 32);
+                    if (key > lim) continue;
+                    const uint32_t off = key - kb;
+                    if ((off >> shf) == (prefix >> shf)) atomicAdd(&hist[(off >> nsh) & (nb - 1)], 1u);
+                }
+                __syncthreads();
+                select_bin(hist, nb, rank, sh);
+                prefix |= static_cast<uint32_t>(sh.bin) << nsh;
+                rank -= sh.before;
+                shf = nsh;
+            }
+            const uint32_t theta = kb + prefix;
+            cut = theta < lim ? theta : lim;
+        }
+        __syncthreads();
+    }
+
+    // ---- 4. compaction into S_k, in slot-list order ----
+    const int64_t set0 = run.set0;
+    int n_kept = 0, a_kept = 0;
+    for (int e0 = 0; e0 < n; e0 += kT * kRun) {
+        int sl[kRun], dd[kRun], eb[kRun], ed[kRun];
+        unsigned long long vv[kRun];
+        bool kp[kRun];
+        int kc = 0, ac = 0;
+        long long xc = 0;
+#pragma unroll
+        for (int r = 0; r < kRun; r++) {
+            const int i = e0 + tid * kRun + r;
+            sl[r] = -1;
+            dd[r] = 0;
+            vv[r] = kEmptyTok;
+            if (i < n) {
+                sl[r] = tld<G>(t.slots + i);
+                vv[r] = tld<G>(t.vals + sl[r]);
+                dd[r] = static_cast<int>(tld<G>(t.keys + sl[r]));
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < kRun; r++) {
+            kp[r] = sl[r] >= 0 && static_cast<uint32_t>(vv[r] >> 32) <= cut;
+            eb[r] = 0;
+            ed[r] = 0;
+            if (kp[r]) {
+                eb[r] = p.g.eoff[dd[r]];
+                ed[r] = p.g.eoff[dd[r] + 1];
+                xc += p.g.xoff[dd[r] + 1] - p.g.xoff[dd[r]];
+                kc++;
+                ac += ed[r] - eb[r];
+            }
+        }
+        run.eps += xc;
+        int2 tot;
+        const int2 ex = block_scan2(kc, ac, sh.scan, &tot);
+        int pos = n_kept + ex.x, apos = a_kept + ex.y;
+#pragma unroll
+        for (int r = 0; r < kRun; r++) {
+            if (kp[r]) {
+                const int64_t rel = set0 + pos;
+                if (rel < ly.svcap) {
+                    const int64_t o = ly.sv0 + rel;
+                    p.sv_state[o] = dd[r];
+                    p.sv_tok[o] = vv[r];
+                    p.sv_ebeg[o] = eb[r];
+                    p.sv_epre[o] = apos;
+                } else {
+                    sh.status = WFST_ECAPACITY;
+                }
+                if (static_cast<uint32_t>(vv[r] >> 32) == kb && atomicCAS(&sh.best_pos, -1, pos) == -1) {
+                    sh.best_eb = eb[r];
+                    sh.best_ed = ed[r];
+                    sh.best_cost = tok_cost(vv[r]);
+                }
+                t.vals[sl[r]] = (vv[r] << 32) | static_cast<uint32_t>(rel);
+                pos++;
+                apos += ed[r] - eb[r];
+            } else if (sl[r] >= 0) {
+                t.vals[sl[r]] = kEmptyTok;
+            }
+        }
+        n_kept += tot.x;
+        a_kept += tot.y;
+    }
+    __syncthreads();
+    const int ns = n_kept;
+    if (ns == 0) return WFST_ENOPATH;
+    if (sh.status) return sh.status;
+    if (tid == 0) {
+        p.sv_off[ly.fo0 + k + 1] = set0 + ns;
+        p.cut_arr[ly.fo0 + k] = cut;
+    }
+    // early-drop seed of the next frame: the cheapest candidate of one best
+    // token of S_k, a real candidate cost of frame k + 1
+    if (wid == 0 && k < Tp) {
+        const float c = sh.best_cost;
+        const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k]) * p.L;
+        uint32_t hint = kEmptyKey;
+        for (int a = sh.best_eb + lane; a < sh.best_ed; a += kWave) {
+            const int4 r = p.g.earc[a];
+            const float t1 = c + __int_as_float(r.z);
+            const uint32_t key = okey(t1 - ldg(row + r.y));
+            hint = key < hint ? key : hint;
+        }
+        hint = wave_min_u32(hint);
+        if (lane == 0) sh.hint = hint;
+    }
+
+    // ---- 5. back-pointers and lattice records ----
+    // Survivors of S_k: the back-pointer of a token reached by an epsilon arc
+    // (its source is in S_k) and the epsilon lattice arcs inside S_k.
+    for (int c0 = wid * kWave; c0 < ns; c0 += kT) {
+        const int i = c0 + lane;
+        int xb = 0, xdeg = 0;
+        float cst = 0.0f;
+        if (i < ns) {
+            const int64_t o = ly.sv0 + set0 + i;
+            const int s = p.sv_state[o];
+            const uint64_t v = p.sv_tok[o];
+            cst = tok_cost(v);
+            const int a = tok_arc(v);
+            if (a < 0) {
+                p.sv_prev[o] = -1;
+            } else {
+                const int info = p.g.arc_src[a];
+                if (info < 0) {
+                    const int sl = tab_find<G>(t, static_cast<uint32_t>(info) & kDstMask);
+                    p.sv_prev[o] = sl >= 0 ? static_cast<int>(static_cast<uint32_t>(tld<G>(t.vals + sl))) : -1;
+                }
+            }
+            if (p.lattice) {
+                xb = p.g.xoff[s];
+                xdeg = p.g.xoff[s + 1] - xb;
+            }
+        }
+        if (!p.lattice) continue;
+        const int incl = wave_incl_scan(xdeg);
+        const int pre = incl - xdeg;
+        const int tot = __shfl(incl, kWave - 1, kWave);
+        for (int k0 = 0; k0 < tot; k0 += kWave) {
+            const int kk = k0 + lane;
+            const int o = owner_lane(pre, kk);
+            const int ob = __shfl(xb, o, kWave);
+            const int op = __shfl(pre, o, kWave);
+            const float oc = __shfl(cst, o, kWave);
+            bool rec = false;
+            int4 r4 = make_int4(0, 0, 0, 0);
+            if (kk < tot) {
+                const int4 x = p.g.xarc[ob + (kk - op)];
+                const float pc = oc + __int_as_float(x.y);
+                if (okey(pc) <= cut) {
+                    const int sl = tab_find<G>(t, static_cast<uint32_t>(x.x) & kDstMask);
+                    const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
+                    rec = dv != kEmptyTok;
+                    r4 = make_int4(static_cast<int>(set0) + c0 + o, static_cast<int>(static_cast<uint32_t>(dv)), x.z,
+                                   __float_as_int(pc));
+                }
+            }
+            put_record(p.lat_x + ly.lx0, ly.lxcap, run.lat_x, &sh.nlat_x, sh, rec, r4);
+        }
+    }
+    // Candidates of the expansion: the winner of each surviving destination
+    // gives its back-pointer; those within the cutoff are emitting lattice arcs.
+    if (k > 0) {
+        const int nc = min(sh.ncand, capC);
+        for (int i0 = wid * kWave; i0 < nc; i0 += kT) {
+            const int i = i0 + lane;
+            bool rec = false;
+            int4 r4 = make_int4(0, 0, 0, 0);
+            if (i < nc) {
+                const int4 c4 = cand[i];
+                const unsigned long long dv = tld<G>(t.vals + c4.w);
+                if (dv != kEmptyTok) {
+                    const int drel = static_cast<int>(static_cast<uint32_t>(dv));
+                    if (static_cast<uint32_t>(dv >> 32) == static_cast<uint32_t>(c4.y + 1))
+                        p.sv_prev[ly.sv0 + drel] = c4.x;
+                    rec = p.lattice && okey(__int_as_float(c4.z)) <= cut;
+                    r4 = make_int4(c4.x, drel, c4.y, c4.z);
+                }
+            }
+            if (p.lattice) put_record(p.lat_e + ly.le0, ly.lecap, run.lat_e, &sh.nlat_e, sh, rec, r4);
+        }
+    }
+    __syncthreads();
+    run.lat_e += sh.nlat_e;
+    run.lat_x += sh.nlat_x;
+    if (sh.status) return sh.status;
+    run.tokens += ns;
+    if (k < Tp) run.arcs += a_kept;
+    run.prev0 = set0;
+    run.set0 = set0 + ns;
+    run.n_prev = ns;
+    run.a_prev = a_kept;
+
+    // ---- 6. clear the table ----
+    for (int i = tid; i < n; i += kT) {
+        const int s2 = tld<G>(t.slots + i);
+        t.keys[s2] = kEmptyKey;
+        t.vals[s2] = kEmptyTok;
+    }
+    __syncthreads();
+    return 0;
+}
+
+__global__ __launch_bounds__(kT) void utt_kernel(Params p)
+{
+    __shared__ uint32_t s_keys[kSlots];
+    __shared__ unsigned long long s_vals[kSlots];
+    __shared__ int32_t s_slots[kFill];
+    __shared__ uint2 s_aux[2 * kGenCap];   // epsilon generations, or the select histogram
+    __shared__ Sh sh;
+
+    const int u = blockIdx.x;
+    const int tid = threadIdx.x;
+    UttState &st = p.st[u];
+    if (st.status != 0) return;
+    const UttLayout &ly = p.lay[u];
+    const int Tp = st.Tp;
+    const float *ll = st.ll;
+
+    Tab<false> lt;
+    lt.keys = s_keys;
+    lt.vals = s_vals;
+    lt.slots = s_slots;
+    lt.mask = kSlots - 1;
+    lt.fill = min(kFill, p.lds_fill);
+    lt.shift = 32 - kSlotBits;
+    Tab<true> gt;
+    const int64_t gbase = static_cast<int64_t>(u) * p.capG;
+    gt.keys = p.gkeys + gbase;
+    gt.vals = p.gvals + gbase;
+    gt.slots = p.gslots + gbase;
+    gt.mask = static_cast<uint32_t>(p.capG - 1);
+    gt.fill = static_cast<int>(p.capG / 4 * 3);
+    gt.shift = 32 - (31 - __clz(static_cast<int>(p.capG)));
+    const int gcap = static_cast<int>(p.capO);
+    uint2 *spill = p.gspill + static_cast<int64_t>(u) * 2 * p.capO;
+    int4 *cand = p.cand + static_cast<int64_t>(u) * p.capC;
+    const int capC = static_cast<int>(p.capC);
+
+    for (int i = tid; i < kSlots; i += kT) {
+        s_keys[i] = kEmptyKey;
+        s_vals[i] = kEmptyTok;
+    }
+    if (tid == 0) {
+        sh.status = 0;
+        sh.hint = kEmptyKey;
+        sh.eps_sum = 0ull;
+    }
+    __syncthreads();
+
+    Run run{};
+    bool gclean = false;
+    int rc = 0;
+    for (int k = 0; k <= Tp; k++) {
+        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, spill, gcap, cand, capC, run, k);
+        if (rc == kOverflow) {
+            // more states than the LDS table holds: redo the frame in device memory
+            for (int i = tid; i < kSlots; i += kT) {
+                s_keys[i] = kEmptyKey;
+                s_vals[i] = kEmptyTok;
+            }
+            if (!gclean) {
+                for (int64_t i = tid; i < p.capG; i += kT) {
+                    gt.keys[i] = kEmptyKey;
+                    gt.vals[i] = kEmptyTok;
+                }
+                gclean = true;
+            }
+            __syncthreads();
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, spill, gcap, cand, capC, run, k);
+            if (rc == kOverflow) rc = WFST_ECAPACITY;
+            run.gframes++;
+        }
+        if (rc != 0) break;
+    }
+    const long long e = wave_sum_ll(run.eps);
+    if (lane_id() == 0 && e) atomicAdd(&sh.eps_sum, static_cast<unsigned long long>(e));
+    __syncthreads();
+    if (tid == 0) {
+        st.sv_base = run.set0;
+        st.n_cur = run.n_prev;
+        st.le_cnt = run.lat_e;
+        st.lx_cnt = run.lat_x;
+        st.tokens = run.tokens;
+        st.arcs_expanded = run.arcs;
+        st.eps_arcs = static_cast<int64_t>(sh.eps_sum);
+        st.gframes = run.gframes;
+        if (rc != 0) st.status = rc;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_utt(const Params &p, hipStream_t s)
+{
+    hipLaunchKernelGGL(utt_kernel, dim3(p.U), dim3(kT), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace wfd

@@ -118,17 +118,57 @@ def test_config2_raw_lattice_and_infinite_beam_prefix(dec, torch_mod, oracle_mod
     parity.assert_same(ro, rg, lattice=True, tag="config 2 infinite beam")
 
 
+class _env:
+    """Set test-hook environment variables of the library for one block."""
+
+    def __init__(self, **kv):
+        self.kv = kv
+
+    def __enter__(self):
+        for k, v in self.kv.items():
+            os.environ[k] = str(v)
+
+    def __exit__(self, *exc):
+        for k in self.kv:
+            os.environ.pop(k, None)
+
+
 def test_epsilon_queue_overflow_path(dec, torch_mod, oracle_mod, cfg2):
-    # a 2-item per-wave epsilon queue sends most epsilon work through the
-    # overflow list and the last-block closure
+    # two epsilon items per generation in LDS: the rest of the closure goes
+    # through the device-memory spill lists
     wl, gh = cfg2
-    os.environ["WFSTDEC_TEST_QUEUE_CAP"] = "2"
-    try:
+    with _env(WFSTDEC_TEST_QUEUE_CAP=2):
         ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:80], gh=gh, beam=13.0,
                       max_active=7000, lattice_beam=8.0)
-    finally:
-        del os.environ["WFSTDEC_TEST_QUEUE_CAP"]
     parity.assert_same(ro, rg, lattice=True, tag="overflow queue")
+
+
+@pytest.mark.parametrize("fill", [1, 40, 700])
+def test_device_memory_table_path(dec, torch_mod, oracle_mod, cfg2, fill):
+    # frames reaching more than `fill` states are redone with the token table
+    # in device memory (every frame for fill = 1, a mix for the others)
+    wl, gh = cfg2
+    with _env(WFSTDEC_TEST_LDS_FILL=fill):
+        ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:60], gh=gh, beam=13.0,
+                      max_active=7000 if fill != 40 else 300, lattice_beam=8.0)
+    parity.assert_same(ro, rg, lattice=True, tag="device table fill %d" % fill)
+    for seed in range(6):
+        g = W.random_small_graph(900 + seed, 300, mean_deg=3.0, eps_frac=0.3, num_labels=5, weights="int",
+                                 final=seed % 2 == 0)
+        ll = W.random_small_loglikes(900 + seed, 25, 5, kind="int")
+        with _env(WFSTDEC_TEST_LDS_FILL=fill, WFSTDEC_TEST_QUEUE_CAP=2):
+            ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=9.0, max_active=[0, 11][seed % 2],
+                          lattice_beam=3.0)
+        parity.assert_same(ro, rg, lattice=True, tag="device table fill %d seed %d" % (fill, seed))
+
+
+def test_per_frame_kernel_path(dec, torch_mod, oracle_mod, cfg2):
+    # the alternative schedule: one expand / prune / record launch per frame
+    wl, gh = cfg2
+    with _env(WFSTDEC_FRAME_KERNELS=1):
+        ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:120], gh=gh, beam=13.0,
+                      max_active=7000, lattice_beam=8.0)
+    parity.assert_same(ro, rg, lattice=True, tag="per-frame kernels")
 
 
 def test_determinism(dec, torch_mod, cfg2):
