@@ -1,7 +1,7 @@
 #!/usr/bin/env python3
 """Benchmark of WFST Viterbi beam decoding with lattice generation on one
 MI355X: decoded frames/s (with RTF, arcs expanded/s and the HBM roofline of
-the arc-expansion kernel) on the 25M-arc LVCSR-scale graph, 64 utterances of
+the search kernel) on the 25M-arc LVCSR-scale graph, 64 utterances of
 300-1,500 frames decoded in one batched call.
 
 One step = one wfst_decode_batch call over the whole batch: label-synchronous
@@ -28,8 +28,18 @@ sys.path.insert(0, ROOT)
 METRIC = "decoded frames/sec (RTF) + arcs expanded/sec + % HBM peak, 25M-arc graph"
 HBM_PEAK_GBS = 8000.0
 FRAME_SHIFT_S = 0.010
-COUNTERS = os.path.join(ROOT, "profiles", "expand_kernel_lvcsr-25m-batch64_counters.txt")
-KERNEL_SRC = os.path.join(ROOT, "paper_1808_00687_amd", "csrc", "search_kernels.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+COUNTERS = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_counters.txt")
+TRACE = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_trace.txt")
+CSRC = os.path.join(ROOT, "paper_1808_00687_amd", "csrc")
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("search_kernel.hip", "device_util.h", "internal.h")]
+KERNEL_NAME = "search_kernel"
+CALIBRATION_MIB = 1024
+TRACE_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_search -o run -- "
+             "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline")
+PMC_CMD = ("timeout -s KILL 180 rocprofv3 --pmc {counter} --output-format csv -d gpurun_out/pmc_{tag} -o run -- "
+           "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile --copy-calibration-mib %d"
+           % CALIBRATION_MIB)
 
 WORKLOADS = {
     "cfg1": (1, True), "cfg2": (2, True), "cfg3": (3, True), "cfg4": (4, True),
@@ -41,20 +51,30 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def expand_bytes(stats_list):
-    """Algorithmic bytes moved by the expansion kernel over one decode: 16 B
-    per expanded token (state, cost, two row offsets), 24 B per emitting arc
-    (dst, ilabel, weight, loglike, 8-byte atomic), 16 B per epsilon arc of a
-    surviving token (dst, weight, 8-byte atomic)."""
-    tok = sum(s["tokens"] - s["tokens_last"] for s in stats_list)
+def search_bytes(stats_list):
+    """Algorithmic device-memory bytes of the search kernel over one batch:
+    per surviving token 32 B (its state, token and back-pointer written,
+    16 B; the emitting and epsilon row offsets of its state read, 16 B), per
+    expanded emitting arc 20 B (16 B arc record, 4 B log-likelihood), per
+    epsilon out-arc of a surviving token 16 B (arc record), per raw lattice
+    record 16 B written."""
+    tok = sum(s["tokens"] for s in stats_list)
     arcs = sum(s["arcs_expanded"] for s in stats_list)
     eps = sum(s["eps_arcs"] for s in stats_list)
-    return 16 * tok + 24 * arcs + 16 * eps
+    lat = sum(s["lattice_raw"] for s in stats_list)
+    return 32 * tok + 20 * arcs + 16 * eps + 16 * lat
 
 
-def read_traffic(expected_launches):
-    """HBM bytes per expansion launch from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source."""
+def kernel_sha() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
+def read_traffic():
+    """HBM bytes per search launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel sources."""
     if not os.path.exists(COUNTERS):
         return None
     kv = {}
@@ -62,13 +82,53 @@ def read_traffic(expected_launches):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    sha = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    if kv.get("kernel_source_sha256") != sha:
+    if kv.get("kernel_source_sha256") != kernel_sha():
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str):
+    """Summaries of the rocprofv3 runs for profiles/: the kernel-trace
+    statistics and the HBM counters of the search kernel, each counter scaled
+    by what it reads for the plain device copy of known size that bench.py
+    runs first (--copy-calibration-mib)."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    lines = ["# rocprofv3 kernel-trace statistics, workload lvcsr-25m-batch64 (64 utterances, 25M-arc graph)",
+             "# command: " + TRACE_CMD,
+             "# summary written by: python3 bench.py --write-profiles gpurun_out/prof_search/run_kernel_stats.csv "
+             "gpurun_out/pmc_fetch/run_counter_collection.csv gpurun_out/pmc_write/run_counter_collection.csv",
+             "%-62s %6s %14s %14s %7s" % ("kernel", "calls", "total_ms", "average_us", "pct")]
+    for r in rows:
+        lines.append("%-62s %6s %14.3f %14.1f %7s" % (r["Name"][:62], r["Calls"], float(r["TotalDurationNs"]) / 1e6,
+                                                      float(r["AverageNs"]) / 1e3, r["Percentage"]))
+    open(TRACE, "w").write("\n".join(lines) + "\n")
+    out = ["# HBM traffic of %s per launch, workload lvcsr-25m-batch64" % KERNEL_NAME,
+           "# fetch command: " + PMC_CMD.format(counter="FETCH_SIZE", tag="fetch"),
+           "# write command: " + PMC_CMD.format(counter="WRITE_SIZE", tag="write"),
+           "# counters are KiB per dispatch; each is scaled by bytes/reading of a %d MiB device copy" % CALIBRATION_MIB]
+    total = 0.0
+    for tag, path in (("fetch", fetch_csv), ("write", write_csv)):
+        rows = list(csv.DictReader(open(path)))
+        copies = sorted(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])[-3:]
+        cal = sorted(copies)[len(copies) // 2]
+        factor = CALIBRATION_MIB * (1 << 20) / (cal * 1024.0)
+        vals = [float(r["Counter_Value"]) for r in rows if KERNEL_NAME in r["Kernel_Name"]]
+        kib = sum(vals) / len(vals)
+        byts = kib * 1024.0 * factor
+        total += byts
+        out += ["%s_counter: %s" % (tag, rows[0]["Counter_Name"]),
+                "%s_copy_reading_kib: %.1f" % (tag, cal),
+                "%s_scale: %.4f" % (tag, factor),
+                "%s_kib_per_launch: %.1f" % (tag, kib),
+                "%s_bytes_per_launch: %.0f" % (tag, byts)]
+    out += ["hbm_bytes_per_launch: %.0f" % total, "kernel_source_sha256: %s" % kernel_sha()]
+    open(COUNTERS, "w").write("\n".join(out) + "\n")
+    print(TRACE)
+    print(COUNTERS)
 
 
 def cpu_baseline(wl, max_seconds: float):
@@ -81,7 +141,7 @@ def cpu_baseline(wl, max_seconds: float):
     o = wl.opts
     g = wl.graph
     n_utt = len(wl.loglikes)
-    sample = list(range(min(n_utt, cores)))
+    sample = list(range(min(n_utt, 3 * cores)))
     if n_utt == 1:
         sample = [0]
     t0 = time.time()
@@ -126,7 +186,12 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0)
     ap.add_argument("--no-profile", action="store_true",
                     help="do not time kernel phases with HIP events")
+    ap.add_argument("--write-profiles", nargs=3, metavar=("STATS_CSV", "FETCH_CSV", "WRITE_CSV"),
+                    help="write the profiles/ summaries from rocprofv3 CSV output and exit")
     args = ap.parse_args()
+    if args.write_profiles:
+        write_profiles(*args.write_profiles)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -219,15 +284,15 @@ def main():
     }
     if profile:
         s0 = stats[0]
-        launches = s0["expand_launches"]
-        exp_ms = s0["expand_ms"]
-        alg = expand_bytes(stats)
+        launches = s0["search_launches"]
+        search_ms = s0["search_ms"]
+        alg = search_bytes(stats)
         per_launch = alg / max(launches, 1)
-        dur_s = exp_ms / 1e3 / max(launches, 1)
+        dur_s = search_ms / 1e3 / max(launches, 1)
         achieved = per_launch / dur_s / 1e9 if dur_s > 0 else None
-        traffic = read_traffic(launches)
+        traffic = read_traffic()
         out["roofline"] = {
-            "kernel": "expand_kernel",
+            "kernel": "search_kernel",
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
@@ -238,8 +303,7 @@ def main():
             "avg_launch_us": dur_s * 1e6,
             "launches": launches,
         }
-        out["kernel_ms"] = {"expand": exp_ms, "prune": s0["prune_ms"], "record": s0["record_ms"],
-                            "final": s0["final_ms"]}
+        out["kernel_ms"] = {"search": search_ms, "final": s0["final_ms"]}
     if not args.no_cpu_baseline:
         log("oracle baseline ...")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)

@@ -208,11 +208,10 @@ typedef struct wfst_stats {
     double decode_ms;          /* wall time of the call that produced this result */
     /* with WFST_PROFILE (batch-wide, the same in every result of a batch):
        device time summed over launches, measured with HIP events */
-    double expand_ms;          /* emitting expansion + epsilon closure */
-    double prune_ms;           /* beam / max-active pruning and compaction */
-    double record_ms;          /* back-pointers and lattice recording */
+    double search_ms;          /* token passing over all frames: expansion, epsilon
+                                  closure, pruning, back-pointers, lattice records */
     double final_ms;           /* final costs, backtrace, lattice pruning and output */
-    int32_t expand_launches;   /* launches of the expansion kernel */
+    int32_t search_launches;   /* launches of the search kernel */
 } wfst_stats;
 
 int wfst_result_stats(const wfst_result *r, wfst_stats *stats);

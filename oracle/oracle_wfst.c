@@ -32,6 +32,13 @@
  *    whose best complete path lies within lattice_beam of the best path.
  *
  * Everything is float32 with no contraction (built with -ffp-contract=off).
+ *
+ * Parity unpinned: the paper fixes none of these conventions, so nothing
+ * outside this file and the decoder pins them: the arc-index tie-break of
+ * recombination, the lowest-state tie-break of the final argmin, the
+ * fall-back to "every state final" when no final state is reached, and the
+ * exact raw-lattice arc criterion (the kept set is pinned against brute
+ * force only on dyadic inputs, where float32 arithmetic is exact).
  */
 #include "oracle_wfst.h"
 

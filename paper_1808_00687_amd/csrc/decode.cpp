@@ -1,12 +1,13 @@
 // Decode driver and result objects of the C ABI.
 //
-// One call decodes a batch of utterances in lock-step: classify frames
-// (label-synchronous compaction), produce token set 0 from the start state,
-// then for every decoded frame run expand -> prune (gather, select, compact)
-// -> record -> advance for the whole batch, and finally the final costs,
-// backtrace and lattice pruning.  Counts stay on the device; the host reads
-// back only the decoded-frame counts (to size the loop) and the results.
+// One call decodes a batch of utterances: classify frames (label-synchronous
+// compaction), one search launch in which a workgroup per utterance produces
+// every token set with its back-pointers and lattice records, then final
+// costs, backtrace, lattice-beam pruning and the sorted lattice.  Buffers
+// are carved from a per-device arena kept between calls; a buffer that
+// overflows makes the call decode again with larger ones.
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cmath>
 #include <cstdio>
@@ -91,52 +92,87 @@ struct DeviceGuard {
     }
 };
 
-// Stream-ordered workspace allocations, released when the attempt ends.
-struct Workspace {
-    hipStream_t s;
-    std::vector<void *> ptrs;
-    hipError_t err = hipSuccess;
-    explicit Workspace(hipStream_t st) : s(st) {}
+// Device workspace of one decode call: every buffer is carved from one
+// arena.  A first pass over the same carving code only measures the size.
+struct Arena {
+    char *base = nullptr;
+    size_t off = 0;
     template <typename T>
     T *get(int64_t count)
     {
-        if (err != hipSuccess) return nullptr;
-        size_t bytes = static_cast<size_t>(std::max<int64_t>(count, 1)) * sizeof(T);
-        void *p = nullptr;
-        err = hipMallocAsync(&p, bytes, s);
-        if (err != hipSuccess) return nullptr;
-        ptrs.push_back(p);
-        return static_cast<T *>(p);
-    }
-    ~Workspace()
-    {
-        for (void *p : ptrs) (void)hipFreeAsync(p, s);
+        const size_t bytes = (static_cast<size_t>(std::max<int64_t>(count, 1)) * sizeof(T) + 255) &
+                             ~static_cast<size_t>(255);
+        T *ptr = base ? reinterpret_cast<T *>(base + off) : nullptr;
+        off += bytes;
+        return ptr;
     }
 };
 
-void keep_pool_memory(int device)
+// One arena per device is kept between calls and only ever grows, so that
+// steady-state decoding allocates nothing.  A call that finds it in use by a
+// concurrent call takes a private allocation instead.
+struct ArenaCache {
+    std::mutex mu;
+    bool busy = false;
+    void *ptr = nullptr;
+    size_t cap = 0;
+};
+
+ArenaCache &arena_cache(int dev)
 {
-    static std::once_flag once[64];
-    if (device < 0 || device >= 64) return;
-    std::call_once(once[device], [device]() {
-        hipMemPool_t pool;
-        if (hipDeviceGetDefaultMemPool(&pool, device) == hipSuccess) {
-            uint64_t thr = std::numeric_limits<uint64_t>::max();
-            (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
-        }
-    });
+    static ArenaCache *c = new ArenaCache[64];
+    return c[dev];
 }
 
-int test_queue_cap()
-{
-    // test hook: a tiny per-wave epsilon queue forces the overflow path
-    const char *v = getenv("WFSTDEC_TEST_QUEUE_CAP");
-    if (!v) return kQueueCap;
-    int q = atoi(v);
-    int c = 2;
-    while (c * 2 <= q && c * 2 <= kQueueCap) c *= 2;
-    return c;
-}
+struct ArenaLease {
+    int dev = -1;
+    void *ptr = nullptr;
+    bool cached = false;
+    ArenaLease() = default;
+    ArenaLease(const ArenaLease &) = delete;
+    ArenaLease &operator=(const ArenaLease &) = delete;
+    hipError_t acquire(int device, size_t need)
+    {
+        dev = device;
+        if (dev >= 0 && dev < 64) {
+            ArenaCache &c = arena_cache(dev);
+            std::lock_guard<std::mutex> lk(c.mu);
+            if (!c.busy) {
+                if (c.cap < need) {
+                    if (c.ptr) (void)hipFree(c.ptr);
+                    c.ptr = nullptr;
+                    c.cap = 0;
+                    size_t want = need + need / 4;
+                    hipError_t e = hipMalloc(&c.ptr, want);
+                    if (e != hipSuccess) {
+                        want = need;
+                        e = hipMalloc(&c.ptr, want);
+                    }
+                    if (e != hipSuccess) {
+                        c.ptr = nullptr;
+                        return e;
+                    }
+                    c.cap = want;
+                }
+                c.busy = true;
+                cached = true;
+                ptr = c.ptr;
+                return hipSuccess;
+            }
+        }
+        return hipMalloc(&ptr, need);
+    }
+    ~ArenaLease()
+    {
+        if (cached) {
+            ArenaCache &c = arena_cache(dev);
+            std::lock_guard<std::mutex> lk(c.mu);
+            c.busy = false;
+        } else if (ptr) {
+            (void)hipFree(ptr);
+        }
+    }
+};
 
 int test_env_int(const char *name, int dflt)
 {
@@ -148,6 +184,7 @@ int test_env_int(const char *name, int dflt)
 }
 
 struct Sizes {
+    int64_t capA;      // tokens per frame on average over an utterance
     int64_t capF;      // tokens per frame
     int64_t capT;      // reached states per frame
     int64_t capO;      // overflow epsilon items per frame (per generation)
@@ -223,29 +260,6 @@ struct Timer {
     }
 };
 
-// Events ordering the two streams of the frame loop.
-struct EventRing {
-    std::vector<hipEvent_t> ev;
-    explicit EventRing(int n) : ev(n, nullptr)
-    {
-        for (auto &e : ev) (void)hipEventCreateWithFlags(&e, hipEventDisableTiming);
-    }
-    hipEvent_t operator[](int i) const { return ev[i % ev.size()]; }
-    ~EventRing()
-    {
-        for (auto e : ev)
-            if (e) (void)hipEventDestroy(e);
-    }
-};
-
-struct StreamHolder {
-    hipStream_t s = nullptr;
-    ~StreamHolder()
-    {
-        if (s) (void)hipStreamDestroy(s);
-    }
-};
-
 // Wall-clock breakdown of one decode call on stderr (WFSTDEC_DEBUG_TIMING=1).
 struct WallTrace {
     bool on = getenv("WFSTDEC_DEBUG_TIMING") != nullptr;
@@ -263,7 +277,7 @@ struct WallTrace {
     }
 };
 
-enum { PH_EXPAND = 0, PH_PRUNE = 1, PH_RECORD = 2, PH_FINAL = 3, PH_COUNT = 4 };
+enum { PH_SEARCH = 0, PH_FINAL = 1, PH_COUNT = 2 };
 
 // One attempt at decoding the batch with the given buffer sizes.  Returns
 // WFST_OK, an error, or WFST_ECAPACITY when a buffer overflowed.
@@ -274,10 +288,6 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     const int64_t N = G.d.n;
     const bool lattice = o.lattice_beam >= 0.0f;
     const int depth = G.eps_depth;
-    // the per-frame kernels (expand / prune / record, one launch each per
-    // frame) instead of the whole-utterance kernel
-    const bool frame_kernels = getenv("WFSTDEC_FRAME_KERNELS") != nullptr;
-    Workspace ws(s);
     Timer tm;
     tm.on = (o.flags & WFST_PROFILE) != 0 && G.device >= 0 && G.device < 64;
     tm.dev = G.device;
@@ -288,14 +298,14 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         UttLayout &l = lay[u];
         const int64_t Tu = T[u];
         l.sv0 = sv;
-        // survivor indices are 32-bit
-        l.svcap = std::min<int64_t>((Tu + 1) * z.capF, std::numeric_limits<int32_t>::max());
+        // survivor indices are 32-bit; one frame may reach capF tokens
+        l.svcap = std::min<int64_t>((Tu + 1) * z.capA + z.capF, std::numeric_limits<int32_t>::max());
         sv += l.svcap;
         l.le0 = le;
-        l.lecap = lattice ? std::max<int64_t>(Tu, 1) * z.capF * z.lat_mult : 0;
+        l.lecap = lattice ? (Tu * z.capA + z.capF) * z.lat_mult : 0;
         le += l.lecap;
         l.lx0 = lx;
-        l.lxcap = lattice ? (Tu + 1) * z.capF * std::max<int64_t>(z.lat_mult / 2, 1) : 0;
+        l.lxcap = lattice ? ((Tu + 1) * z.capA + z.capF) * std::max<int64_t>(z.lat_mult / 2, 1) : 0;
         lx += l.lxcap;
         l.fo0 = fo;
         fo += Tu + 2;
@@ -317,47 +327,54 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.lattice = lattice ? 1 : 0;
     p.blank_id = o.blank_id;
     p.blank_thr = thr;
-    p.qcap = test_queue_cap();
     p.lds_fill = test_env_int("WFSTDEC_TEST_LDS_FILL", 1 << 30);
     p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1024);
-    p.capT = z.capT;
     p.capO = z.capO;
     WallTrace wt;
-    p.st = ws.get<UttState>(U);
-    UttLayout *d_lay = ws.get<UttLayout>(U);
-    p.lay = d_lay;
-    if (frame_kernels) {
-        p.tok = ws.get<uint64_t>(U * N);
-        p.pos = ws.get<int32_t>(U * 3 * N);
-        p.touched = ws.get<int32_t>(U * z.capT);
-        p.pk = ws.get<uint64_t>(U * z.capT);
-        p.ovf = ws.get<uint64_t>(U * z.capO);
-    } else {
-        p.capG = 8192;
-        while (p.capG < z.capT) p.capG *= 2;
-        p.gkeys = ws.get<uint32_t>(U * p.capG);
-        p.gvals = ws.get<unsigned long long>(U * p.capG);
-        p.gslots = ws.get<int32_t>(U * p.capG);
-        p.gspill = ws.get<uint2>(U * 2 * z.capO);
-        p.capC = z.capC;
-        p.cand = ws.get<int4>(U * p.capC);
+    UttLayout *d_lay = nullptr;
+    int64_t *fo_all = nullptr;
+    auto carve = [&](Arena &a) {
+        p.st = a.get<UttState>(U);
+        d_lay = a.get<UttLayout>(U);
+        p.lay = d_lay;
+        p.gkeys = a.get<uint32_t>(U * p.capG);
+        p.gvals = a.get<unsigned long long>(U * p.capG);
+        p.gslots = a.get<int32_t>(U * p.capG);
+        p.gspill = a.get<uint2>(U * 2 * p.capO);
+        p.cand = a.get<int4>(U * p.capC);
+        p.sv_state = a.get<int32_t>(sv);
+        p.sv_tok = a.get<uint64_t>(sv);
+        p.sv_prev = a.get<int32_t>(sv);
+        p.sv_ebeg = a.get<int32_t>(sv);
+        p.sv_epre = a.get<int32_t>(sv);
+        p.e_key = lattice ? a.get<uint32_t>(sv) : nullptr;
+        p.lat_e = lattice ? a.get<int4>(le) : nullptr;
+        p.lat_x = lattice ? a.get<int4>(lx) : nullptr;
+        p.ex_e = lattice ? a.get<float>(le) : nullptr;
+        p.ex_x = lattice ? a.get<float>(lx) : nullptr;
+        fo_all = a.get<int64_t>(4 * fo);
+        p.cut_arr = a.get<uint32_t>(fo);
+        p.kept = a.get<int32_t>(kp);
+        p.path_arc = a.get<int32_t>(pa);
+        p.path_frame = a.get<int32_t>(pa);
+    };
+    p.capG = 8192;
+    while (p.capG < z.capT) p.capG *= 2;
+    p.capO = z.capO;
+    p.capC = z.capC;
+    Arena measure;
+    carve(measure);
+    ArenaLease lease;
+    {
+        const hipError_t ae = lease.acquire(G.device, measure.off);
+        if (ae != hipSuccess) {
+            set_error("decode: workspace allocation of %zu bytes: %s", measure.off, hipGetErrorString(ae));
+            return ae == hipErrorOutOfMemory ? WFST_ENOMEM : WFST_EDEVICE;
+        }
     }
-    p.sv_state = ws.get<int32_t>(sv);
-    p.sv_tok = ws.get<uint64_t>(sv);
-    p.sv_prev = ws.get<int32_t>(sv);
-    p.sv_ebeg = ws.get<int32_t>(sv);
-    p.sv_epre = ws.get<int32_t>(sv);
-    p.e_key = lattice ? ws.get<uint32_t>(sv) : nullptr;
-    p.lat_e = lattice ? ws.get<int4>(le) : nullptr;
-    p.lat_x = lattice ? ws.get<int4>(lx) : nullptr;
-    p.ex_e = lattice ? ws.get<float>(le) : nullptr;
-    p.ex_x = lattice ? ws.get<float>(lx) : nullptr;
-    int64_t *fo_all = ws.get<int64_t>(4 * fo);
-    p.cut_arr = ws.get<uint32_t>(fo);
-    p.kept = ws.get<int32_t>(kp);
-    p.path_arc = ws.get<int32_t>(pa);
-    p.path_frame = ws.get<int32_t>(pa);
-    if (ws.err != hipSuccess) return hip_fail(ws.err, "decode: workspace allocation");
+    Arena arena;
+    arena.base = static_cast<char *>(lease.ptr);
+    carve(arena);
     wt.mark("allocate");
     p.sv_off = fo_all;
     p.le_off = fo_all + fo;
@@ -369,8 +386,6 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         std::memset(&st[u], 0, sizeof(UttState));
         st[u].ll = ll[u];
         st[u].T = T[u];
-        st[u].best = kEmptyKey;
-        st[u].hint = kEmptyKey;
     }
     hipError_t e = hipSuccess;
     auto chk = [&](hipError_t r) {
@@ -379,50 +394,15 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
     chk(hipMemsetAsync(fo_all, 0, 4 * fo * sizeof(int64_t), s));
-    if (frame_kernels) chk(launch_fill_u64(p.tok, U * N, kEmptyTok, s));
     chk(launch_classify(p, s));
-    chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
-    chk(hipStreamSynchronize(s));
-    if (e != hipSuccess) return hip_fail(e, "decode: setup");
+    // decoded frames are at most the frames: size the per-frame launches by T
     int Tmax = 0;
-    for (int u = 0; u < U; u++) Tmax = std::max(Tmax, st[u].Tp);
-    wt.mark("setup+classify");
+    for (int u = 0; u < U; u++) Tmax = std::max(Tmax, T[u]);
+    wt.mark("setup");
 
-    // grid size: one wave per 64 expected tokens
-    const int64_t est = o.max_active > 0 ? std::min<int64_t>(o.max_active, N) : std::min<int64_t>(N, z.capF);
-    auto clampg = [](int64_t g) { return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(g, 8192))); };
-    const int gE = std::min(clampg((U * est + 255) / 256), 1024);
-
-    // Frame loop.  Main stream: expand(k) -> prune(k).  Second stream:
-    // record(k) once prune(k) is done, overlapping expand(k+1)/prune(k+1).
-    // prune(k) overwrites the state->survivor map slot k mod 3 that
-    // record(k-3) and record(k-2) read, so it waits for record(k-2).
-    StreamHolder aux;
-    EventRing pruned(frame_kernels ? 4 : 0), recorded(frame_kernels ? 4 : 0);
-    if (!frame_kernels) {
-        tm.start(s);
-        chk(launch_utt(p, s));
-        tm.stop(PH_EXPAND, s);
-    } else {
-    chk(hipStreamCreateWithFlags(&aux.s, hipStreamNonBlocking));
-    hipStream_t s2 = aux.s;
-    for (int k = 0; k <= Tmax && e == hipSuccess; k++) {
-        tm.start(s);
-        chk(launch_expand(p, k, gE, s));
-        tm.stop(PH_EXPAND, s);
-        if (k >= 2) chk(hipStreamWaitEvent(s, recorded[k - 2], 0));
-        tm.start(s);
-        chk(launch_prune(p, k, s));
-        tm.stop(PH_PRUNE, s);
-        chk(hipEventRecord(pruned[k], s));
-        chk(hipStreamWaitEvent(s2, pruned[k], 0));
-        tm.start(s2);
-        chk(launch_record(p, k, gE, s2));
-        tm.stop(PH_RECORD, s2);
-        chk(hipEventRecord(recorded[k], s2));
-    }
-    chk(hipStreamWaitEvent(s, recorded[Tmax], 0));
-    }
+    tm.start(s);
+    chk(launch_search(p, s));
+    tm.stop(PH_SEARCH, s);
     tm.start(s);
     chk(launch_final(p, s));
     chk(launch_backtrace(p, s));
@@ -483,8 +463,8 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
             chk(hipMemcpyAsync(r->path_arcs.data(), p.path_arc + end - x.path_len, x.path_len * 4, hipMemcpyDeviceToHost, s));
             chk(hipMemcpyAsync(r->path_frames.data(), p.path_frame + end - x.path_len, x.path_len * 4, hipMemcpyDeviceToHost, s));
         }
-        r->stats.tokens = x.tokens;
-        r->stats.tokens_last = x.n_cur;
+        r->stats.tokens = x.n_tok;
+        r->stats.tokens_last = x.n_last;
         r->stats.arcs_expanded = x.arcs_expanded;
         r->stats.eps_arcs = x.eps_arcs;
         r->stats.lattice_raw = x.le_cnt + x.lx_cnt;
@@ -512,12 +492,12 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     wt.mark("copy results");
     if (e != hipSuccess) return hip_fail(e, "decode: results");
 
-    double ph[PH_COUNT] = {0, 0, 0, 0};
+    double ph[PH_COUNT] = {0, 0};
     int nexp = 0;
     for (const auto &x : tm.spans) {
         float ms = 0.0f;
         if (hipEventElapsedTime(&ms, x.a, x.b) == hipSuccess) ph[x.kind] += ms;
-        if (x.kind == PH_EXPAND) nexp++;
+        if (x.kind == PH_SEARCH) nexp++;
     }
     const double wall = std::chrono::duration<double, std::milli>(
                             std::chrono::steady_clock::now().time_since_epoch()).count() - t_start;
@@ -525,11 +505,9 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         wfst_result *r = out[u];
         r->kept.assign(kept_h.begin() + lay[u].kept0, kept_h.begin() + lay[u].kept0 + st[u].Tp);
         r->stats.decode_ms = wall;
-        r->stats.expand_ms = ph[PH_EXPAND];
-        r->stats.prune_ms = ph[PH_PRUNE];
-        r->stats.record_ms = ph[PH_RECORD];
+        r->stats.search_ms = ph[PH_SEARCH];
         r->stats.final_ms = ph[PH_FINAL];
-        r->stats.expand_launches = nexp;
+        r->stats.search_launches = nexp;
         if ((o.flags & WFST_RECORD_TOKENS) && r->status == WFST_OK) {
             // token sets sorted by state for the caller
             const int Tp = st[u].Tp;
@@ -588,7 +566,6 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
                                                : static_cast<float>(std::log(static_cast<double>(o.blank_threshold)));
 
     DeviceGuard dg(G.device);
-    keep_pool_memory(G.device);
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
 
     std::vector<const float *> ll(loglikes, loglikes + n_utt);
@@ -629,20 +606,29 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
     z.capC = std::min<int64_t>(G.d.n_emit + 1, std::max<int64_t>(2 * z.capT, 65536));
     z.capO = std::min<int64_t>(E + 1, std::max<int64_t>(2 * z.capT, 65536));
     z.lat_mult = 2;
+    // average tokens per frame: start from what the last calls needed
+    static std::atomic<int64_t> learned_capA{2048};
+    z.capA = std::min<int64_t>(z.capF, learned_capA.load());
     int rc = WFST_ECAPACITY;
-    for (int attempt = 0; attempt < 6 && rc == WFST_ECAPACITY; attempt++) {
+    for (int attempt = 0; attempt < 8 && rc == WFST_ECAPACITY; attempt++) {
         if (attempt) {
             for (int u = 0; u < n_utt; u++) {
                 delete res[u];
                 res[u] = new (std::nothrow) wfst_result();
             }
-            z.capF = std::min<int64_t>(N, z.capF * 2);
-            z.capT = std::min<int64_t>(N, z.capT * 2);
+            z.capF = std::min<int64_t>(N, z.capF * 4);
+            z.capA = std::min<int64_t>(z.capF, z.capA * 4);
+            z.capT = std::min<int64_t>(N, z.capT * 4);
             z.capO = std::min<int64_t>(E + 1, z.capO * 2);
             z.capC = std::min<int64_t>(G.d.n_emit + 1, z.capC * 2);
             z.lat_mult *= 2;
         }
         rc = run_batch(G, n_utt, ll.data(), T, L, o, thr, s, z, res, t0);
+    }
+    if (rc == WFST_OK) {
+        int64_t cur = learned_capA.load();
+        while (z.capA > cur && !learned_capA.compare_exchange_weak(cur, z.capA)) {
+        }
     }
     if (rc != WFST_OK) {
         for (int u = 0; u < n_utt; u++) delete res[u];

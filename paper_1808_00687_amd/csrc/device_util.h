@@ -121,41 +121,6 @@ __device__ __forceinline__ void set_status(UttState &st, int code)
     atomicCAS(&st.status, 0, code);
 }
 
-// Utterance u takes part in producing token set k.
-__device__ __forceinline__ bool live(const UttState &st, int k)
-{
-    return st.status == 0 && k <= st.Tp;
-}
-
-// Flattened chunk space over utterances: utterance u owns ceil(n_u / per)
-// chunks.  For a group of up to 64 utterances starting at grp, each lane
-// holds its utterance's inclusive chunk prefix.
-struct ChunkGroup {
-    int incl;     // inclusive prefix of this lane's utterance
-    int cnt;      // chunks of this lane's utterance
-    int total;    // chunks in the group
-};
-
-__device__ __forceinline__ ChunkGroup chunk_group(int n_u, int per)
-{
-    ChunkGroup g;
-    g.cnt = (n_u + per - 1) / per;
-    g.incl = wave_incl_scan(g.cnt);
-    g.total = __shfl(g.incl, kWave - 1, kWave);
-    return g;
-}
-
-// For chunk c (wave-uniform, < total) of the group: the lane (utterance
-// offset inside the group) that owns it, and the chunk index inside it.
-__device__ __forceinline__ void chunk_locate(const ChunkGroup &g, int c, int &ul, int &ci)
-{
-    uint64_t m = __ballot(g.incl <= c);
-    ul = __popcll(m);
-    int incl = __shfl(g.incl, ul, kWave);
-    int cnt = __shfl(g.cnt, ul, kWave);
-    ci = c - (incl - cnt);
-}
-
 // Block-wide exclusive scan of one int per thread (blockDim.x a multiple of
 // 64, at most 1024).  `sh` needs 17 ints.  Returns the exclusive prefix and
 // stores the block total in *total.

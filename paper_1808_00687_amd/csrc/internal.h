@@ -27,7 +27,6 @@ constexpr uint32_t kDstMask = 0x7FFFFFFFu;
 constexpr int kHistBits = 12;               // radix-select digit width
 constexpr int kHistBins = 1 << kHistBits;   // bins per utterance histogram
 constexpr int kWave = 64;                   // gfx950 wavefront
-constexpr int kQueueCap = 256;              // per-wave LDS epsilon queue (items)
 
 struct DevGraph {
     int32_t n;
@@ -52,31 +51,19 @@ struct Graph {
     void *mem;   // single device allocation holding every array
 };
 
-// Per-utterance decode state in device memory.  Fields marked "frame" are
-// reset by the advance kernel after each produced token set.
+// Per-utterance decode state in device memory.
 struct UttState {
     const float *ll;      // [T x L] log-likelihoods (device)
     int32_t T;
     int32_t Tp;           // decoded frames (set by the classify kernel)
     int32_t status;       // WFST_OK, WFST_ENOPATH or WFST_ECAPACITY
     int32_t gframes;      // frames whose token table overflowed LDS (redone in device memory)
-    // frame
-    uint32_t best;        // minimum cost key among candidates of the set in production
-    int32_t ntouched;     // states holding a token in the set in production
-    int32_t pad3;
-    uint32_t cut;         // pruning cutoff key of the set in production
-    int32_t n_new;        // survivors appended for the set in production
-    int32_t ovf;          // epsilon items spilled to the overflow list
-    // previous set
-    int32_t n_cur;        // |S_{k-1}|
-    int32_t n_arcs;       // emitting out-arcs of S_{k-1} (the next expansion's work)
-    uint32_t hint;        // key of one candidate cost of the next expansion (early-drop seed)
-    int32_t pad2;
-    // cumulative
-    int64_t sv_base;      // survivor index where the set in production starts
-    int64_t le_cnt;       // emitting lattice records so far
-    int64_t lx_cnt;       // epsilon lattice records so far
-    int64_t tokens;
+    // written by the search kernel when it ends
+    int32_t n_last;       // |S_T'|
+    int32_t pad0;
+    int64_t n_tok;        // survivors of all token sets
+    int64_t le_cnt;       // emitting lattice records
+    int64_t lx_cnt;       // epsilon lattice records
     int64_t arcs_expanded;
     int64_t eps_arcs;
     // final
@@ -111,19 +98,10 @@ struct Params {
     int32_t lattice;
     int32_t blank_id;
     float blank_thr;
-    int32_t qcap;             // effective per-wave queue capacity (<= kQueueCap)
-    int32_t pad;
+    int32_t lds_fill;         // states per frame the LDS token table takes (<= its fill limit)
+    int32_t gen_lds;          // epsilon items per generation kept in LDS (<= its capacity)
     UttState *st;
     const UttLayout *lay;
-    // dense per-utterance tables, U x N
-    uint64_t *tok;
-    int32_t *pos;             // U x 3 x N: survivor index of each state of S_k, slot k mod 3
-    // per-frame scratch, U x capT
-    int32_t *touched;
-    uint64_t *pk;
-    int64_t capT;
-    uint64_t *ovf;            // U x capO overflow epsilon items (state << 32 | cost bits)
-    int64_t capO;
     // survivors (per utterance regions)
     int32_t *sv_state;
     uint64_t *sv_tok;
@@ -146,31 +124,25 @@ struct Params {
     int32_t *kept;
     int32_t *path_arc;
     int32_t *path_frame;
-    // whole-utterance kernel: per-utterance token table in device memory
-    // (frames that overflow LDS), epsilon item spill lists, candidate lists
+    // search scratch per utterance: token table in device memory (frames that
+    // overflow LDS), epsilon item spill lists, emitting candidate lists
     uint32_t *gkeys;          // U x capG
     unsigned long long *gvals;
     int32_t *gslots;
     int64_t capG;             // power of two
-    uint2 *gspill;            // U x 2 x capO
+    uint2 *gspill;            // U x 2 x capO {table slot, cost bits}
+    int64_t capO;
     int4 *cand;               // U x capC {src survivor, user arc, cost bits, table slot}
     int64_t capC;
-    int32_t lds_fill;         // states per frame the LDS table takes (<= its fill limit)
-    int32_t gen_lds;          // epsilon items per generation kept in LDS (<= its capacity)
 };
 
-// ---- launchers (search_kernels.hip / final_kernels.hip) ----
-hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s);
-hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);
+// ---- launchers (search_kernel.hip / final_kernels.hip) ----
 hipError_t launch_classify(const Params &p, hipStream_t s);
-hipError_t launch_expand(const Params &p, int k, int grid, hipStream_t s);
-hipError_t launch_prune(const Params &p, int k, hipStream_t s);
-hipError_t launch_record(const Params &p, int k, int grid, hipStream_t s);
+hipError_t launch_search(const Params &p, hipStream_t s);
 hipError_t launch_final(const Params &p, hipStream_t s);
 hipError_t launch_backtrace(const Params &p, hipStream_t s);
 hipError_t launch_lattice_backward(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
-hipError_t launch_utt(const Params &p, hipStream_t s);
 
 // ---- host helpers (graph.cpp) ----
 void set_error(const char *fmt, ...);

@@ -1,4 +1,4 @@
-// Whole-utterance search kernel: one 1024-thread workgroup per utterance
+// Search kernel: one 1024-thread workgroup per utterance
 // loops over every decoded frame of its utterance (token passing, Sec. 3;
 // the per-frame Viterbi beam search of Alg. 1, with the lattice records of
 // exact lattice generation, Sec. 1 and Sec. 3).
@@ -96,7 +96,7 @@ struct Run {
     int n_prev;          // |S_{k-1}|
     int a_prev;          // emitting out-arcs of S_{k-1}
     int64_t lat_e, lat_x;
-    int64_t tokens, arcs;
+    int64_t arcs;
     int gframes;
     long long eps;       // epsilon out-arcs of survivors (this thread's share)
 };
@@ -646,7 +646,6 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     run.lat_e += sh.nlat_e;
     run.lat_x += sh.nlat_x;
     if (sh.status) return sh.status;
-    run.tokens += ns;
     if (k < Tp) run.arcs += a_kept;
     run.prev0 = set0;
     run.set0 = set0 + ns;
@@ -663,7 +662,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     return 0;
 }
 
-__global__ __launch_bounds__(kT) void utt_kernel(Params p)
+__global__ __launch_bounds__(kT) void search_kernel(Params p)
 {
     __shared__ uint32_t s_keys[kSlots];
     __shared__ unsigned long long s_vals[kSlots];
@@ -739,11 +738,10 @@ __global__ __launch_bounds__(kT) void utt_kernel(Params p)
     if (lane_id() == 0 && e) atomicAdd(&sh.eps_sum, static_cast<unsigned long long>(e));
     __syncthreads();
     if (tid == 0) {
-        st.sv_base = run.set0;
-        st.n_cur = run.n_prev;
+        st.n_tok = run.set0;
+        st.n_last = run.n_prev;
         st.le_cnt = run.lat_e;
         st.lx_cnt = run.lat_x;
-        st.tokens = run.tokens;
         st.arcs_expanded = run.arcs;
         st.eps_arcs = static_cast<int64_t>(sh.eps_sum);
         st.gframes = run.gframes;
@@ -751,11 +749,40 @@ __global__ __launch_bounds__(kT) void utt_kernel(Params p)
     }
 }
 
+// isBlankFrame (Sec. 2, Alg. 1): frame t is blank when its blank
+// log-likelihood exceeds the threshold (log domain); the kept frames are
+// compacted in order, one workgroup per utterance.
+__global__ __launch_bounds__(256) void classify_kernel(Params p)
+{
+    __shared__ int sh_scan[17];
+    const int u = blockIdx.x;
+    UttState &st = p.st[u];
+    const UttLayout &ly = p.lay[u];
+    const int T = st.T;
+    int base = 0;
+    for (int t0 = 0; t0 < T; t0 += blockDim.x) {
+        const int t = t0 + threadIdx.x;
+        int keep = 0;
+        if (t < T) keep = !(st.ll[static_cast<int64_t>(t) * p.L + p.blank_id] > p.blank_thr);
+        int total;
+        const int ex = block_excl_scan(keep, sh_scan, &total);
+        if (keep) p.kept[ly.kept0 + base + ex] = t;
+        base += total;
+    }
+    if (threadIdx.x == 0) st.Tp = base;
+}
+
 }  // namespace
 
-hipError_t launch_utt(const Params &p, hipStream_t s)
+hipError_t launch_classify(const Params &p, hipStream_t s)
 {
-    hipLaunchKernelGGL(utt_kernel, dim3(p.U), dim3(kT), 0, s, p);
+    hipLaunchKernelGGL(classify_kernel, dim3(p.U), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_search(const Params &p, hipStream_t s)
+{
+    hipLaunchKernelGGL(search_kernel, dim3(p.U), dim3(kT), 0, s, p);
     return hipGetLastError();
 }
 

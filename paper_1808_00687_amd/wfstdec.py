@@ -54,9 +54,8 @@ class _Info(C.Structure):
 class _Stats(C.Structure):
     _fields_ = [("frames", C.c_int32), ("frames_decoded", C.c_int32), ("tokens", C.c_int64),
                 ("tokens_last", C.c_int64), ("arcs_expanded", C.c_int64), ("eps_arcs", C.c_int64), ("lattice_raw", C.c_int64),
-                ("lattice_kept", C.c_int64), ("decode_ms", C.c_double), ("expand_ms", C.c_double),
-                ("prune_ms", C.c_double), ("record_ms", C.c_double), ("final_ms", C.c_double),
-                ("expand_launches", C.c_int32)]
+                ("lattice_kept", C.c_int64), ("decode_ms", C.c_double), ("search_ms", C.c_double),
+                ("final_ms", C.c_double), ("search_launches", C.c_int32)]
 
 
 class _LatArc(C.Structure):

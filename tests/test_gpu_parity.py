@@ -162,13 +162,15 @@ def test_device_memory_table_path(dec, torch_mod, oracle_mod, cfg2, fill):
         parity.assert_same(ro, rg, lattice=True, tag="device table fill %d seed %d" % (fill, seed))
 
 
-def test_per_frame_kernel_path(dec, torch_mod, oracle_mod, cfg2):
-    # the alternative schedule: one expand / prune / record launch per frame
+def test_capacity_retry(dec, torch_mod, oracle_mod, cfg2):
+    # a capacity hint of 8 tokens per frame overflows the survivor, lattice,
+    # table and candidate buffers: the library grows them and decodes again
     wl, gh = cfg2
-    with _env(WFSTDEC_FRAME_KERNELS=1):
-        ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:120], gh=gh, beam=13.0,
-                      max_active=7000, lattice_beam=8.0)
-    parity.assert_same(ro, rg, lattice=True, tag="per-frame kernels")
+    ll = wl.loglikes[0][:50]
+    ro = oracle_mod.decode(wl.graph, ll, 13.0, 7000, 8.0)
+    rg = dec.wfst_decode(gh, to_dev(torch_mod, ll), beam=13.0, max_active=7000, lattice_beam=8.0,
+                         record_tokens=True, capacity_hint=8)
+    parity.assert_same(ro, rg, lattice=True, tag="capacity retry")
 
 
 def test_determinism(dec, torch_mod, cfg2):
