@@ -57,25 +57,32 @@ __device__ __forceinline__ uint64_t lanemask_lt() { return (1ull << lane_id()) -
 
 __device__ __forceinline__ int rank_in(uint64_t mask) { return __popcll(mask & lanemask_lt()); }
 
+// Wave-wide inclusive sum with DPP lane moves (no LDS traffic): a
+// Kogge-Stone scan inside each row of 16 lanes, then row 0's total into row
+// 1 (and row 2's into row 3) and lane 31's into rows 2-3.  Lanes whose
+// source lies outside the row read the identity.  Called by the whole wave.
 __device__ __forceinline__ int wave_incl_scan(int x)
 {
-    const int lane = lane_id();
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        int y = __shfl_up(x, d, kWave);
-        if (lane >= d) x += y;
-    }
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31
     return x;
 }
 
+// Wave-wide minimum (unsigned), the same lane moves; the result is lane 63's.
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x)
 {
-#pragma unroll
-    for (int d = kWave / 2; d > 0; d >>= 1) {
-        uint32_t y = __shfl_xor(x, d, kWave);
-        x = y < x ? y : x;
-    }
-    return x;
+    const int id = -1;   // identity: 0xFFFFFFFF
+    x = min(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(id, static_cast<int>(x), 0x111, 0xf, 0xf, false)));
+    x = min(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(id, static_cast<int>(x), 0x112, 0xf, 0xf, false)));
+    x = min(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(id, static_cast<int>(x), 0x114, 0xf, 0xf, false)));
+    x = min(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(id, static_cast<int>(x), 0x118, 0xf, 0xf, false)));
+    x = min(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(id, static_cast<int>(x), 0x142, 0xa, 0xf, false)));
+    x = min(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(id, static_cast<int>(x), 0x143, 0xc, 0xf, false)));
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x), kWave - 1));
 }
 
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t x)

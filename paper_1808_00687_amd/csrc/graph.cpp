@@ -80,7 +80,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     const int64_t n_emit = e - n_eps;
 
     std::vector<int32_t> eoff, xoff, arc_src;
-    std::vector<int4> earc, xarc;
+    std::vector<int4> earc, xarc, srec;
     std::vector<uint8_t> has_eps;
     int32_t depth = 0;
     try {
@@ -136,6 +136,11 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
                 arc_src[a] = s | static_cast<int32_t>(0x80000000u);
             }
         }
+        srec.assign(2 * static_cast<size_t>(n), make_int4(0, 0, 0, 0));
+        for (int32_t s = 0; s < n; s++) {
+            srec[2 * static_cast<size_t>(s)] = make_int4(eoff[s], eoff[s + 1], xoff[s], xoff[s + 1]);
+            if (xoff[s + 1] > xoff[s]) srec[2 * static_cast<size_t>(s) + 1] = xarc[xoff[s]];
+        }
     } catch (const std::bad_alloc &) {
         return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
     }
@@ -147,7 +152,8 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     const size_t b_xarc = align(static_cast<size_t>(n_eps) * 16 + 16);
     const size_t b_src = align(static_cast<size_t>(e) * 4 + 4);
     const size_t b_fin = final_weight ? align(static_cast<size_t>(n) * 4) : 0;
-    const size_t total = b_eoff + b_xoff + b_earc + b_xarc + b_src + b_fin;
+    const size_t b_srec = align(static_cast<size_t>(n) * 32);
+    const size_t total = b_eoff + b_xoff + b_earc + b_xarc + b_src + b_fin + b_srec;
 
     wfst_graph *h = new (std::nothrow) wfst_graph();
     if (!h) return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
@@ -181,6 +187,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     g.d.xarc = static_cast<const int4 *>(put(xarc.data(), xarc.size() * 16, b_xarc));
     g.d.arc_src = static_cast<const int32_t *>(put(arc_src.data(), arc_src.size() * 4, b_src));
     g.d.final_w = final_weight ? static_cast<const float *>(put(final_weight, static_cast<size_t>(n) * 4, b_fin)) : nullptr;
+    g.d.srec = static_cast<const int4 *>(put(srec.data(), srec.size() * 16, b_srec));
     if (err != hipSuccess) {
         (void)hipFree(mem);
         delete h;

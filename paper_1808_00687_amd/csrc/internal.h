@@ -7,6 +7,10 @@
 //              {dst | has_eps << 31, weight bits, user arc, 0}
 //   arc_src[E] user arc -> src state | is_epsilon << 31 (cold, back-pointers)
 //   final_w[N] final costs or null
+//   srec[2N]   32-byte state records: the state's emitting and epsilon row
+//              offsets, then a copy of its first epsilon record (zeros if
+//              none), so that one load gives a state's rows and, for the
+//              common single-epsilon state, its epsilon arc
 // Each state's arcs keep their user order inside the emitting and the
 // epsilon partition.  has_eps marks a destination with epsilon out-arcs, so a
 // kernel that lowers its token knows without another load whether the
@@ -39,6 +43,7 @@ struct DevGraph {
     const int4 *xarc;
     const int32_t *arc_src;
     const float *final_w;
+    const int4 *srec;   // 2 x N: {eoff[s], eoff[s+1], xoff[s], xoff[s+1]}, first epsilon record of s
 };
 
 // Host-side graph object behind the opaque wfst_graph handle.

@@ -1,26 +1,32 @@
-// Search kernel: one 1024-thread workgroup per utterance
-// loops over every decoded frame of its utterance (token passing, Sec. 3;
-// the per-frame Viterbi beam search of Alg. 1, with the lattice records of
-// exact lattice generation, Sec. 1 and Sec. 3).
+// Search kernel: one 1024-thread workgroup per utterance loops over every
+// decoded frame of its utterance (token passing, Sec. 3; the per-frame
+// Viterbi beam search of Alg. 1, with the lattice records of exact lattice
+// generation, Sec. 1 and Sec. 3).
 //
 // Frame k (token set S_k) in one workgroup:
-//   1. expansion of the emitting arcs of S_{k-1}, 64 arcs per wave, found by a
-//      64-ary search over the set's emitting-arc prefix; the frame's tokens
-//      live in a hash table in LDS (state -> packed token), recombination is
-//      an LDS 64-bit atomicMin on (cost key, arc + 1), the first touch of a
-//      state appends its slot to a slot list;
+//   1. expansion of the emitting arcs of S_{k-1}: each wave takes chunks of
+//      64 consecutive arcs of the set, finds their tokens by a 64-ary search
+//      over the set's emitting-arc prefix (kept in LDS for sets of up to
+//      kSetCache tokens) and issues the loads of two chunks together.  The
+//      frame's tokens live in a hash table in LDS (state -> packed token);
+//      recombination is an LDS 64-bit atomicMin on (cost key, arc + 1), the
+//      first touch of a state appends its slot to a slot list;
 //   2. epsilon closure, generation by generation: every lowered token whose
-//      state has epsilon out-arcs is relaxed again until nothing changes;
+//      state has epsilon out-arcs is relaxed again until nothing changes (a
+//      state's first epsilon arc comes with its 32-byte state record);
 //   3. pruning: beam limit from the frame's best cost key and, when more
 //      tokens lie within it than max_active, the exact max_active-th
 //      smallest key by radix select over an LDS histogram;
-//   4. compaction of the survivors into S_k (device memory) in slot-list
-//      order, with the prefix of their emitting out-degrees;
+//   4. compaction of the survivors into S_k (device memory, and LDS for the
+//      next expansion) in slot-list order, with the prefix of their
+//      emitting out-degrees;
 //   5. back-pointer survivor indices and lattice records;
 //   6. clearing of the table.
 // A frame that reaches more states than the LDS table holds is redone with
 // the same code on a table in device memory.  Every table is private to its
 // workgroup: no device-scope synchronisation and no per-frame launches.
+#include <type_traits>
+
 #include "device_util.h"
 
 namespace wfd {
@@ -33,7 +39,9 @@ constexpr int kSlotBits = 13;
 constexpr int kSlots = 1 << kSlotBits;    // LDS hash slots
 constexpr int kFill = 6144;               // LDS states per frame before falling back to device memory
 constexpr int kGenCap = 1024;             // LDS epsilon items per generation
+constexpr int kSetCache = 3008;           // tokens of the previous set kept in LDS for the expansion
 constexpr int kRun = 2;                   // slot-list entries per thread per compaction pass
+constexpr int kChunks = 2;                // 64-arc chunks a wave has in flight in the expansion
 constexpr int kOverflow = 1;              // frame result: the table filled up
 
 static_assert(kHistBins * 4 <= 2 * kGenCap * 8, "the select histogram aliases the epsilon buffers");
@@ -59,15 +67,34 @@ __device__ __forceinline__ T tld(const T *ptr)
         return *ptr;
 }
 
+// Barrier that orders LDS only: device-memory stores issued before it need
+// not be complete.  Used where no other wave reads those stores before a
+// full barrier.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// With the table in device memory its own stores need the full barrier.
+template <bool G>
+__device__ __forceinline__ void table_barrier()
+{
+    if constexpr (G) __syncthreads();
+    else lds_barrier();
+}
+
 // Token table of one frame: keys = state (kEmptyKey if free), vals = packed
 // token (kEmptyTok if none).  After compaction a surviving slot's val holds
 // (user arc + 1) << 32 | survivor index, a pruned one kEmptyTok.  `slots`
 // lists the claimed slots in claim order.
 template <bool G>
 struct Tab {
+    using Slot = typename std::conditional<G, int32_t, uint16_t>::type;
     uint32_t *keys;
     unsigned long long *vals;
-    int32_t *slots;
+    Slot *slots;
     uint32_t mask;
     int fill;
     int shift;   // 32 - log2(slots)
@@ -114,29 +141,6 @@ __device__ __forceinline__ int tab_find(const Tab<G> &t, uint32_t d)
     return -1;
 }
 
-// Slot of state d, claimed if new; -1 (and the overflow flag) if none is free.
-template <bool G>
-__device__ __forceinline__ int tab_claim(const Tab<G> &t, Sh &sh, uint32_t d)
-{
-    uint32_t h = hash_state(d) >> t.shift;
-    for (uint32_t probe = 0; probe <= t.mask; probe++) {
-        uint32_t k = tld<G>(t.keys + h);
-        if (k == kEmptyKey) {
-            k = atomicCAS(t.keys + h, kEmptyKey, d);
-            if (k == kEmptyKey) {
-                const int idx = atomicAdd(&sh.nslots, 1);
-                if (idx < t.fill) t.slots[idx] = static_cast<int32_t>(h);
-                else sh.overflow = 1;
-                return static_cast<int>(h);
-            }
-        }
-        if (k == d) return static_cast<int>(h);
-        h = (h + 1) & t.mask;
-    }
-    sh.overflow = 1;
-    return -1;
-}
-
 // Offer one candidate token per lane (act) to the table; lowered tokens of
 // states with epsilon out-arcs become items of generation `gen`.  Called by
 // the whole wave; returns the lane's slot or -1.
@@ -144,23 +148,48 @@ template <bool G>
 __device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, uint2 *lgen, int glds, uint2 *sgen, int gcap, int gen,
                                      bool act, uint32_t d, bool d_eps, float cand, uint32_t key, int32_t arc)
 {
-    bool impr = false;
+    // slot of state d: a compare-and-swap on the key claims a free slot or
+    // finds the state's own
     int slot = -1;
+    bool claimed = false;
     if (act) {
-        slot = tab_claim<G>(t, sh, d);
-        if (slot >= 0) {
-            const unsigned long long v = make_tok(key, arc);
-            impr = v < atomicMin(t.vals + slot, v);
+        uint32_t h = hash_state(d) >> t.shift;
+        for (uint32_t probe = 0; probe <= t.mask; probe++) {
+            const uint32_t k = atomicCAS(t.keys + h, kEmptyKey, d);
+            if (k == kEmptyKey || k == d) {
+                slot = static_cast<int>(h);
+                claimed = k == kEmptyKey;
+                break;
+            }
+            h = (h + 1) & t.mask;
         }
     }
+    // newly claimed slots join the slot list, one LDS add per wave
+    const uint64_t mc = __ballot(claimed);
+    if (mc) {
+        int b = 0;
+        if (lane_id() == 0) b = atomicAdd(&sh.nslots, __popcll(mc));
+        b = __builtin_amdgcn_readlane(b, 0);
+        if (claimed) {
+            const int idx = b + rank_in(mc);
+            if (idx < t.fill) t.slots[idx] = static_cast<typename Tab<G>::Slot>(slot);
+            else sh.overflow = 1;
+        }
+    }
+    if (act && slot < 0) sh.overflow = 1;
+    bool impr = false;
+    if (slot >= 0) {
+        const unsigned long long v = make_tok(key, arc);
+        impr = v < atomicMin(t.vals + slot, v);
+    }
     const uint32_t mk = wave_min_u32(impr ? key : kEmptyKey);
-    if (lane_id() == 0 && mk < sh.best) atomicMin(&sh.best, mk);
+    if (lane_id() == 0 && mk != kEmptyKey) atomicMin(&sh.best, mk);
     const bool push = impr && d_eps;
     const uint64_t m = __ballot(push);
     if (m) {
         int b = 0;
         if (lane_id() == 0) b = atomicAdd(&sh.gen_n[gen], __popcll(m));
-        b = __shfl(b, 0, kWave);
+        b = __builtin_amdgcn_readlane(b, 0);
         if (push) {
             const int idx = b + rank_in(m);
             const uint2 it = make_uint2(static_cast<uint32_t>(slot), __float_as_uint(cand));
@@ -261,11 +290,121 @@ __device__ __forceinline__ void put_record(int4 *buf, int64_t cap, int64_t base,
     if (!m) return;
     int b = 0;
     if (lane_id() == 0) b = atomicAdd(cnt, __popcll(m));
-    b = __shfl(b, 0, kWave);
+    b = __builtin_amdgcn_readlane(b, 0);
     if (rec) {
         const int64_t idx = base + b + rank_in(m);
         if (idx < cap) buf[idx] = r;
         else sh.status = WFST_ECAPACITY;
+    }
+}
+
+// The expansion's view of S_{k-1}: token costs, emitting-arc prefix and
+// first emitting record of each token's state, in LDS (sets of at most
+// kSetCache tokens) or in the survivor arrays.
+template <bool L>
+struct SetView;
+
+template <>
+struct SetView<true> {
+    const float *cost;
+    const int32_t *epre;
+    const int32_t *ebeg;
+    __device__ float c(int i) const { return cost[i]; }
+};
+
+template <>
+struct SetView<false> {
+    const uint64_t *tok;
+    const int32_t *epre;
+    const int32_t *ebeg;
+    __device__ float c(int i) const { return tok_cost(tok[i]); }
+};
+
+// Emitting expansion of S_{k-1} into the table (step 1).  Every offered
+// candidate is listed: it gives the back-pointer of its destination when it
+// wins, and an emitting lattice arc.
+template <bool G, bool L>
+__device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh, const SetView<L> &v, int n_tok,
+                                       int A, int src0, const float *row, uint2 *aux, int glds, uint2 *spill,
+                                       int gcap, int4 *cand, int capC)
+{
+    const int lane = lane_id();
+    const int wid = threadIdx.x / kWave;
+    for (int c = wid * kChunks; c * kWave < A; c += kW * kChunks) {
+        int ob[kChunks], op[kChunks], ot[kChunks], a[kChunks];
+        float oc[kChunks];
+        bool ok[kChunks];
+#pragma unroll
+        for (int r = 0; r < kChunks; r++) {
+            const int a0 = (c + r) * kWave;
+            a[r] = a0 + lane;
+            ok[r] = false;
+            ob[r] = op[r] = ot[r] = 0;
+            oc[r] = 0.0f;
+            if (a0 < A) {
+                // the 64 tokens from the one owning a0, and each lane's owner among them
+                const int t0 = search_le(v.epre, n_tok, a0);
+                const int tt = t0 + lane;
+                int pre = 0x7FFFFFFF, eb = 0;
+                float cst = 0.0f;
+                if (tt < n_tok) {
+                    pre = v.epre[tt];
+                    eb = v.ebeg[tt];
+                    cst = v.c(tt);
+                }
+                const int win_end = t0 + kWave < n_tok ? v.epre[t0 + kWave] : A;
+                const int o = owner_lane(pre, a[r]);
+                ob[r] = __shfl(eb, o, kWave);
+                op[r] = __shfl(pre, o, kWave);
+                oc[r] = __shfl(cst, o, kWave);
+                ot[r] = t0 + o;
+                ok[r] = a[r] < A;
+                if (ok[r] && a[r] >= win_end) {
+                    // past the window (tokens without emitting arcs): search the rest
+                    int lo = t0 + kWave, hi = n_tok - 1;
+                    while (lo < hi) {
+                        const int mid = (lo + hi + 1) >> 1;
+                        if (v.epre[mid] <= a[r]) lo = mid;
+                        else hi = mid - 1;
+                    }
+                    ob[r] = v.ebeg[lo];
+                    op[r] = v.epre[lo];
+                    oc[r] = v.c(lo);
+                    ot[r] = lo;
+                }
+                ok[r] = ok[r] && op[r] <= a[r];
+            }
+        }
+        int4 rec[kChunks];
+#pragma unroll
+        for (int r = 0; r < kChunks; r++) rec[r] = ok[r] ? p.g.earc[ob[r] + (a[r] - op[r])] : make_int4(0, 0, 0, 0);
+        float lv[kChunks];
+#pragma unroll
+        for (int r = 0; r < kChunks; r++) lv[r] = ok[r] ? ldg(row + rec[r].y) : 0.0f;
+#pragma unroll
+        for (int r = 0; r < kChunks; r++) {
+            const uint32_t bnd = drop_bound(sh.best, p.beam);
+            const float t1 = oc[r] + __int_as_float(rec[r].z);
+            const float cnd = t1 - lv[r];
+            const uint32_t key = okey(cnd);
+            const bool act = ok[r] && key <= bnd;
+            const int slot = offer<G>(t, sh, aux, glds, spill, gcap, 0, act, static_cast<uint32_t>(rec[r].x) & kDstMask,
+                                      rec[r].x < 0, cnd, key, rec[r].w);
+            const bool keep = act && slot >= 0;
+            const uint64_t m = __ballot(keep);
+            if (m) {
+                int b = 0;
+                if (lane == 0) b = atomicAdd(&sh.ncand, __popcll(m));
+                b = __builtin_amdgcn_readlane(b, 0);
+                if (keep) {
+                    const int idx = b + rank_in(m);
+                    if (idx < capC)
+                        cand[idx] = make_int4(src0 + ot[r], rec[r].w, __float_as_int(cnd), slot);
+                    else
+                        sh.status = WFST_ECAPACITY;
+                }
+            }
+        }
     }
 }
 
@@ -274,8 +413,8 @@ __device__ __forceinline__ void put_record(int4 *buf, int64_t cap, int64_t base,
 // a negative WFST error.  Every return is taken by the whole workgroup.
 template <bool G>
 __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
-                                     const Tab<G> &t, uint2 *aux, uint2 *spill, int gcap, int4 *cand,
-                                     int capC, Run &run, int k)
+                                     const Tab<G> &t, uint2 *aux, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
+                                     uint2 *spill, int gcap, int4 *cand, int capC, Run &run, int k)
 {
     const int tid = threadIdx.x;
     const int lane = lane_id();
@@ -298,74 +437,23 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     if (k == 0) {
         if (wid == 0) {
             const int s = p.g.start;
-            (void)offer<G>(t, sh, aux, glds, spill, gcap, 0, lane == 0, static_cast<uint32_t>(s),
-                           p.g.xoff[s + 1] > p.g.xoff[s], 0.0f, okey(0.0f), -1);
+            const int4 lo = p.g.srec[2 * static_cast<int64_t>(s)];
+            (void)offer<G>(t, sh, aux, glds, spill, gcap, 0, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0.0f,
+                           okey(0.0f), -1);
         }
     } else {
-        const int n_tok = run.n_prev;
-        const int A = run.a_prev;
-        const int64_t base = ly.sv0 + run.prev0;
-        const int32_t *epre = p.sv_epre + base;
-        const int32_t *ebeg = p.sv_ebeg + base;
-        const uint64_t *tok = p.sv_tok + base;
         const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k - 1]) * p.L;
-        for (int a0 = wid * kWave; a0 < A; a0 += kT) {
-            const int a_end = min(a0 + kWave, A);
-            int t0 = search_le(epre, n_tok, a0);
-            int done = a0;
-            while (done < a_end) {
-                const int tt = t0 + lane;
-                int pre = 0x7FFFFFFF, eb = 0;
-                float cst = 0.0f;
-                if (tt < n_tok) {
-                    pre = epre[tt];
-                    eb = ebeg[tt];
-                    cst = tok_cost(tok[tt]);
-                }
-                const int win_end = t0 + kWave < n_tok ? epre[t0 + kWave] : A;
-                const int hi = min(a_end, win_end);
-                const int a = done + lane;
-                const int o = owner_lane(pre, a);
-                const int ob = __shfl(eb, o, kWave);
-                const int op = __shfl(pre, o, kWave);
-                const float oc = __shfl(cst, o, kWave);
-                const uint32_t bnd = drop_bound(sh.best, p.beam);
-                bool act = false, d_eps = false;
-                uint32_t d = 0, key = kEmptyKey;
-                int arc = 0;
-                float cnd = 0.0f;
-                if (a < hi && op <= a) {
-                    const int4 r = p.g.earc[ob + (a - op)];
-                    d = static_cast<uint32_t>(r.x) & kDstMask;
-                    d_eps = r.x < 0;
-                    arc = r.w;
-                    const float t1 = oc + __int_as_float(r.z);
-                    cnd = t1 - ldg(row + r.y);
-                    key = okey(cnd);
-                    act = key <= bnd;
-                }
-                const int slot = offer<G>(t, sh, aux, glds, spill, gcap, 0, act, d, d_eps, cnd, key, arc);
-                // every offered candidate is listed: it gives the back-pointer
-                // of its destination when it wins, and an emitting lattice arc
-                const bool keep = act && slot >= 0;
-                const uint64_t m = __ballot(keep);
-                if (m) {
-                    int b = 0;
-                    if (lane == 0) b = atomicAdd(&sh.ncand, __popcll(m));
-                    b = __shfl(b, 0, kWave);
-                    if (keep) {
-                        const int idx = b + rank_in(m);
-                        if (idx < capC)
-                            cand[idx] = make_int4(static_cast<int>(run.prev0) + t0 + o, arc, __float_as_int(cnd), slot);
-                        else
-                            sh.status = WFST_ECAPACITY;
-                    }
-                }
-                done = hi;
-                t0 += kWave;
-            }
+        const int src0 = static_cast<int>(run.prev0);
+        if (run.n_prev <= kSetCache) {
+            SetView<true> v{s_cost, s_epre, s_ebeg};
+            expand<G, true>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, aux, glds, spill, gcap, cand, capC);
+        } else {
+            const int64_t base = ly.sv0 + run.prev0;
+            SetView<false> v{p.sv_tok + base, p.sv_epre + base, p.sv_ebeg + base};
+            expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, aux, glds, spill, gcap, cand, capC);
         }
     }
+    // full barrier: the candidate list is read back after compaction
     __syncthreads();
 
     // ---- 2. epsilon closure ----
@@ -380,10 +468,13 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             const int i = c0 + lane;
             int xb = 0, xd = 0;
             float cst = 0.0f;
+            bool first = false;
+            int4 x0 = make_int4(0, 0, 0, 0);
             if (i < total) {
                 uint2 it;
-                if (i < glds) it = aux[cur * kGenCap + i];
-                else {
+                if (i < glds) {
+                    it = aux[cur * kGenCap + i];
+                } else {
                     const unsigned long long w = ldg(reinterpret_cast<const unsigned long long *>(
                         spill + static_cast<int64_t>(cur) * gcap + (i - glds)));
                     it = make_uint2(static_cast<uint32_t>(w), static_cast<uint32_t>(w >> 32));
@@ -391,11 +482,23 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
                 cst = __uint_as_float(it.y);
                 const uint32_t now = static_cast<uint32_t>(tld<G>(t.vals + it.x) >> 32);
                 if (okey(cst) == now) {   // otherwise a cheaper item of this state follows
-                    const int s = static_cast<int>(tld<G>(t.keys + it.x));
-                    xb = p.g.xoff[s];
-                    xd = p.g.xoff[s + 1] - xb;
+                    const int64_t s = static_cast<int64_t>(tld<G>(t.keys + it.x));
+                    const int4 lo = p.g.srec[2 * s];
+                    x0 = p.g.srec[2 * s + 1];
+                    first = lo.w > lo.z;
+                    xb = lo.z + 1;
+                    xd = max(lo.w - lo.z - 1, 0);
                 }
             }
+            {
+                // the first epsilon arc, from the state record
+                const uint32_t bnd = drop_bound(sh.best, p.beam);
+                const float cnd = cst + __int_as_float(x0.y);
+                const uint32_t key = okey(cnd);
+                (void)offer<G>(t, sh, aux, glds, spill, gcap, nxt, first && key <= bnd,
+                               static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, cnd, key, x0.z);
+            }
+            // the other epsilon arcs, spread over the wave
             const int incl = wave_incl_scan(xd);
             const int pre = incl - xd;
             const int tot = __shfl(incl, kWave - 1, kWave);
@@ -493,7 +596,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             dd[r] = 0;
             vv[r] = kEmptyTok;
             if (i < n) {
-                sl[r] = tld<G>(t.slots + i);
+                sl[r] = static_cast<int>(tld<G>(t.slots + i));
                 vv[r] = tld<G>(t.vals + sl[r]);
                 dd[r] = static_cast<int>(tld<G>(t.keys + sl[r]));
             }
@@ -504,9 +607,10 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             eb[r] = 0;
             ed[r] = 0;
             if (kp[r]) {
-                eb[r] = p.g.eoff[dd[r]];
-                ed[r] = p.g.eoff[dd[r] + 1];
-                xc += p.g.xoff[dd[r] + 1] - p.g.xoff[dd[r]];
+                const int4 rl = p.g.srec[2 * static_cast<int64_t>(dd[r])];
+                eb[r] = rl.x;
+                ed[r] = rl.y;
+                xc += rl.w - rl.z;
                 kc++;
                 ac += ed[r] - eb[r];
             }
@@ -528,6 +632,11 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
                 } else {
                     sh.status = WFST_ECAPACITY;
                 }
+                if (pos < kSetCache) {
+                    s_cost[pos] = tok_cost(vv[r]);
+                    s_epre[pos] = apos;
+                    s_ebeg[pos] = eb[r];
+                }
                 if (static_cast<uint32_t>(vv[r] >> 32) == kb && atomicCAS(&sh.best_pos, -1, pos) == -1) {
                     sh.best_eb = eb[r];
                     sh.best_ed = ed[r];
@@ -543,8 +652,11 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         n_kept += tot.x;
         a_kept += tot.y;
     }
-    __syncthreads();
     const int ns = n_kept;
+    // Steps 5-6 read the survivors from LDS unless the set is larger than
+    // the LDS copy; then their device-memory stores must be complete.
+    if (G || ns > kSetCache) __syncthreads();
+    else lds_barrier();
     if (ns == 0) return WFST_ENOPATH;
     if (sh.status) return sh.status;
     if (tid == 0) {
@@ -568,33 +680,58 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     }
 
     // ---- 5. back-pointers and lattice records ----
-    // Survivors of S_k: the back-pointer of a token reached by an epsilon arc
-    // (its source is in S_k) and the epsilon lattice arcs inside S_k.
-    for (int c0 = wid * kWave; c0 < ns; c0 += kT) {
+    // Survivors of S_k (walked in slot-list order): the back-pointer of a
+    // token reached by an epsilon arc (its source is in S_k) and the epsilon
+    // lattice arcs inside S_k.
+    const bool set_lds = ns <= kSetCache;
+    for (int c0 = wid * kWave; c0 < n; c0 += kT) {
         const int i = c0 + lane;
-        int xb = 0, xdeg = 0;
+        bool surv = false;
+        int rel = 0, a = -1;
+        int64_t s = 0;
         float cst = 0.0f;
-        if (i < ns) {
-            const int64_t o = ly.sv0 + set0 + i;
-            const int s = p.sv_state[o];
-            const uint64_t v = p.sv_tok[o];
-            cst = tok_cost(v);
-            const int a = tok_arc(v);
-            if (a < 0) {
-                p.sv_prev[o] = -1;
-            } else {
-                const int info = p.g.arc_src[a];
-                if (info < 0) {
-                    const int sl = tab_find<G>(t, static_cast<uint32_t>(info) & kDstMask);
-                    p.sv_prev[o] = sl >= 0 ? static_cast<int>(static_cast<uint32_t>(tld<G>(t.vals + sl))) : -1;
-                }
+        if (i < n) {
+            const int sl = static_cast<int>(tld<G>(t.slots + i));
+            const unsigned long long v = tld<G>(t.vals + sl);
+            if (v != kEmptyTok) {
+                surv = true;
+                rel = static_cast<int>(static_cast<uint32_t>(v));
+                a = static_cast<int>(static_cast<uint32_t>(v >> 32)) - 1;
+                s = static_cast<int64_t>(tld<G>(t.keys + sl));
+                cst = set_lds ? s_cost[rel - set0] : tok_cost(p.sv_tok[ly.sv0 + rel]);
             }
+        }
+        int info = 0;
+        int4 lo = make_int4(0, 0, 0, 0), x0 = make_int4(0, 0, 0, 0);
+        if (surv) {
+            if (a >= 0) info = p.g.arc_src[a];
             if (p.lattice) {
-                xb = p.g.xoff[s];
-                xdeg = p.g.xoff[s + 1] - xb;
+                lo = p.g.srec[2 * s];
+                x0 = p.g.srec[2 * s + 1];
+            }
+            if (a < 0) {
+                p.sv_prev[ly.sv0 + rel] = -1;
+            } else if (info < 0) {
+                const int sl = tab_find<G>(t, static_cast<uint32_t>(info) & kDstMask);
+                p.sv_prev[ly.sv0 + rel] = sl >= 0 ? static_cast<int>(static_cast<uint32_t>(tld<G>(t.vals + sl))) : -1;
             }
         }
         if (!p.lattice) continue;
+        {
+            // the first epsilon arc, from the state record
+            bool rec = false;
+            int4 r4 = make_int4(0, 0, 0, 0);
+            const float pc = cst + __int_as_float(x0.y);
+            if (surv && lo.w > lo.z && okey(pc) <= cut) {
+                const int sl = tab_find<G>(t, static_cast<uint32_t>(x0.x) & kDstMask);
+                const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
+                rec = dv != kEmptyTok;
+                r4 = make_int4(rel, static_cast<int>(static_cast<uint32_t>(dv)), x0.z, __float_as_int(pc));
+            }
+            put_record(p.lat_x + ly.lx0, ly.lxcap, run.lat_x, &sh.nlat_x, sh, rec, r4);
+        }
+        const int xb = lo.z + 1;
+        const int xdeg = surv ? max(lo.w - lo.z - 1, 0) : 0;
         const int incl = wave_incl_scan(xdeg);
         const int pre = incl - xdeg;
         const int tot = __shfl(incl, kWave - 1, kWave);
@@ -604,6 +741,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             const int ob = __shfl(xb, o, kWave);
             const int op = __shfl(pre, o, kWave);
             const float oc = __shfl(cst, o, kWave);
+            const int orel = __shfl(rel, o, kWave);
             bool rec = false;
             int4 r4 = make_int4(0, 0, 0, 0);
             if (kk < tot) {
@@ -613,8 +751,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
                     const int sl = tab_find<G>(t, static_cast<uint32_t>(x.x) & kDstMask);
                     const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
                     rec = dv != kEmptyTok;
-                    r4 = make_int4(static_cast<int>(set0) + c0 + o, static_cast<int>(static_cast<uint32_t>(dv)), x.z,
-                                   __float_as_int(pc));
+                    r4 = make_int4(orel, static_cast<int>(static_cast<uint32_t>(dv)), x.z, __float_as_int(pc));
                 }
             }
             put_record(p.lat_x + ly.lx0, ly.lxcap, run.lat_x, &sh.nlat_x, sh, rec, r4);
@@ -642,7 +779,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             if (p.lattice) put_record(p.lat_e + ly.le0, ly.lecap, run.lat_e, &sh.nlat_e, sh, rec, r4);
         }
     }
-    __syncthreads();
+    table_barrier<G>();
     run.lat_e += sh.nlat_e;
     run.lat_x += sh.nlat_x;
     if (sh.status) return sh.status;
@@ -654,11 +791,11 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
 
     // ---- 6. clear the table ----
     for (int i = tid; i < n; i += kT) {
-        const int s2 = tld<G>(t.slots + i);
+        const int s2 = static_cast<int>(tld<G>(t.slots + i));
         t.keys[s2] = kEmptyKey;
         t.vals[s2] = kEmptyTok;
     }
-    __syncthreads();
+    table_barrier<G>();
     return 0;
 }
 
@@ -666,8 +803,11 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
 {
     __shared__ uint32_t s_keys[kSlots];
     __shared__ unsigned long long s_vals[kSlots];
-    __shared__ int32_t s_slots[kFill];
+    __shared__ uint16_t s_slots[kFill];
     __shared__ uint2 s_aux[2 * kGenCap];   // epsilon generations, or the select histogram
+    __shared__ float s_cost[kSetCache];    // the last token set, for the next expansion
+    __shared__ int32_t s_epre[kSetCache];
+    __shared__ int32_t s_ebeg[kSetCache];
     __shared__ Sh sh;
 
     const int u = blockIdx.x;
@@ -713,7 +853,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     bool gclean = false;
     int rc = 0;
     for (int k = 0; k <= Tp; k++) {
-        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, spill, gcap, cand, capC, run, k);
+        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, spill, gcap, cand, capC, run, k);
         if (rc == kOverflow) {
             // more states than the LDS table holds: redo the frame in device memory
             for (int i = tid; i < kSlots; i += kT) {
@@ -728,7 +868,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
                 gclean = true;
             }
             __syncthreads();
-            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, spill, gcap, cand, capC, run, k);
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, spill, gcap, cand, capC, run, k);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
             run.gframes++;
         }
