@@ -104,7 +104,7 @@ struct Params {
     int32_t blank_id;
     float blank_thr;
     int32_t lds_fill;         // states per frame the LDS token table takes (<= its fill limit)
-    int32_t gen_lds;          // epsilon items per generation kept in LDS (<= its capacity)
+    int32_t gen_lds;          // epsilon items per wave queue in LDS (<= its capacity)
     UttState *st;
     const UttLayout *lay;
     // survivors (per utterance regions)

@@ -4,16 +4,19 @@
 // generation, Sec. 1 and Sec. 3).
 //
 // Frame k (token set S_k) in one workgroup:
-//   1. expansion of the emitting arcs of S_{k-1}: each wave takes chunks of
-//      64 consecutive arcs of the set, finds their tokens by a 64-ary search
-//      over the set's emitting-arc prefix (kept in LDS for sets of up to
-//      kSetCache tokens) and issues the loads of two chunks together.  The
+//   1. expansion of the emitting arcs of S_{k-1}: each wave takes up to four
+//      chunks of 64 consecutive arcs of the set, finds their tokens by a
+//      64-ary search over the set's emitting-arc prefix (kept in LDS for sets
+//      of up to kSetCache tokens) and issues all their loads together.  The
 //      frame's tokens live in a hash table in LDS (state -> packed token);
 //      recombination is an LDS 64-bit atomicMin on (cost key, arc + 1), the
 //      first touch of a state appends its slot to a slot list;
-//   2. epsilon closure, generation by generation: every lowered token whose
-//      state has epsilon out-arcs is relaxed again until nothing changes (a
-//      state's first epsilon arc comes with its 32-byte state record);
+//   2. epsilon closure: every lowered token whose state has epsilon
+//      out-arcs goes to its wave's LDS queue, and each wave relaxes its own
+//      queue until it is empty, with no barrier between the rounds (a
+//      state's first epsilon arc comes with its 32-byte state record).
+//      Items beyond a queue's capacity go to a device-memory list that the
+//      whole workgroup relaxes after a barrier;
 //   3. pruning: beam limit from the frame's best cost key and, when more
 //      tokens lie within it than max_active, the exact max_active-th
 //      smallest key by radix select over an LDS histogram;
@@ -38,13 +41,14 @@ constexpr int kW = kT / kWave;            // waves per workgroup
 constexpr int kSlotBits = 13;
 constexpr int kSlots = 1 << kSlotBits;    // LDS hash slots
 constexpr int kFill = 6144;               // LDS states per frame before falling back to device memory
-constexpr int kGenCap = 1024;             // LDS epsilon items per generation
+constexpr int kQueue = 128;               // LDS epsilon items per wave queue
 constexpr int kSetCache = 3008;           // tokens of the previous set kept in LDS for the expansion
 constexpr int kRun = 2;                   // slot-list entries per thread per compaction pass
-constexpr int kChunks = 2;                // 64-arc chunks a wave has in flight in the expansion
+constexpr int kChunks = 4;                // 64-arc chunks a wave has in flight in the expansion
+constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
 constexpr int kOverflow = 1;              // frame result: the table filled up
 
-static_assert(kHistBins * 4 <= 2 * kGenCap * 8, "the select histogram aliases the epsilon buffers");
+static_assert(kHistBins * 4 <= kW * kQueue * 8, "the select histogram aliases the epsilon queues");
 
 __device__ __forceinline__ uint32_t hash_state(uint32_t d) { return d * 0x9E3779B1u; }
 
@@ -106,7 +110,7 @@ struct Sh {
     int status;          // sticky error of the utterance
     uint32_t best;       // smallest cost key among the frame's tokens
     uint32_t hint;       // key of one real candidate of the next frame
-    int gen_n[2];        // epsilon items per generation (LDS part first)
+    int spill_n[2];      // epsilon items in the device-memory lists
     int ncand;           // emitting candidates listed this frame
     int nlat_e, nlat_x;  // lattice records this frame
     int bin, before, cnt;
@@ -132,7 +136,7 @@ template <bool G>
 __device__ __forceinline__ int tab_find(const Tab<G> &t, uint32_t d)
 {
     uint32_t h = hash_state(d) >> t.shift;
-    for (uint32_t probe = 0; probe <= t.mask; probe++) {
+    for (int probe = 0; probe < kMaxProbe; probe++) {
         const uint32_t k = tld<G>(t.keys + h);
         if (k == d) return static_cast<int>(h);
         if (k == kEmptyKey) return -1;
@@ -141,12 +145,23 @@ __device__ __forceinline__ int tab_find(const Tab<G> &t, uint32_t d)
     return -1;
 }
 
+// A wave's epsilon work list: an LDS queue of (table slot, cost bits) items
+// and the device-memory list that takes what does not fit.
+struct WaveQ {
+    uint2 *q;        // this wave's LDS queue
+    int n;           // items in it (the same in every lane)
+    int qcap;        // its capacity (<= kQueue)
+    uint2 *spill;    // device-memory list of the current round
+    int *spill_n;    // its LDS counter
+    int scap;        // its capacity
+};
+
 // Offer one candidate token per lane (act) to the table; lowered tokens of
-// states with epsilon out-arcs become items of generation `gen`.  Called by
+// states with epsilon out-arcs become items of the wave's queue.  Called by
 // the whole wave; returns the lane's slot or -1.
 template <bool G>
-__device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, uint2 *lgen, int glds, uint2 *sgen, int gcap, int gen,
-                                     bool act, uint32_t d, bool d_eps, float cand, uint32_t key, int32_t arc)
+__device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, WaveQ &wq, bool act, uint32_t d, bool d_eps,
+                                     float cand, uint32_t key, int32_t arc)
 {
     // slot of state d: a compare-and-swap on the key claims a free slot or
     // finds the state's own
@@ -154,7 +169,7 @@ __device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, uint2 *lgen, int g
     bool claimed = false;
     if (act) {
         uint32_t h = hash_state(d) >> t.shift;
-        for (uint32_t probe = 0; probe <= t.mask; probe++) {
+        for (int probe = 0; probe < kMaxProbe; probe++) {
             const uint32_t k = atomicCAS(t.keys + h, kEmptyKey, d);
             if (k == kEmptyKey || k == d) {
                 slot = static_cast<int>(h);
@@ -187,18 +202,47 @@ __device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, uint2 *lgen, int g
     const bool push = impr && d_eps;
     const uint64_t m = __ballot(push);
     if (m) {
-        int b = 0;
-        if (lane_id() == 0) b = atomicAdd(&sh.gen_n[gen], __popcll(m));
-        b = __builtin_amdgcn_readlane(b, 0);
         if (push) {
-            const int idx = b + rank_in(m);
+            const int idx = wq.n + rank_in(m);
             const uint2 it = make_uint2(static_cast<uint32_t>(slot), __float_as_uint(cand));
-            if (idx < glds) lgen[gen * kGenCap + idx] = it;
-            else if (idx - glds < gcap) sgen[static_cast<int64_t>(gen) * gcap + (idx - glds)] = it;
+            if (idx < wq.qcap) {
+                wq.q[idx] = it;
+            } else {
+                const int gi = atomicAdd(wq.spill_n, 1);
+                if (gi < wq.scap) wq.spill[gi] = it;
+                else sh.status = WFST_ECAPACITY;
+            }
+        }
+        wq.n = min(wq.n + __popcll(m), wq.qcap);
+    }
+    return slot;
+}
+
+// Append R records per lane (rec[r]) to a list with one LDS add per wave.
+template <int R>
+__device__ __forceinline__ void put_records(int4 *buf, int64_t cap, int64_t base, int *cnt, Sh &sh, const bool *rec,
+                                            const int4 *r4)
+{
+    uint64_t m[R];
+    int pref[R], total = 0;
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        m[r] = __ballot(rec[r]);
+        pref[r] = total;
+        total += __popcll(m[r]);
+    }
+    if (!total) return;
+    int b = 0;
+    if (lane_id() == 0) b = atomicAdd(cnt, total);
+    b = __builtin_amdgcn_readlane(b, 0);
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        if (rec[r]) {
+            const int64_t idx = base + b + pref[r] + rank_in(m[r]);
+            if (idx < cap) buf[idx] = r4[r];
             else sh.status = WFST_ECAPACITY;
         }
     }
-    return slot;
 }
 
 // Largest t in [0, n) with epre[t] <= a (epre non-decreasing, epre[0] <= a).
@@ -325,18 +369,19 @@ struct SetView<false> {
 // wins, and an emitting lattice arc.
 template <bool G, bool L>
 __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh, const SetView<L> &v, int n_tok,
-                                       int A, int src0, const float *row, uint2 *aux, int glds, uint2 *spill,
-                                       int gcap, int4 *cand, int capC)
+                                       int A, int src0, const float *row, WaveQ &wq, int4 *cand, int capC)
 {
     const int lane = lane_id();
     const int wid = threadIdx.x / kWave;
-    for (int c = wid * kChunks; c * kWave < A; c += kW * kChunks) {
+    // wave w takes chunks w, w + kW, w + 2 kW, ... : every wave gets work
+    for (int c = wid; c * kWave < A; c += kW * kChunks) {
+        if (__builtin_amdgcn_readfirstlane(sh.overflow)) break;   // the frame is redone anyway
         int ob[kChunks], op[kChunks], ot[kChunks], a[kChunks];
         float oc[kChunks];
         bool ok[kChunks];
 #pragma unroll
         for (int r = 0; r < kChunks; r++) {
-            const int a0 = (c + r) * kWave;
+            const int a0 = (c + r * kW) * kWave;
             a[r] = a0 + lane;
             ok[r] = false;
             ob[r] = op[r] = ot[r] = 0;
@@ -381,31 +426,176 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
         float lv[kChunks];
 #pragma unroll
         for (int r = 0; r < kChunks; r++) lv[r] = ok[r] ? ldg(row + rec[r].y) : 0.0f;
+        bool act[kChunks], de[kChunks], keep[kChunks];
+        uint32_t d[kChunks], key[kChunks];
+        float cnd[kChunks];
+        int32_t arc[kChunks];
+        int slot[kChunks];
+        uint32_t km = kEmptyKey;
 #pragma unroll
         for (int r = 0; r < kChunks; r++) {
-            const uint32_t bnd = drop_bound(sh.best, p.beam);
             const float t1 = oc[r] + __int_as_float(rec[r].z);
-            const float cnd = t1 - lv[r];
-            const uint32_t key = okey(cnd);
-            const bool act = ok[r] && key <= bnd;
-            const int slot = offer<G>(t, sh, aux, glds, spill, gcap, 0, act, static_cast<uint32_t>(rec[r].x) & kDstMask,
-                                      rec[r].x < 0, cnd, key, rec[r].w);
-            const bool keep = act && slot >= 0;
-            const uint64_t m = __ballot(keep);
-            if (m) {
-                int b = 0;
-                if (lane == 0) b = atomicAdd(&sh.ncand, __popcll(m));
-                b = __builtin_amdgcn_readlane(b, 0);
-                if (keep) {
-                    const int idx = b + rank_in(m);
-                    if (idx < capC)
-                        cand[idx] = make_int4(src0 + ot[r], rec[r].w, __float_as_int(cnd), slot);
-                    else
-                        sh.status = WFST_ECAPACITY;
-                }
-            }
+            cnd[r] = t1 - lv[r];
+            key[r] = okey(cnd[r]);
+            if (ok[r] && key[r] < km) km = key[r];
+            d[r] = static_cast<uint32_t>(rec[r].x) & kDstMask;
+            de[r] = rec[r].x < 0;
+            arc[r] = rec[r].w;
+        }
+        // The batch's own cheapest candidate tightens the early-drop bound; it
+        // is within that bound itself, so it is offered and the frame's best
+        // key may take its value now.
+        km = wave_min_u32(km);
+        const uint32_t cur = sh.best;
+        if (km < cur && lane == 0) atomicMin(&sh.best, km);
+        const uint32_t bnd = drop_bound(km < cur ? km : cur, p.beam);
+#pragma unroll
+        for (int r = 0; r < kChunks; r++) act[r] = ok[r] && key[r] <= bnd;
+#pragma unroll
+        for (int r = 0; r < kChunks; r++) slot[r] = offer<G>(t, sh, wq, act[r], d[r], de[r], cnd[r], key[r], arc[r]);
+        // the candidate list, one LDS add per wave
+        int4 c4[kChunks];
+#pragma unroll
+        for (int r = 0; r < kChunks; r++) {
+            keep[r] = act[r] && slot[r] >= 0;
+            c4[r] = make_int4(src0 + ot[r], arc[r], __float_as_int(cnd[r]), slot[r]);
+        }
+        put_records<kChunks>(cand, capC, 0, &sh.ncand, sh, keep, c4);
+    }
+}
+
+// Relax the epsilon arcs of one item per lane (valid): the item's state
+// still holding the item's cost, i.e. no cheaper item of it follows.
+template <bool G>
+__device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, WaveQ &wq, bool valid, uint2 it)
+{
+    const int lane = lane_id();
+    int xb = 0, xd = 0;
+    bool first = false;
+    int4 x0 = make_int4(0, 0, 0, 0);
+    const float cst = __uint_as_float(it.y);
+    if (valid) {
+        const uint32_t now = static_cast<uint32_t>(tld<G>(t.vals + it.x) >> 32);
+        if (okey(cst) == now) {
+            const int64_t s = static_cast<int64_t>(tld<G>(t.keys + it.x));
+            const int4 lo = p.g.srec[2 * s];
+            x0 = p.g.srec[2 * s + 1];
+            first = lo.w > lo.z;
+            xb = lo.z + 1;
+            xd = max(lo.w - lo.z - 1, 0);
         }
     }
+    {
+        // the first epsilon arc, from the state record
+        const uint32_t bnd = drop_bound(sh.best, p.beam);
+        const float cnd = cst + __int_as_float(x0.y);
+        const uint32_t key = okey(cnd);
+        (void)offer<G>(t, sh, wq, first && key <= bnd, static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, cnd, key,
+                       x0.z);
+    }
+    // the other epsilon arcs, spread over the wave
+    const int incl = wave_incl_scan(xd);
+    const int pre = incl - xd;
+    const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
+    for (int k0 = 0; k0 < tot; k0 += kWave) {
+        const int kk = k0 + lane;
+        const int o = owner_lane(pre, kk);
+        const int ob = __shfl(xb, o, kWave);
+        const int op = __shfl(pre, o, kWave);
+        const float oc = __shfl(cst, o, kWave);
+        const uint32_t bnd = drop_bound(sh.best, p.beam);
+        bool act = false, d_eps = false;
+        uint32_t d = 0, key = kEmptyKey;
+        int arc = 0;
+        float cnd = 0.0f;
+        if (kk < tot) {
+            const int4 r = p.g.xarc[ob + (kk - op)];
+            d = static_cast<uint32_t>(r.x) & kDstMask;
+            d_eps = r.x < 0;
+            arc = r.z;
+            cnd = oc + __int_as_float(r.y);
+            key = okey(cnd);
+            act = key <= bnd;
+        }
+        (void)offer<G>(t, sh, wq, act, d, d_eps, cnd, key, arc);
+    }
+}
+
+// Relax the wave's queue until it is empty (items pushed meanwhile included).
+template <bool G>
+__device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, WaveQ &wq)
+{
+    const int lane = lane_id();
+    while (wq.n > 0) {
+        if (__builtin_amdgcn_readfirstlane(sh.overflow)) {   // the frame is redone anyway
+            wq.n = 0;
+            break;
+        }
+        const int take = min(wq.n, kWave);
+        const int base = wq.n - take;
+        const uint2 it = lane < take ? wq.q[base + lane] : make_uint2(0u, 0u);
+        wq.n = base;
+        relax<G>(p, t, sh, wq, lane < take, it);
+    }
+}
+
+// The epsilon lattice arcs after the first (rows xbeg + 1 .. xbeg + xdeg_all),
+// spread over the wave.
+template <bool G>
+__device__ __forceinline__ void eps_rest(const Params &p, const Tab<G> &t, Sh &sh, const UttLayout &ly, int64_t base,
+                                         uint32_t cut, bool surv, int rel, float cst, int xbeg, int xdeg_all)
+{
+    const int lane = lane_id();
+    const int xb = xbeg + 1;
+    const int xdeg = surv ? max(xdeg_all - 1, 0) : 0;
+    const int incl = wave_incl_scan(xdeg);
+    const int pre = incl - xdeg;
+    const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
+    for (int k0 = 0; k0 < tot; k0 += kWave) {
+        const int kk = k0 + lane;
+        const int o = owner_lane(pre, kk);
+        const int ob = __shfl(xb, o, kWave);
+        const int op = __shfl(pre, o, kWave);
+        const float oc = __shfl(cst, o, kWave);
+        const int orel = __shfl(rel, o, kWave);
+        bool rec = false;
+        int4 r4 = make_int4(0, 0, 0, 0);
+        if (kk < tot) {
+            const int4 x = p.g.xarc[ob + (kk - op)];
+            const float pc = oc + __int_as_float(x.y);
+            if (okey(pc) <= cut) {
+                const int sl = tab_find<G>(t, static_cast<uint32_t>(x.x) & kDstMask);
+                const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
+                rec = dv != kEmptyTok;
+                r4 = make_int4(orel, static_cast<int>(static_cast<uint32_t>(dv)), x.z, __float_as_int(pc));
+            }
+        }
+        put_record(p.lat_x + ly.lx0, ly.lxcap, base, &sh.nlat_x, sh, rec, r4);
+    }
+}
+
+// Epsilon lattice arcs of one survivor per lane (surv): each epsilon arc of
+// its state (rows xbeg .. xbeg + xdeg_all) whose prefix cost is within the
+// set's cutoff.  The first arc comes from the state record (x0), the others
+// from the epsilon rows.
+template <bool G>
+__device__ __forceinline__ void eps_records(const Params &p, const Tab<G> &t, Sh &sh, const UttLayout &ly,
+                                            int64_t base, uint32_t cut, bool surv, int rel, float cst, int xbeg,
+                                            int xdeg_all, int4 x0)
+{
+    {
+        bool rec = false;
+        int4 r4 = make_int4(0, 0, 0, 0);
+        const float pc = cst + __int_as_float(x0.y);
+        if (surv && xdeg_all > 0 && okey(pc) <= cut) {
+            const int sl = tab_find<G>(t, static_cast<uint32_t>(x0.x) & kDstMask);
+            const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
+            rec = dv != kEmptyTok;
+            r4 = make_int4(rel, static_cast<int>(static_cast<uint32_t>(dv)), x0.z, __float_as_int(pc));
+        }
+        put_record(p.lat_x + ly.lx0, ly.lxcap, base, &sh.nlat_x, sh, rec, r4);
+    }
+    eps_rest<G>(p, t, sh, ly, base, cut, surv, rel, cst, xbeg, xdeg_all);
 }
 
 // One frame: produces S_k from S_{k-1} (or from the start state when k = 0).
@@ -419,13 +609,19 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     const int tid = threadIdx.x;
     const int lane = lane_id();
     const int wid = tid / kWave;
-    const int glds = p.gen_lds;
+    WaveQ wq;
+    wq.q = aux + wid * kQueue;
+    wq.n = 0;
+    wq.qcap = min(kQueue, p.gen_lds);
+    wq.spill = spill;
+    wq.spill_n = &sh.spill_n[0];
+    wq.scap = gcap;
 
     if (tid == 0) {
         sh.nslots = 0;
         sh.overflow = 0;
         sh.best = k > 0 ? sh.hint : kEmptyKey;
-        sh.gen_n[0] = sh.gen_n[1] = 0;
+        sh.spill_n[0] = sh.spill_n[1] = 0;
         sh.ncand = 0;
         sh.nlat_e = sh.nlat_x = 0;
         sh.cnt = 0;
@@ -438,95 +634,45 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         if (wid == 0) {
             const int s = p.g.start;
             const int4 lo = p.g.srec[2 * static_cast<int64_t>(s)];
-            (void)offer<G>(t, sh, aux, glds, spill, gcap, 0, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0.0f,
-                           okey(0.0f), -1);
+            (void)offer<G>(t, sh, wq, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0.0f, okey(0.0f), -1);
         }
     } else {
         const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k - 1]) * p.L;
         const int src0 = static_cast<int>(run.prev0);
         if (run.n_prev <= kSetCache) {
             SetView<true> v{s_cost, s_epre, s_ebeg};
-            expand<G, true>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, aux, glds, spill, gcap, cand, capC);
+            expand<G, true>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cand, capC);
         } else {
             const int64_t base = ly.sv0 + run.prev0;
             SetView<false> v{p.sv_tok + base, p.sv_epre + base, p.sv_ebeg + base};
-            expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, aux, glds, spill, gcap, cand, capC);
+            expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cand, capC);
         }
     }
-    // full barrier: the candidate list is read back after compaction
+    // ---- 2. epsilon closure: each wave its own queue, then spill rounds ----
+    drain<G>(p, t, sh, wq);
+    // full barrier: spilled items and the candidate list are read by other waves
     __syncthreads();
-
-    // ---- 2. epsilon closure ----
-    int cur = 0;
+    int sp = 0;
     while (true) {
-        const int total = min(sh.gen_n[cur], glds + gcap);
+        const int total = min(sh.spill_n[sp], gcap);
         if (total == 0 || sh.overflow || sh.status) break;
-        const int nxt = cur ^ 1;
-        if (tid == 0) sh.gen_n[nxt] = 0;
+        const uint2 *list = spill + static_cast<int64_t>(sp) * gcap;
+        if (tid == 0) sh.spill_n[sp ^ 1] = 0;
         __syncthreads();
+        wq.spill = spill + static_cast<int64_t>(sp ^ 1) * gcap;
+        wq.spill_n = &sh.spill_n[sp ^ 1];
         for (int c0 = wid * kWave; c0 < total; c0 += kT) {
             const int i = c0 + lane;
-            int xb = 0, xd = 0;
-            float cst = 0.0f;
-            bool first = false;
-            int4 x0 = make_int4(0, 0, 0, 0);
+            uint2 it = make_uint2(0u, 0u);
             if (i < total) {
-                uint2 it;
-                if (i < glds) {
-                    it = aux[cur * kGenCap + i];
-                } else {
-                    const unsigned long long w = ldg(reinterpret_cast<const unsigned long long *>(
-                        spill + static_cast<int64_t>(cur) * gcap + (i - glds)));
-                    it = make_uint2(static_cast<uint32_t>(w), static_cast<uint32_t>(w >> 32));
-                }
-                cst = __uint_as_float(it.y);
-                const uint32_t now = static_cast<uint32_t>(tld<G>(t.vals + it.x) >> 32);
-                if (okey(cst) == now) {   // otherwise a cheaper item of this state follows
-                    const int64_t s = static_cast<int64_t>(tld<G>(t.keys + it.x));
-                    const int4 lo = p.g.srec[2 * s];
-                    x0 = p.g.srec[2 * s + 1];
-                    first = lo.w > lo.z;
-                    xb = lo.z + 1;
-                    xd = max(lo.w - lo.z - 1, 0);
-                }
+                const unsigned long long w = ldg(reinterpret_cast<const unsigned long long *>(list + i));
+                it = make_uint2(static_cast<uint32_t>(w), static_cast<uint32_t>(w >> 32));
             }
-            {
-                // the first epsilon arc, from the state record
-                const uint32_t bnd = drop_bound(sh.best, p.beam);
-                const float cnd = cst + __int_as_float(x0.y);
-                const uint32_t key = okey(cnd);
-                (void)offer<G>(t, sh, aux, glds, spill, gcap, nxt, first && key <= bnd,
-                               static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, cnd, key, x0.z);
-            }
-            // the other epsilon arcs, spread over the wave
-            const int incl = wave_incl_scan(xd);
-            const int pre = incl - xd;
-            const int tot = __shfl(incl, kWave - 1, kWave);
-            for (int k0 = 0; k0 < tot; k0 += kWave) {
-                const int kk = k0 + lane;
-                const int o = owner_lane(pre, kk);
-                const int ob = __shfl(xb, o, kWave);
-                const int op = __shfl(pre, o, kWave);
-                const float oc = __shfl(cst, o, kWave);
-                const uint32_t bnd = drop_bound(sh.best, p.beam);
-                bool act = false, d_eps = false;
-                uint32_t d = 0, key = kEmptyKey;
-                int arc = 0;
-                float cnd = 0.0f;
-                if (kk < tot) {
-                    const int4 r = p.g.xarc[ob + (kk - op)];
-                    d = static_cast<uint32_t>(r.x) & kDstMask;
-                    d_eps = r.x < 0;
-                    arc = r.z;
-                    cnd = oc + __int_as_float(r.y);
-                    key = okey(cnd);
-                    act = key <= bnd;
-                }
-                (void)offer<G>(t, sh, aux, glds, spill, gcap, nxt, act, d, d_eps, cnd, key, arc);
-            }
+            relax<G>(p, t, sh, wq, i < total, it);
+            drain<G>(p, t, sh, wq);
         }
         __syncthreads();
-        cur = nxt;
+        sp ^= 1;
     }
     if (sh.overflow) return kOverflow;
     if (sh.status) return sh.status;
@@ -581,36 +727,57 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     }
 
     // ---- 4. compaction into S_k, in slot-list order ----
+    // With one pass (n <= kT * kRun) each thread keeps its survivors' state
+    // records and back-pointer sources in registers for step 5: the loads
+    // ride along with the compaction's own.
     const int64_t set0 = run.set0;
+    const bool one_pass = n <= kT * kRun;
     int n_kept = 0, a_kept = 0;
+    // per kept entry: survivor index (-1 if not kept), back-pointer source
+    // (arc_src of the token's arc, or -1 for the start token), cost, the
+    // epsilon rows after the first arc and the first epsilon record
+    int kslot[kRun], krel[kRun], kinfo[kRun], kxb[kRun], kxd[kRun];
+    float kcst[kRun];
+    int4 kx0[kRun];
     for (int e0 = 0; e0 < n; e0 += kT * kRun) {
-        int sl[kRun], dd[kRun], eb[kRun], ed[kRun];
+        int dd[kRun], eb[kRun], ed[kRun];
         unsigned long long vv[kRun];
-        bool kp[kRun];
         int kc = 0, ac = 0;
         long long xc = 0;
 #pragma unroll
         for (int r = 0; r < kRun; r++) {
             const int i = e0 + tid * kRun + r;
-            sl[r] = -1;
+            kslot[r] = -1;
             dd[r] = 0;
             vv[r] = kEmptyTok;
             if (i < n) {
-                sl[r] = static_cast<int>(tld<G>(t.slots + i));
-                vv[r] = tld<G>(t.vals + sl[r]);
-                dd[r] = static_cast<int>(tld<G>(t.keys + sl[r]));
+                kslot[r] = static_cast<int>(tld<G>(t.slots + i));
+                vv[r] = tld<G>(t.vals + kslot[r]);
+                dd[r] = static_cast<int>(tld<G>(t.keys + kslot[r]));
             }
         }
+        bool kp[kRun];
 #pragma unroll
         for (int r = 0; r < kRun; r++) {
-            kp[r] = sl[r] >= 0 && static_cast<uint32_t>(vv[r] >> 32) <= cut;
-            eb[r] = 0;
-            ed[r] = 0;
+            kp[r] = kslot[r] >= 0 && static_cast<uint32_t>(vv[r] >> 32) <= cut;
+            kcst[r] = tok_cost(vv[r]);
+            eb[r] = ed[r] = 0;
+            kinfo[r] = -1;
+            kxb[r] = kxd[r] = 0;
+            kx0[r] = make_int4(0, 0, 0, 0);
             if (kp[r]) {
-                const int4 rl = p.g.srec[2 * static_cast<int64_t>(dd[r])];
-                eb[r] = rl.x;
-                ed[r] = rl.y;
-                xc += rl.w - rl.z;
+                const int64_t s2 = 2 * static_cast<int64_t>(dd[r]);
+                const int4 lo = p.g.srec[s2];
+                if (one_pass) {
+                    if (p.lattice) kx0[r] = p.g.srec[s2 + 1];
+                    const int a = tok_arc(vv[r]);
+                    if (a >= 0) kinfo[r] = p.g.arc_src[a];
+                }
+                eb[r] = lo.x;
+                ed[r] = lo.y;
+                kxb[r] = lo.z;
+                kxd[r] = lo.w - lo.z;
+                xc += lo.w - lo.z;
                 kc++;
                 ac += ed[r] - eb[r];
             }
@@ -621,8 +788,10 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         int pos = n_kept + ex.x, apos = a_kept + ex.y;
 #pragma unroll
         for (int r = 0; r < kRun; r++) {
+            krel[r] = -1;
             if (kp[r]) {
                 const int64_t rel = set0 + pos;
+                krel[r] = static_cast<int>(rel);
                 if (rel < ly.svcap) {
                     const int64_t o = ly.sv0 + rel;
                     p.sv_state[o] = dd[r];
@@ -633,28 +802,29 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
                     sh.status = WFST_ECAPACITY;
                 }
                 if (pos < kSetCache) {
-                    s_cost[pos] = tok_cost(vv[r]);
+                    s_cost[pos] = kcst[r];
                     s_epre[pos] = apos;
                     s_ebeg[pos] = eb[r];
                 }
                 if (static_cast<uint32_t>(vv[r] >> 32) == kb && atomicCAS(&sh.best_pos, -1, pos) == -1) {
                     sh.best_eb = eb[r];
                     sh.best_ed = ed[r];
-                    sh.best_cost = tok_cost(vv[r]);
+                    sh.best_cost = kcst[r];
                 }
-                t.vals[sl[r]] = (vv[r] << 32) | static_cast<uint32_t>(rel);
+                t.vals[kslot[r]] = (vv[r] << 32) | static_cast<uint32_t>(rel);
                 pos++;
                 apos += ed[r] - eb[r];
-            } else if (sl[r] >= 0) {
-                t.vals[sl[r]] = kEmptyTok;
+            } else if (kslot[r] >= 0) {
+                t.vals[kslot[r]] = kEmptyTok;
             }
         }
         n_kept += tot.x;
         a_kept += tot.y;
     }
     const int ns = n_kept;
-    // Steps 5-6 read the survivors from LDS unless the set is larger than
-    // the LDS copy; then their device-memory stores must be complete.
+    // Step 5 reads the survivors from LDS and registers unless the set is
+    // larger than the LDS copy; then their device-memory stores must be
+    // complete.
     if (G || ns > kSetCache) __syncthreads();
     else lds_barrier();
     if (ns == 0) return WFST_ENOPATH;
@@ -680,104 +850,115 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     }
 
     // ---- 5. back-pointers and lattice records ----
-    // Survivors of S_k (walked in slot-list order): the back-pointer of a
-    // token reached by an epsilon arc (its source is in S_k) and the epsilon
+    // The candidate list's first chunks of this wave, loaded ahead of the
+    // survivor pass.
+    const int nc = k > 0 ? min(sh.ncand, capC) : 0;
+    int4 cpre[2];
+#pragma unroll
+    for (int q = 0; q < 2; q++) {
+        const int i = wid * kWave + q * kT + lane;
+        cpre[q] = i < nc ? cand[i] : make_int4(0, 0, 0, 0);
+    }
+    // Survivors of S_k: the back-pointer of a token reached by an epsilon
+    // arc (its source is in S_k), of the start token, and the epsilon
     // lattice arcs inside S_k.
-    const bool set_lds = ns <= kSetCache;
-    for (int c0 = wid * kWave; c0 < n; c0 += kT) {
-        const int i = c0 + lane;
-        bool surv = false;
-        int rel = 0, a = -1;
-        int64_t s = 0;
-        float cst = 0.0f;
-        if (i < n) {
-            const int sl = static_cast<int>(tld<G>(t.slots + i));
-            const unsigned long long v = tld<G>(t.vals + sl);
-            if (v != kEmptyTok) {
-                surv = true;
-                rel = static_cast<int>(static_cast<uint32_t>(v));
-                a = static_cast<int>(static_cast<uint32_t>(v >> 32)) - 1;
-                s = static_cast<int64_t>(tld<G>(t.keys + sl));
-                cst = set_lds ? s_cost[rel - set0] : tok_cost(p.sv_tok[ly.sv0 + rel]);
+    if (one_pass) {
+        bool rec[kRun];
+        int4 r4[kRun];
+#pragma unroll
+        for (int r = 0; r < kRun; r++) {
+            const bool kept = krel[r] >= 0;
+            int src_sl = -1;
+            if (kept && kinfo[r] < 0 && kinfo[r] != -1) src_sl = tab_find<G>(t, static_cast<uint32_t>(kinfo[r]) & kDstMask);
+            // the first epsilon arc's lattice record
+            const float pc = kcst[r] + __int_as_float(kx0[r].y);
+            int dst_sl = -1;
+            if (p.lattice && kept && kxd[r] > 0 && okey(pc) <= cut)
+                dst_sl = tab_find<G>(t, static_cast<uint32_t>(kx0[r].x) & kDstMask);
+            if (kept) {
+                if (kinfo[r] == -1) p.sv_prev[ly.sv0 + krel[r]] = -1;
+                else if (kinfo[r] < 0)
+                    p.sv_prev[ly.sv0 + krel[r]] =
+                        src_sl >= 0 ? static_cast<int>(static_cast<uint32_t>(tld<G>(t.vals + src_sl))) : -1;
             }
+            const unsigned long long dv = dst_sl >= 0 ? tld<G>(t.vals + dst_sl) : kEmptyTok;
+            rec[r] = dv != kEmptyTok;
+            r4[r] = make_int4(krel[r], static_cast<int>(static_cast<uint32_t>(dv)), kx0[r].z, __float_as_int(pc));
         }
-        int info = 0;
-        int4 lo = make_int4(0, 0, 0, 0), x0 = make_int4(0, 0, 0, 0);
-        if (surv) {
-            if (a >= 0) info = p.g.arc_src[a];
-            if (p.lattice) {
-                lo = p.g.srec[2 * s];
-                x0 = p.g.srec[2 * s + 1];
-            }
-            if (a < 0) {
-                p.sv_prev[ly.sv0 + rel] = -1;
-            } else if (info < 0) {
-                const int sl = tab_find<G>(t, static_cast<uint32_t>(info) & kDstMask);
-                p.sv_prev[ly.sv0 + rel] = sl >= 0 ? static_cast<int>(static_cast<uint32_t>(tld<G>(t.vals + sl))) : -1;
-            }
+        if (p.lattice) {
+            put_records<kRun>(p.lat_x + ly.lx0, ly.lxcap, run.lat_x, &sh.nlat_x, sh, rec, r4);
+#pragma unroll
+            for (int r = 0; r < kRun; r++)
+                eps_rest<G>(p, t, sh, ly, run.lat_x, cut, krel[r] >= 0, krel[r], kcst[r], kxb[r], kxd[r]);
         }
-        if (!p.lattice) continue;
-        {
-            // the first epsilon arc, from the state record
-            bool rec = false;
-            int4 r4 = make_int4(0, 0, 0, 0);
-            const float pc = cst + __int_as_float(x0.y);
-            if (surv && lo.w > lo.z && okey(pc) <= cut) {
-                const int sl = tab_find<G>(t, static_cast<uint32_t>(x0.x) & kDstMask);
-                const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
-                rec = dv != kEmptyTok;
-                r4 = make_int4(rel, static_cast<int>(static_cast<uint32_t>(dv)), x0.z, __float_as_int(pc));
-            }
-            put_record(p.lat_x + ly.lx0, ly.lxcap, run.lat_x, &sh.nlat_x, sh, rec, r4);
-        }
-        const int xb = lo.z + 1;
-        const int xdeg = surv ? max(lo.w - lo.z - 1, 0) : 0;
-        const int incl = wave_incl_scan(xdeg);
-        const int pre = incl - xdeg;
-        const int tot = __shfl(incl, kWave - 1, kWave);
-        for (int k0 = 0; k0 < tot; k0 += kWave) {
-            const int kk = k0 + lane;
-            const int o = owner_lane(pre, kk);
-            const int ob = __shfl(xb, o, kWave);
-            const int op = __shfl(pre, o, kWave);
-            const float oc = __shfl(cst, o, kWave);
-            const int orel = __shfl(rel, o, kWave);
-            bool rec = false;
-            int4 r4 = make_int4(0, 0, 0, 0);
-            if (kk < tot) {
-                const int4 x = p.g.xarc[ob + (kk - op)];
-                const float pc = oc + __int_as_float(x.y);
-                if (okey(pc) <= cut) {
-                    const int sl = tab_find<G>(t, static_cast<uint32_t>(x.x) & kDstMask);
-                    const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
-                    rec = dv != kEmptyTok;
-                    r4 = make_int4(orel, static_cast<int>(static_cast<uint32_t>(dv)), x.z, __float_as_int(pc));
+    } else {
+        // more states than one compaction pass holds: the same from memory
+        const bool set_lds = ns <= kSetCache;
+        for (int c0 = wid * kWave; c0 < n; c0 += kT) {
+            const int i = c0 + lane;
+            bool surv = false;
+            int rel = 0, a = -1;
+            int64_t s = 0;
+            float cst = 0.0f;
+            if (i < n) {
+                const int sl = static_cast<int>(tld<G>(t.slots + i));
+                const unsigned long long v = tld<G>(t.vals + sl);
+                if (v != kEmptyTok) {
+                    surv = true;
+                    rel = static_cast<int>(static_cast<uint32_t>(v));
+                    a = static_cast<int>(static_cast<uint32_t>(v >> 32)) - 1;
+                    s = static_cast<int64_t>(tld<G>(t.keys + sl));
+                    cst = set_lds ? s_cost[rel - set0] : tok_cost(p.sv_tok[ly.sv0 + rel]);
                 }
             }
-            put_record(p.lat_x + ly.lx0, ly.lxcap, run.lat_x, &sh.nlat_x, sh, rec, r4);
+            int info = 0;
+            int4 lo = make_int4(0, 0, 0, 0), x0 = make_int4(0, 0, 0, 0);
+            if (surv) {
+                if (a >= 0) info = p.g.arc_src[a];
+                if (p.lattice) {
+                    lo = p.g.srec[2 * s];
+                    x0 = p.g.srec[2 * s + 1];
+                }
+                if (a < 0) {
+                    p.sv_prev[ly.sv0 + rel] = -1;
+                } else if (info < 0) {
+                    const int sl = tab_find<G>(t, static_cast<uint32_t>(info) & kDstMask);
+                    p.sv_prev[ly.sv0 + rel] =
+                        sl >= 0 ? static_cast<int>(static_cast<uint32_t>(tld<G>(t.vals + sl))) : -1;
+                }
+            }
+            if (p.lattice) eps_records<G>(p, t, sh, ly, run.lat_x, cut, surv, rel, cst, lo.z, lo.w - lo.z, x0);
         }
     }
     // Candidates of the expansion: the winner of each surviving destination
     // gives its back-pointer; those within the cutoff are emitting lattice arcs.
-    if (k > 0) {
-        const int nc = min(sh.ncand, capC);
-        for (int i0 = wid * kWave; i0 < nc; i0 += kT) {
-            const int i = i0 + lane;
-            bool rec = false;
-            int4 r4 = make_int4(0, 0, 0, 0);
+    for (int i0 = wid * kWave; i0 < nc; i0 += 2 * kT) {
+        int4 c4[2];
+#pragma unroll
+        for (int q = 0; q < 2; q++) {
+            const int i = i0 + q * kT + lane;
+            if (i0 == wid * kWave) c4[q] = cpre[q];
+            else c4[q] = i < nc ? cand[i] : make_int4(0, 0, 0, 0);
+        }
+        bool rec[2];
+        int4 r4[2];
+#pragma unroll
+        for (int q = 0; q < 2; q++) {
+            const int i = i0 + q * kT + lane;
+            rec[q] = false;
+            r4[q] = make_int4(0, 0, 0, 0);
             if (i < nc) {
-                const int4 c4 = cand[i];
-                const unsigned long long dv = tld<G>(t.vals + c4.w);
+                const unsigned long long dv = tld<G>(t.vals + c4[q].w);
                 if (dv != kEmptyTok) {
                     const int drel = static_cast<int>(static_cast<uint32_t>(dv));
-                    if (static_cast<uint32_t>(dv >> 32) == static_cast<uint32_t>(c4.y + 1))
-                        p.sv_prev[ly.sv0 + drel] = c4.x;
-                    rec = p.lattice && okey(__int_as_float(c4.z)) <= cut;
-                    r4 = make_int4(c4.x, drel, c4.y, c4.z);
+                    if (static_cast<uint32_t>(dv >> 32) == static_cast<uint32_t>(c4[q].y + 1))
+                        p.sv_prev[ly.sv0 + drel] = c4[q].x;
+                    rec[q] = p.lattice && okey(__int_as_float(c4[q].z)) <= cut;
+                    r4[q] = make_int4(c4[q].x, drel, c4[q].y, c4[q].z);
                 }
             }
-            if (p.lattice) put_record(p.lat_e + ly.le0, ly.lecap, run.lat_e, &sh.nlat_e, sh, rec, r4);
         }
+        if (p.lattice) put_records<2>(p.lat_e + ly.le0, ly.lecap, run.lat_e, &sh.nlat_e, sh, rec, r4);
     }
     table_barrier<G>();
     run.lat_e += sh.nlat_e;
@@ -804,7 +985,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     __shared__ uint32_t s_keys[kSlots];
     __shared__ unsigned long long s_vals[kSlots];
     __shared__ uint16_t s_slots[kFill];
-    __shared__ uint2 s_aux[2 * kGenCap];   // epsilon generations, or the select histogram
+    __shared__ uint2 s_aux[kW * kQueue];   // per-wave epsilon queues, or the select histogram
     __shared__ float s_cost[kSetCache];    // the last token set, for the next expansion
     __shared__ int32_t s_epre[kSetCache];
     __shared__ int32_t s_ebeg[kSetCache];
