@@ -304,6 +304,13 @@ def main():
             "launches": launches,
         }
         out["kernel_ms"] = {"search": search_ms, "final": s0["final_ms"]}
+        # the utterance with the most decoded frames sets the search kernel's
+        # duration: its workgroup's time per step of a frame
+        crit = max(stats, key=lambda s: s["frames_decoded"])
+        names = ["expand+queue_closure", "spill_closure", "prune", "compact", "records", "clear"]
+        out["search_steps_ms_longest_utt"] = {n: round(v, 3) for n, v in zip(names, crit["search_phase_ms"])}
+        out["finish_ms_longest_utt"] = {"backtrace": round(crit["backtrace_ms"], 3),
+                                        "lattice_prune": round(crit["lattice_prune_ms"], 3)}
     if not args.no_cpu_baseline:
         log("oracle baseline ...")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)

@@ -212,6 +212,18 @@ typedef struct wfst_stats {
                                   closure, pruning, back-pointers, lattice records */
     double final_ms;           /* final costs, backtrace, lattice pruning and output */
     int32_t search_launches;   /* launches of the search kernel */
+    /* with WFST_PROFILE: this utterance's share of the search, from the
+       device clock of its workgroup, per step of a frame summed over the
+       frames: [0] emitting expansion and the epsilon closure from the wave
+       queues, [1] closure rounds over spilled epsilon items, [2] beam and
+       max-active pruning, [3] compaction of the survivors, [4] back-pointers
+       and lattice records, [5] clearing of the token table */
+    double search_phase_ms[6];
+    /* with WFST_PROFILE: this utterance's backtrace and lattice-beam pruning,
+       from the device clock of the workgroups doing them (they run side by
+       side after the search) */
+    double backtrace_ms;
+    double lattice_prune_ms;
 } wfst_stats;
 
 int wfst_result_stats(const wfst_result *r, wfst_stats *stats);

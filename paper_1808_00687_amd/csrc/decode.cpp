@@ -329,6 +329,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.blank_thr = thr;
     p.lds_fill = test_env_int("WFSTDEC_TEST_LDS_FILL", 1 << 30);
     p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1024);
+    p.profile = tm.on ? 1 : 0;
     p.capO = z.capO;
     WallTrace wt;
     UttLayout *d_lay = nullptr;
@@ -405,8 +406,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     tm.stop(PH_SEARCH, s);
     tm.start(s);
     chk(launch_final(p, s));
-    chk(launch_backtrace(p, s));
-    if (lattice) chk(launch_lattice_backward(p, s));
+    chk(launch_finish(p, s));
     tm.stop(PH_FINAL, s);
     wt.mark("enqueue frames");
     chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
@@ -508,6 +508,16 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         r->stats.search_ms = ph[PH_SEARCH];
         r->stats.final_ms = ph[PH_FINAL];
         r->stats.search_launches = nexp;
+        if (tm.on) {
+            int khz = 0;
+            if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, G.device) == hipSuccess && khz > 0)
+            {
+                for (int i = 0; i < 6; i++)
+                    r->stats.search_phase_ms[i] = static_cast<double>(st[u].phase_ticks[i]) / khz;
+                r->stats.backtrace_ms = static_cast<double>(st[u].finish_ticks[0]) / khz;
+                r->stats.lattice_prune_ms = static_cast<double>(st[u].finish_ticks[1]) / khz;
+            }
+        }
         if ((o.flags & WFST_RECORD_TOKENS) && r->status == WFST_OK) {
             // token sets sorted by state for the caller
             const int Tp = st[u].Tp;

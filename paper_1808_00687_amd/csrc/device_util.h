@@ -123,6 +123,16 @@ __device__ __forceinline__ T ld_relaxed(T *p)
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Barrier that orders LDS only: device-memory stores issued before it need
+// not be complete.  Used where no other wave reads those stores before a
+// full barrier.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ void set_status(UttState &st, int code)
 {
     atomicCAS(&st.status, 0, code);

@@ -59,43 +59,118 @@ __global__ __launch_bounds__(256) void final_kernel(Params p)
         if (p.sv_state[ly.sv0 + i] == bs) st.final_sv = static_cast<int32_t>(i);
 }
 
-// backtrace: follow survivor back-pointers from the final token; arcs are
-// written from the end of the utterance's path region backwards.
-__global__ void backtrace_kernel(Params p)
+// backtrace (Alg. 1), one block per utterance.  Lane 0 follows the
+// survivor back-pointers from the final token, one dependent load per step,
+// and lists the survivors of the path; then the whole block turns them into
+// arcs and original frame indices (an emitting arc of decoded frame j lies
+// in frame kept[j - 1]; epsilon arcs have frame -1).  The path is written at
+// the end of the utterance's path region, last arc last.
+__device__ void backtrace_block(const Params &p, int u, int *sh)
 {
-    const int u = blockIdx.x * blockDim.x + threadIdx.x;
-    if (u >= p.U) return;
     UttState &st = p.st[u];
-    if (st.status != 0) return;
     const UttLayout &ly = p.lay[u];
-    int64_t i = st.final_sv;
-    int j = st.Tp;
-    int cnt = 0;
     const int64_t end = ly.path0 + ly.pathcap;
-    while (true) {
-        const int a = tok_arc(p.sv_tok[ly.sv0 + i]);
-        const int prev = p.sv_prev[ly.sv0 + i];
-        if (a < 0) break;
-        if (cnt >= ly.pathcap || prev < 0) {
-            set_status(st, WFST_ECAPACITY);
-            break;
+    if (threadIdx.x == 0) {
+        int64_t i = st.final_sv;
+        int cnt = 0;
+        while (true) {
+            const uint64_t t = p.sv_tok[ly.sv0 + i];
+            const int prev = p.sv_prev[ly.sv0 + i];
+            if (tok_arc(t) < 0) break;
+            if (cnt >= ly.pathcap || prev < 0) {
+                set_status(st, WFST_ECAPACITY);
+                break;
+            }
+            p.path_arc[end - 1 - cnt] = static_cast<int32_t>(i);
+            cnt++;
+            i = prev;
         }
-        const bool eps = p.g.arc_src[a] < 0;
-        int fr = -1;
-        if (!eps && j == 0) {
-            set_status(st, WFST_ECAPACITY);
-            break;
-        }
-        if (!eps) {
-            fr = p.kept[ly.kept0 + j - 1];
-            j--;
-        }
-        cnt++;
-        p.path_arc[end - cnt] = a;
-        p.path_frame[end - cnt] = fr;
-        i = prev;
+        sh[0] = cnt;
     }
-    st.path_len = cnt;
+    __syncthreads();
+    const int cnt = sh[0];
+    const int Tp = st.Tp;
+    // entry k counts from the final token backwards; its decoded frame is
+    // Tp minus the emitting arcs of entries 0 .. k - 1
+    int carry = 0;
+    for (int k0 = 0; k0 < cnt; k0 += blockDim.x) {
+        const int k = k0 + threadIdx.x;
+        int a = -1;
+        bool emit = false;
+        if (k < cnt) {
+            const int64_t i = p.path_arc[end - 1 - k];
+            a = tok_arc(p.sv_tok[ly.sv0 + i]);
+            emit = p.g.arc_src[a] >= 0;
+        }
+        int total;
+        const int before = carry + block_excl_scan(emit ? 1 : 0, sh + 1, &total);
+        if (k < cnt) {
+            int fr = -1;
+            if (emit) {
+                const int j = Tp - before;
+                if (j >= 1) fr = p.kept[ly.kept0 + j - 1];
+                else set_status(st, WFST_ECAPACITY);
+            }
+            p.path_arc[end - 1 - k] = a;
+            p.path_frame[end - 1 - k] = fr;
+        }
+        carry += total;
+    }
+    if (threadIdx.x == 0) st.path_len = cnt;
+}
+
+constexpr int kLatLds = 8192;   // survivors per token set kept in LDS by the backward pass
+constexpr int kLatT = 1024;     // threads of a finish block
+constexpr int kRE = 4;          // emitting records per thread held in registers
+constexpr int kRX = 2;          // epsilon records per thread held in registers
+constexpr int kRC = 4;          // survivors per thread held in registers
+static_assert(kRX == 2, "the epsilon records are copied out of the prefetch registers pairwise");
+
+// Where the records and survivors of one token set j lie.
+struct LatMeta {
+    int64_t b0, nB;   // S_j
+    int64_t e0, e1;   // emitting records (source in S_j, destination in S_j+1)
+    int64_t x0, x1;   // epsilon records (both ends in S_j)
+};
+
+// Inputs of one token set, loaded a set ahead of their use.
+struct LatRegs {
+    int4 e[kRE];
+    int4 x[kRX];
+    uint64_t t[kRC];
+};
+
+__device__ __forceinline__ LatMeta lat_meta(const Params &p, const UttLayout &ly, int j, int Tp)
+{
+    LatMeta m;
+    const int64_t *so = p.sv_off + ly.fo0;
+    m.b0 = so[j];
+    m.nB = so[j + 1] - so[j];
+    m.e0 = j < Tp ? p.le_off[ly.fo0 + j] : 0;
+    m.e1 = j < Tp ? p.le_off[ly.fo0 + j + 1] : 0;
+    m.x0 = p.lx_off[ly.fo0 + j];
+    m.x1 = p.lx_off[ly.fo0 + j + 1];
+    return m;
+}
+
+__device__ __forceinline__ void lat_fetch(const Params &p, const UttLayout &ly, const LatMeta &m, LatRegs &r)
+{
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int q = 0; q < kRE; q++) {
+        const int64_t i = m.e0 + tid + q * kLatT;
+        r.e[q] = i < m.e1 ? p.lat_e[ly.le0 + i] : make_int4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int q = 0; q < kRX; q++) {
+        const int64_t i = m.x0 + tid + q * kLatT;
+        r.x[q] = i < m.x1 ? p.lat_x[ly.lx0 + i] : make_int4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int q = 0; q < kRC; q++) {
+        const int64_t i = tid + q * kLatT;
+        r.t[q] = i < m.nB ? p.sv_tok[ly.sv0 + m.b0 + i] : kEmptyTok;
+    }
 }
 
 // Lattice-beam pruning, one block per utterance, token sets from last to
@@ -104,32 +179,35 @@ __global__ void backtrace_kernel(Params p)
 // into (j', d) has ex = fl(fl(p - c_j'(d)) + e(j', d)), and e(j, s) is the
 // minimum ex over its recorded out-arcs.  Epsilon arcs inside a set are
 // iterated to their fixed point (the epsilon graph is acyclic).
-__global__ __launch_bounds__(1024) void lattice_backward_kernel(Params p)
+//
+// The costs and extra costs of S_j and S_j+1 live in LDS and the records of
+// a set in registers, loaded while the previous set is processed; a set
+// larger than kLatLds is processed in device memory instead.  Kept arcs are
+// counted per set into lo_off (zeroed by the host), then turned into output
+// offsets.
+__device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh)
 {
-    __shared__ int sh_changed;
-    __shared__ long long sh_cnt;
-    const int u = blockIdx.x;
     UttState &st = p.st[u];
-    if (st.status != 0) return;
     const UttLayout &ly = p.lay[u];
+    const int tid = threadIdx.x;
     const int Tp = st.Tp;
     const float lb = p.lattice_beam;
     const float B = st.final_cost;
     const bool use_final = p.g.final_w != nullptr && st.reached_final;
-    uint32_t *e = p.e_key + ly.sv0;
+    uint32_t *eg = p.e_key + ly.sv0;
+    const uint64_t *tok = p.sv_tok + ly.sv0;
     const int64_t *so = p.sv_off + ly.fo0;
-    const int64_t ntok = so[Tp + 1];
+    unsigned long long *kcnt = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
     const uint32_t kinf = okey(__int_as_float(0x7F800000));
-    for (int64_t i = threadIdx.x; i < ntok; i += blockDim.x) e[i] = kinf;
     // Records were appended token set by token set, so the records of set j
     // are those whose source survivor lies in S_j: locate each set's range by
     // binary search on the source index.
     const int64_t ne = st.le_cnt, nx = st.lx_cnt;
-    for (int j = threadIdx.x; j <= Tp + 1; j += blockDim.x) {
+    for (int j = tid; j <= Tp + 1; j += blockDim.x) {
         const int64_t lo_sv = so[j];
         int64_t a = 0, b = ne;
         while (a < b) {
-            int64_t mid = (a + b) >> 1;
+            const int64_t mid = (a + b) >> 1;
             if (p.lat_e[ly.le0 + mid].x < lo_sv) a = mid + 1;
             else b = mid;
         }
@@ -137,86 +215,225 @@ __global__ __launch_bounds__(1024) void lattice_backward_kernel(Params p)
         a = 0;
         b = nx;
         while (a < b) {
-            int64_t mid = (a + b) >> 1;
+            const int64_t mid = (a + b) >> 1;
             if (p.lat_x[ly.lx0 + mid].x < lo_sv) a = mid + 1;
             else b = mid;
         }
         p.lx_off[ly.fo0 + j] = a;
     }
     __syncthreads();
-    {
-        const int64_t a = p.sv_off[ly.fo0 + Tp], b = p.sv_off[ly.fo0 + Tp + 1];
-        for (int64_t i = a + threadIdx.x; i < b; i += blockDim.x) {
-            int s = p.sv_state[ly.sv0 + i];
-            float c = tok_cost(p.sv_tok[ly.sv0 + i]);
-            float tot = c + (use_final ? p.g.final_w[s] : 0.0f);
-            e[i] = okey(tot - B);
-        }
-    }
-    __syncthreads();
+    int *flag = sh;   // three rotating "changed" flags of the epsilon rounds
+    int hA = 0;          // LDS half holding S_j+1
+    bool a_lds = false;  // S_j+1's costs and extra costs are in that half
+    LatMeta mc = lat_meta(p, ly, Tp, Tp);
+    LatRegs cur;
+    lat_fetch(p, ly, mc, cur);
     for (int j = Tp; j >= 0; j--) {
-        if (threadIdx.x == 0) sh_cnt = 0;
-        __syncthreads();
-        long long kept = 0;
-        if (j < Tp) {
-            const int64_t r0 = p.le_off[ly.fo0 + j], r1 = p.le_off[ly.fo0 + j + 1];
-            for (int64_t r = r0 + threadIdx.x; r < r1; r += blockDim.x) {
-                int4 x = p.lat_e[ly.le0 + r];
-                float cd = tok_cost(p.sv_tok[ly.sv0 + x.y]);
-                float ed = okey_val(ld_relaxed(e + x.y));
-                float d1 = __int_as_float(x.w) - cd;
-                float ex = d1 + ed;
+        const int64_t a0 = so[j + 1], nA = j < Tp ? so[j + 2] - a0 : 0;
+        const bool g = mc.nB > kLatLds || nA > kLatLds;
+        const int hB = hA ^ 1;
+        uint32_t *eA = s_e + hA * kLatLds, *eB = s_e + hB * kLatLds;
+        float *cA = s_c + hA * kLatLds, *cB = s_c + hB * kLatLds;
+        const int64_t b0 = mc.b0, nB = mc.nB;
+        LatMeta mn{};
+        if (j > 0) mn = lat_meta(p, ly, j - 1, Tp);
+        unsigned long long kept = 0;
+        if (!g) {
+            // ---- S_j and S_j+1 in LDS, records in registers ----
+            if (tid == 0) flag[0] = 0;
+#pragma unroll
+            for (int q = 0; q < kRC; q++) {
+                const int64_t i = tid + q * kLatT;
+                if (i < nB) cB[i] = tok_cost(cur.t[q]);
+            }
+            for (int64_t i = tid + kRC * kLatT; i < nB; i += kLatT) cB[i] = tok_cost(tok[b0 + i]);
+            if (j == Tp) {
+                for (int64_t i = tid; i < nB; i += kLatT) {
+                    const float c = tok_cost(tok[b0 + i]);
+                    const float f = use_final ? p.g.final_w[p.sv_state[ly.sv0 + b0 + i]] : 0.0f;
+                    eB[i] = okey((c + f) - B);
+                }
+            } else {
+                for (int64_t i = tid; i < nB; i += kLatT) eB[i] = kinf;
+            }
+            if (!a_lds) {
+                // S_j+1 was processed in device memory: bring it into LDS
+                for (int64_t i = tid; i < nA; i += kLatT) {
+                    eA[i] = ld_relaxed(eg + a0 + i);
+                    cA[i] = tok_cost(tok[a0 + i]);
+                }
+            }
+            lds_barrier();
+            // emitting arcs into S_j+1
+#pragma unroll
+            for (int q = 0; q < kRE; q++) {
+                const int64_t r = mc.e0 + tid + q * kLatT;
+                if (r < mc.e1) {
+                    const int4 x = cur.e[q];
+                    const float d1 = __int_as_float(x.w) - cA[x.y - a0];
+                    const float ex = d1 + okey_val(eA[x.y - a0]);
+                    p.ex_e[ly.le0 + r] = ex;
+                    atomicMin(eB + (x.x - b0), okey(ex));
+                    kept += ex <= lb;
+                }
+            }
+            for (int64_t r = mc.e0 + tid + kRE * kLatT; r < mc.e1; r += kLatT) {
+                const int4 x = p.lat_e[ly.le0 + r];
+                const float d1 = __int_as_float(x.w) - cA[x.y - a0];
+                const float ex = d1 + okey_val(eA[x.y - a0]);
                 p.ex_e[ly.le0 + r] = ex;
-                atomicMin(e + x.x, okey(ex));
+                atomicMin(eB + (x.x - b0), okey(ex));
                 kept += ex <= lb;
             }
-        }
-        __syncthreads();
-        const int64_t q0 = p.lx_off[ly.fo0 + j], q1 = p.lx_off[ly.fo0 + j + 1];
-        if (q1 > q0) {
-            while (true) {
-                if (threadIdx.x == 0) sh_changed = 0;
-                __syncthreads();
-                int changed = 0;
-                for (int64_t r = q0 + threadIdx.x; r < q1; r += blockDim.x) {
-                    int4 x = p.lat_x[ly.lx0 + r];
-                    float cd = tok_cost(p.sv_tok[ly.sv0 + x.y]);
-                    float ed = okey_val(ld_relaxed(e + x.y));
-                    float d1 = __int_as_float(x.w) - cd;
-                    float ex = d1 + ed;
-                    p.ex_x[ly.lx0 + r] = ex;
-                    uint32_t kx = okey(ex);
-                    if (kx < ld_relaxed(e + x.x)) {
-                        atomicMin(e + x.x, kx);
-                        changed = 1;
+            // the next set's inputs, in flight during the epsilon rounds
+            const int4 x_cur[kRX] = {cur.x[0], cur.x[1]};
+            if (j > 0) lat_fetch(p, ly, mn, cur);
+            lds_barrier();
+            if (mc.x1 > mc.x0) {
+                float exr[kRX];
+                unsigned long long kx = 0;
+                for (int it = 0;; it++) {
+                    if (tid == 0) flag[(it + 1) % 3] = 0;
+                    int changed = 0;
+                    kx = 0;
+#pragma unroll
+                    for (int q = 0; q < kRX; q++) {
+                        const int64_t r = mc.x0 + tid + q * kLatT;
+                        exr[q] = 0.0f;
+                        if (r < mc.x1) {
+                            const int4 x = x_cur[q];
+                            const float d1 = __int_as_float(x.w) - cB[x.y - b0];
+                            const float ex = d1 + okey_val(eB[x.y - b0]);
+                            exr[q] = ex;
+                            const uint32_t k = okey(ex);
+                            if (k < eB[x.x - b0]) {
+                                atomicMin(eB + (x.x - b0), k);
+                                changed = 1;
+                            }
+                            kx += ex <= lb;
+                        }
                     }
+                    for (int64_t r = mc.x0 + tid + kRX * kLatT; r < mc.x1; r += kLatT) {
+                        const int4 x = p.lat_x[ly.lx0 + r];
+                        const float d1 = __int_as_float(x.w) - cB[x.y - b0];
+                        const float ex = d1 + okey_val(eB[x.y - b0]);
+                        p.ex_x[ly.lx0 + r] = ex;
+                        const uint32_t k = okey(ex);
+                        if (k < eB[x.x - b0]) {
+                            atomicMin(eB + (x.x - b0), k);
+                            changed = 1;
+                        }
+                        kx += ex <= lb;
+                    }
+                    if (changed) flag[it % 3] = 1;
+                    lds_barrier();
+                    if (!flag[it % 3]) break;
                 }
-                if (changed) sh_changed = 1;
-                __threadfence_block();
-                __syncthreads();
-                const int again = sh_changed;
-                __syncthreads();
-                if (!again) break;
+                // the last round changed nothing: its extra costs are final
+#pragma unroll
+                for (int q = 0; q < kRX; q++) {
+                    const int64_t r = mc.x0 + tid + q * kLatT;
+                    if (r < mc.x1) p.ex_x[ly.lx0 + r] = exr[q];
+                }
+                kept += kx;
             }
-            for (int64_t r = q0 + threadIdx.x; r < q1; r += blockDim.x) kept += p.ex_x[ly.lx0 + r] <= lb;
+            // a following set processed in device memory reads S_j there
+            const bool next_g = j > 0 && (mn.nB > kLatLds || nB > kLatLds);
+            if (next_g)
+                for (int64_t i = tid; i < nB; i += kLatT) eg[b0 + i] = eB[i];
+        } else {
+            // ---- a set larger than the LDS arrays: device memory ----
+            for (int64_t i = tid; i < nB; i += kLatT) {
+                uint32_t e0 = kinf;
+                if (j == Tp) {
+                    const float c = tok_cost(tok[b0 + i]);
+                    const float f = use_final ? p.g.final_w[p.sv_state[ly.sv0 + b0 + i]] : 0.0f;
+                    e0 = okey((c + f) - B);
+                }
+                eg[b0 + i] = e0;
+            }
+            __syncthreads();
+            for (int64_t r = mc.e0 + tid; r < mc.e1; r += kLatT) {
+                const int4 x = p.lat_e[ly.le0 + r];
+                const float d1 = __int_as_float(x.w) - tok_cost(tok[x.y]);
+                const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
+                p.ex_e[ly.le0 + r] = ex;
+                atomicMin(eg + x.x, okey(ex));
+                kept += ex <= lb;
+            }
+            if (j > 0) lat_fetch(p, ly, mn, cur);
+            __syncthreads();
+            if (mc.x1 > mc.x0) {
+                unsigned long long kx = 0;
+                while (true) {
+                    if (tid == 0) flag[0] = 0;
+                    __syncthreads();
+                    int changed = 0;
+                    kx = 0;
+                    for (int64_t r = mc.x0 + tid; r < mc.x1; r += kLatT) {
+                        const int4 x = p.lat_x[ly.lx0 + r];
+                        const float d1 = __int_as_float(x.w) - tok_cost(tok[x.y]);
+                        const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
+                        p.ex_x[ly.lx0 + r] = ex;
+                        const uint32_t k = okey(ex);
+                        if (k < ld_relaxed(eg + x.x)) {
+                            atomicMin(eg + x.x, k);
+                            changed = 1;
+                        }
+                        kx += ex <= lb;
+                    }
+                    if (changed) flag[0] = 1;
+                    __syncthreads();
+                    const int again = flag[0];
+                    __syncthreads();
+                    if (!again) break;
+                }
+                kept += kx;
+            }
         }
-        kept = wave_sum_ll(kept);
-        if (lane_id() == 0 && kept) atomicAdd(reinterpret_cast<unsigned long long *>(&sh_cnt), static_cast<unsigned long long>(kept));
-        __syncthreads();
-        if (threadIdx.x == 0) p.lo_off[ly.fo0 + j] = sh_cnt;
-        __syncthreads();
+        kept = static_cast<unsigned long long>(wave_sum_ll(static_cast<long long>(kept)));
+        if (lane_id() == 0 && kept) atomicAdd(kcnt + j, kept);
+        hA = hB;
+        a_lds = !g;
+        mc = mn;
     }
-    // exclusive prefix over token sets -> output offsets
+    __syncthreads();
+    // kept arcs per set -> output offsets (exclusive prefix over the sets)
+    int64_t carry = 0;
+    for (int j0 = 0; j0 <= Tp; j0 += blockDim.x) {
+        const int j = j0 + tid;
+        const int64_t c = j <= Tp ? static_cast<int64_t>(ld_relaxed(kcnt + j)) : 0;
+        int total;
+        const int ex = block_excl_scan(static_cast<int>(c), sh + 4, &total);
+        if (j <= Tp) p.lo_off[ly.fo0 + j] = carry + ex;
+        carry += total;
+    }
+    if (tid == 0) {
+        p.lo_off[ly.fo0 + Tp + 1] = carry;
+        st.lat_kept = carry;
+    }
+}
+
+// Blocks [0, U): backtrace of utterance b; blocks [U, 2U) (with a lattice):
+// lattice-beam pruning of utterance b - U.  The two are independent and run
+// side by side.
+__global__ __launch_bounds__(kLatT) void finish_kernel(Params p)
+{
+    __shared__ uint32_t s_e[2 * kLatLds];
+    __shared__ float s_c[2 * kLatLds];
+    __shared__ __align__(8) int sh[24];   // flags, a 64-bit count, scan scratch (17 ints)
+    const int b = blockIdx.x;
+    const int u = b < p.U ? b : b - p.U;
+    if (p.st[u].status != 0) return;
     if (threadIdx.x == 0) {
-        int64_t run = 0;
-        for (int j = 0; j <= Tp; j++) {
-            int64_t c = p.lo_off[ly.fo0 + j];
-            p.lo_off[ly.fo0 + j] = run;
-            run += c;
-        }
-        p.lo_off[ly.fo0 + Tp + 1] = run;
-        st.lat_kept = run;
+        sh[0] = 0;
+        *reinterpret_cast<long long *>(sh + 2) = 0;
     }
+    __syncthreads();
+    const uint64_t t0 = p.profile ? wall_clock64() : 0;
+    if (b < p.U) backtrace_block(p, u, sh);
+    else lattice_block(p, u, s_e, s_c, sh);
+    if (p.profile && threadIdx.x == 0) p.st[u].finish_ticks[b < p.U ? 0 : 1] = wall_clock64() - t0;
 }
 
 __device__ __forceinline__ void cas16(int4 *v, int i, int j)
@@ -318,15 +535,9 @@ hipError_t launch_final(const Params &p, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_backtrace(const Params &p, hipStream_t s)
+hipError_t launch_finish(const Params &p, hipStream_t s)
 {
-    hipLaunchKernelGGL(backtrace_kernel, dim3((p.U + 63) / 64), dim3(64), 0, s, p);
-    return hipGetLastError();
-}
-
-hipError_t launch_lattice_backward(const Params &p, hipStream_t s)
-{
-    hipLaunchKernelGGL(lattice_backward_kernel, dim3(p.U), dim3(1024), 0, s, p);
+    hipLaunchKernelGGL(finish_kernel, dim3(p.lattice ? 2 * p.U : p.U), dim3(kLatT), 0, s, p);
     return hipGetLastError();
 }
 

@@ -79,6 +79,8 @@ struct UttState {
     int32_t path_len;
     int32_t pad1;
     int64_t lat_kept;
+    uint64_t phase_ticks[6];   // device clock ticks per search step (profiling only)
+    uint64_t finish_ticks[2];  // device clock ticks of the backtrace and the lattice pruning
 };
 
 // Per-utterance regions inside the shared workspace buffers (element offsets).
@@ -105,6 +107,7 @@ struct Params {
     float blank_thr;
     int32_t lds_fill;         // states per frame the LDS token table takes (<= its fill limit)
     int32_t gen_lds;          // epsilon items per wave queue in LDS (<= its capacity)
+    int32_t profile;          // count device clock ticks per search step
     UttState *st;
     const UttLayout *lay;
     // survivors (per utterance regions)
@@ -145,8 +148,7 @@ struct Params {
 hipError_t launch_classify(const Params &p, hipStream_t s);
 hipError_t launch_search(const Params &p, hipStream_t s);
 hipError_t launch_final(const Params &p, hipStream_t s);
-hipError_t launch_backtrace(const Params &p, hipStream_t s);
-hipError_t launch_lattice_backward(const Params &p, hipStream_t s);
+hipError_t launch_finish(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
 
 // ---- host helpers (graph.cpp) ----

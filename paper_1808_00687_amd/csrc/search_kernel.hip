@@ -71,16 +71,6 @@ __device__ __forceinline__ T tld(const T *ptr)
         return *ptr;
 }
 
-// Barrier that orders LDS only: device-memory stores issued before it need
-// not be complete.  Used where no other wave reads those stores before a
-// full barrier.
-__device__ __forceinline__ void lds_barrier()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
 // With the table in device memory its own stores need the full barrier.
 template <bool G>
 __device__ __forceinline__ void table_barrier()
@@ -130,7 +120,20 @@ struct Run {
     int64_t arcs;
     int gframes;
     long long eps;       // epsilon out-arcs of survivors (this thread's share)
+    uint64_t ph[6];      // device clock ticks per step (thread 0, profiling)
+    uint64_t t_last;
 };
+
+// Profiling: thread 0 adds the device clock since the previous mark to step
+// i (i < 0 only sets the mark).
+__device__ __forceinline__ void phase_mark(const Params &p, Run &run, int i)
+{
+    if (p.profile && threadIdx.x == 0) {
+        const uint64_t t = wall_clock64();
+        if (i >= 0) run.ph[i] += t - run.t_last;
+        run.t_last = t;
+    }
+}
 
 template <bool G>
 __device__ __forceinline__ int tab_find(const Tab<G> &t, uint32_t d)
@@ -628,6 +631,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         sh.best_pos = -1;
     }
     __syncthreads();
+    phase_mark(p, run, -1);
 
     // ---- 1. expansion ----
     if (k == 0) {
@@ -652,6 +656,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     drain<G>(p, t, sh, wq);
     // full barrier: spilled items and the candidate list are read by other waves
     __syncthreads();
+    phase_mark(p, run, 0);
     int sp = 0;
     while (true) {
         const int total = min(sh.spill_n[sp], gcap);
@@ -674,6 +679,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         __syncthreads();
         sp ^= 1;
     }
+    phase_mark(p, run, 1);
     if (sh.overflow) return kOverflow;
     if (sh.status) return sh.status;
 
@@ -725,6 +731,8 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         }
         __syncthreads();
     }
+
+    phase_mark(p, run, 2);
 
     // ---- 4. compaction into S_k, in slot-list order ----
     // With one pass (n <= kT * kRun) each thread keeps its survivors' state
@@ -827,6 +835,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     // complete.
     if (G || ns > kSetCache) __syncthreads();
     else lds_barrier();
+    phase_mark(p, run, 3);
     if (ns == 0) return WFST_ENOPATH;
     if (sh.status) return sh.status;
     if (tid == 0) {
@@ -961,6 +970,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         if (p.lattice) put_records<2>(p.lat_e + ly.le0, ly.lecap, run.lat_e, &sh.nlat_e, sh, rec, r4);
     }
     table_barrier<G>();
+    phase_mark(p, run, 4);
     run.lat_e += sh.nlat_e;
     run.lat_x += sh.nlat_x;
     if (sh.status) return sh.status;
@@ -977,6 +987,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         t.vals[s2] = kEmptyTok;
     }
     table_barrier<G>();
+    phase_mark(p, run, 5);
     return 0;
 }
 
@@ -1066,6 +1077,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
         st.arcs_expanded = run.arcs;
         st.eps_arcs = static_cast<int64_t>(sh.eps_sum);
         st.gframes = run.gframes;
+        for (int i = 0; i < 6; i++) st.phase_ticks[i] = run.ph[i];
         if (rc != 0) st.status = rc;
     }
 }

@@ -55,7 +55,9 @@ class _Stats(C.Structure):
     _fields_ = [("frames", C.c_int32), ("frames_decoded", C.c_int32), ("tokens", C.c_int64),
                 ("tokens_last", C.c_int64), ("arcs_expanded", C.c_int64), ("eps_arcs", C.c_int64), ("lattice_raw", C.c_int64),
                 ("lattice_kept", C.c_int64), ("decode_ms", C.c_double), ("search_ms", C.c_double),
-                ("final_ms", C.c_double), ("search_launches", C.c_int32)]
+                ("final_ms", C.c_double), ("search_launches", C.c_int32),
+                ("search_phase_ms", C.c_double * 6), ("backtrace_ms", C.c_double),
+                ("lattice_prune_ms", C.c_double)]
 
 
 class _LatArc(C.Structure):
@@ -228,6 +230,7 @@ def _collect(h, lattice: bool, tokens: bool) -> WfstResult:
     s = _Stats()
     _check(_lib.wfst_result_stats(h, C.byref(s)), "wfst_result_stats")
     r.stats = {f: getattr(s, f) for f, _ in _Stats._fields_}
+    r.stats["search_phase_ms"] = list(s.search_phase_ms)
     if st != WFST_OK:
         return r
     cost, fs, rf, n = C.c_float(), C.c_int32(), C.c_int32(), C.c_int32()
