@@ -303,11 +303,11 @@ def main():
             "avg_launch_us": dur_s * 1e6,
             "launches": launches,
         }
-        out["kernel_ms"] = {"search": search_ms, "final": s0["final_ms"]}
+        out["kernel_ms"] = {"search": search_ms, "record": s0["record_ms"], "final": s0["final_ms"]}
         # the utterance with the most decoded frames sets the search kernel's
         # duration: its workgroup's time per step of a frame
         crit = max(stats, key=lambda s: s["frames_decoded"])
-        names = ["expand+queue_closure", "spill_closure", "prune", "compact", "records", "clear"]
+        names = ["expand+queue_closure", "spill_closure", "prune", "compact", "clear", "wave0_expand"]
         out["search_steps_ms_longest_utt"] = {n: round(v, 3) for n, v in zip(names, crit["search_phase_ms"])}
         out["finish_ms_longest_utt"] = {"backtrace": round(crit["backtrace_ms"], 3),
                                         "lattice_prune": round(crit["lattice_prune_ms"], 3)}

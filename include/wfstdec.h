@@ -209,15 +209,17 @@ typedef struct wfst_stats {
     /* with WFST_PROFILE (batch-wide, the same in every result of a batch):
        device time summed over launches, measured with HIP events */
     double search_ms;          /* token passing over all frames: expansion, epsilon
-                                  closure, pruning, back-pointers, lattice records */
+                                  closure, pruning */
+    double record_ms;          /* back-pointers and raw lattice records of every frame */
     double final_ms;           /* final costs, backtrace, lattice pruning and output */
     int32_t search_launches;   /* launches of the search kernel */
     /* with WFST_PROFILE: this utterance's share of the search, from the
        device clock of its workgroup, per step of a frame summed over the
        frames: [0] emitting expansion and the epsilon closure from the wave
        queues, [1] closure rounds over spilled epsilon items, [2] beam and
-       max-active pruning, [3] compaction of the survivors, [4] back-pointers
-       and lattice records, [5] clearing of the token table */
+       max-active pruning, [3] compaction of the survivors, [4] clearing of
+       the token table; [5] the emitting expansion as the first wave sees it
+       (part of [0]) */
     double search_phase_ms[6];
     /* with WFST_PROFILE: this utterance's backtrace and lattice-beam pruning,
        from the device clock of the workgroups doing them (they run side by

@@ -188,8 +188,8 @@ struct Sizes {
     int64_t capF;      // tokens per frame
     int64_t capT;      // reached states per frame
     int64_t capO;      // overflow epsilon items per frame (per generation)
-    int64_t capC;      // emitting candidates per frame
-    int64_t lat_mult;  // lattice records per token
+    int64_t em;        // emitting lattice-record slots per token (emitting out-degree)
+    int64_t xm;        // epsilon lattice-record slots per token (epsilon out-degree)
 };
 
 // Events for phase timing, kept for reuse across calls: creating thousands
@@ -277,7 +277,7 @@ struct WallTrace {
     }
 };
 
-enum { PH_SEARCH = 0, PH_FINAL = 1, PH_COUNT = 2 };
+enum { PH_SEARCH = 0, PH_RECORD = 1, PH_FINAL = 2, PH_COUNT = 3 };
 
 // One attempt at decoding the batch with the given buffer sizes.  Returns
 // WFST_OK, an error, or WFST_ECAPACITY when a buffer overflowed.
@@ -301,11 +301,14 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         // survivor indices are 32-bit; one frame may reach capF tokens
         l.svcap = std::min<int64_t>((Tu + 1) * z.capA + z.capF, std::numeric_limits<int32_t>::max());
         sv += l.svcap;
+        // a set's emitting region holds one candidate (and one lattice record)
+        // per emitting out-arc of its tokens, its epsilon region one lattice
+        // record per epsilon out-arc
         l.le0 = le;
-        l.lecap = lattice ? (Tu * z.capA + z.capF) * z.lat_mult : 0;
+        l.lecap = (Tu * z.capA + z.capF) * z.em;
         le += l.lecap;
         l.lx0 = lx;
-        l.lxcap = lattice ? ((Tu + 1) * z.capA + z.capF) * std::max<int64_t>(z.lat_mult / 2, 1) : 0;
+        l.lxcap = lattice ? ((Tu + 1) * z.capA + z.capF) * z.xm : 0;
         lx += l.lxcap;
         l.fo0 = fo;
         fo += Tu + 2;
@@ -342,18 +345,19 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         p.gvals = a.get<unsigned long long>(U * p.capG);
         p.gslots = a.get<int32_t>(U * p.capG);
         p.gspill = a.get<uint2>(U * 2 * p.capO);
-        p.cand = a.get<int4>(U * p.capC);
         p.sv_state = a.get<int32_t>(sv);
         p.sv_tok = a.get<uint64_t>(sv);
         p.sv_prev = a.get<int32_t>(sv);
         p.sv_ebeg = a.get<int32_t>(sv);
         p.sv_epre = a.get<int32_t>(sv);
+        p.sv_x = a.get<int4>(sv);
+        p.cand = a.get<int4>(le);
         p.e_key = lattice ? a.get<uint32_t>(sv) : nullptr;
         p.lat_e = lattice ? a.get<int4>(le) : nullptr;
         p.lat_x = lattice ? a.get<int4>(lx) : nullptr;
         p.ex_e = lattice ? a.get<float>(le) : nullptr;
         p.ex_x = lattice ? a.get<float>(lx) : nullptr;
-        fo_all = a.get<int64_t>(4 * fo);
+        fo_all = a.get<int64_t>(7 * fo);
         p.cut_arr = a.get<uint32_t>(fo);
         p.kept = a.get<int32_t>(kp);
         p.path_arc = a.get<int32_t>(pa);
@@ -362,7 +366,6 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.capG = 8192;
     while (p.capG < z.capT) p.capG *= 2;
     p.capO = z.capO;
-    p.capC = z.capC;
     Arena measure;
     carve(measure);
     ArenaLease lease;
@@ -381,6 +384,9 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.le_off = fo_all + fo;
     p.lx_off = fo_all + 2 * fo;
     p.lo_off = fo_all + 3 * fo;
+    p.le_cnt = fo_all + 4 * fo;
+    p.lx_cnt = fo_all + 5 * fo;
+    p.cand_cnt = fo_all + 6 * fo;
 
     std::vector<UttState> st(U);
     for (int u = 0; u < U; u++) {
@@ -394,7 +400,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     };
     chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
-    chk(hipMemsetAsync(fo_all, 0, 4 * fo * sizeof(int64_t), s));
+    chk(hipMemsetAsync(fo_all, 0, 7 * fo * sizeof(int64_t), s));
     chk(launch_classify(p, s));
     // decoded frames are at most the frames: size the per-frame launches by T
     int Tmax = 0;
@@ -404,6 +410,9 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     tm.start(s);
     chk(launch_search(p, s));
     tm.stop(PH_SEARCH, s);
+    tm.start(s);
+    chk(launch_record(p, Tmax, s));
+    tm.stop(PH_RECORD, s);
     tm.start(s);
     chk(launch_final(p, s));
     chk(launch_finish(p, s));
@@ -492,7 +501,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     wt.mark("copy results");
     if (e != hipSuccess) return hip_fail(e, "decode: results");
 
-    double ph[PH_COUNT] = {0, 0};
+    double ph[PH_COUNT] = {0, 0, 0};
     int nexp = 0;
     for (const auto &x : tm.spans) {
         float ms = 0.0f;
@@ -506,6 +515,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         r->kept.assign(kept_h.begin() + lay[u].kept0, kept_h.begin() + lay[u].kept0 + st[u].Tp);
         r->stats.decode_ms = wall;
         r->stats.search_ms = ph[PH_SEARCH];
+        r->stats.record_ms = ph[PH_RECORD];
         r->stats.final_ms = ph[PH_FINAL];
         r->stats.search_launches = nexp;
         if (tm.on) {
@@ -610,12 +620,16 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
     else if (o.max_active > 0) z.capF = std::min<int64_t>(N, o.max_active + o.max_active / 4 + 256);
     else z.capF = std::min<int64_t>(N, 65536);
     z.capT = std::min<int64_t>(N, std::max<int64_t>(16 * z.capF, 4096));
-    // a frame offers each emitting arc at most once; epsilon items of one
-    // generation are bounded by the candidates that produce them
+    // epsilon items of one generation are bounded by the candidates that
+    // produce them
     const int64_t E = G.d.e;
-    z.capC = std::min<int64_t>(G.d.n_emit + 1, std::max<int64_t>(2 * z.capT, 65536));
     z.capO = std::min<int64_t>(E + 1, std::max<int64_t>(2 * z.capT, 65536));
-    z.lat_mult = 2;
+    // lattice-record slots per token: what the last decodes on this graph
+    // needed, else twice the graph's mean out-degrees
+    z.em = G.rec_em.load();
+    z.xm = G.rec_xm.load();
+    if (z.em <= 0) z.em = std::max<int64_t>(2, 2 * G.d.n_emit / std::max<int64_t>(N, 1) + 1);
+    if (z.xm <= 0) z.xm = std::max<int64_t>(1, 2 * G.d.n_eps / std::max<int64_t>(N, 1) + 1);
     // average tokens per frame: start from what the last calls needed
     static std::atomic<int64_t> learned_capA{2048};
     z.capA = std::min<int64_t>(z.capF, learned_capA.load());
@@ -630,8 +644,8 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
             z.capA = std::min<int64_t>(z.capF, z.capA * 4);
             z.capT = std::min<int64_t>(N, z.capT * 4);
             z.capO = std::min<int64_t>(E + 1, z.capO * 2);
-            z.capC = std::min<int64_t>(G.d.n_emit + 1, z.capC * 2);
-            z.lat_mult *= 2;
+            z.em *= 2;
+            z.xm *= 2;
         }
         rc = run_batch(G, n_utt, ll.data(), T, L, o, thr, s, z, res, t0);
     }
@@ -639,6 +653,16 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
         int64_t cur = learned_capA.load();
         while (z.capA > cur && !learned_capA.compare_exchange_weak(cur, z.capA)) {
         }
+        // the slots per token this batch needed, with a margin
+        int64_t em = 1, xm = 1;
+        for (int u = 0; u < n_utt; u++) {
+            const wfst_stats &x = res[u]->stats;
+            const int64_t tok = std::max<int64_t>(x.tokens, 1);
+            em = std::max<int64_t>(em, (5 * x.arcs_expanded / tok) / 4 + 1);
+            xm = std::max<int64_t>(xm, (5 * x.eps_arcs / tok) / 4 + 1);
+        }
+        G.rec_em.store(std::min(em, z.em));
+        G.rec_xm.store(std::min(xm, z.xm));
     }
     if (rc != WFST_OK) {
         for (int u = 0; u < n_utt; u++) delete res[u];

@@ -51,6 +51,18 @@ __device__ __forceinline__ uint32_t drop_bound(uint32_t m_key, float beam)
     return okey(okey_val(m_key) + beam);
 }
 
+// Load through a pointer known to address device memory (a global rather
+// than a flat access, which would also wait on LDS traffic).
+template <typename T>
+__device__ __forceinline__ T ldg(const T *ptr)
+{
+    return *(const __attribute__((address_space(1))) T *)ptr;
+}
+
+// Multiplicative hash of a state id for the open-addressing tables (the
+// high bits index the table).
+__device__ __forceinline__ uint32_t hash_state(uint32_t d) { return d * 0x9E3779B1u; }
+
 __device__ __forceinline__ int lane_id() { return static_cast<int>(__lane_id()); }
 
 __device__ __forceinline__ uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
@@ -136,6 +148,62 @@ __device__ __forceinline__ void lds_barrier()
 __device__ __forceinline__ void set_status(UttState &st, int code)
 {
     atomicCAS(&st.status, 0, code);
+}
+
+// Largest t in [0, n) with epre[t] <= a (epre non-decreasing, epre[0] <= a).
+__device__ __forceinline__ int search_le(const int32_t *epre, int n, int a)
+{
+    const int lane = lane_id();
+    int lo = 0, end = n;
+    while (end - lo > 1) {
+        const int step = (end - lo + kWave - 1) / kWave;
+        const int idx = lo + lane * step;
+        const int v = idx < end ? epre[idx] : 0x7FFFFFFF;
+        const uint64_t m = __ballot(v <= a);
+        const int l = 63 - __clzll(static_cast<long long>(m));
+        lo += l * step;
+        end = min(lo + step, end);
+    }
+    return lo;
+}
+
+
+// Three block-wide exclusive scans at once (blockDim.x a multiple of 64, at
+// most 1024); `sh` needs 51 ints.  Returns the exclusive prefixes and stores
+// the block totals in *total.
+__device__ __forceinline__ int3 block_scan3(int x, int y, int z, int *sh, int3 *total)
+{
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int nw = blockDim.x / kWave;
+    const int ix = wave_incl_scan(x), iy = wave_incl_scan(y), iz = wave_incl_scan(z);
+    if (lane == kWave - 1) {
+        sh[w] = ix;
+        sh[16 + w] = iy;
+        sh[32 + w] = iz;
+    }
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+        const int vx = threadIdx.x < nw ? sh[threadIdx.x] : 0;
+        const int vy = threadIdx.x < nw ? sh[16 + threadIdx.x] : 0;
+        const int vz = threadIdx.x < nw ? sh[32 + threadIdx.x] : 0;
+        const int sx = wave_incl_scan(vx), sy = wave_incl_scan(vy), sz = wave_incl_scan(vz);
+        if (threadIdx.x < nw) {
+            sh[threadIdx.x] = sx - vx;
+            sh[16 + threadIdx.x] = sy - vy;
+            sh[32 + threadIdx.x] = sz - vz;
+        }
+        if (threadIdx.x == kWave - 1) {
+            sh[48] = sx;
+            sh[49] = sy;
+            sh[50] = sz;
+        }
+    }
+    __syncthreads();
+    const int3 r = make_int3(ix - x + sh[w], iy - y + sh[16 + w], iz - z + sh[32 + w]);
+    *total = make_int3(sh[48], sh[49], sh[50]);
+    __syncthreads();
+    return r;
 }
 
 // Block-wide exclusive scan of one int per thread (blockDim.x a multiple of

@@ -147,9 +147,9 @@ __device__ __forceinline__ LatMeta lat_meta(const Params &p, const UttLayout &ly
     m.b0 = so[j];
     m.nB = so[j + 1] - so[j];
     m.e0 = j < Tp ? p.le_off[ly.fo0 + j] : 0;
-    m.e1 = j < Tp ? p.le_off[ly.fo0 + j + 1] : 0;
+    m.e1 = j < Tp ? m.e0 + p.le_cnt[ly.fo0 + j] : 0;
     m.x0 = p.lx_off[ly.fo0 + j];
-    m.x1 = p.lx_off[ly.fo0 + j + 1];
+    m.x1 = m.x0 + p.lx_cnt[ly.fo0 + j];
     return m;
 }
 
@@ -188,7 +188,7 @@ __device__ __forceinline__ void lat_fetch(const Params &p, const UttLayout &ly, 
 __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh)
 {
     UttState &st = p.st[u];
-    const UttLayout &ly = p.lay[u];
+    const UttLayout ly = p.lay[u];
     const int tid = threadIdx.x;
     const int Tp = st.Tp;
     const float lb = p.lattice_beam;
@@ -199,29 +199,6 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
     const int64_t *so = p.sv_off + ly.fo0;
     unsigned long long *kcnt = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
     const uint32_t kinf = okey(__int_as_float(0x7F800000));
-    // Records were appended token set by token set, so the records of set j
-    // are those whose source survivor lies in S_j: locate each set's range by
-    // binary search on the source index.
-    const int64_t ne = st.le_cnt, nx = st.lx_cnt;
-    for (int j = tid; j <= Tp + 1; j += blockDim.x) {
-        const int64_t lo_sv = so[j];
-        int64_t a = 0, b = ne;
-        while (a < b) {
-            const int64_t mid = (a + b) >> 1;
-            if (p.lat_e[ly.le0 + mid].x < lo_sv) a = mid + 1;
-            else b = mid;
-        }
-        p.le_off[ly.fo0 + j] = a;
-        a = 0;
-        b = nx;
-        while (a < b) {
-            const int64_t mid = (a + b) >> 1;
-            if (p.lat_x[ly.lx0 + mid].x < lo_sv) a = mid + 1;
-            else b = mid;
-        }
-        p.lx_off[ly.fo0 + j] = a;
-    }
-    __syncthreads();
     int *flag = sh;   // three rotating "changed" flags of the epsilon rounds
     int hA = 0;          // LDS half holding S_j+1
     bool a_lds = false;  // S_j+1's costs and extra costs are in that half
@@ -501,13 +478,13 @@ __global__ __launch_bounds__(256) void lattice_emit_kernel(Params p)
         if (part == 0) {
             if (j == st.Tp) continue;
             r0 = p.le_off[ly.fo0 + j];
-            r1 = p.le_off[ly.fo0 + j + 1];
+            r1 = r0 + p.le_cnt[ly.fo0 + j];
             rec = p.lat_e;
             ex = p.ex_e;
             base = ly.le0;
         } else {
             r0 = p.lx_off[ly.fo0 + j];
-            r1 = p.lx_off[ly.fo0 + j + 1];
+            r1 = r0 + p.lx_cnt[ly.fo0 + j];
             rec = p.lat_x;
             ex = p.ex_x;
             base = ly.lx0;

@@ -19,6 +19,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 
 #include "wfstdec.h"
@@ -54,6 +55,9 @@ struct Graph {
     int32_t eps_depth;
     int64_t device_bytes;
     void *mem;   // single device allocation holding every array
+    // lattice-record slots per token that the last decodes on this graph
+    // needed (emitting, epsilon), a starting point for the next ones
+    mutable std::atomic<int64_t> rec_em{0}, rec_xm{0};
 };
 
 // Per-utterance decode state in device memory.
@@ -65,7 +69,7 @@ struct UttState {
     int32_t gframes;      // frames whose token table overflowed LDS (redone in device memory)
     // written by the search kernel when it ends
     int32_t n_last;       // |S_T'|
-    int32_t pad0;
+    int32_t big_sets;     // some token set is too large for the record kernel's LDS table
     int64_t n_tok;        // survivors of all token sets
     int64_t le_cnt;       // emitting lattice records
     int64_t lx_cnt;       // epsilon lattice records
@@ -116,6 +120,11 @@ struct Params {
     int32_t *sv_prev;
     int32_t *sv_ebeg;         // first emitting arc record of the survivor's state
     int32_t *sv_epre;         // exclusive prefix of emitting out-degree within the token set
+    int4 *sv_x;               // epsilon out-degree of the survivor's state and its first
+                              // epsilon arc {degree, dst | has_eps << 31, weight bits, user arc}
+    int4 *cand;               // emitting candidates of each token set's expansion, in the
+                              // set's emitting region: {src survivor, user arc, cost bits, dst state}
+    int64_t *cand_cnt;        // candidates per token set
     uint32_t *e_key;          // lattice backward extra cost per survivor (ordered key)
     // lattice raw records {src survivor, dst survivor, user arc, prefix cost bits}
     int4 *lat_e;
@@ -125,9 +134,11 @@ struct Params {
     int4 *lat_out;            // kept lattice {frame, arc, cost bits, extra bits}
     // per-frame arrays (fo0 region): survivor, lattice-record and output offsets
     int64_t *sv_off;
-    int64_t *le_off;
-    int64_t *lx_off;
+    int64_t *le_off;          // start of each set's emitting-record region (the search reserves)
+    int64_t *lx_off;          // start of each set's epsilon-record region
     int64_t *lo_off;
+    int64_t *le_cnt;          // records in each set's regions (the record kernel writes)
+    int64_t *lx_cnt;
     uint32_t *cut_arr;        // pruning cutoff key of each token set
     int32_t *kept;
     int32_t *path_arc;
@@ -140,14 +151,13 @@ struct Params {
     int64_t capG;             // power of two
     uint2 *gspill;            // U x 2 x capO {table slot, cost bits}
     int64_t capO;
-    int4 *cand;               // U x capC {src survivor, user arc, cost bits, table slot}
-    int64_t capC;
 };
 
 // ---- launchers (search_kernel.hip / final_kernels.hip) ----
 hipError_t launch_classify(const Params &p, hipStream_t s);
 hipError_t launch_search(const Params &p, hipStream_t s);
 hipError_t launch_final(const Params &p, hipStream_t s);
+hipError_t launch_record(const Params &p, int max_frames, hipStream_t s);
 hipError_t launch_finish(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
 

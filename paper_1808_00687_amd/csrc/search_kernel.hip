@@ -1,7 +1,6 @@
 // Search kernel: one 1024-thread workgroup per utterance loops over every
 // decoded frame of its utterance (token passing, Sec. 3; the per-frame
-// Viterbi beam search of Alg. 1, with the lattice records of exact lattice
-// generation, Sec. 1 and Sec. 3).
+// Viterbi beam search of Alg. 1).
 //
 // Frame k (token set S_k) in one workgroup:
 //   1. expansion of the emitting arcs of S_{k-1}: each wave takes up to four
@@ -22,9 +21,11 @@
 //      smallest key by radix select over an LDS histogram;
 //   4. compaction of the survivors into S_k (device memory, and LDS for the
 //      next expansion) in slot-list order, with the prefix of their
-//      emitting out-degrees;
-//   5. back-pointer survivor indices and lattice records;
-//   6. clearing of the table.
+//      emitting out-degrees, and the set's lattice record regions;
+//   5. clearing of the table.
+// Back-pointers and lattice records need nothing the next frame needs: the
+// record kernel derives them afterwards from the stored token sets, every
+// frame of every utterance in parallel.
 // A frame that reaches more states than the LDS table holds is redone with
 // the same code on a table in device memory.  Every table is private to its
 // workgroup: no device-scope synchronisation and no per-frame launches.
@@ -50,15 +51,6 @@ constexpr int kOverflow = 1;              // frame result: the table filled up
 
 static_assert(kHistBins * 4 <= kW * kQueue * 8, "the select histogram aliases the epsilon queues");
 
-__device__ __forceinline__ uint32_t hash_state(uint32_t d) { return d * 0x9E3779B1u; }
-
-// Load through a pointer known to address device memory (a global rather
-// than a flat access, which would also wait on LDS traffic).
-template <typename T>
-__device__ __forceinline__ T ldg(const T *ptr)
-{
-    return *(const __attribute__((address_space(1))) T *)ptr;
-}
 
 // Table loads: plain in LDS; in device memory they bypass the CU's L1, since
 // the table's atomics are performed in L2.
@@ -99,15 +91,10 @@ struct Sh {
     int overflow;        // more states than the table's fill limit
     int status;          // sticky error of the utterance
     uint32_t best;       // smallest cost key among the frame's tokens
-    uint32_t hint;       // key of one real candidate of the next frame
     int spill_n[2];      // epsilon items in the device-memory lists
     int ncand;           // emitting candidates listed this frame
-    int nlat_e, nlat_x;  // lattice records this frame
     int bin, before, cnt;
-    int best_pos, best_eb, best_ed;
-    float best_cost;
-    unsigned long long eps_sum;
-    int scan[40];
+    int scan[52];
 };
 
 // Running values of the utterance, identical in every thread (eps aside).
@@ -116,12 +103,14 @@ struct Run {
     int64_t prev0;       // relative start of S_{k-1}
     int n_prev;          // |S_{k-1}|
     int a_prev;          // emitting out-arcs of S_{k-1}
-    int64_t lat_e, lat_x;
+    int64_t le, lx;      // emitting and epsilon regions reserved so far
+    int64_t le_prev;     // start of S_{k-1}'s emitting region (its candidates)
     int64_t arcs;
+    int64_t eps;         // epsilon out-arcs of the survivors
     int gframes;
-    long long eps;       // epsilon out-arcs of survivors (this thread's share)
     uint64_t ph[6];      // device clock ticks per step (thread 0, profiling)
     uint64_t t_last;
+    uint64_t t_sub;
 };
 
 // Profiling: thread 0 adds the device clock since the previous mark to step
@@ -133,6 +122,18 @@ __device__ __forceinline__ void phase_mark(const Params &p, Run &run, int i)
         if (i >= 0) run.ph[i] += t - run.t_last;
         run.t_last = t;
     }
+}
+
+// Profiling of a part of a step as thread 0 sees it: open, then close into
+// slot i.
+__device__ __forceinline__ void sub_open(const Params &p, Run &run)
+{
+    if (p.profile && threadIdx.x == 0) run.t_sub = wall_clock64();
+}
+
+__device__ __forceinline__ void sub_close(const Params &p, Run &run, int i)
+{
+    if (p.profile && threadIdx.x == 0) run.ph[i] += wall_clock64() - run.t_sub;
 }
 
 template <bool G>
@@ -221,81 +222,6 @@ __device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, WaveQ &wq, bool ac
     return slot;
 }
 
-// Append R records per lane (rec[r]) to a list with one LDS add per wave.
-template <int R>
-__device__ __forceinline__ void put_records(int4 *buf, int64_t cap, int64_t base, int *cnt, Sh &sh, const bool *rec,
-                                            const int4 *r4)
-{
-    uint64_t m[R];
-    int pref[R], total = 0;
-#pragma unroll
-    for (int r = 0; r < R; r++) {
-        m[r] = __ballot(rec[r]);
-        pref[r] = total;
-        total += __popcll(m[r]);
-    }
-    if (!total) return;
-    int b = 0;
-    if (lane_id() == 0) b = atomicAdd(cnt, total);
-    b = __builtin_amdgcn_readlane(b, 0);
-#pragma unroll
-    for (int r = 0; r < R; r++) {
-        if (rec[r]) {
-            const int64_t idx = base + b + pref[r] + rank_in(m[r]);
-            if (idx < cap) buf[idx] = r4[r];
-            else sh.status = WFST_ECAPACITY;
-        }
-    }
-}
-
-// Largest t in [0, n) with epre[t] <= a (epre non-decreasing, epre[0] <= a).
-__device__ __forceinline__ int search_le(const int32_t *epre, int n, int a)
-{
-    const int lane = lane_id();
-    int lo = 0, end = n;
-    while (end - lo > 1) {
-        const int step = (end - lo + kWave - 1) / kWave;
-        const int idx = lo + lane * step;
-        const int v = idx < end ? epre[idx] : 0x7FFFFFFF;
-        const uint64_t m = __ballot(v <= a);
-        const int l = 63 - __clzll(static_cast<long long>(m));
-        lo += l * step;
-        end = min(lo + step, end);
-    }
-    return lo;
-}
-
-// Two block-wide exclusive scans at once; `sh` needs 34 ints.
-__device__ __forceinline__ int2 block_scan2(int x, int y, int *sh, int2 *total)
-{
-    const int lane = lane_id();
-    const int w = threadIdx.x / kWave;
-    const int ix = wave_incl_scan(x), iy = wave_incl_scan(y);
-    if (lane == kWave - 1) {
-        sh[w] = ix;
-        sh[16 + w] = iy;
-    }
-    __syncthreads();
-    if (threadIdx.x < kWave) {
-        const int vx = threadIdx.x < kW ? sh[threadIdx.x] : 0;
-        const int vy = threadIdx.x < kW ? sh[16 + threadIdx.x] : 0;
-        const int sx = wave_incl_scan(vx), sy = wave_incl_scan(vy);
-        if (threadIdx.x < kW) {
-            sh[threadIdx.x] = sx - vx;
-            sh[16 + threadIdx.x] = sy - vy;
-        }
-        if (threadIdx.x == kWave - 1) {
-            sh[32] = sx;
-            sh[33] = sy;
-        }
-    }
-    __syncthreads();
-    const int2 r = make_int2(ix - x + sh[w], iy - y + sh[16 + w]);
-    *total = make_int2(sh[32], sh[33]);
-    __syncthreads();
-    return r;
-}
-
 // Bin holding the rank-th smallest (1-based) of a histogram: sets sh.bin and
 // sh.before (the count in lower bins).
 __device__ __forceinline__ void select_bin(const uint32_t *h, int nbins, int rank, Sh &sh)
@@ -330,21 +256,6 @@ __device__ __forceinline__ int first_shift(uint32_t kb, uint32_t lim)
     return nb > kHistBits ? nb - kHistBits : 0;
 }
 
-__device__ __forceinline__ void put_record(int4 *buf, int64_t cap, int64_t base, int *cnt, Sh &sh, bool rec,
-                                           const int4 &r)
-{
-    const uint64_t m = __ballot(rec);
-    if (!m) return;
-    int b = 0;
-    if (lane_id() == 0) b = atomicAdd(cnt, __popcll(m));
-    b = __builtin_amdgcn_readlane(b, 0);
-    if (rec) {
-        const int64_t idx = base + b + rank_in(m);
-        if (idx < cap) buf[idx] = r;
-        else sh.status = WFST_ECAPACITY;
-    }
-}
-
 // The expansion's view of S_{k-1}: token costs, emitting-arc prefix and
 // first emitting record of each token's state, in LDS (sets of at most
 // kSetCache tokens) or in the survivor arrays.
@@ -367,12 +278,10 @@ struct SetView<false> {
     __device__ float c(int i) const { return tok_cost(tok[i]); }
 };
 
-// Emitting expansion of S_{k-1} into the table (step 1).  Every offered
-// candidate is listed: it gives the back-pointer of its destination when it
-// wins, and an emitting lattice arc.
+// Emitting expansion of S_{k-1} into the table (step 1).
 template <bool G, bool L>
 __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh, const SetView<L> &v, int n_tok,
-                                       int A, int src0, const float *row, WaveQ &wq, int4 *cand, int capC)
+                                       int A, int src0, const float *row, WaveQ &wq, int4 *cbuf)
 {
     const int lane = lane_id();
     const int wid = threadIdx.x / kWave;
@@ -429,11 +338,10 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
         float lv[kChunks];
 #pragma unroll
         for (int r = 0; r < kChunks; r++) lv[r] = ok[r] ? ldg(row + rec[r].y) : 0.0f;
-        bool act[kChunks], de[kChunks], keep[kChunks];
+        bool act[kChunks], de[kChunks];
         uint32_t d[kChunks], key[kChunks];
         float cnd[kChunks];
         int32_t arc[kChunks];
-        int slot[kChunks];
         uint32_t km = kEmptyKey;
 #pragma unroll
         for (int r = 0; r < kChunks; r++) {
@@ -454,16 +362,29 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
         const uint32_t bnd = drop_bound(km < cur ? km : cur, p.beam);
 #pragma unroll
         for (int r = 0; r < kChunks; r++) act[r] = ok[r] && key[r] <= bnd;
+        bool keep[kChunks];
 #pragma unroll
-        for (int r = 0; r < kChunks; r++) slot[r] = offer<G>(t, sh, wq, act[r], d[r], de[r], cnd[r], key[r], arc[r]);
-        // the candidate list, one LDS add per wave
-        int4 c4[kChunks];
+        for (int r = 0; r < kChunks; r++) keep[r] = offer<G>(t, sh, wq, act[r], d[r], de[r], cnd[r], key[r], arc[r]) >= 0;
+        // the offered candidates, for the back-pointers and lattice arcs:
+        // one LDS add per wave
+        uint64_t m[kChunks];
+        int pref[kChunks], total = 0;
 #pragma unroll
         for (int r = 0; r < kChunks; r++) {
-            keep[r] = act[r] && slot[r] >= 0;
-            c4[r] = make_int4(src0 + ot[r], arc[r], __float_as_int(cnd[r]), slot[r]);
+            m[r] = __ballot(keep[r]);
+            pref[r] = total;
+            total += __popcll(m[r]);
         }
-        put_records<kChunks>(cand, capC, 0, &sh.ncand, sh, keep, c4);
+        if (total) {
+            int b = 0;
+            if (lane == 0) b = atomicAdd(&sh.ncand, total);
+            b = __builtin_amdgcn_readlane(b, 0);
+#pragma unroll
+            for (int r = 0; r < kChunks; r++)
+                if (keep[r])
+                    cbuf[b + pref[r] + rank_in(m[r])] =
+                        make_int4(src0 + ot[r], arc[r], __float_as_int(cnd[r]), static_cast<int>(d[r]));
+        }
     }
 }
 
@@ -542,72 +463,13 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
     }
 }
 
-// The epsilon lattice arcs after the first (rows xbeg + 1 .. xbeg + xdeg_all),
-// spread over the wave.
-template <bool G>
-__device__ __forceinline__ void eps_rest(const Params &p, const Tab<G> &t, Sh &sh, const UttLayout &ly, int64_t base,
-                                         uint32_t cut, bool surv, int rel, float cst, int xbeg, int xdeg_all)
-{
-    const int lane = lane_id();
-    const int xb = xbeg + 1;
-    const int xdeg = surv ? max(xdeg_all - 1, 0) : 0;
-    const int incl = wave_incl_scan(xdeg);
-    const int pre = incl - xdeg;
-    const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
-    for (int k0 = 0; k0 < tot; k0 += kWave) {
-        const int kk = k0 + lane;
-        const int o = owner_lane(pre, kk);
-        const int ob = __shfl(xb, o, kWave);
-        const int op = __shfl(pre, o, kWave);
-        const float oc = __shfl(cst, o, kWave);
-        const int orel = __shfl(rel, o, kWave);
-        bool rec = false;
-        int4 r4 = make_int4(0, 0, 0, 0);
-        if (kk < tot) {
-            const int4 x = p.g.xarc[ob + (kk - op)];
-            const float pc = oc + __int_as_float(x.y);
-            if (okey(pc) <= cut) {
-                const int sl = tab_find<G>(t, static_cast<uint32_t>(x.x) & kDstMask);
-                const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
-                rec = dv != kEmptyTok;
-                r4 = make_int4(orel, static_cast<int>(static_cast<uint32_t>(dv)), x.z, __float_as_int(pc));
-            }
-        }
-        put_record(p.lat_x + ly.lx0, ly.lxcap, base, &sh.nlat_x, sh, rec, r4);
-    }
-}
-
-// Epsilon lattice arcs of one survivor per lane (surv): each epsilon arc of
-// its state (rows xbeg .. xbeg + xdeg_all) whose prefix cost is within the
-// set's cutoff.  The first arc comes from the state record (x0), the others
-// from the epsilon rows.
-template <bool G>
-__device__ __forceinline__ void eps_records(const Params &p, const Tab<G> &t, Sh &sh, const UttLayout &ly,
-                                            int64_t base, uint32_t cut, bool surv, int rel, float cst, int xbeg,
-                                            int xdeg_all, int4 x0)
-{
-    {
-        bool rec = false;
-        int4 r4 = make_int4(0, 0, 0, 0);
-        const float pc = cst + __int_as_float(x0.y);
-        if (surv && xdeg_all > 0 && okey(pc) <= cut) {
-            const int sl = tab_find<G>(t, static_cast<uint32_t>(x0.x) & kDstMask);
-            const unsigned long long dv = sl >= 0 ? tld<G>(t.vals + sl) : kEmptyTok;
-            rec = dv != kEmptyTok;
-            r4 = make_int4(rel, static_cast<int>(static_cast<uint32_t>(dv)), x0.z, __float_as_int(pc));
-        }
-        put_record(p.lat_x + ly.lx0, ly.lxcap, base, &sh.nlat_x, sh, rec, r4);
-    }
-    eps_rest<G>(p, t, sh, ly, base, cut, surv, rel, cst, xbeg, xdeg_all);
-}
-
 // One frame: produces S_k from S_{k-1} (or from the start state when k = 0).
 // Returns 0, kOverflow (the table filled up; nothing of S_k was written) or
 // a negative WFST error.  Every return is taken by the whole workgroup.
 template <bool G>
 __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
                                      const Tab<G> &t, uint2 *aux, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
-                                     uint2 *spill, int gcap, int4 *cand, int capC, Run &run, int k)
+                                     uint2 *spill, int gcap, Run &run, int k)
 {
     const int tid = threadIdx.x;
     const int lane = lane_id();
@@ -623,17 +485,16 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     if (tid == 0) {
         sh.nslots = 0;
         sh.overflow = 0;
-        sh.best = k > 0 ? sh.hint : kEmptyKey;
+        sh.best = kEmptyKey;
         sh.spill_n[0] = sh.spill_n[1] = 0;
         sh.ncand = 0;
-        sh.nlat_e = sh.nlat_x = 0;
         sh.cnt = 0;
-        sh.best_pos = -1;
     }
     __syncthreads();
     phase_mark(p, run, -1);
 
     // ---- 1. expansion ----
+    sub_open(p, run);
     if (k == 0) {
         if (wid == 0) {
             const int s = p.g.start;
@@ -643,18 +504,20 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     } else {
         const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k - 1]) * p.L;
         const int src0 = static_cast<int>(run.prev0);
+        int4 *cbuf = p.cand + ly.le0 + run.le_prev;
         if (run.n_prev <= kSetCache) {
             SetView<true> v{s_cost, s_epre, s_ebeg};
-            expand<G, true>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cand, capC);
+            expand<G, true>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cbuf);
         } else {
             const int64_t base = ly.sv0 + run.prev0;
             SetView<false> v{p.sv_tok + base, p.sv_epre + base, p.sv_ebeg + base};
-            expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cand, capC);
+            expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cbuf);
         }
     }
+    sub_close(p, run, 5);
     // ---- 2. epsilon closure: each wave its own queue, then spill rounds ----
     drain<G>(p, t, sh, wq);
-    // full barrier: spilled items and the candidate list are read by other waves
+    // full barrier: spilled items are read by other waves
     __syncthreads();
     phase_mark(p, run, 0);
     int sp = 0;
@@ -735,23 +598,13 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     phase_mark(p, run, 2);
 
     // ---- 4. compaction into S_k, in slot-list order ----
-    // With one pass (n <= kT * kRun) each thread keeps its survivors' state
-    // records and back-pointer sources in registers for step 5: the loads
-    // ride along with the compaction's own.
     const int64_t set0 = run.set0;
-    const bool one_pass = n <= kT * kRun;
-    int n_kept = 0, a_kept = 0;
-    // per kept entry: survivor index (-1 if not kept), back-pointer source
-    // (arc_src of the token's arc, or -1 for the start token), cost, the
-    // epsilon rows after the first arc and the first epsilon record
-    int kslot[kRun], krel[kRun], kinfo[kRun], kxb[kRun], kxd[kRun];
-    float kcst[kRun];
-    int4 kx0[kRun];
+    int n_kept = 0, a_kept = 0, x_kept = 0;
     for (int e0 = 0; e0 < n; e0 += kT * kRun) {
-        int dd[kRun], eb[kRun], ed[kRun];
+        int kslot[kRun], dd[kRun], eb[kRun], ed[kRun];
+        int4 xr[kRun];
         unsigned long long vv[kRun];
-        int kc = 0, ac = 0;
-        long long xc = 0;
+        int kc = 0, ac = 0, xc = 0;
 #pragma unroll
         for (int r = 0; r < kRun; r++) {
             const int i = e0 + tid * kRun + r;
@@ -768,226 +621,88 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
 #pragma unroll
         for (int r = 0; r < kRun; r++) {
             kp[r] = kslot[r] >= 0 && static_cast<uint32_t>(vv[r] >> 32) <= cut;
-            kcst[r] = tok_cost(vv[r]);
             eb[r] = ed[r] = 0;
-            kinfo[r] = -1;
-            kxb[r] = kxd[r] = 0;
-            kx0[r] = make_int4(0, 0, 0, 0);
+            xr[r] = make_int4(0, 0, 0, 0);
             if (kp[r]) {
-                const int64_t s2 = 2 * static_cast<int64_t>(dd[r]);
-                const int4 lo = p.g.srec[s2];
-                if (one_pass) {
-                    if (p.lattice) kx0[r] = p.g.srec[s2 + 1];
-                    const int a = tok_arc(vv[r]);
-                    if (a >= 0) kinfo[r] = p.g.arc_src[a];
-                }
+                const int4 lo = p.g.srec[2 * static_cast<int64_t>(dd[r])];
+                const int4 x0 = p.g.srec[2 * static_cast<int64_t>(dd[r]) + 1];
                 eb[r] = lo.x;
                 ed[r] = lo.y;
-                kxb[r] = lo.z;
-                kxd[r] = lo.w - lo.z;
+                xr[r] = make_int4(lo.w - lo.z, x0.x, x0.y, x0.z);
                 xc += lo.w - lo.z;
                 kc++;
                 ac += ed[r] - eb[r];
             }
         }
-        run.eps += xc;
-        int2 tot;
-        const int2 ex = block_scan2(kc, ac, sh.scan, &tot);
+        int3 tot;
+        const int3 ex = block_scan3(kc, ac, xc, sh.scan, &tot);
         int pos = n_kept + ex.x, apos = a_kept + ex.y;
 #pragma unroll
         for (int r = 0; r < kRun; r++) {
-            krel[r] = -1;
             if (kp[r]) {
                 const int64_t rel = set0 + pos;
-                krel[r] = static_cast<int>(rel);
                 if (rel < ly.svcap) {
                     const int64_t o = ly.sv0 + rel;
                     p.sv_state[o] = dd[r];
                     p.sv_tok[o] = vv[r];
                     p.sv_ebeg[o] = eb[r];
                     p.sv_epre[o] = apos;
+                    p.sv_x[o] = xr[r];
                 } else {
                     sh.status = WFST_ECAPACITY;
                 }
+                const float c = tok_cost(vv[r]);
                 if (pos < kSetCache) {
-                    s_cost[pos] = kcst[r];
+                    s_cost[pos] = c;
                     s_epre[pos] = apos;
                     s_ebeg[pos] = eb[r];
                 }
-                if (static_cast<uint32_t>(vv[r] >> 32) == kb && atomicCAS(&sh.best_pos, -1, pos) == -1) {
-                    sh.best_eb = eb[r];
-                    sh.best_ed = ed[r];
-                    sh.best_cost = kcst[r];
-                }
-                t.vals[kslot[r]] = (vv[r] << 32) | static_cast<uint32_t>(rel);
                 pos++;
                 apos += ed[r] - eb[r];
-            } else if (kslot[r] >= 0) {
-                t.vals[kslot[r]] = kEmptyTok;
             }
         }
         n_kept += tot.x;
         a_kept += tot.y;
+        x_kept += tot.z;
     }
     const int ns = n_kept;
-    // Step 5 reads the survivors from LDS and registers unless the set is
-    // larger than the LDS copy; then their device-memory stores must be
-    // complete.
+    // the next expansion reads S_k from LDS unless it is larger than the LDS
+    // copy; then its device-memory stores must be complete
     if (G || ns > kSetCache) __syncthreads();
     else lds_barrier();
     phase_mark(p, run, 3);
     if (ns == 0) return WFST_ENOPATH;
     if (sh.status) return sh.status;
+    // Token set k, its cutoff and the lattice record regions of set k: one
+    // record per emitting arc of S_k (into S_k+1) at most, one per epsilon
+    // arc of S_k at most.
+    const int64_t a_rec = k < Tp ? a_kept : 0;
+    if (run.le + a_rec > ly.lecap || (p.lattice && run.lx + x_kept > ly.lxcap)) return WFST_ECAPACITY;
     if (tid == 0) {
         p.sv_off[ly.fo0 + k + 1] = set0 + ns;
         p.cut_arr[ly.fo0 + k] = cut;
+        p.le_off[ly.fo0 + k + 1] = run.le + a_rec;
+        p.lx_off[ly.fo0 + k + 1] = run.lx + x_kept;
+        if (k > 0) p.cand_cnt[ly.fo0 + k - 1] = sh.ncand;
     }
-    // early-drop seed of the next frame: the cheapest candidate of one best
-    // token of S_k, a real candidate cost of frame k + 1
-    if (wid == 0 && k < Tp) {
-        const float c = sh.best_cost;
-        const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k]) * p.L;
-        uint32_t hint = kEmptyKey;
-        for (int a = sh.best_eb + lane; a < sh.best_ed; a += kWave) {
-            const int4 r = p.g.earc[a];
-            const float t1 = c + __int_as_float(r.z);
-            const uint32_t key = okey(t1 - ldg(row + r.y));
-            hint = key < hint ? key : hint;
-        }
-        hint = wave_min_u32(hint);
-        if (lane == 0) sh.hint = hint;
-    }
-
-    // ---- 5. back-pointers and lattice records ----
-    // The candidate list's first chunks of this wave, loaded ahead of the
-    // survivor pass.
-    const int nc = k > 0 ? min(sh.ncand, capC) : 0;
-    int4 cpre[2];
-#pragma unroll
-    for (int q = 0; q < 2; q++) {
-        const int i = wid * kWave + q * kT + lane;
-        cpre[q] = i < nc ? cand[i] : make_int4(0, 0, 0, 0);
-    }
-    // Survivors of S_k: the back-pointer of a token reached by an epsilon
-    // arc (its source is in S_k), of the start token, and the epsilon
-    // lattice arcs inside S_k.
-    if (one_pass) {
-        bool rec[kRun];
-        int4 r4[kRun];
-#pragma unroll
-        for (int r = 0; r < kRun; r++) {
-            const bool kept = krel[r] >= 0;
-            int src_sl = -1;
-            if (kept && kinfo[r] < 0 && kinfo[r] != -1) src_sl = tab_find<G>(t, static_cast<uint32_t>(kinfo[r]) & kDstMask);
-            // the first epsilon arc's lattice record
-            const float pc = kcst[r] + __int_as_float(kx0[r].y);
-            int dst_sl = -1;
-            if (p.lattice && kept && kxd[r] > 0 && okey(pc) <= cut)
-                dst_sl = tab_find<G>(t, static_cast<uint32_t>(kx0[r].x) & kDstMask);
-            if (kept) {
-                if (kinfo[r] == -1) p.sv_prev[ly.sv0 + krel[r]] = -1;
-                else if (kinfo[r] < 0)
-                    p.sv_prev[ly.sv0 + krel[r]] =
-                        src_sl >= 0 ? static_cast<int>(static_cast<uint32_t>(tld<G>(t.vals + src_sl))) : -1;
-            }
-            const unsigned long long dv = dst_sl >= 0 ? tld<G>(t.vals + dst_sl) : kEmptyTok;
-            rec[r] = dv != kEmptyTok;
-            r4[r] = make_int4(krel[r], static_cast<int>(static_cast<uint32_t>(dv)), kx0[r].z, __float_as_int(pc));
-        }
-        if (p.lattice) {
-            put_records<kRun>(p.lat_x + ly.lx0, ly.lxcap, run.lat_x, &sh.nlat_x, sh, rec, r4);
-#pragma unroll
-            for (int r = 0; r < kRun; r++)
-                eps_rest<G>(p, t, sh, ly, run.lat_x, cut, krel[r] >= 0, krel[r], kcst[r], kxb[r], kxd[r]);
-        }
-    } else {
-        // more states than one compaction pass holds: the same from memory
-        const bool set_lds = ns <= kSetCache;
-        for (int c0 = wid * kWave; c0 < n; c0 += kT) {
-            const int i = c0 + lane;
-            bool surv = false;
-            int rel = 0, a = -1;
-            int64_t s = 0;
-            float cst = 0.0f;
-            if (i < n) {
-                const int sl = static_cast<int>(tld<G>(t.slots + i));
-                const unsigned long long v = tld<G>(t.vals + sl);
-                if (v != kEmptyTok) {
-                    surv = true;
-                    rel = static_cast<int>(static_cast<uint32_t>(v));
-                    a = static_cast<int>(static_cast<uint32_t>(v >> 32)) - 1;
-                    s = static_cast<int64_t>(tld<G>(t.keys + sl));
-                    cst = set_lds ? s_cost[rel - set0] : tok_cost(p.sv_tok[ly.sv0 + rel]);
-                }
-            }
-            int info = 0;
-            int4 lo = make_int4(0, 0, 0, 0), x0 = make_int4(0, 0, 0, 0);
-            if (surv) {
-                if (a >= 0) info = p.g.arc_src[a];
-                if (p.lattice) {
-                    lo = p.g.srec[2 * s];
-                    x0 = p.g.srec[2 * s + 1];
-                }
-                if (a < 0) {
-                    p.sv_prev[ly.sv0 + rel] = -1;
-                } else if (info < 0) {
-                    const int sl = tab_find<G>(t, static_cast<uint32_t>(info) & kDstMask);
-                    p.sv_prev[ly.sv0 + rel] =
-                        sl >= 0 ? static_cast<int>(static_cast<uint32_t>(tld<G>(t.vals + sl))) : -1;
-                }
-            }
-            if (p.lattice) eps_records<G>(p, t, sh, ly, run.lat_x, cut, surv, rel, cst, lo.z, lo.w - lo.z, x0);
-        }
-    }
-    // Candidates of the expansion: the winner of each surviving destination
-    // gives its back-pointer; those within the cutoff are emitting lattice arcs.
-    for (int i0 = wid * kWave; i0 < nc; i0 += 2 * kT) {
-        int4 c4[2];
-#pragma unroll
-        for (int q = 0; q < 2; q++) {
-            const int i = i0 + q * kT + lane;
-            if (i0 == wid * kWave) c4[q] = cpre[q];
-            else c4[q] = i < nc ? cand[i] : make_int4(0, 0, 0, 0);
-        }
-        bool rec[2];
-        int4 r4[2];
-#pragma unroll
-        for (int q = 0; q < 2; q++) {
-            const int i = i0 + q * kT + lane;
-            rec[q] = false;
-            r4[q] = make_int4(0, 0, 0, 0);
-            if (i < nc) {
-                const unsigned long long dv = tld<G>(t.vals + c4[q].w);
-                if (dv != kEmptyTok) {
-                    const int drel = static_cast<int>(static_cast<uint32_t>(dv));
-                    if (static_cast<uint32_t>(dv >> 32) == static_cast<uint32_t>(c4[q].y + 1))
-                        p.sv_prev[ly.sv0 + drel] = c4[q].x;
-                    rec[q] = p.lattice && okey(__int_as_float(c4[q].z)) <= cut;
-                    r4[q] = make_int4(c4[q].x, drel, c4[q].y, c4[q].z);
-                }
-            }
-        }
-        if (p.lattice) put_records<2>(p.lat_e + ly.le0, ly.lecap, run.lat_e, &sh.nlat_e, sh, rec, r4);
-    }
-    table_barrier<G>();
-    phase_mark(p, run, 4);
-    run.lat_e += sh.nlat_e;
-    run.lat_x += sh.nlat_x;
-    if (sh.status) return sh.status;
-    if (k < Tp) run.arcs += a_kept;
+    run.le_prev = run.le;
+    run.le += a_rec;
+    run.lx += x_kept;
+    run.eps += x_kept;
+    run.arcs += a_rec;
     run.prev0 = set0;
     run.set0 = set0 + ns;
     run.n_prev = ns;
     run.a_prev = a_kept;
 
-    // ---- 6. clear the table ----
+    // ---- 5. clear the table ----
     for (int i = tid; i < n; i += kT) {
         const int s2 = static_cast<int>(tld<G>(t.slots + i));
         t.keys[s2] = kEmptyKey;
         t.vals[s2] = kEmptyTok;
     }
     table_barrier<G>();
-    phase_mark(p, run, 5);
+    phase_mark(p, run, 4);
     return 0;
 }
 
@@ -1006,7 +721,9 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     const int tid = threadIdx.x;
     UttState &st = p.st[u];
     if (st.status != 0) return;
-    const UttLayout &ly = p.lay[u];
+    // the layout is copied into registers: a reference into device memory
+    // would be reloaded after every barrier
+    const UttLayout ly = p.lay[u];
     const int Tp = st.Tp;
     const float *ll = st.ll;
 
@@ -1027,8 +744,6 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     gt.shift = 32 - (31 - __clz(static_cast<int>(p.capG)));
     const int gcap = static_cast<int>(p.capO);
     uint2 *spill = p.gspill + static_cast<int64_t>(u) * 2 * p.capO;
-    int4 *cand = p.cand + static_cast<int64_t>(u) * p.capC;
-    const int capC = static_cast<int>(p.capC);
 
     for (int i = tid; i < kSlots; i += kT) {
         s_keys[i] = kEmptyKey;
@@ -1036,8 +751,6 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     }
     if (tid == 0) {
         sh.status = 0;
-        sh.hint = kEmptyKey;
-        sh.eps_sum = 0ull;
     }
     __syncthreads();
 
@@ -1045,7 +758,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     bool gclean = false;
     int rc = 0;
     for (int k = 0; k <= Tp; k++) {
-        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, spill, gcap, cand, capC, run, k);
+        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, spill, gcap, run, k);
         if (rc == kOverflow) {
             // more states than the LDS table holds: redo the frame in device memory
             for (int i = tid; i < kSlots; i += kT) {
@@ -1060,22 +773,17 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
                 gclean = true;
             }
             __syncthreads();
-            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, spill, gcap, cand, capC, run, k);
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, spill, gcap, run, k);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
             run.gframes++;
         }
         if (rc != 0) break;
     }
-    const long long e = wave_sum_ll(run.eps);
-    if (lane_id() == 0 && e) atomicAdd(&sh.eps_sum, static_cast<unsigned long long>(e));
-    __syncthreads();
     if (tid == 0) {
         st.n_tok = run.set0;
         st.n_last = run.n_prev;
-        st.le_cnt = run.lat_e;
-        st.lx_cnt = run.lat_x;
         st.arcs_expanded = run.arcs;
-        st.eps_arcs = static_cast<int64_t>(sh.eps_sum);
+        st.eps_arcs = run.eps;
         st.gframes = run.gframes;
         for (int i = 0; i < 6; i++) st.phase_ticks[i] = run.ph[i];
         if (rc != 0) st.status = rc;
