@@ -160,55 +160,93 @@ struct WaveQ {
     int scap;        // its capacity
 };
 
-// Offer one candidate token per lane (act) to the table; lowered tokens of
-// states with epsilon out-arcs become items of the wave's queue.  Called by
-// the whole wave; returns the lane's slot or -1.
-template <bool G>
-__device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, WaveQ &wq, bool act, uint32_t d, bool d_eps,
-                                     float cand, uint32_t key, int32_t arc)
+// Offer R candidate tokens per lane (act[r]) to the table; lowered tokens
+// of states with epsilon out-arcs become items of the wave's queue.  The R
+// offers go through each step together, so that their LDS atomics are in
+// flight at the same time.  With BEST the frame's best key takes the
+// smallest offered key (a caller that has already done so passes false):
+// every offered key is at least the final token of its state, so the minimum
+// is the frame's best token either way.  Called by the whole wave; slot[r]
+// receives the candidate's table slot or -1.
+template <bool G, int R, bool BEST>
+__device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const bool *act, const uint32_t *d,
+                                      const bool *d_eps, const float *cand, const uint32_t *key, const int32_t *arc,
+                                      int *slot)
 {
-    // slot of state d: a compare-and-swap on the key claims a free slot or
-    // finds the state's own
-    int slot = -1;
-    bool claimed = false;
-    if (act) {
-        uint32_t h = hash_state(d) >> t.shift;
-        for (int probe = 0; probe < kMaxProbe; probe++) {
-            const uint32_t k = atomicCAS(t.keys + h, kEmptyKey, d);
-            if (k == kEmptyKey || k == d) {
-                slot = static_cast<int>(h);
-                claimed = k == kEmptyKey;
-                break;
-            }
-            h = (h + 1) & t.mask;
+    // slot of each state: a compare-and-swap on the key claims a free slot
+    // or finds the state's own, probing linearly on a collision
+    uint32_t h[R], k[R];
+    bool claimed[R];
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        h[r] = hash_state(d[r]) >> t.shift;
+        k[r] = act[r] ? atomicCAS(t.keys + h[r], kEmptyKey, d[r]) : 0u;
+    }
+    bool over = false;
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        slot[r] = -1;
+        claimed[r] = false;
+        if (!act[r]) continue;
+        for (int probe = 1; k[r] != kEmptyKey && k[r] != d[r]; probe++) {
+            if (probe == kMaxProbe) break;
+            h[r] = (h[r] + 1) & t.mask;
+            k[r] = atomicCAS(t.keys + h[r], kEmptyKey, d[r]);
+        }
+        if (k[r] == kEmptyKey || k[r] == d[r]) {
+            slot[r] = static_cast<int>(h[r]);
+            claimed[r] = k[r] == kEmptyKey;
+        } else {
+            over = true;
         }
     }
     // newly claimed slots join the slot list, one LDS add per wave
-    const uint64_t mc = __ballot(claimed);
-    if (mc) {
+    uint64_t mc[R];
+    int pc[R], nc = 0;
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        mc[r] = __ballot(claimed[r]);
+        pc[r] = nc;
+        nc += __popcll(mc[r]);
+    }
+    if (nc) {
         int b = 0;
-        if (lane_id() == 0) b = atomicAdd(&sh.nslots, __popcll(mc));
+        if (lane_id() == 0) b = atomicAdd(&sh.nslots, nc);
         b = __builtin_amdgcn_readlane(b, 0);
-        if (claimed) {
-            const int idx = b + rank_in(mc);
-            if (idx < t.fill) t.slots[idx] = static_cast<typename Tab<G>::Slot>(slot);
-            else sh.overflow = 1;
+#pragma unroll
+        for (int r = 0; r < R; r++) {
+            if (claimed[r]) {
+                const int idx = b + pc[r] + rank_in(mc[r]);
+                if (idx < t.fill) t.slots[idx] = static_cast<typename Tab<G>::Slot>(slot[r]);
+                else over = true;
+            }
         }
     }
-    if (act && slot < 0) sh.overflow = 1;
-    bool impr = false;
-    if (slot >= 0) {
-        const unsigned long long v = make_tok(key, arc);
-        impr = v < atomicMin(t.vals + slot, v);
+    if (over) sh.overflow = 1;
+    // recombination: the unsigned minimum of (cost key, arc + 1)
+    unsigned long long v[R], old[R];
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        v[r] = make_tok(key[r], arc[r]);
+        old[r] = slot[r] >= 0 ? atomicMin(t.vals + slot[r], v[r]) : 0ull;
     }
-    const uint32_t mk = wave_min_u32(impr ? key : kEmptyKey);
-    if (lane_id() == 0 && mk != kEmptyKey) atomicMin(&sh.best, mk);
-    const bool push = impr && d_eps;
-    const uint64_t m = __ballot(push);
-    if (m) {
+    if (BEST) {
+        uint32_t mk = kEmptyKey;
+#pragma unroll
+        for (int r = 0; r < R; r++)
+            if (act[r] && key[r] < mk) mk = key[r];
+        mk = wave_min_u32(mk);
+        if (lane_id() == 0 && mk != kEmptyKey) atomicMin(&sh.best, mk);
+    }
+    // lowered tokens whose state has epsilon out-arcs
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        const bool push = slot[r] >= 0 && v[r] < old[r] && d_eps[r];
+        const uint64_t m = __ballot(push);
+        if (!m) continue;
         if (push) {
             const int idx = wq.n + rank_in(m);
-            const uint2 it = make_uint2(static_cast<uint32_t>(slot), __float_as_uint(cand));
+            const uint2 it = make_uint2(static_cast<uint32_t>(slot[r]), __float_as_uint(cand[r]));
             if (idx < wq.qcap) {
                 wq.q[idx] = it;
             } else {
@@ -219,6 +257,15 @@ __device__ __forceinline__ int offer(const Tab<G> &t, Sh &sh, WaveQ &wq, bool ac
         }
         wq.n = min(wq.n + __popcll(m), wq.qcap);
     }
+}
+
+// One candidate per lane, the frame's best key included.
+template <bool G>
+__device__ __forceinline__ int offer1(const Tab<G> &t, Sh &sh, WaveQ &wq, bool act, uint32_t d, bool d_eps,
+                                      float cand, uint32_t key, int32_t arc)
+{
+    int slot;
+    offer<G, 1, true>(t, sh, wq, &act, &d, &d_eps, &cand, &key, &arc, &slot);
     return slot;
 }
 
@@ -362,9 +409,11 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
         const uint32_t bnd = drop_bound(km < cur ? km : cur, p.beam);
 #pragma unroll
         for (int r = 0; r < kChunks; r++) act[r] = ok[r] && key[r] <= bnd;
+        int slot[kChunks];
+        offer<G, kChunks, false>(t, sh, wq, act, d, de, cnd, key, arc, slot);
         bool keep[kChunks];
 #pragma unroll
-        for (int r = 0; r < kChunks; r++) keep[r] = offer<G>(t, sh, wq, act[r], d[r], de[r], cnd[r], key[r], arc[r]) >= 0;
+        for (int r = 0; r < kChunks; r++) keep[r] = slot[r] >= 0;
         // the offered candidates, for the back-pointers and lattice arcs:
         // one LDS add per wave
         uint64_t m[kChunks];
@@ -414,7 +463,7 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
         const uint32_t bnd = drop_bound(sh.best, p.beam);
         const float cnd = cst + __int_as_float(x0.y);
         const uint32_t key = okey(cnd);
-        (void)offer<G>(t, sh, wq, first && key <= bnd, static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, cnd, key,
+        (void)offer1<G>(t, sh, wq, first && key <= bnd, static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, cnd, key,
                        x0.z);
     }
     // the other epsilon arcs, spread over the wave
@@ -441,7 +490,7 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             key = okey(cnd);
             act = key <= bnd;
         }
-        (void)offer<G>(t, sh, wq, act, d, d_eps, cnd, key, arc);
+        (void)offer1<G>(t, sh, wq, act, d, d_eps, cnd, key, arc);
     }
 }
 
@@ -499,7 +548,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         if (wid == 0) {
             const int s = p.g.start;
             const int4 lo = p.g.srec[2 * static_cast<int64_t>(s)];
-            (void)offer<G>(t, sh, wq, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0.0f, okey(0.0f), -1);
+            (void)offer1<G>(t, sh, wq, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0.0f, okey(0.0f), -1);
         }
     } else {
         const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k - 1]) * p.L;
