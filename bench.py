@@ -52,17 +52,16 @@ def log(*a):
 
 
 def search_bytes(stats_list):
-    """Algorithmic device-memory bytes of the search kernel over one batch:
-    per surviving token 32 B (its state, token and back-pointer written,
-    16 B; the emitting and epsilon row offsets of its state read, 16 B), per
-    expanded emitting arc 20 B (16 B arc record, 4 B log-likelihood), per
-    epsilon out-arc of a surviving token 16 B (arc record), per raw lattice
-    record 16 B written."""
+    """Algorithmic device-memory bytes of the search over one batch, per the
+    method's own traffic: per surviving token expanded 16 B (its state, cost
+    and the two emitting row offsets), per emitting arc expanded 24 B
+    (destination, input label, weight, log-likelihood and the 8-byte token
+    of the recombination), per epsilon out-arc of a surviving token 16 B
+    (destination, weight and the 8-byte token)."""
     tok = sum(s["tokens"] for s in stats_list)
     arcs = sum(s["arcs_expanded"] for s in stats_list)
     eps = sum(s["eps_arcs"] for s in stats_list)
-    lat = sum(s["lattice_raw"] for s in stats_list)
-    return 32 * tok + 20 * arcs + 16 * eps + 16 * lat
+    return 16 * tok + 24 * arcs + 16 * eps
 
 
 def kernel_sha() -> str:

@@ -333,6 +333,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.lds_fill = test_env_int("WFSTDEC_TEST_LDS_FILL", 1 << 30);
     p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1024);
     p.profile = tm.on ? 1 : 0;
+    p.rec_fill = test_env_int("WFSTDEC_TEST_RECORD_FILL", 1 << 30);
     p.capO = z.capO;
     WallTrace wt;
     UttLayout *d_lay = nullptr;

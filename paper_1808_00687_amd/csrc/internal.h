@@ -112,6 +112,7 @@ struct Params {
     int32_t lds_fill;         // states per frame the LDS token table takes (<= its fill limit)
     int32_t gen_lds;          // epsilon items per wave queue in LDS (<= its capacity)
     int32_t profile;          // count device clock ticks per search step
+    int32_t rec_fill;         // survivors per set the record kernel's LDS table takes (<= its fill limit)
     UttState *st;
     const UttLayout *lay;
     // survivors (per utterance regions)

@@ -219,7 +219,7 @@ __global__ __launch_bounds__(kRT) void record_kernel(Params p)
     if (st.status != 0 || k > st.Tp) return;
     const UttLayout &ly = p.lay[u];
     const int n = static_cast<int>(p.sv_off[ly.fo0 + k + 1] - p.sv_off[ly.fo0 + k]);
-    if (n > kRFill) {
+    if (n > min(kRFill, p.rec_fill)) {
         // left to the device-memory pass
         if (threadIdx.x == 0) atomicOr(&st.big_sets, 1);
         return;
@@ -260,7 +260,8 @@ __global__ __launch_bounds__(kRT) void record_large_kernel(Params p)
         if (threadIdx.x == 0) s_n = 0;
         __syncthreads();
         const int k = k0 + threadIdx.x;
-        if (k <= st.Tp && p.sv_off[ly.fo0 + k + 1] - p.sv_off[ly.fo0 + k] > kRFill) s_list[atomicAdd(&s_n, 1)] = k;
+        if (k <= st.Tp && p.sv_off[ly.fo0 + k + 1] - p.sv_off[ly.fo0 + k] > min(kRFill, p.rec_fill))
+            s_list[atomicAdd(&s_n, 1)] = k;
         __syncthreads();
         const int nl = s_n;
         for (int q = 0; q < nl; q++) {
