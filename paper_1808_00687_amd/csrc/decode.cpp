@@ -331,7 +331,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.blank_id = o.blank_id;
     p.blank_thr = thr;
     p.lds_fill = test_env_int("WFSTDEC_TEST_LDS_FILL", 1 << 30);
-    p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1024);
+    p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1 << 30);
     p.profile = tm.on ? 1 : 0;
     p.rec_fill = test_env_int("WFSTDEC_TEST_RECORD_FILL", 1 << 30);
     p.capO = z.capO;
@@ -363,6 +363,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         p.kept = a.get<int32_t>(kp);
         p.path_arc = a.get<int32_t>(pa);
         p.path_frame = a.get<int32_t>(pa);
+        p.path_packed = a.get<int2>(pa);
     };
     p.capG = 8192;
     while (p.capG < z.capT) p.capG *= 2;
@@ -417,6 +418,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     tm.start(s);
     chk(launch_final(p, s));
     chk(launch_finish(p, s));
+    chk(launch_pack_paths(p, s));
     tm.stop(PH_FINAL, s);
     wt.mark("enqueue frames");
     chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
@@ -454,6 +456,16 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     std::vector<int32_t> kept_h(static_cast<size_t>(kp));
     chk(hipMemcpyAsync(fo_h.data(), p.sv_off, fo * sizeof(int64_t), hipMemcpyDeviceToHost, s));
     chk(hipMemcpyAsync(kept_h.data(), p.kept, kp * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    // the packed best paths, in utterance order
+    int64_t path_total = 0;
+    std::vector<int64_t> path_off(static_cast<size_t>(U), 0);
+    for (int u = 0; u < U; u++) {
+        path_off[u] = path_total;
+        if (st[u].status == WFST_OK) path_total += st[u].path_len;
+    }
+    std::vector<int2> paths_h(static_cast<size_t>(std::max<int64_t>(path_total, 1)));
+    if (path_total)
+        chk(hipMemcpyAsync(paths_h.data(), p.path_packed, path_total * sizeof(int2), hipMemcpyDeviceToHost, s));
     for (int u = 0; u < U; u++) {
         wfst_result *r = out[u];
         const UttState &x = st[u];
@@ -468,11 +480,6 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         r->reached_final = x.reached_final;
         r->path_arcs.resize(x.path_len);
         r->path_frames.resize(x.path_len);
-        const int64_t end = lay[u].path0 + lay[u].pathcap;
-        if (x.path_len) {
-            chk(hipMemcpyAsync(r->path_arcs.data(), p.path_arc + end - x.path_len, x.path_len * 4, hipMemcpyDeviceToHost, s));
-            chk(hipMemcpyAsync(r->path_frames.data(), p.path_frame + end - x.path_len, x.path_len * 4, hipMemcpyDeviceToHost, s));
-        }
         r->stats.tokens = x.n_tok;
         r->stats.tokens_last = x.n_last;
         r->stats.arcs_expanded = x.arcs_expanded;
@@ -513,6 +520,10 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
                             std::chrono::steady_clock::now().time_since_epoch()).count() - t_start;
     for (int u = 0; u < U; u++) {
         wfst_result *r = out[u];
+        for (size_t i = 0; i < r->path_arcs.size(); i++) {
+            r->path_arcs[i] = paths_h[path_off[u] + i].x;
+            r->path_frames[i] = paths_h[path_off[u] + i].y;
+        }
         r->kept.assign(kept_h.begin() + lay[u].kept0, kept_h.begin() + lay[u].kept0 + st[u].Tp);
         r->stats.decode_ms = wall;
         r->stats.search_ms = ph[PH_SEARCH];

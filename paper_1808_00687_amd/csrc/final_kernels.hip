@@ -504,11 +504,48 @@ __global__ __launch_bounds__(256) void lattice_emit_kernel(Params p)
         for (int i = threadIdx.x; i < n; i += blockDim.x) out[i] = buf[i];
 }
 
+// The best paths of all utterances packed one after another (utterance
+// order, each path in order), so that the host copies them at once.  One
+// block: offsets by a block scan over the utterances, then the block copies
+// each path.
+__global__ __launch_bounds__(1024) void pack_paths_kernel(Params p)
+{
+    __shared__ int sh_scan[17];
+    __shared__ int64_t sh_off[1024];
+    __shared__ int sh_len[1024];
+    int64_t carry = 0;
+    for (int u0 = 0; u0 < p.U; u0 += blockDim.x) {
+        const int u = u0 + threadIdx.x;
+        const int len = u < p.U && p.st[u].status == WFST_OK ? p.st[u].path_len : 0;
+        int total;
+        const int ex = block_excl_scan(len, sh_scan, &total);
+        sh_off[threadIdx.x] = carry + ex;
+        sh_len[threadIdx.x] = len;
+        carry += total;
+        __syncthreads();
+        const int nu = min(static_cast<int>(blockDim.x), p.U - u0);
+        for (int v = 0; v < nu; v++) {
+            const UttLayout &ly = p.lay[u0 + v];
+            const int lv = sh_len[v];
+            const int64_t src = ly.path0 + ly.pathcap - lv;
+            for (int i = threadIdx.x; i < lv; i += blockDim.x)
+                p.path_packed[sh_off[v] + i] = make_int2(p.path_arc[src + i], p.path_frame[src + i]);
+        }
+        __syncthreads();
+    }
+}
+
 }  // namespace
 
 hipError_t launch_final(const Params &p, hipStream_t s)
 {
     hipLaunchKernelGGL(final_kernel, dim3(p.U), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_paths(const Params &p, hipStream_t s)
+{
+    hipLaunchKernelGGL(pack_paths_kernel, dim3(1), dim3(1024), 0, s, p);
     return hipGetLastError();
 }
 

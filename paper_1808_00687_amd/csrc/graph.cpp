@@ -1,4 +1,5 @@
 // wfst_load: validation and device layout of the search graph.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -80,7 +81,8 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     const int64_t n_emit = e - n_eps;
 
     std::vector<int32_t> eoff, xoff, arc_src;
-    std::vector<int4> earc, xarc, srec;
+    std::vector<int4> earc, xarc, srec, ctab;
+    int64_t n_closure = 0;
     std::vector<uint8_t> has_eps;
     int32_t depth = 0;
     try {
@@ -141,6 +143,50 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
             srec[2 * static_cast<size_t>(s)] = make_int4(eoff[s], eoff[s + 1], xoff[s], xoff[s + 1]);
             if (xoff[s + 1] > xoff[s]) srec[2 * static_cast<size_t>(s) + 1] = xarc[xoff[s]];
         }
+        // Epsilon-closure lists: for a state whose epsilon paths number at
+        // most kClosureMax and are at most kClosureDepth arcs long, every
+        // such path as one entry {last destination, last arc, length, the
+        // path's weights in order}.  Children come before parents in reverse
+        // topological order, so a state's list is its arcs followed by each
+        // child's list behind the arc to it.
+        std::vector<int32_t> cl_size(static_cast<size_t>(n), 0), cl_depth(static_cast<size_t>(n), 0);
+        std::vector<int64_t> cl_off(static_cast<size_t>(n), -1);
+        for (size_t h = q.size(); h-- > 0;) {
+            const int32_t s = q[h];
+            if (xoff[s + 1] == xoff[s]) continue;
+            int64_t size = 0;
+            int32_t dep = 0;
+            bool child_listed = true;
+            for (int32_t x = xoff[s]; x < xoff[s + 1]; x++) {
+                const int32_t d = xarc[x].x & 0x7FFFFFFF;
+                size += 1 + cl_size[d];
+                dep = std::max(dep, 1 + cl_depth[d]);
+                if (cl_size[d] > 0 && cl_off[d] < 0) child_listed = false;
+            }
+            cl_size[s] = static_cast<int32_t>(std::min<int64_t>(size, kClosureMax + 1));
+            cl_depth[s] = std::min(dep, kClosureDepth + 1);
+            if (size > kClosureMax || dep > kClosureDepth || !child_listed) continue;
+            const int64_t off = static_cast<int64_t>(ctab.size() / 2);
+            if (off + size >= kClosureEntries) continue;
+            for (int32_t x = xoff[s]; x < xoff[s + 1]; x++) {
+                const int4 r = xarc[x];
+                const int32_t d = r.x & 0x7FFFFFFF;
+                ctab.push_back(make_int4(d, r.z, 1, r.y));
+                ctab.push_back(make_int4(0, 0, 0, 0));
+                if (cl_size[d] == 0) continue;
+                for (int32_t i = 0; i < cl_size[d]; i++) {
+                    const int4 c0 = ctab[2 * (cl_off[d] + i)], c1 = ctab[2 * (cl_off[d] + i) + 1];
+                    // the arc to d, then the child's path
+                    const int32_t w[5] = {r.y, c0.w, c1.x, c1.y, c1.z};
+                    ctab.push_back(make_int4(c0.x, c0.y, c0.z + 1, w[0]));
+                    ctab.push_back(make_int4(w[1], w[2], w[3], w[4]));
+                }
+            }
+            cl_off[s] = off;
+            srec[2 * static_cast<size_t>(s) + 1].w =
+                static_cast<int32_t>((static_cast<uint32_t>(off + 1) << 6) | static_cast<uint32_t>(size - 1));
+            n_closure++;
+        }
     } catch (const std::bad_alloc &) {
         return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
     }
@@ -153,7 +199,8 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     const size_t b_src = align(static_cast<size_t>(e) * 4 + 4);
     const size_t b_fin = final_weight ? align(static_cast<size_t>(n) * 4) : 0;
     const size_t b_srec = align(static_cast<size_t>(n) * 32);
-    const size_t total = b_eoff + b_xoff + b_earc + b_xarc + b_src + b_fin + b_srec;
+    const size_t b_ctab = align(ctab.size() * 16 + 16);
+    const size_t total = b_eoff + b_xoff + b_earc + b_xarc + b_src + b_fin + b_srec + b_ctab;
 
     wfst_graph *h = new (std::nothrow) wfst_graph();
     if (!h) return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
@@ -188,6 +235,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     g.d.arc_src = static_cast<const int32_t *>(put(arc_src.data(), arc_src.size() * 4, b_src));
     g.d.final_w = final_weight ? static_cast<const float *>(put(final_weight, static_cast<size_t>(n) * 4, b_fin)) : nullptr;
     g.d.srec = static_cast<const int4 *>(put(srec.data(), srec.size() * 16, b_srec));
+    g.d.ctab = static_cast<const int4 *>(put(ctab.data(), ctab.size() * 16, b_ctab));
     if (err != hipSuccess) {
         (void)hipFree(mem);
         delete h;
@@ -198,6 +246,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     g.max_ilabel = max_il;
     g.eps_depth = depth;
     g.device_bytes = static_cast<int64_t>(total);
+    g.n_closure = n_closure;
     *out = h;
     return WFST_OK;
 }

@@ -10,7 +10,12 @@
 //   srec[2N]   32-byte state records: the state's emitting and epsilon row
 //              offsets, then a copy of its first epsilon record (zeros if
 //              none), so that one load gives a state's rows and, for the
-//              common single-epsilon state, its epsilon arc
+//              common single-epsilon state, its epsilon arc; the copy's last
+//              word locates the state's epsilon-closure list
+//   ctab[]     epsilon-closure lists: every epsilon path from a state (up to
+//              size and length limits) as {last destination, last arc,
+//              length, the weights along the path}, so the closure from a
+//              lowered token needs no chain of dependent loads
 // Each state's arcs keep their user order inside the emitting and the
 // epsilon partition.  has_eps marks a destination with epsilon out-arcs, so a
 // kernel that lowers its token knows without another load whether the
@@ -45,7 +50,15 @@ struct DevGraph {
     const int32_t *arc_src;
     const float *final_w;
     const int4 *srec;   // 2 x N: {eoff[s], eoff[s+1], xoff[s], xoff[s+1]}, first epsilon record of s
+                        // whose 4th word is the state's closure list ((offset + 1) << 6 | size - 1, or 0)
+    const int4 *ctab;   // closure entries, 2 x int4 each: {dst, user arc, path length, w0}, {w1..w4}
 };
+
+// Epsilon-closure lists (built by wfst_load): at most kClosureMax paths of at
+// most kClosureDepth arcs per state, kClosureEntries entries in all.
+constexpr int kClosureMax = 64;
+constexpr int kClosureDepth = 5;
+constexpr int64_t kClosureEntries = (int64_t{1} << 26) - 2;
 
 // Host-side graph object behind the opaque wfst_graph handle.
 struct Graph {
@@ -54,6 +67,7 @@ struct Graph {
     int32_t max_ilabel;
     int32_t eps_depth;
     int64_t device_bytes;
+    int64_t n_closure;   // states with an epsilon-closure list
     void *mem;   // single device allocation holding every array
     // lattice-record slots per token that the last decodes on this graph
     // needed (emitting, epsilon), a starting point for the next ones
@@ -110,7 +124,7 @@ struct Params {
     int32_t blank_id;
     float blank_thr;
     int32_t lds_fill;         // states per frame the LDS token table takes (<= its fill limit)
-    int32_t gen_lds;          // epsilon items per wave queue in LDS (<= its capacity)
+    int32_t gen_lds;          // epsilon pool entries in LDS (<= its capacity)
     int32_t profile;          // count device clock ticks per search step
     int32_t rec_fill;         // survivors per set the record kernel's LDS table takes (<= its fill limit)
     UttState *st;
@@ -144,6 +158,7 @@ struct Params {
     int32_t *kept;
     int32_t *path_arc;
     int32_t *path_frame;
+    int2 *path_packed;        // every utterance's path {arc, frame}, one after another
     // search scratch per utterance: token table in device memory (frames that
     // overflow LDS), epsilon item spill lists, emitting candidate lists
     uint32_t *gkeys;          // U x capG
@@ -160,6 +175,7 @@ hipError_t launch_search(const Params &p, hipStream_t s);
 hipError_t launch_final(const Params &p, hipStream_t s);
 hipError_t launch_record(const Params &p, int max_frames, hipStream_t s);
 hipError_t launch_finish(const Params &p, hipStream_t s);
+hipError_t launch_pack_paths(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
 
 // ---- host helpers (graph.cpp) ----

@@ -439,11 +439,20 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
 
 // Relax the epsilon arcs of one item per lane (valid): the item's state
 // still holding the item's cost, i.e. no cheaper item of it follows.
+//
+// A state with an epsilon-closure list offers every epsilon path from it at
+// once: the path's cost is the item's cost plus the path's weights, added
+// one at a time in path order, which is the arithmetic of relaxing the path
+// arc by arc.  The minimum over paths equals the minimum the arc-by-arc
+// relaxation reaches (fl(x + w) is monotone in x), so the tokens are the
+// same; the list holds every path, so a token it lowers needs no item of its
+// own.  A state without a list relaxes its own arcs, and lowered tokens of
+// states with epsilon arcs become items.
 template <bool G>
 __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, WaveQ &wq, bool valid, uint2 it)
 {
     const int lane = lane_id();
-    int xb = 0, xd = 0;
+    int xb = 0, xd = 0, cb = 0, cn = 0;
     bool first = false;
     int4 x0 = make_int4(0, 0, 0, 0);
     const float cst = __uint_as_float(it.y);
@@ -453,9 +462,47 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             const int64_t s = static_cast<int64_t>(tld<G>(t.keys + it.x));
             const int4 lo = p.g.srec[2 * s];
             x0 = p.g.srec[2 * s + 1];
-            first = lo.w > lo.z;
-            xb = lo.z + 1;
-            xd = max(lo.w - lo.z - 1, 0);
+            const uint32_t cl = static_cast<uint32_t>(x0.w);
+            if (cl) {
+                cb = static_cast<int>(cl >> 6) - 1;
+                cn = static_cast<int>(cl & 63u) + 1;
+            } else {
+                first = lo.w > lo.z;
+                xb = lo.z + 1;
+                xd = max(lo.w - lo.z - 1, 0);
+            }
+        }
+    }
+    // closure lists, spread over the wave
+    {
+        const int incl = wave_incl_scan(cn);
+        const int pre = incl - cn;
+        const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
+        for (int k0 = 0; k0 < tot; k0 += kWave) {
+            const int kk = k0 + lane;
+            const int o = owner_lane(pre, kk);
+            const int ob = __shfl(cb, o, kWave);
+            const int op = __shfl(pre, o, kWave);
+            const float oc = __shfl(cst, o, kWave);
+            const uint32_t bnd = drop_bound(sh.best, p.beam);
+            bool act = false;
+            uint32_t d = 0, key = kEmptyKey;
+            int arc = 0;
+            float cnd = 0.0f;
+            if (kk < tot) {
+                const int64_t e = 2 * static_cast<int64_t>(ob + (kk - op));
+                const int4 c0 = p.g.ctab[e], c1 = p.g.ctab[e + 1];
+                cnd = oc + __int_as_float(c0.w);
+                if (c0.z > 1) cnd = cnd + __int_as_float(c1.x);
+                if (c0.z > 2) cnd = cnd + __int_as_float(c1.y);
+                if (c0.z > 3) cnd = cnd + __int_as_float(c1.z);
+                if (c0.z > 4) cnd = cnd + __int_as_float(c1.w);
+                d = static_cast<uint32_t>(c0.x);
+                arc = c0.y;
+                key = okey(cnd);
+                act = key <= bnd;
+            }
+            (void)offer1<G>(t, sh, wq, act, d, false, cnd, key, arc);
         }
     }
     {
