@@ -217,10 +217,10 @@ typedef struct wfst_stats {
        device clock of its workgroup, per step of a frame summed over the
        frames: [0] emitting expansion and the epsilon closure from the wave
        queues, [1] closure rounds over spilled epsilon items, [2] beam and
-       max-active pruning, [3] compaction of the survivors, [4] clearing of
-       the token table; [5] the emitting expansion as the first wave sees it
+       max-active pruning, [3] compaction of the survivors (which also clears
+       the token table); [4] the emitting expansion as the first wave sees it
        (part of [0]) */
-    double search_phase_ms[6];
+    double search_phase_ms[5];
     /* with WFST_PROFILE: this utterance's backtrace and lattice-beam pruning,
        from the device clock of the workgroups doing them (they run side by
        side after the search) */

@@ -20,9 +20,9 @@
 //      tokens lie within it than max_active, the exact max_active-th
 //      smallest key by radix select over an LDS histogram;
 //   4. compaction of the survivors into S_k (device memory, and LDS for the
-//      next expansion) in slot-list order, with the prefix of their
-//      emitting out-degrees, and the set's lattice record regions;
-//   5. clearing of the table.
+//      next expansion), with the prefix of their emitting out-degrees, and
+//      the set's lattice record regions; the table's slots are cleared as
+//      they are read.
 // Back-pointers and lattice records need nothing the next frame needs: the
 // record kernel derives them afterwards from the stored token sets, every
 // frame of every utterance in parallel.
@@ -44,7 +44,7 @@ constexpr int kSlots = 1 << kSlotBits;    // LDS hash slots
 constexpr int kFill = 6144;               // LDS states per frame before falling back to device memory
 constexpr int kQueue = 128;               // LDS epsilon items per wave queue
 constexpr int kSetCache = 3008;           // tokens of the previous set kept in LDS for the expansion
-constexpr int kRun = 2;                   // slot-list entries per thread per compaction pass
+constexpr int kCompact = 2;               // slot-list chunks a wave has in flight in the compaction
 constexpr int kChunks = 4;                // 64-arc chunks a wave has in flight in the expansion
 constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
 constexpr int kOverflow = 1;              // frame result: the table filled up
@@ -93,6 +93,8 @@ struct Sh {
     uint32_t best;       // smallest cost key among the frame's tokens
     int spill_n[2];      // epsilon items in the device-memory lists
     int ncand;           // emitting candidates listed this frame
+    unsigned long long alloc;   // compaction: emitting degrees << 32 | survivors placed
+    int xsum;            // compaction: epsilon degrees of the survivors
     int bin, before, cnt;
     int scan[52];
 };
@@ -108,7 +110,7 @@ struct Run {
     int64_t arcs;
     int64_t eps;         // epsilon out-arcs of the survivors
     int gframes;
-    uint64_t ph[6];      // device clock ticks per step (thread 0, profiling)
+    uint64_t ph[5];      // device clock ticks per step (thread 0, profiling)
     uint64_t t_last;
     uint64_t t_sub;
 };
@@ -584,6 +586,8 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         sh.best = kEmptyKey;
         sh.spill_n[0] = sh.spill_n[1] = 0;
         sh.ncand = 0;
+        sh.alloc = 0ull;
+        sh.xsum = 0;
         sh.cnt = 0;
     }
     __syncthreads();
@@ -610,7 +614,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cbuf);
         }
     }
-    sub_close(p, run, 5);
+    sub_close(p, run, 4);
     // ---- 2. epsilon closure: each wave its own queue, then spill rounds ----
     drain<G>(p, t, sh, wq);
     // full barrier: spilled items are read by other waves
@@ -693,79 +697,92 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
 
     phase_mark(p, run, 2);
 
-    // ---- 4. compaction into S_k, in slot-list order ----
+    // ---- 4. compaction into S_k ----
+    // Each wave takes chunks of the slot list, clears their slots, loads the
+    // survivors' state records together and places its survivors with one
+    // 64-bit LDS add of (emitting degrees << 32 | count): the returned value
+    // gives their positions and the prefix of emitting degrees before them
+    // at once.  The order of a token set is internal (sets are reported
+    // sorted by state), so no block-wide scan is needed.
+    using Slot = typename Tab<G>::Slot;
     const int64_t set0 = run.set0;
-    int n_kept = 0, a_kept = 0, x_kept = 0;
-    for (int e0 = 0; e0 < n; e0 += kT * kRun) {
-        int kslot[kRun], dd[kRun], eb[kRun], ed[kRun];
-        int4 xr[kRun];
-        unsigned long long vv[kRun];
-        int kc = 0, ac = 0, xc = 0;
+    for (int c = wid; c * kWave < n; c += kW * kCompact) {
+        bool kp[kCompact];
+        unsigned long long vv[kCompact];
+        int dd[kCompact];
 #pragma unroll
-        for (int r = 0; r < kRun; r++) {
-            const int i = e0 + tid * kRun + r;
-            kslot[r] = -1;
-            dd[r] = 0;
+        for (int r = 0; r < kCompact; r++) {
+            const int i = (c + r * kW) * kWave + lane;
+            kp[r] = false;
             vv[r] = kEmptyTok;
+            dd[r] = 0;
             if (i < n) {
-                kslot[r] = static_cast<int>(tld<G>(t.slots + i));
-                vv[r] = tld<G>(t.vals + kslot[r]);
-                dd[r] = static_cast<int>(tld<G>(t.keys + kslot[r]));
+                const Slot sl = tld<G>(t.slots + i);
+                vv[r] = tld<G>(t.vals + sl);
+                dd[r] = static_cast<int>(tld<G>(t.keys + sl));
+                kp[r] = static_cast<uint32_t>(vv[r] >> 32) <= cut;
+                t.keys[sl] = kEmptyKey;
+                t.vals[sl] = kEmptyTok;
             }
         }
-        bool kp[kRun];
+        int4 lo[kCompact], x0[kCompact];
 #pragma unroll
-        for (int r = 0; r < kRun; r++) {
-            kp[r] = kslot[r] >= 0 && static_cast<uint32_t>(vv[r] >> 32) <= cut;
-            eb[r] = ed[r] = 0;
-            xr[r] = make_int4(0, 0, 0, 0);
+        for (int r = 0; r < kCompact; r++) {
+            lo[r] = x0[r] = make_int4(0, 0, 0, 0);
             if (kp[r]) {
-                const int4 lo = p.g.srec[2 * static_cast<int64_t>(dd[r])];
-                const int4 x0 = p.g.srec[2 * static_cast<int64_t>(dd[r]) + 1];
-                eb[r] = lo.x;
-                ed[r] = lo.y;
-                xr[r] = make_int4(lo.w - lo.z, x0.x, x0.y, x0.z);
-                xc += lo.w - lo.z;
-                kc++;
-                ac += ed[r] - eb[r];
+                lo[r] = p.g.srec[2 * static_cast<int64_t>(dd[r])];
+                x0[r] = p.g.srec[2 * static_cast<int64_t>(dd[r]) + 1];
             }
         }
-        int3 tot;
-        const int3 ex = block_scan3(kc, ac, xc, sh.scan, &tot);
-        int pos = n_kept + ex.x, apos = a_kept + ex.y;
 #pragma unroll
-        for (int r = 0; r < kRun; r++) {
-            if (kp[r]) {
-                const int64_t rel = set0 + pos;
-                if (rel < ly.svcap) {
-                    const int64_t o = ly.sv0 + rel;
-                    p.sv_state[o] = dd[r];
-                    p.sv_tok[o] = vv[r];
-                    p.sv_ebeg[o] = eb[r];
-                    p.sv_epre[o] = apos;
-                    p.sv_x[o] = xr[r];
-                } else {
-                    sh.status = WFST_ECAPACITY;
-                }
-                const float c = tok_cost(vv[r]);
-                if (pos < kSetCache) {
-                    s_cost[pos] = c;
-                    s_epre[pos] = apos;
-                    s_ebeg[pos] = eb[r];
-                }
-                pos++;
-                apos += ed[r] - eb[r];
+        for (int r = 0; r < kCompact; r++) {
+            const int cnt = kp[r] ? 1 : 0;
+            const int deg = kp[r] ? lo[r].y - lo[r].x : 0;
+            const int xd = kp[r] ? lo[r].w - lo[r].z : 0;
+            const int ic = wave_incl_scan(cnt);
+            const int id = wave_incl_scan(deg);
+            const int ix = wave_incl_scan(xd);
+            const int tc = __builtin_amdgcn_readlane(ic, kWave - 1);
+            if (tc == 0) continue;
+            const int td = __builtin_amdgcn_readlane(id, kWave - 1);
+            const int tx = __builtin_amdgcn_readlane(ix, kWave - 1);
+            unsigned long long base = 0;
+            if (lane == 0) {
+                base = atomicAdd(&sh.alloc, (static_cast<unsigned long long>(td) << 32) | static_cast<uint32_t>(tc));
+                atomicAdd(&sh.xsum, tx);
+            }
+            base = (static_cast<unsigned long long>(__builtin_amdgcn_readlane(static_cast<int>(base >> 32), 0)) << 32) |
+                   static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(base), 0));
+            if (!kp[r]) continue;
+            const int pos = static_cast<int>(static_cast<uint32_t>(base)) + ic - cnt;
+            const int apos = static_cast<int>(base >> 32) + id - deg;
+            const int64_t rel = set0 + pos;
+            if (rel < ly.svcap) {
+                const int64_t o = ly.sv0 + rel;
+                p.sv_state[o] = dd[r];
+                p.sv_tok[o] = vv[r];
+                p.sv_ebeg[o] = lo[r].x;
+                p.sv_epre[o] = apos;
+                p.sv_x[o] = make_int4(xd, x0[r].x, x0[r].y, x0[r].z);
+            } else {
+                sh.status = WFST_ECAPACITY;
+            }
+            if (pos < kSetCache) {
+                s_cost[pos] = tok_cost(vv[r]);
+                s_epre[pos] = apos;
+                s_ebeg[pos] = lo[r].x;
             }
         }
-        n_kept += tot.x;
-        a_kept += tot.y;
-        x_kept += tot.z;
     }
-    const int ns = n_kept;
     // the next expansion reads S_k from LDS unless it is larger than the LDS
-    // copy; then its device-memory stores must be complete
-    if (G || ns > kSetCache) __syncthreads();
-    else lds_barrier();
+    // copy; then its device-memory stores must be complete (and the cleared
+    // device-memory table before the next offers)
+    table_barrier<G>();
+    if (!G && static_cast<uint32_t>(sh.alloc) > static_cast<uint32_t>(kSetCache)) __syncthreads();
+    const int n_kept = static_cast<int>(static_cast<uint32_t>(sh.alloc));
+    const int a_kept = static_cast<int>(sh.alloc >> 32);
+    const int x_kept = sh.xsum;
+    const int ns = n_kept;
     phase_mark(p, run, 3);
     if (ns == 0) return WFST_ENOPATH;
     if (sh.status) return sh.status;
@@ -791,14 +808,6 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     run.n_prev = ns;
     run.a_prev = a_kept;
 
-    // ---- 5. clear the table ----
-    for (int i = tid; i < n; i += kT) {
-        const int s2 = static_cast<int>(tld<G>(t.slots + i));
-        t.keys[s2] = kEmptyKey;
-        t.vals[s2] = kEmptyTok;
-    }
-    table_barrier<G>();
-    phase_mark(p, run, 4);
     return 0;
 }
 
@@ -881,7 +890,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
         st.arcs_expanded = run.arcs;
         st.eps_arcs = run.eps;
         st.gframes = run.gframes;
-        for (int i = 0; i < 6; i++) st.phase_ticks[i] = run.ph[i];
+        for (int i = 0; i < 5; i++) st.phase_ticks[i] = run.ph[i];
         if (rc != 0) st.status = rc;
     }
 }
