@@ -44,6 +44,7 @@ constexpr int kSlots = 1 << kSlotBits;    // LDS hash slots
 constexpr int kFill = 6144;               // LDS states per frame before falling back to device memory
 constexpr int kQueue = 128;               // LDS epsilon items per wave queue
 constexpr int kSetCache = 3008;           // tokens of the previous set kept in LDS for the expansion
+constexpr int kCs = 128;                  // 64-arc chunks of the previous set with their first token in LDS
 constexpr int kCompact = 2;               // slot-list chunks a wave has in flight in the compaction
 constexpr int kChunks = 4;                // 64-arc chunks a wave has in flight in the expansion
 constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
@@ -316,6 +317,7 @@ struct SetView<true> {
     const float *cost;
     const int32_t *epre;
     const int32_t *ebeg;
+    const uint16_t *cs;   // token owning the first arc of each 64-arc chunk (sets of at most kCs chunks)
     __device__ float c(int i) const { return cost[i]; }
 };
 
@@ -324,6 +326,7 @@ struct SetView<false> {
     const uint64_t *tok;
     const int32_t *epre;
     const int32_t *ebeg;
+    const uint16_t *cs;   // unused
     __device__ float c(int i) const { return tok_cost(tok[i]); }
 };
 
@@ -334,6 +337,8 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
 {
     const int lane = lane_id();
     const int wid = threadIdx.x / kWave;
+    // a set kept in LDS comes with the first token of each chunk
+    const bool use_cs = L && A <= kCs * kWave;
     // wave w takes chunks w, w + kW, w + 2 kW, ... : every wave gets work
     for (int c = wid; c * kWave < A; c += kW * kChunks) {
         if (__builtin_amdgcn_readfirstlane(sh.overflow)) break;   // the frame is redone anyway
@@ -349,7 +354,7 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
             oc[r] = 0.0f;
             if (a0 < A) {
                 // the 64 tokens from the one owning a0, and each lane's owner among them
-                const int t0 = search_le(v.epre, n_tok, a0);
+                const int t0 = use_cs ? static_cast<int>(v.cs[a0 / kWave]) : search_le(v.epre, n_tok, a0);
                 const int tt = t0 + lane;
                 int pre = 0x7FFFFFFF, eb = 0;
                 float cst = 0.0f;
@@ -567,7 +572,7 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
 template <bool G>
 __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
                                      const Tab<G> &t, uint2 *aux, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
-                                     uint2 *spill, int gcap, Run &run, int k)
+                                     uint16_t *s_cs, uint2 *spill, int gcap, Run &run, int k)
 {
     const int tid = threadIdx.x;
     const int lane = lane_id();
@@ -606,11 +611,11 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         const int src0 = static_cast<int>(run.prev0);
         int4 *cbuf = p.cand + ly.le0 + run.le_prev;
         if (run.n_prev <= kSetCache) {
-            SetView<true> v{s_cost, s_epre, s_ebeg};
+            SetView<true> v{s_cost, s_epre, s_ebeg, s_cs};
             expand<G, true>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cbuf);
         } else {
             const int64_t base = ly.sv0 + run.prev0;
-            SetView<false> v{p.sv_tok + base, p.sv_epre + base, p.sv_ebeg + base};
+            SetView<false> v{p.sv_tok + base, p.sv_epre + base, p.sv_ebeg + base, nullptr};
             expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cbuf);
         }
     }
@@ -771,6 +776,9 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
                 s_cost[pos] = tok_cost(vv[r]);
                 s_epre[pos] = apos;
                 s_ebeg[pos] = lo[r].x;
+                // the chunks whose first arc is one of this token's
+                for (int ch = (apos + kWave - 1) / kWave; ch * kWave < apos + deg && ch < kCs; ch++)
+                    s_cs[ch] = static_cast<uint16_t>(pos);
             }
         }
     }
@@ -820,6 +828,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     __shared__ float s_cost[kSetCache];    // the last token set, for the next expansion
     __shared__ int32_t s_epre[kSetCache];
     __shared__ int32_t s_ebeg[kSetCache];
+    __shared__ uint16_t s_cs[kCs];         // first token of each 64-arc chunk of the last set
     __shared__ Sh sh;
 
     const int u = blockIdx.x;
@@ -863,7 +872,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     bool gclean = false;
     int rc = 0;
     for (int k = 0; k <= Tp; k++) {
-        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, spill, gcap, run, k);
+        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, k);
         if (rc == kOverflow) {
             // more states than the LDS table holds: redo the frame in device memory
             for (int i = tid; i < kSlots; i += kT) {
@@ -878,7 +887,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
                 gclean = true;
             }
             __syncthreads();
-            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, spill, gcap, run, k);
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, k);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
             run.gframes++;
         }
