@@ -306,7 +306,8 @@ def main():
         # the utterance with the most decoded frames sets the search kernel's
         # duration: its workgroup's time per step of a frame
         crit = max(stats, key=lambda s: s["frames_decoded"])
-        names = ["expand+queue_closure", "spill_closure", "prune", "compact", "wave0_expand"]
+        names = ["expand+queue_closure", "spill_closure", "prune", "compact", "wave0_expand", "between_frames",
+                 "abandoned_lds_attempts"]
         out["search_steps_ms_longest_utt"] = {n: round(v, 3) for n, v in zip(names, crit["search_phase_ms"])}
         out["finish_ms_longest_utt"] = {"backtrace": round(crit["backtrace_ms"], 3),
                                         "lattice_prune": round(crit["lattice_prune_ms"], 3)}

@@ -219,8 +219,10 @@ typedef struct wfst_stats {
        queues, [1] closure rounds over spilled epsilon items, [2] beam and
        max-active pruning, [3] compaction of the survivors (which also clears
        the token table); [4] the emitting expansion as the first wave sees it
-       (part of [0]) */
-    double search_phase_ms[5];
+       (part of [0]); [5] between frames (bookkeeping and the frame's first
+       barrier); [6] frames abandoned for the device-memory table (their
+       steps are not in [0]-[3]) */
+    double search_phase_ms[7];
     /* with WFST_PROFILE: this utterance's backtrace and lattice-beam pruning,
        from the device clock of the workgroups doing them (they run side by
        side after the search) */

@@ -534,7 +534,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
             int khz = 0;
             if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, G.device) == hipSuccess && khz > 0)
             {
-                for (int i = 0; i < 5; i++)
+                for (int i = 0; i < 7; i++)
                     r->stats.search_phase_ms[i] = static_cast<double>(st[u].phase_ticks[i]) / khz;
                 r->stats.backtrace_ms = static_cast<double>(st[u].finish_ticks[0]) / khz;
                 r->stats.lattice_prune_ms = static_cast<double>(st[u].finish_ticks[1]) / khz;

@@ -97,7 +97,7 @@ struct UttState {
     int32_t path_len;
     int32_t pad1;
     int64_t lat_kept;
-    uint64_t phase_ticks[5];   // device clock ticks per search step (profiling only)
+    uint64_t phase_ticks[7];   // device clock ticks per search step (profiling only)
     uint64_t finish_ticks[2];  // device clock ticks of the backtrace and the lattice pruning
 };
 

@@ -46,7 +46,7 @@ constexpr int kQueue = 128;               // LDS epsilon items per wave queue
 constexpr int kSetCache = 3008;           // tokens of the previous set kept in LDS for the expansion
 constexpr int kCs = 128;                  // 64-arc chunks of the previous set with their first token in LDS
 constexpr int kCompact = 2;               // slot-list chunks a wave has in flight in the compaction
-constexpr int kChunks = 4;                // 64-arc chunks a wave has in flight in the expansion
+constexpr int kChunks = 2;                // 64-arc chunks a wave has in flight in the expansion
 constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
 constexpr int kOverflow = 1;              // frame result: the table filled up
 
@@ -111,45 +111,51 @@ struct Run {
     int64_t arcs;
     int64_t eps;         // epsilon out-arcs of the survivors
     int gframes;
-    uint64_t ph[5];      // device clock ticks per step (thread 0, profiling)
-    uint64_t t_last;
-    uint64_t t_sub;
+};
+
+// Profiling counters, kept by thread 0 in LDS (in registers they would
+// take space in every thread).
+struct Prof {
+    unsigned long long ph[7];    // device clock ticks per step
+    unsigned long long cur[4];   // the current frame's steps
+    unsigned long long t_last;
+    unsigned long long t_sub;
 };
 
 // Profiling: thread 0 adds the device clock since the previous mark to step
-// i (i < 0 only sets the mark).
-__device__ __forceinline__ void phase_mark(const Params &p, Run &run, int i)
+// i of the current frame (0-3), or to the time between frames (5).  A frame
+// that is completed adds its steps to the totals; one abandoned for the
+// device-memory table adds them to slot 6.
+__device__ __forceinline__ void phase_mark(const Params &p, Prof &pf, int i)
 {
     if (p.profile && threadIdx.x == 0) {
-        const uint64_t t = wall_clock64();
-        if (i >= 0) run.ph[i] += t - run.t_last;
-        run.t_last = t;
+        const unsigned long long t = wall_clock64();
+        if (i == 5) pf.ph[5] += t - pf.t_last;
+        else pf.cur[i] += t - pf.t_last;
+        pf.t_last = t;
+    }
+}
+
+__device__ __forceinline__ void phase_fold(const Params &p, Prof &pf, bool done)
+{
+    if (p.profile && threadIdx.x == 0) {
+        for (int i = 0; i < 4; i++) {
+            pf.ph[done ? i : 6] += pf.cur[i];
+            pf.cur[i] = 0;
+        }
     }
 }
 
 // Profiling of a part of a step as thread 0 sees it: open, then close into
 // slot i.
-__device__ __forceinline__ void sub_open(const Params &p, Run &run)
+__device__ __forceinline__ void sub_open(const Params &p, Prof &pf)
 {
-    if (p.profile && threadIdx.x == 0) run.t_sub = wall_clock64();
+    if (p.profile && threadIdx.x == 0) pf.t_sub = wall_clock64();
 }
 
-__device__ __forceinline__ void sub_close(const Params &p, Run &run, int i)
+__device__ __forceinline__ void sub_close(const Params &p, Prof &pf, int i)
 {
-    if (p.profile && threadIdx.x == 0) run.ph[i] += wall_clock64() - run.t_sub;
-}
-
-template <bool G>
-__device__ __forceinline__ int tab_find(const Tab<G> &t, uint32_t d)
-{
-    uint32_t h = hash_state(d) >> t.shift;
-    for (int probe = 0; probe < kMaxProbe; probe++) {
-        const uint32_t k = tld<G>(t.keys + h);
-        if (k == d) return static_cast<int>(h);
-        if (k == kEmptyKey) return -1;
-        h = (h + 1) & t.mask;
-    }
-    return -1;
+    if (p.profile && threadIdx.x == 0) pf.ph[i] += wall_clock64() - pf.t_sub;
 }
 
 // A wave's epsilon work list: an LDS queue of (table slot, cost bits) items
@@ -572,7 +578,7 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
 template <bool G>
 __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
                                      const Tab<G> &t, uint2 *aux, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
-                                     uint16_t *s_cs, uint2 *spill, int gcap, Run &run, int k)
+                                     uint16_t *s_cs, uint2 *spill, int gcap, Run &run, Prof &pf, int k)
 {
     const int tid = threadIdx.x;
     const int lane = lane_id();
@@ -585,6 +591,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     wq.spill_n = &sh.spill_n[0];
     wq.scap = gcap;
 
+    phase_mark(p, pf, 5);
     if (tid == 0) {
         sh.nslots = 0;
         sh.overflow = 0;
@@ -596,10 +603,10 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         sh.cnt = 0;
     }
     __syncthreads();
-    phase_mark(p, run, -1);
+    phase_mark(p, pf, 5);
 
     // ---- 1. expansion ----
-    sub_open(p, run);
+    sub_open(p, pf);
     if (k == 0) {
         if (wid == 0) {
             const int s = p.g.start;
@@ -619,12 +626,12 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cbuf);
         }
     }
-    sub_close(p, run, 4);
+    sub_close(p, pf, 4);
     // ---- 2. epsilon closure: each wave its own queue, then spill rounds ----
     drain<G>(p, t, sh, wq);
     // full barrier: spilled items are read by other waves
     __syncthreads();
-    phase_mark(p, run, 0);
+    phase_mark(p, pf, 0);
     int sp = 0;
     while (true) {
         const int total = min(sh.spill_n[sp], gcap);
@@ -647,8 +654,11 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         __syncthreads();
         sp ^= 1;
     }
-    phase_mark(p, run, 1);
-    if (sh.overflow) return kOverflow;
+    phase_mark(p, pf, 1);
+    if (sh.overflow) {
+        phase_fold(p, pf, false);   // the frame is redone on the device-memory table
+        return kOverflow;
+    }
     if (sh.status) return sh.status;
 
     // ---- 3. pruning ----
@@ -700,7 +710,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         __syncthreads();
     }
 
-    phase_mark(p, run, 2);
+    phase_mark(p, pf, 2);
 
     // ---- 4. compaction into S_k ----
     // Each wave takes chunks of the slot list, clears their slots, loads the
@@ -791,7 +801,8 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     const int a_kept = static_cast<int>(sh.alloc >> 32);
     const int x_kept = sh.xsum;
     const int ns = n_kept;
-    phase_mark(p, run, 3);
+    phase_mark(p, pf, 3);
+    phase_fold(p, pf, true);
     if (ns == 0) return WFST_ENOPATH;
     if (sh.status) return sh.status;
     // Token set k, its cutoff and the lattice record regions of set k: one
@@ -830,6 +841,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     __shared__ int32_t s_ebeg[kSetCache];
     __shared__ uint16_t s_cs[kCs];         // first token of each 64-arc chunk of the last set
     __shared__ Sh sh;
+    __shared__ Prof pf;
 
     const int u = blockIdx.x;
     const int tid = threadIdx.x;
@@ -869,10 +881,16 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     __syncthreads();
 
     Run run{};
+    if (tid == 0) {
+        for (int i = 0; i < 7; i++) pf.ph[i] = 0;
+        for (int i = 0; i < 4; i++) pf.cur[i] = 0;
+        pf.t_last = wall_clock64();
+        pf.t_sub = 0;
+    }
     bool gclean = false;
     int rc = 0;
     for (int k = 0; k <= Tp; k++) {
-        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, k);
+        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k);
         if (rc == kOverflow) {
             // more states than the LDS table holds: redo the frame in device memory
             for (int i = tid; i < kSlots; i += kT) {
@@ -887,7 +905,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
                 gclean = true;
             }
             __syncthreads();
-            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, k);
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
             run.gframes++;
         }
@@ -899,7 +917,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
         st.arcs_expanded = run.arcs;
         st.eps_arcs = run.eps;
         st.gframes = run.gframes;
-        for (int i = 0; i < 5; i++) st.phase_ticks[i] = run.ph[i];
+        for (int i = 0; i < 7; i++) st.phase_ticks[i] = pf.ph[i];
         if (rc != 0) st.status = rc;
     }
 }

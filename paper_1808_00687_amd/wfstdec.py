@@ -56,7 +56,7 @@ class _Stats(C.Structure):
                 ("tokens_last", C.c_int64), ("arcs_expanded", C.c_int64), ("eps_arcs", C.c_int64), ("lattice_raw", C.c_int64),
                 ("lattice_kept", C.c_int64), ("decode_ms", C.c_double), ("search_ms", C.c_double),
                 ("record_ms", C.c_double), ("final_ms", C.c_double), ("search_launches", C.c_int32),
-                ("search_phase_ms", C.c_double * 5), ("backtrace_ms", C.c_double),
+                ("search_phase_ms", C.c_double * 7), ("backtrace_ms", C.c_double),
                 ("lattice_prune_ms", C.c_double)]
 
 
