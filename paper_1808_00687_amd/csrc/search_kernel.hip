@@ -100,7 +100,7 @@ struct Sh {
     int scan[52];
 };
 
-// Running values of the utterance, identical in every thread (eps aside).
+// Running values of the utterance (in LDS, updated by thread 0).
 struct Run {
     int64_t set0;        // relative survivor index where the next set starts
     int64_t prev0;       // relative start of S_{k-1}
@@ -810,22 +810,24 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     // arc of S_k at most.
     const int64_t a_rec = k < Tp ? a_kept : 0;
     if (run.le + a_rec > ly.lecap || (p.lattice && run.lx + x_kept > ly.lxcap)) return WFST_ECAPACITY;
+    // the running values live in LDS: thread 0 updates them, every thread
+    // reads them after the next frame's first barrier
     if (tid == 0) {
         p.sv_off[ly.fo0 + k + 1] = set0 + ns;
         p.cut_arr[ly.fo0 + k] = cut;
         p.le_off[ly.fo0 + k + 1] = run.le + a_rec;
         p.lx_off[ly.fo0 + k + 1] = run.lx + x_kept;
         if (k > 0) p.cand_cnt[ly.fo0 + k - 1] = sh.ncand;
+        run.le_prev = run.le;
+        run.le += a_rec;
+        run.lx += x_kept;
+        run.eps += x_kept;
+        run.arcs += a_rec;
+        run.prev0 = set0;
+        run.set0 = set0 + ns;
+        run.n_prev = ns;
+        run.a_prev = a_kept;
     }
-    run.le_prev = run.le;
-    run.le += a_rec;
-    run.lx += x_kept;
-    run.eps += x_kept;
-    run.arcs += a_rec;
-    run.prev0 = set0;
-    run.set0 = set0 + ns;
-    run.n_prev = ns;
-    run.a_prev = a_kept;
 
     return 0;
 }
@@ -880,7 +882,8 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     }
     __syncthreads();
 
-    Run run{};
+    __shared__ Run run;   // running values of the utterance, updated by thread 0
+    if (tid == 0) run = Run{};
     if (tid == 0) {
         for (int i = 0; i < 7; i++) pf.ph[i] = 0;
         for (int i = 0; i < 4; i++) pf.cur[i] = 0;
@@ -907,7 +910,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
             __syncthreads();
             rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
-            run.gframes++;
+            if (tid == 0) run.gframes++;
         }
         if (rc != 0) break;
     }
