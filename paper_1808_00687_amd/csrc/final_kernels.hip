@@ -120,10 +120,10 @@ __device__ void backtrace_block(const Params &p, int u, int *sh)
 }
 
 constexpr int kLatLds = 8192;   // survivors per token set kept in LDS by the backward pass
-constexpr int kLatT = 1024;     // threads of a finish block
+constexpr int kLatT = 512;      // threads of a finish block
 constexpr int kRE = 4;          // emitting records per thread held in registers
 constexpr int kRX = 2;          // epsilon records per thread held in registers
-constexpr int kRC = 4;          // survivors per thread held in registers
+constexpr int kRC = 6;          // survivors per thread held in registers
 static_assert(kRX == 2, "the epsilon records are copied out of the prefetch registers pairwise");
 
 // Where the records and survivors of one token set j lie.
