@@ -182,8 +182,10 @@ typedef struct wfst_lat_arc {
     float extra;
 } wfst_lat_arc;
 
-/* Lattice-beam-pruned lattice, sorted by (frame, arc), copied to host
- * memory on first call.  n = 0 when the lattice was disabled. */
+/* Lattice-beam-pruned lattice, sorted by (frame, arc), in host memory: the
+ * first call on any result of a batch copies the lattices of the whole batch
+ * in one transfer, which the results share (valid while any of them lives).
+ * n = 0 when the lattice was disabled. */
 int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs);
 
 /* The same lattice in device memory (owned by the result). */

@@ -43,6 +43,15 @@ struct DevBuf {
     }
 };
 
+// The lattices of one batch in host memory: copied from the device buffer in
+// one transfer when the first result asks for its lattice, then shared.
+struct LatHost {
+    std::mutex mu;
+    bool loaded = false;
+    int64_t total = 0;
+    std::vector<wfst_lat_arc> arcs;
+};
+
 }  // namespace
 
 struct wfst_result {
@@ -54,9 +63,7 @@ struct wfst_result {
     int32_t T = 0, Tp = 0;
     std::shared_ptr<DevBuf> lat_dev;
     int64_t lat_off = 0, lat_n = 0;
-    mutable std::mutex lat_mu;
-    mutable std::vector<wfst_lat_arc> lat_host;
-    mutable bool lat_loaded = false;
+    std::shared_ptr<LatHost> lat_host;   // the batch's lattice in host memory, copied on first use
     bool has_tokens = false;
     std::vector<int64_t> tok_off;
     std::vector<int32_t> tok_state, tok_arc;
@@ -434,12 +441,15 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         if (st[u].status == WFST_ECAPACITY) return WFST_ECAPACITY;
 
     std::shared_ptr<DevBuf> lat_buf;
+    std::shared_ptr<LatHost> lat_host;
     if (lattice) {
         int64_t tot = 0;
         for (int u = 0; u < U; u++) {
             lay[u].lo0 = tot;
             if (st[u].status == WFST_OK) tot += st[u].lat_kept;
         }
+        lat_host = std::make_shared<LatHost>();
+        lat_host->total = tot;
         lat_buf = std::make_shared<DevBuf>();
         (void)hipGetDevice(&lat_buf->device);
         chk(hipMalloc(&lat_buf->p, static_cast<size_t>(std::max<int64_t>(tot, 1)) * sizeof(int4)));
@@ -488,6 +498,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         r->stats.lattice_kept = lattice ? x.lat_kept : 0;
         if (lattice) {
             r->lat_dev = lat_buf;
+            r->lat_host = lat_host;
             r->lat_off = lay[u].lo0;
             r->lat_n = x.lat_kept;
         }
@@ -757,19 +768,27 @@ extern "C" int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_
 {
     clear_error();
     if (!r) return fail(WFST_EINVAL, "wfst_result_lattice: NULL result");
-    std::lock_guard<std::mutex> lk(r->lat_mu);
-    if (!r->lat_loaded) {
-        r->lat_host.resize(static_cast<size_t>(r->lat_n));
-        if (r->lat_n) {
-            DeviceGuard dg(r->lat_dev->device);
-            hipError_t e = hipMemcpy(r->lat_host.data(), static_cast<int4 *>(r->lat_dev->p) + r->lat_off,
-                                     r->lat_n * sizeof(wfst_lat_arc), hipMemcpyDeviceToHost);
-            if (e != hipSuccess) return hip_fail(e, "wfst_result_lattice: copy");
+    if (!r->lat_host) {
+        if (n) *n = 0;
+        if (arcs) *arcs = nullptr;
+        return WFST_OK;
+    }
+    LatHost &h = *r->lat_host;
+    {
+        std::lock_guard<std::mutex> lk(h.mu);
+        if (!h.loaded) {
+            h.arcs.resize(static_cast<size_t>(std::max<int64_t>(h.total, 1)));
+            if (h.total) {
+                DeviceGuard dg(r->lat_dev->device);
+                hipError_t e = hipMemcpy(h.arcs.data(), r->lat_dev->p, h.total * sizeof(wfst_lat_arc),
+                                         hipMemcpyDeviceToHost);
+                if (e != hipSuccess) return hip_fail(e, "wfst_result_lattice: copy");
+            }
+            h.loaded = true;
         }
-        r->lat_loaded = true;
     }
     if (n) *n = r->lat_n;
-    if (arcs) *arcs = r->lat_host.data();
+    if (arcs) *arcs = h.arcs.data() + r->lat_off;
     return WFST_OK;
 }
 
