@@ -127,6 +127,7 @@ struct Params {
     int32_t gen_lds;          // epsilon pool entries in LDS (<= its capacity)
     int32_t profile;          // count device clock ticks per search step
     int32_t rec_fill;         // survivors per set the record kernel's LDS table takes (<= its fill limit)
+    int32_t rec_big_fill;     // the same for the large-set pass's LDS table
     UttState *st;
     const UttLayout *lay;
     // survivors (per utterance regions)

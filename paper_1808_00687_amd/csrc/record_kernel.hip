@@ -18,8 +18,8 @@
 // The start token's back-pointer is -1.  The search reserved each set's
 // regions (one entry per emitting and per epsilon out-arc of the set); the
 // block appends into them and stores the counts.  Sets larger than the LDS
-// table are left to a second launch that takes them per utterance with a
-// table in device memory.
+// table are left to a second launch with a larger LDS table (or, beyond that,
+// the utterance's device-memory table).
 #include "device_util.h"
 
 namespace wfd {
@@ -237,24 +237,34 @@ __global__ __launch_bounds__(kRT) void record_kernel(Params p)
     record_set<false>(p, u, k, t, sh);
 }
 
-// One block per utterance: the sets too large for the LDS table, in turn,
-// with the utterance's device-memory table (at most three quarters full:
-// its size bounds the states a frame may reach).
+// The sets too large for record_kernel's table: kLargeParts blocks per
+// utterance share them (set k goes to part k mod kLargeParts); a set of up
+// to kRBigFill survivors uses a 128 KB LDS table, a larger one the
+// utterance's device-memory table (at most three quarters full: its size
+// bounds the states a frame may reach), taken by part 0 alone.
+constexpr int kLargeParts = 4;
+constexpr int kRBigBits = 14;
+constexpr int kRBigFill = (1 << kRBigBits) / 4 * 3;
+
 __global__ __launch_bounds__(kRT) void record_large_kernel(Params p)
 {
+    __shared__ uint32_t s_keys[1 << kRBigBits];
+    __shared__ int32_t s_vals[1 << kRBigBits];
     __shared__ RSh sh;
     __shared__ int s_list[kRT];
     __shared__ int s_n;
     const int u = blockIdx.x;
+    const int part = blockIdx.y;
     const UttState &st = p.st[u];
     if (st.status != 0 || !st.big_sets) return;
     const UttLayout &ly = p.lay[u];
-    RTab<true> t;
+    RTab<true> gt;
     const int64_t gbase = static_cast<int64_t>(u) * p.capG;
-    t.keys = p.gkeys + gbase;
-    t.vals = p.gslots + gbase;
-    t.mask = static_cast<uint32_t>(p.capG - 1);
-    t.shift = 32 - (31 - __clz(static_cast<int>(p.capG)));
+    gt.keys = p.gkeys + gbase;
+    gt.vals = p.gslots + gbase;
+    gt.mask = static_cast<uint32_t>(p.capG - 1);
+    gt.shift = 32 - (31 - __clz(static_cast<int>(p.capG)));
+    const int big_fill = min(kRBigFill, p.rec_big_fill);
     // the large sets, kRT frames at a time
     for (int k0 = 0; k0 <= st.Tp; k0 += kRT) {
         if (threadIdx.x == 0) s_n = 0;
@@ -264,10 +274,27 @@ __global__ __launch_bounds__(kRT) void record_large_kernel(Params p)
             s_list[atomicAdd(&s_n, 1)] = k;
         __syncthreads();
         const int nl = s_n;
-        for (int q = 0; q < nl; q++) {
-            for (int64_t i = threadIdx.x; i < p.capG; i += blockDim.x) t.keys[i] = kEmptyKey;
-            __syncthreads();
-            record_set<true>(p, u, s_list[q], t, sh);
+        for (int i = 0; i < nl; i++) {
+            const int kk = s_list[i];
+            const int n = static_cast<int>(p.sv_off[ly.fo0 + kk + 1] - p.sv_off[ly.fo0 + kk]);
+            if (n <= big_fill) {
+                if (kk % kLargeParts != part) continue;
+                int bits = 10;
+                while (bits < kRBigBits && (1 << bits) < 2 * n) bits++;
+                RTab<false> t;
+                t.keys = s_keys;
+                t.vals = s_vals;
+                t.mask = (1u << bits) - 1u;
+                t.shift = 32 - bits;
+                for (int j = threadIdx.x; j < (1 << bits); j += blockDim.x) s_keys[j] = kEmptyKey;
+                __syncthreads();
+                record_set<false>(p, u, kk, t, sh);
+            } else {
+                if (part != 0) continue;
+                for (int64_t j = threadIdx.x; j < p.capG; j += blockDim.x) gt.keys[j] = kEmptyKey;
+                __syncthreads();
+                record_set<true>(p, u, kk, gt, sh);
+            }
             __syncthreads();
         }
     }
@@ -280,7 +307,7 @@ hipError_t launch_record(const Params &p, int max_frames, hipStream_t s)
     hipLaunchKernelGGL(record_kernel, dim3(max_frames + 1, p.U), dim3(kRT), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(record_large_kernel, dim3(p.U), dim3(kRT), 0, s, p);
+    hipLaunchKernelGGL(record_large_kernel, dim3(p.U, kLargeParts), dim3(kRT), 0, s, p);
     return hipGetLastError();
 }
 

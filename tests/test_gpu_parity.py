@@ -162,21 +162,22 @@ def test_device_memory_table_path(dec, torch_mod, oracle_mod, cfg2, fill):
         parity.assert_same(ro, rg, lattice=True, tag="device table fill %d seed %d" % (fill, seed))
 
 
-@pytest.mark.parametrize("fill", [1, 900])
-def test_record_large_set_path(dec, torch_mod, oracle_mod, cfg2, fill):
+@pytest.mark.parametrize("fill,big", [(1, 1), (900, 1), (1, 1 << 20), (900, 1500)])
+def test_record_large_set_path(dec, torch_mod, oracle_mod, cfg2, fill, big):
     # token sets of more than `fill` survivors get their back-pointers and
-    # lattice records from the per-utterance pass with a device-memory table
-    # (every set for fill = 1, a mix for 900), alone and in a batch
+    # lattice records from the large-set pass: with its LDS table up to `big`
+    # survivors, beyond that with the utterance's device-memory table (every
+    # set for fill = 1, a mix for 900), alone and in a batch
     wl, gh = cfg2
-    with _env(WFSTDEC_TEST_RECORD_FILL=fill):
+    with _env(WFSTDEC_TEST_RECORD_FILL=fill, WFSTDEC_TEST_RECORD_BIG_FILL=big):
         ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:60], gh=gh, beam=13.0,
                       max_active=7000, lattice_beam=8.0)
-        parity.assert_same(ro, rg, lattice=True, tag="record fill %d" % fill)
+        parity.assert_same(ro, rg, lattice=True, tag="record fill %d/%d" % (fill, big))
         lls = [wl.loglikes[0][:40], wl.loglikes[0][10:35]]
         res = dec.wfst_decode_batch(gh, [to_dev(torch_mod, x) for x in lls], 13.0, 7000, 8.0, record_tokens=True)
         for i, x in enumerate(lls):
             ro = oracle_mod.decode(wl.graph, x, 13.0, 7000, 8.0)
-            parity.assert_same(ro, res[i], lattice=True, tag="record fill %d batch %d" % (fill, i))
+            parity.assert_same(ro, res[i], lattice=True, tag="record fill %d/%d batch %d" % (fill, big, i))
 
 
 def test_capacity_retry(dec, torch_mod, oracle_mod, cfg2):
