@@ -834,16 +834,33 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
 
 __global__ __launch_bounds__(kT) void search_kernel(Params p)
 {
-    __shared__ uint32_t s_keys[kSlots];
-    __shared__ unsigned long long s_vals[kSlots];
-    __shared__ uint16_t s_slots[kFill];
-    __shared__ uint2 s_aux[kW * kQueue];   // per-wave epsilon queues, or the select histogram
-    __shared__ float s_cost[kSetCache];    // the last token set, for the next expansion
-    __shared__ int32_t s_epre[kSetCache];
-    __shared__ int32_t s_ebeg[kSetCache];
-    __shared__ uint16_t s_cs[kCs];         // first token of each 64-arc chunk of the last set
-    __shared__ Sh sh;
-    __shared__ Prof pf;
+    // All LDS in one struct, the small fields first: they then lie below
+    // 64 KB, where an LDS instruction reaches them with an immediate offset
+    // instead of an address held in a register.
+    struct Lds {
+        Sh sh;
+        Prof pf;
+        Run run;
+        uint16_t cs[kCs];                  // first token of each 64-arc chunk of the last set
+        uint2 aux[kW * kQueue];            // per-wave epsilon queues, or the select histogram
+        float cost[kSetCache];             // the last token set, for the next expansion
+        int32_t epre[kSetCache];
+        int32_t ebeg[kSetCache];
+        uint16_t slots[kFill];
+        uint32_t keys[kSlots];
+        unsigned long long vals[kSlots];
+    };
+    __shared__ Lds lds;
+    Sh &sh = lds.sh;
+    Prof &pf = lds.pf;
+    uint32_t *s_keys = lds.keys;
+    unsigned long long *s_vals = lds.vals;
+    uint16_t *s_slots = lds.slots;
+    uint2 *s_aux = lds.aux;
+    float *s_cost = lds.cost;
+    int32_t *s_epre = lds.epre;
+    int32_t *s_ebeg = lds.ebeg;
+    uint16_t *s_cs = lds.cs;
 
     const int u = blockIdx.x;
     const int tid = threadIdx.x;
@@ -882,7 +899,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     }
     __syncthreads();
 
-    __shared__ Run run;   // running values of the utterance, updated by thread 0
+    Run &run = lds.run;   // running values of the utterance, updated by thread 0
     if (tid == 0) run = Run{};
     if (tid == 0) {
         for (int i = 0; i < 7; i++) pf.ph[i] = 0;
