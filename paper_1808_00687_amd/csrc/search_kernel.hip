@@ -578,7 +578,8 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
 template <bool G>
 __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
                                      const Tab<G> &t, uint2 *aux, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
-                                     uint16_t *s_cs, uint2 *spill, int gcap, Run &run, Prof &pf, int k)
+                                     uint16_t *s_cs, uint2 *spill, int gcap, Run &run, Prof &pf, int k,
+                                     int &n_ins)
 {
     const int tid = threadIdx.x;
     const int lane = lane_id();
@@ -663,6 +664,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
 
     // ---- 3. pruning ----
     const int n = sh.nslots;
+    n_ins = n;
     const uint32_t kb = sh.best;
     const uint32_t lim = beam_limit(kb, p.beam);
     uint32_t cut = lim;
@@ -908,14 +910,23 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
         pf.t_sub = 0;
     }
     bool gclean = false;
+    // After a frame that needed the device-memory table, the next frames go
+    // there directly while their tables stay close to the LDS limit: a frame
+    // started in LDS would most likely be abandoned half-way.
+    bool in_g = false;
+    const int g_stay = lt.fill - lt.fill / 8;
     int rc = 0;
     for (int k = 0; k <= Tp; k++) {
-        rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k);
-        if (rc == kOverflow) {
-            // more states than the LDS table holds: redo the frame in device memory
-            for (int i = tid; i < kSlots; i += kT) {
-                s_keys[i] = kEmptyKey;
-                s_vals[i] = kEmptyTok;
+        int n_ins = 0;
+        if (!in_g)
+            rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k, n_ins);
+        if (in_g || rc == kOverflow) {
+            if (!in_g) {
+                // the abandoned attempt left states in the LDS table
+                for (int i = tid; i < kSlots; i += kT) {
+                    s_keys[i] = kEmptyKey;
+                    s_vals[i] = kEmptyTok;
+                }
             }
             if (!gclean) {
                 for (int64_t i = tid; i < p.capG; i += kT) {
@@ -925,9 +936,10 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
                 gclean = true;
             }
             __syncthreads();
-            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k);
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k, n_ins);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
             if (tid == 0) run.gframes++;
+            in_g = n_ins > g_stay;
         }
         if (rc != 0) break;
     }
