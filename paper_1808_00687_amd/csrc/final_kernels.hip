@@ -119,12 +119,13 @@ __device__ void backtrace_block(const Params &p, int u, int *sh)
     if (threadIdx.x == 0) st.path_len = cnt;
 }
 
+// s_waitcnt immediate: vmcnt(0), the other counters left free
+constexpr int kWaitVm0 = 0x0F70;
 constexpr int kLatLds = 8192;   // survivors per token set kept in LDS by the backward pass
 constexpr int kLatT = 512;      // threads of a finish block
 constexpr int kRE = 4;          // emitting records per thread held in registers
 constexpr int kRX = 2;          // epsilon records per thread held in registers
 constexpr int kRC = 6;          // survivors per thread held in registers
-static_assert(kRX == 2, "the epsilon records are copied out of the prefetch registers pairwise");
 
 // Where the records and survivors of one token set j lie.
 struct LatMeta {
@@ -151,6 +152,77 @@ __device__ __forceinline__ LatMeta lat_meta(const Params &p, const UttLayout &ly
     m.x0 = p.lx_off[ly.fo0 + j];
     m.x1 = m.x0 + p.lx_cnt[ly.fo0 + j];
     return m;
+}
+
+// The same offsets loaded by lanes 0-5 of each wave with vector loads, to be
+// unpacked a step later: a scalar load would be waited for at the next LDS
+// barrier (scalar loads and LDS share one wait counter), a vector load only
+// where its value is used.
+__device__ __forceinline__ int64_t lat_meta_issue(const Params &p, const UttLayout &ly, int j, int Tp)
+{
+    const int l = lane_id();
+    const int64_t f = ly.fo0 + j;
+    const int64_t *a = nullptr;
+    if (l == 0) a = p.sv_off + f;
+    else if (l == 1) a = p.sv_off + f + 1;
+    else if (l == 2 && j < Tp) a = p.le_off + f;
+    else if (l == 3 && j < Tp) a = p.le_cnt + f;
+    else if (l == 4) a = p.lx_off + f;
+    else if (l == 5) a = p.lx_cnt + f;
+    return a ? *a : 0;
+}
+
+__device__ __forceinline__ int64_t lane64(int64_t v, int l)
+{
+    const int lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint64_t>(v)), l);
+    const int hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint64_t>(v) >> 32), l);
+    return static_cast<int64_t>((static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo));
+}
+
+__device__ __forceinline__ LatMeta lat_meta_take(int64_t v)
+{
+    LatMeta m;
+    m.b0 = lane64(v, 0);
+    m.nB = lane64(v, 1) - m.b0;
+    m.e0 = lane64(v, 2);
+    m.e1 = m.e0 + lane64(v, 3);
+    m.x0 = lane64(v, 4);
+    m.x1 = m.x0 + lane64(v, 5);
+    return m;
+}
+
+// What a step of the backward pass leaves to be stored at the start of the
+// next: the extra costs of its register-held records and its kept count.
+struct LatPend {
+    float ee[kRE];
+    float ex[kRX];
+    int64_t e0, e1, x0, x1;
+    unsigned long long kept;
+    int j;
+};
+
+__device__ __forceinline__ void lat_flush(const Params &p, const UttLayout &ly, LatPend &pd,
+                                          unsigned long long *kcnt)
+{
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int q = 0; q < kRE; q++) {
+        const int64_t r = pd.e0 + tid + q * kLatT;
+        if (r < pd.e1) p.ex_e[ly.le0 + r] = pd.ee[q];
+    }
+#pragma unroll
+    for (int q = 0; q < kRX; q++) {
+        const int64_t r = pd.x0 + tid + q * kLatT;
+        if (r < pd.x1) p.ex_x[ly.lx0 + r] = pd.ex[q];
+    }
+    if (pd.j >= 0) {
+        // a thread keeps fewer than 2^31 arcs of one set
+        const int k = __builtin_amdgcn_readlane(wave_incl_scan(static_cast<int>(pd.kept)), kWave - 1);
+        if (lane_id() == 0 && k) atomicAdd(kcnt + pd.j, static_cast<unsigned long long>(k));
+    }
+    pd.e0 = pd.e1 = pd.x0 = pd.x1 = 0;
+    pd.j = -1;
+    pd.kept = 0;
 }
 
 __device__ __forceinline__ void lat_fetch(const Params &p, const UttLayout &ly, const LatMeta &m, LatRegs &r)
@@ -202,18 +274,36 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
     int *flag = sh;   // three rotating "changed" flags of the epsilon rounds
     int hA = 0;          // LDS half holding S_j+1
     bool a_lds = false;  // S_j+1's costs and extra costs are in that half
+    // Two-deep pipeline: while set j is processed, the records of set j-1
+    // are in flight (loaded into the second register set) and so are the
+    // offsets of set j-2.  The extra costs of the register-held records are
+    // stored at the start of the next step, after the prefetched registers
+    // have been taken over: a wait for a load also waits for every store
+    // issued after it, so stores at the end of a step would stall the next.
     LatMeta mc = lat_meta(p, ly, Tp, Tp);
-    LatRegs cur;
+    LatMeta mn{};
+    if (Tp > 0) mn = lat_meta(p, ly, Tp - 1, Tp);
+    LatRegs cur, nxt;
     lat_fetch(p, ly, mc, cur);
+    LatPend pd;
+    pd.e0 = pd.e1 = pd.x0 = pd.x1 = 0;
+    pd.j = -1;
+    pd.kept = 0;
+    int64_t a0 = so[Tp + 1], nA = 0;   // S_j+1
     for (int j = Tp; j >= 0; j--) {
-        const int64_t a0 = so[j + 1], nA = j < Tp ? so[j + 2] - a0 : 0;
+        // Everything the last step loaded has arrived (it was issued a step
+        // ago).  Waiting for it here, before this step issues its own loads,
+        // tells the compiler so: otherwise its first use of the current set
+        // would wait for the loads issued below as well.
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        if (j > 0) lat_fetch(p, ly, mn, nxt);
+        const int64_t mv2 = j > 1 ? lat_meta_issue(p, ly, j - 2, Tp) : 0;
+        lat_flush(p, ly, pd, kcnt);
         const bool g = mc.nB > kLatLds || nA > kLatLds;
         const int hB = hA ^ 1;
         uint32_t *eA = s_e + hA * kLatLds, *eB = s_e + hB * kLatLds;
         float *cA = s_c + hA * kLatLds, *cB = s_c + hB * kLatLds;
         const int64_t b0 = mc.b0, nB = mc.nB;
-        LatMeta mn{};
-        if (j > 0) mn = lat_meta(p, ly, j - 1, Tp);
         unsigned long long kept = 0;
         if (!g) {
             // ---- S_j and S_j+1 in LDS, records in registers ----
@@ -245,15 +335,18 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
 #pragma unroll
             for (int q = 0; q < kRE; q++) {
                 const int64_t r = mc.e0 + tid + q * kLatT;
+                pd.ee[q] = 0.0f;
                 if (r < mc.e1) {
                     const int4 x = cur.e[q];
                     const float d1 = __int_as_float(x.w) - cA[x.y - a0];
                     const float ex = d1 + okey_val(eA[x.y - a0]);
-                    p.ex_e[ly.le0 + r] = ex;
+                    pd.ee[q] = ex;
                     atomicMin(eB + (x.x - b0), okey(ex));
                     kept += ex <= lb;
                 }
             }
+            pd.e0 = mc.e0;
+            pd.e1 = mc.e1;
             for (int64_t r = mc.e0 + tid + kRE * kLatT; r < mc.e1; r += kLatT) {
                 const int4 x = p.lat_e[ly.le0 + r];
                 const float d1 = __int_as_float(x.w) - cA[x.y - a0];
@@ -262,9 +355,6 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                 atomicMin(eB + (x.x - b0), okey(ex));
                 kept += ex <= lb;
             }
-            // the next set's inputs, in flight during the epsilon rounds
-            const int4 x_cur[kRX] = {cur.x[0], cur.x[1]};
-            if (j > 0) lat_fetch(p, ly, mn, cur);
             lds_barrier();
             if (mc.x1 > mc.x0) {
                 float exr[kRX];
@@ -278,7 +368,7 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                         const int64_t r = mc.x0 + tid + q * kLatT;
                         exr[q] = 0.0f;
                         if (r < mc.x1) {
-                            const int4 x = x_cur[q];
+                            const int4 x = cur.x[q];
                             const float d1 = __int_as_float(x.w) - cB[x.y - b0];
                             const float ex = d1 + okey_val(eB[x.y - b0]);
                             exr[q] = ex;
@@ -308,10 +398,9 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                 }
                 // the last round changed nothing: its extra costs are final
 #pragma unroll
-                for (int q = 0; q < kRX; q++) {
-                    const int64_t r = mc.x0 + tid + q * kLatT;
-                    if (r < mc.x1) p.ex_x[ly.lx0 + r] = exr[q];
-                }
+                for (int q = 0; q < kRX; q++) pd.ex[q] = exr[q];
+                pd.x0 = mc.x0;
+                pd.x1 = mc.x1;
                 kept += kx;
             }
             // a following set processed in device memory reads S_j there
@@ -338,7 +427,6 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                 atomicMin(eg + x.x, okey(ex));
                 kept += ex <= lb;
             }
-            if (j > 0) lat_fetch(p, ly, mn, cur);
             __syncthreads();
             if (mc.x1 > mc.x0) {
                 unsigned long long kx = 0;
@@ -368,12 +456,17 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                 kept += kx;
             }
         }
-        kept = static_cast<unsigned long long>(wave_sum_ll(static_cast<long long>(kept)));
-        if (lane_id() == 0 && kept) atomicAdd(kcnt + j, kept);
+        pd.kept = kept;
+        pd.j = j;
+        a0 = b0;
+        nA = nB;
         hA = hB;
         a_lds = !g;
+        if (j > 0) cur = nxt;
         mc = mn;
+        mn = j > 1 ? lat_meta_take(mv2) : LatMeta{};
     }
+    lat_flush(p, ly, pd, kcnt);
     __syncthreads();
     // kept arcs per set -> output offsets (exclusive prefix over the sets)
     int64_t carry = 0;
