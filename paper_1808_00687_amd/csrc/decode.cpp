@@ -342,6 +342,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     p.profile = tm.on ? 1 : 0;
     p.rec_fill = test_env_int("WFSTDEC_TEST_RECORD_FILL", 1 << 30);
     p.rec_big_fill = test_env_int("WFSTDEC_TEST_RECORD_BIG_FILL", 1 << 30);
+    p.lat_lds = test_env_int("WFSTDEC_TEST_LATTICE_LDS", 1 << 30);
     p.capO = z.capO;
     WallTrace wt;
     UttLayout *d_lay = nullptr;

@@ -290,6 +290,8 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
     pd.j = -1;
     pd.kept = 0;
     int64_t a0 = so[Tp + 1], nA = 0;   // S_j+1
+    bool b_ready = false;              // S_j's extra costs are initialised in LDS
+    const int64_t lcap = min(kLatLds, p.lat_lds);
     for (int j = Tp; j >= 0; j--) {
         // Everything the last step loaded has arrived (it was issued a step
         // ago).  Waiting for it here, before this step issues its own loads,
@@ -299,7 +301,7 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
         if (j > 0) lat_fetch(p, ly, mn, nxt);
         const int64_t mv2 = j > 1 ? lat_meta_issue(p, ly, j - 2, Tp) : 0;
         lat_flush(p, ly, pd, kcnt);
-        const bool g = mc.nB > kLatLds || nA > kLatLds;
+        const bool g = mc.nB > lcap || nA > lcap;
         const int hB = hA ^ 1;
         uint32_t *eA = s_e + hA * kLatLds, *eB = s_e + hB * kLatLds;
         float *cA = s_c + hA * kLatLds, *cB = s_c + hB * kLatLds;
@@ -314,14 +316,19 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                 if (i < nB) cB[i] = tok_cost(cur.t[q]);
             }
             for (int64_t i = tid + kRC * kLatT; i < nB; i += kLatT) cB[i] = tok_cost(tok[b0 + i]);
-            if (j == Tp) {
-                for (int64_t i = tid; i < nB; i += kLatT) {
-                    const float c = tok_cost(tok[b0 + i]);
-                    const float f = use_final ? p.g.final_w[p.sv_state[ly.sv0 + b0 + i]] : 0.0f;
-                    eB[i] = okey((c + f) - B);
+            // The costs of S_j are first read after the next barrier; its
+            // extra costs were set to +inf by the previous step unless that
+            // step ran in device memory (or this is the last set).
+            if (!b_ready) {
+                if (j == Tp) {
+                    for (int64_t i = tid; i < nB; i += kLatT) {
+                        const float c = tok_cost(tok[b0 + i]);
+                        const float f = use_final ? p.g.final_w[p.sv_state[ly.sv0 + b0 + i]] : 0.0f;
+                        eB[i] = okey((c + f) - B);
+                    }
+                } else {
+                    for (int64_t i = tid; i < nB; i += kLatT) eB[i] = kinf;
                 }
-            } else {
-                for (int64_t i = tid; i < nB; i += kLatT) eB[i] = kinf;
             }
             if (!a_lds) {
                 // S_j+1 was processed in device memory: bring it into LDS
@@ -330,7 +337,7 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                     cA[i] = tok_cost(tok[a0 + i]);
                 }
             }
-            lds_barrier();
+            if (!b_ready || !a_lds) lds_barrier();
             // emitting arcs into S_j+1
 #pragma unroll
             for (int q = 0; q < kRE; q++) {
@@ -356,6 +363,11 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                 kept += ex <= lb;
             }
             lds_barrier();
+            // S_j+1 is no longer read: its half takes the extra costs of
+            // S_j-1, +inf until the next step's arcs lower them
+            const bool next_lds = j > 0 && mn.nB <= lcap && nB <= lcap;
+            if (next_lds)
+                for (int64_t i = tid; i < mn.nB; i += kLatT) eA[i] = kinf;
             if (mc.x1 > mc.x0) {
                 float exr[kRX];
                 unsigned long long kx = 0;
@@ -403,12 +415,17 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                 pd.x1 = mc.x1;
                 kept += kx;
             }
+            // the epsilon rounds' barriers publish that initialisation;
+            // without rounds one barrier does
+            if (next_lds && mc.x1 <= mc.x0) lds_barrier();
+            b_ready = next_lds;
             // a following set processed in device memory reads S_j there
-            const bool next_g = j > 0 && (mn.nB > kLatLds || nB > kLatLds);
+            const bool next_g = j > 0 && (mn.nB > lcap || nB > lcap);
             if (next_g)
                 for (int64_t i = tid; i < nB; i += kLatT) eg[b0 + i] = eB[i];
         } else {
             // ---- a set larger than the LDS arrays: device memory ----
+            b_ready = false;
             for (int64_t i = tid; i < nB; i += kLatT) {
                 uint32_t e0 = kinf;
                 if (j == Tp) {

@@ -128,6 +128,7 @@ struct Params {
     int32_t profile;          // count device clock ticks per search step
     int32_t rec_fill;         // survivors per set the record kernel's LDS table takes (<= its fill limit)
     int32_t rec_big_fill;     // the same for the large-set pass's LDS table
+    int32_t lat_lds;          // survivors per set the lattice backward pass keeps in LDS (<= its capacity)
     UttState *st;
     const UttLayout *lay;
     // survivors (per utterance regions)

@@ -162,6 +162,26 @@ def test_device_memory_table_path(dec, torch_mod, oracle_mod, cfg2, fill):
         parity.assert_same(ro, rg, lattice=True, tag="device table fill %d seed %d" % (fill, seed))
 
 
+@pytest.mark.parametrize("cap", [0, 25, 3900])
+def test_lattice_device_memory_path(dec, torch_mod, oracle_mod, cfg2, cap):
+    # the lattice backward pass keeps token sets of at most `cap` survivors in
+    # LDS and does larger ones in device memory: every set for cap = 0, a mix
+    # of both (and the hand-overs between them) for the others
+    wl, gh = cfg2
+    with _env(WFSTDEC_TEST_LATTICE_LDS=cap):
+        ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:80], gh=gh, beam=13.0,
+                      max_active=7000, lattice_beam=8.0)
+    parity.assert_same(ro, rg, lattice=True, tag="lattice lds %d" % cap)
+    for seed in range(6):
+        g = W.random_small_graph(950 + seed, 300, mean_deg=3.0, eps_frac=0.3, num_labels=5, weights="int",
+                                 final=seed % 2 == 0)
+        ll = W.random_small_loglikes(950 + seed, 25, 5, kind="int")
+        with _env(WFSTDEC_TEST_LATTICE_LDS=cap):
+            ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=9.0, max_active=[0, 11][seed % 2],
+                          lattice_beam=3.0)
+        parity.assert_same(ro, rg, lattice=True, tag="lattice lds %d seed %d" % (cap, seed))
+
+
 @pytest.mark.parametrize("fill,big", [(1, 1), (900, 1), (1, 1 << 20), (900, 1500)])
 def test_record_large_set_path(dec, torch_mod, oracle_mod, cfg2, fill, big):
     # token sets of more than `fill` survivors get their back-pointers and
