@@ -137,8 +137,12 @@ int wfst_decode(const wfst_graph *g, const float *loglikes, int32_t T, int32_t L
 
 /*
  * wfst_decode_batch -- decode n_utt independent utterances against one
- * graph in lock-step on one device (one launch per phase per frame for the
- * whole batch).
+ * graph on one device.  Each utterance runs in one workgroup for all of its
+ * frames.  Batches of 32 or more utterances are split into up to four
+ * groups of similar lengths; the groups' launches run on the library's own
+ * streams beside hip_stream (forked from and joined back into it with
+ * events), so the record and lattice passes of short utterances overlap the
+ * search of long ones.  Results do not depend on the grouping.
  *
  *   loglikes   [n_utt] host array of pointers, each [T[u] x L] float32
  *   T          [n_utt] host array of frame counts
@@ -211,7 +215,8 @@ typedef struct wfst_stats {
     /* with WFST_PROFILE (batch-wide, the same in every result of a batch):
        device time summed over launches, measured with HIP events */
     double search_ms;          /* token passing over all frames: expansion, epsilon
-                                  closure, pruning */
+                                  closure, pruning (launches of different groups
+                                  overlap, so the sum can exceed the wall time) */
     double record_ms;          /* back-pointers and raw lattice records of every frame */
     double final_ms;           /* final costs, backtrace, lattice pruning and output */
     int32_t search_launches;   /* launches of the search kernel */
@@ -230,6 +235,9 @@ typedef struct wfst_stats {
        side after the search) */
     double backtrace_ms;
     double lattice_prune_ms;
+    /* with WFST_PROFILE (batch-wide): from the start of the first search
+       launch to the end of the last one (the groups' launches overlap) */
+    double search_span_ms;
 } wfst_stats;
 
 int wfst_result_stats(const wfst_result *r, wfst_stats *stats);

@@ -286,12 +286,44 @@ struct WallTrace {
 
 enum { PH_SEARCH = 0, PH_RECORD = 1, PH_FINAL = 2, PH_COUNT = 3 };
 
+// Streams of the library's own (default priority, per device, created once)
+// on which groups of a batch run beside the caller's stream.
+constexpr int kAuxStreams = 3;
+
+hipStream_t aux_stream(int dev, int i)
+{
+    static std::mutex mu;
+    static hipStream_t tab[64][kAuxStreams] = {};
+    if (dev < 0 || dev >= 64 || i < 0 || i >= kAuxStreams) return nullptr;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!tab[dev][i] && hipStreamCreateWithFlags(&tab[dev][i], hipStreamNonBlocking) != hipSuccess)
+        tab[dev][i] = nullptr;
+    return tab[dev][i];
+}
+
 // One attempt at decoding the batch with the given buffer sizes.  Returns
 // WFST_OK, an error, or WFST_ECAPACITY when a buffer overflowed.
-int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, int L,
+int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T_in, int L,
               const wfst_decode_opts &o, float thr, hipStream_t s, const Sizes &z,
-              std::vector<wfst_result *> &out, double t_start)
+              std::vector<wfst_result *> &out_in, double t_start)
 {
+    // Utterances in order of length: a group of similar lengths runs its
+    // search, record and final passes on a stream of its own, so a group of
+    // short utterances does its record and lattice passes while the longer
+    // ones still search.  Results do not depend on the grouping.
+    std::vector<int> perm(static_cast<size_t>(U));
+    std::iota(perm.begin(), perm.end(), 0);
+    std::stable_sort(perm.begin(), perm.end(), [&](int a, int b) { return T_in[a] < T_in[b]; });
+    std::vector<const float *> ll_v(static_cast<size_t>(U));
+    std::vector<int32_t> T_v(static_cast<size_t>(U));
+    std::vector<wfst_result *> out(static_cast<size_t>(U));
+    for (int i = 0; i < U; i++) {
+        ll_v[i] = ll_in[perm[i]];
+        T_v[i] = T_in[perm[i]];
+        out[i] = out_in[perm[i]];
+    }
+    const float *const *ll = ll_v.data();
+    const int32_t *T = T_v.data();
     const int64_t N = G.d.n;
     const bool lattice = o.lattice_beam >= 0.0f;
     const int depth = G.eps_depth;
@@ -418,20 +450,68 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
     for (int u = 0; u < U; u++) Tmax = std::max(Tmax, T[u]);
     wt.mark("setup");
 
+    // groups of at least 16 utterances, at most one per stream
+    const int ng = std::max(1, std::min(1 + kAuxStreams, U / 16));
+    std::vector<hipStream_t> gs(static_cast<size_t>(ng), s);
+    std::vector<hipEvent_t> evs;
+    for (int g = 1; g < ng; g++) {
+        gs[g] = aux_stream(G.device, g - 1);
+        if (!gs[g]) chk(hipErrorOutOfMemory);
+    }
+    if (ng > 1 && e == hipSuccess) {
+        hipEvent_t fork = event_pool().get(G.device);
+        if (!fork) chk(hipErrorOutOfMemory);
+        else {
+            evs.push_back(fork);
+            chk(hipEventRecord(fork, s));
+            for (int g = 1; g < ng; g++) chk(hipStreamWaitEvent(gs[g], fork, 0));
+        }
+    }
+    for (int g = 0; g < ng && e == hipSuccess; g++) {
+        const int u0 = static_cast<int>(static_cast<int64_t>(U) * g / ng);
+        const int u1 = static_cast<int>(static_cast<int64_t>(U) * (g + 1) / ng);
+        Params pg = p;
+        pg.U = u1 - u0;
+        pg.st = p.st + u0;
+        pg.lay = p.lay + u0;
+        pg.gkeys = p.gkeys + u0 * p.capG;
+        pg.gvals = p.gvals + u0 * p.capG;
+        pg.gslots = p.gslots + u0 * p.capG;
+        pg.gspill = p.gspill + static_cast<int64_t>(u0) * 2 * p.capO;
+        int Tg = 0;
+        for (int u = u0; u < u1; u++) Tg = std::max(Tg, T[u]);
+        const hipStream_t q = gs[g];
+        tm.start(q);
+        chk(launch_search(pg, q));
+        tm.stop(PH_SEARCH, q);
+        tm.start(q);
+        chk(launch_record(pg, Tg, q));
+        tm.stop(PH_RECORD, q);
+        tm.start(q);
+        chk(launch_final(pg, q));
+        chk(launch_finish(pg, q));
+        tm.stop(PH_FINAL, q);
+        if (g > 0) {
+            hipEvent_t join = event_pool().get(G.device);
+            if (!join) {
+                chk(hipErrorOutOfMemory);
+                break;
+            }
+            evs.push_back(join);
+            chk(hipEventRecord(join, q));
+            chk(hipStreamWaitEvent(s, join, 0));
+        }
+    }
     tm.start(s);
-    chk(launch_search(p, s));
-    tm.stop(PH_SEARCH, s);
-    tm.start(s);
-    chk(launch_record(p, Tmax, s));
-    tm.stop(PH_RECORD, s);
-    tm.start(s);
-    chk(launch_final(p, s));
-    chk(launch_finish(p, s));
     chk(launch_pack_paths(p, s));
     tm.stop(PH_FINAL, s);
     wt.mark("enqueue frames");
     chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
     chk(hipStreamSynchronize(s));
+    // the groups' streams are done once s is (after an error too, before the
+    // workspace is given back)
+    for (int g = 1; g < ng; g++) chk(hipStreamSynchronize(gs[g]));
+    for (hipEvent_t x : evs) event_pool().put(G.device, x);
     wt.mark("wait search");
     if (wt.on) {
         int64_t gf = 0;
@@ -524,10 +604,20 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
 
     double ph[PH_COUNT] = {0, 0, 0};
     int nexp = 0;
+    // the search launches' span, on the clock of the first one's start event
+    hipEvent_t s_ref = nullptr;
+    double s_lo = 0.0, s_hi = 0.0;
     for (const auto &x : tm.spans) {
         float ms = 0.0f;
         if (hipEventElapsedTime(&ms, x.a, x.b) == hipSuccess) ph[x.kind] += ms;
-        if (x.kind == PH_SEARCH) nexp++;
+        if (x.kind != PH_SEARCH) continue;
+        nexp++;
+        if (!s_ref) s_ref = x.a;
+        float a = 0.0f, b = 0.0f;
+        if (hipEventElapsedTime(&a, s_ref, x.a) == hipSuccess && hipEventElapsedTime(&b, s_ref, x.b) == hipSuccess) {
+            s_lo = std::min(s_lo, static_cast<double>(a));
+            s_hi = std::max(s_hi, static_cast<double>(b));
+        }
     }
     const double wall = std::chrono::duration<double, std::milli>(
                             std::chrono::steady_clock::now().time_since_epoch()).count() - t_start;
@@ -543,6 +633,7 @@ int run_batch(const Graph &G, int U, const float *const *ll, const int32_t *T, i
         r->stats.record_ms = ph[PH_RECORD];
         r->stats.final_ms = ph[PH_FINAL];
         r->stats.search_launches = nexp;
+        r->stats.search_span_ms = s_hi - s_lo;
         if (tm.on) {
             int khz = 0;
             if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, G.device) == hipSuccess && khz > 0)

@@ -57,7 +57,7 @@ class _Stats(C.Structure):
                 ("lattice_kept", C.c_int64), ("decode_ms", C.c_double), ("search_ms", C.c_double),
                 ("record_ms", C.c_double), ("final_ms", C.c_double), ("search_launches", C.c_int32),
                 ("search_phase_ms", C.c_double * 7), ("backtrace_ms", C.c_double),
-                ("lattice_prune_ms", C.c_double)]
+                ("lattice_prune_ms", C.c_double), ("search_span_ms", C.c_double)]
 
 
 class _LatArc(C.Structure):

@@ -235,6 +235,23 @@ def test_batch_matches_single_and_oracle(dec, torch_mod, oracle_mod):
     gh.free()
 
 
+def test_batch_groups_match_oracle(dec, torch_mod, oracle_mod):
+    # 70 utterances of mixed lengths, in caller order unlike their length
+    # order: the batch runs as four length groups on separate streams, and
+    # every result must still be the oracle's for its own utterance
+    g = W.random_small_graph(931, 2000, mean_deg=3.0, eps_frac=0.2, num_labels=16)
+    gh = dec.load_graph(g)
+    rng = np.random.default_rng(931)
+    lens = [int(x) for x in rng.integers(0, 90, size=70)]
+    lls = [W.random_small_loglikes(940 + u, T, 16) for u, T in enumerate(lens)]
+    res = dec.wfst_decode_batch(gh, [to_dev(torch_mod, x) for x in lls], beam=9.0, max_active=120,
+                                lattice_beam=4.0, record_tokens=True)
+    for u, (x, r) in enumerate(zip(lls, res)):
+        ro = oracle_mod.decode(g, x, 9.0, 120, 4.0)
+        parity.assert_same(ro, r, lattice=True, tag="grouped batch utt %d (T=%d)" % (u, lens[u]))
+    gh.free()
+
+
 def test_lsd_small_ctc(dec, torch_mod, oracle_mod):
     g = W.random_small_graph(950, 5000, mean_deg=2.0, eps_frac=0.1, num_labels=30)
     n = g.num_states
