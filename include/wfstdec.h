@@ -95,7 +95,8 @@ int wfst_graph_get_info(const wfst_graph *g, wfst_graph_info *info);
 /* decode options */
 #define WFST_RECORD_TOKENS 1u  /* keep every token set for wfst_result_tokens */
 #define WFST_LOGLIKES_HOST 2u  /* loglikes pointers are host memory (copied to the device first) */
-#define WFST_PROFILE 4u        /* time the kernel phases with HIP events on the decode stream */
+#define WFST_PROFILE 4u        /* time the kernel phases with HIP events on the decode streams */
+#define WFST_PROFILE_STEPS 8u  /* also read the device clock per step inside the kernels (slower) */
 
 typedef struct wfst_decode_opts {
     float beam;               /* > 0 (may be +inf): keep tokens with cost <= best + beam */
@@ -107,7 +108,7 @@ typedef struct wfst_decode_opts {
                                  frame t is skipped when ll[t][blank_id] > log(blank_threshold);
                                  <= 0 or NaN: WFST_EINVAL */
     int32_t blank_id;         /* log-likelihood column of the blank unit, in [0, L) */
-    uint32_t flags;           /* WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST */
+    uint32_t flags;           /* WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST | WFST_PROFILE | WFST_PROFILE_STEPS */
     int64_t capacity_hint;    /* 0: automatic; else tokens per frame to reserve */
 } wfst_decode_opts;
 
@@ -220,7 +221,7 @@ typedef struct wfst_stats {
     double record_ms;          /* back-pointers and raw lattice records of every frame */
     double final_ms;           /* final costs, backtrace, lattice pruning and output */
     int32_t search_launches;   /* launches of the search kernel */
-    /* with WFST_PROFILE: this utterance's share of the search, from the
+    /* with WFST_PROFILE_STEPS: this utterance's share of the search, from the
        device clock of its workgroup, per step of a frame summed over the
        frames: [0] emitting expansion and the epsilon closure from the wave
        queues, [1] closure rounds over spilled epsilon items, [2] beam and
@@ -230,7 +231,7 @@ typedef struct wfst_stats {
        barrier); [6] frames abandoned for the device-memory table (their
        steps are not in [0]-[3]) */
     double search_phase_ms[7];
-    /* with WFST_PROFILE: this utterance's backtrace and lattice-beam pruning,
+    /* with WFST_PROFILE_STEPS: this utterance's backtrace and lattice-beam pruning,
        from the device clock of the workgroups doing them (they run side by
        side after the search) */
     double backtrace_ms;

@@ -371,7 +371,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     p.blank_thr = thr;
     p.lds_fill = test_env_int("WFSTDEC_TEST_LDS_FILL", 1 << 30);
     p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1 << 30);
-    p.profile = tm.on ? 1 : 0;
+    p.profile = (o.flags & WFST_PROFILE_STEPS) ? 1 : 0;
     p.rec_fill = test_env_int("WFSTDEC_TEST_RECORD_FILL", 1 << 30);
     p.rec_big_fill = test_env_int("WFSTDEC_TEST_RECORD_BIG_FILL", 1 << 30);
     p.lat_lds = test_env_int("WFSTDEC_TEST_LATTICE_LDS", 1 << 30);
@@ -634,7 +634,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         r->stats.final_ms = ph[PH_FINAL];
         r->stats.search_launches = nexp;
         r->stats.search_span_ms = s_hi - s_lo;
-        if (tm.on) {
+        if (p.profile) {
             int khz = 0;
             if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, G.device) == hipSuccess && khz > 0)
             {

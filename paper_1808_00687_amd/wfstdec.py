@@ -31,6 +31,7 @@ WFST_EDEVICE = -5
 WFST_RECORD_TOKENS = 1
 WFST_LOGLIKES_HOST = 2
 WFST_PROFILE = 4
+WFST_PROFILE_STEPS = 8
 
 
 class WfstError(RuntimeError):
@@ -320,8 +321,8 @@ def _stream_handle(stream):
 def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_active: int = 0,
                       lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
                       record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
-                      stream=None) -> List[WfstResult]:
-    """Decode utterances in lock-step (wfst_decode_batch).  ``loglikes`` are
+                      stream=None, profile_steps: bool = False) -> List[WfstResult]:
+    """Decode a batch of utterances (wfst_decode_batch).  ``loglikes`` are
     [T_u x L] float32 tensors on the graph's device (or numpy arrays)."""
     keep: list = []
     ptrs, Ts, L, host = [], [], None, None
@@ -335,7 +336,7 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
         Ts.append(shape[0])
     n = len(ptrs)
     flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
-        (WFST_PROFILE if profile else 0)
+        (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0)
     o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint)
     parr = (C.c_void_p * n)(*ptrs)
     tarr = np.array(Ts, np.int32)
@@ -356,13 +357,13 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
 def wfst_decode(graph: WfstGraph, loglikes, beam: float, max_active: int = 0,
                 lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
                 record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
-                stream=None) -> WfstResult:
+                stream=None, profile_steps: bool = False) -> WfstResult:
     """Decode one utterance (wfst_decode).  Returns the result also when the
     status is WFST_ENOPATH; other errors raise WfstError."""
     keep: list = []
     ptr, shape, host = _ll_ptr(loglikes, keep)
     flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
-        (WFST_PROFILE if profile else 0)
+        (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0)
     o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint)
     out = C.c_void_p()
     rc = _lib.wfst_decode(graph.handle, ptr, shape[0], shape[1], C.byref(o), _stream_handle(stream),
