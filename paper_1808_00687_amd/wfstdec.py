@@ -220,7 +220,30 @@ def _arr(ptr, n, dt):
     return np.ctypeslib.as_array(ptr, shape=(n,)).astype(dt, copy=True)
 
 
-def _collect(h, lattice: bool, tokens: bool) -> WfstResult:
+def _lattice_views(outs) -> list:
+    """Each result's lattice as an [n x 4] int32 view of one host copy: the
+    lattices of a batch lie in one host buffer the results share, copied here
+    once instead of once per result."""
+    spans = []
+    for h in outs:
+        ln = C.c_int64()
+        la = C.POINTER(_LatArc)()
+        _check(_lib.wfst_result_lattice(h, C.byref(ln), C.byref(la)), "wfst_result_lattice")
+        spans.append((C.cast(la, C.c_void_p).value or 0, ln.value))
+    live = [(p, m) for p, m in spans if m > 0 and p]
+    if not live:
+        return [np.zeros((0, 4), np.int32)] * len(spans)
+    base = min(p for p, _ in live)
+    end = max(p + 16 * m for p, m in live)
+    big = np.ctypeslib.as_array(C.cast(C.c_void_p(base), C.POINTER(C.c_int32)), shape=((end - base) // 16, 4)).copy()
+    views = []
+    for p, m in spans:
+        i = (p - base) // 16 if m > 0 and p else 0
+        views.append(big[i:i + m] if m > 0 and p else np.zeros((0, 4), np.int32))
+    return views
+
+
+def _collect(h, lattice: bool, tokens: bool, lat=None) -> WfstResult:
     st = _lib.wfst_result_status(h)
     r = WfstResult(status=st)
     nf, nd = C.c_int32(), C.c_int32()
@@ -242,17 +265,13 @@ def _collect(h, lattice: bool, tokens: bool) -> WfstResult:
     r.path_arcs = _arr(pa, n.value, np.int32)
     r.path_frames = _arr(pf, n.value, np.int32)
     if lattice:
-        ln = C.c_int64()
-        la = C.POINTER(_LatArc)()
-        _check(_lib.wfst_result_lattice(h, C.byref(ln), C.byref(la)), "wfst_result_lattice")
-        if ln.value:
-            raw = np.ctypeslib.as_array(C.cast(la, C.POINTER(C.c_int32)), shape=(ln.value, 4)).copy()
-        else:
-            raw = np.zeros((0, 4), np.int32)
-        r.lat_frame = raw[:, 0].copy()
-        r.lat_arc = raw[:, 1].copy()
-        r.lat_cost = raw[:, 2].copy().view(np.float32)
-        r.lat_extra = raw[:, 3].copy().view(np.float32)
+        if lat is None:
+            lat = _lattice_views([h])[0]
+        fl = lat.view(np.float32)
+        r.lat_frame = lat[:, 0]
+        r.lat_arc = lat[:, 1]
+        r.lat_cost = fl[:, 2]
+        r.lat_extra = fl[:, 3]
     if tokens:
         offs = [0]
         states, costs, arcs = [], [], []
@@ -346,8 +365,9 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
     _check(rc, "wfst_decode_batch")
     res = []
     try:
-        for h in outs:
-            res.append(_collect(h, lattice_beam >= 0, record_tokens))
+        lats = _lattice_views(outs) if lattice_beam >= 0 else [None] * n
+        for h, lat in zip(outs, lats):
+            res.append(_collect(h, lattice_beam >= 0, record_tokens, lat))
     finally:
         for h in outs:
             _lib.wfst_result_free(h)
