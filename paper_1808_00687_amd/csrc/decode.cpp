@@ -450,7 +450,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     for (int u = 0; u < U; u++) Tmax = std::max(Tmax, T[u]);
     wt.mark("setup");
 
-    // groups of at least 16 utterances, at most one per stream
+    // one group per 16 utterances, at most one per stream
     const int ng = std::max(1, std::min(1 + kAuxStreams, U / 16));
     std::vector<hipStream_t> gs(static_cast<size_t>(ng), s);
     std::vector<hipEvent_t> evs;
@@ -467,9 +467,18 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
             for (int g = 1; g < ng; g++) chk(hipStreamWaitEvent(gs[g], fork, 0));
         }
     }
+    // Group bounds: equal groups, except that with four groups the last
+    // (longest) one is half as large and the first takes the rest: after the
+    // last search ends only that group's record and lattice passes remain.
+    std::vector<int> gb(static_cast<size_t>(ng) + 1);
+    for (int g = 0; g <= ng; g++) gb[g] = static_cast<int>(static_cast<int64_t>(U) * g / ng);
+    if (ng == 4) {
+        static const int kEighths[5] = {0, 3, 5, 7, 8};
+        for (int g = 0; g <= ng; g++) gb[g] = static_cast<int>(static_cast<int64_t>(U) * kEighths[g] / 8);
+    }
     for (int g = 0; g < ng && e == hipSuccess; g++) {
-        const int u0 = static_cast<int>(static_cast<int64_t>(U) * g / ng);
-        const int u1 = static_cast<int>(static_cast<int64_t>(U) * (g + 1) / ng);
+        const int u0 = gb[g];
+        const int u1 = gb[g + 1];
         Params pg = p;
         pg.U = u1 - u0;
         pg.st = p.st + u0;
