@@ -123,6 +123,11 @@ def _load():
             lib.oracle_decode.argtypes = [C.c_int32, C.c_int64, i32p, i32p, i32p, i32p, f32p,
                                           C.c_int32, f32p, f32p, C.c_int32, C.c_int32,
                                           C.c_float, C.c_int32, C.c_float, C.c_float, C.c_int32]
+            lib.oracle_decode_ext.restype = C.POINTER(_Result)
+            lib.oracle_decode_ext.argtypes = [C.c_int32, C.c_int64, i32p, i32p, i32p, i32p, f32p,
+                                              C.c_int32, f32p, f32p, C.c_int32, C.c_int32,
+                                              C.c_float, C.c_int32, C.c_float, C.c_float, i32p,
+                                              C.c_int32, C.c_int32]
             lib.oracle_validate_graph.restype = C.c_int
             lib.oracle_validate_graph.argtypes = [C.c_int32, C.c_int64, i32p, i32p, i32p, i32p,
                                                   f32p, C.c_int32, f32p]
@@ -165,19 +170,23 @@ def validate_graph(g) -> int:
 
 def decode(g, loglikes: np.ndarray, beam: float, max_active: int = 0,
            lattice_beam: float = -1.0, blank_threshold: float = 2.0,
-           blank_id: int = 0) -> OracleResult:
+           blank_id: int = 0, blank_ids=None, frame_stride: int = 1) -> OracleResult:
     """Decode one utterance on the CPU.  ``g`` has the fields of
-    ``workloads.Graph``; ``loglikes`` is float32 [T x L]."""
+    ``workloads.Graph``; ``loglikes`` is float32 [T x L].  ``blank_ids``
+    (a set of blank-like units) replaces ``blank_id`` when given;
+    ``frame_stride`` decodes every frame_stride-th frame only."""
     lib = _load()
     src, dst, il, ol, w, fw = _graph_arrays(g)
     ll = np.ascontiguousarray(loglikes, dtype=np.float32)
     if ll.ndim != 2:
         raise ValueError("loglikes must be [T x L]")
     T, L = ll.shape
-    rp = lib.oracle_decode(g.num_states, src.shape[0], _p(src, C.c_int32), _p(dst, C.c_int32),
-                           _p(il, C.c_int32), _p(ol, C.c_int32), _p(w, C.c_float), g.start,
-                           _p(fw, C.c_float), _p(ll, C.c_float), T, L, beam, max_active,
-                           lattice_beam, blank_threshold, blank_id)
+    ids = np.ascontiguousarray([blank_id] if blank_ids is None else blank_ids, dtype=np.int32)
+    rp = lib.oracle_decode_ext(g.num_states, src.shape[0], _p(src, C.c_int32), _p(dst, C.c_int32),
+                               _p(il, C.c_int32), _p(ol, C.c_int32), _p(w, C.c_float), g.start,
+                               _p(fw, C.c_float), _p(ll, C.c_float), T, L, beam, max_active,
+                               lattice_beam, blank_threshold, _p(ids, C.c_int32), ids.shape[0],
+                               frame_stride)
     if not rp:
         raise MemoryError("oracle_decode returned NULL")
     try:

@@ -24,7 +24,10 @@
  *  - Label-synchronous decoding (Sec. 2, Alg. 1): a frame is blank when the
  *    blank posterior exceeds the threshold (the set U); blank frames leave
  *    the token set untouched (Eq. 2 drops their factors), so the search runs
- *    on the T - |U| remaining frames only (Eq. 3).
+ *    on the T - |U| remaining frames only (Eq. 3).  For the HMM topologies
+ *    the paper names (a blank-like state per phone, Sec. 2) the blank is a
+ *    set of units and a frame is blank when one of them exceeds the
+ *    threshold; a lower frame rate decodes every frame_stride-th frame.
  *  - finalTransition then backtrace (Alg. 1): add final costs, take the best
  *    state, follow back-pointers.
  *  - Exact lattices (Sec. 1, Sec. 3): arcs between surviving tokens whose
@@ -306,13 +309,26 @@ oracle_result *oracle_decode(int32_t n, int64_t e, const int32_t *src, const int
                              int32_t T, int32_t L, float beam, int32_t max_active,
                              float lattice_beam, float blank_threshold, int32_t blank_id)
 {
+    return oracle_decode_ext(n, e, src, dst, ilabel, olabel, weight, start, final_weight, ll, T, L, beam,
+                             max_active, lattice_beam, blank_threshold, &blank_id, 1, 1);
+}
+
+oracle_result *oracle_decode_ext(int32_t n, int64_t e, const int32_t *src, const int32_t *dst,
+                                 const int32_t *ilabel, const int32_t *olabel, const float *weight,
+                                 int32_t start, const float *final_weight, const float *ll,
+                                 int32_t T, int32_t L, float beam, int32_t max_active,
+                                 float lattice_beam, float blank_threshold,
+                                 const int32_t *blank_ids, int32_t nb, int32_t stride)
+{
     oracle_result *r = calloc(1, sizeof(oracle_result));
     if (!r) return NULL;
     r->status = oracle_validate_graph(n, e, src, dst, ilabel, olabel, weight, start, final_weight);
     if (r->status != ORACLE_OK) return r;
     int32_t max_il = 0;
     for (int64_t a = 0; a < e; a++) if (ilabel[a] > max_il) max_il = ilabel[a];
-    if (T < 0 || L < 1 || max_il > L || blank_id < 0 || blank_id >= L || !(beam > 0.0f) ||
+    int bad_ids = nb < 1 || !blank_ids;
+    for (int32_t i = 0; !bad_ids && i < nb; i++) bad_ids = blank_ids[i] < 0 || blank_ids[i] >= L;
+    if (T < 0 || L < 1 || max_il > L || bad_ids || stride < 1 || !(beam > 0.0f) ||
         isnan(lattice_beam) || !(blank_threshold > 0.0f) || (T > 0 && !ll)) {
         r->status = ORACLE_EINVAL;
         return r;
@@ -345,11 +361,17 @@ oracle_result *oracle_decode(int32_t n, int64_t e, const int32_t *src, const int
 
     /* isBlankFrame (Sec. 2, Alg. 1): U = {u : y_blank^u > threshold}, compared
      * in the log domain against one float32 threshold; a threshold above 1
-     * makes no frame blank (frame-synchronous decoding). */
+     * makes no frame blank (frame-synchronous decoding).  With several
+     * blank-like units a frame is blank when any of them passes; with a
+     * frame stride only every stride-th frame is a candidate. */
     float thr = blank_threshold > 1.0f ? INFINITY : (float)log((double)blank_threshold);
     int32_t Tp = 0;
-    for (int32_t t = 0; t < T; t++)
-        if (!(ll[(int64_t)t * L + blank_id] > thr)) kept[Tp++] = t;
+    for (int32_t t = 0; t < T; t += stride) {
+        int blank = 0;
+        for (int32_t i = 0; i < nb; i++)
+            if (ll[(int64_t)t * L + blank_ids[i]] > thr) blank = 1;
+        if (!blank) kept[Tp++] = t;
+    }
 
     /* token set 0: the start token and its epsilon closure */
     touch(&w, start, make_tok(0.0f, -1));

@@ -83,6 +83,20 @@ oracle_result *oracle_decode(int32_t num_states, int64_t num_arcs, const int32_t
                              int32_t max_active, float lattice_beam, float blank_threshold,
                              int32_t blank_id);
 
+/* The same with the label-synchronous test over a set of blank-like units
+ * (HMM topologies whose blank-like state is one unit per phone, Sec. 2):
+ * frame t is blank when some unit of blank_ids[0..num_blank_ids) has a
+ * log-likelihood above log(blank_threshold).  Only frames t with
+ * t % frame_stride == 0 are candidates for decoding at all (a lower frame
+ * rate; frame_stride >= 1).  oracle_decode is this call with the single unit
+ * blank_id and stride 1. */
+oracle_result *oracle_decode_ext(int32_t num_states, int64_t num_arcs, const int32_t *src,
+                                 const int32_t *dst, const int32_t *ilabel, const int32_t *olabel,
+                                 const float *weight, int32_t start, const float *final_weight,
+                                 const float *loglikes, int32_t T, int32_t L, float beam,
+                                 int32_t max_active, float lattice_beam, float blank_threshold,
+                                 const int32_t *blank_ids, int32_t num_blank_ids, int32_t frame_stride);
+
 void oracle_free(oracle_result *r);
 
 #ifdef __cplusplus

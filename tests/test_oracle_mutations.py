@@ -26,8 +26,11 @@ MUTATIONS = {
     "closure_no_repush": ("if (touch(w, d, make_tok(cand, a)) && !w->inq[d]) {", "if (touch(w, d, make_tok(cand, a)) && 0) {"),
     "eps_weight_dropped": ("float cand = c + g->w[a];", "float cand = c;"),
     "final_weight_ignored": ("float f = final_weight ? final_weight[S[i].state] : 0.0f;", "float f = 0.0f;"),
-    "blank_test_inverted": ("if (!(ll[(int64_t)t * L + blank_id] > thr)) kept[Tp++] = t;",
-                            "if (!(ll[(int64_t)t * L + blank_id] < thr)) kept[Tp++] = t;"),
+    "blank_test_inverted": ("if (ll[(int64_t)t * L + blank_ids[i]] > thr) blank = 1;",
+                            "if (ll[(int64_t)t * L + blank_ids[i]] < thr) blank = 1;"),
+    "blank_set_first_unit_only": ("for (int32_t i = 0; i < nb; i++)\n            if (ll",
+                                  "for (int32_t i = 0; i < 1; i++)\n            if (ll"),
+    "frame_stride_ignored": ("for (int32_t t = 0; t < T; t += stride) {", "for (int32_t t = 0; t < T; t++) {"),
     "lattice_extra_sign": ("R[k].ex = d1 + e_node[R[k].gd];", "R[k].ex = d1 - e_node[R[k].gd];"),
     "lattice_prefix_swapped": ("float d1 = R[k].p - tok_cost(S[R[k].gd].tok);\n                    R[k].ex",
                                "float d1 = tok_cost(S[R[k].gd].tok) - R[k].p;\n                    R[k].ex"),

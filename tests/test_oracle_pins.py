@@ -398,6 +398,105 @@ def test_lsd_work_scales_with_kept_frames(oracle_mod):
 
 
 # ----------------------------------------------------------------------------
+# label-synchronous decoding over a set of blank-like units, lower frame rate
+# ----------------------------------------------------------------------------
+
+def _hmm_small(seed, k):
+    """A graph whose every state has a self-loop on one of k blank-like units
+    (columns 0..k-1, as one per phone of an HMM topology); its other emitting
+    arcs read columns k..k+5."""
+    g = W.random_small_graph(seed, 400, mean_deg=2.0, eps_frac=0.1, num_labels=6)
+    n = g.num_states
+    rng = np.random.default_rng(seed)
+    src = np.concatenate([np.arange(n), g.src]).astype(np.int32)
+    dst = np.concatenate([np.arange(n), g.dst]).astype(np.int32)
+    il = np.concatenate([rng.integers(1, k + 1, size=n), np.where(g.ilabel == 0, 0, g.ilabel + k)]).astype(np.int32)
+    w = np.concatenate([np.full(n, 0.5), g.weight]).astype(np.float32)
+    order = np.argsort(src, kind="stable")
+    return W.Graph(n, src[order], dst[order], il[order], np.zeros_like(src), w[order])
+
+
+def _hmm_loglikes(seed, t, k):
+    """log-softmax rows over k + 6 units; on about 70% of the frames one
+    blank-like unit, drawn at random, is raised by 7."""
+    rng = np.random.default_rng(seed)
+    z = rng.normal(0.0, 1.0, size=(t, k + 6))
+    hot = rng.random(t) < 0.7
+    z[np.flatnonzero(hot), rng.integers(0, k, size=t)[hot]] += 7.0
+    z = z - z.max(axis=1, keepdims=True)
+    return (z - np.log(np.exp(z).sum(axis=1, keepdims=True))).astype(np.float32)
+
+
+def _assert_lsd_is_fsd_on(lsd, fsd, kept):
+    assert lsd.status == 0 and fsd.status == 0
+    np.testing.assert_array_equal(lsd.kept, kept)
+    for j in range(kept.size + 1):
+        for x, y in zip(lsd.token_set(j), fsd.token_set(j)):
+            np.testing.assert_array_equal(x, y)
+    assert _bits(lsd.cost) == _bits(fsd.cost)
+    np.testing.assert_array_equal(lsd.path_arcs, fsd.path_arcs)
+    remap = np.where(fsd.path_frames >= 0, kept[np.maximum(fsd.path_frames, 0)], -1)
+    np.testing.assert_array_equal(lsd.path_frames, remap)
+    np.testing.assert_array_equal(lsd.lat_arc, fsd.lat_arc)
+    np.testing.assert_array_equal(lsd.lat_frame, fsd.lat_frame)
+    np.testing.assert_array_equal(_bits(lsd.lat_extra), _bits(fsd.lat_extra))
+
+
+def test_blank_set_of_one_unit_is_the_single_blank(oracle_mod):
+    g = _ctc_small(4)
+    ll = W.random_small_loglikes(4, 70, 6, blank_boost=6.0)
+    kept = np.flatnonzero(~(ll[:, 0] > np.float32(math.log(0.9))))
+    fsd = oracle_mod.decode(g, np.ascontiguousarray(ll[kept]), 8.0, 50, 4.0, blank_threshold=2.0)
+    a = oracle_mod.decode(g, ll, 8.0, 50, 4.0, blank_threshold=0.9, blank_id=0)
+    b = oracle_mod.decode(g, ll, 8.0, 50, 4.0, blank_threshold=0.9, blank_ids=[0])
+    _assert_lsd_is_fsd_on(a, fsd, kept)
+    _assert_lsd_is_fsd_on(b, fsd, kept)
+    assert 0 < kept.size < 70
+
+
+@pytest.mark.parametrize("thr", [0.5, 0.95])
+def test_blank_set_equals_fsd_on_kept_frames(oracle_mod, thr):
+    k = 3
+    g = _hmm_small(5, k)
+    ll = _hmm_loglikes(5, 90, k)
+    # a frame is blank when any blank-like unit passes the threshold
+    kept = np.flatnonzero(~(ll[:, :k] > np.float32(math.log(thr))).any(axis=1))
+    lsd = oracle_mod.decode(g, ll, 8.0, 60, 4.0, blank_threshold=thr, blank_ids=[0, 1, 2])
+    fsd = oracle_mod.decode(g, np.ascontiguousarray(ll[kept]), 8.0, 60, 4.0, blank_threshold=2.0)
+    assert 0 < kept.size < 90
+    _assert_lsd_is_fsd_on(lsd, fsd, kept)
+    # the set's order and repeats do not matter
+    again = oracle_mod.decode(g, ll, 8.0, 60, 4.0, blank_threshold=thr, blank_ids=[2, 0, 2, 1])
+    _assert_lsd_is_fsd_on(again, fsd, kept)
+
+
+@pytest.mark.parametrize("stride", [1, 2, 3])
+def test_frame_stride_equals_fsd_on_subsampled_frames(oracle_mod, stride):
+    k = 3
+    g = _hmm_small(6, k)
+    ll = _hmm_loglikes(6, 61, k)
+    kept = np.arange(0, 61, stride)
+    lsd = oracle_mod.decode(g, ll, 8.0, 60, 4.0, blank_threshold=2.0, frame_stride=stride)
+    fsd = oracle_mod.decode(g, np.ascontiguousarray(ll[kept]), 8.0, 60, 4.0, blank_threshold=2.0)
+    _assert_lsd_is_fsd_on(lsd, fsd, kept)
+    # with blank-like units too: the stride's frames, then the blank test
+    thr = 0.9
+    both = kept[~(ll[kept, :k] > np.float32(math.log(thr))).any(axis=1)]
+    lsd = oracle_mod.decode(g, ll, 8.0, 60, 4.0, blank_threshold=thr, blank_ids=[0, 1, 2], frame_stride=stride)
+    fsd = oracle_mod.decode(g, np.ascontiguousarray(ll[both]), 8.0, 60, 4.0, blank_threshold=2.0)
+    _assert_lsd_is_fsd_on(lsd, fsd, both)
+
+
+def test_blank_set_and_stride_validation(oracle_mod):
+    g = _hmm_small(7, 2)
+    ll = _hmm_loglikes(7, 10, 2)
+    assert oracle_mod.decode(g, ll, 8.0, blank_threshold=0.9, blank_ids=[]).status == -1
+    assert oracle_mod.decode(g, ll, 8.0, blank_threshold=0.9, blank_ids=[0, 8]).status == -1
+    assert oracle_mod.decode(g, ll, 8.0, blank_threshold=0.9, blank_ids=[-1]).status == -1
+    assert oracle_mod.decode(g, ll, 8.0, frame_stride=0).status == -1
+
+
+# ----------------------------------------------------------------------------
 # lattices
 # ----------------------------------------------------------------------------
 
