@@ -44,9 +44,12 @@ PMC_CMD = ("timeout -s KILL 180 rocprofv3 --pmc {counter} --output-format csv -d
            "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile --copy-calibration-mib %d"
            % CALIBRATION_MIB)
 
+# name: (config, label-synchronous, frame stride); cfg6 is the HMM-topology
+# stand-in (a set of blank-like units), not one of the five listed configs
 WORKLOADS = {
-    "cfg1": (1, True), "cfg2": (2, True), "cfg3": (3, True), "cfg4": (4, True),
-    "cfg5": (5, True), "cfg5fsd": (5, False),
+    "cfg1": (1, True, 1), "cfg2": (2, True, 1), "cfg3": (3, True, 1), "cfg4": (4, True, 1),
+    "cfg5": (5, True, 1), "cfg5fsd": (5, False, 1),
+    "cfg6": (6, True, 1), "cfg6fsd": (6, False, 1), "cfg6stride3": (6, True, 3),
 }
 
 
@@ -162,7 +165,8 @@ def cpu_baseline(wl, max_seconds: float):
     t0 = time.time()
     with ThreadPoolExecutor(max_workers=cores) as ex:
         res = list(ex.map(lambda u: oracle.decode(g, wl.loglikes[u], o.beam, o.max_active, o.lattice_beam,
-                                                  o.blank_threshold, o.blank_id), sample))
+                                                  o.blank_threshold, o.blank_id, o.blank_ids,
+                                                  o.frame_stride), sample))
     wall = time.time() - t0
     frames = sum(r.num_decoded for r in res)
     busy = sum(r.seconds for r in res)
@@ -222,9 +226,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU", file=sys.stderr)
         sys.exit(1)
-    cfg, lsd = WORKLOADS[args.workload]
+    cfg, lsd, stride = WORKLOADS[args.workload]
     t = time.time()
-    wl = workloads.workload(cfg, lsd=lsd)
+    wl = workloads.workload(cfg, lsd=lsd, frame_stride=stride)
     log("workload %s generated in %.1fs (%d states, %d arcs, %d utterances)" % (
         wl.name, time.time() - t, wl.graph.num_states, wl.graph.num_arcs, len(wl.loglikes)))
     if args.copy_calibration_mib:
@@ -240,7 +244,8 @@ def main():
 
     def step(profile, steps=False):
         return wfstdec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, o.blank_threshold,
-                                         o.blank_id, profile=profile, stream=stream, profile_steps=steps)
+                                         o.blank_id, profile=profile, stream=stream, profile_steps=steps,
+                                         blank_ids=o.blank_ids, frame_stride=o.frame_stride)
 
     for i in range(args.warmup):
         res = step(False)
@@ -288,6 +293,8 @@ def main():
             "max_active": o.max_active,
             "lattice_beam": o.lattice_beam,
             "blank_threshold": o.blank_threshold,
+            "blank_units": len(o.blank_ids) if o.blank_ids else 1,
+            "frame_stride": o.frame_stride,
             "parallelism": "utterance batch of %d on 1 GPU" % len(wl.loglikes),
         },
         "rtf": sec / (frames * FRAME_SHIFT_S),

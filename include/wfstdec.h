@@ -10,7 +10,9 @@
  *     ("token recombination", Sec. 3 and Fig. 2);
  *   - label-synchronous decoding (Sec. 2, Eq. 2, Alg. 1): frames whose blank
  *     posterior exceeds a threshold (the set U) are skipped, so the search
- *     runs on T - |U| frames (Eq. 3);
+ *     runs on T - |U| frames (Eq. 3); for the HMM topologies of Sec. 2 the
+ *     blank is a set of blank-like units, and a lower frame rate decodes
+ *     every k-th frame;
  *   - finalTransition then backtrace (Alg. 1);
  *   - exact lattice generation and lattice pruning (Sec. 1, Sec. 3).
  *
@@ -110,9 +112,19 @@ typedef struct wfst_decode_opts {
     int32_t blank_id;         /* log-likelihood column of the blank unit, in [0, L) */
     uint32_t flags;           /* WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST | WFST_PROFILE | WFST_PROFILE_STEPS */
     int64_t capacity_hint;    /* 0: automatic; else tokens per frame to reserve */
+    /* HMM topologies whose blank-like state is one unit per phone (Sec. 2):
+       with num_blank_ids > 0, blank_ids[0..num_blank_ids) (host memory,
+       columns in [0, L), order and repeats irrelevant) replace blank_id, and a
+       frame is blank when any of them passes the threshold */
+    const int32_t *blank_ids;
+    int32_t num_blank_ids;    /* 0: the single unit blank_id; < 0: WFST_EINVAL */
+    int32_t frame_stride;     /* decode only frames t with t % frame_stride == 0 (a lower frame
+                                 rate; the blank test then applies to those); 0 counts as 1;
+                                 < 0: WFST_EINVAL */
 } wfst_decode_opts;
 
-/* Fill opts with defaults: beam 16, max_active 0, no lattice, FSD, blank 0. */
+/* Fill opts with defaults: beam 16, max_active 0, no lattice, FSD, blank 0,
+   no blank-unit set, frame stride 1. */
 void wfst_default_opts(wfst_decode_opts *opts);
 
 /*

@@ -367,7 +367,12 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     p.max_active = o.max_active;
     p.lattice_beam = o.lattice_beam;
     p.lattice = lattice ? 1 : 0;
-    p.blank_id = o.blank_id;
+    // the blank-like units: the set when given, else the single blank unit
+    std::vector<int32_t> blank_h;
+    if (o.num_blank_ids > 0) blank_h.assign(o.blank_ids, o.blank_ids + o.num_blank_ids);
+    else blank_h.push_back(o.blank_id);
+    p.n_blank = static_cast<int32_t>(blank_h.size());
+    p.frame_stride = std::max(1, o.frame_stride);
     p.blank_thr = thr;
     p.lds_fill = test_env_int("WFSTDEC_TEST_LDS_FILL", 1 << 30);
     p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1 << 30);
@@ -400,6 +405,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         p.ex_e = lattice ? a.get<float>(le) : nullptr;
         p.ex_x = lattice ? a.get<float>(lx) : nullptr;
         fo_all = a.get<int64_t>(7 * fo);
+        p.blank_ids = a.get<int32_t>(p.n_blank);
         p.cut_arr = a.get<uint32_t>(fo);
         p.kept = a.get<int32_t>(kp);
         p.path_arc = a.get<int32_t>(pa);
@@ -444,6 +450,8 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
     chk(hipMemsetAsync(fo_all, 0, 7 * fo * sizeof(int64_t), s));
+    chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), blank_h.data(), blank_h.size() * sizeof(int32_t),
+                       hipMemcpyHostToDevice, s));
     chk(launch_classify(p, s));
     // decoded frames are at most the frames: size the per-frame launches by T
     int Tmax = 0;
@@ -702,6 +710,11 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
     if (!(o.blank_threshold > 0.0f)) return fail(WFST_EINVAL, "decode: blank_threshold must be > 0");
     if (L < 1 || L < G.max_ilabel) return fail(WFST_EINVAL, "decode: L smaller than the largest ilabel");
     if (o.blank_id < 0 || o.blank_id >= L) return fail(WFST_EINVAL, "decode: blank_id out of range");
+    if (o.num_blank_ids < 0 || (o.num_blank_ids > 0 && !o.blank_ids))
+        return fail(WFST_EINVAL, "decode: bad blank-unit set");
+    for (int i = 0; i < o.num_blank_ids; i++)
+        if (o.blank_ids[i] < 0 || o.blank_ids[i] >= L) return fail(WFST_EINVAL, "decode: blank unit out of range");
+    if (o.frame_stride < 0) return fail(WFST_EINVAL, "decode: negative frame_stride");
     if (o.capacity_hint < 0) return fail(WFST_EINVAL, "decode: negative capacity_hint");
     for (int u = 0; u < n_utt; u++) {
         if (T[u] < 0) return fail(WFST_EINVAL, "decode: negative T");
@@ -810,6 +823,9 @@ extern "C" void wfst_default_opts(wfst_decode_opts *o)
     o->blank_id = 0;
     o->flags = 0;
     o->capacity_hint = 0;
+    o->blank_ids = nullptr;
+    o->num_blank_ids = 0;
+    o->frame_stride = 1;
 }
 
 extern "C" int wfst_decode(const wfst_graph *g, const float *loglikes, int32_t T, int32_t L,

@@ -121,7 +121,9 @@ struct Params {
     int32_t max_active;
     float lattice_beam;
     int32_t lattice;
-    int32_t blank_id;
+    const int32_t *blank_ids;   // the blank-like units (device memory)
+    int32_t n_blank;
+    int32_t frame_stride;       // >= 1
     float blank_thr;
     int32_t lds_fill;         // states per frame the LDS token table takes (<= its fill limit)
     int32_t gen_lds;          // epsilon pool entries in LDS (<= its capacity)

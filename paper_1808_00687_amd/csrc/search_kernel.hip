@@ -955,8 +955,10 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
 }
 
 // isBlankFrame (Sec. 2, Alg. 1): frame t is blank when its blank
-// log-likelihood exceeds the threshold (log domain); the kept frames are
-// compacted in order, one workgroup per utterance.
+// log-likelihood exceeds the threshold (log domain); with a set of
+// blank-like units (HMM topologies, Sec. 2) when any of them does.  Only
+// every frame_stride-th frame is a candidate (a lower frame rate).  The kept
+// frames are compacted in order, one workgroup per utterance.
 __global__ __launch_bounds__(256) void classify_kernel(Params p)
 {
     __shared__ int sh_scan[17];
@@ -968,7 +970,12 @@ __global__ __launch_bounds__(256) void classify_kernel(Params p)
     for (int t0 = 0; t0 < T; t0 += blockDim.x) {
         const int t = t0 + threadIdx.x;
         int keep = 0;
-        if (t < T) keep = !(st.ll[static_cast<int64_t>(t) * p.L + p.blank_id] > p.blank_thr);
+        if (t < T && t % p.frame_stride == 0) {
+            const float *row = st.ll + static_cast<int64_t>(t) * p.L;
+            keep = 1;
+            for (int i = 0; i < p.n_blank; i++)
+                if (row[p.blank_ids[i]] > p.blank_thr) keep = 0;
+        }
         int total;
         const int ex = block_excl_scan(keep, sh_scan, &total);
         if (keep) p.kept[ly.kept0 + base + ex] = t;

@@ -43,7 +43,8 @@ class WfstError(RuntimeError):
 class _Opts(C.Structure):
     _fields_ = [("beam", C.c_float), ("max_active", C.c_int32), ("lattice_beam", C.c_float),
                 ("blank_threshold", C.c_float), ("blank_id", C.c_int32), ("flags", C.c_uint32),
-                ("capacity_hint", C.c_int64)]
+                ("capacity_hint", C.c_int64), ("blank_ids", C.c_void_p), ("num_blank_ids", C.c_int32),
+                ("frame_stride", C.c_int32)]
 
 
 class _Info(C.Structure):
@@ -295,7 +296,8 @@ def _collect(h, lattice: bool, tokens: bool, lat=None) -> WfstResult:
 # decode
 # --------------------------------------------------------------------------
 
-def _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint) -> _Opts:
+def _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint,
+          blank_ids=None, frame_stride=1, keep=None) -> _Opts:
     o = _Opts()
     _lib.wfst_default_opts(C.byref(o))
     o.beam = beam
@@ -305,6 +307,13 @@ def _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capa
     o.blank_id = blank_id
     o.flags = flags
     o.capacity_hint = capacity_hint
+    if blank_ids is not None:
+        ids = np.ascontiguousarray(blank_ids, dtype=np.int32)
+        if keep is not None:
+            keep.append(ids)
+        o.blank_ids = ids.ctypes.data if ids.size else None
+        o.num_blank_ids = ids.size if ids.size else -1   # an empty set is an error
+    o.frame_stride = frame_stride
     return o
 
 
@@ -340,7 +349,8 @@ def _stream_handle(stream):
 def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_active: int = 0,
                       lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
                       record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
-                      stream=None, profile_steps: bool = False) -> List[WfstResult]:
+                      stream=None, profile_steps: bool = False, blank_ids=None,
+                      frame_stride: int = 1) -> List[WfstResult]:
     """Decode a batch of utterances (wfst_decode_batch).  ``loglikes`` are
     [T_u x L] float32 tensors on the graph's device (or numpy arrays)."""
     keep: list = []
@@ -356,7 +366,8 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
     n = len(ptrs)
     flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
         (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0)
-    o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint)
+    o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint,
+              blank_ids, frame_stride, keep)
     parr = (C.c_void_p * n)(*ptrs)
     tarr = np.array(Ts, np.int32)
     outs = (C.c_void_p * n)()
@@ -377,14 +388,16 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
 def wfst_decode(graph: WfstGraph, loglikes, beam: float, max_active: int = 0,
                 lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
                 record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
-                stream=None, profile_steps: bool = False) -> WfstResult:
+                stream=None, profile_steps: bool = False, blank_ids=None,
+                frame_stride: int = 1) -> WfstResult:
     """Decode one utterance (wfst_decode).  Returns the result also when the
     status is WFST_ENOPATH; other errors raise WfstError."""
     keep: list = []
     ptr, shape, host = _ll_ptr(loglikes, keep)
     flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
         (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0)
-    o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint)
+    o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint,
+              blank_ids, frame_stride, keep)
     out = C.c_void_p()
     rc = _lib.wfst_decode(graph.handle, ptr, shape[0], shape[1], C.byref(o), _stream_handle(stream),
                           C.byref(out))

@@ -79,6 +79,8 @@ class DecodeOpts:
     lattice_beam: float = -1.0     # < 0: no lattice
     blank_threshold: float = 2.0   # > 1: frame synchronous
     blank_id: int = 0
+    blank_ids: Optional[tuple] = None   # a set of blank-like units instead of blank_id
+    frame_stride: int = 1               # decode every frame_stride-th frame
 
 
 @dataclasses.dataclass
@@ -202,6 +204,37 @@ def graph_cfg5() -> Graph:
     return Graph(n, src, dst, il, np.zeros(tot, np.int32), w)
 
 
+HMM_BLANK_UNITS = 8   # blank-like units of the HMM-topology stand-in (columns 0..7)
+
+
+def graph_cfg6() -> Graph:
+    """HMM-topology stand-in for the LSD variant the paper extends to HMM
+    models whose topology has a blank-like state (Sec. 2): the config-5
+    shape, but each state's self-loop reads one of HMM_BLANK_UNITS blank-like
+    units (ilabels 1..8, one per "phone" group, drawn per state), and the
+    rank-law arcs read the labels 9..80."""
+    rng = rng_for(6, GRAPH)
+    n = 5_000_000
+    k = HMM_BLANK_UNITS
+    deg = rank_law_degrees(n, 10_000_000, 1.2, 200, rng)
+    a = arcs_from_degrees(n, deg, 0.15, 80, 2.0, rng, first_label=k + 1)
+    loop_w = rng.exponential(2.0, size=n).astype(np.float32)
+    loop_il = rng.integers(1, k + 1, size=n).astype(np.int32)
+    tot = n + a["src"].shape[0]
+    rows = np.zeros(n + 1, dtype=np.int64)
+    rows[1:] = np.cumsum(deg + 1)
+    loop_pos = rows[:-1]
+    other_pos = np.ones(tot, dtype=bool)
+    other_pos[loop_pos] = False
+    src = np.empty(tot, np.int32); dst = np.empty(tot, np.int32)
+    il = np.empty(tot, np.int32); w = np.empty(tot, np.float32)
+    src[loop_pos] = np.arange(n, dtype=np.int32); dst[loop_pos] = np.arange(n, dtype=np.int32)
+    il[loop_pos] = loop_il; w[loop_pos] = loop_w
+    src[other_pos] = a["src"]; dst[other_pos] = a["dst"]
+    il[other_pos] = a["ilabel"]; w[other_pos] = a["weight"]
+    return Graph(n, src, dst, il, np.zeros(tot, np.int32), w)
+
+
 # --------------------------------------------------------------------------
 # log-likelihoods
 # --------------------------------------------------------------------------
@@ -227,6 +260,17 @@ def loglikes_ctc(cfg: int, utt: int, t: int, num_labels: int, boost: float = 8.0
     return np.ascontiguousarray(log_softmax_rows(z))
 
 
+def loglikes_hmm(cfg: int, utt: int, t: int, num_labels: int, k: int, boost: float = 8.0,
+                 p_blank: float = 0.85) -> np.ndarray:
+    """Logits N(0, 1); on frames drawn with probability p_blank one of the k
+    blank-like units, drawn per frame, is raised by ``boost``."""
+    rng = rng_for(cfg, LOGLIKES, utt)
+    z = rng.normal(0.0, 1.0, size=(t, num_labels))
+    m = np.flatnonzero(rng.random(t) < p_blank)
+    z[m, rng.integers(0, k, size=t)[m]] += boost
+    return np.ascontiguousarray(log_softmax_rows(z))
+
+
 def batch_lengths(n_utt: int = 64, lo: int = 300, hi: int = 1500) -> np.ndarray:
     rng = rng_for(4, LOGLIKES, 10_000)
     return rng.integers(lo, hi + 1, size=n_utt)
@@ -242,14 +286,16 @@ _graph_cache: dict = {}
 def graph_for(cfg: int) -> Graph:
     key = 3 if cfg == 4 else cfg
     if key not in _graph_cache:
-        _graph_cache[key] = {1: graph_cfg1, 2: graph_cfg2, 3: graph_cfg3, 5: graph_cfg5}[key]()
+        _graph_cache[key] = {1: graph_cfg1, 2: graph_cfg2, 3: graph_cfg3, 5: graph_cfg5, 6: graph_cfg6}[key]()
     return _graph_cache[key]
 
 
-def workload(cfg: int, n_utt: Optional[int] = None, lsd: bool = True) -> Workload:
-    """Config ``cfg`` (1..5).  For cfg 4, ``n_utt`` limits the number of
-    utterances (default 64); for cfg 5, ``lsd`` selects label-synchronous
-    (threshold 0.95) or frame-synchronous (threshold 2) decoding."""
+def workload(cfg: int, n_utt: Optional[int] = None, lsd: bool = True, frame_stride: int = 1) -> Workload:
+    """Config ``cfg`` (1..6).  For cfg 4, ``n_utt`` limits the number of
+    utterances (default 64); for cfg 5 and 6, ``lsd`` selects label-synchronous
+    (threshold 0.95) or frame-synchronous (threshold 2) decoding; cfg 6 is
+    the HMM-topology stand-in (a set of blank-like units), decoded every
+    ``frame_stride``-th frame."""
     g = graph_for(cfg)
     if cfg == 1:
         ll = [loglikes_gauss(1, 0, 50, 64, 2.0)]
@@ -274,7 +320,15 @@ def workload(cfg: int, n_utt: Optional[int] = None, lsd: bool = True) -> Workloa
         return Workload(5, "ctc-lsd" if lsd else "ctc-fsd", g, 80, ll,
                         DecodeOpts(beam=14.0, max_active=8000, lattice_beam=8.0,
                                    blank_threshold=thr, blank_id=0))
-    raise ValueError("cfg must be 1..5")
+    if cfg == 6:
+        k = HMM_BLANK_UNITS
+        ll = [loglikes_hmm(6, 0, 2000, 80, k)]
+        thr = 0.95 if lsd else 2.0
+        name = ("hmm-lsd" if lsd else "hmm-fsd") + ("-stride%d" % frame_stride if frame_stride > 1 else "")
+        return Workload(6, name, g, 80, ll,
+                        DecodeOpts(beam=14.0, max_active=8000, lattice_beam=8.0, blank_threshold=thr,
+                                   blank_ids=tuple(range(k)), frame_stride=frame_stride))
+    raise ValueError("cfg must be 1..6")
 
 
 # --------------------------------------------------------------------------
@@ -311,6 +365,30 @@ def random_small_graph(seed: int, n: int, mean_deg: float = 2.0, eps_frac: float
                       np.float32(np.inf)).astype(np.float32)
     return Graph(n, src.astype(np.int32), dst.astype(np.int32), il.astype(np.int32),
                  np.zeros(e, np.int32), w, 0, fw)
+
+
+def random_small_hmm_graph(seed: int, k: int, n: int = 400) -> Graph:
+    """A small graph whose every state has a self-loop on one of k
+    blank-like units (columns 0..k-1, one per phone of an HMM topology);
+    its other emitting arcs read columns k..k+5."""
+    g = random_small_graph(seed, n, mean_deg=2.0, eps_frac=0.1, num_labels=6)
+    rng = np.random.default_rng(np.random.SeedSequence([1808, 687, 97, seed]))
+    src = np.concatenate([np.arange(n), g.src]).astype(np.int32)
+    dst = np.concatenate([np.arange(n), g.dst]).astype(np.int32)
+    il = np.concatenate([rng.integers(1, k + 1, size=n), np.where(g.ilabel == 0, 0, g.ilabel + k)]).astype(np.int32)
+    w = np.concatenate([np.full(n, 0.5), g.weight]).astype(np.float32)
+    order = np.argsort(src, kind="stable")
+    return Graph(n, src[order], dst[order], il[order], np.zeros_like(src), w[order])
+
+
+def random_small_hmm_loglikes(seed: int, t: int, k: int) -> np.ndarray:
+    """log-softmax rows over k + 6 units; on about 70% of the frames one
+    blank-like unit, drawn at random, is raised by 7."""
+    rng = np.random.default_rng(np.random.SeedSequence([1808, 687, 96, seed]))
+    z = rng.normal(0.0, 1.0, size=(t, k + 6))
+    hot = rng.random(t) < 0.7
+    z[np.flatnonzero(hot), rng.integers(0, k, size=t)[hot]] += 7.0
+    return np.ascontiguousarray(log_softmax_rows(z))
 
 
 def random_small_loglikes(seed: int, t: int, num_labels: int, kind: str = "gauss",

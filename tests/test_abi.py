@@ -87,3 +87,31 @@ def test_validation_agrees_with_oracle(oracle_mod, name, g):
         assert got in (0, wfstdec.WFST_EDEVICE)
     else:
         assert got == wfstdec.WFST_EINVAL
+
+
+def test_ctypes_structs_match_the_header(tmp_path):
+    # the binding's ctypes mirrors of the header's structs: same size, same
+    # field offsets (read from a C program compiled against the header)
+    import ctypes
+    import subprocess
+    from paper_1808_00687_amd import wfstdec
+    mirrors = {"wfst_decode_opts": wfstdec._Opts, "wfst_stats": wfstdec._Stats,
+               "wfst_graph_info": wfstdec._Info, "wfst_lat_arc": wfstdec._LatArc}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "wfstdec.h"', "int main(void) {"]
+    for cname, py in mirrors.items():
+        lines.append('printf("%s size %%zu\\n", sizeof(%s));' % (cname, cname))
+        for f, _ in py._fields_:
+            lines.append('printf("%s %s %%zu\\n", offsetof(%s, %s));' % (cname, f, cname, f))
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    got = {}
+    for ln in subprocess.check_output([str(exe)], text=True).splitlines():
+        a, b, c = ln.split()
+        got[(a, b)] = int(c)
+    for cname, py in mirrors.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for f, _ in py._fields_:
+            assert got[(cname, f)] == getattr(py, f).offset, (cname, f)

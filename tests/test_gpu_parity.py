@@ -45,14 +45,15 @@ def to_dev(torch_mod, ll):
 
 def both(dec, torch_mod, oracle_mod, g, ll, gh=None, tokens=True, **o):
     ro = oracle_mod.decode(g, ll, o.get("beam", INF), o.get("max_active", 0), o.get("lattice_beam", -1.0),
-                           o.get("blank_threshold", 2.0), o.get("blank_id", 0))
+                           o.get("blank_threshold", 2.0), o.get("blank_id", 0), o.get("blank_ids"),
+                           o.get("frame_stride", 1))
     own = gh is None
     if own:
         gh = dec.load_graph(g)
     rg = dec.wfst_decode(gh, to_dev(torch_mod, ll), beam=o.get("beam", INF), max_active=o.get("max_active", 0),
                          lattice_beam=o.get("lattice_beam", -1.0),
                          blank_threshold=o.get("blank_threshold", 2.0), blank_id=o.get("blank_id", 0),
-                         record_tokens=tokens)
+                         record_tokens=tokens, blank_ids=o.get("blank_ids"), frame_stride=o.get("frame_stride", 1))
     if own:
         gh.free()
     return ro, rg
@@ -268,6 +269,28 @@ def test_lsd_small_ctc(dec, torch_mod, oracle_mod):
         parity.assert_same(ro, rg, lattice=True, tag="lsd thr %g" % thr)
 
 
+@pytest.mark.parametrize("thr,stride", [(0.95, 1), (0.5, 1), (0.9, 2), (2.0, 3), (0.95, 4)])
+def test_lsd_blank_unit_set_and_stride(dec, torch_mod, oracle_mod, thr, stride):
+    # HMM topology: several blank-like units; a lower frame rate by a stride
+    k = 3
+    g = W.random_small_hmm_graph(960, k, n=2000)
+    gh = dec.load_graph(g)
+    for seed in range(4):
+        ll = W.random_small_hmm_loglikes(970 + seed, 120, k)
+        ro, rg = both(dec, torch_mod, oracle_mod, g, ll, gh=gh, beam=10.0, max_active=300, lattice_beam=5.0,
+                      blank_threshold=thr, blank_ids=[2, 0, 1], frame_stride=stride)
+        parity.assert_same(ro, rg, lattice=True, tag="hmm thr %g stride %d seed %d" % (thr, stride, seed))
+    # the batch path (length groups) with the same options
+    lls = [W.random_small_hmm_loglikes(980 + u, 20 + 3 * u, k) for u in range(36)]
+    res = dec.wfst_decode_batch(gh, [to_dev(torch_mod, x) for x in lls], beam=10.0, max_active=300,
+                                lattice_beam=5.0, blank_threshold=thr, record_tokens=True, blank_ids=[0, 1, 2],
+                                frame_stride=stride)
+    for u, (x, r) in enumerate(zip(lls, res)):
+        ro = oracle_mod.decode(g, x, 10.0, 300, 5.0, thr, 0, [0, 1, 2], stride)
+        parity.assert_same(ro, r, lattice=True, tag="hmm batch utt %d" % u)
+    gh.free()
+
+
 def test_edge_cases(dec, torch_mod, oracle_mod):
     def gr(n, arcs, final=None):
         a = np.array(arcs, np.float64).reshape(-1, 5)
@@ -299,7 +322,9 @@ def test_argument_errors(dec, torch_mod):
     x = to_dev(torch_mod, np.zeros((1, 3), np.float32))
     assert dec.wfst_decode(gh, x, 1.0).status == 0
     for kw in (dict(beam=0.0), dict(beam=float("nan")), dict(beam=1.0, blank_id=3),
-               dict(beam=1.0, blank_threshold=0.0), dict(beam=1.0, lattice_beam=float("nan"))):
+               dict(beam=1.0, blank_threshold=0.0), dict(beam=1.0, lattice_beam=float("nan")),
+               dict(beam=1.0, blank_ids=[0, 3]), dict(beam=1.0, blank_ids=[-1]), dict(beam=1.0, blank_ids=[]),
+               dict(beam=1.0, frame_stride=-1)):
         with pytest.raises(dec.WfstError) as e:
             dec.wfst_decode(gh, x, **kw)
         assert e.value.code == dec.WFST_EINVAL
@@ -351,6 +376,23 @@ def test_config4_batch_sampled(dec, torch_mod, oracle_mod, cfg3):
         say("oracle on utterance", u)
         ro = oracle_mod.decode(g, wl.loglikes[u], o.beam, o.max_active, o.lattice_beam)
         parity.assert_same(ro, res[u], lattice=True, tokens=False, tag="config 4 utt %d" % u)
+
+
+def test_config6_hmm_lsd_and_stride(dec, torch_mod, oracle_mod):
+    # the HMM-topology stand-in at full size: eight blank-like units, with and
+    # without a frame stride of 3
+    wl = W.workload(6, lsd=True)
+    g = wl.graph
+    gh = dec.load_graph(g)
+    o = wl.opts
+    for thr, stride in ((0.95, 1), (0.95, 3), (2.0, 3)):
+        say("config 6 threshold", thr, "stride", stride)
+        ro, rg = both(dec, torch_mod, oracle_mod, g, wl.loglikes[0], gh=gh, beam=o.beam,
+                      max_active=o.max_active, lattice_beam=o.lattice_beam, blank_threshold=thr,
+                      blank_ids=list(o.blank_ids), frame_stride=stride)
+        parity.assert_same(ro, rg, lattice=True, tag="config 6 thr %g stride %d" % (thr, stride))
+        say("decoded", rg.num_decoded, "of", rg.num_frames, "arcs", rg.stats["arcs_expanded"])
+    gh.free()
 
 
 def test_config5_lsd_and_fsd(dec, torch_mod, oracle_mod):

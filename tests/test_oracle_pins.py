@@ -402,29 +402,11 @@ def test_lsd_work_scales_with_kept_frames(oracle_mod):
 # ----------------------------------------------------------------------------
 
 def _hmm_small(seed, k):
-    """A graph whose every state has a self-loop on one of k blank-like units
-    (columns 0..k-1, as one per phone of an HMM topology); its other emitting
-    arcs read columns k..k+5."""
-    g = W.random_small_graph(seed, 400, mean_deg=2.0, eps_frac=0.1, num_labels=6)
-    n = g.num_states
-    rng = np.random.default_rng(seed)
-    src = np.concatenate([np.arange(n), g.src]).astype(np.int32)
-    dst = np.concatenate([np.arange(n), g.dst]).astype(np.int32)
-    il = np.concatenate([rng.integers(1, k + 1, size=n), np.where(g.ilabel == 0, 0, g.ilabel + k)]).astype(np.int32)
-    w = np.concatenate([np.full(n, 0.5), g.weight]).astype(np.float32)
-    order = np.argsort(src, kind="stable")
-    return W.Graph(n, src[order], dst[order], il[order], np.zeros_like(src), w[order])
+    return W.random_small_hmm_graph(seed, k)
 
 
 def _hmm_loglikes(seed, t, k):
-    """log-softmax rows over k + 6 units; on about 70% of the frames one
-    blank-like unit, drawn at random, is raised by 7."""
-    rng = np.random.default_rng(seed)
-    z = rng.normal(0.0, 1.0, size=(t, k + 6))
-    hot = rng.random(t) < 0.7
-    z[np.flatnonzero(hot), rng.integers(0, k, size=t)[hot]] += 7.0
-    z = z - z.max(axis=1, keepdims=True)
-    return (z - np.log(np.exp(z).sum(axis=1, keepdims=True))).astype(np.float32)
+    return W.random_small_hmm_loglikes(seed, t, k)
 
 
 def _assert_lsd_is_fsd_on(lsd, fsd, kept):
