@@ -429,6 +429,12 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     arena.base = static_cast<char *>(lease.ptr);
     carve(arena);
     wt.mark("allocate");
+    if (wt.on) {
+        const double gib = 1.0 / (1024.0 * 1024.0 * 1024.0);
+        fprintf(stderr, "[wfstdec] workspace %.2f GiB: survivors %.2f, emitting regions %.2f, epsilon regions %.2f\n",
+                measure.off * gib, sv * (lattice ? 44.0 : 40.0) * gib, le * (lattice ? 36.0 : 16.0) * gib,
+                lx * 20.0 * gib);
+    }
     p.sv_off = fo_all;
     p.le_off = fo_all + fo;
     p.lx_off = fo_all + 2 * fo;
