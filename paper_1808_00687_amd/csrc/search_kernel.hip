@@ -49,6 +49,7 @@ constexpr int kCompact = 2;               // slot-list chunks a wave has in flig
 constexpr int kChunks = 2;                // 64-arc chunks a wave has in flight in the expansion
 constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
 constexpr int kOverflow = 1;              // frame result: the table filled up
+constexpr uint32_t kNoKey = 0xFFFFFFFEu;   // a key no state has (state ids are below 2^31)
 
 static_assert(kHistBins * 4 <= kW * kQueue * 8, "the select histogram aliases the epsilon queues");
 
@@ -187,9 +188,20 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
     uint32_t h[R], k[R];
     bool claimed[R];
 #pragma unroll
-    for (int r = 0; r < R; r++) {
-        h[r] = hash_state(d[r]) >> t.shift;
-        k[r] = act[r] ? atomicCAS(t.keys + h[r], kEmptyKey, d[r]) : 0u;
+    for (int r = 0; r < R; r++) h[r] = hash_state(d[r]) >> t.shift;
+    if constexpr (!G) {
+        // In LDS every lane issues its compare-and-swap, so that the R
+        // atomics of the wave are in flight together instead of one branch
+        // (and one wait) each: an inactive lane compares and swaps a key no
+        // state has, at a slot of its own, which changes nothing.
+#pragma unroll
+        for (int r = 0; r < R; r++) {
+            const uint32_t at = act[r] ? h[r] : (h[r] + lane_id()) & t.mask;
+            k[r] = atomicCAS(t.keys + at, act[r] ? kEmptyKey : kNoKey, act[r] ? d[r] : kNoKey);
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < R; r++) k[r] = act[r] ? atomicCAS(t.keys + h[r], kEmptyKey, d[r]) : 0u;
     }
     bool over = false;
 #pragma unroll
@@ -207,6 +219,21 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
             claimed[r] = k[r] == kEmptyKey;
         } else {
             over = true;
+        }
+    }
+    // recombination: the unsigned minimum of (cost key, arc + 1); issued
+    // before the slot-list add below, so that their LDS round trips overlap
+    // (in LDS without a branch: a lane without a slot takes the minimum of
+    // a slot of its own and the empty token, which changes nothing)
+    unsigned long long v[R], old[R];
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        v[r] = make_tok(key[r], arc[r]);
+        if constexpr (!G) {
+            const uint32_t at = slot[r] >= 0 ? static_cast<uint32_t>(slot[r]) : (h[r] + lane_id()) & t.mask;
+            old[r] = atomicMin(t.vals + at, slot[r] >= 0 ? v[r] : kEmptyTok);
+        } else {
+            old[r] = slot[r] >= 0 ? atomicMin(t.vals + slot[r], v[r]) : 0ull;
         }
     }
     // newly claimed slots join the slot list, one LDS add per wave
@@ -232,13 +259,6 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
         }
     }
     if (over) sh.overflow = 1;
-    // recombination: the unsigned minimum of (cost key, arc + 1)
-    unsigned long long v[R], old[R];
-#pragma unroll
-    for (int r = 0; r < R; r++) {
-        v[r] = make_tok(key[r], arc[r]);
-        old[r] = slot[r] >= 0 ? atomicMin(t.vals + slot[r], v[r]) : 0ull;
-    }
     if (BEST) {
         uint32_t mk = kEmptyKey;
 #pragma unroll
