@@ -567,10 +567,14 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
 
     wt.mark("lattice output");
     // gather results
-    std::vector<int64_t> fo_h(static_cast<size_t>(fo));
-    std::vector<int32_t> kept_h(static_cast<size_t>(kp));
-    chk(hipMemcpyAsync(fo_h.data(), p.sv_off, fo * sizeof(int64_t), hipMemcpyDeviceToHost, s));
-    chk(hipMemcpyAsync(kept_h.data(), p.kept, kp * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    // the set offsets serve only the token sets; the kept frames are every
+    // frame when no frame can be skipped
+    const bool want_tokens = (o.flags & WFST_RECORD_TOKENS) != 0;
+    const bool all_frames = !(thr < std::numeric_limits<float>::infinity()) && p.frame_stride == 1;
+    std::vector<int64_t> fo_h(want_tokens ? static_cast<size_t>(fo) : 0);
+    std::vector<int32_t> kept_h(all_frames ? 0 : static_cast<size_t>(kp));
+    if (want_tokens) chk(hipMemcpyAsync(fo_h.data(), p.sv_off, fo * sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    if (!all_frames) chk(hipMemcpyAsync(kept_h.data(), p.kept, kp * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     // the packed best paths, in utterance order
     int64_t path_total = 0;
     std::vector<int64_t> path_off(static_cast<size_t>(U), 0);
@@ -650,7 +654,12 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
             r->path_arcs[i] = paths_h[path_off[u] + i].x;
             r->path_frames[i] = paths_h[path_off[u] + i].y;
         }
-        r->kept.assign(kept_h.begin() + lay[u].kept0, kept_h.begin() + lay[u].kept0 + st[u].Tp);
+        if (all_frames) {
+            r->kept.resize(static_cast<size_t>(std::max(st[u].Tp, 0)));
+            std::iota(r->kept.begin(), r->kept.end(), 0);
+        } else {
+            r->kept.assign(kept_h.begin() + lay[u].kept0, kept_h.begin() + lay[u].kept0 + st[u].Tp);
+        }
         r->stats.decode_ms = wall;
         r->stats.search_ms = ph[PH_SEARCH];
         r->stats.record_ms = ph[PH_RECORD];
