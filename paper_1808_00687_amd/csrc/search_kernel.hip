@@ -496,7 +496,10 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             const int4 lo = p.g.srec[2 * s];
             x0 = p.g.srec[2 * s + 1];
             const uint32_t cl = static_cast<uint32_t>(x0.w);
-            if (cl) {
+            // A list of one path is the state's only epsilon arc, into a
+            // state without epsilon arcs: the copy of that arc in the state
+            // record offers it below without loading the list.
+            if (cl && (cl & 63u) != 0u) {
                 cb = static_cast<int>(cl >> 6) - 1;
                 cn = static_cast<int>(cl & 63u) + 1;
             } else {
