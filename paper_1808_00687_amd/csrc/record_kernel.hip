@@ -242,7 +242,7 @@ __global__ __launch_bounds__(kRT) void record_kernel(Params p)
 // to kRBigFill survivors uses a 128 KB LDS table, a larger one the
 // utterance's device-memory table (at most three quarters full: its size
 // bounds the states a frame may reach), taken by part 0 alone.
-constexpr int kLargeParts = 4;
+constexpr int kLargeParts = 8;
 constexpr int kRBigBits = 14;
 constexpr int kRBigFill = (1 << kRBigBits) / 4 * 3;
 
