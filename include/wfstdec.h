@@ -155,7 +155,9 @@ int wfst_decode(const wfst_graph *g, const float *loglikes, int32_t T, int32_t L
  * groups of similar lengths; the groups' launches run on the library's own
  * streams beside hip_stream (forked from and joined back into it with
  * events), so the record and lattice passes of short utterances overlap the
- * search of long ones.  Results do not depend on the grouping.
+ * search of long ones.  Results do not depend on the grouping.  Concurrent
+ * batch calls on one device share the library's streams, so their group
+ * launches queue behind one another.
  *
  *   loglikes   [n_utt] host array of pointers, each [T[u] x L] float32
  *   T          [n_utt] host array of frame counts
