@@ -166,25 +166,28 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
             cl_size[s] = static_cast<int32_t>(std::min<int64_t>(size, kClosureMax + 1));
             cl_depth[s] = std::min(dep, kClosureDepth + 1);
             if (size > kClosureMax || dep > kClosureDepth || !child_listed) continue;
-            const int64_t off = static_cast<int64_t>(ctab.size() / 2);
+            const int64_t off = static_cast<int64_t>(ctab.size() / kClosureStride);
             if (off + size >= kClosureEntries) continue;
             for (int32_t x = xoff[s]; x < xoff[s + 1]; x++) {
                 const int4 r = xarc[x];
                 const int32_t d = r.x & 0x7FFFFFFF;
                 ctab.push_back(make_int4(d, r.z, 1, r.y));
                 ctab.push_back(make_int4(0, 0, 0, 0));
+                ctab.push_back(make_int4(0, 0, 0, 0));
                 if (cl_size[d] == 0) continue;
                 for (int32_t i = 0; i < cl_size[d]; i++) {
-                    const int4 c0 = ctab[2 * (cl_off[d] + i)], c1 = ctab[2 * (cl_off[d] + i) + 1];
-                    // the arc to d, then the child's path
-                    const int32_t w[5] = {r.y, c0.w, c1.x, c1.y, c1.z};
-                    ctab.push_back(make_int4(c0.x, c0.y, c0.z + 1, w[0]));
-                    ctab.push_back(make_int4(w[1], w[2], w[3], w[4]));
+                    const size_t ci = kClosureStride * static_cast<size_t>(cl_off[d] + i);
+                    const int4 c0 = ctab[ci], c1 = ctab[ci + 1], c2 = ctab[ci + 2];
+                    // the arc to d, then the child's path (at most
+                    // kClosureDepth - 1 arcs, so its last weight slot is free)
+                    ctab.push_back(make_int4(c0.x, c0.y, c0.z + 1, r.y));
+                    ctab.push_back(make_int4(c0.w, c1.x, c1.y, c1.z));
+                    ctab.push_back(make_int4(c1.w, c2.x, c2.y, c2.z));
                 }
             }
             cl_off[s] = off;
-            srec[2 * static_cast<size_t>(s) + 1].w =
-                static_cast<int32_t>((static_cast<uint32_t>(off + 1) << 6) | static_cast<uint32_t>(size - 1));
+            srec[2 * static_cast<size_t>(s) + 1].w = static_cast<int32_t>(
+                (static_cast<uint32_t>(off + 1) << kClosureSizeBits) | static_cast<uint32_t>(size - 1));
             n_closure++;
         }
     } catch (const std::bad_alloc &) {

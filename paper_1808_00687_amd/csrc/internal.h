@@ -14,8 +14,9 @@
 //              word locates the state's epsilon-closure list
 //   ctab[]     epsilon-closure lists: every epsilon path from a state (up to
 //              size and length limits) as {last destination, last arc,
-//              length, the weights along the path}, so the closure from a
-//              lowered token needs no chain of dependent loads
+//              length, the weights along the path} in three 16-byte words,
+//              so the closure from a lowered token needs no chain of
+//              dependent loads
 // Each state's arcs keep their user order inside the emitting and the
 // epsilon partition.  has_eps marks a destination with epsilon out-arcs, so a
 // kernel that lowers its token knows without another load whether the
@@ -50,15 +51,20 @@ struct DevGraph {
     const int32_t *arc_src;
     const float *final_w;
     const int4 *srec;   // 2 x N: {eoff[s], eoff[s+1], xoff[s], xoff[s+1]}, first epsilon record of s
-                        // whose 4th word is the state's closure list ((offset + 1) << 6 | size - 1, or 0)
-    const int4 *ctab;   // closure entries, 2 x int4 each: {dst, user arc, path length, w0}, {w1..w4}
+                        // whose 4th word is the state's closure list
+                        // ((offset + 1) << kClosureSizeBits | size - 1, or 0)
+    const int4 *ctab;   // closure entries, 3 x int4 each: {dst, user arc, path length, w0}, {w1..w4}, {w5..w8}
 };
 
 // Epsilon-closure lists (built by wfst_load): at most kClosureMax paths of at
-// most kClosureDepth arcs per state, kClosureEntries entries in all.
-constexpr int kClosureMax = 64;
-constexpr int kClosureDepth = 5;
-constexpr int64_t kClosureEntries = (int64_t{1} << 26) - 2;
+// most kClosureDepth arcs per state, kClosureEntries entries in all.  The
+// state record's closure word holds a list's size - 1 in its low
+// kClosureSizeBits bits and its first entry + 1 above them.
+constexpr int kClosureSizeBits = 8;
+constexpr int kClosureMax = 1 << kClosureSizeBits;
+constexpr int kClosureDepth = 9;
+constexpr int kClosureStride = 3;   // int4 words per entry
+constexpr int64_t kClosureEntries = (int64_t{1} << (32 - kClosureSizeBits)) - 2;
 
 // Host-side graph object behind the opaque wfst_graph handle.
 struct Graph {

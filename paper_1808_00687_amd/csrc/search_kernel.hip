@@ -499,9 +499,10 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             // A list of one path is the state's only epsilon arc, into a
             // state without epsilon arcs: the copy of that arc in the state
             // record offers it below without loading the list.
-            if (cl && (cl & 63u) != 0u) {
-                cb = static_cast<int>(cl >> 6) - 1;
-                cn = static_cast<int>(cl & 63u) + 1;
+            constexpr uint32_t kSizeMask = (1u << kClosureSizeBits) - 1u;
+            if (cl && (cl & kSizeMask) != 0u) {
+                cb = static_cast<int>(cl >> kClosureSizeBits) - 1;
+                cn = static_cast<int>(cl & kSizeMask) + 1;
             } else {
                 first = lo.w > lo.z;
                 xb = lo.z + 1;
@@ -526,13 +527,20 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             int arc = 0;
             float cnd = 0.0f;
             if (kk < tot) {
-                const int64_t e = 2 * static_cast<int64_t>(ob + (kk - op));
+                const int64_t e = kClosureStride * static_cast<int64_t>(ob + (kk - op));
                 const int4 c0 = p.g.ctab[e], c1 = p.g.ctab[e + 1];
+                // paths of more than five arcs are rare: their last weights
+                // are loaded when the path is seen to need them
+                const int4 c2 = c0.z > 5 ? p.g.ctab[e + 2] : make_int4(0, 0, 0, 0);
                 cnd = oc + __int_as_float(c0.w);
                 if (c0.z > 1) cnd = cnd + __int_as_float(c1.x);
                 if (c0.z > 2) cnd = cnd + __int_as_float(c1.y);
                 if (c0.z > 3) cnd = cnd + __int_as_float(c1.z);
                 if (c0.z > 4) cnd = cnd + __int_as_float(c1.w);
+                if (c0.z > 5) cnd = cnd + __int_as_float(c2.x);
+                if (c0.z > 6) cnd = cnd + __int_as_float(c2.y);
+                if (c0.z > 7) cnd = cnd + __int_as_float(c2.z);
+                if (c0.z > 8) cnd = cnd + __int_as_float(c2.w);
                 d = static_cast<uint32_t>(c0.x);
                 arc = c0.y;
                 key = okey(cnd);

@@ -367,6 +367,67 @@ def random_small_graph(seed: int, n: int, mean_deg: float = 2.0, eps_frac: float
                  np.zeros(e, np.int32), w, 0, fw)
 
 
+def closure_shapes_graph(seed: int, num_labels: int = 5) -> Graph:
+    """A graph of epsilon structures around the sizes where a decoder may
+    switch between precomputed closure lists and arc-by-arc relaxation:
+    epsilon chains of 1 to 12 arcs, and two-level fans whose heads have 2 to
+    300 epsilon paths (k arcs to states with m epsilon arcs each, k (m + 1)
+    paths), some with chains behind their leaves.  Epsilon arcs go to higher
+    state ids (the graph is epsilon-acyclic); every state also has one to
+    three emitting arcs to uniformly drawn states, and the start state has an
+    emitting arc to every structure's head.  Weights are Exp(1) in float32."""
+    rng = np.random.default_rng(np.random.SeedSequence([1808, 687, 95, seed]))
+    eps_arcs = []   # (src, dst)
+    heads = []
+    nxt = [1]       # state 0 is the start state
+
+    def new_state():
+        nxt[0] += 1
+        return nxt[0] - 1
+
+    def chain(length, head=None):
+        a = new_state() if head is None else head
+        h = a
+        for _ in range(length):
+            b = new_state()
+            eps_arcs.append((a, b))
+            a = b
+        return h
+
+    for length in (1, 2, 5, 6, 8, 9, 10, 12):
+        heads.append(chain(length))
+    for k, m, tail in ((1, 1, 0), (16, 15, 0), (16, 16, 0), (8, 31, 0), (2, 127, 0), (1, 255, 0), (1, 256, 0),
+                       (3, 4, 7), (4, 2, 6), (20, 14, 0)):
+        a = new_state()
+        heads.append(a)
+        for _ in range(k):
+            b = new_state()
+            eps_arcs.append((a, b))
+            for _ in range(m):
+                c = new_state()
+                eps_arcs.append((b, c))
+                if tail:
+                    chain(tail, head=c)
+    n = nxt[0]
+    src = [np.asarray([e[0] for e in eps_arcs], np.int64)]
+    dst = [np.asarray([e[1] for e in eps_arcs], np.int64)]
+    il = [np.zeros(len(eps_arcs), np.int64)]
+    deg = rng.integers(1, 4, size=n)
+    es = np.repeat(np.arange(n), deg)
+    src.append(es)
+    dst.append(rng.integers(0, n, size=es.size))
+    il.append(rng.integers(1, num_labels + 1, size=es.size))
+    hs = np.asarray(heads, np.int64)
+    src.append(np.zeros(hs.size, np.int64))
+    dst.append(hs)
+    il.append(rng.integers(1, num_labels + 1, size=hs.size))
+    src, dst, il = np.concatenate(src), np.concatenate(dst), np.concatenate(il)
+    w = rng.exponential(1.0, size=src.size).astype(np.float32)
+    order = np.argsort(src, kind="stable")
+    return Graph(n, src[order].astype(np.int32), dst[order].astype(np.int32), il[order].astype(np.int32),
+                 np.zeros(src.size, np.int32), w[order])
+
+
 def random_small_hmm_graph(seed: int, k: int, n: int = 400) -> Graph:
     """A small graph whose every state has a self-loop on one of k
     blank-like units (columns 0..k-1, one per phone of an HMM topology);

@@ -81,6 +81,19 @@ def test_small_random_graphs(dec, torch_mod, oracle_mod, seed, kind):
     parity.assert_same(ro, rg, lattice=lb >= 0, tag="seed %d" % seed)
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_epsilon_closure_shapes(dec, torch_mod, oracle_mod, seed):
+    # epsilon chains and fans just inside and just outside the sizes and
+    # lengths of precomputed closure lists, with float32 weights whose sums
+    # depend on the order of the additions
+    g = W.closure_shapes_graph(seed)
+    ll = W.random_small_loglikes(60 + seed, 12, 5)
+    for beam, max_active, lb in ((INF, 0, INF), (6.0, 400, 3.0), (2.5, 0, 1.0)):
+        ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=beam, max_active=max_active, lattice_beam=lb)
+        parity.assert_same(ro, rg, lattice=True, tag="closure shapes %d beam %g" % (seed, beam))
+    say("closure shapes", seed, "tokens", rg.stats["tokens"], "eps arcs", rg.stats.get("eps_arcs"))
+
+
 def test_config1_full(dec, torch_mod, oracle_mod):
     wl = W.workload(1)
     o = wl.opts
