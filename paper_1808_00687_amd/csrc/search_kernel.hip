@@ -47,6 +47,7 @@ constexpr int kSetCache = 3008;           // tokens of the previous set kept in 
 constexpr int kCs = 128;                  // 64-arc chunks of the previous set with their first token in LDS
 constexpr int kCompact = 2;               // slot-list chunks a wave has in flight in the compaction
 constexpr int kChunks = 2;                // 64-arc chunks a wave has in flight in the expansion
+constexpr int kRelChunks = 2;             // 64-path chunks of closure lists a wave has in flight
 constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
 constexpr int kOverflow = 1;              // frame result: the table filled up
 constexpr uint32_t kNoKey = 0xFFFFFFFEu;   // a key no state has (state ids are below 2^31)
@@ -510,43 +511,62 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             }
         }
     }
-    // closure lists, spread over the wave
+    // closure lists, spread over the wave, kRelChunks chunks of paths per
+    // step so that their loads are in flight together; paths of more than
+    // five arcs are rare: their last weights are loaded when the path is seen
+    // to need them
     {
         const int incl = wave_incl_scan(cn);
         const int pre = incl - cn;
         const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
-        for (int k0 = 0; k0 < tot; k0 += kWave) {
-            const int kk = k0 + lane;
-            const int o = owner_lane(pre, kk);
-            const int ob = __shfl(cb, o, kWave);
-            const int op = __shfl(pre, o, kWave);
-            const float oc = __shfl(cst, o, kWave);
-            const uint32_t bnd = drop_bound(sh.best, p.beam);
-            bool act = false;
-            uint32_t d = 0, key = kEmptyKey;
-            int arc = 0;
-            float cnd = 0.0f;
-            if (kk < tot) {
-                const int64_t e = kClosureStride * static_cast<int64_t>(ob + (kk - op));
-                const int4 c0 = p.g.ctab[e], c1 = p.g.ctab[e + 1];
-                // paths of more than five arcs are rare: their last weights
-                // are loaded when the path is seen to need them
-                const int4 c2 = c0.z > 5 ? p.g.ctab[e + 2] : make_int4(0, 0, 0, 0);
-                cnd = oc + __int_as_float(c0.w);
-                if (c0.z > 1) cnd = cnd + __int_as_float(c1.x);
-                if (c0.z > 2) cnd = cnd + __int_as_float(c1.y);
-                if (c0.z > 3) cnd = cnd + __int_as_float(c1.z);
-                if (c0.z > 4) cnd = cnd + __int_as_float(c1.w);
-                if (c0.z > 5) cnd = cnd + __int_as_float(c2.x);
-                if (c0.z > 6) cnd = cnd + __int_as_float(c2.y);
-                if (c0.z > 7) cnd = cnd + __int_as_float(c2.z);
-                if (c0.z > 8) cnd = cnd + __int_as_float(c2.w);
-                d = static_cast<uint32_t>(c0.x);
-                arc = c0.y;
-                key = okey(cnd);
-                act = key <= bnd;
+        for (int k0 = 0; k0 < tot; k0 += kWave * kRelChunks) {
+            int4 c0[kRelChunks], c1[kRelChunks];
+            float oc[kRelChunks];
+            int64_t e[kRelChunks];
+#pragma unroll
+            for (int r = 0; r < kRelChunks; r++) {
+                const int kk = k0 + r * kWave + lane;
+                c0[r] = c1[r] = make_int4(0, 0, 0, 0);
+                oc[r] = 0.0f;
+                e[r] = 0;
+                if (k0 + r * kWave < tot) {
+                    const int o = owner_lane(pre, kk);
+                    const int ob = __shfl(cb, o, kWave);
+                    const int op = __shfl(pre, o, kWave);
+                    oc[r] = __shfl(cst, o, kWave);
+                    if (kk < tot) {
+                        e[r] = kClosureStride * static_cast<int64_t>(ob + (kk - op));
+                        c0[r] = p.g.ctab[e[r]];
+                        c1[r] = p.g.ctab[e[r] + 1];
+                    }
+                }
             }
-            (void)offer1<G>(t, sh, wq, act, d, false, cnd, key, arc);
+            const uint32_t bnd = drop_bound(sh.best, p.beam);
+            bool act[kRelChunks], de[kRelChunks];
+            uint32_t d[kRelChunks], key[kRelChunks];
+            int32_t arc[kRelChunks];
+            float cnd[kRelChunks];
+#pragma unroll
+            for (int r = 0; r < kRelChunks; r++) {
+                const int4 c2 = c0[r].z > 5 ? p.g.ctab[e[r] + 2] : make_int4(0, 0, 0, 0);
+                float c = oc[r] + __int_as_float(c0[r].w);
+                if (c0[r].z > 1) c = c + __int_as_float(c1[r].x);
+                if (c0[r].z > 2) c = c + __int_as_float(c1[r].y);
+                if (c0[r].z > 3) c = c + __int_as_float(c1[r].z);
+                if (c0[r].z > 4) c = c + __int_as_float(c1[r].w);
+                if (c0[r].z > 5) c = c + __int_as_float(c2.x);
+                if (c0[r].z > 6) c = c + __int_as_float(c2.y);
+                if (c0[r].z > 7) c = c + __int_as_float(c2.z);
+                if (c0[r].z > 8) c = c + __int_as_float(c2.w);
+                cnd[r] = c;
+                d[r] = static_cast<uint32_t>(c0[r].x);
+                de[r] = false;
+                arc[r] = c0[r].y;
+                key[r] = okey(c);
+                act[r] = k0 + r * kWave + lane < tot && key[r] <= bnd;
+            }
+            int slot[kRelChunks];
+            offer<G, kRelChunks, true>(t, sh, wq, act, d, de, cnd, key, arc, slot);
         }
     }
     {
