@@ -512,21 +512,21 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
         }
     }
     // closure lists, spread over the wave, kRelChunks chunks of paths per
-    // step so that their loads are in flight together; paths of more than
-    // five arcs are rare: their last weights are loaded when the path is seen
-    // to need them
+    // step so that their loads (all three words of an entry: a load that
+    // waited for the path length would add a round trip) are in flight
+    // together
     {
         const int incl = wave_incl_scan(cn);
         const int pre = incl - cn;
         const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
         for (int k0 = 0; k0 < tot; k0 += kWave * kRelChunks) {
-            int4 c0[kRelChunks], c1[kRelChunks];
+            int4 c0[kRelChunks], c1[kRelChunks], c2[kRelChunks];
             float oc[kRelChunks];
             int64_t e[kRelChunks];
 #pragma unroll
             for (int r = 0; r < kRelChunks; r++) {
                 const int kk = k0 + r * kWave + lane;
-                c0[r] = c1[r] = make_int4(0, 0, 0, 0);
+                c0[r] = c1[r] = c2[r] = make_int4(0, 0, 0, 0);
                 oc[r] = 0.0f;
                 e[r] = 0;
                 if (k0 + r * kWave < tot) {
@@ -538,6 +538,7 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
                         e[r] = kClosureStride * static_cast<int64_t>(ob + (kk - op));
                         c0[r] = p.g.ctab[e[r]];
                         c1[r] = p.g.ctab[e[r] + 1];
+                        c2[r] = p.g.ctab[e[r] + 2];
                     }
                 }
             }
@@ -548,16 +549,15 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             float cnd[kRelChunks];
 #pragma unroll
             for (int r = 0; r < kRelChunks; r++) {
-                const int4 c2 = c0[r].z > 5 ? p.g.ctab[e[r] + 2] : make_int4(0, 0, 0, 0);
                 float c = oc[r] + __int_as_float(c0[r].w);
                 if (c0[r].z > 1) c = c + __int_as_float(c1[r].x);
                 if (c0[r].z > 2) c = c + __int_as_float(c1[r].y);
                 if (c0[r].z > 3) c = c + __int_as_float(c1[r].z);
                 if (c0[r].z > 4) c = c + __int_as_float(c1[r].w);
-                if (c0[r].z > 5) c = c + __int_as_float(c2.x);
-                if (c0[r].z > 6) c = c + __int_as_float(c2.y);
-                if (c0[r].z > 7) c = c + __int_as_float(c2.z);
-                if (c0[r].z > 8) c = c + __int_as_float(c2.w);
+                if (c0[r].z > 5) c = c + __int_as_float(c2[r].x);
+                if (c0[r].z > 6) c = c + __int_as_float(c2[r].y);
+                if (c0[r].z > 7) c = c + __int_as_float(c2[r].z);
+                if (c0[r].z > 8) c = c + __int_as_float(c2[r].w);
                 cnd[r] = c;
                 d[r] = static_cast<uint32_t>(c0[r].x);
                 de[r] = false;
