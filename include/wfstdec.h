@@ -90,6 +90,10 @@ typedef struct wfst_graph_info {
     int32_t max_ilabel;       /* decode needs L >= max_ilabel */
     int32_t epsilon_depth;    /* longest epsilon path (arcs) */
     int64_t device_bytes;     /* device memory held by the layout */
+    int64_t num_closure_states; /* states whose whole epsilon closure is precomputed as a list
+                                   of paths (at most 256 paths of at most 9 arcs each); the
+                                   others relax their epsilon arcs one level at a time.  The
+                                   results are the same either way. */
 } wfst_graph_info;
 
 int wfst_graph_get_info(const wfst_graph *g, wfst_graph_info *info);

@@ -276,5 +276,6 @@ extern "C" int wfst_graph_get_info(const wfst_graph *h, wfst_graph_info *info)
     info->max_ilabel = h->g.max_ilabel;
     info->epsilon_depth = h->g.eps_depth;
     info->device_bytes = h->g.device_bytes;
+    info->num_closure_states = h->g.n_closure;
     return WFST_OK;
 }

@@ -50,7 +50,7 @@ class _Opts(C.Structure):
 class _Info(C.Structure):
     _fields_ = [("num_states", C.c_int32), ("num_arcs", C.c_int64), ("num_emitting", C.c_int64),
                 ("num_epsilon", C.c_int64), ("max_ilabel", C.c_int32), ("epsilon_depth", C.c_int32),
-                ("device_bytes", C.c_int64)]
+                ("device_bytes", C.c_int64), ("num_closure_states", C.c_int64)]
 
 
 class _Stats(C.Structure):

@@ -81,17 +81,42 @@ def test_small_random_graphs(dec, torch_mod, oracle_mod, seed, kind):
     parity.assert_same(ro, rg, lattice=lb >= 0, tag="seed %d" % seed)
 
 
+def listed_closure_states(g, max_paths, max_len):
+    """States whose epsilon closure is at most max_paths paths of at most
+    max_len arcs, every child with epsilon arcs being such a state too
+    (epsilon arcs of these graphs go to higher state ids)."""
+    eps = g.ilabel == 0
+    kids = {}
+    for s, d in zip(g.src[eps].tolist(), g.dst[eps].tolist()):
+        kids.setdefault(s, []).append(d)
+    size, depth, listed = {}, {}, {}
+    for s in sorted(kids, reverse=True):
+        sz = sum(1 + size.get(d, 0) for d in kids[s])
+        dp = max(1 + depth.get(d, 0) for d in kids[s])
+        ok = all(listed.get(d, True) for d in kids[s])
+        size[s], depth[s] = min(sz, max_paths + 1), min(dp, max_len + 1)
+        listed[s] = sz <= max_paths and dp <= max_len and ok
+    return sum(listed.values())
+
+
 @pytest.mark.parametrize("seed", range(4))
 def test_epsilon_closure_shapes(dec, torch_mod, oracle_mod, seed):
     # epsilon chains and fans just inside and just outside the sizes and
     # lengths of precomputed closure lists, with float32 weights whose sums
     # depend on the order of the additions
     g = W.closure_shapes_graph(seed)
+    gh = dec.load_graph(g)
+    # the library lists closures up to 256 paths of up to 9 arcs (the
+    # results do not show it: they are the same either way)
+    n_listed = gh.info()["num_closure_states"]
+    assert n_listed == listed_closure_states(g, 256, 9)
+    assert n_listed > listed_closure_states(g, 64, 5)
     ll = W.random_small_loglikes(60 + seed, 12, 5)
     for beam, max_active, lb in ((INF, 0, INF), (6.0, 400, 3.0), (2.5, 0, 1.0)):
-        ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=beam, max_active=max_active, lattice_beam=lb)
+        ro, rg = both(dec, torch_mod, oracle_mod, g, ll, gh=gh, beam=beam, max_active=max_active, lattice_beam=lb)
         parity.assert_same(ro, rg, lattice=True, tag="closure shapes %d beam %g" % (seed, beam))
-    say("closure shapes", seed, "tokens", rg.stats["tokens"], "eps arcs", rg.stats.get("eps_arcs"))
+    gh.free()
+    say("closure shapes", seed, "listed", n_listed, "tokens", rg.stats["tokens"])
 
 
 def test_config1_full(dec, torch_mod, oracle_mod):
