@@ -122,10 +122,10 @@ __device__ void backtrace_block(const Params &p, int u, int *sh)
 // s_waitcnt immediate: vmcnt(0), the other counters left free
 constexpr int kWaitVm0 = 0x0F70;
 constexpr int kLatLds = 8192;   // survivors per token set kept in LDS by the backward pass
-constexpr int kLatT = 512;      // threads of a finish block
-constexpr int kRE = 4;          // emitting records per thread held in registers
+constexpr int kLatT = 768;      // threads of a finish block
+constexpr int kRE = 3;          // emitting records per thread held in registers
 constexpr int kRX = 2;          // epsilon records per thread held in registers
-constexpr int kRC = 6;          // survivors per thread held in registers
+constexpr int kRC = 4;          // survivors per thread held in registers
 
 // Where the records and survivors of one token set j lie.
 struct LatMeta {
