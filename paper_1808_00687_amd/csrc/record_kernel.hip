@@ -26,7 +26,7 @@ namespace wfd {
 
 namespace {
 
-constexpr int kRT = 512;                // threads of a record block
+constexpr int kRT = 1024;               // threads of a record block
 constexpr int kRSlotBits = 13;
 constexpr int kRSlots = 1 << kRSlotBits;
 constexpr int kRFill = kRSlots / 4 * 3; // survivors per set the LDS table takes
