@@ -353,6 +353,24 @@ def test_edge_cases(dec, torch_mod, oracle_mod):
     assert rg.reached_final == 0
 
 
+def test_long_utterance(dec, torch_mod, oracle_mod):
+    # more frames than a 16-bit index holds: frame offsets, per-frame launch
+    # grids and the lattice pass's chain over the sets all span them
+    # a small graph whose states all have a self-loop, so no path dies out
+    b = W.random_small_graph(990, 60, mean_deg=3.0, eps_frac=0.2, num_labels=5)
+    n = b.num_states
+    src = np.concatenate([np.arange(n), b.src]).astype(np.int32)
+    order = np.argsort(src, kind="stable")
+    g = W.Graph(n, src[order], np.concatenate([np.arange(n), b.dst]).astype(np.int32)[order],
+                np.concatenate([np.full(n, 1), b.ilabel]).astype(np.int32)[order], np.zeros(src.size, np.int32),
+                np.concatenate([np.full(n, 1.5), b.weight]).astype(np.float32)[order])
+    ll = W.random_small_loglikes(990, 70000, 5)
+    ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=8.0, max_active=12, lattice_beam=3.0)
+    assert ro.status == 0
+    parity.assert_same(ro, rg, lattice=True, tag="70k frames")
+    say("70k frames: cost", rg.cost, "tokens", rg.stats["tokens"], "lattice", rg.stats["lattice_kept"])
+
+
 def test_argument_errors(dec, torch_mod):
     g = W.Graph(2, np.array([0], np.int32), np.array([1], np.int32), np.array([3], np.int32),
                 np.array([0], np.int32), np.array([1.0], np.float32))
