@@ -149,38 +149,83 @@ def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str):
     print(COUNTERS)
 
 
-def cpu_baseline(wl, max_seconds: float):
-    """The oracle as it stands, on host cores, over a bounded sample of the
-    same workload (whole utterances, one per thread)."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+# A GPU machine grants one process at most this many host threads, whatever the
+# affinity mask shows.
+HOST_THREAD_SHARE = 16
+
+
+def cpu_baseline(wl):
+    """The oracle as it stands, on the host cores, over the same workload:
+    every utterance, one oracle call per thread of a pool over the usable
+    cores, rate = decoded frames / wall seconds of the pool.  A batch
+    workload also gets a one-core rate over its first four utterances (run
+    one after another), so the figure can be scaled per core."""
     import oracle
     oracle.build()
-    cores = len(os.sched_getaffinity(0))
-    cores = max(1, min(cores, 16))
+    visible = len(os.sched_getaffinity(0))
+    cores = max(1, min(visible, HOST_THREAD_SHARE))
     o = wl.opts
     g = wl.graph
     n_utt = len(wl.loglikes)
-    sample = list(range(min(n_utt, 3 * cores)))
-    if n_utt == 1:
-        sample = [0]
-    t0 = time.time()
-    with ThreadPoolExecutor(max_workers=cores) as ex:
-        res = list(ex.map(lambda u: oracle.decode(g, wl.loglikes[u], o.beam, o.max_active, o.lattice_beam,
-                                                  o.blank_threshold, o.blank_id, o.blank_ids,
-                                                  o.frame_stride), sample))
-    wall = time.time() - t0
+
+    def run(u):
+        return oracle.decode(g, wl.loglikes[u], o.beam, o.max_active, o.lattice_beam, o.blank_threshold,
+                             o.blank_id, o.blank_ids, o.frame_stride)
+
+    threads = min(cores, n_utt)
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        res = list(ex.map(run, range(n_utt)))
+    wall = time.perf_counter() - t0
     frames = sum(r.num_decoded for r in res)
-    busy = sum(r.seconds for r in res)
-    threads = min(cores, len(sample))
-    rate = frames / (busy / threads) if busy > 0 else None
-    return {
-        "value": rate,
+    out = {
+        "value": frames / wall,
         "unit": "frames/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": "%d whole utterance(s) (%d decoded frames) of the same workload, one oracle call per "
-                  "thread; rate = frames / (summed decode time / threads); wall %.1fs" % (
-                      len(sample), frames, wall),
+        "sample": "all %d utterance(s) of the workload (%d decoded frames), one oracle call per thread of a "
+                  "%d-thread pool, rate = decoded frames / wall seconds (%.2f s)" % (n_utt, frames, threads, wall),
+        "cpu_model": cpu_model(),
+        "cores_visible": visible,
     }
+    if n_utt > 1:
+        k = min(4, n_utt)
+        t0 = time.perf_counter()
+        one = [run(u) for u in range(k)]
+        w1 = time.perf_counter() - t0
+        out["one_core"] = {"value": sum(r.num_decoded for r in one) / w1, "unit": "frames/s",
+                           "sample": "utterances 0..%d one after another on one thread (%.2f s)" % (k - 1, w1)}
+    return out
+
+
+def copy_bandwidth(torch, mib: int = 2048, reps: int = 5):
+    """Achievable HBM bandwidth: a plain device-to-device copy of `mib` MiB,
+    timed with HIP events; bytes moved = read + write."""
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    torch.cuda.empty_cache()
+    return 2.0 * mib * (1 << 20) / (ms / 1e3) / 1e9
 
 
 def copy_calibration(torch, mib: int):
@@ -201,7 +246,6 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="cfg4", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=30.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0)
     ap.add_argument("--no-profile", action="store_true",
                     help="do not time kernel phases with HIP events")
@@ -253,13 +297,12 @@ def main():
     torch.cuda.synchronize()
     profile = not args.no_profile
     t0 = time.perf_counter()
-    all_res = []
+    res = None
     for i in range(args.steps):
-        all_res.append(step(profile))
+        res = step(profile)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / max(args.steps, 1)
-    res = all_res[-1]
     bad = [r.status for r in res if r.status != 0]
     if bad:
         log("warning: %d utterances without a path" % len(bad))
@@ -316,6 +359,7 @@ def main():
         dur_s = s0["search_span_ms"] / 1e3
         achieved = alg / dur_s / 1e9 if dur_s > 0 else None
         traffic = read_traffic()
+        copy_gbs = copy_bandwidth(torch)
         out["roofline"] = {
             "kernel": "search_kernel",
             "bound": "hbm",
@@ -323,6 +367,8 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS if achieved else None,
+            "copy_gbs": copy_gbs,
+            "frac_of_copy": achieved / copy_gbs if achieved and copy_gbs else None,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": alg,
             "avg_launch_us": dur_s * 1e6,
@@ -344,7 +390,7 @@ def main():
                                         "lattice_prune": round(crit["lattice_prune_ms"], 3)}
     if not args.no_cpu_baseline:
         log("oracle baseline ...")
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(out), flush=True)
 
 

@@ -174,29 +174,42 @@ int wfst_decode_batch(const wfst_graph *g, int32_t n_utt, const float *const *lo
                       const int32_t *T, int32_t L, const wfst_decode_opts *opts,
                       void *hip_stream, wfst_result **out_array);
 
-/* Status of the utterance: WFST_OK or WFST_ENOPATH. */
+/* Status of the utterance: WFST_OK, or WFST_ENOPATH when a token set of
+   the search (Alg. 1) became empty.  r == NULL: WFST_EINVAL. */
 int wfst_result_status(const wfst_result *r);
 
 /*
- * Best path: its cost (final cost included), final state, whether a final
- * state was reached (0 means the all-final fallback was used), and n arcs
- * in path order with, per arc, the original frame it consumed (-1 for
- * epsilon arcs).  Pointers stay valid until wfst_result_free.
+ * Best path, the output of finalTransition and backtrace (Alg. 1): its cost
+ * (final cost included), final state, whether a final state was reached (0
+ * means the all-final fallback was used), and n arcs in path order with,
+ * per arc, the original frame it consumed (-1 for epsilon arcs).  Any output
+ * pointer may be NULL.  Pointers stay valid until wfst_result_free.
+ * Errors: WFST_EINVAL (r == NULL), the utterance's status when it has no
+ * path.
  */
 int wfst_result_best(const wfst_result *r, float *cost, int32_t *final_state,
                      int32_t *reached_final, int32_t *n, const int32_t **arcs,
                      const int32_t **frames);
 
-/* Frame counts and, for each decoded frame j, the original frame index. */
+/*
+ * Frame counts of label-synchronous decoding (Sec. 2, Eq. 3): T, the number
+ * T' = T - |U| of decoded frames, and for each decoded frame j its original
+ * frame index (the frames left after removing the blank set U, Alg. 1),
+ * host memory owned by the result.  Any output pointer may be NULL.
+ * Errors: WFST_EINVAL (r == NULL).
+ */
 int wfst_result_frames(const wfst_result *r, int32_t *num_frames, int32_t *num_decoded,
                        const int32_t **orig_frame);
 
 /*
- * Lattice arc: `frame` is the token set j (0..T') holding the arc's source
- * (an emitting arc goes from token set j to j + 1 and consumed decoded frame
- * j; an epsilon arc stays inside token set j); `arc` is the user arc index;
- * `cost` is the best prefix cost through the arc; `extra` is how much the
- * best complete path through the arc costs above the best path.
+ * Lattice arc of the exact (state-level) lattice (Sec. 1, Sec. 3): `frame`
+ * is the token set j (0..T') holding the arc's source; the destination's
+ * token set follows from the arc's kind (an emitting arc goes from token set
+ * j to j + 1 and consumed decoded frame j; an epsilon arc stays inside token
+ * set j), so it is not stored; `arc` is the user arc index; `cost` is the
+ * best prefix cost through the arc; `extra` is how much the best complete
+ * path through the arc costs above the best path (the lattice beam keeps
+ * arcs whose extra is at most lattice_beam).  16 bytes, 4-byte aligned.
  */
 typedef struct wfst_lat_arc {
     int32_t frame;
@@ -205,18 +218,28 @@ typedef struct wfst_lat_arc {
     float extra;
 } wfst_lat_arc;
 
-/* Lattice-beam-pruned lattice, sorted by (frame, arc), in host memory: the
- * first call on any result of a batch copies the lattices of the whole batch
- * in one transfer, which the results share (valid while any of them lives).
- * n = 0 when the lattice was disabled. */
+/*
+ * Lattice-beam-pruned lattice (Sec. 1, Sec. 3), sorted by (frame, arc), in
+ * host memory owned by the results: the first call on any result of a batch
+ * copies the lattices of the whole batch in one transfer, which the results
+ * share (valid while any of them lives).  n = 0 and arcs = NULL when the
+ * lattice was disabled.  Errors: WFST_EINVAL (r == NULL), WFST_EDEVICE
+ * (copy failed).
+ */
 int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs);
 
-/* The same lattice in device memory (owned by the result). */
+/* The same lattice in device memory of the graph's device, owned by the
+   results of the batch (valid while any of them lives); arcs = NULL when
+   the lattice was disabled.  Errors: WFST_EINVAL (r == NULL). */
 int wfst_result_lattice_device(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs);
 
 /*
- * Token set j (0..T') sorted by state: states, float32 costs and
- * back-pointer arcs (-1 for the start token).  Needs WFST_RECORD_TOKENS.
+ * Token set S_j (j = 0..T'), the surviving tokens of token passing after
+ * decoded frame j (Sec. 3, Fig. 2; the beam search of Alg. 1), sorted by
+ * state: n states, their float32 costs and back-pointer arcs (the user arc
+ * of the recombination winner, -1 for the start token).  Host memory owned
+ * by the result.  Needs WFST_RECORD_TOKENS.  Errors: WFST_EINVAL (r == NULL,
+ * decoded without WFST_RECORD_TOKENS, j out of range).
  */
 int wfst_result_tokens(const wfst_result *r, int32_t j, int32_t *n, const int32_t **state,
                        const float **cost, const int32_t **bp_arc);
@@ -259,9 +282,56 @@ typedef struct wfst_stats {
     double search_span_ms;
 } wfst_stats;
 
+/* Counters and timings of the utterance's decode (the work measures of
+   Eq. 3: decoded frames, tokens and arcs expanded).  Errors: WFST_EINVAL. */
 int wfst_result_stats(const wfst_result *r, wfst_stats *stats);
 
+/* Release a result (NULL is allowed). */
 void wfst_result_free(wfst_result *r);
+
+/*
+ * Test and debugging switches, process-wide (for the test suite, not for
+ * production use).  They force the decoder's rarely taken paths on small
+ * inputs and change the order of its parallel work; the results must not
+ * depend on them, except that fail_lattice_alloc makes decodes fail.  A zero
+ * field keeps the library's default; a positive fill or capacity is used only
+ * when it is below the default.
+ *
+ *   lds_fill           states per frame the search's LDS token table takes
+ *                      before the frame is redone with the table in device
+ *                      memory
+ *   queue_cap          epsilon items per wave queue in LDS before items spill
+ *                      to device memory
+ *   record_fill        survivors per token set that the record pass handles
+ *                      with its LDS table (larger sets go to the large-set
+ *                      pass)
+ *   record_big_fill    the same for the large-set pass (larger sets use a
+ *                      device-memory table)
+ *   lattice_lds        survivors per token set that lattice pruning keeps in
+ *                      LDS; -1 keeps none (every set in device memory)
+ *   permute            nonzero: hash the token tables with another multiplier
+ *                      and expand the arc chunks of a token set in reverse
+ *                      order, so that slots, claim order, survivor order and
+ *                      the order of every atomic differ
+ *   fail_lattice_alloc nonzero: the allocation of the lattice output fails,
+ *                      as when device memory is exhausted: the decode returns
+ *                      WFST_ENOMEM before launching anything that writes it
+ *
+ * opts == NULL restores every default.  Takes effect for decodes started
+ * after the call returns.  Errors: WFST_EINVAL for a negative field other
+ * than lattice_lds = -1.
+ */
+typedef struct wfst_debug_opts {
+    int32_t lds_fill;
+    int32_t queue_cap;
+    int32_t record_fill;
+    int32_t record_big_fill;
+    int32_t lattice_lds;
+    int32_t permute;
+    int32_t fail_lattice_alloc;
+} wfst_debug_opts;
+
+int wfst_set_debug_opts(const wfst_debug_opts *opts);
 
 /* Message for the last error raised on the calling thread ("" if none). */
 const char *wfst_last_error(void);

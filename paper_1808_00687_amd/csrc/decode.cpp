@@ -52,6 +52,96 @@ struct LatHost {
     std::vector<wfst_lat_arc> arcs;
 };
 
+// Lattice output buffers.  The results of a batch share one buffer; when the
+// last of them is freed the buffer returns to a small per-device pool, so a
+// steady sequence of decodes allocates no lattice memory.
+constexpr int kLatPoolKeep = 4;
+
+struct LatPool {
+    std::mutex mu;
+    std::vector<std::pair<size_t, void *>> free_bufs[64];
+};
+
+LatPool &lat_pool()
+{
+    static LatPool *p = new LatPool();
+    return *p;
+}
+
+struct LatBuf {
+    void *p = nullptr;
+    size_t bytes = 0;
+    int device = 0;
+    LatBuf() = default;
+    LatBuf(const LatBuf &) = delete;
+    LatBuf &operator=(const LatBuf &) = delete;
+    ~LatBuf()
+    {
+        if (!p) return;
+        void *drop = nullptr;
+        if (device >= 0 && device < 64) {
+            LatPool &pool = lat_pool();
+            std::lock_guard<std::mutex> lk(pool.mu);
+            auto &fl = pool.free_bufs[device];
+            fl.emplace_back(bytes, p);
+            if (static_cast<int>(fl.size()) > kLatPoolKeep) {
+                // keep the largest buffers
+                auto it = std::min_element(fl.begin(), fl.end());
+                drop = it->second;
+                fl.erase(it);
+            }
+        } else {
+            drop = p;
+        }
+        if (drop) {
+            int cur = 0;
+            (void)hipGetDevice(&cur);
+            if (cur != device) (void)hipSetDevice(device);
+            (void)hipFree(drop);
+            if (cur != device) (void)hipSetDevice(cur);
+        }
+    }
+};
+
+// A lattice output buffer of at least `need` bytes on the current device:
+// the smallest pooled one that fits, else a new allocation.
+hipError_t lat_take(int device, size_t need, bool fail, std::shared_ptr<LatBuf> &out)
+{
+    if (fail) return hipErrorOutOfMemory;
+    auto b = std::make_shared<LatBuf>();
+    b->device = device;
+    if (device >= 0 && device < 64) {
+        LatPool &pool = lat_pool();
+        std::lock_guard<std::mutex> lk(pool.mu);
+        auto &fl = pool.free_bufs[device];
+        int best = -1;
+        for (int i = 0; i < static_cast<int>(fl.size()); i++)
+            if (fl[i].first >= need && (best < 0 || fl[i].first < fl[best].first)) best = i;
+        if (best >= 0) {
+            b->bytes = fl[best].first;
+            b->p = fl[best].second;
+            fl.erase(fl.begin() + best);
+            out = b;
+            return hipSuccess;
+        }
+    }
+    const size_t want = std::max<size_t>(need + need / 4, size_t{1} << 20);
+    hipError_t e = hipMalloc(&b->p, want);
+    if (e != hipSuccess) {
+        b->p = nullptr;
+        e = hipMalloc(&b->p, need);
+        if (e != hipSuccess) {
+            b->p = nullptr;
+            return e;
+        }
+        b->bytes = need;
+    } else {
+        b->bytes = want;
+    }
+    out = b;
+    return hipSuccess;
+}
+
 }  // namespace
 
 struct wfst_result {
@@ -61,7 +151,7 @@ struct wfst_result {
     int32_t reached_final = 0;
     std::vector<int32_t> path_arcs, path_frames, kept;
     int32_t T = 0, Tp = 0;
-    std::shared_ptr<DevBuf> lat_dev;
+    std::shared_ptr<LatBuf> lat_dev;
     int64_t lat_off = 0, lat_n = 0;
     std::shared_ptr<LatHost> lat_host;   // the batch's lattice in host memory, copied on first use
     bool has_tokens = false;
@@ -181,14 +271,27 @@ struct ArenaLease {
     }
 };
 
-int test_env_int(const char *name, int dflt)
+// Test and debugging switches (wfst_set_debug_opts), process-wide.
+struct DebugState {
+    std::mutex mu;
+    wfst_debug_opts o{};
+};
+
+DebugState &debug_state()
 {
-    // test hooks: small values force the overflow paths of the search
-    const char *v = getenv(name);
-    if (!v) return dflt;
-    const int x = atoi(v);
-    return x >= 1 && x < dflt ? x : dflt;
+    static DebugState *d = new DebugState();
+    return *d;
 }
+
+wfst_debug_opts debug_snapshot()
+{
+    DebugState &d = debug_state();
+    std::lock_guard<std::mutex> lk(d.mu);
+    return d.o;
+}
+
+// A positive override below the default replaces it.
+int limit_or(int32_t v, int dflt) { return v >= 1 && v < dflt ? v : dflt; }
 
 struct Sizes {
     int64_t capA;      // tokens per frame on average over an utterance
@@ -301,11 +404,112 @@ hipStream_t aux_stream(int dev, int i)
     return tab[dev][i];
 }
 
+// Element counts of the workspace regions summed over a batch.
+struct Totals {
+    int64_t sv = 0, le = 0, lx = 0, fo = 0, kp = 0, pa = 0;
+};
+
+// Regions of one utterance of Tu frames, appended after those in `tot`.
+void layout_utt(int64_t Tu, const Sizes &z, bool lattice, int depth, Totals &tot, UttLayout &l)
+{
+    l.sv0 = tot.sv;
+    // survivor indices are 32-bit; one frame may reach capF tokens
+    l.svcap = std::min<int64_t>((Tu + 1) * z.capA + z.capF, std::numeric_limits<int32_t>::max());
+    tot.sv += l.svcap;
+    // a set's emitting region holds one candidate (and one lattice record)
+    // per emitting out-arc of its tokens, its epsilon region one lattice
+    // record per epsilon out-arc
+    l.le0 = tot.le;
+    l.lecap = (Tu * z.capA + z.capF) * z.em;
+    tot.le += l.lecap;
+    l.lx0 = tot.lx;
+    l.lxcap = lattice ? ((Tu + 1) * z.capA + z.capF) * z.xm : 0;
+    tot.lx += l.lxcap;
+    l.fo0 = tot.fo;
+    tot.fo += Tu + 2;
+    l.kept0 = tot.kp;
+    tot.kp += std::max<int64_t>(Tu, 1);
+    l.path0 = tot.pa;
+    l.pathcap = (Tu + 1) * (depth + 1) + 1;
+    tot.pa += l.pathcap;
+    l.lo0 = 0;
+}
+
+// Option-derived kernel parameters shared by every decode entry point.
+void set_params(Params &p, const Graph &G, int U, int L, const wfst_decode_opts &o, float thr,
+                const wfst_debug_opts &dbg, const Sizes &z, int n_blank)
+{
+    p.g = G.d;
+    p.U = U;
+    p.L = L;
+    p.beam = o.beam;
+    p.max_active = o.max_active;
+    p.lattice_beam = o.lattice_beam;
+    p.lattice = o.lattice_beam >= 0.0f ? 1 : 0;
+    p.n_blank = n_blank;
+    p.frame_stride = std::max(1, o.frame_stride);
+    p.blank_thr = thr;
+    p.lds_fill = limit_or(dbg.lds_fill, 1 << 30);
+    p.gen_lds = limit_or(dbg.queue_cap, 1 << 30);
+    p.profile = (o.flags & WFST_PROFILE_STEPS) ? 1 : 0;
+    p.rec_fill = limit_or(dbg.record_fill, 1 << 30);
+    p.rec_big_fill = limit_or(dbg.record_big_fill, 1 << 30);
+    p.lat_lds = dbg.lattice_lds < 0 ? 0 : limit_or(dbg.lattice_lds, 1 << 30);
+    p.hash_mul = dbg.permute ? kHashMulAlt : kHashMul;
+    p.reverse = dbg.permute ? 1 : 0;
+    p.capG = 8192;
+    while (p.capG < z.capT) p.capG *= 2;
+    p.capO = z.capO;
+}
+
+// Carve every workspace buffer of U utterances with the region totals
+// `tot` from the arena (a measuring arena only adds up the size).  The
+// per-frame offset arrays come from *fo_all (7 arrays of tot.fo entries).
+void carve_ws(Arena &a, Params &p, int U, const Totals &tot, UttLayout **d_lay, int64_t **fo_all)
+{
+    const bool lattice = p.lattice != 0;
+    p.st = a.get<UttState>(U);
+    *d_lay = a.get<UttLayout>(U);
+    p.lay = *d_lay;
+    p.gkeys = a.get<uint32_t>(U * p.capG);
+    p.gvals = a.get<unsigned long long>(U * p.capG);
+    p.gslots = a.get<int32_t>(U * p.capG);
+    p.gspill = a.get<uint2>(U * 2 * p.capO);
+    p.sv_state = a.get<int32_t>(tot.sv);
+    p.sv_tok = a.get<uint64_t>(tot.sv);
+    p.sv_prev = a.get<int32_t>(tot.sv);
+    p.sv_ebeg = a.get<int32_t>(tot.sv);
+    p.sv_epre = a.get<int32_t>(tot.sv);
+    p.sv_x = a.get<int4>(tot.sv);
+    p.cand = a.get<int4>(tot.le);
+    p.e_key = lattice ? a.get<uint32_t>(tot.sv) : nullptr;
+    p.lat_e = lattice ? a.get<int4>(tot.le) : nullptr;
+    p.lat_x = lattice ? a.get<int4>(tot.lx) : nullptr;
+    p.ex_e = lattice ? a.get<float>(tot.le) : nullptr;
+    p.ex_x = lattice ? a.get<float>(tot.lx) : nullptr;
+    *fo_all = a.get<int64_t>(7 * tot.fo);
+    p.blank_ids = a.get<int32_t>(p.n_blank);
+    p.cut_arr = a.get<uint32_t>(tot.fo);
+    p.kept = a.get<int32_t>(tot.kp);
+    p.path_arc = a.get<int32_t>(tot.pa);
+    p.path_frame = a.get<int32_t>(tot.pa);
+    p.path_packed = a.get<int2>(tot.pa);
+    const int64_t fo = tot.fo;
+    int64_t *f = *fo_all;
+    p.sv_off = f;
+    p.le_off = f ? f + fo : nullptr;
+    p.lx_off = f ? f + 2 * fo : nullptr;
+    p.lo_off = f ? f + 3 * fo : nullptr;
+    p.le_cnt = f ? f + 4 * fo : nullptr;
+    p.lx_cnt = f ? f + 5 * fo : nullptr;
+    p.cand_cnt = f ? f + 6 * fo : nullptr;
+}
+
 // One attempt at decoding the batch with the given buffer sizes.  Returns
 // WFST_OK, an error, or WFST_ECAPACITY when a buffer overflowed.
 int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T_in, int L,
               const wfst_decode_opts &o, float thr, hipStream_t s, const Sizes &z,
-              std::vector<wfst_result *> &out_in, double t_start)
+              std::vector<wfst_result *> &out_in, double t_start, const wfst_debug_opts &dbg)
 {
     // Utterances in order of length: a group of similar lengths runs its
     // search, record and final passes on a stream of its own, so a group of
@@ -324,7 +528,6 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     }
     const float *const *ll = ll_v.data();
     const int32_t *T = T_v.data();
-    const int64_t N = G.d.n;
     const bool lattice = o.lattice_beam >= 0.0f;
     const int depth = G.eps_depth;
     Timer tm;
@@ -332,91 +535,21 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     tm.dev = G.device;
 
     std::vector<UttLayout> lay(U);
-    int64_t sv = 0, le = 0, lx = 0, fo = 0, kp = 0, pa = 0;
-    for (int u = 0; u < U; u++) {
-        UttLayout &l = lay[u];
-        const int64_t Tu = T[u];
-        l.sv0 = sv;
-        // survivor indices are 32-bit; one frame may reach capF tokens
-        l.svcap = std::min<int64_t>((Tu + 1) * z.capA + z.capF, std::numeric_limits<int32_t>::max());
-        sv += l.svcap;
-        // a set's emitting region holds one candidate (and one lattice record)
-        // per emitting out-arc of its tokens, its epsilon region one lattice
-        // record per epsilon out-arc
-        l.le0 = le;
-        l.lecap = (Tu * z.capA + z.capF) * z.em;
-        le += l.lecap;
-        l.lx0 = lx;
-        l.lxcap = lattice ? ((Tu + 1) * z.capA + z.capF) * z.xm : 0;
-        lx += l.lxcap;
-        l.fo0 = fo;
-        fo += Tu + 2;
-        l.kept0 = kp;
-        kp += std::max<int64_t>(Tu, 1);
-        l.path0 = pa;
-        l.pathcap = (Tu + 1) * (depth + 1) + 1;
-        pa += l.pathcap;
-        l.lo0 = 0;
-    }
+    Totals tot;
+    for (int u = 0; u < U; u++) layout_utt(T[u], z, lattice, depth, tot, lay[u]);
+    const int64_t fo = tot.fo, kp = tot.kp;
 
-    Params p{};
-    p.g = G.d;
-    p.U = U;
-    p.L = L;
-    p.beam = o.beam;
-    p.max_active = o.max_active;
-    p.lattice_beam = o.lattice_beam;
-    p.lattice = lattice ? 1 : 0;
     // the blank-like units: the set when given, else the single blank unit
     std::vector<int32_t> blank_h;
     if (o.num_blank_ids > 0) blank_h.assign(o.blank_ids, o.blank_ids + o.num_blank_ids);
     else blank_h.push_back(o.blank_id);
-    p.n_blank = static_cast<int32_t>(blank_h.size());
-    p.frame_stride = std::max(1, o.frame_stride);
-    p.blank_thr = thr;
-    p.lds_fill = test_env_int("WFSTDEC_TEST_LDS_FILL", 1 << 30);
-    p.gen_lds = test_env_int("WFSTDEC_TEST_QUEUE_CAP", 1 << 30);
-    p.profile = (o.flags & WFST_PROFILE_STEPS) ? 1 : 0;
-    p.rec_fill = test_env_int("WFSTDEC_TEST_RECORD_FILL", 1 << 30);
-    p.rec_big_fill = test_env_int("WFSTDEC_TEST_RECORD_BIG_FILL", 1 << 30);
-    p.lat_lds = test_env_int("WFSTDEC_TEST_LATTICE_LDS", 1 << 30);
-    p.capO = z.capO;
+    Params p{};
+    set_params(p, G, U, L, o, thr, dbg, z, static_cast<int32_t>(blank_h.size()));
     WallTrace wt;
     UttLayout *d_lay = nullptr;
     int64_t *fo_all = nullptr;
-    auto carve = [&](Arena &a) {
-        p.st = a.get<UttState>(U);
-        d_lay = a.get<UttLayout>(U);
-        p.lay = d_lay;
-        p.gkeys = a.get<uint32_t>(U * p.capG);
-        p.gvals = a.get<unsigned long long>(U * p.capG);
-        p.gslots = a.get<int32_t>(U * p.capG);
-        p.gspill = a.get<uint2>(U * 2 * p.capO);
-        p.sv_state = a.get<int32_t>(sv);
-        p.sv_tok = a.get<uint64_t>(sv);
-        p.sv_prev = a.get<int32_t>(sv);
-        p.sv_ebeg = a.get<int32_t>(sv);
-        p.sv_epre = a.get<int32_t>(sv);
-        p.sv_x = a.get<int4>(sv);
-        p.cand = a.get<int4>(le);
-        p.e_key = lattice ? a.get<uint32_t>(sv) : nullptr;
-        p.lat_e = lattice ? a.get<int4>(le) : nullptr;
-        p.lat_x = lattice ? a.get<int4>(lx) : nullptr;
-        p.ex_e = lattice ? a.get<float>(le) : nullptr;
-        p.ex_x = lattice ? a.get<float>(lx) : nullptr;
-        fo_all = a.get<int64_t>(7 * fo);
-        p.blank_ids = a.get<int32_t>(p.n_blank);
-        p.cut_arr = a.get<uint32_t>(fo);
-        p.kept = a.get<int32_t>(kp);
-        p.path_arc = a.get<int32_t>(pa);
-        p.path_frame = a.get<int32_t>(pa);
-        p.path_packed = a.get<int2>(pa);
-    };
-    p.capG = 8192;
-    while (p.capG < z.capT) p.capG *= 2;
-    p.capO = z.capO;
     Arena measure;
-    carve(measure);
+    carve_ws(measure, p, U, tot, &d_lay, &fo_all);
     ArenaLease lease;
     {
         const hipError_t ae = lease.acquire(G.device, measure.off);
@@ -427,21 +560,14 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     }
     Arena arena;
     arena.base = static_cast<char *>(lease.ptr);
-    carve(arena);
+    carve_ws(arena, p, U, tot, &d_lay, &fo_all);
     wt.mark("allocate");
     if (wt.on) {
         const double gib = 1.0 / (1024.0 * 1024.0 * 1024.0);
         fprintf(stderr, "[wfstdec] workspace %.2f GiB: survivors %.2f, emitting regions %.2f, epsilon regions %.2f\n",
-                measure.off * gib, sv * (lattice ? 44.0 : 40.0) * gib, le * (lattice ? 36.0 : 16.0) * gib,
-                lx * 20.0 * gib);
+                measure.off * gib, tot.sv * (lattice ? 44.0 : 40.0) * gib, tot.le * (lattice ? 36.0 : 16.0) * gib,
+                tot.lx * 20.0 * gib);
     }
-    p.sv_off = fo_all;
-    p.le_off = fo_all + fo;
-    p.lx_off = fo_all + 2 * fo;
-    p.lo_off = fo_all + 3 * fo;
-    p.le_cnt = fo_all + 4 * fo;
-    p.lx_cnt = fo_all + 5 * fo;
-    p.cand_cnt = fo_all + 6 * fo;
 
     std::vector<UttState> st(U);
     for (int u = 0; u < U; u++) {
@@ -455,7 +581,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     };
     chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
-    chk(hipMemsetAsync(fo_all, 0, 7 * fo * sizeof(int64_t), s));
+    chk(launch_zero(fo_all, 7 * fo * sizeof(int64_t), s));
     chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), blank_h.data(), blank_h.size() * sizeof(int32_t),
                        hipMemcpyHostToDevice, s));
     chk(launch_classify(p, s));
@@ -545,7 +671,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     for (int u = 0; u < U; u++)
         if (st[u].status == WFST_ECAPACITY) return WFST_ECAPACITY;
 
-    std::shared_ptr<DevBuf> lat_buf;
+    std::shared_ptr<LatBuf> lat_buf;
     std::shared_ptr<LatHost> lat_host;
     if (lattice) {
         int64_t tot = 0;
@@ -555,9 +681,10 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         }
         lat_host = std::make_shared<LatHost>();
         lat_host->total = tot;
-        lat_buf = std::make_shared<DevBuf>();
-        (void)hipGetDevice(&lat_buf->device);
-        chk(hipMalloc(&lat_buf->p, static_cast<size_t>(std::max<int64_t>(tot, 1)) * sizeof(int4)));
+        // every stream is idle here: on failure nothing is left running
+        const hipError_t le = lat_take(G.device, static_cast<size_t>(std::max<int64_t>(tot, 1)) * sizeof(int4),
+                                       dbg.fail_lattice_alloc != 0, lat_buf);
+        if (le != hipSuccess) return hip_fail(le, "decode: lattice output allocation");
         p.lat_out = static_cast<int4 *>(lat_buf->p);
         chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
         tm.start(s);
@@ -709,17 +836,40 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     return WFST_OK;
 }
 
-int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglikes, const int32_t *T,
-                int32_t L, const wfst_decode_opts *opts, void *hip_stream, wfst_result **out_array)
+std::atomic<int64_t> &learned_capA()
 {
-    clear_error();
-    const double t0 = std::chrono::duration<double, std::milli>(
-                          std::chrono::steady_clock::now().time_since_epoch()).count();
-    if (!gh || !opts || !out_array || !T || !loglikes) return fail(WFST_EINVAL, "decode: NULL argument");
-    if (n_utt < 1) return fail(WFST_EINVAL, "decode: n_utt must be >= 1");
-    for (int u = 0; u < n_utt; u++) out_array[u] = nullptr;
-    const Graph &G = gh->g;
-    const wfst_decode_opts o = *opts;
+    static std::atomic<int64_t> a{2048};
+    return a;
+}
+
+// Buffer sizes before anything is learned from earlier decodes (capA, the
+// average tokens per frame, is left to the caller).
+Sizes initial_sizes(const Graph &G, const wfst_decode_opts &o)
+{
+    const int64_t N = G.d.n;
+    Sizes z{};
+    if (o.capacity_hint > 0) z.capF = std::min<int64_t>(o.capacity_hint, N);
+    else if (o.max_active > 0) z.capF = std::min<int64_t>(N, o.max_active + o.max_active / 4 + 256);
+    else z.capF = std::min<int64_t>(N, 65536);
+    z.capT = std::min<int64_t>(N, std::max<int64_t>(16 * z.capF, 4096));
+    // epsilon items of one generation are bounded by the candidates that
+    // produce them
+    const int64_t E = G.d.e;
+    z.capO = std::min<int64_t>(E + 1, std::max<int64_t>(2 * z.capT, 65536));
+    // lattice-record slots per token: what the last decodes on this graph
+    // needed, else twice the graph's mean out-degrees
+    z.em = G.rec_em.load();
+    z.xm = G.rec_xm.load();
+    if (z.em <= 0) z.em = std::max<int64_t>(2, 2 * G.d.n_emit / std::max<int64_t>(N, 1) + 1);
+    if (z.xm <= 0) z.xm = std::max<int64_t>(1, 2 * G.d.n_eps / std::max<int64_t>(N, 1) + 1);
+    z.capA = 0;
+    return z;
+}
+
+// Checks of the decode options shared by every entry point; on success *thr
+// is the log-domain blank threshold.
+int check_opts(const Graph &G, const wfst_decode_opts &o, int32_t L, float *thr)
+{
     if (!(o.beam > 0.0f)) return fail(WFST_EINVAL, "decode: beam must be > 0");
     if (std::isnan(o.lattice_beam)) return fail(WFST_EINVAL, "decode: lattice_beam is NaN");
     if (!(o.blank_threshold > 0.0f)) return fail(WFST_EINVAL, "decode: blank_threshold must be > 0");
@@ -731,12 +881,32 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
         if (o.blank_ids[i] < 0 || o.blank_ids[i] >= L) return fail(WFST_EINVAL, "decode: blank unit out of range");
     if (o.frame_stride < 0) return fail(WFST_EINVAL, "decode: negative frame_stride");
     if (o.capacity_hint < 0) return fail(WFST_EINVAL, "decode: negative capacity_hint");
+    *thr = o.blank_threshold > 1.0f ? std::numeric_limits<float>::infinity()
+                                    : static_cast<float>(std::log(static_cast<double>(o.blank_threshold)));
+    return WFST_OK;
+}
+
+int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglikes, const int32_t *T,
+                int32_t L, const wfst_decode_opts *opts, void *hip_stream, wfst_result **out_array)
+{
+    clear_error();
+    const double t0 = std::chrono::duration<double, std::milli>(
+                          std::chrono::steady_clock::now().time_since_epoch()).count();
+    if (!gh || !opts || !out_array || !T || !loglikes) return fail(WFST_EINVAL, "decode: NULL argument");
+    if (n_utt < 1) return fail(WFST_EINVAL, "decode: n_utt must be >= 1");
+    for (int u = 0; u < n_utt; u++) out_array[u] = nullptr;
+    const Graph &G = gh->g;
+    const wfst_decode_opts o = *opts;
+    const wfst_debug_opts dbg = debug_snapshot();
+    float thr = 0.0f;
+    {
+        const int rc0 = check_opts(G, o, L, &thr);
+        if (rc0 != WFST_OK) return rc0;
+    }
     for (int u = 0; u < n_utt; u++) {
         if (T[u] < 0) return fail(WFST_EINVAL, "decode: negative T");
         if (T[u] > 0 && !loglikes[u]) return fail(WFST_EINVAL, "decode: NULL loglikes");
     }
-    const float thr = o.blank_threshold > 1.0f ? std::numeric_limits<float>::infinity()
-                                               : static_cast<float>(std::log(static_cast<double>(o.blank_threshold)));
 
     DeviceGuard dg(G.device);
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
@@ -768,24 +938,10 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
         }
     }
     const int64_t N = G.d.n;
-    Sizes z;
-    if (o.capacity_hint > 0) z.capF = std::min<int64_t>(o.capacity_hint, N);
-    else if (o.max_active > 0) z.capF = std::min<int64_t>(N, o.max_active + o.max_active / 4 + 256);
-    else z.capF = std::min<int64_t>(N, 65536);
-    z.capT = std::min<int64_t>(N, std::max<int64_t>(16 * z.capF, 4096));
-    // epsilon items of one generation are bounded by the candidates that
-    // produce them
     const int64_t E = G.d.e;
-    z.capO = std::min<int64_t>(E + 1, std::max<int64_t>(2 * z.capT, 65536));
-    // lattice-record slots per token: what the last decodes on this graph
-    // needed, else twice the graph's mean out-degrees
-    z.em = G.rec_em.load();
-    z.xm = G.rec_xm.load();
-    if (z.em <= 0) z.em = std::max<int64_t>(2, 2 * G.d.n_emit / std::max<int64_t>(N, 1) + 1);
-    if (z.xm <= 0) z.xm = std::max<int64_t>(1, 2 * G.d.n_eps / std::max<int64_t>(N, 1) + 1);
+    Sizes z = initial_sizes(G, o);
     // average tokens per frame: start from what the last calls needed
-    static std::atomic<int64_t> learned_capA{2048};
-    z.capA = std::min<int64_t>(z.capF, learned_capA.load());
+    z.capA = std::min<int64_t>(z.capF, learned_capA().load());
     int rc = WFST_ECAPACITY;
     for (int attempt = 0; attempt < 8 && rc == WFST_ECAPACITY; attempt++) {
         if (attempt) {
@@ -800,11 +956,11 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
             z.em *= 2;
             z.xm *= 2;
         }
-        rc = run_batch(G, n_utt, ll.data(), T, L, o, thr, s, z, res, t0);
+        rc = run_batch(G, n_utt, ll.data(), T, L, o, thr, s, z, res, t0, dbg);
     }
     if (rc == WFST_OK) {
-        int64_t cur = learned_capA.load();
-        while (z.capA > cur && !learned_capA.compare_exchange_weak(cur, z.capA)) {
+        int64_t cur = learned_capA().load();
+        while (z.capA > cur && !learned_capA().compare_exchange_weak(cur, z.capA)) {
         }
         // the slots per token this batch needed, with a margin
         int64_t em = 1, xm = 1;
@@ -960,3 +1116,19 @@ extern "C" int wfst_result_stats(const wfst_result *r, wfst_stats *stats)
 }
 
 extern "C" void wfst_result_free(wfst_result *r) { delete r; }
+
+extern "C" int wfst_set_debug_opts(const wfst_debug_opts *opts)
+{
+    clear_error();
+    wfst_debug_opts o{};
+    if (opts) {
+        o = *opts;
+        if (o.lds_fill < 0 || o.queue_cap < 0 || o.record_fill < 0 || o.record_big_fill < 0 ||
+            o.lattice_lds < -1 || o.permute < 0 || o.fail_lattice_alloc < 0)
+            return fail(WFST_EINVAL, "wfst_set_debug_opts: negative field");
+    }
+    DebugState &d = debug_state();
+    std::lock_guard<std::mutex> lk(d.mu);
+    d.o = o;
+    return WFST_OK;
+}

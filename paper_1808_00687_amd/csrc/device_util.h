@@ -61,7 +61,18 @@ __device__ __forceinline__ T ldg(const T *ptr)
 
 // Multiplicative hash of a state id for the open-addressing tables (the
 // high bits index the table).
-__device__ __forceinline__ uint32_t hash_state(uint32_t d) { return d * 0x9E3779B1u; }
+__device__ __forceinline__ uint32_t hash_state(uint32_t d, uint32_t mul) { return d * mul; }
+
+// Order LDS stores of some lanes of a wave before loads of the same
+// locations by other lanes of the wave: to the compiler such a hand-over is
+// a data race unless fenced, and it may serve a lane's load from that lane's
+// own earlier store.
+__device__ __forceinline__ void wave_lds_handover()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 __device__ __forceinline__ int lane_id() { return static_cast<int>(__lane_id()); }
 

@@ -1,6 +1,8 @@
 // End-of-utterance kernels: finalTransition and backtrace (Alg. 1 of the
 // paper), lattice-beam pruning of the recorded lattice (the backward pass of
 // exact lattice generation, Sec. 1 and Sec. 3), and the sorted lattice output.
+#include <algorithm>
+
 #include "device_util.h"
 
 namespace wfd {
@@ -645,7 +647,30 @@ __global__ __launch_bounds__(1024) void pack_paths_kernel(Params p)
     }
 }
 
+// Zero a buffer (a kernel rather than a memset node, so the decode's
+// enqueued work is kernels and copies only).
+__global__ __launch_bounds__(256) void zero_kernel(uint4 *p, int64_t n16, uint32_t *tail, int ntail)
+{
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16; i += stride)
+        p[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0u;
+}
+
 }  // namespace
+
+hipError_t launch_zero(void *ptr, size_t bytes, hipStream_t s)
+{
+    // ptr is 256-byte aligned (arena carving) and bytes a multiple of 4
+    if (bytes == 0) return hipSuccess;
+    const int64_t n16 = static_cast<int64_t>(bytes / 16);
+    const int ntail = static_cast<int>((bytes % 16) / 4);
+    uint32_t *tail = reinterpret_cast<uint32_t *>(static_cast<char *>(ptr) + n16 * 16);
+    const int64_t blocks = std::min<int64_t>(std::max<int64_t>((n16 + 255) / 256, 1), 1024);
+    hipLaunchKernelGGL(zero_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, static_cast<uint4 *>(ptr),
+                       n16, tail, ntail);
+    return hipGetLastError();
+}
 
 hipError_t launch_final(const Params &p, hipStream_t s)
 {

@@ -12,21 +12,21 @@
 
 namespace wfd {
 
-static thread_local std::string g_err;
+// The calling thread's last error message, in a fixed buffer (setting it
+// allocates nothing).
+static thread_local char g_err[512];
 
 void set_error(const char *fmt, ...)
 {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof(buf), fmt, ap);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
     va_end(ap);
-    g_err = buf;
 }
 
-void clear_error() { g_err.clear(); }
+void clear_error() { g_err[0] = '\0'; }
 
-const char *last_error() { return g_err.c_str(); }
+const char *last_error() { return g_err; }
 
 }  // namespace wfd
 

@@ -38,6 +38,10 @@ constexpr uint32_t kDstMask = 0x7FFFFFFFu;
 constexpr int kHistBits = 12;               // radix-select digit width
 constexpr int kHistBins = 1 << kHistBits;   // bins per utterance histogram
 constexpr int kWave = 64;                   // gfx950 wavefront
+// Multipliers of the state hash of the token tables (odd, so the map is a
+// bijection); the second one is the debugging permutation.
+constexpr uint32_t kHashMul = 0x9E3779B1u;
+constexpr uint32_t kHashMulAlt = 0x85EBCA77u;
 
 struct DevGraph {
     int32_t n;
@@ -137,6 +141,8 @@ struct Params {
     int32_t rec_fill;         // survivors per set the record kernel's LDS table takes (<= its fill limit)
     int32_t rec_big_fill;     // the same for the large-set pass's LDS table
     int32_t lat_lds;          // survivors per set the lattice backward pass keeps in LDS (<= its capacity)
+    uint32_t hash_mul;        // state hash multiplier of the token tables
+    int32_t reverse;          // expand a set's arc chunks last to first (a debugging permutation)
     UttState *st;
     const UttLayout *lay;
     // survivors (per utterance regions)
@@ -187,6 +193,7 @@ hipError_t launch_record(const Params &p, int max_frames, hipStream_t s);
 hipError_t launch_finish(const Params &p, hipStream_t s);
 hipError_t launch_pack_paths(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
+hipError_t launch_zero(void *ptr, size_t bytes, hipStream_t s);   // ptr 16-byte aligned, bytes % 4 == 0
 
 // ---- host helpers (graph.cpp) ----
 void set_error(const char *fmt, ...);

@@ -40,6 +40,7 @@ struct RTab {
     int32_t *vals;
     uint32_t mask;
     int shift;   // 32 - log2(slots)
+    uint32_t mul;   // hash multiplier
 };
 
 template <bool G, typename T>
@@ -54,7 +55,7 @@ __device__ __forceinline__ T rld(const T *ptr)
 template <bool G>
 __device__ __forceinline__ void rt_insert(const RTab<G> &t, uint32_t s, int32_t v)
 {
-    uint32_t h = hash_state(s) >> t.shift;
+    uint32_t h = hash_state(s, t.mul) >> t.shift;
     // survivor states are distinct: the first free slot on the probe path is s's
     while (atomicCAS(t.keys + h, kEmptyKey, s) != kEmptyKey) h = (h + 1) & t.mask;
     t.vals[h] = v;
@@ -63,7 +64,7 @@ __device__ __forceinline__ void rt_insert(const RTab<G> &t, uint32_t s, int32_t 
 template <bool G>
 __device__ __forceinline__ int32_t rt_find(const RTab<G> &t, uint32_t s)
 {
-    uint32_t h = hash_state(s) >> t.shift;
+    uint32_t h = hash_state(s, t.mul) >> t.shift;
     for (uint32_t probe = 0; probe <= t.mask; probe++) {
         const uint32_t k = rld<G>(t.keys + h);
         if (k == s) return rld<G>(t.vals + h);
@@ -232,6 +233,7 @@ __global__ __launch_bounds__(kRT) void record_kernel(Params p)
     t.vals = s_vals;
     t.mask = (1u << bits) - 1u;
     t.shift = 32 - bits;
+    t.mul = p.hash_mul;
     for (int i = threadIdx.x; i < (1 << bits); i += blockDim.x) s_keys[i] = kEmptyKey;
     __syncthreads();
     record_set<false>(p, u, k, t, sh);
@@ -264,6 +266,7 @@ __global__ __launch_bounds__(kRT) void record_large_kernel(Params p)
     gt.vals = p.gslots + gbase;
     gt.mask = static_cast<uint32_t>(p.capG - 1);
     gt.shift = 32 - (31 - __clz(static_cast<int>(p.capG)));
+    gt.mul = p.hash_mul;
     const int big_fill = min(kRBigFill, p.rec_big_fill);
     // the large sets, kRT frames at a time
     for (int k0 = 0; k0 <= st.Tp; k0 += kRT) {
@@ -286,6 +289,7 @@ __global__ __launch_bounds__(kRT) void record_large_kernel(Params p)
                 t.vals = s_vals;
                 t.mask = (1u << bits) - 1u;
                 t.shift = 32 - bits;
+                t.mul = p.hash_mul;
                 for (int j = threadIdx.x; j < (1 << bits); j += blockDim.x) s_keys[j] = kEmptyKey;
                 __syncthreads();
                 record_set<false>(p, u, kk, t, sh);

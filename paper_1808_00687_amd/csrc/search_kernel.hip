@@ -87,6 +87,7 @@ struct Tab {
     uint32_t mask;
     int fill;
     int shift;   // 32 - log2(slots)
+    uint32_t mul;   // hash multiplier
 };
 
 struct Sh {
@@ -189,7 +190,7 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
     uint32_t h[R], k[R];
     bool claimed[R];
 #pragma unroll
-    for (int r = 0; r < R; r++) h[r] = hash_state(d[r]) >> t.shift;
+    for (int r = 0; r < R; r++) h[r] = hash_state(d[r], t.mul) >> t.shift;
     if constexpr (!G) {
         // In LDS every lane issues its compare-and-swap, so that the R
         // atomics of the wave are in flight together instead of one branch
@@ -366,6 +367,7 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
     const int wid = threadIdx.x / kWave;
     // a set kept in LDS comes with the first token of each chunk
     const bool use_cs = L && A <= kCs * kWave;
+    const int nch = (A + kWave - 1) / kWave;
     // wave w takes chunks w, w + kW, w + 2 kW, ... : every wave gets work
     for (int c = wid; c * kWave < A; c += kW * kChunks) {
         if (__builtin_amdgcn_readfirstlane(sh.overflow)) break;   // the frame is redone anyway
@@ -374,7 +376,10 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
         bool ok[kChunks];
 #pragma unroll
         for (int r = 0; r < kChunks; r++) {
-            const int a0 = (c + r * kW) * kWave;
+            // chunk c + r kW, or with the debugging permutation the chunk as
+            // far from the end
+            const int ch = p.reverse ? nch - 1 - (c + r * kW) : c + r * kW;
+            const int a0 = ch < 0 ? A : ch * kWave;
             a[r] = a0 + lane;
             ok[r] = false;
             ob[r] = op[r] = ot[r] = 0;
@@ -617,6 +622,8 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
         }
         const int take = min(wq.n, kWave);
         const int base = wq.n - take;
+        // items were stored by other lanes of the wave
+        wave_lds_handover();
         const uint2 it = lane < take ? wq.q[base + lane] : make_uint2(0u, 0u);
         wq.n = base;
         relax<G>(p, t, sh, wq, lane < take, it);
@@ -932,6 +939,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     lt.mask = kSlots - 1;
     lt.fill = min(kFill, p.lds_fill);
     lt.shift = 32 - kSlotBits;
+    lt.mul = p.hash_mul;
     Tab<true> gt;
     const int64_t gbase = static_cast<int64_t>(u) * p.capG;
     gt.keys = p.gkeys + gbase;
@@ -940,6 +948,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     gt.mask = static_cast<uint32_t>(p.capG - 1);
     gt.fill = static_cast<int>(p.capG / 4 * 3);
     gt.shift = 32 - (31 - __clz(static_cast<int>(p.capG)));
+    gt.mul = p.hash_mul;
     const int gcap = static_cast<int>(p.capO);
     uint2 *spill = p.gspill + static_cast<int64_t>(u) * 2 * p.capO;
 

@@ -62,6 +62,12 @@ class _Stats(C.Structure):
                 ("lattice_prune_ms", C.c_double), ("search_span_ms", C.c_double)]
 
 
+class _DebugOpts(C.Structure):
+    _fields_ = [("lds_fill", C.c_int32), ("queue_cap", C.c_int32), ("record_fill", C.c_int32),
+                ("record_big_fill", C.c_int32), ("lattice_lds", C.c_int32), ("permute", C.c_int32),
+                ("fail_lattice_alloc", C.c_int32)]
+
+
 class _LatArc(C.Structure):
     _fields_ = [("frame", C.c_int32), ("arc", C.c_int32), ("cost", C.c_float), ("extra", C.c_float)]
 
@@ -103,6 +109,8 @@ def _load_lib():
     lib.wfst_result_stats.restype = C.c_int
     lib.wfst_result_free.argtypes = [vp]
     lib.wfst_result_free.restype = None
+    lib.wfst_set_debug_opts.argtypes = [C.POINTER(_DebugOpts)]
+    lib.wfst_set_debug_opts.restype = C.c_int
     lib.wfst_last_error.argtypes = []
     lib.wfst_last_error.restype = C.c_char_p
     return lib
@@ -118,6 +126,32 @@ def wfst_last_error() -> str:
 def _check(rc: int, what: str):
     if rc != WFST_OK:
         raise WfstError(rc, "%s: %s" % (what, wfst_last_error()))
+
+
+def wfst_set_debug_opts(**fields) -> None:
+    """Process-wide test and debugging switches (wfst_set_debug_opts in
+    include/wfstdec.h); no arguments restores the defaults."""
+    if not fields:
+        _check(_lib.wfst_set_debug_opts(None), "wfst_set_debug_opts")
+        return
+    o = _DebugOpts()
+    for k, v in fields.items():
+        setattr(o, k, int(v))
+    _check(_lib.wfst_set_debug_opts(C.byref(o)), "wfst_set_debug_opts")
+
+
+class debug_opts:
+    """Context manager: wfst_set_debug_opts(**fields) inside, defaults after."""
+
+    def __init__(self, **fields):
+        self.fields = fields
+
+    def __enter__(self):
+        wfst_set_debug_opts(**self.fields)
+        return self
+
+    def __exit__(self, *exc):
+        wfst_set_debug_opts()
 
 
 def _i32(a):

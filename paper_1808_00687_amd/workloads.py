@@ -335,12 +335,23 @@ def workload(cfg: int, n_utt: Optional[int] = None, lsd: bool = True, frame_stri
 # small graphs for pins, fuzz and tie forcing
 # --------------------------------------------------------------------------
 
+# float32 values at the edges of the number format: signed zeros, the
+# smallest subnormal, a mid subnormal, the largest subnormal, the smallest
+# normal, and small dyadics (so sums of them tie exactly)
+EDGE_WEIGHTS = np.array([0.0, -0.0, 1e-45, -1e-45, 2.9e-39, 1.1754942e-38, 1.17549435e-38, 0.5, 1.0, 0.0],
+                        np.float32)
+EDGE_LOGLIKES = np.array([0.0, -0.0, -1e-45, 1e-45, -2.9e-39, -1.1754942e-38, -1.17549435e-38, -0.5, -1.0,
+                          -np.inf], np.float32)
+
+
 def random_small_graph(seed: int, n: int, mean_deg: float = 2.0, eps_frac: float = 0.2,
                        num_labels: int = 4, weights: str = "exp",
                        final: bool = False) -> Graph:
     """Small random WFST.  ``weights``: "exp" (Exp(1) float32), "int"
-    (integers 0..3, forcing cost ties) or "dyadic" (multiples of 1/16 in
-    [0, 4), exact in float32 sums of modest length)."""
+    (integers 0..3, forcing cost ties), "dyadic" (multiples of 1/16 in
+    [0, 4), exact in float32 sums of modest length) or "edge" (float32
+    special values: signed zeros, subnormals, the smallest normal and a few
+    small dyadics; epsilon arcs draw only the non-negative ones)."""
     rng = np.random.default_rng(np.random.SeedSequence([1808, 687, 99, seed]))
     deg = rng.poisson(mean_deg, size=n)
     src = np.repeat(np.arange(n), deg)
@@ -357,6 +368,9 @@ def random_small_graph(seed: int, n: int, mean_deg: float = 2.0, eps_frac: float
         w = rng.integers(0, 4, size=e).astype(np.float32)
     elif weights == "dyadic":
         w = (rng.integers(0, 64, size=e) / 16.0).astype(np.float32)
+    elif weights == "edge":
+        w = EDGE_WEIGHTS[rng.integers(0, EDGE_WEIGHTS.size, size=e)]
+        w = np.where(is_eps & (w < 0), -w, w).astype(np.float32)
     else:
         raise ValueError(weights)
     fw = None
@@ -455,7 +469,9 @@ def random_small_hmm_loglikes(seed: int, t: int, k: int) -> np.ndarray:
 def random_small_loglikes(seed: int, t: int, num_labels: int, kind: str = "gauss",
                           blank_boost: float = 0.0) -> np.ndarray:
     """``kind``: "gauss" (log-softmax of N(0,2)), "int" (negative integers
-    0..-3, forcing ties) or "dyadic" (multiples of -1/16 in (-4, 0])."""
+    0..-3, forcing ties), "dyadic" (multiples of -1/16 in (-4, 0]) or "edge"
+    (float32 special values, -inf included, and one column that is -inf on
+    every frame)."""
     rng = np.random.default_rng(np.random.SeedSequence([1808, 687, 98, seed]))
     if kind == "gauss":
         z = rng.normal(0.0, 2.0, size=(t, num_labels))
@@ -467,4 +483,9 @@ def random_small_loglikes(seed: int, t: int, num_labels: int, kind: str = "gauss
         return np.ascontiguousarray(-rng.integers(0, 4, size=(t, num_labels)).astype(np.float32))
     if kind == "dyadic":
         return np.ascontiguousarray((-rng.integers(0, 64, size=(t, num_labels)) / 16.0).astype(np.float32))
+    if kind == "edge":
+        x = EDGE_LOGLIKES[rng.integers(0, EDGE_LOGLIKES.size, size=(t, num_labels))]
+        if num_labels > 1:
+            x[:, int(rng.integers(0, num_labels))] = -np.inf
+        return np.ascontiguousarray(x.astype(np.float32))
     raise ValueError(kind)

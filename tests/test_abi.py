@@ -115,3 +115,14 @@ def test_ctypes_structs_match_the_header(tmp_path):
         assert got[(cname, "size")] == ctypes.sizeof(py), cname
         for f, _ in py._fields_:
             assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
+
+
+def test_debug_opts_validation():
+    # host-side only: the switches are checked and stored without a device call
+    from paper_1808_00687_amd import wfstdec
+    wfstdec.wfst_set_debug_opts(lds_fill=5, lattice_lds=-1, permute=1)
+    for bad in (dict(lds_fill=-1), dict(lattice_lds=-2), dict(permute=-3), dict(fail_lattice_alloc=-1)):
+        with pytest.raises(wfstdec.WfstError) as e:
+            wfstdec.wfst_set_debug_opts(**bad)
+        assert e.value.code == wfstdec.WFST_EINVAL
+    wfstdec.wfst_set_debug_opts()

@@ -157,26 +157,11 @@ def test_config2_raw_lattice_and_infinite_beam_prefix(dec, torch_mod, oracle_mod
     parity.assert_same(ro, rg, lattice=True, tag="config 2 infinite beam")
 
 
-class _env:
-    """Set test-hook environment variables of the library for one block."""
-
-    def __init__(self, **kv):
-        self.kv = kv
-
-    def __enter__(self):
-        for k, v in self.kv.items():
-            os.environ[k] = str(v)
-
-    def __exit__(self, *exc):
-        for k in self.kv:
-            os.environ.pop(k, None)
-
-
 def test_epsilon_queue_overflow_path(dec, torch_mod, oracle_mod, cfg2):
     # two epsilon items per generation in LDS: the rest of the closure goes
     # through the device-memory spill lists
     wl, gh = cfg2
-    with _env(WFSTDEC_TEST_QUEUE_CAP=2):
+    with dec.debug_opts(queue_cap=2):
         ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:80], gh=gh, beam=13.0,
                       max_active=7000, lattice_beam=8.0)
     parity.assert_same(ro, rg, lattice=True, tag="overflow queue")
@@ -187,7 +172,7 @@ def test_device_memory_table_path(dec, torch_mod, oracle_mod, cfg2, fill):
     # frames reaching more than `fill` states are redone with the token table
     # in device memory (every frame for fill = 1, a mix for the others)
     wl, gh = cfg2
-    with _env(WFSTDEC_TEST_LDS_FILL=fill):
+    with dec.debug_opts(lds_fill=fill):
         ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:60], gh=gh, beam=13.0,
                       max_active=7000 if fill != 40 else 300, lattice_beam=8.0)
     parity.assert_same(ro, rg, lattice=True, tag="device table fill %d" % fill)
@@ -195,19 +180,19 @@ def test_device_memory_table_path(dec, torch_mod, oracle_mod, cfg2, fill):
         g = W.random_small_graph(900 + seed, 300, mean_deg=3.0, eps_frac=0.3, num_labels=5, weights="int",
                                  final=seed % 2 == 0)
         ll = W.random_small_loglikes(900 + seed, 25, 5, kind="int")
-        with _env(WFSTDEC_TEST_LDS_FILL=fill, WFSTDEC_TEST_QUEUE_CAP=2):
+        with dec.debug_opts(lds_fill=fill, queue_cap=2):
             ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=9.0, max_active=[0, 11][seed % 2],
                           lattice_beam=3.0)
         parity.assert_same(ro, rg, lattice=True, tag="device table fill %d seed %d" % (fill, seed))
 
 
-@pytest.mark.parametrize("cap", [0, 25, 3900])
+@pytest.mark.parametrize("cap", [-1, 25, 3900])
 def test_lattice_device_memory_path(dec, torch_mod, oracle_mod, cfg2, cap):
     # the lattice backward pass keeps token sets of at most `cap` survivors in
-    # LDS and does larger ones in device memory: every set for cap = 0, a mix
-    # of both (and the hand-overs between them) for the others
+    # LDS and does larger ones in device memory: every set for cap = -1 (none
+    # in LDS), a mix of both (and the hand-overs between them) for the others
     wl, gh = cfg2
-    with _env(WFSTDEC_TEST_LATTICE_LDS=cap):
+    with dec.debug_opts(lattice_lds=cap):
         ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:80], gh=gh, beam=13.0,
                       max_active=7000, lattice_beam=8.0)
     parity.assert_same(ro, rg, lattice=True, tag="lattice lds %d" % cap)
@@ -215,7 +200,7 @@ def test_lattice_device_memory_path(dec, torch_mod, oracle_mod, cfg2, cap):
         g = W.random_small_graph(950 + seed, 300, mean_deg=3.0, eps_frac=0.3, num_labels=5, weights="int",
                                  final=seed % 2 == 0)
         ll = W.random_small_loglikes(950 + seed, 25, 5, kind="int")
-        with _env(WFSTDEC_TEST_LATTICE_LDS=cap):
+        with dec.debug_opts(lattice_lds=cap):
             ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=9.0, max_active=[0, 11][seed % 2],
                           lattice_beam=3.0)
         parity.assert_same(ro, rg, lattice=True, tag="lattice lds %d seed %d" % (cap, seed))
@@ -228,7 +213,7 @@ def test_record_large_set_path(dec, torch_mod, oracle_mod, cfg2, fill, big):
     # survivors, beyond that with the utterance's device-memory table (every
     # set for fill = 1, a mix for 900), alone and in a batch
     wl, gh = cfg2
-    with _env(WFSTDEC_TEST_RECORD_FILL=fill, WFSTDEC_TEST_RECORD_BIG_FILL=big):
+    with dec.debug_opts(record_fill=fill, record_big_fill=big):
         ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:60], gh=gh, beam=13.0,
                       max_active=7000, lattice_beam=8.0)
         parity.assert_same(ro, rg, lattice=True, tag="record fill %d/%d" % (fill, big))
@@ -260,6 +245,110 @@ def test_determinism(dec, torch_mod, cfg2):
         np.testing.assert_array_equal(getattr(a, f), getattr(b, f))
     np.testing.assert_array_equal(parity.bits(a.tok_cost), parity.bits(b.tok_cost))
     np.testing.assert_array_equal(parity.bits(a.lat_extra), parity.bits(b.lat_extra))
+
+
+def test_order_permutation_is_bit_identical(dec, torch_mod, oracle_mod, cfg2):
+    # another hash multiplier (other slots, claim order, probe sequences and
+    # survivor order) and the arc chunks of every set expanded last to first:
+    # every output must be bit-identical, and the oracle's
+    wl, gh = cfg2
+    o = wl.opts
+    x = to_dev(torch_mod, wl.loglikes[0][:150])
+    a = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    with dec.debug_opts(permute=1):
+        b = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+        with dec.debug_opts(permute=1, lds_fill=300, queue_cap=3, record_fill=200, lattice_lds=100):
+            c = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    ro = oracle_mod.decode(wl.graph, wl.loglikes[0][:150], o.beam, o.max_active, o.lattice_beam)
+    for r, tag in ((a, "plain"), (b, "permuted"), (c, "permuted, small tables")):
+        parity.assert_same(ro, r, lattice=True, tag=tag)
+    for seed in range(8):
+        g = W.random_small_graph(1200 + seed, 400, mean_deg=3.0, eps_frac=0.3, num_labels=5, weights="int",
+                                 final=seed % 2 == 0)
+        lls = [W.random_small_loglikes(1200 + 10 * seed + u, 10 + 7 * u, 5, kind="int") for u in range(5)]
+        gs = dec.load_graph(g)
+        with dec.debug_opts(permute=1):
+            res = dec.wfst_decode_batch(gs, [to_dev(torch_mod, y) for y in lls], 9.0, [0, 13][seed % 2], 4.0,
+                                        record_tokens=True)
+        gs.free()
+        for u, (y, r) in enumerate(zip(lls, res)):
+            parity.assert_same(oracle_mod.decode(g, y, 9.0, [0, 13][seed % 2], 4.0), r, lattice=True,
+                               tag="permuted seed %d utt %d" % (seed, u))
+
+
+def test_lattice_alloc_failure_returns_enomem(dec, torch_mod, oracle_mod, cfg2):
+    # the lattice output cannot be allocated: the call fails with WFST_ENOMEM,
+    # and the next decode works
+    wl, gh = cfg2
+    o = wl.opts
+    ll = wl.loglikes[0][:40]
+    x = to_dev(torch_mod, ll)
+    with dec.debug_opts(fail_lattice_alloc=1):
+        with pytest.raises(dec.WfstError) as e:
+            dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam)
+        assert e.value.code == dec.WFST_ENOMEM
+        with pytest.raises(dec.WfstError) as e:
+            dec.wfst_decode_batch(gh, [x, x], o.beam, o.max_active, o.lattice_beam)
+        assert e.value.code == dec.WFST_ENOMEM
+        # without a lattice nothing is allocated
+        r = dec.wfst_decode(gh, x, o.beam, o.max_active, -1.0)
+        assert r.status == 0
+    r = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    parity.assert_same(oracle_mod.decode(wl.graph, ll, o.beam, o.max_active, o.lattice_beam), r, lattice=True,
+                       tag="after the failed allocation")
+
+
+def _golden_graph(fx):
+    a = np.array(fx["arcs_src_dst_ilabel_olabel_weight"], np.float64).reshape(-1, 5)
+    return W.Graph(fx["num_states"], a[:, 0].astype(np.int32), a[:, 1].astype(np.int32), a[:, 2].astype(np.int32),
+                   a[:, 3].astype(np.int32), a[:, 4].astype(np.float32), fx.get("start", 0))
+
+
+def test_golden_cases(dec, torch_mod, oracle_mod):
+    # the hand-computed cases of tests/golden on the GPU: the token sets of
+    # the recombination example (and its tie variant), and the raw lattice
+    # with an epsilon arc above the cutoff and two exactly at it
+    import json
+    here = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+    fx = json.load(open(os.path.join(here, "fig2_recombination.json")))
+    ll = np.array(fx["loglikes"], np.float32)
+    for variant in ("base", "tie"):
+        if variant == "tie":
+            fx["arcs_src_dst_ilabel_olabel_weight"][3][4] = fx["tie_variant"]["arc3_weight"]
+        g = _golden_graph(fx)
+        ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=fx["beam"], lattice_beam=INF)
+        parity.assert_same(ro, rg, lattice=True, tag="fig2 " + variant)
+        exp = fx["tie_variant"] if variant == "tie" else fx["expected"]
+        assert list(rg.path_arcs) == exp["best_path"]
+        st, cb, bp = rg.token_set(2)
+        assert {str(int(s)): [float(c), int(b)] for s, c, b in zip(st, cb.view(np.float32), bp)} == \
+            exp["token_set_2"]
+    fx = json.load(open(os.path.join(here, "eps_lattice_cutoff.json")))
+    g = _golden_graph(fx)
+    ll = np.array(fx["loglikes"], np.float32)
+    ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=fx["beam"], lattice_beam=INF)
+    parity.assert_same(ro, rg, lattice=True, tag="epsilon cutoff")
+    raw = fx["expected"]["raw_lattice_frame_arc_cost_extra"]
+    assert rg.stats["lattice_raw"] == len(raw)
+    assert [[int(f), int(a), float(c), float(e)] for f, a, c, e in
+            zip(rg.lat_frame, rg.lat_arc, rg.lat_cost, rg.lat_extra)] == raw
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_fp32_edge_values(dec, torch_mod, oracle_mod, seed):
+    # signed zeros, subnormal weights and log-likelihoods (a flush to zero
+    # would change cost bits), -inf log-likelihood columns, +inf final
+    # weights, subnormal beams (ties at the beam edge) and exact ties
+    rng = np.random.default_rng(3000 + seed)
+    n = int(rng.integers(5, 300))
+    g = W.random_small_graph(3000 + seed, n, mean_deg=3.0, eps_frac=0.3, num_labels=4, weights="edge",
+                             final=seed % 2 == 1)
+    ll = W.random_small_loglikes(3000 + seed, int(rng.integers(1, 30)), 4, kind="edge")
+    beam = [INF, 1e-45, 2.9e-39, 1.17549435e-38, 0.5, 1.0][seed % 6]
+    max_active = [0, 0, 1, 3, 17][seed % 5]
+    lb = [INF, 0.0, 1e-45, 0.5][seed % 4]
+    ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=beam, max_active=max_active, lattice_beam=lb)
+    parity.assert_same(ro, rg, lattice=True, tag="edge values seed %d" % seed)
 
 
 def test_batch_matches_single_and_oracle(dec, torch_mod, oracle_mod):
@@ -414,24 +503,30 @@ def test_config3_full(dec, torch_mod, oracle_mod, cfg3):
     parity.assert_path_consistent(g, rg, wl.loglikes[0])
 
 
-def test_config4_batch_sampled(dec, torch_mod, oracle_mod, cfg3):
-    # the benchmark's batch (64 utterances on the 25M-arc graph); the oracle
-    # checks two utterances in full, every utterance is checked for a
-    # consistent best path
+def test_config4_batch_full(dec, torch_mod, oracle_mod, cfg3):
+    # the benchmark's batch (64 utterances on the 25M-arc graph, one batched
+    # call in the launch configuration the benchmark times): every utterance
+    # against the oracle, token sets of every frame included
+    from concurrent.futures import ThreadPoolExecutor
     g, gh = cfg3
     wl = W.workload(4)
     o = wl.opts
     xs = [to_dev(torch_mod, x) for x in wl.loglikes]
     say("batch decode of %d utterances" % len(xs))
-    res = dec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, record_tokens=False)
-    for u, r in enumerate(res):
-        assert r.status == 0
-        parity.assert_path_consistent(g, r, wl.loglikes[u])
-        assert r.lat_arc.size >= r.path_arcs.size
-    for u in (int(np.argmin([x.shape[0] for x in wl.loglikes])), 17):
-        say("oracle on utterance", u)
+    res = dec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    del xs
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    say("oracle on %d utterances, %d threads" % (len(res), threads))
+
+    def check(u):
         ro = oracle_mod.decode(g, wl.loglikes[u], o.beam, o.max_active, o.lattice_beam)
-        parity.assert_same(ro, res[u], lattice=True, tokens=False, tag="config 4 utt %d" % u)
+        parity.assert_same(ro, res[u], lattice=True, tokens=True, tag="config 4 utt %d" % u)
+        parity.assert_path_consistent(g, res[u], wl.loglikes[u])
+        return ro.tokens
+
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        toks = list(ex.map(check, range(len(res))))
+    say("config 4: %d utterances, %d tokens compared" % (len(res), sum(toks)))
 
 
 def test_config6_hmm_lsd_and_stride(dec, torch_mod, oracle_mod):

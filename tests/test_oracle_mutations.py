@@ -19,6 +19,8 @@ MUTATIONS = {
     "loglike_column": ("float cand = t1 - row[ilabel[a] - 1];", "float cand = t1 - row[ilabel[a] % L];"),
     "add_order": ("float t1 = c + weight[a];\n                float cand = t1 - row[ilabel[a] - 1];",
                   "float t1 = weight[a] - row[ilabel[a] - 1];\n                float cand = c + t1;"),
+    "subnormal_flush": ("float cand = t1 - row[ilabel[a] - 1];\n                touch",
+                        "float cand = t1 - row[ilabel[a] - 1];\n                if (fabsf(cand) < FLT_MIN) cand = 0.0f;\n                touch"),
     "dropped_weight": ("float t1 = c + weight[a];\n                float cand", "float t1 = c;\n                float cand"),
     "tie_break_reversed": ("| (uint32_t)(arc + 1);", "| (uint32_t)(0x7fffffff - arc);"),
     "beam_exclusive": ("if (k <= lim) scratch[nk++] = k;", "if (k < lim) scratch[nk++] = k;"),
@@ -37,6 +39,8 @@ MUTATIONS = {
     "lattice_eps_not_iterated": ("if (okey(ex) < okey(e_node[R[k].gs])) { e_node[R[k].gs] = ex; changed = 1; }",
                                  "if (okey(ex) < okey(e_node[R[k].gs])) { e_node[R[k].gs] = ex; }"),
     "lattice_cut_strict": ("if (okey(p) > cuts[j + 1]) continue;", "if (okey(p) >= cuts[j + 1]) continue;"),
+    "eps_lattice_cut_dropped": ("if (okey(p) > cuts[j]) continue;", "if (0) continue;"),
+    "eps_lattice_cut_strict": ("if (okey(p) > cuts[j]) continue;", "if (okey(p) >= cuts[j]) continue;"),
     "final_tie_highest_state": ("if (okey(tot[i - lo]) < okey(tot[best - lo])) best = i;",
                                 "if (okey(tot[i - lo]) <= okey(tot[best - lo])) best = i;"),
 }

@@ -99,6 +99,86 @@ def test_brute_force_final_weights(oracle_mod, seed):
     _check_against_brute_force(oracle_mod, g, ll)
 
 
+def _check_edge_against_brute_force(oracle_mod, g, ll):
+    # with -inf log-likelihoods a path can reach +inf: such tokens are never
+    # kept, so the decode has a path exactly when some complete path of the
+    # graph has a finite cost
+    bf = pins.brute_force(g, ll)
+    if not any(np.isfinite(pins.path_cost(g, a, ll)) for _, a, _ in bf["complete"]):
+        assert oracle_mod.decode(g, ll, beam=INF).status == oracle_mod.ORACLE_ENOPATH
+        return None
+    return _check_against_brute_force(oracle_mod, g, ll)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_brute_force_fp32_edge_values(oracle_mod, seed):
+    # signed zeros, subnormal weights and log-likelihoods (a flush to zero
+    # would change the cost bits), -inf log-likelihood columns, +inf final
+    # weights, and the exact ties such small values produce
+    g = W.random_small_graph(600 + seed, 6, mean_deg=3.0, eps_frac=0.3, num_labels=4, weights="edge",
+                             final=seed % 2 == 1)
+    ll = W.random_small_loglikes(600 + seed, 3, 4, kind="edge")
+    _check_edge_against_brute_force(oracle_mod, g, ll)
+
+
+def test_fp32_edge_values_keep_subnormals_and_zero_signs(oracle_mod):
+    # a hand-checked chain: subnormal weights and log-likelihoods add up
+    # exactly (no flush to zero); a -0.0 weight or log-likelihood leaves +0.0
+    # costs at +0.0; a -inf log-likelihood gives +inf, which is pruned
+    tiny = np.float32(1e-45)
+    sub = np.float32(2.9e-39)
+    g = _graph(4, [[0, 1, 1, 0, float(tiny)], [1, 2, 2, 0, -0.0], [2, 3, 0, 0, float(sub)], [2, 2, 3, 0, 0.0]])
+    ll = np.array([[-tiny, 0.0, -np.inf], [0.0, -0.0, -np.inf]], np.float32)
+    r = oracle_mod.decode(g, ll, beam=INF, lattice_beam=INF)
+    assert r.status == 0
+    st, cb, bp = r.token_set(1)
+    assert list(st) == [1] and int(cb[0]) == 2 and list(bp) == [0]       # 1e-45 + 1e-45 = 2e-45 (bits 2)
+    st, cb, bp = r.token_set(2)
+    # state 2: (2e-45 + -0) - (-0) = 2e-45; the self-loop reads -inf, so it is not a path
+    # state 3 via epsilon: 2e-45 + 2.9e-39
+    c3 = np.float32(np.float32(2 * tiny) + sub)
+    assert list(st) == [2, 3]
+    assert list(cb) == [2, int(_bits(c3))] and list(bp) == [1, 2]
+    assert int(_bits(r.cost)) == 2 and r.final_state == 2
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("beam", [1e-45, 2.9e-39, 1.17549435e-38, 0.5, INF])
+@pytest.mark.parametrize("max_active", [0, 1, 3])
+def test_star_graph_fp32_edge_values_beam_edge(oracle_mod, seed, beam, max_active):
+    # one frame from the start to K leaves with special-value weights and
+    # log-likelihoods: the survivors are the leaves whose cost key is within
+    # key(fl(best + beam)) (at most key(FLT_MAX)) and, when more than
+    # max_active are, within the max_active-th smallest key; every comparison
+    # on ordered keys, so -0.0 sorts below +0.0
+    rng = np.random.default_rng(2000 + seed)
+    K, L = 40, 4
+    w = W.EDGE_WEIGHTS[rng.integers(0, W.EDGE_WEIGHTS.size, K)]
+    lab = rng.integers(1, L + 1, K)
+    ll = W.EDGE_LOGLIKES[rng.integers(0, W.EDGE_LOGLIKES.size, (1, L))].astype(np.float32)
+    g = _graph(K + 1, [[0, k + 1, lab[k], 0, float(w[k])] for k in range(K)])
+    c = np.array([np.float32(np.float32(np.float32(0.0) + w[k]) - ll[0, lab[k] - 1]) for k in range(K)],
+                 np.float32)
+    keys = pins.okeys(c)
+    b = pins.okey_value(np.array([keys.min()], np.uint32))[0]
+    lim = min(int(pins.okeys(np.array([np.float32(b + np.float32(beam))]))[0]),
+              int(pins.okeys(np.array([np.finfo(np.float32).max], np.float32))[0]))
+    inb = np.sort(keys[keys <= lim])
+    cut = lim
+    if max_active > 0 and inb.size > max_active:
+        cut = min(cut, int(inb[max_active - 1]))
+    exp = np.flatnonzero(keys <= cut) + 1
+    r = oracle_mod.decode(g, ll, beam=beam, max_active=max_active, lattice_beam=INF)
+    if exp.size == 0:
+        assert r.status == oracle_mod.ORACLE_ENOPATH
+        return
+    st, cb_, bp = r.token_set(1)
+    np.testing.assert_array_equal(st, exp)
+    np.testing.assert_array_equal(cb_, _bits(c[exp - 1]))
+    np.testing.assert_array_equal(bp, exp - 1)
+    np.testing.assert_array_equal(r.lat_arc, exp - 1)
+
+
 def test_final_fallback_when_no_final_state_reached(oracle_mod):
     # 0 -a-> 1, only state 0 is final: after one frame no final state is active
     g = _graph(2, [[0, 1, 1, 0, 0.5]], final=[0.0, INF])
@@ -167,6 +247,32 @@ def test_fig2_recombination_golden(oracle_mod):
                 assert c == exp[str(int(s))][0] and b == exp[str(int(s))][1]
         assert r.cost == fx["expected"]["best_cost"]
         assert list(r.path_arcs) == path
+
+
+def test_eps_lattice_cutoff_golden(oracle_mod):
+    # finite beam: an epsilon arc between two survivors whose own prefix cost
+    # lies above the set's cutoff is not a lattice arc; arcs exactly at the
+    # cutoff are (hand-computed values in the fixture)
+    fx = json.load(open(os.path.join(GOLDEN, "eps_lattice_cutoff.json")))
+    g = _graph(fx["num_states"], fx["arcs_src_dst_ilabel_olabel_weight"], start=fx["start"])
+    ll = np.array(fx["loglikes"], np.float32)
+    exp = fx["expected"]
+    r = oracle_mod.decode(g, ll, beam=fx["beam"], lattice_beam=INF)
+    assert r.status == 0
+    assert pins.okey_value(np.array([r.cut_key[1]], np.uint32))[0] == exp["cutoff_set_1"]
+    st, cb, bp = r.token_set(1)
+    t1 = exp["token_set_1"]
+    assert [int(s) for s in st] == sorted(int(k) for k in t1)
+    for s, c, b in zip(st, cb.view(np.float32), bp):
+        assert c == t1[str(int(s))][0] and b == t1[str(int(s))][1]
+    assert r.cost == exp["best_cost"] and list(r.path_arcs) == exp["best_path"]
+    raw = exp["raw_lattice_frame_arc_cost_extra"]
+    assert r.lat_raw == len(raw)
+    got = [[int(f), int(a), float(c), float(e)] for f, a, c, e in zip(r.lat_frame, r.lat_arc, r.lat_cost,
+                                                                       r.lat_extra)]
+    assert got == raw
+    r = oracle_mod.decode(g, ll, beam=fx["beam"], lattice_beam=1.0)
+    assert [[int(f), int(a)] for f, a in zip(r.lat_frame, r.lat_arc)] == exp["lattice_beam_1"]["frame_arc"]
 
 
 def test_single_state_self_loops_sum_of_best_loglikes(oracle_mod):
