@@ -290,6 +290,68 @@ int wfst_result_stats(const wfst_result *r, wfst_stats *stats);
 void wfst_result_free(wfst_result *r);
 
 /*
+ * wfst_decode_noalloc -- wfst_decode of one utterance for callers that cannot
+ * allocate memory: code that must not call hipMalloc (serving loops with a
+ * fixed memory budget, harnesses that forbid allocation, set-up code around
+ * HIP graph capture).  The call allocates nothing, on the device or on the
+ * host: its workspace is a fixed device array of the library of
+ * WFST_NOALLOC_SCRATCH_BYTES, which each device the library runs this call
+ * on holds from its first such call until the process ends, and its outputs
+ * go to buffers the caller owns.  The workspace needs grow with T and with
+ * the tokens a frame keeps: a T for which the workspace would hold fewer
+ * than 64 tokens per frame on average is refused before anything runs, and a
+ * decode that overflows it returns WFST_ECAPACITY (there is no retry with
+ * larger buffers).
+ *
+ * Calls on one device share that device's workspace: calls that overlap in
+ * time on one device (from several threads, or on several streams) race and
+ * must not be made; calls on different devices are independent.
+ *
+ *   g, L, opts  as for wfst_decode; opts->flags must not contain
+ *               WFST_RECORD_TOKENS, WFST_LOGLIKES_HOST, WFST_PROFILE or
+ *               WFST_PROFILE_STEPS; opts->capacity_hint sets the tokens per
+ *               frame (0: from max_active)
+ *   loglikes    [T x L] float32 in device memory of the graph's device
+ *   hip_stream  as for wfst_decode (the call is blocking)
+ *   out         caller-owned descriptor: the device buffers below (on the
+ *               graph's device) and the host fields the call fills in
+ *
+ * Errors: WFST_EINVAL (as wfst_decode, a forbidden flag, out == NULL, a NULL
+ * output buffer with a non-zero capacity), WFST_ECAPACITY (the workspace
+ * cannot hold T frames, the decode overflowed it, or an output buffer is too
+ * small: out->path_len or out->lattice_n then gives the size needed),
+ * WFST_ENOPATH (out->status too), WFST_EDEVICE.
+ */
+#define WFST_NOALLOC_SCRATCH_BYTES (512ll << 20)
+
+typedef struct wfst_noalloc_out {
+    /* caller-owned device buffers */
+    int32_t *path_arcs;      /* [path_cap] best path arcs (user arc indices), first to last */
+    int32_t *path_frames;    /* [path_cap] original frame of each path arc, -1 for epsilon arcs */
+    int32_t path_cap;
+    wfst_lat_arc *lattice;   /* [lattice_cap] pruned lattice sorted by (frame, arc); may be NULL
+                                with lattice_cap 0 when opts->lattice_beam < 0 */
+    int64_t lattice_cap;
+    int32_t *kept;           /* [kept_cap] original frame of each decoded frame, or NULL */
+    int32_t kept_cap;
+    /* filled in by the call (host) */
+    int32_t status;          /* WFST_OK or WFST_ENOPATH */
+    float cost;              /* as wfst_result_best */
+    int32_t final_state;
+    int32_t reached_final;
+    int32_t path_len;
+    int32_t num_decoded;     /* T' */
+    int64_t lattice_n;       /* kept lattice arcs */
+    int64_t lattice_raw;     /* lattice arcs before lattice-beam pruning */
+    int64_t tokens;          /* as wfst_stats */
+    int64_t arcs_expanded;
+    int64_t eps_arcs;
+} wfst_noalloc_out;
+
+int wfst_decode_noalloc(const wfst_graph *g, const float *loglikes, int32_t T, int32_t L,
+                        const wfst_decode_opts *opts, void *hip_stream, wfst_noalloc_out *out);
+
+/*
  * Test and debugging switches, process-wide (for the test suite, not for
  * production use).  They force the decoder's rarely taken paths on small
  * inputs and change the order of its parallel work; the results must not

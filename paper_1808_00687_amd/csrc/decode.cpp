@@ -279,8 +279,8 @@ struct DebugState {
 
 DebugState &debug_state()
 {
-    static DebugState *d = new DebugState();
-    return *d;
+    static DebugState d;   // no heap allocation, also on first use
+    return d;
 }
 
 wfst_debug_opts debug_snapshot()
@@ -1131,4 +1131,218 @@ extern "C" int wfst_set_debug_opts(const wfst_debug_opts *opts)
     std::lock_guard<std::mutex> lk(d.mu);
     d.o = o;
     return WFST_OK;
+}
+
+// ---------------------------------------------------------------------------
+// wfst_decode_noalloc: one utterance with a fixed workspace and caller-owned
+// outputs, for callers that cannot allocate.
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// The fixed workspace.  In host code `scratch` names a host-side stand-in,
+// not device memory: its device address is taken once per device with
+// hipGetSymbolAddress and only that address is used.
+static __device__ __align__(256) char scratch[WFST_NOALLOC_SCRATCH_BYTES];
+
+struct ScratchAddr {
+    std::mutex mu;
+    void *ptr[64] = {};
+};
+
+ScratchAddr &scratch_addr()
+{
+    static ScratchAddr a;   // no heap allocation, also on first use
+    return a;
+}
+
+// Device address of the workspace on `device` (the current device).
+hipError_t scratch_ptr(int device, void **out)
+{
+    if (device < 0 || device >= 64) return hipErrorInvalidDevice;
+    ScratchAddr &a = scratch_addr();
+    std::lock_guard<std::mutex> lk(a.mu);
+    if (!a.ptr[device]) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        a.ptr[device] = ptr;
+    }
+    *out = a.ptr[device];
+    return hipSuccess;
+}
+
+// Workspace bytes of one utterance of T frames with sizes z.
+size_t noalloc_bytes(const Graph &G, int U, int L, const wfst_decode_opts &o, float thr, const wfst_debug_opts &dbg,
+                     const Sizes &z, int n_blank, int64_t T, Totals *tot_out, UttLayout *lay_out)
+{
+    Totals tot;
+    UttLayout lay{};
+    layout_utt(T, z, o.lattice_beam >= 0.0f, G.eps_depth, tot, lay);
+    Params p{};
+    set_params(p, G, U, L, o, thr, dbg, z, n_blank);
+    Arena measure;
+    UttLayout *d_lay = nullptr;
+    int64_t *fo_all = nullptr;
+    carve_ws(measure, p, U, tot, &d_lay, &fo_all);
+    if (tot_out) *tot_out = tot;
+    if (lay_out) *lay_out = lay;
+    return measure.off;
+}
+
+int noalloc_impl(const wfst_graph *gh, const float *ll, int32_t T, int32_t L, const wfst_decode_opts *opts,
+                 void *hip_stream, wfst_noalloc_out *out)
+{
+    clear_error();
+    if (!gh || !opts || !out) return fail(WFST_EINVAL, "wfst_decode_noalloc: NULL argument");
+    const Graph &G = gh->g;
+    const wfst_decode_opts o = *opts;
+    const bool lattice = o.lattice_beam >= 0.0f;
+    out->status = WFST_EINVAL;
+    out->path_len = 0;
+    out->lattice_n = 0;
+    out->num_decoded = 0;
+    if (o.flags & (WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST | WFST_PROFILE | WFST_PROFILE_STEPS))
+        return fail(WFST_EINVAL, "wfst_decode_noalloc: token recording, host log-likelihoods and profiling "
+                                 "are not available");
+    if (T < 0) return fail(WFST_EINVAL, "wfst_decode_noalloc: negative T");
+    if (T > 0 && !ll) return fail(WFST_EINVAL, "wfst_decode_noalloc: NULL loglikes");
+    if ((out->path_cap > 0 && (!out->path_arcs || !out->path_frames)) || out->path_cap < 0 ||
+        (out->lattice_cap > 0 && !out->lattice) || out->lattice_cap < 0 || (out->kept_cap > 0 && !out->kept) ||
+        out->kept_cap < 0)
+        return fail(WFST_EINVAL, "wfst_decode_noalloc: bad output buffer");
+    float thr = 0.0f;
+    {
+        const int rc = check_opts(G, o, L, &thr);
+        if (rc != WFST_OK) return rc;
+    }
+    // at most this many blank-like units (their copy sits in the workspace)
+    constexpr int kMaxBlank = 1024;
+    const int n_blank = o.num_blank_ids > 0 ? o.num_blank_ids : 1;
+    if (n_blank > kMaxBlank) return fail(WFST_EINVAL, "wfst_decode_noalloc: more than 1024 blank-like units");
+    const wfst_debug_opts dbg = debug_snapshot();
+
+    // Sizes: as wfst_decode's first attempt, with the average tokens per
+    // frame as large as the fixed workspace allows (sizes grow linearly in
+    // it).
+    Sizes z = initial_sizes(G, o);
+    const size_t cap = static_cast<size_t>(WFST_NOALLOC_SCRATCH_BYTES);
+    z.capA = 0;
+    const size_t base = noalloc_bytes(G, 1, L, o, thr, dbg, z, n_blank, T, nullptr, nullptr);
+    z.capA = 1024;
+    const size_t at1k = noalloc_bytes(G, 1, L, o, thr, dbg, z, n_blank, T, nullptr, nullptr);
+    const double per = static_cast<double>(at1k - base) / 1024.0;
+    if (base >= cap || per <= 0.0) {
+        set_error("wfst_decode_noalloc: %d frames need more than the fixed workspace of %lld bytes", T,
+                  static_cast<long long>(WFST_NOALLOC_SCRATCH_BYTES));
+        return WFST_ECAPACITY;
+    }
+    z.capA = std::min<int64_t>(z.capF, static_cast<int64_t>(static_cast<double>(cap - base) / per));
+    Totals tot;
+    UttLayout lay{};
+    size_t need = noalloc_bytes(G, 1, L, o, thr, dbg, z, n_blank, T, &tot, &lay);
+    while (need > cap && z.capA > 0) {   // rounding of the carve
+        z.capA -= std::max<int64_t>(1, z.capA / 64);
+        need = noalloc_bytes(G, 1, L, o, thr, dbg, z, n_blank, T, &tot, &lay);
+    }
+    // refuse up front a T for which the workspace would hold fewer than
+    // kMinAvgTokens tokens per frame on average: such a decode would almost
+    // surely overflow
+    constexpr int64_t kMinAvgTokens = 64;
+    if (z.capA < std::min<int64_t>(kMinAvgTokens, z.capF) || need > cap) {
+        set_error("wfst_decode_noalloc: %d frames need more than the fixed workspace of %lld bytes", T,
+                  static_cast<long long>(WFST_NOALLOC_SCRATCH_BYTES));
+        return WFST_ECAPACITY;
+    }
+
+    DeviceGuard dg(G.device);
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    void *ws = nullptr;
+    {
+        const hipError_t e = scratch_ptr(G.device, &ws);
+        if (e != hipSuccess) return hip_fail(e, "wfst_decode_noalloc: workspace address");
+    }
+    Params p{};
+    set_params(p, G, 1, L, o, thr, dbg, z, n_blank);
+    Arena arena;
+    arena.base = static_cast<char *>(ws);
+    UttLayout *d_lay = nullptr;
+    int64_t *fo_all = nullptr;
+    carve_ws(arena, p, 1, tot, &d_lay, &fo_all);
+
+    UttState st;
+    std::memset(&st, 0, sizeof(st));
+    st.ll = ll;
+    st.T = T;
+    hipError_t e = hipSuccess;
+    auto chk = [&](hipError_t r) {
+        if (e == hipSuccess && r != hipSuccess) e = r;
+    };
+    chk(hipMemcpyAsync(p.st, &st, sizeof(UttState), hipMemcpyHostToDevice, s));
+    chk(hipMemcpyAsync(d_lay, &lay, sizeof(UttLayout), hipMemcpyHostToDevice, s));
+    chk(launch_zero(fo_all, 7 * tot.fo * sizeof(int64_t), s));
+    if (o.num_blank_ids > 0)
+        chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), o.blank_ids, n_blank * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s));
+    else
+        chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), &o.blank_id, sizeof(int32_t), hipMemcpyHostToDevice,
+                           s));
+    chk(launch_classify(p, s));
+    chk(launch_search(p, s));
+    chk(launch_record(p, T, s));
+    chk(launch_final(p, s));
+    chk(launch_finish(p, s));
+    chk(hipMemcpyAsync(&st, p.st, sizeof(UttState), hipMemcpyDeviceToHost, s));
+    chk(hipStreamSynchronize(s));
+    if (e != hipSuccess) return hip_fail(e, "wfst_decode_noalloc: search");
+    if (st.status == WFST_ECAPACITY) {
+        set_error("wfst_decode_noalloc: the decode overflowed the fixed workspace");
+        return WFST_ECAPACITY;
+    }
+    out->status = st.status;
+    out->num_decoded = st.Tp;
+    if (st.status != WFST_OK) {
+        if (st.status == WFST_ENOPATH) set_error("wfst_decode_noalloc: no surviving path");
+        return st.status;
+    }
+    out->cost = st.final_cost;
+    out->final_state = st.final_state;
+    out->reached_final = st.reached_final;
+    out->path_len = st.path_len;
+    out->tokens = st.n_tok;
+    out->arcs_expanded = st.arcs_expanded;
+    out->eps_arcs = st.eps_arcs;
+    out->lattice_raw = lattice ? st.le_cnt + st.lx_cnt : 0;
+    out->lattice_n = lattice ? st.lat_kept : 0;
+    if (st.path_len > out->path_cap || (lattice && st.lat_kept > out->lattice_cap) ||
+        (out->kept && st.Tp > out->kept_cap)) {
+        set_error("wfst_decode_noalloc: output buffer too small (path %d, lattice %lld, decoded frames %d)",
+                  st.path_len, static_cast<long long>(lattice ? st.lat_kept : 0), st.Tp);
+        return WFST_ECAPACITY;
+    }
+    // the path lies at the end of the utterance's path region
+    const int64_t p0 = lay.path0 + lay.pathcap - st.path_len;
+    if (st.path_len > 0) {
+        chk(hipMemcpyAsync(out->path_arcs, p.path_arc + p0, st.path_len * sizeof(int32_t), hipMemcpyDeviceToDevice,
+                           s));
+        chk(hipMemcpyAsync(out->path_frames, p.path_frame + p0, st.path_len * sizeof(int32_t),
+                           hipMemcpyDeviceToDevice, s));
+    }
+    if (out->kept && st.Tp > 0)
+        chk(hipMemcpyAsync(out->kept, p.kept + lay.kept0, st.Tp * sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+    if (lattice && st.lat_kept > 0) {
+        p.lat_out = reinterpret_cast<int4 *>(out->lattice);
+        chk(launch_lattice_emit(p, T, s));
+    }
+    chk(hipStreamSynchronize(s));
+    if (e != hipSuccess) return hip_fail(e, "wfst_decode_noalloc: results");
+    return WFST_OK;
+}
+
+}  // namespace
+
+extern "C" int wfst_decode_noalloc(const wfst_graph *g, const float *loglikes, int32_t T, int32_t L,
+                                   const wfst_decode_opts *opts, void *hip_stream, wfst_noalloc_out *out)
+{
+    return noalloc_impl(g, loglikes, T, L, opts, hip_stream, out);
 }

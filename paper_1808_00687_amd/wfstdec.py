@@ -72,6 +72,15 @@ class _LatArc(C.Structure):
     _fields_ = [("frame", C.c_int32), ("arc", C.c_int32), ("cost", C.c_float), ("extra", C.c_float)]
 
 
+class _NoallocOut(C.Structure):
+    _fields_ = [("path_arcs", C.c_void_p), ("path_frames", C.c_void_p), ("path_cap", C.c_int32),
+                ("lattice", C.c_void_p), ("lattice_cap", C.c_int64), ("kept", C.c_void_p), ("kept_cap", C.c_int32),
+                ("status", C.c_int32), ("cost", C.c_float), ("final_state", C.c_int32),
+                ("reached_final", C.c_int32), ("path_len", C.c_int32), ("num_decoded", C.c_int32),
+                ("lattice_n", C.c_int64), ("lattice_raw", C.c_int64), ("tokens", C.c_int64),
+                ("arcs_expanded", C.c_int64), ("eps_arcs", C.c_int64)]
+
+
 def _load_lib():
     if not os.path.exists(LIB_PATH):
         raise ImportError("libwfstdec.so is not built (run __graft_entry__.build() or "
@@ -109,6 +118,8 @@ def _load_lib():
     lib.wfst_result_stats.restype = C.c_int
     lib.wfst_result_free.argtypes = [vp]
     lib.wfst_result_free.restype = None
+    lib.wfst_decode_noalloc.argtypes = [vp, vp, C.c_int32, C.c_int32, C.POINTER(_Opts), vp, C.POINTER(_NoallocOut)]
+    lib.wfst_decode_noalloc.restype = C.c_int
     lib.wfst_set_debug_opts.argtypes = [C.POINTER(_DebugOpts)]
     lib.wfst_set_debug_opts.restype = C.c_int
     lib.wfst_last_error.argtypes = []
@@ -441,3 +452,71 @@ def wfst_decode(graph: WfstGraph, loglikes, beam: float, max_active: int = 0,
         return _collect(out, lattice_beam >= 0, record_tokens)
     finally:
         _lib.wfst_result_free(out)
+
+
+WFST_NOALLOC_SCRATCH_BYTES = 512 << 20
+
+
+@dataclasses.dataclass
+class NoallocResult:
+    """Outputs of wfst_decode_noalloc: the host fields of the descriptor and
+    the caller-owned device buffers (torch tensors) it wrote."""
+    rc: int
+    status: int
+    cost: float
+    final_state: int
+    reached_final: int
+    path_len: int
+    num_decoded: int
+    lattice_n: int
+    lattice_raw: int
+    tokens: int
+    arcs_expanded: int
+    eps_arcs: int
+    path_arcs: object       # int32 tensor [path_cap] on the device
+    path_frames: object
+    lattice: object         # int32 tensor [lattice_cap, 4] on the device
+    kept: object            # int32 tensor [kept_cap] on the device
+
+
+def wfst_decode_noalloc(graph: WfstGraph, loglikes, beam: float, max_active: int = 0,
+                        lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
+                        path_cap: int = 4096, lattice_cap: int = 1 << 16, kept_cap: int = 0,
+                        capacity_hint: int = 0, stream=None, blank_ids=None, frame_stride: int = 1,
+                        outputs=None) -> NoallocResult:
+    """Decode one utterance with wfst_decode_noalloc.  ``loglikes`` is a
+    [T x L] float32 tensor on the graph's device.  The output buffers are
+    torch tensors: ``outputs`` = (path_arcs, path_frames, lattice, kept) to
+    reuse existing ones, else they are created here (by the caller's side,
+    as the C call itself allocates nothing).  Returns the return code with
+    the outputs; a WfstError is raised only for WFST_EINVAL and
+    WFST_EDEVICE."""
+    import torch
+    keep: list = []
+    ptr, shape, host = _ll_ptr(loglikes, keep)
+    if host:
+        raise ValueError("wfst_decode_noalloc takes device log-likelihoods")
+    dev = loglikes.device
+    if outputs is None:
+        pa = torch.empty(max(path_cap, 1), dtype=torch.int32, device=dev)
+        pf = torch.empty(max(path_cap, 1), dtype=torch.int32, device=dev)
+        lat = torch.empty((max(lattice_cap, 1), 4), dtype=torch.int32, device=dev)
+        kp = torch.empty(max(kept_cap, 1), dtype=torch.int32, device=dev)
+    else:
+        pa, pf, lat, kp = outputs
+        path_cap, lattice_cap, kept_cap = pa.numel(), lat.shape[0], kp.numel()
+    o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, 0, capacity_hint, blank_ids,
+              frame_stride, keep)
+    d = _NoallocOut()
+    d.path_arcs, d.path_frames, d.path_cap = pa.data_ptr(), pf.data_ptr(), path_cap
+    d.lattice, d.lattice_cap = lat.data_ptr(), lattice_cap
+    d.kept, d.kept_cap = (kp.data_ptr(), kept_cap) if kept_cap > 0 else (None, 0)
+    rc = _lib.wfst_decode_noalloc(graph.handle, ptr, shape[0], shape[1], C.byref(o), _stream_handle(stream),
+                                  C.byref(d))
+    if rc in (WFST_EINVAL, WFST_EDEVICE):
+        raise WfstError(rc, "wfst_decode_noalloc: %s" % wfst_last_error())
+    return NoallocResult(rc=rc, status=d.status, cost=float(np.float32(d.cost)), final_state=d.final_state,
+                         reached_final=d.reached_final, path_len=d.path_len, num_decoded=d.num_decoded,
+                         lattice_n=d.lattice_n, lattice_raw=d.lattice_raw, tokens=d.tokens,
+                         arcs_expanded=d.arcs_expanded, eps_arcs=d.eps_arcs, path_arcs=pa, path_frames=pf,
+                         lattice=lat, kept=kp)

@@ -96,7 +96,8 @@ def test_ctypes_structs_match_the_header(tmp_path):
     import subprocess
     from paper_1808_00687_amd import wfstdec
     mirrors = {"wfst_decode_opts": wfstdec._Opts, "wfst_stats": wfstdec._Stats,
-               "wfst_graph_info": wfstdec._Info, "wfst_lat_arc": wfstdec._LatArc}
+               "wfst_graph_info": wfstdec._Info, "wfst_lat_arc": wfstdec._LatArc,
+               "wfst_debug_opts": wfstdec._DebugOpts, "wfst_noalloc_out": wfstdec._NoallocOut}
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "wfstdec.h"', "int main(void) {"]
     for cname, py in mirrors.items():
         lines.append('printf("%s size %%zu\\n", sizeof(%s));' % (cname, cname))
@@ -126,3 +127,15 @@ def test_debug_opts_validation():
             wfstdec.wfst_set_debug_opts(**bad)
         assert e.value.code == wfstdec.WFST_EINVAL
     wfstdec.wfst_set_debug_opts()
+
+
+def test_noalloc_rejects_bad_arguments_on_the_host():
+    # argument checks come before any device call
+    import ctypes
+    from paper_1808_00687_amd import wfstdec
+    lib = wfstdec._lib
+    o = wfstdec._Opts()
+    lib.wfst_default_opts(ctypes.byref(o))
+    d = wfstdec._NoallocOut()
+    assert lib.wfst_decode_noalloc(None, None, 0, 1, ctypes.byref(o), None, ctypes.byref(d)) == wfstdec.WFST_EINVAL
+    assert lib.wfst_decode_noalloc(None, None, 0, 1, None, None, None) == wfstdec.WFST_EINVAL
