@@ -404,6 +404,10 @@ hipStream_t aux_stream(int dev, int i)
     return tab[dev][i];
 }
 
+// Per-frame offset arrays of an utterance: survivors, emitting and epsilon
+// record regions, lattice output, emitting and epsilon record counts.
+constexpr int kOffsetArrays = 6;
+
 // Element counts of the workspace regions summed over a batch.
 struct Totals {
     int64_t sv = 0, le = 0, lx = 0, fo = 0, kp = 0, pa = 0;
@@ -416,11 +420,11 @@ void layout_utt(int64_t Tu, const Sizes &z, bool lattice, int depth, Totals &tot
     // survivor indices are 32-bit; one frame may reach capF tokens
     l.svcap = std::min<int64_t>((Tu + 1) * z.capA + z.capF, std::numeric_limits<int32_t>::max());
     tot.sv += l.svcap;
-    // a set's emitting region holds one candidate (and one lattice record)
-    // per emitting out-arc of its tokens, its epsilon region one lattice
-    // record per epsilon out-arc
+    // with a lattice, a set's emitting region holds one lattice record per
+    // emitting out-arc of its tokens, its epsilon region one per epsilon
+    // out-arc
     l.le0 = tot.le;
-    l.lecap = (Tu * z.capA + z.capF) * z.em;
+    l.lecap = lattice ? (Tu * z.capA + z.capF) * z.em : 0;
     tot.le += l.lecap;
     l.lx0 = tot.lx;
     l.lxcap = lattice ? ((Tu + 1) * z.capA + z.capF) * z.xm : 0;
@@ -472,22 +476,22 @@ void carve_ws(Arena &a, Params &p, int U, const Totals &tot, UttLayout **d_lay, 
     *d_lay = a.get<UttLayout>(U);
     p.lay = *d_lay;
     p.gkeys = a.get<uint32_t>(U * p.capG);
-    p.gvals = a.get<unsigned long long>(U * p.capG);
+    p.gvals = a.get<uint32_t>(U * p.capG);
     p.gslots = a.get<int32_t>(U * p.capG);
     p.gspill = a.get<uint2>(U * 2 * p.capO);
     p.sv_state = a.get<int32_t>(tot.sv);
-    p.sv_tok = a.get<uint64_t>(tot.sv);
+    p.sv_key = a.get<uint32_t>(tot.sv);
     p.sv_prev = a.get<int32_t>(tot.sv);
+    p.sv_arc = a.get<int32_t>(tot.sv);
     p.sv_ebeg = a.get<int32_t>(tot.sv);
     p.sv_epre = a.get<int32_t>(tot.sv);
-    p.sv_x = a.get<int4>(tot.sv);
-    p.cand = a.get<int4>(tot.le);
+    p.sv_win = a.get<unsigned long long>(tot.sv);
     p.e_key = lattice ? a.get<uint32_t>(tot.sv) : nullptr;
     p.lat_e = lattice ? a.get<int4>(tot.le) : nullptr;
     p.lat_x = lattice ? a.get<int4>(tot.lx) : nullptr;
     p.ex_e = lattice ? a.get<float>(tot.le) : nullptr;
     p.ex_x = lattice ? a.get<float>(tot.lx) : nullptr;
-    *fo_all = a.get<int64_t>(7 * tot.fo);
+    *fo_all = a.get<int64_t>(kOffsetArrays * tot.fo);
     p.blank_ids = a.get<int32_t>(p.n_blank);
     p.cut_arr = a.get<uint32_t>(tot.fo);
     p.kept = a.get<int32_t>(tot.kp);
@@ -502,7 +506,6 @@ void carve_ws(Arena &a, Params &p, int U, const Totals &tot, UttLayout **d_lay, 
     p.lo_off = f ? f + 3 * fo : nullptr;
     p.le_cnt = f ? f + 4 * fo : nullptr;
     p.lx_cnt = f ? f + 5 * fo : nullptr;
-    p.cand_cnt = f ? f + 6 * fo : nullptr;
 }
 
 // One attempt at decoding the batch with the given buffer sizes.  Returns
@@ -565,8 +568,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     if (wt.on) {
         const double gib = 1.0 / (1024.0 * 1024.0 * 1024.0);
         fprintf(stderr, "[wfstdec] workspace %.2f GiB: survivors %.2f, emitting regions %.2f, epsilon regions %.2f\n",
-                measure.off * gib, tot.sv * (lattice ? 44.0 : 40.0) * gib, tot.le * (lattice ? 36.0 : 16.0) * gib,
-                tot.lx * 20.0 * gib);
+                measure.off * gib, tot.sv * (lattice ? 36.0 : 32.0) * gib, tot.le * 20.0 * gib, tot.lx * 20.0 * gib);
     }
 
     std::vector<UttState> st(U);
@@ -581,7 +583,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     };
     chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
-    chk(launch_zero(fo_all, 7 * fo * sizeof(int64_t), s));
+    chk(launch_zero(fo_all, kOffsetArrays * fo * sizeof(int64_t), s));
     chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), blank_h.data(), blank_h.size() * sizeof(int32_t),
                        hipMemcpyHostToDevice, s));
     chk(launch_classify(p, s));
@@ -670,6 +672,9 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     if (e != hipSuccess) return hip_fail(e, "decode: search");
     for (int u = 0; u < U; u++)
         if (st[u].status == WFST_ECAPACITY) return WFST_ECAPACITY;
+    for (int u = 0; u < U; u++)
+        if (st[u].status == kStatusNoBackPointer)
+            return fail(WFST_EDEVICE, "decode: internal error, a surviving token without a back-pointer");
 
     std::shared_ptr<LatBuf> lat_buf;
     std::shared_ptr<LatHost> lat_host;
@@ -739,17 +744,19 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
             r->lat_n = x.lat_kept;
         }
     }
-    std::vector<std::vector<int32_t>> tst(U);
-    std::vector<std::vector<uint64_t>> ttk(U);
+    std::vector<std::vector<int32_t>> tst(U), tarc(U);
+    std::vector<std::vector<uint32_t>> tkey(U);
     if (o.flags & WFST_RECORD_TOKENS) {
         chk(hipStreamSynchronize(s));
         for (int u = 0; u < U; u++) {
             if (st[u].status != WFST_OK) continue;
             const int64_t ntok = fo_h[lay[u].fo0 + st[u].Tp + 1];
             tst[u].resize(static_cast<size_t>(ntok));
-            ttk[u].resize(static_cast<size_t>(ntok));
+            tkey[u].resize(static_cast<size_t>(ntok));
+            tarc[u].resize(static_cast<size_t>(ntok));
             chk(hipMemcpyAsync(tst[u].data(), p.sv_state + lay[u].sv0, ntok * 4, hipMemcpyDeviceToHost, s));
-            chk(hipMemcpyAsync(ttk[u].data(), p.sv_tok + lay[u].sv0, ntok * 8, hipMemcpyDeviceToHost, s));
+            chk(hipMemcpyAsync(tkey[u].data(), p.sv_key + lay[u].sv0, ntok * 4, hipMemcpyDeviceToHost, s));
+            chk(hipMemcpyAsync(tarc[u].data(), p.sv_arc + lay[u].sv0, ntok * 4, hipMemcpyDeviceToHost, s));
         }
     }
     chk(hipStreamSynchronize(s));
@@ -820,14 +827,13 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
                 std::sort(idx.begin(), idx.end(), [&](int64_t x, int64_t y) { return tst[u][x] < tst[u][y]; });
                 for (int64_t i = a; i < b; i++) {
                     const int64_t q = idx[i - a];
-                    const uint64_t t = ttk[u][q];
-                    const uint32_t k = static_cast<uint32_t>(t >> 32);
+                    const uint32_t k = tkey[u][q];
                     const uint32_t bits = (k >> 31) ? (k & 0x7FFFFFFFu) : ~k;
                     float c;
                     std::memcpy(&c, &bits, 4);
                     r->tok_state[i] = tst[u][q];
                     r->tok_cost[i] = c;
-                    r->tok_arc[i] = static_cast<int32_t>(static_cast<uint32_t>(t)) - 1;
+                    r->tok_arc[i] = tarc[u][q];
                 }
             }
         }
@@ -1280,7 +1286,7 @@ int noalloc_impl(const wfst_graph *gh, const float *ll, int32_t T, int32_t L, co
     };
     chk(hipMemcpyAsync(p.st, &st, sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, &lay, sizeof(UttLayout), hipMemcpyHostToDevice, s));
-    chk(launch_zero(fo_all, 7 * tot.fo * sizeof(int64_t), s));
+    chk(launch_zero(fo_all, kOffsetArrays * tot.fo * sizeof(int64_t), s));
     if (o.num_blank_ids > 0)
         chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), o.blank_ids, n_blank * sizeof(int32_t),
                            hipMemcpyHostToDevice, s));
@@ -1295,6 +1301,8 @@ int noalloc_impl(const wfst_graph *gh, const float *ll, int32_t T, int32_t L, co
     chk(hipMemcpyAsync(&st, p.st, sizeof(UttState), hipMemcpyDeviceToHost, s));
     chk(hipStreamSynchronize(s));
     if (e != hipSuccess) return hip_fail(e, "wfst_decode_noalloc: search");
+    if (st.status == kStatusNoBackPointer)
+        return fail(WFST_EDEVICE, "wfst_decode_noalloc: internal error, a surviving token without a back-pointer");
     if (st.status == WFST_ECAPACITY) {
         set_error("wfst_decode_noalloc: the decode overflowed the fixed workspace");
         return WFST_ECAPACITY;

@@ -29,7 +29,7 @@ __global__ __launch_bounds__(256) void final_kernel(Params p)
         uint64_t m = ~0ull;
         for (int64_t i = a + threadIdx.x; i < b; i += blockDim.x) {
             int s = p.sv_state[ly.sv0 + i];
-            float c = tok_cost(p.sv_tok[ly.sv0 + i]);
+            float c = okey_val(p.sv_key[ly.sv0 + i]);
             float f = use_final ? p.g.final_w[s] : 0.0f;
             float tot = c + f;
             uint64_t v = (static_cast<uint64_t>(okey(tot)) << 32) | static_cast<uint32_t>(s);
@@ -76,9 +76,9 @@ __device__ void backtrace_block(const Params &p, int u, int *sh)
         int64_t i = st.final_sv;
         int cnt = 0;
         while (true) {
-            const uint64_t t = p.sv_tok[ly.sv0 + i];
+            const int a = p.sv_arc[ly.sv0 + i];
             const int prev = p.sv_prev[ly.sv0 + i];
-            if (tok_arc(t) < 0) break;
+            if (a < 0) break;
             if (cnt >= ly.pathcap || prev < 0) {
                 set_status(st, WFST_ECAPACITY);
                 break;
@@ -101,7 +101,7 @@ __device__ void backtrace_block(const Params &p, int u, int *sh)
         bool emit = false;
         if (k < cnt) {
             const int64_t i = p.path_arc[end - 1 - k];
-            a = tok_arc(p.sv_tok[ly.sv0 + i]);
+            a = p.sv_arc[ly.sv0 + i];
             emit = p.g.arc_src[a] >= 0;
         }
         int total;
@@ -140,7 +140,7 @@ struct LatMeta {
 struct LatRegs {
     int4 e[kRE];
     int4 x[kRX];
-    uint64_t t[kRC];
+    uint32_t t[kRC];   // cost keys
 };
 
 __device__ __forceinline__ LatMeta lat_meta(const Params &p, const UttLayout &ly, int j, int Tp)
@@ -243,7 +243,7 @@ __device__ __forceinline__ void lat_fetch(const Params &p, const UttLayout &ly, 
 #pragma unroll
     for (int q = 0; q < kRC; q++) {
         const int64_t i = tid + q * kLatT;
-        r.t[q] = i < m.nB ? p.sv_tok[ly.sv0 + m.b0 + i] : kEmptyTok;
+        r.t[q] = i < m.nB ? p.sv_key[ly.sv0 + m.b0 + i] : kEmptyKey;
     }
 }
 
@@ -269,7 +269,7 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
     const float B = st.final_cost;
     const bool use_final = p.g.final_w != nullptr && st.reached_final;
     uint32_t *eg = p.e_key + ly.sv0;
-    const uint64_t *tok = p.sv_tok + ly.sv0;
+    const uint32_t *tok = p.sv_key + ly.sv0;   // cost keys
     const int64_t *so = p.sv_off + ly.fo0;
     unsigned long long *kcnt = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
     const uint32_t kinf = okey(__int_as_float(0x7F800000));
@@ -315,16 +315,16 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
 #pragma unroll
             for (int q = 0; q < kRC; q++) {
                 const int64_t i = tid + q * kLatT;
-                if (i < nB) cB[i] = tok_cost(cur.t[q]);
+                if (i < nB) cB[i] = okey_val(cur.t[q]);
             }
-            for (int64_t i = tid + kRC * kLatT; i < nB; i += kLatT) cB[i] = tok_cost(tok[b0 + i]);
+            for (int64_t i = tid + kRC * kLatT; i < nB; i += kLatT) cB[i] = okey_val(tok[b0 + i]);
             // The costs of S_j are first read after the next barrier; its
             // extra costs were set to +inf by the previous step unless that
             // step ran in device memory (or this is the last set).
             if (!b_ready) {
                 if (j == Tp) {
                     for (int64_t i = tid; i < nB; i += kLatT) {
-                        const float c = tok_cost(tok[b0 + i]);
+                        const float c = okey_val(tok[b0 + i]);
                         const float f = use_final ? p.g.final_w[p.sv_state[ly.sv0 + b0 + i]] : 0.0f;
                         eB[i] = okey((c + f) - B);
                     }
@@ -336,7 +336,7 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                 // S_j+1 was processed in device memory: bring it into LDS
                 for (int64_t i = tid; i < nA; i += kLatT) {
                     eA[i] = ld_relaxed(eg + a0 + i);
-                    cA[i] = tok_cost(tok[a0 + i]);
+                    cA[i] = okey_val(tok[a0 + i]);
                 }
             }
             if (!b_ready || !a_lds) lds_barrier();
@@ -431,7 +431,7 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
             for (int64_t i = tid; i < nB; i += kLatT) {
                 uint32_t e0 = kinf;
                 if (j == Tp) {
-                    const float c = tok_cost(tok[b0 + i]);
+                    const float c = okey_val(tok[b0 + i]);
                     const float f = use_final ? p.g.final_w[p.sv_state[ly.sv0 + b0 + i]] : 0.0f;
                     e0 = okey((c + f) - B);
                 }
@@ -440,7 +440,7 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
             __syncthreads();
             for (int64_t r = mc.e0 + tid; r < mc.e1; r += kLatT) {
                 const int4 x = p.lat_e[ly.le0 + r];
-                const float d1 = __int_as_float(x.w) - tok_cost(tok[x.y]);
+                const float d1 = __int_as_float(x.w) - okey_val(tok[x.y]);
                 const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
                 p.ex_e[ly.le0 + r] = ex;
                 atomicMin(eg + x.x, okey(ex));
@@ -456,7 +456,7 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
                     kx = 0;
                     for (int64_t r = mc.x0 + tid; r < mc.x1; r += kLatT) {
                         const int4 x = p.lat_x[ly.lx0 + r];
-                        const float d1 = __int_as_float(x.w) - tok_cost(tok[x.y]);
+                        const float d1 = __int_as_float(x.w) - okey_val(tok[x.y]);
                         const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
                         p.ex_x[ly.lx0 + r] = ex;
                         const uint32_t k = okey(ex);

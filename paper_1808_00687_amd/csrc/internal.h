@@ -33,6 +33,9 @@
 namespace wfd {
 
 constexpr uint64_t kEmptyTok = ~0ull;
+// Utterance status of a survivor that the record pass found no back-pointer
+// for (never expected: reported as a device error)
+constexpr int kStatusNoBackPointer = -9;
 constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
 constexpr uint32_t kDstMask = 0x7FFFFFFFu;
 constexpr int kHistBits = 12;               // radix-select digit width
@@ -145,17 +148,17 @@ struct Params {
     int32_t reverse;          // expand a set's arc chunks last to first (a debugging permutation)
     UttState *st;
     const UttLayout *lay;
-    // survivors (per utterance regions)
+    // survivors (per utterance regions); the search writes state, cost key,
+    // first emitting record and emitting prefix, the record pass the
+    // back-pointer (source survivor and user arc)
     int32_t *sv_state;
-    uint64_t *sv_tok;
-    int32_t *sv_prev;
+    uint32_t *sv_key;         // ordered key of the token cost
+    int32_t *sv_prev;         // survivor the back-pointer arc leaves from (-1 for the start token)
+    int32_t *sv_arc;          // back-pointer user arc (-1 for the start token)
     int32_t *sv_ebeg;         // first emitting arc record of the survivor's state
     int32_t *sv_epre;         // exclusive prefix of emitting out-degree within the token set
-    int4 *sv_x;               // epsilon out-degree of the survivor's state and its first
-                              // epsilon arc {degree, dst | has_eps << 31, weight bits, user arc}
-    int4 *cand;               // emitting candidates of each token set's expansion, in the
-                              // set's emitting region: {src survivor, user arc, cost bits, dst state}
-    int64_t *cand_cnt;        // candidates per token set
+    unsigned long long *sv_win;   // record pass scratch for sets beyond its LDS table:
+                                  // (user arc + 1) << 32 | source survivor of the winning arc
     uint32_t *e_key;          // lattice backward extra cost per survivor (ordered key)
     // lattice raw records {src survivor, dst survivor, user arc, prefix cost bits}
     int4 *lat_e;
@@ -178,7 +181,7 @@ struct Params {
     // search scratch per utterance: token table in device memory (frames that
     // overflow LDS), epsilon item spill lists, emitting candidate lists
     uint32_t *gkeys;          // U x capG
-    unsigned long long *gvals;
+    uint32_t *gvals;
     int32_t *gslots;
     int64_t capG;             // power of two
     uint2 *gspill;            // U x 2 x capO {table slot, cost bits}

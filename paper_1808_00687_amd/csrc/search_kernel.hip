@@ -3,13 +3,15 @@
 // Viterbi beam search of Alg. 1).
 //
 // Frame k (token set S_k) in one workgroup:
-//   1. expansion of the emitting arcs of S_{k-1}: each wave takes up to four
-//      chunks of 64 consecutive arcs of the set, finds their tokens by a
+//   1. expansion of the emitting arcs of S_{k-1}: each wave takes two chunks
+//      of 64 consecutive arcs of the set at a time, finds their tokens by a
 //      64-ary search over the set's emitting-arc prefix (kept in LDS for sets
-//      of up to kSetCache tokens) and issues all their loads together.  The
-//      frame's tokens live in a hash table in LDS (state -> packed token);
-//      recombination is an LDS 64-bit atomicMin on (cost key, arc + 1), the
-//      first touch of a state appends its slot to a slot list;
+//      of up to kSetCache tokens) and issues all their loads together; the
+//      frame's log-likelihood row sits in LDS (loaded during the previous
+//      frame's compaction).  The frame's tokens live in a hash table in LDS
+//      (state -> cost key); recombination is an LDS 32-bit atomicMin on the
+//      ordered cost key, the first touch of a state appends its slot to a
+//      slot list;
 //   2. epsilon closure: every lowered token whose state has epsilon
 //      out-arcs goes to its wave's LDS queue, and each wave relaxes its own
 //      queue until it is empty, with no barrier between the rounds (a
@@ -25,7 +27,10 @@
 //      they are read.
 // Back-pointers and lattice records need nothing the next frame needs: the
 // record kernel derives them afterwards from the stored token sets, every
-// frame of every utterance in parallel.
+// frame of every utterance in parallel (a token's back-pointer is the lowest
+// arc whose candidate cost equals the token's cost, which is what a minimum
+// over (cost, arc) pairs would have kept), so the search keeps costs only
+// and writes nothing per candidate.
 // A frame that reaches more states than the LDS table holds is redone with
 // the same code on a table in device memory.  Every table is private to its
 // workgroup: no device-scope synchronisation and no per-frame launches.
@@ -51,6 +56,7 @@ constexpr int kRelChunks = 2;             // 64-path chunks of closure lists a w
 constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
 constexpr int kOverflow = 1;              // frame result: the table filled up
 constexpr uint32_t kNoKey = 0xFFFFFFFEu;   // a key no state has (state ids are below 2^31)
+constexpr int kRowMax = 6144;             // log-likelihood columns a frame's LDS row holds
 
 static_assert(kHistBins * 4 <= kW * kQueue * 8, "the select histogram aliases the epsilon queues");
 
@@ -74,15 +80,14 @@ __device__ __forceinline__ void table_barrier()
     else lds_barrier();
 }
 
-// Token table of one frame: keys = state (kEmptyKey if free), vals = packed
-// token (kEmptyTok if none).  After compaction a surviving slot's val holds
-// (user arc + 1) << 32 | survivor index, a pruned one kEmptyTok.  `slots`
-// lists the claimed slots in claim order.
+// Token table of one frame: keys = state (kEmptyKey if free), vals = the
+// ordered cost key of the state's token (kEmptyKey if none).  `slots` lists
+// the claimed slots in claim order.
 template <bool G>
 struct Tab {
     using Slot = typename std::conditional<G, int32_t, uint16_t>::type;
     uint32_t *keys;
-    unsigned long long *vals;
+    uint32_t *vals;
     Slot *slots;
     uint32_t mask;
     int fill;
@@ -96,7 +101,6 @@ struct Sh {
     int status;          // sticky error of the utterance
     uint32_t best;       // smallest cost key among the frame's tokens
     int spill_n[2];      // epsilon items in the device-memory lists
-    int ncand;           // emitting candidates listed this frame
     unsigned long long alloc;   // compaction: emitting degrees << 32 | survivors placed
     int xsum;            // compaction: epsilon degrees of the survivors
     int bin, before, cnt;
@@ -110,7 +114,6 @@ struct Run {
     int n_prev;          // |S_{k-1}|
     int a_prev;          // emitting out-arcs of S_{k-1}
     int64_t le, lx;      // emitting and epsilon regions reserved so far
-    int64_t le_prev;     // start of S_{k-1}'s emitting region (its candidates)
     int64_t arcs;
     int64_t eps;         // epsilon out-arcs of the survivors
     int gframes;
@@ -172,19 +175,18 @@ struct WaveQ {
     int scap;        // its capacity
 };
 
-// Offer R candidate tokens per lane (act[r]) to the table; lowered tokens
+// Offer R candidate costs per lane (act[r]) to the table; lowered tokens
 // of states with epsilon out-arcs become items of the wave's queue.  The R
 // offers go through each step together, so that their LDS atomics are in
 // flight at the same time.  With BEST the frame's best key takes the
 // smallest offered key (a caller that has already done so passes false):
 // every offered key is at least the final token of its state, so the minimum
-// is the frame's best token either way.  Called by the whole wave; slot[r]
-// receives the candidate's table slot or -1.
+// is the frame's best token either way.  Called by the whole wave.
 template <bool G, int R, bool BEST>
 __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const bool *act, const uint32_t *d,
-                                      const bool *d_eps, const float *cand, const uint32_t *key, const int32_t *arc,
-                                      int *slot)
+                                      const bool *d_eps, const float *cand, const uint32_t *key)
 {
+    int slot[R];
     // slot of each state: a compare-and-swap on the key claims a free slot
     // or finds the state's own, probing linearly on a collision
     uint32_t h[R], k[R];
@@ -223,19 +225,18 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
             over = true;
         }
     }
-    // recombination: the unsigned minimum of (cost key, arc + 1); issued
-    // before the slot-list add below, so that their LDS round trips overlap
-    // (in LDS without a branch: a lane without a slot takes the minimum of
-    // a slot of its own and the empty token, which changes nothing)
-    unsigned long long v[R], old[R];
+    // recombination: the unsigned minimum of the cost keys; issued before
+    // the slot-list add below, so that their LDS round trips overlap (in LDS
+    // without a branch: a lane without a slot takes the minimum of a slot of
+    // its own and the empty key, which changes nothing)
+    uint32_t old[R];
 #pragma unroll
     for (int r = 0; r < R; r++) {
-        v[r] = make_tok(key[r], arc[r]);
         if constexpr (!G) {
             const uint32_t at = slot[r] >= 0 ? static_cast<uint32_t>(slot[r]) : (h[r] + lane_id()) & t.mask;
-            old[r] = atomicMin(t.vals + at, slot[r] >= 0 ? v[r] : kEmptyTok);
+            old[r] = atomicMin(t.vals + at, slot[r] >= 0 ? key[r] : kEmptyKey);
         } else {
-            old[r] = slot[r] >= 0 ? atomicMin(t.vals + slot[r], v[r]) : 0ull;
+            old[r] = slot[r] >= 0 ? atomicMin(t.vals + slot[r], key[r]) : 0u;
         }
     }
     // newly claimed slots join the slot list, one LDS add per wave
@@ -272,7 +273,7 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
     // lowered tokens whose state has epsilon out-arcs
 #pragma unroll
     for (int r = 0; r < R; r++) {
-        const bool push = slot[r] >= 0 && v[r] < old[r] && d_eps[r];
+        const bool push = slot[r] >= 0 && key[r] < old[r] && d_eps[r];
         const uint64_t m = __ballot(push);
         if (!m) continue;
         if (push) {
@@ -292,12 +293,10 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
 
 // One candidate per lane, the frame's best key included.
 template <bool G>
-__device__ __forceinline__ int offer1(const Tab<G> &t, Sh &sh, WaveQ &wq, bool act, uint32_t d, bool d_eps,
-                                      float cand, uint32_t key, int32_t arc)
+__device__ __forceinline__ void offer1(const Tab<G> &t, Sh &sh, WaveQ &wq, bool act, uint32_t d, bool d_eps,
+                                       float cand, uint32_t key)
 {
-    int slot;
-    offer<G, 1, true>(t, sh, wq, &act, &d, &d_eps, &cand, &key, &arc, &slot);
-    return slot;
+    offer<G, 1, true>(t, sh, wq, &act, &d, &d_eps, &cand, &key);
 }
 
 // Bin holding the rank-th smallest (1-based) of a histogram: sets sh.bin and
@@ -351,27 +350,30 @@ struct SetView<true> {
 
 template <>
 struct SetView<false> {
-    const uint64_t *tok;
+    const uint32_t *key;
     const int32_t *epre;
     const int32_t *ebeg;
     const uint16_t *cs;   // unused
-    __device__ float c(int i) const { return tok_cost(tok[i]); }
+    __device__ float c(int i) const { return okey_val(key[i]); }
 };
 
-// Emitting expansion of S_{k-1} into the table (step 1).
+// Emitting expansion of S_{k-1} into the table (step 1).  The frame's
+// log-likelihood row is read from LDS (srow) when it fits there, else from
+// device memory (grow).
 template <bool G, bool L>
 __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh, const SetView<L> &v, int n_tok,
-                                       int A, int src0, const float *row, WaveQ &wq, int4 *cbuf)
+                                       int A, const float *srow, const float *grow, WaveQ &wq)
 {
     const int lane = lane_id();
     const int wid = threadIdx.x / kWave;
     // a set kept in LDS comes with the first token of each chunk
     const bool use_cs = L && A <= kCs * kWave;
+    const bool row_lds = p.L <= kRowMax;
     const int nch = (A + kWave - 1) / kWave;
     // wave w takes chunks w, w + kW, w + 2 kW, ... : every wave gets work
     for (int c = wid; c * kWave < A; c += kW * kChunks) {
         if (__builtin_amdgcn_readfirstlane(sh.overflow)) break;   // the frame is redone anyway
-        int ob[kChunks], op[kChunks], ot[kChunks], a[kChunks];
+        int ob[kChunks], op[kChunks], a[kChunks];
         float oc[kChunks];
         bool ok[kChunks];
 #pragma unroll
@@ -382,7 +384,7 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
             const int a0 = ch < 0 ? A : ch * kWave;
             a[r] = a0 + lane;
             ok[r] = false;
-            ob[r] = op[r] = ot[r] = 0;
+            ob[r] = op[r] = 0;
             oc[r] = 0.0f;
             if (a0 < A) {
                 // the 64 tokens from the one owning a0, and each lane's owner among them
@@ -400,7 +402,6 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
                 ob[r] = __shfl(eb, o, kWave);
                 op[r] = __shfl(pre, o, kWave);
                 oc[r] = __shfl(cst, o, kWave);
-                ot[r] = t0 + o;
                 ok[r] = a[r] < A;
                 if (ok[r] && a[r] >= win_end) {
                     // past the window (tokens without emitting arcs): search the rest
@@ -413,7 +414,6 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
                     ob[r] = v.ebeg[lo];
                     op[r] = v.epre[lo];
                     oc[r] = v.c(lo);
-                    ot[r] = lo;
                 }
                 ok[r] = ok[r] && op[r] <= a[r];
             }
@@ -423,11 +423,10 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
         for (int r = 0; r < kChunks; r++) rec[r] = ok[r] ? p.g.earc[ob[r] + (a[r] - op[r])] : make_int4(0, 0, 0, 0);
         float lv[kChunks];
 #pragma unroll
-        for (int r = 0; r < kChunks; r++) lv[r] = ok[r] ? ldg(row + rec[r].y) : 0.0f;
+        for (int r = 0; r < kChunks; r++) lv[r] = !ok[r] ? 0.0f : row_lds ? srow[rec[r].y] : ldg(grow + rec[r].y);
         bool act[kChunks], de[kChunks];
         uint32_t d[kChunks], key[kChunks];
         float cnd[kChunks];
-        int32_t arc[kChunks];
         uint32_t km = kEmptyKey;
 #pragma unroll
         for (int r = 0; r < kChunks; r++) {
@@ -437,7 +436,6 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
             if (ok[r] && key[r] < km) km = key[r];
             d[r] = static_cast<uint32_t>(rec[r].x) & kDstMask;
             de[r] = rec[r].x < 0;
-            arc[r] = rec[r].w;
         }
         // The batch's own cheapest candidate tightens the early-drop bound; it
         // is within that bound itself, so it is offered and the frame's best
@@ -448,31 +446,7 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
         const uint32_t bnd = drop_bound(km < cur ? km : cur, p.beam);
 #pragma unroll
         for (int r = 0; r < kChunks; r++) act[r] = ok[r] && key[r] <= bnd;
-        int slot[kChunks];
-        offer<G, kChunks, false>(t, sh, wq, act, d, de, cnd, key, arc, slot);
-        bool keep[kChunks];
-#pragma unroll
-        for (int r = 0; r < kChunks; r++) keep[r] = slot[r] >= 0;
-        // the offered candidates, for the back-pointers and lattice arcs:
-        // one LDS add per wave
-        uint64_t m[kChunks];
-        int pref[kChunks], total = 0;
-#pragma unroll
-        for (int r = 0; r < kChunks; r++) {
-            m[r] = __ballot(keep[r]);
-            pref[r] = total;
-            total += __popcll(m[r]);
-        }
-        if (total) {
-            int b = 0;
-            if (lane == 0) b = atomicAdd(&sh.ncand, total);
-            b = __builtin_amdgcn_readlane(b, 0);
-#pragma unroll
-            for (int r = 0; r < kChunks; r++)
-                if (keep[r])
-                    cbuf[b + pref[r] + rank_in(m[r])] =
-                        make_int4(src0 + ot[r], arc[r], __float_as_int(cnd[r]), static_cast<int>(d[r]));
-        }
+        offer<G, kChunks, false>(t, sh, wq, act, d, de, cnd, key);
     }
 }
 
@@ -496,7 +470,7 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
     int4 x0 = make_int4(0, 0, 0, 0);
     const float cst = __uint_as_float(it.y);
     if (valid) {
-        const uint32_t now = static_cast<uint32_t>(tld<G>(t.vals + it.x) >> 32);
+        const uint32_t now = tld<G>(t.vals + it.x);
         if (okey(cst) == now) {
             const int64_t s = static_cast<int64_t>(tld<G>(t.keys + it.x));
             const int4 lo = p.g.srec[2 * s];
@@ -550,7 +524,6 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             const uint32_t bnd = drop_bound(sh.best, p.beam);
             bool act[kRelChunks], de[kRelChunks];
             uint32_t d[kRelChunks], key[kRelChunks];
-            int32_t arc[kRelChunks];
             float cnd[kRelChunks];
 #pragma unroll
             for (int r = 0; r < kRelChunks; r++) {
@@ -566,12 +539,10 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
                 cnd[r] = c;
                 d[r] = static_cast<uint32_t>(c0[r].x);
                 de[r] = false;
-                arc[r] = c0[r].y;
                 key[r] = okey(c);
                 act[r] = k0 + r * kWave + lane < tot && key[r] <= bnd;
             }
-            int slot[kRelChunks];
-            offer<G, kRelChunks, true>(t, sh, wq, act, d, de, cnd, key, arc, slot);
+            offer<G, kRelChunks, true>(t, sh, wq, act, d, de, cnd, key);
         }
     }
     {
@@ -579,8 +550,7 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
         const uint32_t bnd = drop_bound(sh.best, p.beam);
         const float cnd = cst + __int_as_float(x0.y);
         const uint32_t key = okey(cnd);
-        (void)offer1<G>(t, sh, wq, first && key <= bnd, static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, cnd, key,
-                       x0.z);
+        offer1<G>(t, sh, wq, first && key <= bnd, static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, cnd, key);
     }
     // the other epsilon arcs, spread over the wave
     const int incl = wave_incl_scan(xd);
@@ -595,18 +565,16 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
         const uint32_t bnd = drop_bound(sh.best, p.beam);
         bool act = false, d_eps = false;
         uint32_t d = 0, key = kEmptyKey;
-        int arc = 0;
         float cnd = 0.0f;
         if (kk < tot) {
             const int4 r = p.g.xarc[ob + (kk - op)];
             d = static_cast<uint32_t>(r.x) & kDstMask;
             d_eps = r.x < 0;
-            arc = r.z;
             cnd = oc + __int_as_float(r.y);
             key = okey(cnd);
             act = key <= bnd;
         }
-        (void)offer1<G>(t, sh, wq, act, d, d_eps, cnd, key, arc);
+        offer1<G>(t, sh, wq, act, d, d_eps, cnd, key);
     }
 }
 
@@ -636,8 +604,8 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
 template <bool G>
 __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
                                      const Tab<G> &t, uint2 *aux, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
-                                     uint16_t *s_cs, uint2 *spill, int gcap, Run &run, Prof &pf, int k,
-                                     int &n_ins)
+                                     uint16_t *s_cs, float *s_row, uint2 *spill, int gcap, Run &run, Prof &pf,
+                                     int k, int &n_ins)
 {
     const int tid = threadIdx.x;
     const int lane = lane_id();
@@ -656,7 +624,6 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         sh.overflow = 0;
         sh.best = kEmptyKey;
         sh.spill_n[0] = sh.spill_n[1] = 0;
-        sh.ncand = 0;
         sh.alloc = 0ull;
         sh.xsum = 0;
         sh.cnt = 0;
@@ -670,19 +637,17 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         if (wid == 0) {
             const int s = p.g.start;
             const int4 lo = p.g.srec[2 * static_cast<int64_t>(s)];
-            (void)offer1<G>(t, sh, wq, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0.0f, okey(0.0f), -1);
+            offer1<G>(t, sh, wq, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0.0f, okey(0.0f));
         }
     } else {
         const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k - 1]) * p.L;
-        const int src0 = static_cast<int>(run.prev0);
-        int4 *cbuf = p.cand + ly.le0 + run.le_prev;
         if (run.n_prev <= kSetCache) {
             SetView<true> v{s_cost, s_epre, s_ebeg, s_cs};
-            expand<G, true>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cbuf);
+            expand<G, true>(p, t, sh, v, run.n_prev, run.a_prev, s_row, row, wq);
         } else {
             const int64_t base = ly.sv0 + run.prev0;
-            SetView<false> v{p.sv_tok + base, p.sv_epre + base, p.sv_ebeg + base, nullptr};
-            expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, src0, row, wq, cbuf);
+            SetView<false> v{p.sv_key + base, p.sv_epre + base, p.sv_ebeg + base, nullptr};
+            expand<G, false>(p, t, sh, v, run.n_prev, run.a_prev, s_row, row, wq);
         }
     }
     sub_close(p, pf, 4);
@@ -733,7 +698,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         __syncthreads();
         int cnt = 0;
         for (int i = tid; i < n; i += kT) {
-            const uint32_t key = static_cast<uint32_t>(tld<G>(t.vals + tld<G>(t.slots + i)) >> 32);
+            const uint32_t key = tld<G>(t.vals + tld<G>(t.slots + i));
             if (key <= lim) {
                 cnt++;
                 atomicAdd(&hist[(key - kb) >> shf], 1u);
@@ -753,7 +718,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
                 for (int i = tid; i < nb; i += kT) hist[i] = 0u;
                 __syncthreads();
                 for (int i = tid; i < n; i += kT) {
-                    const uint32_t key = static_cast<uint32_t>(tld<G>(t.vals + tld<G>(t.slots + i)) >> 32);
+                    const uint32_t key = tld<G>(t.vals + tld<G>(t.slots + i));
                     if (key > lim) continue;
                     const uint32_t off = key - kb;
                     if ((off >> shf) == (prefix >> shf)) atomicAdd(&hist[(off >> nsh) & (nb - 1)], 1u);
@@ -779,35 +744,46 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     // gives their positions and the prefix of emitting degrees before them
     // at once.  The order of a token set is internal (sets are reported
     // sorted by state), so no block-wide scan is needed.
+    // The next frame's log-likelihood row is loaded meanwhile (the expansion
+    // that read this frame's row is over: every wave has passed the barrier
+    // after the closure), and stored into LDS at the end.
+    const bool next_row = p.L <= kRowMax && k < Tp;
+    constexpr int kRowPer = kRowMax / kT;
+    float rv[kRowPer];
+    if (next_row) {
+        const float *nrow = ll + static_cast<int64_t>(p.kept[ly.kept0 + k]) * p.L;
+#pragma unroll
+        for (int j = 0; j < kRowPer; j++) {
+            const int i = tid + j * kT;
+            rv[j] = i < p.L ? ldg(nrow + i) : 0.0f;
+        }
+    }
     using Slot = typename Tab<G>::Slot;
     const int64_t set0 = run.set0;
     for (int c = wid; c * kWave < n; c += kW * kCompact) {
         bool kp[kCompact];
-        unsigned long long vv[kCompact];
+        uint32_t vv[kCompact];
         int dd[kCompact];
 #pragma unroll
         for (int r = 0; r < kCompact; r++) {
             const int i = (c + r * kW) * kWave + lane;
             kp[r] = false;
-            vv[r] = kEmptyTok;
+            vv[r] = kEmptyKey;
             dd[r] = 0;
             if (i < n) {
                 const Slot sl = tld<G>(t.slots + i);
                 vv[r] = tld<G>(t.vals + sl);
                 dd[r] = static_cast<int>(tld<G>(t.keys + sl));
-                kp[r] = static_cast<uint32_t>(vv[r] >> 32) <= cut;
+                kp[r] = vv[r] <= cut;
                 t.keys[sl] = kEmptyKey;
-                t.vals[sl] = kEmptyTok;
+                t.vals[sl] = kEmptyKey;
             }
         }
-        int4 lo[kCompact], x0[kCompact];
+        int4 lo[kCompact];
 #pragma unroll
         for (int r = 0; r < kCompact; r++) {
-            lo[r] = x0[r] = make_int4(0, 0, 0, 0);
-            if (kp[r]) {
-                lo[r] = p.g.srec[2 * static_cast<int64_t>(dd[r])];
-                x0[r] = p.g.srec[2 * static_cast<int64_t>(dd[r]) + 1];
-            }
+            lo[r] = make_int4(0, 0, 0, 0);
+            if (kp[r]) lo[r] = p.g.srec[2 * static_cast<int64_t>(dd[r])];
         }
 #pragma unroll
         for (int r = 0; r < kCompact; r++) {
@@ -835,21 +811,27 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             if (rel < ly.svcap) {
                 const int64_t o = ly.sv0 + rel;
                 p.sv_state[o] = dd[r];
-                p.sv_tok[o] = vv[r];
+                p.sv_key[o] = vv[r];
                 p.sv_ebeg[o] = lo[r].x;
                 p.sv_epre[o] = apos;
-                p.sv_x[o] = make_int4(xd, x0[r].x, x0[r].y, x0[r].z);
             } else {
                 sh.status = WFST_ECAPACITY;
             }
             if (pos < kSetCache) {
-                s_cost[pos] = tok_cost(vv[r]);
+                s_cost[pos] = okey_val(vv[r]);
                 s_epre[pos] = apos;
                 s_ebeg[pos] = lo[r].x;
                 // the chunks whose first arc is one of this token's
                 for (int ch = (apos + kWave - 1) / kWave; ch * kWave < apos + deg && ch < kCs; ch++)
                     s_cs[ch] = static_cast<uint16_t>(pos);
             }
+        }
+    }
+    if (next_row) {
+#pragma unroll
+        for (int j = 0; j < kRowPer; j++) {
+            const int i = tid + j * kT;
+            if (i < p.L) s_row[i] = rv[j];
         }
     }
     // the next expansion reads S_k from LDS unless it is larger than the LDS
@@ -867,9 +849,10 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     if (sh.status) return sh.status;
     // Token set k, its cutoff and the lattice record regions of set k: one
     // record per emitting arc of S_k (into S_k+1) at most, one per epsilon
-    // arc of S_k at most.
+    // arc of S_k at most.  The emitting offsets also give the record pass
+    // the emitting arcs of each set.
     const int64_t a_rec = k < Tp ? a_kept : 0;
-    if (run.le + a_rec > ly.lecap || (p.lattice && run.lx + x_kept > ly.lxcap)) return WFST_ECAPACITY;
+    if (p.lattice && (run.le + a_rec > ly.lecap || run.lx + x_kept > ly.lxcap)) return WFST_ECAPACITY;
     // the running values live in LDS: thread 0 updates them, every thread
     // reads them after the next frame's first barrier
     if (tid == 0) {
@@ -877,8 +860,6 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         p.cut_arr[ly.fo0 + k] = cut;
         p.le_off[ly.fo0 + k + 1] = run.le + a_rec;
         p.lx_off[ly.fo0 + k + 1] = run.lx + x_kept;
-        if (k > 0) p.cand_cnt[ly.fo0 + k - 1] = sh.ncand;
-        run.le_prev = run.le;
         run.le += a_rec;
         run.lx += x_kept;
         run.eps += x_kept;
@@ -908,13 +889,15 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
         int32_t ebeg[kSetCache];
         uint16_t slots[kFill];
         uint32_t keys[kSlots];
-        unsigned long long vals[kSlots];
+        uint32_t vals[kSlots];
+        float row[kRowMax];                // the frame's log-likelihood row (L <= kRowMax)
     };
     __shared__ Lds lds;
     Sh &sh = lds.sh;
     Prof &pf = lds.pf;
     uint32_t *s_keys = lds.keys;
-    unsigned long long *s_vals = lds.vals;
+    uint32_t *s_vals = lds.vals;
+    float *s_row = lds.row;
     uint16_t *s_slots = lds.slots;
     uint2 *s_aux = lds.aux;
     float *s_cost = lds.cost;
@@ -954,7 +937,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
 
     for (int i = tid; i < kSlots; i += kT) {
         s_keys[i] = kEmptyKey;
-        s_vals[i] = kEmptyTok;
+        s_vals[i] = kEmptyKey;
     }
     if (tid == 0) {
         sh.status = 0;
@@ -979,24 +962,26 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     for (int k = 0; k <= Tp; k++) {
         int n_ins = 0;
         if (!in_g)
-            rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k, n_ins);
+            rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, run, pf,
+                              k, n_ins);
         if (in_g || rc == kOverflow) {
             if (!in_g) {
                 // the abandoned attempt left states in the LDS table
                 for (int i = tid; i < kSlots; i += kT) {
                     s_keys[i] = kEmptyKey;
-                    s_vals[i] = kEmptyTok;
+                    s_vals[i] = kEmptyKey;
                 }
             }
             if (!gclean) {
                 for (int64_t i = tid; i < p.capG; i += kT) {
                     gt.keys[i] = kEmptyKey;
-                    gt.vals[i] = kEmptyTok;
+                    gt.vals[i] = kEmptyKey;
                 }
                 gclean = true;
             }
             __syncthreads();
-            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, spill, gcap, run, pf, k, n_ins);
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, run, pf,
+                             k, n_ins);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
             if (tid == 0) run.gframes++;
             in_g = n_ins > g_stay;
