@@ -62,7 +62,7 @@ typedef struct wfst_result wfst_result;
  *   num_arcs     E, 0 <= E < 2^31 - 1
  *   src, dst     [E] host int32, src sorted ascending, both in [0, N)
  *   ilabel       [E] host int32 >= 0 (0 = epsilon)
- *   olabel       [E] host int32 >= 0 (0 = none); kept for the caller only
+ *   olabel       [E] host int32 >= 0 (0 = none); read by the word-level lattice
  *   weight       [E] host float32, finite; epsilon arcs need weight >= 0
  *   start_state  in [0, N)  (the start node S of Alg. 1)
  *   final_weight [N] host float32 or NULL; NULL makes every state final with
@@ -103,6 +103,8 @@ int wfst_graph_get_info(const wfst_graph *g, wfst_graph_info *info);
 #define WFST_LOGLIKES_HOST 2u  /* loglikes pointers are host memory (copied to the device first) */
 #define WFST_PROFILE 4u        /* time the kernel phases with HIP events on the decode streams */
 #define WFST_PROFILE_STEPS 8u  /* also read the device clock per step inside the kernels (slower) */
+#define WFST_WORD_LATTICE 16u  /* also build the word-level lattice of the pruned lattice (needs
+                                  lattice_beam >= 0): wfst_result_words */
 
 typedef struct wfst_decode_opts {
     float beam;               /* > 0 (may be +inf): keep tokens with cost <= best + beam */
@@ -114,7 +116,8 @@ typedef struct wfst_decode_opts {
                                  frame t is skipped when ll[t][blank_id] > log(blank_threshold);
                                  <= 0 or NaN: WFST_EINVAL */
     int32_t blank_id;         /* log-likelihood column of the blank unit, in [0, L) */
-    uint32_t flags;           /* WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST | WFST_PROFILE | WFST_PROFILE_STEPS */
+    uint32_t flags;           /* WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST | WFST_PROFILE | WFST_PROFILE_STEPS |
+                                 WFST_WORD_LATTICE */
     int64_t capacity_hint;    /* 0: automatic; else tokens per frame to reserve */
     /* HMM topologies whose blank-like state is one unit per phone (Sec. 2):
        with num_blank_ids > 0, blank_ids[0..num_blank_ids) (host memory,
@@ -280,7 +283,23 @@ typedef struct wfst_stats {
     /* with WFST_PROFILE (batch-wide): from the start of the first search
        launch to the end of the last one (the groups' launches overlap) */
     double search_span_ms;
+    int64_t word_sequences;    /* with WFST_WORD_LATTICE: word sequences of the lattice */
 } wfst_stats;
+
+/*
+ * Word-level lattice (needs WFST_WORD_LATTICE): every word sequence of the
+ * pruned lattice -- the non-zero output labels along a complete lattice path
+ * from the start token to the last token set -- with the best cost of a
+ * complete path that outputs it (final cost included, as for the best path).
+ * This map is what determinising the exact lattice over its output labels
+ * keeps for second-pass rescoring (Sec. 1).  The n sequences are sorted by
+ * cost (ties by the sequence, lexicographically); sequence k is
+ * words[offsets[k] .. offsets[k + 1]); the best one is the best path's.
+ * Host memory owned by the result.  Errors: WFST_EINVAL (r == NULL, decoded
+ * without WFST_WORD_LATTICE), the utterance's status when it has no path.
+ */
+int wfst_result_words(const wfst_result *r, int64_t *n, const int64_t **offsets, const int32_t **words,
+                      const float **costs);
 
 /* Counters and timings of the utterance's decode (the work measures of
    Eq. 3: decoded frames, tokens and arcs expanded).  Errors: WFST_EINVAL. */
@@ -308,8 +327,8 @@ void wfst_result_free(wfst_result *r);
  * must not be made; calls on different devices are independent.
  *
  *   g, L, opts  as for wfst_decode; opts->flags must not contain
- *               WFST_RECORD_TOKENS, WFST_LOGLIKES_HOST, WFST_PROFILE or
- *               WFST_PROFILE_STEPS; opts->capacity_hint sets the tokens per
+ *               WFST_RECORD_TOKENS, WFST_LOGLIKES_HOST, WFST_PROFILE,
+ *               WFST_PROFILE_STEPS or WFST_WORD_LATTICE; opts->capacity_hint sets the tokens per
  *               frame (0: from max_active)
  *   loglikes    [T x L] float32 in device memory of the graph's device
  *   hip_stream  as for wfst_decode (the call is blocking)

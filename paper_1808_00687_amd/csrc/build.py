@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "libwfstdec.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["graph.cpp", "decode.cpp", "search_kernel.hip", "record_kernel.hip", "final_kernels.hip"]
+SOURCES = ["graph.cpp", "decode.cpp", "search_kernel.hip", "record_kernel.hip", "final_kernels.hip", "word_kernel.hip"]
 HEADERS = ["internal.h", "device_util.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -154,6 +154,10 @@ struct wfst_result {
     std::shared_ptr<LatBuf> lat_dev;
     int64_t lat_off = 0, lat_n = 0;
     std::shared_ptr<LatHost> lat_host;   // the batch's lattice in host memory, copied on first use
+    bool has_words = false;
+    std::vector<int64_t> w_off;        // word sequences: offsets into w_words
+    std::vector<int32_t> w_words;
+    std::vector<float> w_cost;
     bool has_tokens = false;
     std::vector<int64_t> tok_off;
     std::vector<int32_t> tok_state, tok_arc;
@@ -215,10 +219,11 @@ struct ArenaCache {
     size_t cap = 0;
 };
 
-ArenaCache &arena_cache(int dev)
+ArenaCache &arena_cache(int dev, int kind = 0)
 {
-    static ArenaCache *c = new ArenaCache[64];
-    return c[dev];
+    // kind 0: the decode workspace; kind 1: the word-lattice pass
+    static ArenaCache *c = new ArenaCache[2 * 64];
+    return c[kind * 64 + dev];
 }
 
 struct ArenaLease {
@@ -228,11 +233,13 @@ struct ArenaLease {
     ArenaLease() = default;
     ArenaLease(const ArenaLease &) = delete;
     ArenaLease &operator=(const ArenaLease &) = delete;
-    hipError_t acquire(int device, size_t need)
+    int kind = 0;
+    hipError_t acquire(int device, size_t need, int which = 0)
     {
         dev = device;
+        kind = which;
         if (dev >= 0 && dev < 64) {
-            ArenaCache &c = arena_cache(dev);
+            ArenaCache &c = arena_cache(dev, kind);
             std::lock_guard<std::mutex> lk(c.mu);
             if (!c.busy) {
                 if (c.cap < need) {
@@ -262,7 +269,7 @@ struct ArenaLease {
     ~ArenaLease()
     {
         if (cached) {
-            ArenaCache &c = arena_cache(dev);
+            ArenaCache &c = arena_cache(dev, kind);
             std::lock_guard<std::mutex> lk(c.mu);
             c.busy = false;
         } else if (ptr) {
@@ -404,6 +411,9 @@ hipStream_t aux_stream(int dev, int i)
     return tab[dev][i];
 }
 
+// run_batch result: the word-lattice tables overflowed (final, not retried)
+constexpr int kWordCapacity = -10;
+
 // Per-frame offset arrays of an utterance: survivors, emitting and epsilon
 // record regions, lattice output, emitting and epsilon record counts.
 constexpr int kOffsetArrays = 6;
@@ -506,6 +516,137 @@ void carve_ws(Arena &a, Params &p, int U, const Totals &tot, UttLayout **d_lay, 
     p.lo_off = f ? f + 3 * fo : nullptr;
     p.le_cnt = f ? f + 4 * fo : nullptr;
     p.lx_cnt = f ? f + 5 * fo : nullptr;
+}
+
+// The word-level lattice of every utterance with a path (after lattice
+// pruning, on stream s, with the decode's workspace still in place): the
+// forward pass over (node, word prefix) in word_kernel.hip, then the listed
+// sequences written out and copied to the results, sorted by cost and
+// sequence.  Capacities start from the lattice sizes and grow on overflow.
+int run_words(const Graph &G, Params &p, int U, const std::vector<UttLayout> &lay, const std::vector<UttState> &st,
+              const Totals &tot, hipStream_t s, std::vector<wfst_result *> &out)
+{
+    int64_t maxk = 1;
+    for (int u = 0; u < U; u++)
+        if (st[u].status == WFST_OK) maxk = std::max<int64_t>(maxk, st[u].lat_kept);
+    int64_t capH = 4096;
+    while (capH < 32 * maxk) capH *= 2;
+    std::vector<int32_t> on(static_cast<size_t>(4) * U);
+    for (int attempt = 0; attempt < 4; attempt++) {
+        const int64_t capW = capH;
+        WordWs ws{};
+        ws.capH = capH;
+        ws.capW = capW;
+        auto carve = [&](Arena &a) {
+            ws.hkey = a.get<unsigned long long>(U * capH);
+            ws.hval = a.get<uint32_t>(U * capH);
+            ws.hnext = a.get<int32_t>(U * capH);
+            ws.ents = a.get<int32_t>(U * capH);
+            ws.heads = a.get<int32_t>(tot.sv);
+            ws.tkey = a.get<unsigned long long>(U * capW);
+            ws.tdep = a.get<int32_t>(U * capW);
+            ws.tbest = a.get<uint32_t>(U * capW);
+            ws.out_id = a.get<int2>(U * (capW + 1));
+            ws.out_n = a.get<int32_t>(4 * U);
+            ws.root_best = a.get<uint32_t>(U);
+            ws.set_start = a.get<int32_t>(tot.fo);
+        };
+        Arena measure;
+        carve(measure);
+        ArenaLease lease;
+        hipError_t e = lease.acquire(G.device, measure.off, 1);
+        if (e != hipSuccess) return hip_fail(e, "decode: word-lattice workspace");
+        Arena arena;
+        arena.base = static_cast<char *>(lease.ptr);
+        carve(arena);
+        auto chk = [&](hipError_t r) {
+            if (e == hipSuccess && r != hipSuccess) e = r;
+        };
+        chk(launch_word(p, ws, s));
+        chk(hipMemcpyAsync(on.data(), ws.out_n, on.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+        chk(hipStreamSynchronize(s));
+        if (e != hipSuccess) return hip_fail(e, "decode: word lattice");
+        bool over = false;
+        for (int u = 0; u < U; u++)
+            if (st[u].status == WFST_OK && on[4 * u + 2] != 0) over = true;
+        if (over) {
+            capH *= 8;
+            continue;
+        }
+        // listed sequences: offsets (n + 1 per utterance) and words
+        std::vector<int64_t> bseq(static_cast<size_t>(U)), bword(static_cast<size_t>(U));
+        int64_t ns = 0, nw = 0;
+        for (int u = 0; u < U; u++) {
+            bseq[u] = ns;
+            bword[u] = nw;
+            if (st[u].status != WFST_OK) continue;
+            ns += on[4 * u];
+            nw += on[4 * u + 1];
+        }
+        const size_t b_off = ((static_cast<size_t>(ns + U) * 8) + 255) & ~static_cast<size_t>(255);
+        const size_t b_words = ((static_cast<size_t>(std::max<int64_t>(nw, 1)) * 4) + 255) & ~static_cast<size_t>(255);
+        const size_t b_base = static_cast<size_t>(U) * 8;
+        std::shared_ptr<LatBuf> obuf;
+        e = lat_take(G.device, b_off + b_words + 2 * b_base, false, obuf);
+        if (e != hipSuccess) return hip_fail(e, "decode: word-lattice output");
+        char *ob = static_cast<char *>(obuf->p);
+        int64_t *d_off = reinterpret_cast<int64_t *>(ob);
+        int32_t *d_words = reinterpret_cast<int32_t *>(ob + b_off);
+        int64_t *d_bseq = reinterpret_cast<int64_t *>(ob + b_off + b_words);
+        int64_t *d_bword = d_bseq + U;
+        chk(hipMemcpyAsync(d_bseq, bseq.data(), b_base, hipMemcpyHostToDevice, s));
+        chk(hipMemcpyAsync(d_bword, bword.data(), b_base, hipMemcpyHostToDevice, s));
+        chk(launch_word_flatten(p, ws, d_off, d_words, d_bseq, d_bword, s));
+        std::vector<int64_t> h_off(static_cast<size_t>(ns + U));
+        std::vector<int32_t> h_words(static_cast<size_t>(std::max<int64_t>(nw, 1)));
+        std::vector<int2> h_id;
+        if (ns + U > 0) chk(hipMemcpyAsync(h_off.data(), d_off, (ns + U) * 8, hipMemcpyDeviceToHost, s));
+        if (nw > 0) chk(hipMemcpyAsync(h_words.data(), d_words, nw * 4, hipMemcpyDeviceToHost, s));
+        std::vector<std::vector<int2>> ids(static_cast<size_t>(U));
+        for (int u = 0; u < U; u++) {
+            if (st[u].status != WFST_OK || on[4 * u] == 0) continue;
+            ids[u].resize(static_cast<size_t>(on[4 * u]));
+            chk(hipMemcpyAsync(ids[u].data(), ws.out_id + u * (capW + 1), on[4 * u] * sizeof(int2),
+                               hipMemcpyDeviceToHost, s));
+        }
+        chk(hipStreamSynchronize(s));
+        if (e != hipSuccess) return hip_fail(e, "decode: word-lattice results");
+        for (int u = 0; u < U; u++) {
+            wfst_result *r = out[u];
+            r->has_words = true;
+            r->w_off.assign(1, 0);
+            r->w_words.clear();
+            r->w_cost.clear();
+            if (st[u].status != WFST_OK) continue;
+            const int n = on[4 * u];
+            const int64_t *of = h_off.data() + bseq[u] + u;
+            const int32_t *wd = h_words.data() + bword[u];
+            // sort by (cost key, sequence)
+            std::vector<int> idx(static_cast<size_t>(n));
+            std::iota(idx.begin(), idx.end(), 0);
+            std::sort(idx.begin(), idx.end(), [&](int a, int b) {
+                const uint32_t ka = static_cast<uint32_t>(ids[u][a].y), kb = static_cast<uint32_t>(ids[u][b].y);
+                if (ka != kb) return ka < kb;
+                return std::lexicographical_compare(wd + of[a], wd + of[a + 1], wd + of[b], wd + of[b + 1]);
+            });
+            r->w_off.reserve(static_cast<size_t>(n) + 1);
+            r->w_cost.reserve(static_cast<size_t>(n));
+            for (int q : idx) {
+                r->w_words.insert(r->w_words.end(), wd + of[q], wd + of[q + 1]);
+                r->w_off.push_back(static_cast<int64_t>(r->w_words.size()));
+                const uint32_t k = static_cast<uint32_t>(ids[u][q].y);
+                const uint32_t bits = (k >> 31) ? (k & 0x7FFFFFFFu) : ~k;
+                float c;
+                std::memcpy(&c, &bits, 4);
+                r->w_cost.push_back(c);
+            }
+            r->stats.word_sequences = n;
+        }
+        return WFST_OK;
+    }
+    set_error("decode: the word-lattice tables overflowed (more than %lld entries per utterance)",
+              static_cast<long long>(capH / 8));
+    return WFST_ECAPACITY;
 }
 
 // One attempt at decoding the batch with the given buffer sizes.  Returns
@@ -698,6 +839,14 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     }
 
     wt.mark("lattice output");
+    if (lattice && (o.flags & WFST_WORD_LATTICE)) {
+        const int wr = run_words(G, p, U, lay, st, tot, s, out);
+        // the decode itself fit: more attempts with larger decode buffers
+        // would not help the word tables
+        if (wr == WFST_ECAPACITY) return kWordCapacity;
+        if (wr != WFST_OK) return wr;
+        wt.mark("word lattice");
+    }
     // gather results
     // the set offsets serve only the token sets; the kept frames are every
     // frame when no frame can be skipped
@@ -887,6 +1036,8 @@ int check_opts(const Graph &G, const wfst_decode_opts &o, int32_t L, float *thr)
         if (o.blank_ids[i] < 0 || o.blank_ids[i] >= L) return fail(WFST_EINVAL, "decode: blank unit out of range");
     if (o.frame_stride < 0) return fail(WFST_EINVAL, "decode: negative frame_stride");
     if (o.capacity_hint < 0) return fail(WFST_EINVAL, "decode: negative capacity_hint");
+    if ((o.flags & WFST_WORD_LATTICE) && !(o.lattice_beam >= 0.0f))
+        return fail(WFST_EINVAL, "decode: the word-level lattice needs lattice_beam >= 0");
     *thr = o.blank_threshold > 1.0f ? std::numeric_limits<float>::infinity()
                                     : static_cast<float>(std::log(static_cast<double>(o.blank_threshold)));
     return WFST_OK;
@@ -979,9 +1130,10 @@ int decode_impl(const wfst_graph *gh, int32_t n_utt, const float *const *loglike
         G.rec_em.store(std::min(em, z.em));
         G.rec_xm.store(std::min(xm, z.xm));
     }
+    if (rc == kWordCapacity) rc = WFST_ECAPACITY;   // message set by the word pass
+    else if (rc == WFST_ECAPACITY) set_error("decode: buffers overflowed; raise capacity_hint");
     if (rc != WFST_OK) {
         for (int u = 0; u < n_utt; u++) delete res[u];
-        if (rc == WFST_ECAPACITY) set_error("decode: buffers overflowed; raise capacity_hint");
         return rc;
     }
     for (int u = 0; u < n_utt; u++) out_array[u] = res[u];
@@ -1113,6 +1265,20 @@ extern "C" int wfst_result_tokens(const wfst_result *r, int32_t j, int32_t *n, c
     return WFST_OK;
 }
 
+extern "C" int wfst_result_words(const wfst_result *r, int64_t *n, const int64_t **offsets, const int32_t **words,
+                                 const float **costs)
+{
+    clear_error();
+    if (!r) return fail(WFST_EINVAL, "wfst_result_words: NULL result");
+    if (!r->has_words) return fail(WFST_EINVAL, "wfst_result_words: decoded without WFST_WORD_LATTICE");
+    if (r->status != WFST_OK) return fail(r->status, "wfst_result_words: utterance has no path");
+    if (n) *n = static_cast<int64_t>(r->w_cost.size());
+    if (offsets) *offsets = r->w_off.data();
+    if (words) *words = r->w_words.data();
+    if (costs) *costs = r->w_cost.data();
+    return WFST_OK;
+}
+
 extern "C" int wfst_result_stats(const wfst_result *r, wfst_stats *stats)
 {
     clear_error();
@@ -1208,7 +1374,7 @@ int noalloc_impl(const wfst_graph *gh, const float *ll, int32_t T, int32_t L, co
     out->path_len = 0;
     out->lattice_n = 0;
     out->num_decoded = 0;
-    if (o.flags & (WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST | WFST_PROFILE | WFST_PROFILE_STEPS))
+    if (o.flags & (WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST | WFST_PROFILE | WFST_PROFILE_STEPS | WFST_WORD_LATTICE))
         return fail(WFST_EINVAL, "wfst_decode_noalloc: token recording, host log-likelihoods and profiling "
                                  "are not available");
     if (T < 0) return fail(WFST_EINVAL, "wfst_decode_noalloc: negative T");

@@ -82,6 +82,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
 
     std::vector<int32_t> eoff, xoff, arc_src;
     std::vector<int4> earc, xarc, srec, ctab;
+    std::vector<int2> uarc;
     int64_t n_closure = 0;
     std::vector<uint8_t> has_eps;
     int32_t depth = 0;
@@ -124,6 +125,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
         earc.resize(static_cast<size_t>(n_emit));
         xarc.resize(static_cast<size_t>(n_eps));
         arc_src.resize(static_cast<size_t>(e));
+        uarc.resize(static_cast<size_t>(e));
         std::vector<int32_t> ef(eoff.begin(), eoff.end() - 1), xf(xoff.begin(), xoff.end() - 1);
         for (int64_t a = 0; a < e; a++) {
             int32_t s = src[a], d = dst[a];
@@ -131,9 +133,11 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
             int32_t wb;
             std::memcpy(&wb, &weight[a], 4);
             if (ilabel[a]) {
+                uarc[a] = make_int2(olabel[a], ef[s]);
                 earc[ef[s]++] = make_int4(dflag, ilabel[a] - 1, wb, static_cast<int32_t>(a));
                 arc_src[a] = s;
             } else {
+                uarc[a] = make_int2(olabel[a], xf[s]);
                 xarc[xf[s]++] = make_int4(dflag, wb, static_cast<int32_t>(a), 0);
                 arc_src[a] = s | static_cast<int32_t>(0x80000000u);
             }
@@ -203,7 +207,8 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     const size_t b_fin = final_weight ? align(static_cast<size_t>(n) * 4) : 0;
     const size_t b_srec = align(static_cast<size_t>(n) * 32);
     const size_t b_ctab = align(ctab.size() * 16 + 16);
-    const size_t total = b_eoff + b_xoff + b_earc + b_xarc + b_src + b_fin + b_srec + b_ctab;
+    const size_t b_uarc = align(static_cast<size_t>(e) * 8 + 8);
+    const size_t total = b_eoff + b_xoff + b_earc + b_xarc + b_src + b_fin + b_srec + b_ctab + b_uarc;
 
     wfst_graph *h = new (std::nothrow) wfst_graph();
     if (!h) return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
@@ -239,6 +244,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     g.d.final_w = final_weight ? static_cast<const float *>(put(final_weight, static_cast<size_t>(n) * 4, b_fin)) : nullptr;
     g.d.srec = static_cast<const int4 *>(put(srec.data(), srec.size() * 16, b_srec));
     g.d.ctab = static_cast<const int4 *>(put(ctab.data(), ctab.size() * 16, b_ctab));
+    g.d.uarc = static_cast<const int2 *>(put(uarc.data(), uarc.size() * 8, b_uarc));
     if (err != hipSuccess) {
         (void)hipFree(mem);
         delete h;

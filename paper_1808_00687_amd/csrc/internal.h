@@ -61,6 +61,7 @@ struct DevGraph {
                         // whose 4th word is the state's closure list
                         // ((offset + 1) << kClosureSizeBits | size - 1, or 0)
     const int4 *ctab;   // closure entries, 3 x int4 each: {dst, user arc, path length, w0}, {w1..w4}, {w5..w8}
+    const int2 *uarc;   // per user arc: {olabel, index of its record in earc or xarc}
 };
 
 // Epsilon-closure lists (built by wfst_load): at most kClosureMax paths of at
@@ -188,6 +189,44 @@ struct Params {
     int64_t capO;
 };
 
+// Workspace of the word-level lattice pass (word_kernel.hip), uniform
+// capacities per utterance: capH (node, word prefix) entries, capW word-trie
+// nodes (both powers of two).
+struct WordWs {
+    unsigned long long *hkey;   // U x capH: node << 32 | trie id (~0 = free)
+    uint32_t *hval;             // U x capH: cost key of the entry
+    int32_t *hnext;             // U x capH: next entry of the same node
+    int32_t *ents;              // U x capH: entries in claim order
+    int32_t *heads;             // per survivor (utterance survivor regions): first entry of the node
+    unsigned long long *tkey;   // U x capW: parent << 32 | word (~0 = free)
+    int32_t *tdep;              // U x capW: sequence length of the node
+    uint32_t *tbest;            // U x capW: best total cost key of the sequence
+    int2 *out_id;               // U x (capW + 1): listed sequences {trie id (-1 = empty), cost key}
+    int32_t *out_n;             // U x 4: sequences, words, status
+    uint32_t *root_best;        // U: best total of the empty sequence
+    int32_t *set_start;         // per token set (utterance frame regions): first entry of the set
+    int64_t capH, capW;
+};
+
+// The slices of utterance u.
+__host__ __device__ inline WordWs word_ws_of(const WordWs &w, int u, const UttLayout &ly)
+{
+    WordWs r = w;
+    r.hkey += u * w.capH;
+    r.hval += u * w.capH;
+    r.hnext += u * w.capH;
+    r.ents += u * w.capH;
+    r.tkey += u * w.capW;
+    r.tdep += u * w.capW;
+    r.tbest += u * w.capW;
+    r.out_id += u * (w.capW + 1);
+    r.out_n += 4 * u;
+    r.root_best += u;
+    r.heads += ly.sv0;
+    r.set_start += ly.fo0;
+    return r;
+}
+
 // ---- launchers (search_kernel.hip / final_kernels.hip) ----
 hipError_t launch_classify(const Params &p, hipStream_t s);
 hipError_t launch_search(const Params &p, hipStream_t s);
@@ -197,6 +236,9 @@ hipError_t launch_finish(const Params &p, hipStream_t s);
 hipError_t launch_pack_paths(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);
 hipError_t launch_zero(void *ptr, size_t bytes, hipStream_t s);   // ptr 16-byte aligned, bytes % 4 == 0
+hipError_t launch_word(const Params &p, const WordWs &ws, hipStream_t s);
+hipError_t launch_word_flatten(const Params &p, const WordWs &ws, int64_t *off, int32_t *words,
+                               const int64_t *base_seq, const int64_t *base_word, hipStream_t s);
 
 // ---- host helpers (graph.cpp) ----
 void set_error(const char *fmt, ...);

@@ -32,6 +32,7 @@ WFST_RECORD_TOKENS = 1
 WFST_LOGLIKES_HOST = 2
 WFST_PROFILE = 4
 WFST_PROFILE_STEPS = 8
+WFST_WORD_LATTICE = 16
 
 
 class WfstError(RuntimeError):
@@ -59,7 +60,8 @@ class _Stats(C.Structure):
                 ("lattice_kept", C.c_int64), ("decode_ms", C.c_double), ("search_ms", C.c_double),
                 ("record_ms", C.c_double), ("final_ms", C.c_double), ("search_launches", C.c_int32),
                 ("search_phase_ms", C.c_double * 7), ("backtrace_ms", C.c_double),
-                ("lattice_prune_ms", C.c_double), ("search_span_ms", C.c_double)]
+                ("lattice_prune_ms", C.c_double), ("search_span_ms", C.c_double),
+                ("word_sequences", C.c_int64)]
 
 
 class _DebugOpts(C.Structure):
@@ -114,6 +116,9 @@ def _load_lib():
     lib.wfst_result_tokens.argtypes = [vp, C.c_int32, i32p, C.POINTER(i32p), C.POINTER(f32p),
                                        C.POINTER(i32p)]
     lib.wfst_result_tokens.restype = C.c_int
+    lib.wfst_result_words.argtypes = [vp, C.POINTER(C.c_int64), C.POINTER(C.POINTER(C.c_int64)),
+                                      C.POINTER(i32p), C.POINTER(f32p)]
+    lib.wfst_result_words.restype = C.c_int
     lib.wfst_result_stats.argtypes = [vp, C.POINTER(_Stats)]
     lib.wfst_result_stats.restype = C.c_int
     lib.wfst_result_free.argtypes = [vp]
@@ -253,6 +258,7 @@ class WfstResult:
     tok_cost: Optional[np.ndarray] = None
     tok_arc: Optional[np.ndarray] = None
     stats: Optional[dict] = None
+    words: Optional[list] = None          # word-level lattice: [(word tuple, float32 cost)] sorted by cost
 
     def token_set(self, j: int):
         """(state, cost bits, back-pointer arc) of token set j, sorted by state."""
@@ -289,7 +295,7 @@ def _lattice_views(outs) -> list:
     return views
 
 
-def _collect(h, lattice: bool, tokens: bool, lat=None) -> WfstResult:
+def _collect(h, lattice: bool, tokens: bool, lat=None, words: bool = False) -> WfstResult:
     st = _lib.wfst_result_status(h)
     r = WfstResult(status=st)
     nf, nd = C.c_int32(), C.c_int32()
@@ -318,6 +324,15 @@ def _collect(h, lattice: bool, tokens: bool, lat=None) -> WfstResult:
         r.lat_arc = lat[:, 1]
         r.lat_cost = fl[:, 2]
         r.lat_extra = fl[:, 3]
+    if words:
+        wn = C.c_int64()
+        wo = C.POINTER(C.c_int64)()
+        ww, wc = C.POINTER(C.c_int32)(), C.POINTER(C.c_float)()
+        _check(_lib.wfst_result_words(h, C.byref(wn), C.byref(wo), C.byref(ww), C.byref(wc)), "wfst_result_words")
+        off = _arr(wo, wn.value + 1, np.int64)
+        wl = _arr(ww, int(off[-1]) if wn.value else 0, np.int32)
+        cs = _arr(wc, wn.value, np.float32)
+        r.words = [(tuple(int(x) for x in wl[off[k]:off[k + 1]]), np.float32(cs[k])) for k in range(wn.value)]
     if tokens:
         offs = [0]
         states, costs, arcs = [], [], []
@@ -395,7 +410,7 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
                       lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
                       record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
                       stream=None, profile_steps: bool = False, blank_ids=None,
-                      frame_stride: int = 1) -> List[WfstResult]:
+                      frame_stride: int = 1, word_lattice: bool = False) -> List[WfstResult]:
     """Decode a batch of utterances (wfst_decode_batch).  ``loglikes`` are
     [T_u x L] float32 tensors on the graph's device (or numpy arrays)."""
     keep: list = []
@@ -410,7 +425,8 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
         Ts.append(shape[0])
     n = len(ptrs)
     flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
-        (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0)
+        (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0) | \
+        (WFST_WORD_LATTICE if word_lattice else 0)
     o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint,
               blank_ids, frame_stride, keep)
     parr = (C.c_void_p * n)(*ptrs)
@@ -423,7 +439,7 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
     try:
         lats = _lattice_views(outs) if lattice_beam >= 0 else [None] * n
         for h, lat in zip(outs, lats):
-            res.append(_collect(h, lattice_beam >= 0, record_tokens, lat))
+            res.append(_collect(h, lattice_beam >= 0, record_tokens, lat, word_lattice))
     finally:
         for h in outs:
             _lib.wfst_result_free(h)
@@ -434,13 +450,14 @@ def wfst_decode(graph: WfstGraph, loglikes, beam: float, max_active: int = 0,
                 lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
                 record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
                 stream=None, profile_steps: bool = False, blank_ids=None,
-                frame_stride: int = 1) -> WfstResult:
+                frame_stride: int = 1, word_lattice: bool = False) -> WfstResult:
     """Decode one utterance (wfst_decode).  Returns the result also when the
     status is WFST_ENOPATH; other errors raise WfstError."""
     keep: list = []
     ptr, shape, host = _ll_ptr(loglikes, keep)
     flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
-        (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0)
+        (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0) | \
+        (WFST_WORD_LATTICE if word_lattice else 0)
     o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint,
               blank_ids, frame_stride, keep)
     out = C.c_void_p()
@@ -449,7 +466,7 @@ def wfst_decode(graph: WfstGraph, loglikes, beam: float, max_active: int = 0,
     if rc not in (WFST_OK, WFST_ENOPATH) or not out:
         raise WfstError(rc, "wfst_decode: %s" % wfst_last_error())
     try:
-        return _collect(out, lattice_beam >= 0, record_tokens)
+        return _collect(out, lattice_beam >= 0, record_tokens, None, word_lattice)
     finally:
         _lib.wfst_result_free(out)
 
