@@ -105,6 +105,13 @@ int wfst_graph_get_info(const wfst_graph *g, wfst_graph_info *info);
 #define WFST_PROFILE_STEPS 8u  /* also read the device clock per step inside the kernels (slower) */
 #define WFST_WORD_LATTICE 16u  /* also build the word-level lattice of the pruned lattice (needs
                                   lattice_beam >= 0): wfst_result_words */
+#define WFST_INCREMENTAL_LATTICE 32u /* record and prune the lattice incrementally, beside the
+                                  search on a second stream (Sec. 3): every 32 decoded frames
+                                  the finished frames' lattice arcs are pruned against the
+                                  search frontier, so the raw lattice needs rings of a few
+                                  chunks instead of regions for the whole utterance; the
+                                  result is bit-identical.  Batches of up to 96 utterances
+                                  (larger batches decode without it) */
 
 typedef struct wfst_decode_opts {
     float beam;               /* > 0 (may be +inf): keep tokens with cost <= best + beam */
@@ -117,7 +124,7 @@ typedef struct wfst_decode_opts {
                                  <= 0 or NaN: WFST_EINVAL */
     int32_t blank_id;         /* log-likelihood column of the blank unit, in [0, L) */
     uint32_t flags;           /* WFST_RECORD_TOKENS | WFST_LOGLIKES_HOST | WFST_PROFILE | WFST_PROFILE_STEPS |
-                                 WFST_WORD_LATTICE */
+                                 WFST_WORD_LATTICE | WFST_INCREMENTAL_LATTICE */
     int64_t capacity_hint;    /* 0: automatic; else tokens per frame to reserve */
     /* HMM topologies whose blank-like state is one unit per phone (Sec. 2):
        with num_blank_ids > 0, blank_ids[0..num_blank_ids) (host memory,
@@ -284,6 +291,9 @@ typedef struct wfst_stats {
        launch to the end of the last one (the groups' launches overlap) */
     double search_span_ms;
     int64_t word_sequences;    /* with WFST_WORD_LATTICE: word sequences of the lattice */
+    int64_t lattice_incremental; /* lattice arcs left for the final lattice pruning by the
+                                    incremental pass beside the search (lattice_raw without it) */
+    int64_t workspace_bytes;   /* device workspace of the decode call (batch-wide) */
 } wfst_stats;
 
 /*
@@ -397,10 +407,14 @@ int wfst_decode_noalloc(const wfst_graph *g, const float *loglikes, int32_t T, i
  *   fail_lattice_alloc nonzero: the allocation of the lattice output fails,
  *                      as when device memory is exhausted: the decode returns
  *                      WFST_ENOMEM before launching anything that writes it
+ *   lattice_chunk      token sets per chunk of the incremental lattice pass
+ *                      (WFST_INCREMENTAL_LATTICE); -1 turns the pass off
+ *   lattice_ring       raw records the incremental pass's rings hold (a
+ *                      small ring makes chunks end early and wrap around)
  *
  * opts == NULL restores every default.  Takes effect for decodes started
  * after the call returns.  Errors: WFST_EINVAL for a negative field other
- * than lattice_lds = -1.
+ * than lattice_lds = -1 and lattice_chunk = -1.
  */
 typedef struct wfst_debug_opts {
     int32_t lds_fill;
@@ -410,6 +424,8 @@ typedef struct wfst_debug_opts {
     int32_t lattice_lds;
     int32_t permute;
     int32_t fail_lattice_alloc;
+    int32_t lattice_chunk;
+    int32_t lattice_ring;
 } wfst_debug_opts;
 
 int wfst_set_debug_opts(const wfst_debug_opts *opts);

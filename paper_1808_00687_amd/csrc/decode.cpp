@@ -398,7 +398,19 @@ enum { PH_SEARCH = 0, PH_RECORD = 1, PH_FINAL = 2, PH_COUNT = 3 };
 
 // Streams of the library's own (default priority, per device, created once)
 // on which groups of a batch run beside the caller's stream.
-constexpr int kAuxStreams = 3;
+// (up to three search groups beside the caller's stream, or one stream for
+// the incremental lattice pass)
+constexpr int kGroupStreams = 3;
+constexpr int kAuxStreams = kGroupStreams + 1;
+// Token sets between the search's progress reports to the incremental
+// lattice pass, and the largest batch that uses it (its blocks and the
+// search's must be resident together: two per utterance, one per CU).
+constexpr int kStreamK = 32;
+constexpr int kStreamMaxUtts = 96;
+// The lattice regions with the incremental pass: this fraction of the
+// one-shot regions (the pass keeps a few percent of the raw arcs; an
+// overflow grows every buffer and decodes again)
+constexpr int64_t kCompactDiv = 8;
 
 hipStream_t aux_stream(int dev, int i)
 {
@@ -415,8 +427,10 @@ hipStream_t aux_stream(int dev, int i)
 constexpr int kWordCapacity = -10;
 
 // Per-frame offset arrays of an utterance: survivors, emitting and epsilon
-// record regions, lattice output, emitting and epsilon record counts.
-constexpr int kOffsetArrays = 6;
+// record regions, lattice output, emitting and epsilon record counts, and the
+// the search's reservations (arrays of their own with the incremental
+// lattice pass).
+constexpr int kOffsetArrays = 8;
 
 // Element counts of the workspace regions summed over a batch.
 struct Totals {
@@ -424,7 +438,7 @@ struct Totals {
 };
 
 // Regions of one utterance of Tu frames, appended after those in `tot`.
-void layout_utt(int64_t Tu, const Sizes &z, bool lattice, int depth, Totals &tot, UttLayout &l)
+void layout_utt(int64_t Tu, const Sizes &z, bool lattice, int depth, Totals &tot, UttLayout &l, int64_t cdiv = 1)
 {
     l.sv0 = tot.sv;
     // survivor indices are 32-bit; one frame may reach capF tokens
@@ -434,10 +448,10 @@ void layout_utt(int64_t Tu, const Sizes &z, bool lattice, int depth, Totals &tot
     // emitting out-arc of its tokens, its epsilon region one per epsilon
     // out-arc
     l.le0 = tot.le;
-    l.lecap = lattice ? (Tu * z.capA + z.capF) * z.em : 0;
+    l.lecap = lattice ? std::max<int64_t>((Tu * z.capA + z.capF) * z.em / cdiv, z.capF * z.em) : 0;
     tot.le += l.lecap;
     l.lx0 = tot.lx;
-    l.lxcap = lattice ? ((Tu + 1) * z.capA + z.capF) * z.xm : 0;
+    l.lxcap = lattice ? std::max<int64_t>(((Tu + 1) * z.capA + z.capF) * z.xm / cdiv, z.capF * z.xm) : 0;
     tot.lx += l.lxcap;
     l.fo0 = tot.fo;
     tot.fo += Tu + 2;
@@ -451,7 +465,7 @@ void layout_utt(int64_t Tu, const Sizes &z, bool lattice, int depth, Totals &tot
 
 // Option-derived kernel parameters shared by every decode entry point.
 void set_params(Params &p, const Graph &G, int U, int L, const wfst_decode_opts &o, float thr,
-                const wfst_debug_opts &dbg, const Sizes &z, int n_blank)
+                const wfst_debug_opts &dbg, const Sizes &z, int n_blank, bool stream)
 {
     p.g = G.d;
     p.U = U;
@@ -474,11 +488,26 @@ void set_params(Params &p, const Graph &G, int U, int L, const wfst_decode_opts 
     p.capG = 8192;
     while (p.capG < z.capT) p.capG *= 2;
     p.capO = z.capO;
+    // the incremental lattice pass: chunks of stream_k token sets, rings
+    // for two chunks' raw records
+    p.stream_k = 0;
+    p.rce = p.rcx = 0;
+    if (stream && p.lattice && (o.flags & WFST_INCREMENTAL_LATTICE) && dbg.lattice_chunk >= 0) {
+        p.stream_k = dbg.lattice_chunk > 0 ? dbg.lattice_chunk : kStreamK;
+        const int64_t per = 2 * p.stream_k * z.capA + 2 * z.capF;
+        p.rce = per * z.em;
+        p.rcx = per * z.xm;
+        if (dbg.lattice_ring > 0) {
+            p.rce = std::min<int64_t>(p.rce, dbg.lattice_ring);
+            p.rcx = std::min<int64_t>(p.rcx, dbg.lattice_ring);
+        }
+    }
 }
 
 // Carve every workspace buffer of U utterances with the region totals
 // `tot` from the arena (a measuring arena only adds up the size).  The
-// per-frame offset arrays come from *fo_all (7 arrays of tot.fo entries).
+// per-frame offset arrays come from *fo_all (kOffsetArrays arrays of tot.fo
+// entries).
 void carve_ws(Arena &a, Params &p, int U, const Totals &tot, UttLayout **d_lay, int64_t **fo_all)
 {
     const bool lattice = p.lattice != 0;
@@ -516,6 +545,20 @@ void carve_ws(Arena &a, Params &p, int U, const Totals &tot, UttLayout **d_lay, 
     p.lo_off = f ? f + 3 * fo : nullptr;
     p.le_cnt = f ? f + 4 * fo : nullptr;
     p.lx_cnt = f ? f + 5 * fo : nullptr;
+    // the reservations: separate arrays when the incremental lattice pass
+    // writes compact offsets into le_off / lx_off while the search still
+    // reserves (possibly on another chiplet), else the same arrays
+    p.rle_off = p.stream_k && f ? f + 6 * fo : p.le_off;
+    p.rlx_off = p.stream_k && f ? f + 7 * fo : p.lx_off;
+    if (p.stream_k) {
+        p.prog = a.get<int32_t>(U);
+        p.rng_e = a.get<int4>(U * p.rce);
+        p.rng_ee = a.get<float>(U * p.rce);
+        p.rng_x = a.get<int4>(U * p.rcx);
+        p.rng_xe = a.get<float>(U * p.rcx);
+        p.rkeys = a.get<uint32_t>(U * p.capG);
+        p.rvals = a.get<int32_t>(U * p.capG);
+    }
 }
 
 // The word-level lattice of every utterance with a path (after lattice
@@ -680,7 +723,11 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
 
     std::vector<UttLayout> lay(U);
     Totals tot;
-    for (int u = 0; u < U; u++) layout_utt(T[u], z, lattice, depth, tot, lay[u]);
+    // with the incremental lattice pass the lattice regions only take the
+    // arcs that pass its pruning, a small part of the raw lattice
+    const bool incremental = lattice && (o.flags & WFST_INCREMENTAL_LATTICE) && U <= kStreamMaxUtts &&
+                             dbg.lattice_chunk >= 0;
+    for (int u = 0; u < U; u++) layout_utt(T[u], z, lattice, depth, tot, lay[u], incremental ? kCompactDiv : 1);
     const int64_t fo = tot.fo, kp = tot.kp;
 
     // the blank-like units: the set when given, else the single blank unit
@@ -688,7 +735,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     if (o.num_blank_ids > 0) blank_h.assign(o.blank_ids, o.blank_ids + o.num_blank_ids);
     else blank_h.push_back(o.blank_id);
     Params p{};
-    set_params(p, G, U, L, o, thr, dbg, z, static_cast<int32_t>(blank_h.size()));
+    set_params(p, G, U, L, o, thr, dbg, z, static_cast<int32_t>(blank_h.size()), U <= kStreamMaxUtts);
     WallTrace wt;
     UttLayout *d_lay = nullptr;
     int64_t *fo_all = nullptr;
@@ -725,6 +772,9 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
     chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
     chk(launch_zero(fo_all, kOffsetArrays * fo * sizeof(int64_t), s));
+    // the progress counts start at 0: a stale count from an earlier decode
+    // would let the lattice pass read token sets before they exist
+    if (p.stream_k) chk(launch_zero(p.prog, U * sizeof(int32_t), s));
     chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), blank_h.data(), blank_h.size() * sizeof(int32_t),
                        hipMemcpyHostToDevice, s));
     chk(launch_classify(p, s));
@@ -734,20 +784,32 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     wt.mark("setup");
 
     // one group per 16 utterances, at most one per stream
-    const int ng = std::max(1, std::min(1 + kAuxStreams, U / 16));
-    std::vector<hipStream_t> gs(static_cast<size_t>(ng), s);
+    // With the incremental lattice pass the whole batch is one search
+    // launch on the caller's stream and one lattice launch beside it on a
+    // stream of the library's (the records are made during the search, so
+    // length groups gain nothing, and every stream more may share a hardware
+    // queue with a waiting lattice launch).  Otherwise one group per 16
+    // utterances, at most one per stream.
+    const bool streaming = p.stream_k > 0;
+    const int ng = streaming ? 1 : std::max(1, std::min(1 + kGroupStreams, U / 16));
+    std::vector<hipStream_t> gs(static_cast<size_t>(ng), s), ls(static_cast<size_t>(ng), nullptr);
     std::vector<hipEvent_t> evs;
     for (int g = 1; g < ng; g++) {
         gs[g] = aux_stream(G.device, g - 1);
         if (!gs[g]) chk(hipErrorOutOfMemory);
     }
-    if (ng > 1 && e == hipSuccess) {
+    if (streaming) {
+        ls[0] = aux_stream(G.device, kGroupStreams);
+        if (!ls[0]) chk(hipErrorOutOfMemory);
+    }
+    if ((ng > 1 || streaming) && e == hipSuccess) {
         hipEvent_t fork = event_pool().get(G.device);
         if (!fork) chk(hipErrorOutOfMemory);
         else {
             evs.push_back(fork);
             chk(hipEventRecord(fork, s));
             for (int g = 1; g < ng; g++) chk(hipStreamWaitEvent(gs[g], fork, 0));
+            if (streaming) chk(hipStreamWaitEvent(ls[0], fork, 0));
         }
     }
     // Group bounds: equal groups, except that with four groups the last
@@ -770,15 +832,40 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         pg.gvals = p.gvals + u0 * p.capG;
         pg.gslots = p.gslots + u0 * p.capG;
         pg.gspill = p.gspill + static_cast<int64_t>(u0) * 2 * p.capO;
+        if (streaming) {
+            pg.prog = p.prog + u0;
+            pg.rng_e = p.rng_e + u0 * p.rce;
+            pg.rng_ee = p.rng_ee + u0 * p.rce;
+            pg.rng_x = p.rng_x + u0 * p.rcx;
+            pg.rng_xe = p.rng_xe + u0 * p.rcx;
+            pg.rkeys = p.rkeys + u0 * p.capG;
+            pg.rvals = p.rvals + u0 * p.capG;
+        }
         int Tg = 0;
         for (int u = u0; u < u1; u++) Tg = std::max(Tg, T[u]);
         const hipStream_t q = gs[g];
         tm.start(q);
         chk(launch_search(pg, q));
         tm.stop(PH_SEARCH, q);
-        tm.start(q);
-        chk(launch_record(pg, Tg, q));
-        tm.stop(PH_RECORD, q);
+        if (streaming) {
+            // the incremental lattice pass follows the search on its own
+            // stream; the final passes wait for it
+            tm.start(ls[g]);
+            chk(launch_lattice_stream(pg, ls[g]));
+            tm.stop(PH_RECORD, ls[g]);
+            hipEvent_t done = event_pool().get(G.device);
+            if (!done) {
+                chk(hipErrorOutOfMemory);
+                break;
+            }
+            evs.push_back(done);
+            chk(hipEventRecord(done, ls[g]));
+            chk(hipStreamWaitEvent(q, done, 0));
+        } else {
+            tm.start(q);
+            chk(launch_record(pg, Tg, q));
+            tm.stop(PH_RECORD, q);
+        }
         tm.start(q);
         chk(launch_final(pg, q));
         chk(launch_finish(pg, q));
@@ -803,6 +890,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     // the groups' streams are done once s is (after an error too, before the
     // workspace is given back)
     for (int g = 1; g < ng; g++) chk(hipStreamSynchronize(gs[g]));
+    for (int g = 0; streaming && g < ng; g++) chk(hipStreamSynchronize(ls[g]));
     for (hipEvent_t x : evs) event_pool().put(G.device, x);
     wt.mark("wait search");
     if (wt.on) {
@@ -813,9 +901,12 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     if (e != hipSuccess) return hip_fail(e, "decode: search");
     for (int u = 0; u < U; u++)
         if (st[u].status == WFST_ECAPACITY) return WFST_ECAPACITY;
-    for (int u = 0; u < U; u++)
+    for (int u = 0; u < U; u++) {
         if (st[u].status == kStatusNoBackPointer)
             return fail(WFST_EDEVICE, "decode: internal error, a surviving token without a back-pointer");
+        if (st[u].status == kStatusStreamTimeout)
+            return fail(WFST_EDEVICE, "decode: internal error, the lattice pass stopped waiting for the search");
+    }
 
     std::shared_ptr<LatBuf> lat_buf;
     std::shared_ptr<LatHost> lat_host;
@@ -886,6 +977,8 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         r->stats.eps_arcs = x.eps_arcs;
         r->stats.lattice_raw = x.le_cnt + x.lx_cnt;
         r->stats.lattice_kept = lattice ? x.lat_kept : 0;
+        r->stats.lattice_incremental = p.stream_k ? x.lat_inc : r->stats.lattice_raw;
+        r->stats.workspace_bytes = static_cast<int64_t>(measure.off);
         if (lattice) {
             r->lat_dev = lat_buf;
             r->lat_host = lat_host;
@@ -1296,7 +1389,8 @@ extern "C" int wfst_set_debug_opts(const wfst_debug_opts *opts)
     if (opts) {
         o = *opts;
         if (o.lds_fill < 0 || o.queue_cap < 0 || o.record_fill < 0 || o.record_big_fill < 0 ||
-            o.lattice_lds < -1 || o.permute < 0 || o.fail_lattice_alloc < 0)
+            o.lattice_lds < -1 || o.permute < 0 || o.fail_lattice_alloc < 0 || o.lattice_chunk < -1 ||
+            o.lattice_ring < 0)
             return fail(WFST_EINVAL, "wfst_set_debug_opts: negative field");
     }
     DebugState &d = debug_state();
@@ -1352,7 +1446,7 @@ size_t noalloc_bytes(const Graph &G, int U, int L, const wfst_decode_opts &o, fl
     UttLayout lay{};
     layout_utt(T, z, o.lattice_beam >= 0.0f, G.eps_depth, tot, lay);
     Params p{};
-    set_params(p, G, U, L, o, thr, dbg, z, n_blank);
+    set_params(p, G, U, L, o, thr, dbg, z, n_blank, false);
     Arena measure;
     UttLayout *d_lay = nullptr;
     int64_t *fo_all = nullptr;
@@ -1435,7 +1529,7 @@ int noalloc_impl(const wfst_graph *gh, const float *ll, int32_t T, int32_t L, co
         if (e != hipSuccess) return hip_fail(e, "wfst_decode_noalloc: workspace address");
     }
     Params p{};
-    set_params(p, G, 1, L, o, thr, dbg, z, n_blank);
+    set_params(p, G, 1, L, o, thr, dbg, z, n_blank, false);
     Arena arena;
     arena.base = static_cast<char *>(ws);
     UttLayout *d_lay = nullptr;

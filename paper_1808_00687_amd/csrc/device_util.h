@@ -156,6 +156,20 @@ __device__ __forceinline__ void lds_barrier()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Wait until this wave's device-memory loads and stores have completed
+// (s_waitcnt vmcnt(0); the other counters left free).  Before a barrier it
+// makes the wave's stores visible in L2 to the block's later atomics and
+// L2 loads, without the cache write-back and invalidation of a device-scope
+// fence.
+__device__ __forceinline__ void vm_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Barrier after which the block's device-memory stores are complete.
+__device__ __forceinline__ void block_sync_vm()
+{
+    vm_wait();
+    __syncthreads();
+}
+
 __device__ __forceinline__ void set_status(UttState &st, int code)
 {
     atomicCAS(&st.status, 0, code);

@@ -36,6 +36,9 @@ constexpr uint64_t kEmptyTok = ~0ull;
 // Utterance status of a survivor that the record pass found no back-pointer
 // for (never expected: reported as a device error)
 constexpr int kStatusNoBackPointer = -9;
+// Utterance status: the incremental lattice pass stopped waiting for the
+// search (never expected: reported as a device error)
+constexpr int kStatusStreamTimeout = -11;
 constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
 constexpr uint32_t kDstMask = 0x7FFFFFFFu;
 constexpr int kHistBits = 12;               // radix-select digit width
@@ -111,6 +114,7 @@ struct UttState {
     int32_t path_len;
     int32_t pad1;
     int64_t lat_kept;
+    int64_t lat_inc;      // lattice records the incremental pass kept for the final pass
     uint64_t phase_ticks[7];   // device clock ticks per search step (profiling only)
     uint64_t finish_ticks[2];  // device clock ticks of the backtrace and the lattice pruning
 };
@@ -147,6 +151,20 @@ struct Params {
     int32_t lat_lds;          // survivors per set the lattice backward pass keeps in LDS (<= its capacity)
     uint32_t hash_mul;        // state hash multiplier of the token tables
     int32_t reverse;          // expand a set's arc chunks last to first (a debugging permutation)
+    // Incremental lattice pass beside the search (stream_k > 0): the search
+    // publishes in prog[u] how many token sets are complete, every stream_k
+    // sets and at the end (-1 when it failed); the lattice pass records the
+    // finished sets into a ring of raw records, prunes them against the
+    // frontier and keeps the survivors in the lattice regions.
+    int32_t stream_k;
+    int32_t *prog;            // per utterance
+    int4 *rng_e;              // U x rce raw emitting records
+    float *rng_ee;            // their extra costs
+    int4 *rng_x;              // U x rcx raw epsilon records
+    float *rng_xe;
+    int64_t rce, rcx;         // ring capacities (records per utterance)
+    uint32_t *rkeys;          // U x capG: the lattice pass's own device-memory table (large sets)
+    int32_t *rvals;
     UttState *st;
     const UttLayout *lay;
     // survivors (per utterance regions); the search writes state, cost key,
@@ -169,8 +187,12 @@ struct Params {
     int4 *lat_out;            // kept lattice {frame, arc, cost bits, extra bits}
     // per-frame arrays (fo0 region): survivor, lattice-record and output offsets
     int64_t *sv_off;
-    int64_t *le_off;          // start of each set's emitting-record region (the search reserves)
-    int64_t *lx_off;          // start of each set's epsilon-record region
+    int64_t *le_off;          // start of each set's emitting lattice records (what the final pass reads)
+    int64_t *lx_off;          // start of each set's epsilon lattice records
+    int64_t *rle_off;         // the search's reservation: one emitting-record slot per emitting out-arc
+    int64_t *rlx_off;         // of each set and one epsilon slot per epsilon out-arc, prefix over the
+                              // sets (the same arrays as le_off / lx_off unless the incremental
+                              // lattice pass compacts the records elsewhere)
     int64_t *lo_off;
     int64_t *le_cnt;          // records in each set's regions (the record kernel writes)
     int64_t *lx_cnt;
@@ -232,6 +254,7 @@ hipError_t launch_classify(const Params &p, hipStream_t s);
 hipError_t launch_search(const Params &p, hipStream_t s);
 hipError_t launch_final(const Params &p, hipStream_t s);
 hipError_t launch_record(const Params &p, int max_frames, hipStream_t s);
+hipError_t launch_lattice_stream(const Params &p, hipStream_t s);
 hipError_t launch_finish(const Params &p, hipStream_t s);
 hipError_t launch_pack_paths(const Params &p, hipStream_t s);
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s);

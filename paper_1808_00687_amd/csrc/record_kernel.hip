@@ -82,16 +82,27 @@ __device__ __forceinline__ int32_t rt_find(const RTab<G> &t, uint32_t s)
     return -1;
 }
 
-// Append one record per lane (rec) at base + a block counter, one LDS add per
-// wave.  The region was reserved large enough by the search.
-__device__ __forceinline__ void append(int4 *buf, int64_t base, int *cnt, bool rec, const int4 &r)
+// Where a set's records go: buf[base + i], or with ring > 0 the ring
+// buf[(base + i) % ring] (base then counts records ever written to it).
+struct RecOut {
+    int4 *buf;
+    int64_t base;
+    int64_t ring;
+};
+
+// Append one record per lane (rec) at a block counter, one LDS add per
+// wave.  The region or ring was reserved large enough.
+__device__ __forceinline__ void append(const RecOut &o, int *cnt, bool rec, const int4 &r)
 {
     const uint64_t m = __ballot(rec);
     if (!m) return;
     int b = 0;
     if (lane_id() == 0) b = atomicAdd(cnt, __popcll(m));
     b = __builtin_amdgcn_readlane(b, 0);
-    if (rec) buf[base + b + rank_in(m)] = r;
+    if (rec) {
+        const int64_t i = o.base + b + rank_in(m);
+        o.buf[o.ring ? i % o.ring : i] = r;
+    }
 }
 
 struct RSh {
@@ -127,9 +138,11 @@ __device__ __forceinline__ bool into_set(const Params &p, const RTab<G> &t, unsi
 
 // Back-pointers and records of token set k of utterance u, with the table t
 // (cleared, of 2^(32 - t.shift) slots) and the winner array win (one entry
-// per survivor of S_k: in LDS, or with GW in device memory).
+// per survivor of S_k: in LDS, or with GW in device memory).  The epsilon
+// records of S_k go to xo, the emitting records into S_k (from S_{k-1}) to eo.
 template <bool G, bool GW>
-__device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsigned long long *win, RSh &sh)
+__device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsigned long long *win, RSh &sh,
+                           const RecOut &eo, const RecOut &xo)
 {
     const UttLayout ly = p.lay[u];
     UttState &st = p.st[u];
@@ -150,10 +163,10 @@ __device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsi
         win[i] = kNoWin;
     }
     if (tid == 0) sh.nx = sh.ne = 0;
+    if constexpr (G || GW) vm_wait();
     __syncthreads();
 
     // ---- 2. the epsilon arcs of S_k ----
-    const int64_t xbase = ly.lx0 + p.lx_off[ly.fo0 + k];
     for (int i0 = wid * kWave; i0 < n; i0 += nw * kWave) {
         const int i = i0 + lane;
         int xd = 0;
@@ -171,7 +184,7 @@ __device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsi
             int4 r4 = make_int4(0, 0, 0, 0);
             const bool rec = into_set<G>(p, t, win, b0, sv_key, cut, xd > 0, cst + __int_as_float(x.y), x.z,
                                          static_cast<int32_t>(b0 + i), static_cast<uint32_t>(x.x) & kDstMask, r4);
-            append(p.lat_x, xbase, &sh.nx, rec, r4);
+            append(xo, &sh.nx, rec, r4);
         }
         // the others, from the epsilon rows, spread over the lanes
         const int xr = max(xd - 1, 0);
@@ -191,7 +204,7 @@ __device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsi
             int4 r4 = make_int4(0, 0, 0, 0);
             const bool rec = into_set<G>(p, t, win, b0, sv_key, cut, q < tot, oc + __int_as_float(y.y), y.z,
                                          static_cast<int32_t>(b0 + i0 + o), static_cast<uint32_t>(y.x) & kDstMask, r4);
-            append(p.lat_x, xbase, &sh.nx, rec, r4);
+            append(xo, &sh.nx, rec, r4);
         }
     }
 
@@ -199,8 +212,7 @@ __device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsi
     if (k > 0) {
         const int64_t b1 = so[k - 1];
         const int n1 = static_cast<int>(b0 - b1);
-        const int64_t r0 = ly.le0 + p.le_off[ly.fo0 + k - 1];
-        const int a1 = static_cast<int>(p.le_off[ly.fo0 + k] - p.le_off[ly.fo0 + k - 1]);
+        const int a1 = static_cast<int>(p.rle_off[ly.fo0 + k] - p.rle_off[ly.fo0 + k - 1]);
         const float *row = st.ll + static_cast<int64_t>(p.kept[ly.kept0 + k - 1]) * p.L;
         for (int i0 = wid * kWave; i0 < n1; i0 += nw * kWave) {
             const int i = i0 + lane;
@@ -233,12 +245,12 @@ __device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsi
                 const bool rec = into_set<G>(p, t, win, b0, sv_key, cut, q < tot, t1 - lv, y.w,
                                              static_cast<int32_t>(b1 + i0 + o), static_cast<uint32_t>(y.x) & kDstMask,
                                              r4);
-                append(p.lat_e, r0, &sh.ne, rec, r4);
+                append(eo, &sh.ne, rec, r4);
             }
         }
     }
     // device-memory winners: every atomic complete before they are read back
-    if constexpr (GW) __threadfence();
+    if constexpr (GW) vm_wait();
     __syncthreads();
 
     // ---- 4. back-pointers ----
@@ -264,6 +276,18 @@ __device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsi
         atomicAdd(reinterpret_cast<unsigned long long *>(&st.lx_cnt), static_cast<unsigned long long>(sh.nx));
         atomicAdd(reinterpret_cast<unsigned long long *>(&st.le_cnt), static_cast<unsigned long long>(sh.ne));
     }
+}
+
+// The lattice regions the search reserved for set k: emitting records into
+// S_k (the region of S_{k-1}) and epsilon records of S_k.
+__device__ __forceinline__ RecOut lin_e(const Params &p, const UttLayout &ly, int k)
+{
+    return RecOut{p.lat_e, k > 0 ? ly.le0 + p.rle_off[ly.fo0 + k - 1] : 0, 0};
+}
+
+__device__ __forceinline__ RecOut lin_x(const Params &p, const UttLayout &ly, int k)
+{
+    return RecOut{p.lat_x, ly.lx0 + p.rlx_off[ly.fo0 + k], 0};
 }
 
 // One block per (set k, utterance u) whose set fits the LDS table.
@@ -295,7 +319,7 @@ __global__ __launch_bounds__(kRT) void record_kernel(Params p)
     t.mul = p.hash_mul;
     for (int i = threadIdx.x; i < (1 << bits); i += blockDim.x) s_keys[i] = kEmptyKey;
     __syncthreads();
-    record_set<false, false>(p, u, k, t, s_win, sh);
+    record_set<false, false>(p, u, k, t, s_win, sh, lin_e(p, ly, k), lin_x(p, ly, k));
 }
 
 // The sets too large for record_kernel's table: kLargeParts blocks per
@@ -353,19 +377,282 @@ __global__ __launch_bounds__(kRT) void record_large_kernel(Params p)
                 t.mul = p.hash_mul;
                 for (int j = threadIdx.x; j < (1 << bits); j += blockDim.x) s_keys[j] = kEmptyKey;
                 __syncthreads();
-                record_set<false, true>(p, u, kk, t, win, sh);
+                record_set<false, true>(p, u, kk, t, win, sh, lin_e(p, ly, kk), lin_x(p, ly, kk));
             } else {
                 if (part != 0) continue;
                 for (int64_t j = threadIdx.x; j < p.capG; j += blockDim.x) gt.keys[j] = kEmptyKey;
                 __syncthreads();
-                record_set<true, true>(p, u, kk, gt, win, sh);
+                record_set<true, true>(p, u, kk, gt, win, sh, lin_e(p, ly, kk), lin_x(p, ly, kk));
             }
             __syncthreads();
         }
     }
 }
 
+// ---------------------------------------------------------------------------
+// Incremental lattice pass beside the search (the paper runs lattice
+// pruning on a stream of its own, concurrently with decoding, Sec. 3).
+//
+// One block per utterance follows the search: every stream_k token sets it
+// records the finished sets (back-pointers, and raw lattice records into a
+// ring) and prunes the raw records of the chunk against the frontier: with
+// the extra cost of every token of the frontier set taken as 0, the backward
+// pass gives each arc a lower bound of its final extra cost (every final
+// extra cost is >= 0, and each step fl(fl(p - c) + e) is monotone in e),
+// so an arc whose bound already exceeds the lattice beam is never kept, and
+// removing it changes no kept arc's extra cost (a node with an extra cost
+// within the beam keeps the out-arc that gives it).  The survivors are
+// appended to the lattice regions, where the final pass (finish_kernel)
+// prunes them exactly.  The raw records thus need a ring of a chunk's size
+// instead of regions for the whole utterance.
+// ---------------------------------------------------------------------------
+
+constexpr long long kSpinLimit = 1LL << 30;   // polls of the progress count before giving up
+struct LSh {
+    RSh r;
+    int prog;
+    int cnt;
+    int flag;
+};
+
+// Wait until the search has published at least `need` finished token sets
+// (or failed: -1).  Thread 0 polls with relaxed loads (an acquire on every
+// poll would invalidate the caches the searches on the same chiplet use);
+// one acquire fence after the count is seen makes the sets visible.
+// Returns the count, or -2 after the spin limit.
+__device__ __forceinline__ int wait_sets(const Params &p, int u, int need, LSh &sh)
+{
+    if (threadIdx.x == 0) {
+        int v = 0;
+        for (long long i = 0;; i++) {
+            v = __hip_atomic_load(p.prog + u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (v >= need || v < 0) break;
+            if (i >= kSpinLimit) {
+                v = -2;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(64);
+        }
+        sh.prog = v;
+    }
+    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    return sh.prog;
+}
+
+// Extra-cost lower bounds of the raw records of source sets [a, b) with the
+// extra cost of every token of set b taken as 0 (the frontier), then the
+// records within the lattice beam appended to the lattice regions.  With
+// b > Tp (the last chunk) every record is kept for the final pass.
+// Returns 0 or WFST_ECAPACITY.
+__device__ int prune_chunk(const Params &p, int u, const UttLayout &ly, int a, int b, int Tp, LSh &sh, int64_t &ke,
+                           int64_t &kx)
+{
+    const int tid = threadIdx.x;
+    const int nt = blockDim.x;
+    const int64_t *so = p.sv_off + ly.fo0;
+    const uint32_t *key = p.sv_key + ly.sv0;
+    uint32_t *eg = p.e_key + ly.sv0;
+    const int4 *re = p.rng_e + u * p.rce;
+    float *ree = p.rng_ee + u * p.rce;
+    const int4 *rx = p.rng_x + u * p.rcx;
+    float *rxe = p.rng_xe + u * p.rcx;
+    const float lb = p.lattice_beam;
+    const uint32_t kinf = okey(__int_as_float(0x7F800000));
+    const bool last = b > Tp;
+    if (!last) {
+        for (int64_t i = so[b] + tid; i < so[b + 1]; i += nt) eg[i] = okey(0.0f);
+        block_sync_vm();
+        for (int j = b - 1; j >= a; j--) {
+            for (int64_t i = so[j] + tid; i < so[j + 1]; i += nt) eg[i] = kinf;
+            block_sync_vm();
+            const int64_t e0 = p.rle_off[ly.fo0 + j], ne = p.le_cnt[ly.fo0 + j];
+            for (int64_t r = tid; r < ne; r += nt) {
+                const int64_t q = (e0 + r) % p.rce;
+                const int4 x = re[q];
+                const float d1 = __int_as_float(x.w) - okey_val(key[x.y]);
+                const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
+                ree[q] = ex;
+                atomicMin(eg + x.x, okey(ex));
+            }
+            block_sync_vm();
+            const int64_t x0 = p.rlx_off[ly.fo0 + j], nx = p.lx_cnt[ly.fo0 + j];
+            while (nx > 0) {
+                if (tid == 0) sh.flag = 0;
+                block_sync_vm();
+                int changed = 0;
+                for (int64_t r = tid; r < nx; r += nt) {
+                    const int64_t q = (x0 + r) % p.rcx;
+                    const int4 x = rx[q];
+                    const float d1 = __int_as_float(x.w) - okey_val(key[x.y]);
+                    const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
+                    rxe[q] = ex;
+                    const uint32_t k = okey(ex);
+                    if (k < ld_relaxed(eg + x.x)) {
+                        atomicMin(eg + x.x, k);
+                        changed = 1;
+                    }
+                }
+                if (changed) sh.flag = 1;
+                block_sync_vm();
+                const int again = sh.flag;
+                block_sync_vm();
+                if (!again) break;
+            }
+        }
+    }
+    block_sync_vm();
+    // the survivors of each source set, appended to the lattice regions
+    for (int j = a; j < b && j <= Tp; j++) {
+        for (int kind = 0; kind < 2; kind++) {
+            const bool em = kind == 0;
+            if (em && j == Tp) {
+                if (tid == 0) {
+                    p.le_off[ly.fo0 + j] = ke;
+                    p.le_cnt[ly.fo0 + j] = 0;
+                }
+                continue;
+            }
+            const int64_t r0 = em ? p.rle_off[ly.fo0 + j] : p.rlx_off[ly.fo0 + j];
+            const int64_t n = em ? p.le_cnt[ly.fo0 + j] : p.lx_cnt[ly.fo0 + j];
+            const int64_t ring = em ? p.rce : p.rcx;
+            const int4 *src = em ? re : rx;
+            const float *sx = em ? ree : rxe;
+            int4 *dst = em ? p.lat_e + ly.le0 : p.lat_x + ly.lx0;
+            const int64_t cap = em ? ly.lecap : ly.lxcap;
+            int64_t &fill = em ? ke : kx;
+            if (tid == 0) sh.cnt = 0;
+            block_sync_vm();
+            for (int64_t r0i = 0; r0i < n; r0i += nt) {
+                const int64_t r = r0i + tid;
+                bool keep = false;
+                int4 x = make_int4(0, 0, 0, 0);
+                if (r < n) {
+                    const int64_t q = (r0 + r) % ring;
+                    x = src[q];
+                    keep = last || sx[q] <= lb;
+                }
+                const uint64_t m = __ballot(keep);
+                int bw = 0;
+                if (m && lane_id() == 0) bw = atomicAdd(&sh.cnt, __popcll(m));
+                bw = __builtin_amdgcn_readlane(bw, 0);
+                if (keep) {
+                    const int64_t at = fill + bw + rank_in(m);
+                    if (at < cap) dst[at] = x;
+                }
+            }
+            block_sync_vm();
+            const int c = sh.cnt;
+            block_sync_vm();
+            if (fill + c > cap) return WFST_ECAPACITY;
+            if (tid == 0) {
+                if (em) {
+                    p.le_off[ly.fo0 + j] = fill;
+                    p.le_cnt[ly.fo0 + j] = c;
+                } else {
+                    p.lx_off[ly.fo0 + j] = fill;
+                    p.lx_cnt[ly.fo0 + j] = c;
+                }
+            }
+            fill += c;
+        }
+    }
+    block_sync_vm();
+    return 0;
+}
+
+__global__ __launch_bounds__(kRT) void lattice_stream_kernel(Params p)
+{
+    __shared__ uint32_t s_keys[kRSlots];
+    __shared__ int32_t s_vals[kRSlots];
+    __shared__ unsigned long long s_win[kRFill];
+    __shared__ LSh sh;
+    const int u = blockIdx.x;
+    UttState &st = p.st[u];
+    const int Tp = st.Tp;   // from the classify kernel, before the search
+    const UttLayout &ly = p.lay[u];
+    const int64_t *so = p.sv_off + ly.fo0;
+    const int64_t *rle = p.rle_off + ly.fo0;
+    const int64_t *rlx = p.rlx_off + ly.fo0;
+    const int K = p.stream_k;
+    int4 *re = p.rng_e + u * p.rce;
+    int4 *rx = p.rng_x + u * p.rcx;
+    RTab<true> gt;
+    const int64_t gbase = static_cast<int64_t>(u) * p.capG;
+    gt.keys = p.rkeys + gbase;
+    gt.vals = p.rvals + gbase;
+    gt.mask = static_cast<uint32_t>(p.capG - 1);
+    gt.shift = 32 - (31 - __clz(static_cast<int>(p.capG)));
+    gt.mul = p.hash_mul;
+    int64_t ke = 0, kx = 0;       // records kept in the lattice regions
+    int rec = 0;                  // token sets recorded
+    int prog = 0;
+    int a = 0;                    // first source set not pruned yet
+    int rc = 0;
+    // A set's raw records sit in the rings at its reserved offsets (the
+    // search reserves one slot per out-arc of the set), modulo the ring: the
+    // emitting records of source set j from rle[j], its epsilon records from
+    // rlx[j].  A chunk of source sets [a, b) and the epsilon records of set b
+    // must fit the rings at once.
+    while (a <= Tp) {
+        const int bmax = min(a + K, Tp + 1);
+        const int need = min(bmax, Tp) + 1;
+        if (prog < need) {
+            prog = wait_sets(p, u, need, sh);
+            if (prog < 0) {
+                rc = prog == -2 ? kStatusStreamTimeout : 0;
+                break;
+            }
+        }
+        // record sets up to bmax while the rings hold them: set k brings the
+        // emitting records of source set k - 1 and the epsilon records of k
+        int b = bmax;
+        for (int k = rec; k <= min(bmax, Tp); k++) {
+            if (rle[k] - rle[a] > p.rce || rlx[k + 1] - rlx[a] > p.rcx) {
+                b = k - 1;
+                break;
+            }
+            const int n = static_cast<int>(so[k + 1] - so[k]);
+            const RecOut eo{re, k > 0 ? rle[k - 1] : 0, p.rce}, xo{rx, rlx[k], p.rcx};
+            if (n <= min(kRFill, p.rec_fill)) {
+                int bits = 10;
+                while (bits < kRSlotBits && (1 << bits) < 2 * n) bits++;
+                RTab<false> t;
+                t.keys = s_keys;
+                t.vals = s_vals;
+                t.mask = (1u << bits) - 1u;
+                t.shift = 32 - bits;
+                t.mul = p.hash_mul;
+                for (int i = threadIdx.x; i < (1 << bits); i += blockDim.x) s_keys[i] = kEmptyKey;
+                __syncthreads();
+                record_set<false, false>(p, u, k, t, s_win, sh.r, eo, xo);
+            } else {
+                for (int64_t j = threadIdx.x; j < p.capG; j += blockDim.x) gt.keys[j] = kEmptyKey;
+                block_sync_vm();
+                record_set<true, true>(p, u, k, gt, p.sv_win + ly.sv0 + so[k], sh.r, eo, xo);
+            }
+            rec = k + 1;
+            __syncthreads();
+        }
+        if (b <= a) {
+            rc = WFST_ECAPACITY;   // one token set does not fit the rings
+            break;
+        }
+        rc = prune_chunk(p, u, ly, a, b, Tp, sh, ke, kx);
+        if (rc) break;
+        a = b;
+    }
+    if (rc && threadIdx.x == 0) set_status(st, rc);
+    if (!rc && threadIdx.x == 0) st.lat_inc = ke + kx;
+}
+
 }  // namespace
+
+hipError_t launch_lattice_stream(const Params &p, hipStream_t s)
+{
+    hipLaunchKernelGGL(lattice_stream_kernel, dim3(p.U), dim3(kRT), 0, s, p);
+    return hipGetLastError();
+}
 
 hipError_t launch_record(const Params &p, int max_frames, hipStream_t s)
 {

@@ -852,14 +852,17 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     // arc of S_k at most.  The emitting offsets also give the record pass
     // the emitting arcs of each set.
     const int64_t a_rec = k < Tp ? a_kept : 0;
-    if (p.lattice && (run.le + a_rec > ly.lecap || run.lx + x_kept > ly.lxcap)) return WFST_ECAPACITY;
+    // (with the incremental lattice pass the regions only bound the ring use
+    // per set; the pass checks its own capacities)
+    if (p.lattice && !p.stream_k && (run.le + a_rec > ly.lecap || run.lx + x_kept > ly.lxcap))
+        return WFST_ECAPACITY;
     // the running values live in LDS: thread 0 updates them, every thread
     // reads them after the next frame's first barrier
     if (tid == 0) {
         p.sv_off[ly.fo0 + k + 1] = set0 + ns;
         p.cut_arr[ly.fo0 + k] = cut;
-        p.le_off[ly.fo0 + k + 1] = run.le + a_rec;
-        p.lx_off[ly.fo0 + k + 1] = run.lx + x_kept;
+        p.rle_off[ly.fo0 + k + 1] = run.le + a_rec;
+        p.rlx_off[ly.fo0 + k + 1] = run.lx + x_kept;
         run.le += a_rec;
         run.lx += x_kept;
         run.eps += x_kept;
@@ -908,7 +911,10 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     const int u = blockIdx.x;
     const int tid = threadIdx.x;
     UttState &st = p.st[u];
-    if (st.status != 0) return;
+    if (st.status != 0) {
+        if (p.stream_k && tid == 0) __hip_atomic_store(p.prog + u, -1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
     // the layout is copied into registers: a reference into device memory
     // would be reloaded after every barrier
     const UttLayout ly = p.lay[u];
@@ -987,6 +993,15 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
             in_g = n_ins > g_stay;
         }
         if (rc != 0) break;
+        // publish every stream_k finished token sets to the incremental
+        // lattice pass: every wave's stores of the sets complete in L2 first
+        // (the last barrier of a frame orders LDS only), then one release
+        // store of the count (which writes the cache back for the pass,
+        // possibly on another chiplet)
+        if (p.stream_k && (k + 1) % p.stream_k == 0 && k < Tp) {
+            block_sync_vm();
+            if (tid == 0) __hip_atomic_store(p.prog + u, k + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
     if (tid == 0) {
         st.n_tok = run.set0;
@@ -996,6 +1011,10 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
         st.gframes = run.gframes;
         for (int i = 0; i < 7; i++) st.phase_ticks[i] = pf.ph[i];
         if (rc != 0) st.status = rc;
+    }
+    if (p.stream_k) {
+        block_sync_vm();
+        if (tid == 0) __hip_atomic_store(p.prog + u, rc == 0 ? Tp + 1 : -1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 

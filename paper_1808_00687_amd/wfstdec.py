@@ -33,6 +33,7 @@ WFST_LOGLIKES_HOST = 2
 WFST_PROFILE = 4
 WFST_PROFILE_STEPS = 8
 WFST_WORD_LATTICE = 16
+WFST_INCREMENTAL_LATTICE = 32
 
 
 class WfstError(RuntimeError):
@@ -61,13 +62,14 @@ class _Stats(C.Structure):
                 ("record_ms", C.c_double), ("final_ms", C.c_double), ("search_launches", C.c_int32),
                 ("search_phase_ms", C.c_double * 7), ("backtrace_ms", C.c_double),
                 ("lattice_prune_ms", C.c_double), ("search_span_ms", C.c_double),
-                ("word_sequences", C.c_int64)]
+                ("word_sequences", C.c_int64), ("lattice_incremental", C.c_int64),
+                ("workspace_bytes", C.c_int64)]
 
 
 class _DebugOpts(C.Structure):
     _fields_ = [("lds_fill", C.c_int32), ("queue_cap", C.c_int32), ("record_fill", C.c_int32),
                 ("record_big_fill", C.c_int32), ("lattice_lds", C.c_int32), ("permute", C.c_int32),
-                ("fail_lattice_alloc", C.c_int32)]
+                ("fail_lattice_alloc", C.c_int32), ("lattice_chunk", C.c_int32), ("lattice_ring", C.c_int32)]
 
 
 class _LatArc(C.Structure):
@@ -410,7 +412,8 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
                       lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
                       record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
                       stream=None, profile_steps: bool = False, blank_ids=None,
-                      frame_stride: int = 1, word_lattice: bool = False) -> List[WfstResult]:
+                      frame_stride: int = 1, word_lattice: bool = False,
+                      incremental_lattice: bool = False) -> List[WfstResult]:
     """Decode a batch of utterances (wfst_decode_batch).  ``loglikes`` are
     [T_u x L] float32 tensors on the graph's device (or numpy arrays)."""
     keep: list = []
@@ -426,7 +429,7 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
     n = len(ptrs)
     flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
         (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0) | \
-        (WFST_WORD_LATTICE if word_lattice else 0)
+        (WFST_WORD_LATTICE if word_lattice else 0) | (WFST_INCREMENTAL_LATTICE if incremental_lattice else 0)
     o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint,
               blank_ids, frame_stride, keep)
     parr = (C.c_void_p * n)(*ptrs)
@@ -450,14 +453,15 @@ def wfst_decode(graph: WfstGraph, loglikes, beam: float, max_active: int = 0,
                 lattice_beam: float = -1.0, blank_threshold: float = 2.0, blank_id: int = 0,
                 record_tokens: bool = False, profile: bool = False, capacity_hint: int = 0,
                 stream=None, profile_steps: bool = False, blank_ids=None,
-                frame_stride: int = 1, word_lattice: bool = False) -> WfstResult:
+                frame_stride: int = 1, word_lattice: bool = False,
+                incremental_lattice: bool = False) -> WfstResult:
     """Decode one utterance (wfst_decode).  Returns the result also when the
     status is WFST_ENOPATH; other errors raise WfstError."""
     keep: list = []
     ptr, shape, host = _ll_ptr(loglikes, keep)
     flags = (WFST_RECORD_TOKENS if record_tokens else 0) | (WFST_LOGLIKES_HOST if host else 0) | \
         (WFST_PROFILE if profile else 0) | (WFST_PROFILE_STEPS if profile_steps else 0) | \
-        (WFST_WORD_LATTICE if word_lattice else 0)
+        (WFST_WORD_LATTICE if word_lattice else 0) | (WFST_INCREMENTAL_LATTICE if incremental_lattice else 0)
     o = _opts(beam, max_active, lattice_beam, blank_threshold, blank_id, flags, capacity_hint,
               blank_ids, frame_stride, keep)
     out = C.c_void_p()

@@ -276,6 +276,47 @@ def test_order_permutation_is_bit_identical(dec, torch_mod, oracle_mod, cfg2):
                                tag="permuted seed %d utt %d" % (seed, u))
 
 
+def test_incremental_lattice_pass_is_exact(dec, torch_mod, oracle_mod, cfg2):
+    # WFST_INCREMENTAL_LATTICE: a pass beside the search prunes every chunk
+    # of token sets against its frontier (extra cost 0 there) and keeps the
+    # survivors for the final pass.  The result must be bit-identical to
+    # pruning the whole lattice after the search, and the oracle's; chunks of
+    # 1 and 3 sets and rings too small for a chunk (chunks end early, records
+    # wrap around the ring) included.
+    wl, gh = cfg2
+    o = wl.opts
+    ll = wl.loglikes[0][:160]
+    x = to_dev(torch_mod, ll)
+    ro = oracle_mod.decode(wl.graph, ll, o.beam, o.max_active, o.lattice_beam)
+    whole = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    parity.assert_same(ro, whole, lattice=True, tag="after the search")
+    for chunk, ring in ((0, 0), (1, 0), (3, 0), (3, 90000), (32, 150000)):
+        with dec.debug_opts(lattice_chunk=chunk, lattice_ring=ring):
+            r = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, record_tokens=True,
+                                incremental_lattice=True)
+        parity.assert_same(ro, r, lattice=True, tag="chunk %d ring %d" % (chunk, ring))
+        assert r.stats["lattice_incremental"] < whole.stats["lattice_raw"]
+        say("chunk %d ring %d: raw %d, kept by the incremental pass %d, final %d" % (
+            chunk, ring, r.stats["lattice_raw"], r.stats["lattice_incremental"], r.stats["lattice_kept"]))
+    # the switch that turns the pass off gives the one-shot path
+    with dec.debug_opts(lattice_chunk=-1):
+        r = dec.wfst_decode(gh, x, o.beam, o.max_active, o.lattice_beam, incremental_lattice=True)
+    assert r.stats["lattice_incremental"] == r.stats["lattice_raw"]
+    for seed in range(8):
+        g = W.random_small_graph(1300 + seed, 300, mean_deg=3.0, eps_frac=0.3, num_labels=5, weights="int",
+                                 final=seed % 2 == 0)
+        lls = [W.random_small_loglikes(1300 + 10 * seed + u, 5 + 9 * u, 5, kind="int") for u in range(6)]
+        gs = dec.load_graph(g)
+        for chunk, ring in ((1, 0), (2, 3000), (5, 0)):
+            with dec.debug_opts(lattice_chunk=chunk, lattice_ring=ring):
+                res = dec.wfst_decode_batch(gs, [to_dev(torch_mod, y) for y in lls], 9.0, [0, 13][seed % 2],
+                                            [INF, 2.5][seed % 2], record_tokens=True, incremental_lattice=True)
+            for u, (y, r) in enumerate(zip(lls, res)):
+                parity.assert_same(oracle_mod.decode(g, y, 9.0, [0, 13][seed % 2], [INF, 2.5][seed % 2]), r,
+                                   lattice=True, tag="seed %d chunk %d ring %d utt %d" % (seed, chunk, ring, u))
+        gs.free()
+
+
 def test_lattice_alloc_failure_returns_enomem(dec, torch_mod, oracle_mod, cfg2):
     # the lattice output cannot be allocated: the call fails with WFST_ENOMEM,
     # and the next decode works
@@ -527,6 +568,34 @@ def test_config4_batch_full(dec, torch_mod, oracle_mod, cfg3):
     with ThreadPoolExecutor(max_workers=threads) as ex:
         toks = list(ex.map(check, range(len(res))))
     say("config 4: %d utterances, %d tokens compared" % (len(res), sum(toks)))
+
+
+def test_config4_incremental_lattice(dec, torch_mod, oracle_mod, cfg3):
+    # the benchmark's batch with the incremental lattice pass: every
+    # utterance's lattice, path and token sets bit-identical to the one-shot
+    # pass, with a smaller workspace
+    g, gh = cfg3
+    wl = W.workload(4)
+    o = wl.opts
+    xs = [to_dev(torch_mod, x) for x in wl.loglikes]
+    one = dec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    inc = dec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, record_tokens=True,
+                                incremental_lattice=True)
+    for u, (a, b) in enumerate(zip(one, inc)):
+        assert a.status == b.status == 0
+        for f in ("tok_off", "tok_state", "tok_arc", "path_arcs", "path_frames", "lat_frame", "lat_arc"):
+            np.testing.assert_array_equal(getattr(a, f), getattr(b, f), err_msg="utt %d %s" % (u, f))
+        for f in ("tok_cost", "lat_cost", "lat_extra"):
+            np.testing.assert_array_equal(parity.bits(getattr(a, f)), parity.bits(getattr(b, f)),
+                                          err_msg="utt %d %s" % (u, f))
+        assert parity.bits(a.cost) == parity.bits(b.cost)
+        assert a.stats["lattice_raw"] == b.stats["lattice_raw"]
+    raw = sum(r.stats["lattice_raw"] for r in one)
+    kept = sum(r.stats["lattice_incremental"] for r in inc)
+    ws_one, ws_inc = one[0].stats["workspace_bytes"], inc[0].stats["workspace_bytes"]
+    say("config 4: raw lattice %d arcs, %d left by the incremental pass; workspace %.2f GiB one-shot, "
+        "%.2f GiB incremental" % (raw, kept, ws_one / 2**30, ws_inc / 2**30))
+    assert kept < raw and ws_inc < ws_one
 
 
 def test_config6_hmm_lsd_and_stride(dec, torch_mod, oracle_mod):
