@@ -140,6 +140,31 @@ __device__ __forceinline__ int owner_lane(int pre, int k)
     return lo;
 }
 
+// Owner lane of position k0 + lane (the same as owner_lane(pre, k0 + lane))
+// for counts cnt whose exclusive prefix pre is non-decreasing over lanes,
+// pre <= k0 in lane 0.  A lane whose first item lies at position 1..63 of the
+// window sends its id there (ds_permute; a position no lane writes reads 0),
+// position 0 takes the last lane whose first item is at most k0 (a ballot),
+// and an inclusive maximum scan carries each owner over its items.  One LDS
+// lane swizzle and six DPP steps instead of six dependent shuffles.  Called
+// by the whole wave.
+__device__ __forceinline__ int owner_scan(int pre, int cnt, int k0)
+{
+    const int lane = lane_id();
+    const int s = pre - k0;
+    const bool push = cnt > 0 && s > 0 && s < kWave;
+    const int got = __builtin_amdgcn_ds_permute(push ? s * 4 : 0, push ? lane + 1 : 0);
+    const uint64_t m = __ballot(pre <= k0);
+    int v = lane == 0 ? kWave - __clzll(static_cast<long long>(m)) : got;
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false));   // row_shr:1
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false));   // row_shr:2
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false));   // row_shr:4
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false));   // row_shr:8
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false));   // row_bcast:15
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false));   // row_bcast:31
+    return v - 1;
+}
+
 template <typename T>
 __device__ __forceinline__ T ld_relaxed(T *p)
 {

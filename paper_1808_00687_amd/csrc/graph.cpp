@@ -80,7 +80,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     }
     const int64_t n_emit = e - n_eps;
 
-    std::vector<int32_t> eoff, xoff, arc_src;
+    std::vector<int32_t> eoff, xoff, arc_src, eua;
     std::vector<int4> earc, xarc, srec, ctab;
     std::vector<int2> uarc;
     int64_t n_closure = 0;
@@ -123,6 +123,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
         if (static_cast<int64_t>(q.size()) != n) return fail(WFST_EINVAL, "wfst_load: epsilon cycle");
 
         earc.resize(static_cast<size_t>(n_emit));
+        eua.resize(static_cast<size_t>(n_emit));
         xarc.resize(static_cast<size_t>(n_eps));
         arc_src.resize(static_cast<size_t>(e));
         uarc.resize(static_cast<size_t>(e));
@@ -134,7 +135,8 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
             std::memcpy(&wb, &weight[a], 4);
             if (ilabel[a]) {
                 uarc[a] = make_int2(olabel[a], ef[s]);
-                earc[ef[s]++] = make_int4(dflag, ilabel[a] - 1, wb, static_cast<int32_t>(a));
+                eua[ef[s]] = static_cast<int32_t>(a);
+                earc[ef[s]++] = make_int4(dflag, ilabel[a] - 1, wb, 0);
                 arc_src[a] = s;
             } else {
                 uarc[a] = make_int2(olabel[a], xf[s]);
@@ -194,6 +196,10 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
                 (static_cast<uint32_t>(off + 1) << kClosureSizeBits) | static_cast<uint32_t>(size - 1));
             n_closure++;
         }
+        // every arc record carries its destination's closure word: an
+        // epsilon work item then reaches the list without the state record
+        for (auto &r : earc) r.w = srec[2 * static_cast<size_t>(r.x & 0x7FFFFFFF) + 1].w;
+        for (auto &r : xarc) r.w = srec[2 * static_cast<size_t>(r.x & 0x7FFFFFFF) + 1].w;
     } catch (const std::bad_alloc &) {
         return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
     }
@@ -202,13 +208,14 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     const size_t b_eoff = align((static_cast<size_t>(n) + 1) * 4);
     const size_t b_xoff = b_eoff;
     const size_t b_earc = align(static_cast<size_t>(n_emit) * 16 + 16);
+    const size_t b_eua = align(static_cast<size_t>(n_emit) * 4 + 4);
     const size_t b_xarc = align(static_cast<size_t>(n_eps) * 16 + 16);
     const size_t b_src = align(static_cast<size_t>(e) * 4 + 4);
     const size_t b_fin = final_weight ? align(static_cast<size_t>(n) * 4) : 0;
     const size_t b_srec = align(static_cast<size_t>(n) * 32);
     const size_t b_ctab = align(ctab.size() * 16 + 16);
     const size_t b_uarc = align(static_cast<size_t>(e) * 8 + 8);
-    const size_t total = b_eoff + b_xoff + b_earc + b_xarc + b_src + b_fin + b_srec + b_ctab + b_uarc;
+    const size_t total = b_eoff + b_xoff + b_earc + b_eua + b_xarc + b_src + b_fin + b_srec + b_ctab + b_uarc;
 
     wfst_graph *h = new (std::nothrow) wfst_graph();
     if (!h) return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
@@ -239,6 +246,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     g.d.eoff = static_cast<const int32_t *>(put(eoff.data(), eoff.size() * 4, b_eoff));
     g.d.xoff = static_cast<const int32_t *>(put(xoff.data(), xoff.size() * 4, b_xoff));
     g.d.earc = static_cast<const int4 *>(put(earc.data(), earc.size() * 16, b_earc));
+    g.d.eua = static_cast<const int32_t *>(put(eua.data(), eua.size() * 4, b_eua));
     g.d.xarc = static_cast<const int4 *>(put(xarc.data(), xarc.size() * 16, b_xarc));
     g.d.arc_src = static_cast<const int32_t *>(put(arc_src.data(), arc_src.size() * 4, b_src));
     g.d.final_w = final_weight ? static_cast<const float *>(put(final_weight, static_cast<size_t>(n) * 4, b_fin)) : nullptr;

@@ -55,9 +55,10 @@ struct DevGraph {
     int64_t e;
     int64_t n_emit, n_eps;
     const int32_t *eoff;
-    const int4 *earc;
+    const int4 *earc;   // emitting records by source: {dst | has-epsilon bit, ilabel - 1, weight, closure word of dst}
+    const int32_t *eua; // user arc of each emitting record
     const int32_t *xoff;
-    const int4 *xarc;
+    const int4 *xarc;   // epsilon records by source: {dst | has-epsilon bit, weight, user arc, closure word of dst}
     const int32_t *arc_src;
     const float *final_w;
     const int4 *srec;   // 2 x N: {eoff[s], eoff[s+1], xoff[s], xoff[s+1]}, first epsilon record of s

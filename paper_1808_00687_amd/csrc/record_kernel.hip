@@ -235,14 +235,16 @@ __device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsi
                 const int op = __shfl(pre, o, kWave);
                 const float oc = __shfl(cst, o, kWave);
                 int4 y = make_int4(0, 0, 0, 0);
+                int32_t ua = 0;
                 float lv = 0.0f;
                 if (q < tot) {
                     y = p.g.earc[ob + (q - op)];
+                    ua = p.g.eua[ob + (q - op)];
                     lv = ldg(row + y.y);
                 }
                 const float t1 = oc + __int_as_float(y.z);
                 int4 r4 = make_int4(0, 0, 0, 0);
-                const bool rec = into_set<G>(p, t, win, b0, sv_key, cut, q < tot, t1 - lv, y.w,
+                const bool rec = into_set<G>(p, t, win, b0, sv_key, cut, q < tot, t1 - lv, ua,
                                              static_cast<int32_t>(b1 + i0 + o), static_cast<uint32_t>(y.x) & kDstMask,
                                              r4);
                 append(eo, &sh.ne, rec, r4);

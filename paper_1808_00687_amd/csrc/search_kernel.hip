@@ -165,9 +165,11 @@ __device__ __forceinline__ void sub_close(const Params &p, Prof &pf, int i)
 }
 
 // A wave's epsilon work list: an LDS queue of (table slot, cost bits) items
-// and the device-memory list that takes what does not fit.
+// with the closure word of each item's state (0 if not known), and the
+// device-memory list that takes what does not fit (without closure words).
 struct WaveQ {
     uint2 *q;        // this wave's LDS queue
+    uint32_t *ql;    // the items' closure words
     int n;           // items in it (the same in every lane)
     int qcap;        // its capacity (<= kQueue)
     uint2 *spill;    // device-memory list of the current round
@@ -176,7 +178,8 @@ struct WaveQ {
 };
 
 // Offer R candidate costs per lane (act[r]) to the table; lowered tokens
-// of states with epsilon out-arcs become items of the wave's queue.  The R
+// of states with epsilon out-arcs become items of the wave's queue, with the
+// closure word cl[r] of the state when the caller knows it (else 0).  The R
 // offers go through each step together, so that their LDS atomics are in
 // flight at the same time.  With BEST the frame's best key takes the
 // smallest offered key (a caller that has already done so passes false):
@@ -184,7 +187,7 @@ struct WaveQ {
 // is the frame's best token either way.  Called by the whole wave.
 template <bool G, int R, bool BEST>
 __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const bool *act, const uint32_t *d,
-                                      const bool *d_eps, const float *cand, const uint32_t *key)
+                                      const bool *d_eps, const uint32_t *cl, const float *cand, const uint32_t *key)
 {
     int slot[R];
     // slot of each state: a compare-and-swap on the key claims a free slot
@@ -281,6 +284,7 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
             const uint2 it = make_uint2(static_cast<uint32_t>(slot[r]), __float_as_uint(cand[r]));
             if (idx < wq.qcap) {
                 wq.q[idx] = it;
+                wq.ql[idx] = cl[r];
             } else {
                 const int gi = atomicAdd(wq.spill_n, 1);
                 if (gi < wq.scap) wq.spill[gi] = it;
@@ -294,9 +298,9 @@ __device__ __forceinline__ void offer(const Tab<G> &t, Sh &sh, WaveQ &wq, const 
 // One candidate per lane, the frame's best key included.
 template <bool G>
 __device__ __forceinline__ void offer1(const Tab<G> &t, Sh &sh, WaveQ &wq, bool act, uint32_t d, bool d_eps,
-                                       float cand, uint32_t key)
+                                       uint32_t cl, float cand, uint32_t key)
 {
-    offer<G, 1, true>(t, sh, wq, &act, &d, &d_eps, &cand, &key);
+    offer<G, 1, true>(t, sh, wq, &act, &d, &d_eps, &cl, &cand, &key);
 }
 
 // Bin holding the rank-th smallest (1-based) of a histogram: sets sh.bin and
@@ -390,15 +394,16 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
                 // the 64 tokens from the one owning a0, and each lane's owner among them
                 const int t0 = use_cs ? static_cast<int>(v.cs[a0 / kWave]) : search_le(v.epre, n_tok, a0);
                 const int tt = t0 + lane;
-                int pre = 0x7FFFFFFF, eb = 0;
+                int pre = 0x7FFFFFFF, eb = 0, nx = 0x7FFFFFFF;
                 float cst = 0.0f;
                 if (tt < n_tok) {
                     pre = v.epre[tt];
                     eb = v.ebeg[tt];
                     cst = v.c(tt);
+                    nx = tt + 1 < n_tok ? v.epre[tt + 1] : A;
                 }
-                const int win_end = t0 + kWave < n_tok ? v.epre[t0 + kWave] : A;
-                const int o = owner_lane(pre, a[r]);
+                const int win_end = t0 + kWave < n_tok ? __builtin_amdgcn_readlane(nx, kWave - 1) : A;
+                const int o = owner_scan(pre, nx - pre, a0);
                 ob[r] = __shfl(eb, o, kWave);
                 op[r] = __shfl(pre, o, kWave);
                 oc[r] = __shfl(cst, o, kWave);
@@ -425,7 +430,7 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
 #pragma unroll
         for (int r = 0; r < kChunks; r++) lv[r] = !ok[r] ? 0.0f : row_lds ? srow[rec[r].y] : ldg(grow + rec[r].y);
         bool act[kChunks], de[kChunks];
-        uint32_t d[kChunks], key[kChunks];
+        uint32_t d[kChunks], key[kChunks], cw[kChunks];
         float cnd[kChunks];
         uint32_t km = kEmptyKey;
 #pragma unroll
@@ -436,6 +441,7 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
             if (ok[r] && key[r] < km) km = key[r];
             d[r] = static_cast<uint32_t>(rec[r].x) & kDstMask;
             de[r] = rec[r].x < 0;
+            cw[r] = static_cast<uint32_t>(rec[r].w);
         }
         // The batch's own cheapest candidate tightens the early-drop bound; it
         // is within that bound itself, so it is offered and the frame's best
@@ -446,7 +452,7 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
         const uint32_t bnd = drop_bound(km < cur ? km : cur, p.beam);
 #pragma unroll
         for (int r = 0; r < kChunks; r++) act[r] = ok[r] && key[r] <= bnd;
-        offer<G, kChunks, false>(t, sh, wq, act, d, de, cnd, key);
+        offer<G, kChunks, false>(t, sh, wq, act, d, de, cw, cnd, key);
     }
 }
 
@@ -460,33 +466,41 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
 // relaxation reaches (fl(x + w) is monotone in x), so the tokens are the
 // same; the list holds every path, so a token it lowers needs no item of its
 // own.  A state without a list relaxes its own arcs, and lowered tokens of
-// states with epsilon arcs become items.
+// states with epsilon arcs become items.  An item that comes with its
+// state's closure word (icl, from the arc that reached the state) goes to
+// the list without loading the state record.
 template <bool G>
-__device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, WaveQ &wq, bool valid, uint2 it)
+__device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, WaveQ &wq, bool valid, uint2 it,
+                                      uint32_t icl)
 {
     const int lane = lane_id();
     int xb = 0, xd = 0, cb = 0, cn = 0;
     bool first = false;
     int4 x0 = make_int4(0, 0, 0, 0);
     const float cst = __uint_as_float(it.y);
+    constexpr uint32_t kSizeMask = (1u << kClosureSizeBits) - 1u;
     if (valid) {
         const uint32_t now = tld<G>(t.vals + it.x);
         if (okey(cst) == now) {
-            const int64_t s = static_cast<int64_t>(tld<G>(t.keys + it.x));
-            const int4 lo = p.g.srec[2 * s];
-            x0 = p.g.srec[2 * s + 1];
-            const uint32_t cl = static_cast<uint32_t>(x0.w);
-            // A list of one path is the state's only epsilon arc, into a
-            // state without epsilon arcs: the copy of that arc in the state
-            // record offers it below without loading the list.
-            constexpr uint32_t kSizeMask = (1u << kClosureSizeBits) - 1u;
-            if (cl && (cl & kSizeMask) != 0u) {
-                cb = static_cast<int>(cl >> kClosureSizeBits) - 1;
-                cn = static_cast<int>(cl & kSizeMask) + 1;
+            if (icl) {
+                cb = static_cast<int>(icl >> kClosureSizeBits) - 1;
+                cn = static_cast<int>(icl & kSizeMask) + 1;
             } else {
-                first = lo.w > lo.z;
-                xb = lo.z + 1;
-                xd = max(lo.w - lo.z - 1, 0);
+                const int64_t s = static_cast<int64_t>(tld<G>(t.keys + it.x));
+                const int4 lo = p.g.srec[2 * s];
+                x0 = p.g.srec[2 * s + 1];
+                const uint32_t cl = static_cast<uint32_t>(x0.w);
+                // A list of one path is the state's only epsilon arc, into
+                // a state without epsilon arcs: the copy of that arc in the
+                // state record offers it below without loading the list.
+                if (cl && (cl & kSizeMask) != 0u) {
+                    cb = static_cast<int>(cl >> kClosureSizeBits) - 1;
+                    cn = static_cast<int>(cl & kSizeMask) + 1;
+                } else {
+                    first = lo.w > lo.z;
+                    xb = lo.z + 1;
+                    xd = max(lo.w - lo.z - 1, 0);
+                }
             }
         }
     }
@@ -509,7 +523,7 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
                 oc[r] = 0.0f;
                 e[r] = 0;
                 if (k0 + r * kWave < tot) {
-                    const int o = owner_lane(pre, kk);
+                    const int o = owner_scan(pre, cn, k0 + r * kWave);
                     const int ob = __shfl(cb, o, kWave);
                     const int op = __shfl(pre, o, kWave);
                     oc[r] = __shfl(cst, o, kWave);
@@ -523,7 +537,7 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             }
             const uint32_t bnd = drop_bound(sh.best, p.beam);
             bool act[kRelChunks], de[kRelChunks];
-            uint32_t d[kRelChunks], key[kRelChunks];
+            uint32_t d[kRelChunks], key[kRelChunks], cw[kRelChunks];
             float cnd[kRelChunks];
 #pragma unroll
             for (int r = 0; r < kRelChunks; r++) {
@@ -539,18 +553,20 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
                 cnd[r] = c;
                 d[r] = static_cast<uint32_t>(c0[r].x);
                 de[r] = false;
+                cw[r] = 0u;
                 key[r] = okey(c);
                 act[r] = k0 + r * kWave + lane < tot && key[r] <= bnd;
             }
-            offer<G, kRelChunks, true>(t, sh, wq, act, d, de, cnd, key);
+            offer<G, kRelChunks, true>(t, sh, wq, act, d, de, cw, cnd, key);
         }
     }
-    {
-        // the first epsilon arc, from the state record
+    if (__ballot(first)) {
+        // the first epsilon arc, from the state record (the closure word of
+        // its destination is not at hand there)
         const uint32_t bnd = drop_bound(sh.best, p.beam);
         const float cnd = cst + __int_as_float(x0.y);
         const uint32_t key = okey(cnd);
-        offer1<G>(t, sh, wq, first && key <= bnd, static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, cnd, key);
+        offer1<G>(t, sh, wq, first && key <= bnd, static_cast<uint32_t>(x0.x) & kDstMask, x0.x < 0, 0u, cnd, key);
     }
     // the other epsilon arcs, spread over the wave
     const int incl = wave_incl_scan(xd);
@@ -558,23 +574,24 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
     const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
     for (int k0 = 0; k0 < tot; k0 += kWave) {
         const int kk = k0 + lane;
-        const int o = owner_lane(pre, kk);
+        const int o = owner_scan(pre, xd, k0);
         const int ob = __shfl(xb, o, kWave);
         const int op = __shfl(pre, o, kWave);
         const float oc = __shfl(cst, o, kWave);
         const uint32_t bnd = drop_bound(sh.best, p.beam);
         bool act = false, d_eps = false;
-        uint32_t d = 0, key = kEmptyKey;
+        uint32_t d = 0, key = kEmptyKey, cw = 0u;
         float cnd = 0.0f;
         if (kk < tot) {
             const int4 r = p.g.xarc[ob + (kk - op)];
             d = static_cast<uint32_t>(r.x) & kDstMask;
             d_eps = r.x < 0;
+            cw = static_cast<uint32_t>(r.w);
             cnd = oc + __int_as_float(r.y);
             key = okey(cnd);
             act = key <= bnd;
         }
-        offer1<G>(t, sh, wq, act, d, d_eps, cnd, key);
+        offer1<G>(t, sh, wq, act, d, d_eps, cw, cnd, key);
     }
 }
 
@@ -593,8 +610,9 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
         // items were stored by other lanes of the wave
         wave_lds_handover();
         const uint2 it = lane < take ? wq.q[base + lane] : make_uint2(0u, 0u);
+        const uint32_t icl = lane < take ? wq.ql[base + lane] : 0u;
         wq.n = base;
-        relax<G>(p, t, sh, wq, lane < take, it);
+        relax<G>(p, t, sh, wq, lane < take, it, icl);
     }
 }
 
@@ -603,7 +621,7 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
 // a negative WFST error.  Every return is taken by the whole workgroup.
 template <bool G>
 __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
-                                     const Tab<G> &t, uint2 *aux, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
+                                     const Tab<G> &t, uint2 *aux, uint32_t *auxl, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
                                      uint16_t *s_cs, float *s_row, uint2 *spill, int gcap, Run &run, Prof &pf,
                                      int k, int &n_ins)
 {
@@ -612,6 +630,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     const int wid = tid / kWave;
     WaveQ wq;
     wq.q = aux + wid * kQueue;
+    wq.ql = auxl + wid * kQueue;
     wq.n = 0;
     wq.qcap = min(kQueue, p.gen_lds);
     wq.spill = spill;
@@ -637,7 +656,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         if (wid == 0) {
             const int s = p.g.start;
             const int4 lo = p.g.srec[2 * static_cast<int64_t>(s)];
-            offer1<G>(t, sh, wq, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0.0f, okey(0.0f));
+            offer1<G>(t, sh, wq, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0u, 0.0f, okey(0.0f));
         }
     } else {
         const float *row = ll + static_cast<int64_t>(p.kept[ly.kept0 + k - 1]) * p.L;
@@ -672,7 +691,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
                 const unsigned long long w = ldg(reinterpret_cast<const unsigned long long *>(list + i));
                 it = make_uint2(static_cast<uint32_t>(w), static_cast<uint32_t>(w >> 32));
             }
-            relax<G>(p, t, sh, wq, i < total, it);
+            relax<G>(p, t, sh, wq, i < total, it, 0u);
             drain<G>(p, t, sh, wq);
         }
         __syncthreads();
@@ -887,6 +906,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
         Run run;
         uint16_t cs[kCs];                  // first token of each 64-arc chunk of the last set
         uint2 aux[kW * kQueue];            // per-wave epsilon queues, or the select histogram
+        uint32_t auxl[kW * kQueue];        // the queue items' closure words
         float cost[kSetCache];             // the last token set, for the next expansion
         int32_t epre[kSetCache];
         int32_t ebeg[kSetCache];
@@ -903,6 +923,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     float *s_row = lds.row;
     uint16_t *s_slots = lds.slots;
     uint2 *s_aux = lds.aux;
+    uint32_t *s_auxl = lds.auxl;
     float *s_cost = lds.cost;
     int32_t *s_epre = lds.epre;
     int32_t *s_ebeg = lds.ebeg;
@@ -968,7 +989,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     for (int k = 0; k <= Tp; k++) {
         int n_ins = 0;
         if (!in_g)
-            rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, run, pf,
+            rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_auxl, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, run, pf,
                               k, n_ins);
         if (in_g || rc == kOverflow) {
             if (!in_g) {
@@ -986,7 +1007,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
                 gclean = true;
             }
             __syncthreads();
-            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, run, pf,
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_auxl, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, run, pf,
                              k, n_ins);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
             if (tid == 0) run.gframes++;
