@@ -101,13 +101,18 @@ struct Sh {
     int status;          // sticky error of the utterance
     uint32_t best;       // smallest cost key among the frame's tokens
     int spill_n[2];      // epsilon items in the device-memory lists
-    unsigned long long alloc;   // compaction: emitting degrees << 32 | survivors placed
-    int xsum;            // compaction: epsilon degrees of the survivors
+    // compaction results of frames of even and odd index: every wave reads
+    // its frame's after the frame's last barrier, while thread 0 may already
+    // clear the next frame's
+    unsigned long long alloc[2];   // emitting degrees << 32 | survivors placed
+    int xsum[2];         // epsilon degrees of the survivors
     int bin, before, cnt;
     int scan[52];
 };
 
-// Running values of the utterance (in LDS, updated by thread 0).
+// Running values of the utterance (in LDS): frame k reads the copy of
+// index k & 1 and thread 0 writes the other, so that no wave still reading
+// the frame's values after its last barrier sees them change.
 struct Run {
     int64_t set0;        // relative survivor index where the next set starts
     int64_t prev0;       // relative start of S_{k-1}
@@ -116,7 +121,6 @@ struct Run {
     int64_t le, lx;      // emitting and epsilon regions reserved so far
     int64_t arcs;
     int64_t eps;         // epsilon out-arcs of the survivors
-    int gframes;
 };
 
 // Profiling counters, kept by thread 0 in LDS (in registers they would
@@ -456,6 +460,22 @@ __device__ __forceinline__ void expand(const Params &p, const Tab<G> &t, Sh &sh,
     }
 }
 
+// Weight j (1-8) of a closure entry's path from the entry's second and
+// third words (j a constant after unrolling).
+__device__ __forceinline__ int path_weight(const int4 &c1, const int4 &c2, int j)
+{
+    switch (j) {
+    case 1: return c1.x;
+    case 2: return c1.y;
+    case 3: return c1.z;
+    case 4: return c1.w;
+    case 5: return c2.x;
+    case 6: return c2.y;
+    case 7: return c2.z;
+    default: return c2.w;
+    }
+}
+
 // Relax the epsilon arcs of one item per lane (valid): the item's state
 // still holding the item's cost, i.e. no cheaper item of it follows.
 //
@@ -541,16 +561,23 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
             float cnd[kRelChunks];
 #pragma unroll
             for (int r = 0; r < kRelChunks; r++) {
-                float c = oc[r] + __int_as_float(c0[r].w);
-                if (c0[r].z > 1) c = c + __int_as_float(c1[r].x);
-                if (c0[r].z > 2) c = c + __int_as_float(c1[r].y);
-                if (c0[r].z > 3) c = c + __int_as_float(c1[r].z);
-                if (c0[r].z > 4) c = c + __int_as_float(c1[r].w);
-                if (c0[r].z > 5) c = c + __int_as_float(c2[r].x);
-                if (c0[r].z > 6) c = c + __int_as_float(c2[r].y);
-                if (c0[r].z > 7) c = c + __int_as_float(c2[r].z);
-                if (c0[r].z > 8) c = c + __int_as_float(c2[r].w);
-                cnd[r] = c;
+                cnd[r] = oc[r] + __int_as_float(c0[r].w);
+            }
+            // the later weights in path order, while any path of the wave
+            // has more (most paths are one or two arcs long)
+#pragma unroll
+            for (int j = 1; j < kClosureDepth; j++) {
+                bool more = false;
+#pragma unroll
+                for (int r = 0; r < kRelChunks; r++) more = more || c0[r].z > j;
+                if (!__ballot(more)) break;
+#pragma unroll
+                for (int r = 0; r < kRelChunks; r++)
+                    if (c0[r].z > j) cnd[r] = cnd[r] + __int_as_float(path_weight(c1[r], c2[r], j));
+            }
+#pragma unroll
+            for (int r = 0; r < kRelChunks; r++) {
+                const float c = cnd[r];
                 d[r] = static_cast<uint32_t>(c0[r].x);
                 de[r] = false;
                 cw[r] = 0u;
@@ -622,12 +649,13 @@ __device__ __forceinline__ void drain(const Params &p, const Tab<G> &t, Sh &sh, 
 template <bool G>
 __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const float *ll, int Tp, Sh &sh,
                                      const Tab<G> &t, uint2 *aux, uint32_t *auxl, float *s_cost, int32_t *s_epre, int32_t *s_ebeg,
-                                     uint16_t *s_cs, float *s_row, uint2 *spill, int gcap, Run &run, Prof &pf,
+                                     uint16_t *s_cs, float *s_row, uint2 *spill, int gcap, Run *runs, Prof &pf,
                                      int k, int &n_ins)
 {
     const int tid = threadIdx.x;
     const int lane = lane_id();
     const int wid = tid / kWave;
+    const Run &run = runs[k & 1];
     WaveQ wq;
     wq.q = aux + wid * kQueue;
     wq.ql = auxl + wid * kQueue;
@@ -643,8 +671,8 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         sh.overflow = 0;
         sh.best = kEmptyKey;
         sh.spill_n[0] = sh.spill_n[1] = 0;
-        sh.alloc = 0ull;
-        sh.xsum = 0;
+        sh.alloc[k & 1] = 0ull;
+        sh.xsum[k & 1] = 0;
         sh.cnt = 0;
     }
     __syncthreads();
@@ -779,6 +807,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     }
     using Slot = typename Tab<G>::Slot;
     const int64_t set0 = run.set0;
+    int xacc = 0;   // epsilon degrees of this lane's survivors
     for (int c = wid; c * kWave < n; c += kW * kCompact) {
         bool kp[kCompact];
         uint32_t vv[kCompact];
@@ -806,25 +835,21 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
         }
 #pragma unroll
         for (int r = 0; r < kCompact; r++) {
-            const int cnt = kp[r] ? 1 : 0;
+            const uint64_t km = __ballot(kp[r]);
+            if (!km) continue;
+            const int tc = __popcll(km);
             const int deg = kp[r] ? lo[r].y - lo[r].x : 0;
-            const int xd = kp[r] ? lo[r].w - lo[r].z : 0;
-            const int ic = wave_incl_scan(cnt);
+            xacc += kp[r] ? lo[r].w - lo[r].z : 0;
             const int id = wave_incl_scan(deg);
-            const int ix = wave_incl_scan(xd);
-            const int tc = __builtin_amdgcn_readlane(ic, kWave - 1);
-            if (tc == 0) continue;
             const int td = __builtin_amdgcn_readlane(id, kWave - 1);
-            const int tx = __builtin_amdgcn_readlane(ix, kWave - 1);
             unsigned long long base = 0;
-            if (lane == 0) {
-                base = atomicAdd(&sh.alloc, (static_cast<unsigned long long>(td) << 32) | static_cast<uint32_t>(tc));
-                atomicAdd(&sh.xsum, tx);
-            }
+            if (lane == 0)
+                base = atomicAdd(&sh.alloc[k & 1],
+                                 (static_cast<unsigned long long>(td) << 32) | static_cast<uint32_t>(tc));
             base = (static_cast<unsigned long long>(__builtin_amdgcn_readlane(static_cast<int>(base >> 32), 0)) << 32) |
                    static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(base), 0));
             if (!kp[r]) continue;
-            const int pos = static_cast<int>(static_cast<uint32_t>(base)) + ic - cnt;
+            const int pos = static_cast<int>(static_cast<uint32_t>(base)) + rank_in(km);
             const int apos = static_cast<int>(base >> 32) + id - deg;
             const int64_t rel = set0 + pos;
             if (rel < ly.svcap) {
@@ -846,6 +871,10 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
             }
         }
     }
+    {
+        const int tx = wave_incl_scan(xacc);
+        if (lane == kWave - 1 && tx) atomicAdd(&sh.xsum[k & 1], tx);
+    }
     if (next_row) {
 #pragma unroll
         for (int j = 0; j < kRowPer; j++) {
@@ -857,10 +886,11 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     // copy; then its device-memory stores must be complete (and the cleared
     // device-memory table before the next offers)
     table_barrier<G>();
-    if (!G && static_cast<uint32_t>(sh.alloc) > static_cast<uint32_t>(kSetCache)) __syncthreads();
-    const int n_kept = static_cast<int>(static_cast<uint32_t>(sh.alloc));
-    const int a_kept = static_cast<int>(sh.alloc >> 32);
-    const int x_kept = sh.xsum;
+    const unsigned long long alloc = sh.alloc[k & 1];
+    if (!G && static_cast<uint32_t>(alloc) > static_cast<uint32_t>(kSetCache)) __syncthreads();
+    const int n_kept = static_cast<int>(static_cast<uint32_t>(alloc));
+    const int a_kept = static_cast<int>(alloc >> 32);
+    const int x_kept = sh.xsum[k & 1];
     const int ns = n_kept;
     phase_mark(p, pf, 3);
     phase_fold(p, pf, true);
@@ -875,21 +905,22 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     // per set; the pass checks its own capacities)
     if (p.lattice && !p.stream_k && (run.le + a_rec > ly.lecap || run.lx + x_kept > ly.lxcap))
         return WFST_ECAPACITY;
-    // the running values live in LDS: thread 0 updates them, every thread
-    // reads them after the next frame's first barrier
+    // the next frame's running values: thread 0 writes the other copy,
+    // which every thread reads after the next frame's first barrier
     if (tid == 0) {
         p.sv_off[ly.fo0 + k + 1] = set0 + ns;
         p.cut_arr[ly.fo0 + k] = cut;
         p.rle_off[ly.fo0 + k + 1] = run.le + a_rec;
         p.rlx_off[ly.fo0 + k + 1] = run.lx + x_kept;
-        run.le += a_rec;
-        run.lx += x_kept;
-        run.eps += x_kept;
-        run.arcs += a_rec;
-        run.prev0 = set0;
-        run.set0 = set0 + ns;
-        run.n_prev = ns;
-        run.a_prev = a_kept;
+        Run &nx = runs[(k + 1) & 1];
+        nx.le = run.le + a_rec;
+        nx.lx = run.lx + x_kept;
+        nx.eps = run.eps + x_kept;
+        nx.arcs = run.arcs + a_rec;
+        nx.prev0 = set0;
+        nx.set0 = set0 + ns;
+        nx.n_prev = ns;
+        nx.a_prev = a_kept;
     }
 
     return 0;
@@ -903,7 +934,7 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     struct Lds {
         Sh sh;
         Prof pf;
-        Run run;
+        Run run[2];
         uint16_t cs[kCs];                  // first token of each 64-arc chunk of the last set
         uint2 aux[kW * kQueue];            // per-wave epsilon queues, or the select histogram
         uint32_t auxl[kW * kQueue];        // the queue items' closure words
@@ -971,8 +1002,10 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     }
     __syncthreads();
 
-    Run &run = lds.run;   // running values of the utterance, updated by thread 0
-    if (tid == 0) run = Run{};
+    Run *runs = lds.run;   // running values of the utterance, written by thread 0
+    if (tid == 0) runs[0] = Run{};
+    int gframes = 0;       // frames redone on the device-memory table (thread 0's count)
+    int kd = 0;            // frames completed
     if (tid == 0) {
         for (int i = 0; i < 7; i++) pf.ph[i] = 0;
         for (int i = 0; i < 4; i++) pf.cur[i] = 0;
@@ -989,8 +1022,8 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
     for (int k = 0; k <= Tp; k++) {
         int n_ins = 0;
         if (!in_g)
-            rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_auxl, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, run, pf,
-                              k, n_ins);
+            rc = frame<false>(p, ly, ll, Tp, sh, lt, s_aux, s_auxl, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, runs,
+                              pf, k, n_ins);
         if (in_g || rc == kOverflow) {
             if (!in_g) {
                 // the abandoned attempt left states in the LDS table
@@ -1007,13 +1040,14 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
                 gclean = true;
             }
             __syncthreads();
-            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_auxl, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, run, pf,
-                             k, n_ins);
+            rc = frame<true>(p, ly, ll, Tp, sh, gt, s_aux, s_auxl, s_cost, s_epre, s_ebeg, s_cs, s_row, spill, gcap, runs,
+                             pf, k, n_ins);
             if (rc == kOverflow) rc = WFST_ECAPACITY;
-            if (tid == 0) run.gframes++;
+            gframes++;
             in_g = n_ins > g_stay;
         }
         if (rc != 0) break;
+        kd = k + 1;
         // publish every stream_k finished token sets to the incremental
         // lattice pass: every wave's stores of the sets complete in L2 first
         // (the last barrier of a frame orders LDS only), then one release
@@ -1025,11 +1059,12 @@ __global__ __launch_bounds__(kT) void search_kernel(Params p)
         }
     }
     if (tid == 0) {
+        const Run &run = runs[kd & 1];
         st.n_tok = run.set0;
         st.n_last = run.n_prev;
         st.arcs_expanded = run.arcs;
         st.eps_arcs = run.eps;
-        st.gframes = run.gframes;
+        st.gframes = gframes;
         for (int i = 0; i < 7; i++) st.phase_ticks[i] = pf.ph[i];
         if (rc != 0) st.status = rc;
     }

@@ -81,6 +81,22 @@ def test_small_random_graphs(dec, torch_mod, oracle_mod, seed, kind):
     parity.assert_same(ro, rg, lattice=lb >= 0, tag="seed %d" % seed)
 
 
+@pytest.mark.parametrize("L", [6145, 9000])
+def test_wide_label_rows(dec, torch_mod, oracle_mod, L):
+    # more log-likelihood columns than the search keeps in LDS: the emitting
+    # expansion reads the row from device memory (labels spread over the
+    # whole row)
+    for seed in range(6):
+        rng = np.random.default_rng(900 + seed)
+        g = W.random_small_graph(900 + seed, int(rng.integers(20, 300)), mean_deg=2.5, eps_frac=0.3,
+                                 num_labels=5, weights=["exp", "dyadic"][seed % 2], final=seed % 3 == 0)
+        g.ilabel = np.where(g.ilabel > 0, rng.integers(1, L + 1, size=g.ilabel.size), 0).astype(np.int32)
+        ll = rng.normal(0.0, 2.0, size=(int(rng.integers(1, 30)), L)).astype(np.float32)
+        ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=[INF, 5.0, 9.0][seed % 3],
+                      max_active=[0, 20][seed % 2], lattice_beam=[3.0, INF][seed % 2])
+        parity.assert_same(ro, rg, lattice=True, tag="L %d seed %d" % (L, seed))
+
+
 def listed_closure_states(g, max_paths, max_len):
     """States whose epsilon closure is at most max_paths paths of at most
     max_len arcs, every child with epsilon arcs being such a state too
@@ -568,6 +584,31 @@ def test_config4_batch_full(dec, torch_mod, oracle_mod, cfg3):
     with ThreadPoolExecutor(max_workers=threads) as ex:
         toks = list(ex.map(check, range(len(res))))
     say("config 4: %d utterances, %d tokens compared" % (len(res), sum(toks)))
+
+
+def test_config4_wide_rows(dec, torch_mod, oracle_mod, cfg3):
+    # the benchmark batch with its rows widened past what the search keeps in
+    # LDS (6,000 columns padded to 6,400): rows read from device memory, the
+    # same results as the oracle, token sets included
+    from concurrent.futures import ThreadPoolExecutor
+    g, gh = cfg3
+    wl = W.workload(4)
+    o = wl.opts
+    rng = np.random.default_rng(44)
+    lls = [np.concatenate([x, rng.normal(0.0, 1.0, size=(x.shape[0], 400)).astype(np.float32)], axis=1)
+           for x in wl.loglikes]
+    xs = [to_dev(torch_mod, x) for x in lls]
+    say("batch decode of %d widened utterances" % len(xs))
+    res = dec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, record_tokens=True)
+    del xs
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+
+    def check(u):
+        ro = oracle_mod.decode(g, lls[u], o.beam, o.max_active, o.lattice_beam)
+        parity.assert_same(ro, res[u], lattice=True, tokens=True, tag="wide config 4 utt %d" % u)
+
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        list(ex.map(check, range(len(res))))
 
 
 def test_config4_incremental_lattice(dec, torch_mod, oracle_mod, cfg3):
