@@ -31,6 +31,7 @@ FRAME_SHIFT_S = 0.010
 PROFILES = os.path.join(ROOT, "profiles")
 COUNTERS = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_counters.txt")
 TRACE = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_trace.txt")
+SQ = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_sq.txt")
 CSRC = os.path.join(ROOT, "paper_1808_00687_amd", "csrc")
 KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("search_kernel.hip", "device_util.h", "internal.h")]
 KERNEL_NAME = "search_kernel"
@@ -43,6 +44,12 @@ TRACE_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out
 PMC_CMD = ("timeout -s KILL 180 rocprofv3 --pmc {counter} --output-format csv -d gpurun_out/pmc_{tag} -o run -- "
            "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile --copy-calibration-mib %d"
            % CALIBRATION_MIB)
+SQ_PASSES = (("a", "SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY SQ_INSTS_VALU "
+                   "SQ_INSTS_LDS SQ_INSTS_SALU"),
+             ("b", "SQ_INSTS_VMEM_RD SQ_INSTS_VMEM_WR SQ_INSTS_BRANCH SQ_WAIT_INST_LDS SQ_ACTIVE_INST_VALU "
+                   "SQ_ACTIVE_INST_LDS SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS_ATOMIC"))
+SQ_CMD = ("timeout -s KILL 120 rocprofv3 --pmc {counters} --output-format csv -d gpurun_out/sq{tag} -o run -- "
+          "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile")
 
 # name: (config, label-synchronous, frame stride); cfg6 is the HMM-topology
 # stand-in (a set of blank-like units), not one of the five listed configs
@@ -149,6 +156,46 @@ def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str):
     print(COUNTERS)
 
 
+def write_sq_profile(csv_a: str, csv_b: str):
+    """Summary of the two SQ counter passes (SQ_PASSES) over the search
+    kernel for profiles/: counts summed over the batch's launches, and per
+    wave and decoded frame (a utterance's 16 waves run all its frames)."""
+    import csv
+    from paper_1808_00687_amd import workloads
+    wl = workloads.workload(4)
+    frames = sum(x.shape[0] for x in wl.loglikes)
+    waves = 16 * len(wl.loglikes)
+    per = waves * frames / len(wl.loglikes)
+    tot = {}
+    for path in (csv_a, csv_b):
+        for r in csv.DictReader(open(path)):
+            if KERNEL_NAME in r["Kernel_Name"]:
+                tot[r["Counter_Name"]] = tot.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    lines = ["# SQ counters of %s, workload lvcsr-25m-batch64 (64 utterances, 25M-arc graph), summed over the "
+             "batch's %d concurrent launches (%d waves)" % (KERNEL_NAME, GROUP_LAUNCHES, waves)]
+    for tag, counters in SQ_PASSES:
+        lines.append("# pass %s: %s" % (tag, SQ_CMD.format(counters=counters, tag=tag)))
+    lines += ["# summary written by: python3 bench.py --write-sq-profile gpurun_out/sqa/run_counter_collection.csv "
+              "gpurun_out/sqb/run_counter_collection.csv",
+              "# the cycle counters count in units of four cycles; per_wave_frame = count / (waves x frames per "
+              "utterance), %d decoded frames" % frames,
+              "%-24s %14s %16s" % ("counter", "count", "per_wave_frame")]
+    for name in sorted(tot):
+        lines.append("%-24s %14.4g %16.1f" % (name, tot[name], tot[name] / per))
+    w = tot.get("SQ_WAVE_CYCLES", 0.0)
+    if w:
+        for name in ("SQ_WAIT_ANY", "SQ_ACTIVE_INST_ANY", "SQ_WAIT_INST_ANY"):
+            if name in tot:
+                lines.append("%s / SQ_WAVE_CYCLES: %.2f" % (name, tot[name] / w))
+    if "SQ_INSTS_VALU" in tot and w:
+        # four waves share a SIMD; a wave64 VALU instruction holds it for one
+        # four-cycle unit
+        lines.append("SIMD busy with VALU, share of wave time: %.2f" % (4.0 * tot["SQ_INSTS_VALU"] / w))
+    lines.append("kernel_source_sha256: %s" % kernel_sha())
+    open(SQ, "w").write("\n".join(lines) + "\n")
+    print(SQ)
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -251,9 +298,14 @@ def main():
                     help="do not time kernel phases with HIP events")
     ap.add_argument("--write-profiles", nargs=3, metavar=("STATS_CSV", "FETCH_CSV", "WRITE_CSV"),
                     help="write the profiles/ summaries from rocprofv3 CSV output and exit")
+    ap.add_argument("--write-sq-profile", nargs=2, metavar=("PASS_A_CSV", "PASS_B_CSV"),
+                    help="write the SQ counter summary for profiles/ and exit")
     args = ap.parse_args()
     if args.write_profiles:
         write_profiles(*args.write_profiles)
+        return
+    if args.write_sq_profile:
+        write_sq_profile(*args.write_sq_profile)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))

@@ -50,7 +50,7 @@ constexpr int kFill = 6144;               // LDS states per frame before falling
 constexpr int kQueue = 128;               // LDS epsilon items per wave queue
 constexpr int kSetCache = 3008;           // tokens of the previous set kept in LDS for the expansion
 constexpr int kCs = 128;                  // 64-arc chunks of the previous set with their first token in LDS
-constexpr int kCompact = 2;               // slot-list chunks a wave has in flight in the compaction
+constexpr int kCompact = 1;               // slot-list chunks a wave has in flight in the compaction
 constexpr int kChunks = 2;                // 64-arc chunks a wave has in flight in the expansion
 constexpr int kRelChunks = 2;             // 64-path chunks of closure lists a wave has in flight
 constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
@@ -499,9 +499,14 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
     int4 x0 = make_int4(0, 0, 0, 0);
     const float cst = __uint_as_float(it.y);
     constexpr uint32_t kSizeMask = (1u << kClosureSizeBits) - 1u;
+    // Epsilon weights are not negative (the loader rejects such graphs), so
+    // every path from the item costs at least the item (fl(x + w) >= x for
+    // w >= 0): an item above the early-drop bound offers nothing that could
+    // survive, and is dropped before its loads.
+    const uint32_t ibnd = drop_bound(sh.best, p.beam);
     if (valid) {
         const uint32_t now = tld<G>(t.vals + it.x);
-        if (okey(cst) == now) {
+        if (okey(cst) == now && now <= ibnd) {
             if (icl) {
                 cb = static_cast<int>(icl >> kClosureSizeBits) - 1;
                 cn = static_cast<int>(icl & kSizeMask) + 1;
