@@ -298,6 +298,10 @@ def main():
                     help="do not time kernel phases with HIP events")
     ap.add_argument("--write-profiles", nargs=3, metavar=("STATS_CSV", "FETCH_CSV", "WRITE_CSV"),
                     help="write the profiles/ summaries from rocprofv3 CSV output and exit")
+    ap.add_argument("--incremental-lattice", action="store_true",
+                    help="decode with the incremental lattice pass beside the search (not the benchmark line)")
+    ap.add_argument("--word-lattice", action="store_true",
+                    help="also build the word-level lattice (not the benchmark line)")
     ap.add_argument("--write-sq-profile", nargs=2, metavar=("PASS_A_CSV", "PASS_B_CSV"),
                     help="write the SQ counter summary for profiles/ and exit")
     args = ap.parse_args()
@@ -341,7 +345,9 @@ def main():
     def step(profile, steps=False):
         return wfstdec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam, o.blank_threshold,
                                          o.blank_id, profile=profile, stream=stream, profile_steps=steps,
-                                         blank_ids=o.blank_ids, frame_stride=o.frame_stride)
+                                         blank_ids=o.blank_ids, frame_stride=o.frame_stride,
+                                         incremental_lattice=args.incremental_lattice,
+                                         word_lattice=args.word_lattice)
 
     for i in range(args.warmup):
         res = step(False)
@@ -391,6 +397,8 @@ def main():
             "blank_units": len(o.blank_ids) if o.blank_ids else 1,
             "frame_stride": o.frame_stride,
             "parallelism": "utterance batch of %d on 1 GPU" % len(wl.loglikes),
+            "lattice_mode": ("incremental" if args.incremental_lattice else "one-shot")
+                            + (" + word lattice" if args.word_lattice else ""),
         },
         "rtf": sec / (frames * FRAME_SHIFT_S),
         "original_frames_per_s": frames / sec,
