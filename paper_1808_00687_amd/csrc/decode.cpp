@@ -967,7 +967,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         r->stats.frames_decoded = x.Tp;
         if (x.status != WFST_OK) continue;
         r->cost = x.final_cost;
-        r->final_state = x.final_state;
+        r->final_state = user_state(G, x.final_state);
         r->reached_final = x.reached_final;
         r->path_arcs.resize(x.path_len);
         r->path_frames.resize(x.path_len);
@@ -1073,7 +1073,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
                     const uint32_t bits = (k >> 31) ? (k & 0x7FFFFFFFu) : ~k;
                     float c;
                     std::memcpy(&c, &bits, 4);
-                    r->tok_state[i] = tst[u][q];
+                    r->tok_state[i] = user_state(G, tst[u][q]);
                     r->tok_cost[i] = c;
                     r->tok_arc[i] = tarc[u][q];
                 }
@@ -1574,7 +1574,7 @@ int noalloc_impl(const wfst_graph *gh, const float *ll, int32_t T, int32_t L, co
         return st.status;
     }
     out->cost = st.final_cost;
-    out->final_state = st.final_state;
+    out->final_state = user_state(G, st.final_state);
     out->reached_final = st.reached_final;
     out->path_len = st.path_len;
     out->tokens = st.n_tok;

@@ -83,6 +83,11 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     std::vector<int32_t> eoff, xoff, arc_src, eua;
     std::vector<int4> earc, xarc, srec, ctab;
     std::vector<int2> uarc;
+    // the node layout (see below)
+    std::vector<int32_t> hdr_pos, node_eua;
+    std::vector<int4> node;
+    std::vector<float> node_fin;
+    int64_t n_units = 0;
     int64_t n_closure = 0;
     std::vector<uint8_t> has_eps;
     int32_t depth = 0;
@@ -200,22 +205,62 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
         // epsilon work item then reaches the list without the state record
         for (auto &r : earc) r.w = srec[2 * static_cast<size_t>(r.x & 0x7FFFFFFF) + 1].w;
         for (auto &r : xarc) r.w = srec[2 * static_cast<size_t>(r.x & 0x7FFFFFFF) + 1].w;
+
+        // Node layout: each state's two records (its rows, then its first
+        // epsilon record with its closure word) followed by its emitting
+        // arcs, in one array of 16-byte units.  A state's id on the device is
+        // the unit index of its first record, so the record that tells the
+        // compaction a survivor's rows shares a cache line with the first
+        // arcs the next expansion reads.  Ids keep the states' order (ties
+        // broken by the lowest id stay the same).
+        hdr_pos.resize(static_cast<size_t>(n));
+        for (int32_t s = 0; s < n; s++) {
+            hdr_pos[s] = static_cast<int32_t>(n_units);
+            n_units += 2 + (eoff[s + 1] - eoff[s]);
+            if (n_units >= 0x7FFFFFFFLL) return fail(WFST_EINVAL, "wfst_load: graph too large (2^31 16-byte units)");
+        }
+        auto remap = [&](int32_t x) {   // keeps the has-epsilon flag
+            return hdr_pos[x & 0x7FFFFFFF] | (x & static_cast<int32_t>(0x80000000u));
+        };
+        node.assign(static_cast<size_t>(n_units), make_int4(0, 0, 0, 0));
+        node_eua.assign(static_cast<size_t>(n_units), 0);
+        if (final_weight) node_fin.assign(static_cast<size_t>(n_units), 0.0f);
+        for (int32_t s = 0; s < n; s++) {
+            const int64_t h = hdr_pos[s];
+            const int32_t deg = eoff[s + 1] - eoff[s];
+            node[h] = make_int4(static_cast<int32_t>(h + 2), static_cast<int32_t>(h + 2 + deg), xoff[s], xoff[s + 1]);
+            int4 x0 = srec[2 * static_cast<size_t>(s) + 1];
+            if (xoff[s + 1] > xoff[s]) x0.x = remap(x0.x);
+            node[h + 1] = x0;
+            for (int32_t j = 0; j < deg; j++) {
+                int4 r = earc[eoff[s] + j];
+                r.x = remap(r.x);
+                node[h + 2 + j] = r;
+                node_eua[h + 2 + j] = eua[eoff[s] + j];
+            }
+            if (final_weight) node_fin[h] = final_weight[s];
+        }
+        for (auto &r : xarc) r.x = remap(r.x);
+        for (size_t i = 0; i < ctab.size(); i += kClosureStride) ctab[i].x = hdr_pos[ctab[i].x];
+        for (int64_t a = 0; a < e; a++)
+            if (ilabel[a]) uarc[a].y = hdr_pos[src[a]] + 2 + (uarc[a].y - eoff[src[a]]);
+        std::vector<int4>().swap(earc);
+        std::vector<int4>().swap(srec);
+        std::vector<int32_t>().swap(eua);
     } catch (const std::bad_alloc &) {
         return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
     }
 
     auto align = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
-    const size_t b_eoff = align((static_cast<size_t>(n) + 1) * 4);
-    const size_t b_xoff = b_eoff;
-    const size_t b_earc = align(static_cast<size_t>(n_emit) * 16 + 16);
-    const size_t b_eua = align(static_cast<size_t>(n_emit) * 4 + 4);
+    const size_t units = static_cast<size_t>(n_units);
+    const size_t b_node = align(units * 16 + 16);
+    const size_t b_eua = align(units * 4 + 4);
     const size_t b_xarc = align(static_cast<size_t>(n_eps) * 16 + 16);
     const size_t b_src = align(static_cast<size_t>(e) * 4 + 4);
-    const size_t b_fin = final_weight ? align(static_cast<size_t>(n) * 4) : 0;
-    const size_t b_srec = align(static_cast<size_t>(n) * 32);
+    const size_t b_fin = final_weight ? align(units * 4) : 0;
     const size_t b_ctab = align(ctab.size() * 16 + 16);
     const size_t b_uarc = align(static_cast<size_t>(e) * 8 + 8);
-    const size_t total = b_eoff + b_xoff + b_earc + b_eua + b_xarc + b_src + b_fin + b_srec + b_ctab + b_uarc;
+    const size_t total = b_node + b_eua + b_xarc + b_src + b_fin + b_ctab + b_uarc;
 
     wfst_graph *h = new (std::nothrow) wfst_graph();
     if (!h) return fail(WFST_ENOMEM, "wfst_load: host allocation failed");
@@ -240,17 +285,16 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     };
     g.d.n = n;
     g.d.e = e;
-    g.d.start = start;
+    g.d.start = hdr_pos[start];
     g.d.n_emit = n_emit;
     g.d.n_eps = n_eps;
-    g.d.eoff = static_cast<const int32_t *>(put(eoff.data(), eoff.size() * 4, b_eoff));
-    g.d.xoff = static_cast<const int32_t *>(put(xoff.data(), xoff.size() * 4, b_xoff));
-    g.d.earc = static_cast<const int4 *>(put(earc.data(), earc.size() * 16, b_earc));
-    g.d.eua = static_cast<const int32_t *>(put(eua.data(), eua.size() * 4, b_eua));
+    g.d.node = static_cast<const int4 *>(put(node.data(), node.size() * 16, b_node));
+    g.d.earc = g.d.node;
+    g.d.srec = g.d.node;
+    g.d.eua = static_cast<const int32_t *>(put(node_eua.data(), node_eua.size() * 4, b_eua));
     g.d.xarc = static_cast<const int4 *>(put(xarc.data(), xarc.size() * 16, b_xarc));
     g.d.arc_src = static_cast<const int32_t *>(put(arc_src.data(), arc_src.size() * 4, b_src));
-    g.d.final_w = final_weight ? static_cast<const float *>(put(final_weight, static_cast<size_t>(n) * 4, b_fin)) : nullptr;
-    g.d.srec = static_cast<const int4 *>(put(srec.data(), srec.size() * 16, b_srec));
+    g.d.final_w = final_weight ? static_cast<const float *>(put(node_fin.data(), units * 4, b_fin)) : nullptr;
     g.d.ctab = static_cast<const int4 *>(put(ctab.data(), ctab.size() * 16, b_ctab));
     g.d.uarc = static_cast<const int2 *>(put(uarc.data(), uarc.size() * 8, b_uarc));
     if (err != hipSuccess) {
@@ -264,6 +308,7 @@ extern "C" int wfst_load(int32_t n, int64_t e, const int32_t *src, const int32_t
     g.eps_depth = depth;
     g.device_bytes = static_cast<int64_t>(total);
     g.n_closure = n_closure;
+    g.hdr_pos = std::move(hdr_pos);
     *out = h;
     return WFST_OK;
 }

@@ -25,8 +25,10 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cstdint>
+#include <vector>
 
 #include "wfstdec.h"
 
@@ -49,23 +51,32 @@ constexpr int kWave = 64;                   // gfx950 wavefront
 constexpr uint32_t kHashMul = 0x9E3779B1u;
 constexpr uint32_t kHashMulAlt = 0x85EBCA77u;
 
+// The graph on the device.  States are numbered by the position of their
+// first record in `node`, an array of 16-byte units where each state's two
+// records are followed by its emitting arcs:
+//   node[s]     = {first emitting arc, end of its emitting arcs (both unit
+//                  indices into node), first and end epsilon record in xarc}
+//   node[s + 1] = the state's first epsilon record (destination, weight,
+//                  user arc) with the state's closure word as its 4th word
+//                  ((first entry + 1) << kClosureSizeBits | size - 1, 0 if
+//                  it has no list)
+//   node[a]     = an emitting arc: {dst | has-epsilon bit << 31, ilabel - 1,
+//                  weight bits, closure word of dst}
+// Ids keep the order of the user's state ids; Graph::hdr_pos maps back.
 struct DevGraph {
     int32_t n;
-    int32_t start;
+    int32_t start;      // device id of the start state
     int64_t e;
     int64_t n_emit, n_eps;
-    const int32_t *eoff;
-    const int4 *earc;   // emitting records by source: {dst | has-epsilon bit, ilabel - 1, weight, closure word of dst}
-    const int32_t *eua; // user arc of each emitting record
-    const int32_t *xoff;
+    const int4 *node;
+    const int4 *earc;   // = node (arc records by unit index)
+    const int4 *srec;   // = node (state records by device id)
+    const int32_t *eua; // user arc of each emitting arc record, by unit index
     const int4 *xarc;   // epsilon records by source: {dst | has-epsilon bit, weight, user arc, closure word of dst}
     const int32_t *arc_src;
-    const float *final_w;
-    const int4 *srec;   // 2 x N: {eoff[s], eoff[s+1], xoff[s], xoff[s+1]}, first epsilon record of s
-                        // whose 4th word is the state's closure list
-                        // ((offset + 1) << kClosureSizeBits | size - 1, or 0)
+    const float *final_w;   // by device id (0 elsewhere), or NULL
     const int4 *ctab;   // closure entries, 3 x int4 each: {dst, user arc, path length, w0}, {w1..w4}, {w5..w8}
-    const int2 *uarc;   // per user arc: {olabel, index of its record in earc or xarc}
+    const int2 *uarc;   // per user arc: {olabel, index of its record in node or xarc}
 };
 
 // Epsilon-closure lists (built by wfst_load): at most kClosureMax paths of at
@@ -86,11 +97,20 @@ struct Graph {
     int32_t eps_depth;
     int64_t device_bytes;
     int64_t n_closure;   // states with an epsilon-closure list
+    std::vector<int32_t> hdr_pos;   // device id of each user state (increasing)
     void *mem;   // single device allocation holding every array
     // lattice-record slots per token that the last decodes on this graph
     // needed (emitting, epsilon), a starting point for the next ones
     mutable std::atomic<int64_t> rec_em{0}, rec_xm{0};
 };
+
+// The user's state id of a device state id (-1 stays -1).
+inline int32_t user_state(const Graph &g, int32_t dev)
+{
+    if (dev < 0) return dev;
+    const auto it = std::upper_bound(g.hdr_pos.begin(), g.hdr_pos.end(), dev);
+    return static_cast<int32_t>(it - g.hdr_pos.begin()) - 1;
+}
 
 // Per-utterance decode state in device memory.
 struct UttState {

@@ -175,8 +175,8 @@ __device__ void record_set(const Params &p, int u, int k, const RTab<G> &t, unsi
         if (i < n) {
             const int64_t s = sv_state[b0 + i];
             cst = okey_val(sv_key[b0 + i]);
-            lo = p.g.srec[2 * s];
-            x = p.g.srec[2 * s + 1];
+            lo = p.g.srec[s];
+            x = p.g.srec[s + 1];
             xd = lo.w - lo.z;
         }
         // the first epsilon arc, copied into the state record

@@ -512,8 +512,8 @@ __device__ __forceinline__ void relax(const Params &p, const Tab<G> &t, Sh &sh, 
                 cn = static_cast<int>(icl & kSizeMask) + 1;
             } else {
                 const int64_t s = static_cast<int64_t>(tld<G>(t.keys + it.x));
-                const int4 lo = p.g.srec[2 * s];
-                x0 = p.g.srec[2 * s + 1];
+                const int4 lo = p.g.srec[s];
+                x0 = p.g.srec[s + 1];
                 const uint32_t cl = static_cast<uint32_t>(x0.w);
                 // A list of one path is the state's only epsilon arc, into
                 // a state without epsilon arcs: the copy of that arc in the
@@ -688,7 +688,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     if (k == 0) {
         if (wid == 0) {
             const int s = p.g.start;
-            const int4 lo = p.g.srec[2 * static_cast<int64_t>(s)];
+            const int4 lo = p.g.srec[s];
             offer1<G>(t, sh, wq, lane == 0, static_cast<uint32_t>(s), lo.w > lo.z, 0u, 0.0f, okey(0.0f));
         }
     } else {
@@ -836,7 +836,7 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
 #pragma unroll
         for (int r = 0; r < kCompact; r++) {
             lo[r] = make_int4(0, 0, 0, 0);
-            if (kp[r]) lo[r] = p.g.srec[2 * static_cast<int64_t>(dd[r])];
+            if (kp[r]) lo[r] = p.g.srec[dd[r]];
         }
 #pragma unroll
         for (int r = 0; r < kCompact; r++) {
