@@ -20,7 +20,7 @@ OUT = os.path.join(PKG, "libwfstdec.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["graph.cpp", "decode.cpp", "search_kernel.hip", "record_kernel.hip", "final_kernels.hip", "word_kernel.hip"]
-HEADERS = ["internal.h", "device_util.h"]
+HEADERS = ["internal.h", "device_util.h", "record_set.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -50,7 +50,6 @@ constexpr int kFill = 6144;               // LDS states per frame before falling
 constexpr int kQueue = 128;               // LDS epsilon items per wave queue
 constexpr int kSetCache = 3008;           // tokens of the previous set kept in LDS for the expansion
 constexpr int kCs = 128;                  // 64-arc chunks of the previous set with their first token in LDS
-constexpr int kCompact = 1;               // slot-list chunks a wave has in flight in the compaction
 constexpr int kChunks = 2;                // 64-arc chunks a wave has in flight in the expansion
 constexpr int kRelChunks = 2;             // 64-path chunks of closure lists a wave has in flight
 constexpr int kMaxProbe = 64;             // linear-probe bound (the fill limit keeps probes short)
@@ -813,87 +812,97 @@ __device__ __forceinline__ int frame(const Params &p, const UttLayout &ly, const
     using Slot = typename Tab<G>::Slot;
     const int64_t set0 = run.set0;
     int xacc = 0;   // epsilon degrees of this lane's survivors
-    for (int c = wid; c * kWave < n; c += kW * kCompact) {
-        bool kp[kCompact];
-        uint32_t vv[kCompact];
-        int dd[kCompact];
-#pragma unroll
-        for (int r = 0; r < kCompact; r++) {
-            const int i = (c + r * kW) * kWave + lane;
-            kp[r] = false;
-            vv[r] = kEmptyKey;
-            dd[r] = 0;
-            if (i < n) {
-                const Slot sl = tld<G>(t.slots + i);
-                vv[r] = tld<G>(t.vals + sl);
-                dd[r] = static_cast<int>(tld<G>(t.keys + sl));
-                kp[r] = vv[r] <= cut;
-                t.keys[sl] = kEmptyKey;
-                t.vals[sl] = kEmptyKey;
-            }
+    // The row goes into LDS in the wave's first chunk, after its state-record
+    // loads and before its first survivor stores: vector memory operations
+    // complete in issue order, so a wait for the row after any store would
+    // also wait for that store.
+    bool row_due = next_row;
+    for (int c = wid; c * kWave < n; c += kW) {
+        const int i = c * kWave + lane;
+        bool kp = false;
+        uint32_t vv = kEmptyKey;
+        int dd = 0;
+        if (i < n) {
+            const Slot sl = tld<G>(t.slots + i);
+            vv = tld<G>(t.vals + sl);
+            dd = static_cast<int>(tld<G>(t.keys + sl));
+            kp = vv <= cut;
+            t.keys[sl] = kEmptyKey;
+            t.vals[sl] = kEmptyKey;
         }
-        int4 lo[kCompact];
+        int4 lo = make_int4(0, 0, 0, 0);
+        if (kp) lo = p.g.srec[dd];
+        if (row_due) {
 #pragma unroll
-        for (int r = 0; r < kCompact; r++) {
-            lo[r] = make_int4(0, 0, 0, 0);
-            if (kp[r]) lo[r] = p.g.srec[dd[r]];
+            for (int j = 0; j < kRowPer; j++) {
+                const int ri = tid + j * kT;
+                if (ri < p.L) s_row[ri] = rv[j];
+            }
+            row_due = false;
         }
-#pragma unroll
-        for (int r = 0; r < kCompact; r++) {
-            const uint64_t km = __ballot(kp[r]);
-            if (!km) continue;
-            const int tc = __popcll(km);
-            const int deg = kp[r] ? lo[r].y - lo[r].x : 0;
-            xacc += kp[r] ? lo[r].w - lo[r].z : 0;
-            const int id = wave_incl_scan(deg);
-            const int td = __builtin_amdgcn_readlane(id, kWave - 1);
-            unsigned long long base = 0;
-            if (lane == 0)
-                base = atomicAdd(&sh.alloc[k & 1],
-                                 (static_cast<unsigned long long>(td) << 32) | static_cast<uint32_t>(tc));
-            base = (static_cast<unsigned long long>(__builtin_amdgcn_readlane(static_cast<int>(base >> 32), 0)) << 32) |
-                   static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(base), 0));
-            if (!kp[r]) continue;
-            const int pos = static_cast<int>(static_cast<uint32_t>(base)) + rank_in(km);
-            const int apos = static_cast<int>(base >> 32) + id - deg;
-            const int64_t rel = set0 + pos;
-            if (rel < ly.svcap) {
-                const int64_t o = ly.sv0 + rel;
-                p.sv_state[o] = dd[r];
-                p.sv_key[o] = vv[r];
-                p.sv_ebeg[o] = lo[r].x;
-                p.sv_epre[o] = apos;
-            } else {
-                sh.status = WFST_ECAPACITY;
-            }
-            if (pos < kSetCache) {
-                s_cost[pos] = okey_val(vv[r]);
-                s_epre[pos] = apos;
-                s_ebeg[pos] = lo[r].x;
-                // the chunks whose first arc is one of this token's
-                for (int ch = (apos + kWave - 1) / kWave; ch * kWave < apos + deg && ch < kCs; ch++)
-                    s_cs[ch] = static_cast<uint16_t>(pos);
-            }
+        // (lo is used on every path: a load left pending into the next round
+        // would make that round wait before writing its registers)
+        const uint64_t km = __ballot(kp);
+        const int tc = __popcll(km);
+        const int deg = kp ? lo.y - lo.x : 0;
+        xacc += kp ? lo.w - lo.z : 0;
+        const int id = wave_incl_scan(deg);
+        const int td = __builtin_amdgcn_readlane(id, kWave - 1);
+        unsigned long long base = 0;
+        if (lane == 0 && tc)
+            base = atomicAdd(&sh.alloc[k & 1], (static_cast<unsigned long long>(td) << 32) | static_cast<uint32_t>(tc));
+        base = (static_cast<unsigned long long>(__builtin_amdgcn_readlane(static_cast<int>(base >> 32), 0)) << 32) |
+               static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(base), 0));
+        if (!kp) continue;
+        const int pos = static_cast<int>(static_cast<uint32_t>(base)) + rank_in(km);
+        const int apos = static_cast<int>(base >> 32) + id - deg;
+        if (pos < kSetCache) {
+            // to the survivor arrays after the barrier below
+            s_cost[pos] = okey_val(vv);
+            s_epre[pos] = apos;
+            s_ebeg[pos] = lo.x;
+            // the chunks whose first arc is one of this token's
+            for (int ch = (apos + kWave - 1) / kWave; ch * kWave < apos + deg && ch < kCs; ch++)
+                s_cs[ch] = static_cast<uint16_t>(pos);
+        } else if (set0 + pos < ly.svcap) {
+            const int64_t o = ly.sv0 + set0 + pos;
+            p.sv_state[o] = dd;
+            p.sv_key[o] = vv;
+            p.sv_ebeg[o] = lo.x;
+            p.sv_epre[o] = apos;
         }
     }
     {
         const int tx = wave_incl_scan(xacc);
         if (lane == kWave - 1 && tx) atomicAdd(&sh.xsum[k & 1], tx);
     }
-    if (next_row) {
+    if (row_due) {
 #pragma unroll
         for (int j = 0; j < kRowPer; j++) {
-            const int i = tid + j * kT;
-            if (i < p.L) s_row[i] = rv[j];
+            const int ri = tid + j * kT;
+            if (ri < p.L) s_row[ri] = rv[j];
         }
     }
-    // the next expansion reads S_k from LDS unless it is larger than the LDS
-    // copy; then its device-memory stores must be complete (and the cleared
-    // device-memory table before the next offers)
+    // (with the device-memory table, its cleared slots before the next offers)
     table_barrier<G>();
     const unsigned long long alloc = sh.alloc[k & 1];
-    if (!G && static_cast<uint32_t>(alloc) > static_cast<uint32_t>(kSetCache)) __syncthreads();
     const int n_kept = static_cast<int>(static_cast<uint32_t>(alloc));
+    // The survivors placed in the LDS copy go to the survivor arrays now, in
+    // one batch of stores that overlaps the next frame's start (a state's id
+    // is its first emitting unit minus 2).  Stores inside the loop above
+    // would make each of its rounds wait for them.
+    if (set0 + n_kept > ly.svcap) return WFST_ECAPACITY;
+    for (int i = tid; i < min(n_kept, kSetCache); i += kT) {
+        const int64_t o = ly.sv0 + set0 + i;
+        const int32_t eb = s_ebeg[i];
+        p.sv_state[o] = eb - 2;
+        p.sv_key[o] = okey(s_cost[i]);
+        p.sv_ebeg[o] = eb;
+        p.sv_epre[o] = s_epre[i];
+    }
+    // the next expansion reads S_k from LDS unless it is larger than the LDS
+    // copy; then it reads the survivor arrays, which other waves wrote
+    if (static_cast<uint32_t>(alloc) > static_cast<uint32_t>(kSetCache)) __syncthreads();
     const int a_kept = static_cast<int>(alloc >> 32);
     const int x_kept = sh.xsum[k & 1];
     const int ns = n_kept;
