@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 from concurrent.futures import ThreadPoolExecutor
@@ -33,7 +34,8 @@ COUNTERS = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_counters.txt"
 TRACE = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_trace.txt")
 SQ = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_sq.txt")
 CSRC = os.path.join(ROOT, "paper_1808_00687_amd", "csrc")
-KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("search_kernel.hip", "device_util.h", "internal.h")]
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("search_body.h", "search_kernel.hip", "search_record_kernel.hip",
+                                                   "record_set.h", "device_util.h", "internal.h")]
 KERNEL_NAME = "search_kernel"
 # the 64-utterance batch's search is this many concurrent launches (the
 # library's length groups: at most four, of at least 16 utterances each)
@@ -41,15 +43,21 @@ GROUP_LAUNCHES = 4
 CALIBRATION_MIB = 1024
 TRACE_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_search -o run -- "
              "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline")
+# The counter passes run with the record workgroups off (--record-groups -1):
+# the last length group's search launch then holds its search alone, and the
+# counters count the search's work only.
 PMC_CMD = ("timeout -s KILL 180 rocprofv3 --pmc {counter} --output-format csv -d gpurun_out/pmc_{tag} -o run -- "
-           "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile --copy-calibration-mib %d"
-           % CALIBRATION_MIB)
+           "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile --record-groups -1 "
+           "--copy-calibration-mib %d" % CALIBRATION_MIB)
 SQ_PASSES = (("a", "SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY SQ_INSTS_VALU "
                    "SQ_INSTS_LDS SQ_INSTS_SALU"),
              ("b", "SQ_INSTS_VMEM_RD SQ_INSTS_VMEM_WR SQ_INSTS_BRANCH SQ_WAIT_INST_LDS SQ_ACTIVE_INST_VALU "
                    "SQ_ACTIVE_INST_LDS SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS_ATOMIC"))
 SQ_CMD = ("timeout -s KILL 120 rocprofv3 --pmc {counters} --output-format csv -d gpurun_out/sq{tag} -o run -- "
-          "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile")
+          "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile --record-groups -1")
+OVERLAP = os.path.join(PROFILES, "lattice_stream_kernel_lvcsr-25m-batch64_overlap.txt")
+OVERLAP_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_incr -o run -- "
+               "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-profile --incremental-lattice")
 
 # name: (config, label-synchronous, frame stride); cfg6 is the HMM-topology
 # stand-in (a set of blank-like units), not one of the five listed configs
@@ -134,7 +142,8 @@ def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str):
            % (KERNEL_NAME, GROUP_LAUNCHES),
            "# fetch command: " + PMC_CMD.format(counter="FETCH_SIZE", tag="fetch"),
            "# write command: " + PMC_CMD.format(counter="WRITE_SIZE", tag="write"),
-           "# counters are KiB per dispatch; each is scaled by bytes/reading of a %d MiB device copy" % CALIBRATION_MIB]
+           "# counters are KiB per dispatch; each is scaled by bytes/reading of a %d MiB device copy" % CALIBRATION_MIB,
+           "# taken with the record workgroups off (--record-groups -1): the search's own traffic"]
     total = 0.0
     for tag, path in (("fetch", fetch_csv), ("write", write_csv)):
         rows = list(csv.DictReader(open(path)))
@@ -194,6 +203,64 @@ def write_sq_profile(csv_a: str, csv_b: str):
     lines.append("kernel_source_sha256: %s" % kernel_sha())
     open(SQ, "w").write("\n".join(lines) + "\n")
     print(SQ)
+
+
+def write_overlap_profile(trace_csv: str):
+    """Summary of a kernel trace of the incremental lattice mode for
+    profiles/: per batch, the interval of the search launch and of the
+    lattice pass beside it on the library's second stream, how long the two
+    ran at the same time, and the kernels that follow the search."""
+    import csv
+    rows = sorted(((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"])
+                   for r in csv.DictReader(open(trace_csv)) if "wfd::" in r["Kernel_Name"]))
+    # a batch starts with the kernels the decode launches before its search
+    # (clearing and frame classification)
+    starts, first = [], 0
+    for si, r in enumerate(rows):
+        if KERNEL_NAME in r[2]:
+            i = si
+            while i > first and any(k in rows[i - 1][2] for k in ("zero_kernel", "classify_kernel")):
+                i -= 1
+            starts.append((i, si))
+            first = si + 1
+    lines = ["# kernel trace of the incremental lattice mode, workload lvcsr-25m-batch64 (64 utterances, "
+             "25M-arc graph): one search launch per batch on the decode stream, one lattice_stream_kernel "
+             "launch beside it on a second stream",
+             "# command: " + OVERLAP_CMD,
+             "# summary written by: python3 bench.py --write-overlap-profile gpurun_out/prof_incr/run_kernel_trace.csv",
+             "# times in ms relative to the batch's first kernel start; overlap = time both kernels ran",
+             "%5s %9s %9s %9s %9s %9s %9s %9s" % ("batch", "search0", "search1", "lat0", "lat1", "overlap",
+                                                 "lat_after", "batch_end")]
+    agg = []
+    for b, (i, si) in enumerate(starts):
+        window = rows[i:starts[b + 1][0] if b + 1 < len(starts) else len(rows)]
+        t0 = min(r[0] for r in window)
+        s0, s1 = rows[si][0], rows[si][1]
+        lat = [r for r in window if "lattice_stream_kernel" in r[2]]
+        if not lat:
+            continue
+        l0, l1 = lat[0][0], lat[0][1]
+        ov = max(0, min(s1, l1) - max(s0, l0))
+        end = max(r[1] for r in window)
+        vals = [(x - t0) / 1e6 for x in (s0, s1, l0, l1)] + [ov / 1e6, max(0, l1 - s1) / 1e6, (end - t0) / 1e6]
+        agg.append(vals)
+        lines.append("%5d " % b + " ".join("%9.2f" % v for v in vals))
+    if len(agg) > 1:
+        tail = agg[1:]
+        mean = [sum(v[j] for v in tail) / len(tail) for j in range(len(tail[0]))]
+        lines.append("mean over batches 1..%d: search %.2f ms, lattice pass %.2f ms, overlap %.2f ms (%.0f%% of "
+                     "the search), lattice pass after the search %.2f ms, batch %.2f ms"
+                     % (len(agg) - 1, mean[1] - mean[0], mean[3] - mean[2], mean[4],
+                        100.0 * mean[4] / max(mean[1] - mean[0], 1e-9), mean[5], mean[6]))
+    names = {}
+    for r in rows[starts[min(1, len(starts) - 1)][0]:] if starts else []:
+        k = re.findall(r"(\w+)\(", r[2])
+        names.setdefault(k[0] if k else r[2], []).append((r[1] - r[0]) / 1e6)
+    lines.append("%-28s %6s %12s" % ("kernel (batches 1..)", "calls", "mean_ms"))
+    for k in sorted(names, key=lambda k: -sum(names[k])):
+        lines.append("%-28s %6d %12.3f" % (k, len(names[k]), sum(names[k]) / len(names[k])))
+    open(OVERLAP, "w").write("\n".join(lines) + "\n")
+    print(OVERLAP)
 
 
 def cpu_model() -> str:
@@ -304,7 +371,15 @@ def main():
                     help="also build the word-level lattice (not the benchmark line)")
     ap.add_argument("--write-sq-profile", nargs=2, metavar=("PASS_A_CSV", "PASS_B_CSV"),
                     help="write the SQ counter summary for profiles/ and exit")
+    ap.add_argument("--record-groups", type=int, default=0,
+                    help="record workgroups in the last length group's search launch (-1: none, the record "
+                         "kernel runs after that search; 0: the library's default)")
+    ap.add_argument("--write-overlap-profile", metavar="TRACE_CSV",
+                    help="write the incremental-mode overlap summary for profiles/ and exit")
     args = ap.parse_args()
+    if args.write_overlap_profile:
+        write_overlap_profile(args.write_overlap_profile)
+        return
     if args.write_profiles:
         write_profiles(*args.write_profiles)
         return
@@ -349,6 +424,8 @@ def main():
                                          incremental_lattice=args.incremental_lattice,
                                          word_lattice=args.word_lattice)
 
+    if args.record_groups:
+        wfstdec.wfst_set_debug_opts(record_groups=args.record_groups)
     for i in range(args.warmup):
         res = step(False)
         log("warmup %d done" % i)
@@ -399,6 +476,9 @@ def main():
             "parallelism": "utterance batch of %d on 1 GPU" % len(wl.loglikes),
             "lattice_mode": ("incremental" if args.incremental_lattice else "one-shot")
                             + (" + word lattice" if args.word_lattice else ""),
+            "record_pass": ("beside the search (incremental pass)" if args.incremental_lattice else
+                            "after each length group's search" if args.record_groups < 0 else
+                            "beside the last length group's search, after the others'"),
         },
         "rtf": sec / (frames * FRAME_SHIFT_S),
         "original_frames_per_s": frames / sec,

@@ -411,10 +411,17 @@ int wfst_decode_noalloc(const wfst_graph *g, const float *loglikes, int32_t T, i
  *                      (WFST_INCREMENTAL_LATTICE); -1 turns the pass off
  *   lattice_ring       raw records the incremental pass's rings hold (a
  *                      small ring makes chunks end early and wrap around)
+ *   record_groups      record workgroups appended to the search launch of
+ *                      the batch's last length group, which derive its
+ *                      back-pointers and raw lattice records while it
+ *                      searches; -1 leaves that group to the record kernel
+ *                      after its search
+ *   record_publish     token sets between the search's progress reports to
+ *                      those workgroups
  *
  * opts == NULL restores every default.  Takes effect for decodes started
  * after the call returns.  Errors: WFST_EINVAL for a negative field other
- * than lattice_lds = -1 and lattice_chunk = -1.
+ * than lattice_lds = -1, lattice_chunk = -1 and record_groups = -1.
  */
 typedef struct wfst_debug_opts {
     int32_t lds_fill;
@@ -426,6 +433,8 @@ typedef struct wfst_debug_opts {
     int32_t fail_lattice_alloc;
     int32_t lattice_chunk;
     int32_t lattice_ring;
+    int32_t record_groups;
+    int32_t record_publish;
 } wfst_debug_opts;
 
 int wfst_set_debug_opts(const wfst_debug_opts *opts);

@@ -19,8 +19,9 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "libwfstdec.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["graph.cpp", "decode.cpp", "search_kernel.hip", "record_kernel.hip", "final_kernels.hip", "word_kernel.hip"]
-HEADERS = ["internal.h", "device_util.h", "record_set.h"]
+SOURCES = ["graph.cpp", "decode.cpp", "search_kernel.hip", "search_record_kernel.hip", "record_kernel.hip",
+           "final_kernels.hip", "word_kernel.hip"]
+HEADERS = ["internal.h", "device_util.h", "record_set.h", "search_body.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

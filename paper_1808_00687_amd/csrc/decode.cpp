@@ -407,6 +407,11 @@ constexpr int kAuxStreams = kGroupStreams + 1;
 // search's must be resident together: two per utterance, one per CU).
 constexpr int kStreamK = 32;
 constexpr int kStreamMaxUtts = 96;
+// Record workgroups appended to the search launch of the last (longest)
+// length group, and the token sets between the search's progress reports to
+// them: the record pass of those utterances then ends with their search.
+constexpr int kRecGroups = 96;
+constexpr int kRecPublish = 16;
 // The lattice regions with the incremental pass: this fraction of the
 // one-shot regions (the pass keeps a few percent of the raw arcs; an
 // overflow grows every buffer and decodes again)
@@ -550,8 +555,12 @@ void carve_ws(Arena &a, Params &p, int U, const Totals &tot, UttLayout **d_lay, 
     // reserves (possibly on another chiplet), else the same arrays
     p.rle_off = p.stream_k && f ? f + 6 * fo : p.le_off;
     p.rlx_off = p.stream_k && f ? f + 7 * fo : p.lx_off;
+    if (p.stream_k || p.rec_wg) {
+        // progress counts, then the record workgroups' item counter
+        p.prog = a.get<int32_t>(U + 1);
+        p.rec_next = p.prog + U;
+    }
     if (p.stream_k) {
-        p.prog = a.get<int32_t>(U);
         p.rng_e = a.get<int4>(U * p.rce);
         p.rng_ee = a.get<float>(U * p.rce);
         p.rng_x = a.get<int4>(U * p.rcx);
@@ -736,6 +745,11 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     else blank_h.push_back(o.blank_id);
     Params p{};
     set_params(p, G, U, L, o, thr, dbg, z, static_cast<int32_t>(blank_h.size()), U <= kStreamMaxUtts);
+    // record workgroups beside the last length group's search (the
+    // incremental pass records beside the search itself)
+    const int rec_wg = p.stream_k || dbg.record_groups < 0 ? 0 : (dbg.record_groups > 0 ? dbg.record_groups : kRecGroups);
+    const int rec_pub = dbg.record_publish > 0 ? dbg.record_publish : kRecPublish;
+    p.rec_wg = rec_wg;
     WallTrace wt;
     UttLayout *d_lay = nullptr;
     int64_t *fo_all = nullptr;
@@ -774,7 +788,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     chk(launch_zero(fo_all, kOffsetArrays * fo * sizeof(int64_t), s));
     // the progress counts start at 0: a stale count from an earlier decode
     // would let the lattice pass read token sets before they exist
-    if (p.stream_k) chk(launch_zero(p.prog, U * sizeof(int32_t), s));
+    if (p.prog) chk(launch_zero(p.prog, (U + 1) * sizeof(int32_t), s));
     chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), blank_h.data(), blank_h.size() * sizeof(int32_t),
                        hipMemcpyHostToDevice, s));
     chk(launch_classify(p, s));
@@ -843,6 +857,15 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         }
         int Tg = 0;
         for (int u = u0; u < u1; u++) Tg = std::max(Tg, T[u]);
+        pg.pub_k = p.stream_k;
+        pg.rec_wg = 0;
+        const bool fused = rec_wg > 0 && g == ng - 1 && pg.U <= kRecMaxUtts;
+        if (fused) {
+            pg.prog = p.prog + u0;
+            pg.pub_k = rec_pub;
+            pg.rec_wg = rec_wg;
+            pg.rec_tmax = Tg;
+        }
         const hipStream_t q = gs[g];
         tm.start(q);
         chk(launch_search(pg, q));
@@ -862,8 +885,10 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
             chk(hipEventRecord(done, ls[g]));
             chk(hipStreamWaitEvent(q, done, 0));
         } else {
+            // with record workgroups in the search launch only the sets
+            // beyond their LDS table are left
             tm.start(q);
-            chk(launch_record(pg, Tg, q));
+            chk(fused ? launch_record_large(pg, q) : launch_record(pg, Tg, q));
             tm.stop(PH_RECORD, q);
         }
         tm.start(q);
@@ -905,7 +930,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         if (st[u].status == kStatusNoBackPointer)
             return fail(WFST_EDEVICE, "decode: internal error, a surviving token without a back-pointer");
         if (st[u].status == kStatusStreamTimeout)
-            return fail(WFST_EDEVICE, "decode: internal error, the lattice pass stopped waiting for the search");
+            return fail(WFST_EDEVICE, "decode: internal error, a pass beside the search stopped waiting for it");
     }
 
     std::shared_ptr<LatBuf> lat_buf;
@@ -1390,7 +1415,7 @@ extern "C" int wfst_set_debug_opts(const wfst_debug_opts *opts)
         o = *opts;
         if (o.lds_fill < 0 || o.queue_cap < 0 || o.record_fill < 0 || o.record_big_fill < 0 ||
             o.lattice_lds < -1 || o.permute < 0 || o.fail_lattice_alloc < 0 || o.lattice_chunk < -1 ||
-            o.lattice_ring < 0)
+            o.lattice_ring < 0 || o.record_groups < -1 || o.record_publish < 0)
             return fail(WFST_EINVAL, "wfst_set_debug_opts: negative field");
     }
     DebugState &d = debug_state();

@@ -38,9 +38,12 @@ constexpr uint64_t kEmptyTok = ~0ull;
 // Utterance status of a survivor that the record pass found no back-pointer
 // for (never expected: reported as a device error)
 constexpr int kStatusNoBackPointer = -9;
-// Utterance status: the incremental lattice pass stopped waiting for the
-// search (never expected: reported as a device error)
+// Utterance status: the incremental lattice pass or the record workgroups
+// stopped waiting for the search (never expected: reported as a device error)
 constexpr int kStatusStreamTimeout = -11;
+// utterances a search launch with record workgroups may hold (their LDS
+// keeps a progress count per utterance)
+constexpr int kRecMaxUtts = 256;
 constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;
 constexpr uint32_t kDstMask = 0x7FFFFFFFu;
 constexpr int kHistBits = 12;               // radix-select digit width
@@ -230,6 +233,15 @@ struct Params {
     int64_t capG;             // power of two
     uint2 *gspill;            // U x 2 x capO {table slot, cost bits}
     int64_t capO;
+    // The search publishes prog[u] every pub_k token sets (0: never): for
+    // the incremental pass, or for rec_wg record workgroups appended to the
+    // search launch, which take (set, utterance) items from *rec_next (zeroed
+    // before the launch) up to set rec_tmax.  (Last: the offsets of the
+    // fields above, which the search reads, stay as they were.)
+    int32_t pub_k;
+    int32_t rec_wg;           // at most kRecMaxUtts utterances in such a launch
+    int32_t rec_tmax;
+    int32_t *rec_next;
 };
 
 // Workspace of the word-level lattice pass (word_kernel.hip), uniform
@@ -270,11 +282,16 @@ __host__ __device__ inline WordWs word_ws_of(const WordWs &w, int u, const UttLa
     return r;
 }
 
-// ---- launchers (search_kernel.hip / final_kernels.hip) ----
+// ---- launchers (search_kernel.hip, search_record_kernel.hip, record_kernel.hip, final_kernels.hip) ----
 hipError_t launch_classify(const Params &p, hipStream_t s);
 hipError_t launch_search(const Params &p, hipStream_t s);
+// the search launch with p.rec_wg record workgroups (launch_search calls it)
+hipError_t launch_search_record(const Params &p, hipStream_t s);
 hipError_t launch_final(const Params &p, hipStream_t s);
 hipError_t launch_record(const Params &p, int max_frames, hipStream_t s);
+// only the sets larger than the record kernel's LDS table (after a search
+// launch with record workgroups)
+hipError_t launch_record_large(const Params &p, hipStream_t s);
 hipError_t launch_lattice_stream(const Params &p, hipStream_t s);
 hipError_t launch_finish(const Params &p, hipStream_t s);
 hipError_t launch_pack_paths(const Params &p, hipStream_t s);

@@ -379,13 +379,18 @@ hipError_t launch_lattice_stream(const Params &p, hipStream_t s)
     return hipGetLastError();
 }
 
+hipError_t launch_record_large(const Params &p, hipStream_t s)
+{
+    hipLaunchKernelGGL(record_large_kernel, dim3(p.U, kLargeParts), dim3(kRT), 0, s, p);
+    return hipGetLastError();
+}
+
 hipError_t launch_record(const Params &p, int max_frames, hipStream_t s)
 {
     hipLaunchKernelGGL(record_kernel, dim3(max_frames + 1, p.U), dim3(kRT), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(record_large_kernel, dim3(p.U, kLargeParts), dim3(kRT), 0, s, p);
-    return hipGetLastError();
+    return launch_record_large(p, s);
 }
 
 }  // namespace wfd

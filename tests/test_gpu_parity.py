@@ -437,6 +437,42 @@ def test_batch_groups_match_oracle(dec, torch_mod, oracle_mod):
     gh.free()
 
 
+@pytest.mark.parametrize("groups,publish,fill", [(-1, 0, 0), (0, 0, 0), (1, 1, 0), (2, 3, 0), (5, 1, 8),
+                                                   (64, 7, 0)])
+def test_record_workgroups_beside_search(dec, torch_mod, oracle_mod, groups, publish, fill):
+    # The record pass of the last length group runs in workgroups appended to
+    # its search launch, which wait for the search's progress reports (every
+    # `publish` token sets); -1 leaves it to the record kernel after the
+    # search.  One workgroup reporting every set, a few, and more workgroups
+    # than items per report; sets beyond a small record table (fill) go to the
+    # large-set pass after the launch.  A 70-utterance batch (four length
+    # groups), a 12-utterance one (a single group) and a label-synchronous
+    # batch whose decoded frames are fewer than its frames: every result is
+    # the oracle's.
+    g = W.random_small_graph(990, 2500, mean_deg=3.0, eps_frac=0.25, num_labels=16)
+    gh = dec.load_graph(g)
+    rng = np.random.default_rng(991)
+    batches = [[int(x) for x in rng.integers(0, 90, size=70)], [int(x) for x in rng.integers(1, 140, size=12)]]
+    with dec.debug_opts(record_groups=groups, record_publish=publish, record_fill=fill):
+        for b, lens in enumerate(batches):
+            lls = [W.random_small_loglikes(1000 + 100 * b + u, T, 16) for u, T in enumerate(lens)]
+            res = dec.wfst_decode_batch(gh, [to_dev(torch_mod, x) for x in lls], beam=9.0, max_active=140,
+                                        lattice_beam=4.0, record_tokens=True)
+            for u, (x, r) in enumerate(zip(lls, res)):
+                ro = oracle_mod.decode(g, x, 9.0, 140, 4.0)
+                parity.assert_same(ro, r, lattice=True, tokens=True,
+                                   tag="batch %d utt %d (T=%d) groups %d publish %d" % (b, u, lens[u], groups,
+                                                                                        publish))
+        lls = [W.random_small_loglikes(1300 + u, 30 + 7 * u, 16, blank_boost=6.0) for u in range(20)]
+        res = dec.wfst_decode_batch(gh, [to_dev(torch_mod, x) for x in lls], beam=9.0, max_active=140,
+                                    lattice_beam=4.0, blank_threshold=0.9, blank_id=0, record_tokens=True)
+        for u, (x, r) in enumerate(zip(lls, res)):
+            ro = oracle_mod.decode(g, x, 9.0, 140, 4.0, 0.9, 0)
+            parity.assert_same(ro, r, lattice=True, tokens=True, tag="lsd utt %d groups %d" % (u, groups))
+        assert sum(r.num_decoded for r in res) < sum(x.shape[0] for x in lls)
+    gh.free()
+
+
 def test_lsd_small_ctc(dec, torch_mod, oracle_mod):
     g = W.random_small_graph(950, 5000, mean_deg=2.0, eps_frac=0.1, num_labels=30)
     n = g.num_states
