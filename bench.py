@@ -134,9 +134,12 @@ def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str):
         spans = [max(e for _, e in ks[i:i + GROUP_LAUNCHES]) - ks[i][0]
                  for i in range(0, len(ks) - GROUP_LAUNCHES + 1, GROUP_LAUNCHES)]
         if spans:
-            lines.append("# %s: %d concurrent launches per batch; span per batch (first start to last end), "
-                         "average over %d batches: %.1f us" % (KERNEL_NAME, GROUP_LAUNCHES, len(spans),
-                                                               sum(spans) / len(spans) / 1e3))
+            # the first batch is the untimed warm-up
+            timed = spans[1:] or spans
+            lines.append("# %s: %d concurrent launches per batch; span per batch (first start to last end): %s us; "
+                         "average over the %d batches after the warm-up: %.1f us"
+                         % (KERNEL_NAME, GROUP_LAUNCHES, " ".join("%.0f" % (x / 1e3) for x in spans), len(timed),
+                            sum(timed) / len(timed) / 1e3))
     open(TRACE, "w").write("\n".join(lines) + "\n")
     out = ["# HBM traffic of %s per batch (its %d concurrent launches summed), workload lvcsr-25m-batch64"
            % (KERNEL_NAME, GROUP_LAUNCHES),
@@ -254,7 +257,7 @@ def write_overlap_profile(trace_csv: str):
                         100.0 * mean[4] / max(mean[1] - mean[0], 1e-9), mean[5], mean[6]))
     names = {}
     for r in rows[starts[min(1, len(starts) - 1)][0]:] if starts else []:
-        k = re.findall(r"(\w+)\(", r[2])
+        k = re.findall(r"(\w+)(?:<[^>]*>)?\(", r[2])
         names.setdefault(k[0] if k else r[2], []).append((r[1] - r[0]) / 1e6)
     lines.append("%-28s %6s %12s" % ("kernel (batches 1..)", "calls", "mean_ms"))
     for k in sorted(names, key=lambda k: -sum(names[k])):

@@ -414,8 +414,10 @@ int wfst_decode_noalloc(const wfst_graph *g, const float *loglikes, int32_t T, i
  *   record_groups      record workgroups appended to the search launch of
  *                      the batch's last length group, which derive its
  *                      back-pointers and raw lattice records while it
- *                      searches; -1 leaves that group to the record kernel
- *                      after its search
+ *                      searches (by default only when the batch has more
+ *                      than one length group; a positive count applies to
+ *                      a single group too); -1 leaves that group to the
+ *                      record kernel after its search
  *   record_publish     token sets between the search's progress reports to
  *                      those workgroups
  *

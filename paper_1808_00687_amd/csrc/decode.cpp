@@ -859,7 +859,10 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         for (int u = u0; u < u1; u++) Tg = std::max(Tg, T[u]);
         pg.pub_k = p.stream_k;
         pg.rec_wg = 0;
-        const bool fused = rec_wg > 0 && g == ng - 1 && pg.U <= kRecMaxUtts;
+        // (by default only when the batch has several groups: alone, a
+        // group's record pass after its search is short and all parallel,
+        // and the progress reports would slow its search for nothing)
+        const bool fused = rec_wg > 0 && g == ng - 1 && pg.U <= kRecMaxUtts && (ng > 1 || dbg.record_groups > 0);
         if (fused) {
             pg.prog = p.prog + u0;
             pg.pub_k = rec_pub;

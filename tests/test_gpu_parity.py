@@ -446,9 +446,10 @@ def test_record_workgroups_beside_search(dec, torch_mod, oracle_mod, groups, pub
     # search.  One workgroup reporting every set, a few, and more workgroups
     # than items per report; sets beyond a small record table (fill) go to the
     # large-set pass after the launch.  A 70-utterance batch (four length
-    # groups), a 12-utterance one (a single group) and a label-synchronous
-    # batch whose decoded frames are fewer than its frames: every result is
-    # the oracle's.
+    # groups), a 12-utterance one (a single group: record workgroups only
+    # with an explicit count) and a 36-utterance label-synchronous batch
+    # whose decoded frames are fewer than its frames: every result is the
+    # oracle's.
     g = W.random_small_graph(990, 2500, mean_deg=3.0, eps_frac=0.25, num_labels=16)
     gh = dec.load_graph(g)
     rng = np.random.default_rng(991)
@@ -463,7 +464,7 @@ def test_record_workgroups_beside_search(dec, torch_mod, oracle_mod, groups, pub
                 parity.assert_same(ro, r, lattice=True, tokens=True,
                                    tag="batch %d utt %d (T=%d) groups %d publish %d" % (b, u, lens[u], groups,
                                                                                         publish))
-        lls = [W.random_small_loglikes(1300 + u, 30 + 7 * u, 16, blank_boost=6.0) for u in range(20)]
+        lls = [W.random_small_loglikes(1300 + u, 30 + 3 * u, 16, blank_boost=6.0) for u in range(36)]
         res = dec.wfst_decode_batch(gh, [to_dev(torch_mod, x) for x in lls], beam=9.0, max_active=140,
                                     lattice_beam=4.0, blank_threshold=0.9, blank_id=0, record_tokens=True)
         for u, (x, r) in enumerate(zip(lls, res)):
