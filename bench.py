@@ -30,9 +30,17 @@ METRIC = "decoded frames/sec (RTF) + arcs expanded/sec + % HBM peak, 25M-arc gra
 HBM_PEAK_GBS = 8000.0
 FRAME_SHIFT_S = 0.010
 PROFILES = os.path.join(ROOT, "profiles")
-COUNTERS = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_counters.txt")
-TRACE = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_trace.txt")
 SQ = os.path.join(PROFILES, "search_kernel_lvcsr-25m-batch64_sq.txt")
+# the workloads with kernel-trace and HBM-counter summaries in profiles/
+PROFILED = {"cfg4": "lvcsr-25m-batch64", "cfg4x256": "lvcsr-25m-batch256"}
+
+
+def profile_path(workload: str, kind: str) -> str:
+    return os.path.join(PROFILES, "search_kernel_%s_%s.txt" % (PROFILED[workload], kind))
+
+
+def wl_flag(workload: str) -> str:
+    return "" if workload == "cfg4" else " --workload " + workload
 CSRC = os.path.join(ROOT, "paper_1808_00687_amd", "csrc")
 KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("search_body.h", "search_kernel.hip", "search_record_kernel.hip",
                                                    "record_set.h", "device_util.h", "internal.h")]
@@ -42,13 +50,13 @@ KERNEL_NAME = "search_kernel"
 GROUP_LAUNCHES = 4
 CALIBRATION_MIB = 1024
 TRACE_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_search -o run -- "
-             "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline")
+             "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline{wl}")
 # The counter passes run with the record workgroups off (--record-groups -1):
 # the last length group's search launch then holds its search alone, and the
 # counters count the search's work only.
 PMC_CMD = ("timeout -s KILL 180 rocprofv3 --pmc {counter} --output-format csv -d gpurun_out/pmc_{tag} -o run -- "
            "python3 bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-profile --record-groups -1 "
-           "--copy-calibration-mib %d" % CALIBRATION_MIB)
+           "--copy-calibration-mib %d{wl}" % CALIBRATION_MIB)
 SQ_PASSES = (("a", "SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY SQ_INSTS_VALU "
                    "SQ_INSTS_LDS SQ_INSTS_SALU"),
              ("b", "SQ_INSTS_VMEM_RD SQ_INSTS_VMEM_WR SQ_INSTS_BRANCH SQ_WAIT_INST_LDS SQ_ACTIVE_INST_VALU "
@@ -59,12 +67,15 @@ OVERLAP = os.path.join(PROFILES, "lattice_stream_kernel_lvcsr-25m-batch64_overla
 OVERLAP_CMD = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_incr -o run -- "
                "python3 bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-profile --incremental-lattice")
 
-# name: (config, label-synchronous, frame stride); cfg6 is the HMM-topology
-# stand-in (a set of blank-like units), not one of the five listed configs
+# name: (config, label-synchronous, frame stride, utterances); cfg6 is the
+# HMM-topology stand-in (a set of blank-like units), not one of the five
+# listed configs; cfg4x256 is config 4's workload at the batch that fills
+# every CU with a search workgroup (the same 64 utterances first)
 WORKLOADS = {
-    "cfg1": (1, True, 1), "cfg2": (2, True, 1), "cfg3": (3, True, 1), "cfg4": (4, True, 1),
-    "cfg5": (5, True, 1), "cfg5fsd": (5, False, 1),
-    "cfg6": (6, True, 1), "cfg6fsd": (6, False, 1), "cfg6stride3": (6, True, 3),
+    "cfg1": (1, True, 1, None), "cfg2": (2, True, 1, None), "cfg3": (3, True, 1, None),
+    "cfg4": (4, True, 1, None), "cfg4x256": (4, True, 1, 256),
+    "cfg5": (5, True, 1, None), "cfg5fsd": (5, False, 1, None),
+    "cfg6": (6, True, 1, None), "cfg6fsd": (6, False, 1, None), "cfg6stride3": (6, True, 3, None),
 }
 
 
@@ -92,13 +103,13 @@ def kernel_sha() -> str:
     return h.hexdigest()
 
 
-def read_traffic():
+def read_traffic(workload: str):
     """HBM bytes of a batch's search launches from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel sources."""
-    if not os.path.exists(COUNTERS):
+    summary of the workload, if it was taken on the current kernel sources."""
+    if workload not in PROFILED or not os.path.exists(profile_path(workload, "counters")):
         return None
     kv = {}
-    for line in open(COUNTERS):
+    for line in open(profile_path(workload, "counters")):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
@@ -110,17 +121,20 @@ def read_traffic():
         return None
 
 
-def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str):
+def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str, workload: str = "cfg4"):
     """Summaries of the rocprofv3 runs for profiles/: the kernel-trace
     statistics and the HBM counters of the search kernel, each counter scaled
     by what it reads for the plain device copy of known size that bench.py
     runs first (--copy-calibration-mib)."""
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
-    lines = ["# rocprofv3 kernel-trace statistics, workload lvcsr-25m-batch64 (64 utterances, 25M-arc graph)",
-             "# command: " + TRACE_CMD,
+    wl = wl_flag(workload)
+    n_utt = WORKLOADS[workload][3] or 64
+    lines = ["# rocprofv3 kernel-trace statistics, workload %s (%d utterances, 25M-arc graph)"
+             % (PROFILED[workload], n_utt),
+             "# command: " + TRACE_CMD.format(wl=wl),
              "# summary written by: python3 bench.py --write-profiles gpurun_out/prof_search/run_kernel_stats.csv "
-             "gpurun_out/pmc_fetch/run_counter_collection.csv gpurun_out/pmc_write/run_counter_collection.csv",
+             "gpurun_out/pmc_fetch/run_counter_collection.csv gpurun_out/pmc_write/run_counter_collection.csv" + wl,
              "%-62s %6s %14s %14s %7s" % ("kernel", "calls", "total_ms", "average_us", "pct")]
     for r in rows:
         lines.append("%-62s %6s %14.3f %14.1f %7s" % (r["Name"][:62], r["Calls"], float(r["TotalDurationNs"]) / 1e6,
@@ -140,11 +154,11 @@ def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str):
                          "average over the %d batches after the warm-up: %.1f us"
                          % (KERNEL_NAME, GROUP_LAUNCHES, " ".join("%.0f" % (x / 1e3) for x in spans), len(timed),
                             sum(timed) / len(timed) / 1e3))
-    open(TRACE, "w").write("\n".join(lines) + "\n")
-    out = ["# HBM traffic of %s per batch (its %d concurrent launches summed), workload lvcsr-25m-batch64"
-           % (KERNEL_NAME, GROUP_LAUNCHES),
-           "# fetch command: " + PMC_CMD.format(counter="FETCH_SIZE", tag="fetch"),
-           "# write command: " + PMC_CMD.format(counter="WRITE_SIZE", tag="write"),
+    open(profile_path(workload, "trace"), "w").write("\n".join(lines) + "\n")
+    out = ["# HBM traffic of %s per batch (its %d concurrent launches summed), workload %s"
+           % (KERNEL_NAME, GROUP_LAUNCHES, PROFILED[workload]),
+           "# fetch command: " + PMC_CMD.format(counter="FETCH_SIZE", tag="fetch", wl=wl),
+           "# write command: " + PMC_CMD.format(counter="WRITE_SIZE", tag="write", wl=wl),
            "# counters are KiB per dispatch; each is scaled by bytes/reading of a %d MiB device copy" % CALIBRATION_MIB,
            "# taken with the record workgroups off (--record-groups -1): the search's own traffic"]
     total = 0.0
@@ -163,9 +177,9 @@ def write_profiles(stats_csv: str, fetch_csv: str, write_csv: str):
                 "%s_kib_per_batch: %.1f" % (tag, kib),
                 "%s_bytes_per_batch: %.0f" % (tag, byts)]
     out += ["hbm_bytes_per_batch: %.0f" % total, "kernel_source_sha256: %s" % kernel_sha()]
-    open(COUNTERS, "w").write("\n".join(out) + "\n")
-    print(TRACE)
-    print(COUNTERS)
+    open(profile_path(workload, "counters"), "w").write("\n".join(out) + "\n")
+    print(profile_path(workload, "trace"))
+    print(profile_path(workload, "counters"))
 
 
 def write_sq_profile(csv_a: str, csv_b: str):
@@ -384,7 +398,7 @@ def main():
         write_overlap_profile(args.write_overlap_profile)
         return
     if args.write_profiles:
-        write_profiles(*args.write_profiles)
+        write_profiles(*args.write_profiles, workload=args.workload)
         return
     if args.write_sq_profile:
         write_sq_profile(*args.write_sq_profile)
@@ -404,9 +418,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU", file=sys.stderr)
         sys.exit(1)
-    cfg, lsd, stride = WORKLOADS[args.workload]
+    cfg, lsd, stride, n_utt = WORKLOADS[args.workload]
     t = time.time()
-    wl = workloads.workload(cfg, lsd=lsd, frame_stride=stride)
+    wl = workloads.workload(cfg, n_utt=n_utt, lsd=lsd, frame_stride=stride)
     log("workload %s generated in %.1fs (%d states, %d arcs, %d utterances)" % (
         wl.name, time.time() - t, wl.graph.num_states, wl.graph.num_arcs, len(wl.loglikes)))
     if args.copy_calibration_mib:
@@ -501,7 +515,7 @@ def main():
         alg = search_bytes(stats)
         dur_s = s0["search_span_ms"] / 1e3
         achieved = alg / dur_s / 1e9 if dur_s > 0 else None
-        traffic = read_traffic()
+        traffic = read_traffic(args.workload)
         copy_gbs = copy_bandwidth(torch)
         out["roofline"] = {
             "kernel": "search_kernel",

@@ -309,8 +309,9 @@ def workload(cfg: int, n_utt: Optional[int] = None, lsd: bool = True, frame_stri
         return Workload(3, "lvcsr-25m", g, 6000, ll,
                         DecodeOpts(beam=15.0, max_active=10000, lattice_beam=8.0))
     if cfg == 4:
-        lens = batch_lengths()
         n = 64 if n_utt is None else n_utt
+        # (a longer draw starts with the same 64 lengths)
+        lens = batch_lengths(max(64, n))
         ll = [loglikes_gauss(4, u, int(lens[u]), 6000, 3.0) for u in range(n)]
         return Workload(4, "lvcsr-25m-batch%d" % n, g, 6000, ll,
                         DecodeOpts(beam=15.0, max_active=10000, lattice_beam=8.0))
