@@ -278,6 +278,79 @@ struct ArenaLease {
     }
 };
 
+// Page-locked host memory for the transfers of one call (utterance states
+// and layouts in, states, kept frames, paths and set offsets out): one
+// buffer per device, kept between calls and only ever grown, so that each
+// transfer is a single DMA into memory the runtime need not pin on the fly
+// and steady-state decoding allocates nothing.  A call that finds it in use
+// by a concurrent call takes a private one; if pinning fails, pageable
+// memory serves (slower transfers, same results).
+struct PinnedCache {
+    std::mutex mu;
+    bool busy = false;
+    void *ptr = nullptr;
+    size_t cap = 0;
+};
+
+PinnedCache &pinned_cache(int dev)
+{
+    static PinnedCache *c = new PinnedCache[64];
+    return c[dev];
+}
+
+struct PinnedLease {
+    int dev = -1;
+    char *ptr = nullptr;
+    bool cached = false;
+    bool pinned = false;
+    std::vector<char> fallback;
+    PinnedLease() = default;
+    PinnedLease(const PinnedLease &) = delete;
+    PinnedLease &operator=(const PinnedLease &) = delete;
+    void acquire(int device, size_t need)
+    {
+        dev = device;
+        if (dev >= 0 && dev < 64) {
+            PinnedCache &c = pinned_cache(dev);
+            std::lock_guard<std::mutex> lk(c.mu);
+            if (!c.busy) {
+                if (c.cap < need) {
+                    if (c.ptr) (void)hipHostFree(c.ptr);
+                    c.ptr = nullptr;
+                    c.cap = 0;
+                    const size_t want = need + need / 4;
+                    if (hipHostMalloc(&c.ptr, want, hipHostMallocDefault) == hipSuccess) c.cap = want;
+                    else c.ptr = nullptr;
+                }
+                if (c.ptr) {
+                    c.busy = true;
+                    cached = pinned = true;
+                    ptr = static_cast<char *>(c.ptr);
+                    return;
+                }
+            }
+        }
+        void *q = nullptr;
+        if (hipHostMalloc(&q, need, hipHostMallocDefault) == hipSuccess) {
+            pinned = true;
+            ptr = static_cast<char *>(q);
+            return;
+        }
+        fallback.resize(need);
+        ptr = fallback.data();
+    }
+    ~PinnedLease()
+    {
+        if (cached) {
+            PinnedCache &c = pinned_cache(dev);
+            std::lock_guard<std::mutex> lk(c.mu);
+            c.busy = false;
+        } else if (pinned) {
+            (void)hipHostFree(ptr);
+        }
+    }
+};
+
 // Test and debugging switches (wfst_set_debug_opts), process-wide.
 struct DebugState {
     std::mutex mu;
@@ -783,13 +856,36 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     auto chk = [&](hipError_t r) {
         if (e == hipSuccess && r != hipSuccess) e = r;
     };
-    chk(hipMemcpyAsync(p.st, st.data(), U * sizeof(UttState), hipMemcpyHostToDevice, s));
-    chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
+    // host staging of the call's transfers: states, layouts and blank ids
+    // in; states, kept frames, packed paths and (with token sets) the set
+    // offsets out
+    const bool want_tokens = (o.flags & WFST_RECORD_TOKENS) != 0;
+    const bool all_frames = !(thr < std::numeric_limits<float>::infinity()) && p.frame_stride == 1;
+    auto rnd = [](size_t b) { return (b + 255) & ~static_cast<size_t>(255); };
+    const size_t g_lay = rnd(U * sizeof(UttState));
+    const size_t g_blank = g_lay + rnd(U * sizeof(UttLayout));
+    const size_t g_kept = g_blank + rnd(blank_h.size() * sizeof(int32_t));
+    const size_t g_path = g_kept + (all_frames ? 0 : rnd(static_cast<size_t>(kp) * sizeof(int32_t)));
+    const size_t g_fo = g_path + rnd(static_cast<size_t>(std::max<int64_t>(tot.pa, 1)) * sizeof(int2));
+    const size_t g_end = g_fo + (want_tokens ? rnd(static_cast<size_t>(fo) * sizeof(int64_t)) : 0);
+    PinnedLease stage;
+    stage.acquire(G.device, g_end);
+    UttState *h_st = reinterpret_cast<UttState *>(stage.ptr);
+    UttLayout *h_lay = reinterpret_cast<UttLayout *>(stage.ptr + g_lay);
+    int32_t *h_blank = reinterpret_cast<int32_t *>(stage.ptr + g_blank);
+    const int32_t *kept_h = reinterpret_cast<const int32_t *>(stage.ptr + g_kept);
+    const int2 *paths_h = reinterpret_cast<const int2 *>(stage.ptr + g_path);
+    const int64_t *fo_h = reinterpret_cast<const int64_t *>(stage.ptr + g_fo);
+    std::memcpy(h_st, st.data(), U * sizeof(UttState));
+    std::memcpy(h_lay, lay.data(), U * sizeof(UttLayout));
+    std::memcpy(h_blank, blank_h.data(), blank_h.size() * sizeof(int32_t));
+    chk(hipMemcpyAsync(p.st, h_st, U * sizeof(UttState), hipMemcpyHostToDevice, s));
+    chk(hipMemcpyAsync(d_lay, h_lay, U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
     chk(launch_zero(fo_all, kOffsetArrays * fo * sizeof(int64_t), s));
     // the progress counts start at 0: a stale count from an earlier decode
     // would let the lattice pass read token sets before they exist
     if (p.prog) chk(launch_zero(p.prog, (U + 1) * sizeof(int32_t), s));
-    chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), blank_h.data(), blank_h.size() * sizeof(int32_t),
+    chk(hipMemcpyAsync(const_cast<int32_t *>(p.blank_ids), h_blank, blank_h.size() * sizeof(int32_t),
                        hipMemcpyHostToDevice, s));
     chk(launch_classify(p, s));
     // decoded frames are at most the frames: size the per-frame launches by T
@@ -913,13 +1009,14 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     chk(launch_pack_paths(p, s));
     tm.stop(PH_FINAL, s);
     wt.mark("enqueue frames");
-    chk(hipMemcpyAsync(st.data(), p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
+    chk(hipMemcpyAsync(h_st, p.st, U * sizeof(UttState), hipMemcpyDeviceToHost, s));
     chk(hipStreamSynchronize(s));
     // the groups' streams are done once s is (after an error too, before the
     // workspace is given back)
     for (int g = 1; g < ng; g++) chk(hipStreamSynchronize(gs[g]));
     for (int g = 0; streaming && g < ng; g++) chk(hipStreamSynchronize(ls[g]));
     for (hipEvent_t x : evs) event_pool().put(G.device, x);
+    std::memcpy(st.data(), h_st, U * sizeof(UttState));
     wt.mark("wait search");
     if (wt.on) {
         int64_t gf = 0;
@@ -951,7 +1048,9 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
                                        dbg.fail_lattice_alloc != 0, lat_buf);
         if (le != hipSuccess) return hip_fail(le, "decode: lattice output allocation");
         p.lat_out = static_cast<int4 *>(lat_buf->p);
-        chk(hipMemcpyAsync(d_lay, lay.data(), U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
+        // (the stream has drained: the staged layouts were consumed)
+        std::memcpy(h_lay, lay.data(), U * sizeof(UttLayout));
+        chk(hipMemcpyAsync(d_lay, h_lay, U * sizeof(UttLayout), hipMemcpyHostToDevice, s));
         tm.start(s);
         chk(launch_lattice_emit(p, Tmax, s));
         tm.stop(PH_FINAL, s);
@@ -969,12 +1068,10 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     // gather results
     // the set offsets serve only the token sets; the kept frames are every
     // frame when no frame can be skipped
-    const bool want_tokens = (o.flags & WFST_RECORD_TOKENS) != 0;
-    const bool all_frames = !(thr < std::numeric_limits<float>::infinity()) && p.frame_stride == 1;
-    std::vector<int64_t> fo_h(want_tokens ? static_cast<size_t>(fo) : 0);
-    std::vector<int32_t> kept_h(all_frames ? 0 : static_cast<size_t>(kp));
-    if (want_tokens) chk(hipMemcpyAsync(fo_h.data(), p.sv_off, fo * sizeof(int64_t), hipMemcpyDeviceToHost, s));
-    if (!all_frames) chk(hipMemcpyAsync(kept_h.data(), p.kept, kp * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    if (want_tokens)
+        chk(hipMemcpyAsync(const_cast<int64_t *>(fo_h), p.sv_off, fo * sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    if (!all_frames)
+        chk(hipMemcpyAsync(const_cast<int32_t *>(kept_h), p.kept, kp * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     // the packed best paths, in utterance order
     int64_t path_total = 0;
     std::vector<int64_t> path_off(static_cast<size_t>(U), 0);
@@ -982,9 +1079,10 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         path_off[u] = path_total;
         if (st[u].status == WFST_OK) path_total += st[u].path_len;
     }
-    std::vector<int2> paths_h(static_cast<size_t>(std::max<int64_t>(path_total, 1)));
+    if (path_total > std::max<int64_t>(tot.pa, 1)) return fail(WFST_EDEVICE, "decode: internal error, path overflow");
     if (path_total)
-        chk(hipMemcpyAsync(paths_h.data(), p.path_packed, path_total * sizeof(int2), hipMemcpyDeviceToHost, s));
+        chk(hipMemcpyAsync(const_cast<int2 *>(paths_h), p.path_packed, path_total * sizeof(int2),
+                           hipMemcpyDeviceToHost, s));
     for (int u = 0; u < U; u++) {
         wfst_result *r = out[u];
         const UttState &x = st[u];
@@ -1062,7 +1160,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
             r->kept.resize(static_cast<size_t>(std::max(st[u].Tp, 0)));
             std::iota(r->kept.begin(), r->kept.end(), 0);
         } else {
-            r->kept.assign(kept_h.begin() + lay[u].kept0, kept_h.begin() + lay[u].kept0 + st[u].Tp);
+            r->kept.assign(kept_h + lay[u].kept0, kept_h + lay[u].kept0 + st[u].Tp);
         }
         r->stats.decode_ms = wall;
         r->stats.search_ms = ph[PH_SEARCH];
@@ -1084,7 +1182,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
             // token sets sorted by state for the caller
             const int Tp = st[u].Tp;
             r->has_tokens = true;
-            r->tok_off.assign(fo_h.begin() + lay[u].fo0, fo_h.begin() + lay[u].fo0 + Tp + 2);
+            r->tok_off.assign(fo_h + lay[u].fo0, fo_h + lay[u].fo0 + Tp + 2);
             const int64_t ntok = r->tok_off.back();
             r->tok_state.resize(static_cast<size_t>(ntok));
             r->tok_cost.resize(static_cast<size_t>(ntok));
