@@ -351,6 +351,46 @@ struct PinnedLease {
     }
 };
 
+// Launches whose workgroups wait on other workgroups (the record
+// workgroups beside a search, the incremental lattice pass) need the waited-on
+// workgroups to find CUs: one call per device at a time uses them, and only
+// when the batch's search workgroups and the waiting ones fit the device's
+// CUs together.  A call that cannot take the device's flag decodes without
+// them (the same results).
+std::atomic<bool> &wait_flag(int dev)
+{
+    static std::atomic<bool> *f = new std::atomic<bool>[64]();
+    return f[dev];
+}
+
+int device_cus(int dev)
+{
+    static std::atomic<int> *n = new std::atomic<int>[64]();
+    int v = n[dev].load();
+    if (v == 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) v = -1;
+        n[dev].store(v);
+    }
+    return v;
+}
+
+struct WaitGuard {
+    int dev = -1;
+    bool held = false;
+    bool take(int device)
+    {
+        if (device < 0 || device >= 64) return false;
+        bool expect = false;
+        held = wait_flag(device).compare_exchange_strong(expect, true);
+        if (held) dev = device;
+        return held;
+    }
+    ~WaitGuard()
+    {
+        if (held) wait_flag(dev).store(false);
+    }
+};
+
 // Test and debugging switches (wfst_set_debug_opts), process-wide.
 struct DebugState {
     std::mutex mu;
@@ -807,8 +847,16 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     Totals tot;
     // with the incremental lattice pass the lattice regions only take the
     // arcs that pass its pruning, a small part of the raw lattice
-    const bool incremental = lattice && (o.flags & WFST_INCREMENTAL_LATTICE) && U <= kStreamMaxUtts &&
-                             dbg.lattice_chunk >= 0;
+    // launches that wait on others (see WaitGuard)
+    const bool want_inc = lattice && (o.flags & WFST_INCREMENTAL_LATTICE) && U <= kStreamMaxUtts &&
+                          dbg.lattice_chunk >= 0;
+    const int rec_want = dbg.record_groups < 0 ? 0 : (dbg.record_groups > 0 ? dbg.record_groups : kRecGroups);
+    const int ng_est = std::max(1, std::min(1 + kGroupStreams, U / 16));
+    const bool want_rec = !want_inc && rec_want > 0 && (ng_est > 1 || dbg.record_groups > 0) &&
+                          U + rec_want <= device_cus(G.device);
+    WaitGuard wguard;
+    const bool waits = (want_inc || want_rec) && wguard.take(G.device);
+    const bool incremental = want_inc && waits;
     for (int u = 0; u < U; u++) layout_utt(T[u], z, lattice, depth, tot, lay[u], incremental ? kCompactDiv : 1);
     const int64_t fo = tot.fo, kp = tot.kp;
 
@@ -817,10 +865,10 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
     if (o.num_blank_ids > 0) blank_h.assign(o.blank_ids, o.blank_ids + o.num_blank_ids);
     else blank_h.push_back(o.blank_id);
     Params p{};
-    set_params(p, G, U, L, o, thr, dbg, z, static_cast<int32_t>(blank_h.size()), U <= kStreamMaxUtts);
+    set_params(p, G, U, L, o, thr, dbg, z, static_cast<int32_t>(blank_h.size()), incremental);
     // record workgroups beside the last length group's search (the
     // incremental pass records beside the search itself)
-    const int rec_wg = p.stream_k || dbg.record_groups < 0 ? 0 : (dbg.record_groups > 0 ? dbg.record_groups : kRecGroups);
+    const int rec_wg = want_rec && waits ? rec_want : 0;
     const int rec_pub = dbg.record_publish > 0 ? dbg.record_publish : kRecPublish;
     p.rec_wg = rec_wg;
     WallTrace wt;

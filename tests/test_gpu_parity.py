@@ -474,6 +474,42 @@ def test_record_workgroups_beside_search(dec, torch_mod, oracle_mod, groups, pub
     gh.free()
 
 
+def test_concurrent_decodes_match(dec, torch_mod, oracle_mod):
+    # Three host threads decode the same batch at once: the calls that find
+    # the device's workspace, staging buffer or waiting-launch flag taken use
+    # their own or decode without record workgroups, and every result is the
+    # sequential decode's, bit for bit (and the oracle's for a sample).
+    from concurrent.futures import ThreadPoolExecutor
+    g = W.random_small_graph(1400, 2500, mean_deg=3.0, eps_frac=0.25, num_labels=16)
+    gh = dec.load_graph(g)
+    lens = [20 + (7 * u) % 60 for u in range(40)]
+    lls = [W.random_small_loglikes(1410 + u, T, 16) for u, T in enumerate(lens)]
+    xs = [to_dev(torch_mod, x) for x in lls]
+
+    def run(_):
+        return dec.wfst_decode_batch(gh, xs, beam=9.0, max_active=140, lattice_beam=4.0, record_tokens=True)
+
+    ref = run(None)
+    for u in (0, 17, 39):
+        parity.assert_same(oracle_mod.decode(g, lls[u], 9.0, 140, 4.0), ref[u], lattice=True, tokens=True,
+                           tag="sequential utt %d" % u)
+    with ThreadPoolExecutor(max_workers=3) as ex:
+        outs = list(ex.map(run, range(6)))
+    for k, res in enumerate(outs):
+        for u, (a, b) in enumerate(zip(ref, res)):
+            tag = "call %d utt %d" % (k, u)
+            assert a.status == b.status and a.num_decoded == b.num_decoded, tag
+            assert np.float32(a.cost).view(np.uint32) == np.float32(b.cost).view(np.uint32), tag
+            np.testing.assert_array_equal(a.path_arcs, b.path_arcs, err_msg=tag)
+            for f in ("lat_frame", "lat_arc", "lat_cost", "lat_extra", "tok_state", "tok_cost", "tok_arc"):
+                x, y = getattr(a, f), getattr(b, f)
+                if x is not None and x.dtype == np.float32:
+                    x, y = x.view(np.uint32), y.view(np.uint32)
+                np.testing.assert_array_equal(x, y, err_msg=tag + " " + f)
+            assert a.stats["lattice_raw"] == b.stats["lattice_raw"], tag
+    gh.free()
+
+
 def test_lsd_small_ctc(dec, torch_mod, oracle_mod):
     g = W.random_small_graph(950, 5000, mean_deg=2.0, eps_frac=0.1, num_labels=30)
     n = g.num_states
