@@ -1079,6 +1079,8 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
             return fail(WFST_EDEVICE, "decode: internal error, a surviving token without a back-pointer");
         if (st[u].status == kStatusStreamTimeout)
             return fail(WFST_EDEVICE, "decode: internal error, a pass beside the search stopped waiting for it");
+        if (st[u].status == kStatusLatticeWait)
+            return fail(WFST_EDEVICE, "decode: internal error, the one-wave lattice pass stopped waiting");
     }
 
     std::shared_ptr<LatBuf> lat_buf;
@@ -1737,6 +1739,8 @@ int noalloc_impl(const wfst_graph *gh, const float *ll, int32_t T, int32_t L, co
     if (e != hipSuccess) return hip_fail(e, "wfst_decode_noalloc: search");
     if (st.status == kStatusNoBackPointer)
         return fail(WFST_EDEVICE, "wfst_decode_noalloc: internal error, a surviving token without a back-pointer");
+    if (st.status == kStatusLatticeWait)
+        return fail(WFST_EDEVICE, "wfst_decode_noalloc: internal error, the one-wave lattice pass stopped waiting");
     if (st.status == WFST_ECAPACITY) {
         set_error("wfst_decode_noalloc: the decode overflowed the fixed workspace");
         return WFST_ECAPACITY;

@@ -259,7 +259,7 @@ __device__ __forceinline__ void lat_fetch(const Params &p, const UttLayout &ly, 
 // larger than kLatLds is processed in device memory instead.  Kept arcs are
 // counted per set into lo_off (zeroed by the host), then turned into output
 // offsets.
-__device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh)
+__device__ void lattice_sets(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh)
 {
     UttState &st = p.st[u];
     const UttLayout ly = p.lay[u];
@@ -486,6 +486,235 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
         mn = j > 1 ? lat_meta_take(mv2) : LatMeta{};
     }
     lat_flush(p, ly, pd, kcnt);
+}
+
+// ---------------------------------------------------------------------------
+// The backward pass of an utterance whose token sets all hold at most
+// kSmallSet survivors, emitting records and epsilon records (the CTC-style
+// configurations).  The block pass spends a set's time mostly on a dozen
+// waves' bookkeeping and barriers, whatever the set's size.  Here one wave
+// (wave 0) computes the nodes' extra costs set after set from LDS alone,
+// while the block's other waves load the coming sets into a ring of LDS
+// slots; each slot is handed over with a workgroup-scope flag, filled after
+// the previous set in it has been consumed.  Then the whole block derives
+// every record's extra cost from its destination's, and the kept counts, set
+// by set in parallel.  The arithmetic is the block pass's, step for step, so
+// the extra costs, the kept arcs and their order are the same bit for bit.
+// Every wait is bounded: a pass that stops hearing from the other side
+// reports an error instead of hanging.
+// ---------------------------------------------------------------------------
+constexpr int kSmallSet = 64;                 // survivors and records per set (one per lane)
+constexpr int kRing = 16;                     // sets in flight between the loading waves and wave 0
+constexpr long long kSmallSpin = 1LL << 24;   // polls of one flag before the pass gives up
+
+struct SmallSlot {
+    int b0;                   // the set's first survivor (utterance-relative)
+    int nB, ne, nx;           // survivors, emitting records (into the next set), epsilon records
+    uint32_t key[kSmallSet];  // survivors' cost keys
+    int es[kSmallSet];        // emitting records: source survivor (this set),
+    int ed[kSmallSet];        // destination survivor (the next set)
+    uint32_t ep[kSmallSet];   // and candidate cost bits
+    int xs[kSmallSet];        // epsilon records (both ends in this set)
+    int xd[kSmallSet];
+    uint32_t xp[kSmallSet];
+};
+static_assert(kRing * sizeof(SmallSlot) <= 2 * kLatLds * sizeof(float), "the ring fits the cost half of the LDS");
+
+// Wait until *f >= v (every lane reads the same LDS word); false if the pass
+// has failed or the wait gave up (then it marks the pass failed).
+__device__ __forceinline__ bool small_wait(int *f, int v, int *fail)
+{
+    for (long long i = 0;; i++) {
+        if (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= v) break;
+        if (__hip_atomic_load(fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= kSmallSpin) {
+            __hip_atomic_store(fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            return false;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    return true;
+}
+
+// Returns false (having done nothing) when some set is too large; then the
+// block pass runs.  Called by the whole block.
+__device__ bool lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh)
+{
+    UttState &st = p.st[u];
+    const UttLayout ly = p.lay[u];
+    const int tid = threadIdx.x;
+    const int lane = lane_id();
+    const int wid = tid / kWave;
+    const int nw = blockDim.x / kWave;
+    const int Tp = st.Tp;
+    const int64_t *so = p.sv_off + ly.fo0;
+    // ---- every set small enough? ----
+    if (tid == 0) sh[21] = p.lat_lds >= kSmallSet && nw > 1 ? 1 : 0;
+    __syncthreads();
+    for (int j = tid; j <= Tp; j += blockDim.x) {
+        const int64_t nB = so[j + 1] - so[j];
+        const int64_t ne = j < Tp ? p.le_cnt[ly.fo0 + j] : 0;
+        const int64_t nx = p.lx_cnt[ly.fo0 + j];
+        if (nB > kSmallSet || ne > kSmallSet || nx > kSmallSet) sh[21] = 0;
+    }
+    __syncthreads();
+    if (!sh[21]) return false;
+
+    const float lb = p.lattice_beam;
+    const float B = st.final_cost;
+    const bool use_final = p.g.final_w != nullptr && st.reached_final;
+    uint32_t *eg = p.e_key + ly.sv0;
+    const uint32_t *tok = p.sv_key + ly.sv0;
+    unsigned long long *kcnt = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
+    const uint32_t kinf = okey(__int_as_float(0x7F800000));
+    // LDS: extra-cost keys and costs of two sets, the flags, the ring
+    uint32_t *se = s_e;
+    float *sc = reinterpret_cast<float *>(s_e + 2 * kSmallSet);
+    int *filled = reinterpret_cast<int *>(s_e + 4 * kSmallSet);   // per slot: 1 + the last set placed
+    int *done = filled + kRing;                                     // sets wave 0 has finished
+    int *fail = done + 1;
+    SmallSlot *ring = reinterpret_cast<SmallSlot *>(s_c);
+    if (tid < kRing) filled[tid] = 0;
+    if (tid == 0) {
+        *done = 0;
+        *fail = 0;
+    }
+    __syncthreads();
+
+    if (wid > 0) {
+        // ---- the loading waves: set n (the n-th from the last) into slot n mod kRing ----
+        for (int n = wid - 1; n <= Tp; n += nw - 1) {
+            const int slot = n % kRing;
+            if (n >= kRing && !small_wait(done, n - kRing + 1, fail)) break;
+            const int j = Tp - n;
+            const int b0 = static_cast<int>(so[j]);
+            const int nB = static_cast<int>(so[j + 1] - so[j]);
+            const int ne = j < Tp ? static_cast<int>(p.le_cnt[ly.fo0 + j]) : 0;
+            const int nx = static_cast<int>(p.lx_cnt[ly.fo0 + j]);
+            uint32_t key = 0;
+            int4 e = make_int4(0, 0, 0, 0), x = make_int4(0, 0, 0, 0);
+            if (lane < nB) key = tok[b0 + lane];
+            if (lane < ne) e = p.lat_e[ly.le0 + p.le_off[ly.fo0 + j] + lane];
+            if (lane < nx) x = p.lat_x[ly.lx0 + p.lx_off[ly.fo0 + j] + lane];
+            SmallSlot &sl = ring[slot];
+            sl.key[lane] = key;
+            sl.es[lane] = e.x;
+            sl.ed[lane] = e.y;
+            sl.ep[lane] = static_cast<uint32_t>(e.w);
+            sl.xs[lane] = x.x;
+            sl.xd[lane] = x.y;
+            sl.xp[lane] = static_cast<uint32_t>(x.w);
+            if (lane == 0) {
+                sl.b0 = b0;
+                sl.nB = nB;
+                sl.ne = ne;
+                sl.nx = nx;
+            }
+            // the slot's contents before its flag
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            if (lane == 0) __hip_atomic_store(filled + slot, n + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+    } else {
+        // ---- wave 0: the sets from last to first (the block pass's steps) ----
+        int hA = 0, a0 = 0;   // the half holding S_j+1, and its first survivor
+        for (int n = 0; n <= Tp; n++) {
+            const int j = Tp - n;
+            const SmallSlot &sl = ring[n % kRing];
+            if (!small_wait(filled + n % kRing, n + 1, fail)) break;
+            const int b0 = sl.b0, nB = sl.nB, ne = sl.ne, nx = sl.nx;
+            const int hB = hA ^ 1;
+            uint32_t *eA = se + hA * kSmallSet, *eB = se + hB * kSmallSet;
+            float *cA = sc + hA * kSmallSet, *cB = sc + hB * kSmallSet;
+            if (lane < nB) {
+                const float c = okey_val(sl.key[lane]);
+                cB[lane] = c;
+                uint32_t e0 = kinf;
+                if (j == Tp) {
+                    const float f = use_final ? p.g.final_w[p.sv_state[ly.sv0 + b0 + lane]] : 0.0f;
+                    e0 = okey((c + f) - B);
+                }
+                eB[lane] = e0;
+            }
+            wave_lds_handover();
+            // emitting arcs into S_j+1
+            if (lane < ne) {
+                const int d = sl.ed[lane] - a0;
+                const float d1 = __uint_as_float(sl.ep[lane]) - cA[d];
+                const float ex = d1 + okey_val(eA[d]);
+                atomicMin(eB + (sl.es[lane] - b0), okey(ex));
+            }
+            wave_lds_handover();
+            // epsilon arcs inside S_j, to their fixed point
+            while (nx > 0) {
+                bool changed = false;
+                if (lane < nx) {
+                    const int d = sl.xd[lane] - b0;
+                    const float d1 = __uint_as_float(sl.xp[lane]) - cB[d];
+                    const float ex = d1 + okey_val(eB[d]);
+                    const uint32_t k = okey(ex);
+                    if (k < eB[sl.xs[lane] - b0]) {
+                        atomicMin(eB + (sl.xs[lane] - b0), k);
+                        changed = true;
+                    }
+                }
+                wave_lds_handover();
+                if (!__ballot(changed)) break;
+            }
+            // S_j's extra costs, for the records below
+            if (lane < nB) eg[b0 + lane] = eB[lane];
+            // the slot has been read: it may take a later set
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            if (lane == 0) __hip_atomic_store(done, n + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            hA = hB;
+            a0 = b0;
+        }
+    }
+    // every node's extra cost is stored before any record reads it
+    block_sync_vm();
+    if (*fail) {
+        if (tid == 0) set_status(st, kStatusLatticeWait);
+        return true;
+    }
+    // ---- every record's extra cost and the kept arcs of each set ----
+    for (int n = wid; n <= Tp; n += nw) {
+        const int j = Tp - n;
+        const int ne = j < Tp ? static_cast<int>(p.le_cnt[ly.fo0 + j]) : 0;
+        const int nx = static_cast<int>(p.lx_cnt[ly.fo0 + j]);
+        int kept = 0;
+        if (lane < ne) {
+            const int64_t r = ly.le0 + p.le_off[ly.fo0 + j] + lane;
+            const int4 x = p.lat_e[r];
+            const float d1 = __int_as_float(x.w) - okey_val(tok[x.y]);
+            const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
+            p.ex_e[r] = ex;
+            kept += ex <= lb;
+        }
+        if (lane < nx) {
+            const int64_t r = ly.lx0 + p.lx_off[ly.fo0 + j] + lane;
+            const int4 x = p.lat_x[r];
+            const float d1 = __int_as_float(x.w) - okey_val(tok[x.y]);
+            const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
+            p.ex_x[r] = ex;
+            kept += ex <= lb;
+        }
+        const int k = __builtin_amdgcn_readlane(wave_incl_scan(kept), kWave - 1);
+        if (lane == 0) kcnt[j] = static_cast<unsigned long long>(k);
+    }
+    vm_wait();
+    return true;
+}
+
+// Lattice-beam pruning of utterance u by one block: the one-wave pass when
+// every set is small, else the block pass; then the kept counts become the
+// output offsets.
+__device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh)
+{
+    UttState &st = p.st[u];
+    const UttLayout ly = p.lay[u];
+    const int tid = threadIdx.x;
+    const int Tp = st.Tp;
+    unsigned long long *kcnt = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
+    if (!lattice_small(p, u, s_e, s_c, sh)) lattice_sets(p, u, s_e, s_c, sh);
     __syncthreads();
     // kept arcs per set -> output offsets (exclusive prefix over the sets)
     int64_t carry = 0;

@@ -41,6 +41,9 @@ constexpr int kStatusNoBackPointer = -9;
 // Utterance status: the incremental lattice pass or the record workgroups
 // stopped waiting for the search (never expected: reported as a device error)
 constexpr int kStatusStreamTimeout = -11;
+// Utterance status: the one-wave lattice pass and its loading waves stopped
+// waiting for each other (never expected: reported as a device error)
+constexpr int kStatusLatticeWait = -12;
 // utterances a search launch with record workgroups may hold (their LDS
 // keeps a progress count per utterance)
 constexpr int kRecMaxUtts = 256;
