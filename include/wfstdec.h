@@ -441,6 +441,11 @@ typedef struct wfst_debug_opts {
 
 int wfst_set_debug_opts(const wfst_debug_opts *opts);
 
+/* One environment switch, read once per process: WFSTDEC_DEBUG_TIMING (any
+ * value) prints a wall-clock breakdown of each decode call on stderr (setup,
+ * search, results; the workspace split and the frames redone on the
+ * device-memory token table).  It changes no result. */
+
 /* Message for the last error raised on the calling thread ("" if none). */
 const char *wfst_last_error(void);
 

@@ -490,9 +490,16 @@ struct Timer {
     }
 };
 
-// Wall-clock breakdown of one decode call on stderr (WFSTDEC_DEBUG_TIMING=1).
+// Wall-clock breakdown of each decode call on stderr when the environment
+// variable WFSTDEC_DEBUG_TIMING is set (read once per process).
+bool debug_timing()
+{
+    static const bool on = getenv("WFSTDEC_DEBUG_TIMING") != nullptr;
+    return on;
+}
+
 struct WallTrace {
-    bool on = getenv("WFSTDEC_DEBUG_TIMING") != nullptr;
+    bool on = debug_timing();
     double t = now();
     static double now()
     {
