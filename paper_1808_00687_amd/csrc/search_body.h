@@ -33,7 +33,14 @@
 // and writes nothing per candidate.
 // A frame that reaches more states than the LDS table holds is redone with
 // the same code on a table in device memory.  Every table is private to its
-// workgroup: no device-scope synchronisation and no per-frame launches.
+// workgroup and there are no per-frame launches; the only device-scope
+// synchronisation is the search's progress count, published every pub_k
+// token sets when record workgroups (below) or the incremental lattice pass
+// follow it.
+//
+// This header is compiled twice, once per translation unit:
+// search_kernel.hip instantiates the search alone, search_record_kernel.hip
+// the search with record workgroups appended to its launch.
 #pragma once
 
 #include <type_traits>
