@@ -420,10 +420,15 @@ int wfst_decode_noalloc(const wfst_graph *g, const float *loglikes, int32_t T, i
  *                      record kernel after its search
  *   record_publish     token sets between the search's progress reports to
  *                      those workgroups
+ *   lattice_pipe       lattice pruning's streamed pass (for utterances whose
+ *                      sets are too large for the one-wave pass): -1 never
+ *                      (the block pass instead), 0 where the utterance's
+ *                      sets hold few records on average, 1 wherever it fits
  *
  * opts == NULL restores every default.  Takes effect for decodes started
  * after the call returns.  Errors: WFST_EINVAL for a negative field other
- * than lattice_lds = -1, lattice_chunk = -1 and record_groups = -1.
+ * than lattice_lds = -1, lattice_chunk = -1, record_groups = -1 and
+ * lattice_pipe = -1.
  */
 typedef struct wfst_debug_opts {
     int32_t lds_fill;
@@ -437,6 +442,7 @@ typedef struct wfst_debug_opts {
     int32_t lattice_ring;
     int32_t record_groups;
     int32_t record_publish;
+    int32_t lattice_pipe;
 } wfst_debug_opts;
 
 int wfst_set_debug_opts(const wfst_debug_opts *opts);

@@ -608,6 +608,7 @@ void set_params(Params &p, const Graph &G, int U, int L, const wfst_decode_opts 
     p.rec_fill = limit_or(dbg.record_fill, 1 << 30);
     p.rec_big_fill = limit_or(dbg.record_big_fill, 1 << 30);
     p.lat_lds = dbg.lattice_lds < 0 ? 0 : limit_or(dbg.lattice_lds, 1 << 30);
+    p.lat_pipe = dbg.lattice_pipe < 0 ? -1 : (dbg.lattice_pipe > 0 ? 1 : 0);
     p.hash_mul = dbg.permute ? kHashMulAlt : kHashMul;
     p.reverse = dbg.permute ? 1 : 0;
     p.capG = 8192;
@@ -1573,7 +1574,7 @@ extern "C" int wfst_set_debug_opts(const wfst_debug_opts *opts)
         o = *opts;
         if (o.lds_fill < 0 || o.queue_cap < 0 || o.record_fill < 0 || o.record_big_fill < 0 ||
             o.lattice_lds < -1 || o.permute < 0 || o.fail_lattice_alloc < 0 || o.lattice_chunk < -1 ||
-            o.lattice_ring < 0 || o.record_groups < -1 || o.record_publish < 0)
+            o.lattice_ring < 0 || o.record_groups < -1 || o.record_publish < 0 || o.lattice_pipe < -1)
             return fail(WFST_EINVAL, "wfst_set_debug_opts: negative field");
     }
     DebugState &d = debug_state();

@@ -536,9 +536,48 @@ __device__ __forceinline__ bool small_wait(int *f, int v, int *fail)
     return true;
 }
 
-// Returns false (having done nothing) when some set is too large; then the
-// block pass runs.  Called by the whole block.
-__device__ bool lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh)
+// Every record's extra cost from its destination's (stored in e_key by the
+// pass that computed the nodes') and the kept arcs of each set, the sets in
+// parallel, one wave each: the block pass's arithmetic.
+__device__ void lattice_records(const Params &p, const UttLayout &ly, int Tp)
+{
+    const int lane = lane_id();
+    const int wid = threadIdx.x / kWave;
+    const int nw = blockDim.x / kWave;
+    const float lb = p.lattice_beam;
+    const uint32_t *eg = p.e_key + ly.sv0;
+    const uint32_t *tok = p.sv_key + ly.sv0;
+    unsigned long long *kcnt = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
+    for (int n = wid; n <= Tp; n += nw) {
+        const int j = Tp - n;
+        const int ne = j < Tp ? static_cast<int>(p.le_cnt[ly.fo0 + j]) : 0;
+        const int nx = static_cast<int>(p.lx_cnt[ly.fo0 + j]);
+        int kept = 0;
+        const int64_t e0 = ly.le0 + (j < Tp ? p.le_off[ly.fo0 + j] : 0);
+        for (int i = lane; i < ne; i += kWave) {
+            const int4 x = p.lat_e[e0 + i];
+            const float d1 = __int_as_float(x.w) - okey_val(tok[x.y]);
+            const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
+            p.ex_e[e0 + i] = ex;
+            kept += ex <= lb;
+        }
+        const int64_t x0 = ly.lx0 + p.lx_off[ly.fo0 + j];
+        for (int i = lane; i < nx; i += kWave) {
+            const int4 x = p.lat_x[x0 + i];
+            const float d1 = __int_as_float(x.w) - okey_val(tok[x.y]);
+            const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
+            p.ex_x[x0 + i] = ex;
+            kept += ex <= lb;
+        }
+        const int k = __builtin_amdgcn_readlane(wave_incl_scan(kept), kWave - 1);
+        if (lane == 0) kcnt[j] = static_cast<unsigned long long>(k);
+    }
+    vm_wait();
+}
+
+// Called by the whole block when every set holds at most kSmallSet
+// survivors, emitting records and epsilon records.
+__device__ void lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c)
 {
     UttState &st = p.st[u];
     const UttLayout ly = p.lay[u];
@@ -548,18 +587,6 @@ __device__ bool lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c,
     const int nw = blockDim.x / kWave;
     const int Tp = st.Tp;
     const int64_t *so = p.sv_off + ly.fo0;
-    // ---- every set small enough? ----
-    if (tid == 0) sh[21] = p.lat_lds >= kSmallSet && nw > 1 ? 1 : 0;
-    __syncthreads();
-    for (int j = tid; j <= Tp; j += blockDim.x) {
-        const int64_t nB = so[j + 1] - so[j];
-        const int64_t ne = j < Tp ? p.le_cnt[ly.fo0 + j] : 0;
-        const int64_t nx = p.lx_cnt[ly.fo0 + j];
-        if (nB > kSmallSet || ne > kSmallSet || nx > kSmallSet) sh[21] = 0;
-    }
-    __syncthreads();
-    if (!sh[21]) return false;
-
     const float lb = p.lattice_beam;
     const float B = st.final_cost;
     const bool use_final = p.g.final_w != nullptr && st.reached_final;
@@ -673,48 +700,460 @@ __device__ bool lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c,
     block_sync_vm();
     if (*fail) {
         if (tid == 0) set_status(st, kStatusLatticeWait);
-        return true;
+        return;
     }
-    // ---- every record's extra cost and the kept arcs of each set ----
-    for (int n = wid; n <= Tp; n += nw) {
-        const int j = Tp - n;
-        const int ne = j < Tp ? static_cast<int>(p.le_cnt[ly.fo0 + j]) : 0;
-        const int nx = static_cast<int>(p.lx_cnt[ly.fo0 + j]);
-        int kept = 0;
-        if (lane < ne) {
-            const int64_t r = ly.le0 + p.le_off[ly.fo0 + j] + lane;
-            const int4 x = p.lat_e[r];
-            const float d1 = __int_as_float(x.w) - okey_val(tok[x.y]);
-            const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
-            p.ex_e[r] = ex;
-            kept += ex <= lb;
+    lattice_records(p, ly, Tp);
+}
+
+// ---------------------------------------------------------------------------
+// The backward pass of an utterance with larger sets: at most kLatLds
+// survivors and ring-capacity epsilon records each.  The roles are the
+// one-wave pass's, with a stream in place of fixed slots.  A set's stream
+// holds, in this order, the initial extra-cost keys of its survivors (the
+// last set only), its emitting records and its epsilon records, each an
+// 8-byte entry: the source's and destination's offsets in their sets and the
+// record's first difference fl(p - c(d)), which the loading waves compute
+// from device memory.  Every set's place in the stream is the prefix of the
+// sizes before it, computed up front, so the loading waves (wave w takes the
+// sets w-1, w-1+11, ...) write side by side into a ring of LDS entries, 512
+// at a time, each piece once wave 0 has read what those ring positions held
+// before.  Wave 0 takes the sets in order and the pieces as they arrive; it
+// computes the nodes' extra costs as the block pass does and, on the way,
+// every record's extra cost (an epsilon record's from the round that changed
+// nothing) and the kept arcs of the set, so the records are read once.  The
+// arithmetic is the block pass's, step for step.  Every wait is bounded.
+//
+// Progress: wave 0 waits only for the loader of its current set, which has
+// finished its earlier sets (wave 0 has read them) and waits, if at all, for
+// ring positions at most a piece ahead of wave 0's, or, for the epsilon
+// records (read until the set is done), at most the ring's capacity ahead.
+// ---------------------------------------------------------------------------
+constexpr int kPipeCap = 8192;     // ring entries (8 bytes each): the cost half of the LDS
+constexpr int kPipePiece = 512;    // entries per hand-over (8 per lane)
+constexpr int kPipeSlots = 32;     // sets described ahead of wave 0
+constexpr int kPipeAvg = 640;      // stream entries per set up to which the pass beats the block pass
+static_assert(kPipeCap * sizeof(uint2) == 2 * kLatLds * sizeof(float), "the ring is the cost half of the LDS");
+static_assert(kLatLds <= 65536, "a survivor's offset in its set fits 16 bits");
+
+struct PipeMeta {
+    int64_t re, rx;       // the set's first emitting and first epsilon record
+    int b0, nB, ne, nx;   // first survivor (utterance-relative) and the counts
+    int start;            // the set's first stream position
+    int pad;
+};
+
+// The lattice block's LDS control words.
+struct LatCtl {
+    PipeMeta meta[kPipeSlots];
+    int filled[kPipeSlots];   // per slot: 1 + the last set described there
+    int prog[kPipeSlots];     // per slot: stream position up to which its set is written
+    int done;                 // sets wave 0 has finished
+    int consumed;             // stream position up to which wave 0 has read
+    int fail;
+    int mB, mE, mX;           // largest set, emitting and epsilon record counts
+    unsigned long long total; // stream entries of the utterance
+};
+
+// Wait until *f >= v; LDS-only ordering (the waiting wave's device-memory
+// stores are not waited for).  False if the pass has failed or the wait gave
+// up (then it marks the pass failed).
+__device__ __forceinline__ bool pipe_wait(const int *f, int v, int *fail)
+{
+    for (long long i = 0;; i++) {
+        if (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= v) break;
+        if (__hip_atomic_load(fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= kSmallSpin) {
+            __hip_atomic_store(fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            return false;
         }
-        if (lane < nx) {
-            const int64_t r = ly.lx0 + p.lx_off[ly.fo0 + j] + lane;
-            const int4 x = p.lat_x[r];
-            const float d1 = __int_as_float(x.w) - okey_val(tok[x.y]);
-            const float ex = d1 + okey_val(ld_relaxed(eg + x.y));
-            p.ex_x[r] = ex;
-            kept += ex <= lb;
-        }
-        const int k = __builtin_amdgcn_readlane(wave_incl_scan(kept), kWave - 1);
-        if (lane == 0) kcnt[j] = static_cast<unsigned long long>(k);
+        __builtin_amdgcn_s_sleep(1);
     }
-    vm_wait();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
     return true;
 }
 
-// Lattice-beam pruning of utterance u by one block: the one-wave pass when
-// every set is small, else the block pass; then the kept counts become the
-// output offsets.
-__device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh)
+// The wave's LDS accesses so far, then *f = v.
+__device__ __forceinline__ void pipe_publish(int *f, int v)
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    if (lane_id() == 0) __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// A loading wave: sets pw, pw + np, ... into the stream.
+__device__ void pipe_load(const Params &p, const UttLayout &ly, const UttState &st, LatCtl *ctl, uint2 *ring,
+                          int pw, int np)
+{
+    const int lane = lane_id();
+    const int Tp = st.Tp;
+    const float B = st.final_cost;
+    const bool use_final = p.g.final_w != nullptr && st.reached_final;
+    const int64_t *so = p.sv_off + ly.fo0;
+    const uint32_t *tok = p.sv_key + ly.sv0;
+    const unsigned long long *start_of = reinterpret_cast<const unsigned long long *>(p.lo_off + ly.fo0);
+    constexpr int kQ = kPipePiece / kWave;
+    for (int n = pw; n <= Tp; n += np) {
+        const int j = Tp - n;
+        const int slot = n % kPipeSlots;
+        const int b0 = static_cast<int>(so[j]);
+        const int b1 = static_cast<int>(so[j + 1]);
+        const int nB = b1 - b0;
+        const int ne = j < Tp ? static_cast<int>(p.le_cnt[ly.fo0 + j]) : 0;
+        const int nx = static_cast<int>(p.lx_cnt[ly.fo0 + j]);
+        const int64_t re = ly.le0 + (j < Tp ? p.le_off[ly.fo0 + j] : 0);
+        const int64_t rx = ly.lx0 + p.lx_off[ly.fo0 + j];
+        const int start = static_cast<int>(ld_relaxed(start_of + j));
+        if (n >= kPipeSlots && !pipe_wait(&ctl->done, n - kPipeSlots + 1, &ctl->fail)) return;
+        if (lane == 0) {
+            PipeMeta &m = ctl->meta[slot];
+            m.re = re;
+            m.rx = rx;
+            m.b0 = b0;
+            m.nB = nB;
+            m.ne = ne;
+            m.nx = nx;
+            m.start = start;
+            ctl->prog[slot] = start;
+        }
+        pipe_publish(ctl->filled + slot, n + 1);
+        int pos = start;
+        if (n == 0) {
+            // the last set: fl(fl(c + f) - B) of every survivor
+            for (int i0 = 0; i0 < nB; i0 += kPipePiece) {
+                uint32_t v[kQ];
+#pragma unroll
+                for (int q = 0; q < kQ; q++) {
+                    const int i = i0 + q * kWave + lane;
+                    v[q] = 0;
+                    if (i < nB) {
+                        const float c = okey_val(tok[b0 + i]);
+                        const float f = use_final ? p.g.final_w[p.sv_state[ly.sv0 + b0 + i]] : 0.0f;
+                        v[q] = okey((c + f) - B);
+                    }
+                }
+                const int end = start + min(i0 + kPipePiece, nB);
+                if (!pipe_wait(&ctl->consumed, end - kPipeCap, &ctl->fail)) return;
+#pragma unroll
+                for (int q = 0; q < kQ; q++) {
+                    const int i = i0 + q * kWave + lane;
+                    if (i < nB) ring[(start + i) & (kPipeCap - 1)] = make_uint2(v[q], 0u);
+                }
+                pipe_publish(ctl->prog + slot, end);
+            }
+            pos += nB;
+        }
+        // the records: emitting (destination in S_j+1), then epsilon
+        const int nr = ne + nx;
+        for (int i0 = 0; i0 < nr; i0 += kPipePiece) {
+            int4 x[kQ];
+#pragma unroll
+            for (int q = 0; q < kQ; q++) {
+                const int i = i0 + q * kWave + lane;
+                x[q] = make_int4(0, 0, 0, 0);
+                if (i < ne) x[q] = p.lat_e[re + i];
+                else if (i < nr) x[q] = p.lat_x[rx + (i - ne)];
+            }
+            uint2 v[kQ];
+#pragma unroll
+            for (int q = 0; q < kQ; q++) {
+                const int i = i0 + q * kWave + lane;
+                v[q] = make_uint2(0u, 0u);
+                if (i < nr) {
+                    const float d1 = __int_as_float(x[q].w) - okey_val(tok[x[q].y]);
+                    const int base = i < ne ? b1 : b0;
+                    v[q] = make_uint2(static_cast<uint32_t>(x[q].x - b0) << 16 | static_cast<uint32_t>(x[q].y - base),
+                                      __float_as_uint(d1));
+                }
+            }
+            const int end = pos + min(i0 + kPipePiece, nr);
+            if (!pipe_wait(&ctl->consumed, end - kPipeCap, &ctl->fail)) return;
+#pragma unroll
+            for (int q = 0; q < kQ; q++) {
+                const int i = i0 + q * kWave + lane;
+                if (i < nr) ring[(pos + i) & (kPipeCap - 1)] = v[q];
+            }
+            pipe_publish(ctl->prog + slot, end);
+        }
+    }
+}
+
+// Wave 0's wait for stream position `end` of the set in `slot`: `have` is
+// the position it last saw written.  Before it blocks it reports what it has
+// read (up to `cur`), which the loaders may be waiting for.
+__device__ __forceinline__ bool pipe_need(LatCtl *ctl, int slot, int end, int &have, int cur)
+{
+    if (have >= end) return true;
+    pipe_publish(&ctl->consumed, cur);
+    for (long long i = 0;; i++) {
+        const int v = __hip_atomic_load(ctl->prog + slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (v >= end) {
+            have = v;
+            break;
+        }
+        if (__hip_atomic_load(&ctl->fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= kSmallSpin) {
+            __hip_atomic_store(&ctl->fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            return false;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    return true;
+}
+
+// kQ entries per lane of a set's emitting records for wave 0: entries i0..
+// of the region starting at stream position r; kFull when all of them exist,
+// else the missing lanes repeat the region's last entry with a key that
+// lowers nothing.  The loads carry no condition, so they are issued together.
+template <bool kFull, int kQ>
+__device__ __forceinline__ void pipe_emit(const uint2 *ring, int r, int i0, int ne, const uint32_t *eA, uint32_t *eB,
+                                          float *exo, float lb, int &kept)
+{
+    const int lane = lane_id();
+    uint2 v[kQ];
+#pragma unroll
+    for (int q = 0; q < kQ; q++) {
+        const int i = i0 + q * kWave + lane;
+        v[q] = ring[(r + (kFull ? i : min(i, ne - 1))) & (kPipeCap - 1)];
+    }
+    float ex[kQ];
+#pragma unroll
+    for (int q = 0; q < kQ; q++) ex[q] = __uint_as_float(v[q].y) + okey_val(eA[v[q].x & 0xFFFFu]);
+#pragma unroll
+    for (int q = 0; q < kQ; q++) {
+        const int i = i0 + q * kWave + lane;
+        const bool ok = kFull || i < ne;
+        atomicMin(eB + (v[q].x >> 16), ok ? okey(ex[q]) : 0xFFFFFFFFu);
+        if (ok) exo[i] = ex[q];
+        kept += ok && ex[q] <= lb;
+    }
+}
+
+// The same for an epsilon round.
+template <bool kFull, int kQ>
+__device__ __forceinline__ void pipe_eps(const uint2 *ring, int r, int i0, int nx, uint32_t *eB, float *exo, float lb,
+                                         int &kx, bool &changed)
+{
+    const int lane = lane_id();
+    uint2 v[kQ];
+#pragma unroll
+    for (int q = 0; q < kQ; q++) {
+        const int i = i0 + q * kWave + lane;
+        v[q] = ring[(r + (kFull ? i : min(i, nx - 1))) & (kPipeCap - 1)];
+    }
+    uint32_t ed[kQ], es[kQ];
+#pragma unroll
+    for (int q = 0; q < kQ; q++) {
+        ed[q] = eB[v[q].x & 0xFFFFu];
+        es[q] = eB[v[q].x >> 16];
+    }
+#pragma unroll
+    for (int q = 0; q < kQ; q++) {
+        const int i = i0 + q * kWave + lane;
+        const bool ok = kFull || i < nx;
+        const float ex = __uint_as_float(v[q].y) + okey_val(ed[q]);
+        const uint32_t k = okey(ex);
+        if (ok && k < es[q]) {
+            atomicMin(eB + (v[q].x >> 16), k);
+            changed = true;
+        }
+        if (ok) exo[i] = ex;
+        kx += ok && ex <= lb;
+    }
+}
+
+__device__ __forceinline__ int64_t uniform64(int64_t v)
+{
+    const uint64_t u = static_cast<uint64_t>(v);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32));
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Wave 0: the sets from last to first.
+__device__ void pipe_chain(const Params &p, const UttLayout &ly, int Tp, LatCtl *ctl, const uint2 *ring,
+                           uint32_t *se)
+{
+    const int lane = lane_id();
+    const float lb = p.lattice_beam;
+    const uint32_t kinf = okey(__int_as_float(0x7F800000));
+    unsigned long long *kcnt = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
+    constexpr int kQ = kPipePiece / kWave;
+    int hA = 0;   // the half holding S_j+1
+    for (int n = 0; n <= Tp; n++) {
+        const int j = Tp - n;
+        const int slot = n % kPipeSlots;
+        if (!pipe_wait(ctl->filled + slot, n + 1, &ctl->fail)) return;
+        const PipeMeta &mm = ctl->meta[slot];
+        const int nB = __builtin_amdgcn_readfirstlane(mm.nB);
+        const int ne = __builtin_amdgcn_readfirstlane(mm.ne);
+        const int nx = __builtin_amdgcn_readfirstlane(mm.nx);
+        const int start = __builtin_amdgcn_readfirstlane(mm.start);
+        float *exe = p.ex_e + uniform64(mm.re);
+        float *exx = p.ex_x + uniform64(mm.rx);
+        const int hB = hA ^ 1;
+        const uint32_t *eA = se + hA * kLatLds;
+        uint32_t *eB = se + hB * kLatLds;
+        int pos = start;
+        int have = start;
+        if (n == 0) {
+            for (int i0 = 0; i0 < nB; i0 += kPipePiece) {
+                if (!pipe_need(ctl, slot, pos + min(i0 + kPipePiece, nB), have, pos + i0)) return;
+                uint32_t v[kQ];
+#pragma unroll
+                for (int q = 0; q < kQ; q++) v[q] = ring[(pos + min(i0 + q * kWave + lane, nB - 1)) & (kPipeCap - 1)].x;
+#pragma unroll
+                for (int q = 0; q < kQ; q++) eB[min(i0 + q * kWave + lane, nB - 1)] = v[q];
+            }
+            pos += nB;
+        } else {
+            for (int i0 = 0; i0 < nB; i0 += 2 * kWave) {
+                eB[min(i0 + lane, nB - 1)] = kinf;
+                eB[min(i0 + kWave + lane, nB - 1)] = kinf;
+            }
+        }
+        wave_lds_handover();
+        int kept = 0;
+        // emitting arcs into S_j+1
+        for (int i0 = 0; i0 < ne; i0 += kPipePiece) {
+            const int left = ne - i0;
+            if (!pipe_need(ctl, slot, pos + min(i0 + kPipePiece, ne), have, pos + i0)) return;
+            if (left >= kPipePiece) pipe_emit<true, kQ>(ring, pos, i0, ne, eA, eB, exe, lb, kept);
+            else if (left > 4 * kWave) pipe_emit<false, kQ>(ring, pos, i0, ne, eA, eB, exe, lb, kept);
+            else if (left > 2 * kWave) pipe_emit<false, 4>(ring, pos, i0, ne, eA, eB, exe, lb, kept);
+            else if (left > kWave) pipe_emit<false, 2>(ring, pos, i0, ne, eA, eB, exe, lb, kept);
+            else pipe_emit<false, 1>(ring, pos, i0, ne, eA, eB, exe, lb, kept);
+            // what has been read may be refilled (not after the last piece:
+            // the set's end reports it)
+            if (left > kPipePiece) pipe_publish(&ctl->consumed, pos + i0 + kPipePiece);
+        }
+        pos += ne;
+        wave_lds_handover();
+        // epsilon arcs inside S_j, to their fixed point; the round that
+        // changes nothing stores the final extra costs last
+        if (nx > 0) {
+            if (!pipe_need(ctl, slot, pos + nx, have, pos)) return;
+            int kx = 0;
+            for (;;) {
+                bool changed = false;
+                kx = 0;
+                for (int i0 = 0; i0 < nx; i0 += kPipePiece) {
+                    const int left = nx - i0;
+                    if (left >= kPipePiece) pipe_eps<true, kQ>(ring, pos, i0, nx, eB, exx, lb, kx, changed);
+                    else if (left > 4 * kWave) pipe_eps<false, kQ>(ring, pos, i0, nx, eB, exx, lb, kx, changed);
+                    else if (left > 2 * kWave) pipe_eps<false, 4>(ring, pos, i0, nx, eB, exx, lb, kx, changed);
+                    else if (left > kWave) pipe_eps<false, 2>(ring, pos, i0, nx, eB, exx, lb, kx, changed);
+                    else pipe_eps<false, 1>(ring, pos, i0, nx, eB, exx, lb, kx, changed);
+                }
+                wave_lds_handover();
+                if (!__ballot(changed)) break;
+            }
+            kept += kx;
+            pos += nx;
+        }
+        const int k = __builtin_amdgcn_readlane(wave_incl_scan(kept), kWave - 1);
+        if (lane == 0) kcnt[j] = static_cast<unsigned long long>(k);
+        // the set's entries are read: the loaders may reuse them and its slot
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        if (lane == 0) {
+            __hip_atomic_store(&ctl->consumed, pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            __hip_atomic_store(&ctl->done, n + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+        hA = hB;
+    }
+}
+
+// Called by the whole block when the pass applies (see the caller).
+__device__ void lattice_pipe(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh, LatCtl *ctl)
 {
     UttState &st = p.st[u];
     const UttLayout ly = p.lay[u];
     const int tid = threadIdx.x;
+    const int wid = tid / kWave;
+    const int nw = blockDim.x / kWave;
     const int Tp = st.Tp;
+    const int64_t *so = p.sv_off + ly.fo0;
+    unsigned long long *start_of = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
+    // every set's first stream position (in the kept-count words, which the
+    // pass overwrites once the set is done)
+    int carry = 0;
+    for (int n0 = 0; n0 <= Tp; n0 += blockDim.x) {
+        const int n = n0 + tid;
+        int sz = 0;
+        if (n <= Tp) {
+            const int j = Tp - n;
+            sz = static_cast<int>((n == 0 ? so[j + 1] - so[j] : 0) + (j < Tp ? p.le_cnt[ly.fo0 + j] : 0) +
+                                  p.lx_cnt[ly.fo0 + j]);
+        }
+        int total;
+        const int ex = block_excl_scan(sz, sh + 4, &total);
+        if (n <= Tp) start_of[Tp - n] = static_cast<unsigned long long>(carry + ex);
+        carry += total;
+    }
+    if (tid < kPipeSlots) {
+        ctl->filled[tid] = 0;
+        ctl->prog[tid] = 0;
+    }
+    if (tid == 0) {
+        ctl->done = 0;
+        ctl->consumed = 0;
+        ctl->fail = 0;
+    }
+    block_sync_vm();
+    uint2 *ring = reinterpret_cast<uint2 *>(s_c);
+    if (wid == 0) pipe_chain(p, ly, Tp, ctl, ring, s_e);
+    else pipe_load(p, ly, st, ctl, ring, wid - 1, nw - 1);
+    vm_wait();
+    __syncthreads();
+    if (ctl->fail && tid == 0) set_status(st, kStatusLatticeWait);
+}
+
+// Lattice-beam pruning of utterance u by one block: the one-wave pass when
+// every set is small, else the streamed pass when every set fits it, else the
+// block pass; then the kept counts become the output offsets.
+__device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c, int *sh, LatCtl *ctl)
+{
+    UttState &st = p.st[u];
+    const UttLayout ly = p.lay[u];
+    const int tid = threadIdx.x;
+    const int nw = blockDim.x / kWave;
+    const int Tp = st.Tp;
+    const int64_t *so = p.sv_off + ly.fo0;
     unsigned long long *kcnt = reinterpret_cast<unsigned long long *>(p.lo_off + ly.fo0);
-    if (!lattice_small(p, u, s_e, s_c, sh)) lattice_sets(p, u, s_e, s_c, sh);
+    // the largest set and record counts, and the streamed pass's total
+    if (tid == 0) {
+        ctl->mB = ctl->mE = ctl->mX = 0;
+        ctl->total = 0;
+    }
+    __syncthreads();
+    {
+        int64_t mb = 0, me = 0, mx = 0;
+        unsigned long long tot = 0;
+        for (int j = tid; j <= Tp; j += blockDim.x) {
+            const int64_t nB = so[j + 1] - so[j];
+            const int64_t ne = j < Tp ? p.le_cnt[ly.fo0 + j] : 0;
+            const int64_t nx = p.lx_cnt[ly.fo0 + j];
+            mb = max(mb, nB);
+            me = max(me, ne);
+            mx = max(mx, nx);
+            tot += static_cast<unsigned long long>((j == Tp ? nB : 0) + ne + nx);
+        }
+        constexpr int64_t kBig = 1 << 30;
+        atomicMax(&ctl->mB, static_cast<int>(min(mb, kBig)));
+        atomicMax(&ctl->mE, static_cast<int>(min(me, kBig)));
+        atomicMax(&ctl->mX, static_cast<int>(min(mx, kBig)));
+        atomicAdd(&ctl->total, tot);
+    }
+    __syncthreads();
+    const int mB = ctl->mB, mE = ctl->mE, mX = ctl->mX;
+    const bool small = nw > 1 && p.lat_lds >= kSmallSet && mB <= kSmallSet && mE <= kSmallSet && mX <= kSmallSet;
+    // The streamed pass's time grows with the records, the block pass's
+    // mostly with the sets: the streamed one where sets are small on average
+    // (or wherever it fits when lat_pipe > 0).
+    const unsigned long long tot = ctl->total;
+    const bool piped = nw > 1 && p.lat_pipe >= 0 && mB <= min(kLatLds, p.lat_lds) && mX <= kPipeCap &&
+                       tot < (1ull << 30) &&
+                       (p.lat_pipe > 0 || tot <= static_cast<unsigned long long>(kPipeAvg) * (Tp + 1));
+    if (small) lattice_small(p, u, s_e, s_c);
+    else if (piped) lattice_pipe(p, u, s_e, s_c, sh, ctl);
+    else lattice_sets(p, u, s_e, s_c, sh);
     __syncthreads();
     // kept arcs per set -> output offsets (exclusive prefix over the sets)
     int64_t carry = 0;
@@ -737,9 +1176,10 @@ __device__ void lattice_block(const Params &p, int u, uint32_t *s_e, float *s_c,
 // side by side.
 __global__ __launch_bounds__(kLatT) void finish_kernel(Params p)
 {
-    __shared__ uint32_t s_e[2 * kLatLds];
-    __shared__ float s_c[2 * kLatLds];
+    __shared__ __align__(16) uint32_t s_e[2 * kLatLds];
+    __shared__ __align__(16) float s_c[2 * kLatLds];
     __shared__ __align__(8) int sh[24];   // flags, a 64-bit count, scan scratch (17 ints)
+    __shared__ LatCtl ctl;
     const int b = blockIdx.x;
     const int u = b < p.U ? b : b - p.U;
     if (p.st[u].status != 0) return;
@@ -750,7 +1190,7 @@ __global__ __launch_bounds__(kLatT) void finish_kernel(Params p)
     __syncthreads();
     const uint64_t t0 = p.profile ? wall_clock64() : 0;
     if (b < p.U) backtrace_block(p, u, sh);
-    else lattice_block(p, u, s_e, s_c, sh);
+    else lattice_block(p, u, s_e, s_c, sh, &ctl);
     if (p.profile && threadIdx.x == 0) p.st[u].finish_ticks[b < p.U ? 0 : 1] = wall_clock64() - t0;
 }
 

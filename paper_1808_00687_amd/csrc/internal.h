@@ -245,6 +245,8 @@ struct Params {
     int32_t rec_wg;           // at most kRecMaxUtts utterances in such a launch
     int32_t rec_tmax;
     int32_t *rec_next;
+    int32_t lat_pipe;         // the lattice backward pass's streamed form: -1 never, 0 where sets are
+                              // small on average, 1 wherever it fits
 };
 
 // Workspace of the word-level lattice pass (word_kernel.hip), uniform

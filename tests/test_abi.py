@@ -121,8 +121,10 @@ def test_ctypes_structs_match_the_header(tmp_path):
 def test_debug_opts_validation():
     # host-side only: the switches are checked and stored without a device call
     from paper_1808_00687_amd import wfstdec
-    wfstdec.wfst_set_debug_opts(lds_fill=5, lattice_lds=-1, permute=1)
-    for bad in (dict(lds_fill=-1), dict(lattice_lds=-2), dict(permute=-3), dict(fail_lattice_alloc=-1)):
+    wfstdec.wfst_set_debug_opts(lds_fill=5, lattice_lds=-1, permute=1, lattice_pipe=-1)
+    wfstdec.wfst_set_debug_opts(lattice_pipe=1)
+    for bad in (dict(lds_fill=-1), dict(lattice_lds=-2), dict(permute=-3), dict(fail_lattice_alloc=-1),
+                dict(lattice_pipe=-2)):
         with pytest.raises(wfstdec.WfstError) as e:
             wfstdec.wfst_set_debug_opts(**bad)
         assert e.value.code == wfstdec.WFST_EINVAL

@@ -222,6 +222,30 @@ def test_lattice_device_memory_path(dec, torch_mod, oracle_mod, cfg2, cap):
         parity.assert_same(ro, rg, lattice=True, tag="lattice lds %d seed %d" % (cap, seed))
 
 
+@pytest.mark.parametrize("mode", [-1, 1])
+def test_lattice_streamed_pass(dec, torch_mod, oracle_mod, cfg2, mode):
+    # lattice pruning's streamed pass (one wave computes the nodes' extra
+    # costs from an LDS ring of records that the block's other waves fill),
+    # forced on wherever it fits (1) and off (-1): sets of thousands of
+    # records that wrap around the ring every few sets, with epsilon rounds
+    # over several pieces, and random graphs with epsilon-heavy sets of a few
+    # hundred tokens
+    wl, gh = cfg2
+    with dec.debug_opts(lattice_pipe=mode):
+        ro, rg = both(dec, torch_mod, oracle_mod, wl.graph, wl.loglikes[0][:120], gh=gh, beam=13.0,
+                      max_active=7000, lattice_beam=8.0)
+    parity.assert_same(ro, rg, lattice=True, tag="streamed pass %d" % mode)
+    assert rg.stats["lattice_raw"] > 8192 * 4
+    for seed in range(8):
+        g = W.random_small_graph(1300 + seed, 600 + 200 * seed, mean_deg=3.0, eps_frac=0.35, num_labels=5,
+                                 weights=["int", "exp"][seed % 2], final=seed % 3 == 0)
+        ll = W.random_small_loglikes(1300 + seed, 30, 5, kind=["int", "gauss"][seed % 2])
+        with dec.debug_opts(lattice_pipe=mode):
+            ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=[INF, 9.0][seed % 2],
+                          max_active=[0, 300][seed % 2 if seed < 4 else 0], lattice_beam=[3.0, INF][seed % 2])
+        parity.assert_same(ro, rg, lattice=True, tag="streamed pass %d seed %d" % (mode, seed))
+
+
 @pytest.mark.parametrize("fill,big", [(1, 1), (900, 1), (1, 1 << 20), (900, 1500)])
 def test_record_large_set_path(dec, torch_mod, oracle_mod, cfg2, fill, big):
     # token sets of more than `fill` survivors get their back-pointers and
@@ -657,6 +681,29 @@ def test_config4_batch_full(dec, torch_mod, oracle_mod, cfg3):
     with ThreadPoolExecutor(max_workers=threads) as ex:
         toks = list(ex.map(check, range(len(res))))
     say("config 4: %d utterances, %d tokens compared" % (len(res), sum(toks)))
+
+
+def test_config4_streamed_lattice_pass(dec, torch_mod, oracle_mod, cfg3):
+    # the benchmark's batch with lattice pruning's streamed pass forced on
+    # (by default its utterances, of about 1,200 records per set, take the
+    # block pass): the same lattice, extra costs and kept counts as the
+    # default call, and the oracle's on two utterances
+    g, gh = cfg3
+    wl = W.workload(4)
+    o = wl.opts
+    xs = [to_dev(torch_mod, x) for x in wl.loglikes]
+    a = dec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam)
+    with dec.debug_opts(lattice_pipe=1):
+        b = dec.wfst_decode_batch(gh, xs, o.beam, o.max_active, o.lattice_beam)
+    del xs
+    for u, (ra, rb) in enumerate(zip(a, b)):
+        for f in ("lat_frame", "lat_arc", "path_arcs"):
+            np.testing.assert_array_equal(getattr(ra, f), getattr(rb, f), err_msg="utt %d %s" % (u, f))
+        np.testing.assert_array_equal(parity.bits(ra.lat_cost), parity.bits(rb.lat_cost), err_msg="utt %d" % u)
+        np.testing.assert_array_equal(parity.bits(ra.lat_extra), parity.bits(rb.lat_extra), err_msg="utt %d" % u)
+    for u in (0, 37):
+        ro = oracle_mod.decode(g, wl.loglikes[u], o.beam, o.max_active, o.lattice_beam)
+        parity.assert_same(ro, b[u], lattice=True, tokens=False, tag="config 4 streamed utt %d" % u)
 
 
 def test_config4_wide_rows(dec, torch_mod, oracle_mod, cfg3):
