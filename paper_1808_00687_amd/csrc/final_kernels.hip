@@ -1203,9 +1203,10 @@ __device__ __forceinline__ void cas16(int4 *v, int i, int j)
     }
 }
 
-// Ascending sort of n records by arc id (unique within a token set): the
-// bitonic network in its "flip" form, where every comparator puts the
-// smaller key first, so positions >= n act as +inf and are never touched.
+// Ascending sort of n records by arc id (unique within a token set) by the
+// whole block: the bitonic network in its "flip" form, where every
+// comparator puts the smaller key first, so positions >= n act as +inf and
+// are never touched.
 __device__ void sort_records(int4 *v, int n)
 {
     int n2 = 1;
@@ -1229,60 +1230,169 @@ __device__ void sort_records(int4 *v, int n)
     }
 }
 
-constexpr int kSortLds = 2048;
+constexpr int kEmitK = 512;     // kept arcs of a set that one wave sorts in LDS
+constexpr int kEmitW = 4;       // waves per block of the output pass
+constexpr int kEmitQ = 4;       // records per lane in flight in the scan
+constexpr int kEmitDefer = 256; // larger sets a block keeps for its joint pass
 
-// One block per (token set j, utterance): gather the kept arcs of set j,
-// sort them by arc and write {frame, arc, cost, extra}.
-__global__ __launch_bounds__(256) void lattice_emit_kernel(Params p)
+// A set's record offsets, loaded a set ahead of their use.
+struct EmitMeta {
+    int64_t o0, o1;   // output range (kept-arc offsets)
+    int64_t e0, x0;   // first emitting and first epsilon record
+    int64_t ne, nx;
+};
+
+__device__ __forceinline__ EmitMeta emit_meta(const Params &p, const UttLayout &ly, int j, int Tp)
 {
-    __shared__ int4 buf[kSortLds];
-    __shared__ int sh_n;
-    const int u = blockIdx.y;
-    const int j = blockIdx.x;
-    UttState &st = p.st[u];
-    if (st.status != 0 || j > st.Tp) return;
-    const UttLayout &ly = p.lay[u];
+    EmitMeta m;
+    m.o0 = p.lo_off[ly.fo0 + j];
+    m.o1 = p.lo_off[ly.fo0 + j + 1];
+    m.e0 = ly.le0 + (j < Tp ? p.le_off[ly.fo0 + j] : 0);
+    m.ne = j < Tp ? p.le_cnt[ly.fo0 + j] : 0;
+    m.x0 = ly.lx0 + p.lx_off[ly.fo0 + j];
+    m.nx = p.lx_cnt[ly.fo0 + j];
+    return m;
+}
+
+// A set with more kept arcs than a wave's buffer, by one wave: each kept
+// record's rank is the number of kept records of smaller arc (only when the
+// block's list of such sets is full).
+__device__ void emit_set_counted(const Params &p, const EmitMeta &c, int j, int n, int4 *out)
+{
+    const int lane = lane_id();
     const float lb = p.lattice_beam;
-    const int64_t o0 = p.lo_off[ly.fo0 + j];
-    const int n = static_cast<int>(p.lo_off[ly.fo0 + j + 1] - o0);
-    if (n == 0) return;
-    int4 *out = p.lat_out + ly.lo0 + o0;
-    const bool in_lds = n <= kSortLds;
-    int4 *v = in_lds ? buf : out;
-    if (threadIdx.x == 0) sh_n = 0;
-    __syncthreads();
-    for (int part = 0; part < 2; part++) {
-        int64_t r0, r1;
-        const int4 *rec;
-        const float *ex;
-        int64_t base;
-        if (part == 0) {
-            if (j == st.Tp) continue;
-            r0 = p.le_off[ly.fo0 + j];
-            r1 = r0 + p.le_cnt[ly.fo0 + j];
-            rec = p.lat_e;
-            ex = p.ex_e;
-            base = ly.le0;
-        } else {
-            r0 = p.lx_off[ly.fo0 + j];
-            r1 = r0 + p.lx_cnt[ly.fo0 + j];
-            rec = p.lat_x;
-            ex = p.ex_x;
-            base = ly.lx0;
+    const int ne = static_cast<int>(c.ne);
+    const int nr = ne + static_cast<int>(c.nx);
+    for (int a0 = 0; a0 < nr; a0 += kWave) {
+        const int a = a0 + lane;
+        bool ka = false;
+        float xa = 0.0f;
+        int4 ra = make_int4(0, 0, 0, 0);
+        if (a < nr) {
+            xa = a < ne ? p.ex_e[c.e0 + a] : p.ex_x[c.x0 + (a - ne)];
+            ka = xa <= lb;
+            if (ka) ra = a < ne ? p.lat_e[c.e0 + a] : p.lat_x[c.x0 + (a - ne)];
         }
-        for (int64_t r = r0 + threadIdx.x; r < r1; r += blockDim.x) {
-            float x = ex[base + r];
-            if (x <= lb) {
-                int slot = atomicAdd(&sh_n, 1);
-                int4 q = rec[base + r];
-                if (slot < n) v[slot] = make_int4(j, q.z, q.w, __float_as_int(x));
+        if (!__ballot(ka)) continue;
+        int rank = 0;
+        for (int b0 = 0; b0 < nr; b0 += kWave) {
+            const int b = b0 + lane;
+            int arc = 0x7FFFFFFF;   // not kept: larger than every arc
+            if (b < nr) {
+                const float xb = b < ne ? p.ex_e[c.e0 + b] : p.ex_x[c.x0 + (b - ne)];
+                if (xb <= lb) arc = (b < ne ? p.lat_e[c.e0 + b] : p.lat_x[c.x0 + (b - ne)]).z;
+            }
+            for (int l = 0; l < kWave; l++) rank += __builtin_amdgcn_readlane(arc, l) < ra.z;
+        }
+        if (ka && rank < n) out[rank] = make_int4(j, ra.z, ra.w, __float_as_int(xa));
+    }
+}
+
+// The sorted lattice output: {frame, arc, cost, extra} of every kept arc,
+// each set's arcs in ascending arc order (arc ids are unique within a set).
+// A wave takes every (gridDim.x * kEmitW)-th set of its utterance: it scans
+// the set's extra costs, places the kept records in its LDS buffer by their
+// order in the scan, and writes each to its rank among them.  Sets with more
+// kept arcs than a wave's buffer wait in a list for the whole block, which
+// then gathers each into the four buffers together (or, beyond those, into
+// the output itself) and sorts it with the bitonic network.
+__global__ __launch_bounds__(kEmitW * kWave) void lattice_emit_kernel(Params p)
+{
+    __shared__ int4 buf[kEmitW * kEmitK];
+    __shared__ int defer[kEmitDefer];
+    __shared__ int n_defer, sh_n;
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int u = blockIdx.y;
+    const UttState &st = p.st[u];
+    if (st.status != 0) return;
+    const UttLayout &ly = p.lay[u];
+    const int Tp = st.Tp;
+    const float lb = p.lattice_beam;
+    const int step = gridDim.x * kEmitW;
+    if (threadIdx.x == 0) n_defer = 0;
+    __syncthreads();
+    int4 *wb = buf + w * kEmitK;
+    int j = blockIdx.x * kEmitW + w;
+    EmitMeta m{};
+    if (j <= Tp) m = emit_meta(p, ly, j, Tp);
+    for (; j <= Tp; j += step) {
+        const EmitMeta c = m;
+        if (j + step <= Tp) m = emit_meta(p, ly, j + step, Tp);
+        const int n = static_cast<int>(c.o1 - c.o0);
+        int4 *out = p.lat_out + ly.lo0 + c.o0;
+        const int ne = static_cast<int>(c.ne);
+        const int nr = ne + static_cast<int>(c.nx);
+        if (n <= 0 || nr <= 0) continue;
+        if (n > kEmitK) {
+            int d = 0;
+            if (lane == 0) d = atomicAdd(&n_defer, 1);
+            d = __builtin_amdgcn_readfirstlane(d);
+            if (d < kEmitDefer) {
+                if (lane == 0) defer[d] = j;
+            } else {
+                emit_set_counted(p, c, j, n, out);
+            }
+            continue;
+        }
+        int cnt = 0;
+        for (int i0 = 0; i0 < nr; i0 += kEmitQ * kWave) {
+            float x[kEmitQ];
+#pragma unroll
+            for (int q = 0; q < kEmitQ; q++) {
+                const int i = min(i0 + q * kWave + lane, nr - 1);
+                x[q] = i < ne ? p.ex_e[c.e0 + i] : p.ex_x[c.x0 + (i - ne)];
+            }
+#pragma unroll
+            for (int q = 0; q < kEmitQ; q++) {
+                const int i = i0 + q * kWave + lane;
+                const bool kp = i < nr && x[q] <= lb;
+                const uint64_t km = __ballot(kp);
+                const int slot = cnt + __popcll(km & lanemask_lt());
+                if (kp && slot < kEmitK) {
+                    const int4 r = i < ne ? p.lat_e[c.e0 + i] : p.lat_x[c.x0 + (i - ne)];
+                    wb[slot] = make_int4(j, r.z, r.w, __float_as_int(x[q]));
+                }
+                cnt += __popcll(km);
             }
         }
+        wave_lds_handover();
+        const int m2 = min(cnt, n);
+        for (int a = lane; a < m2; a += kWave) {
+            const int4 e = wb[a];
+            int rank = 0;
+            for (int b = 0; b < m2; b++) rank += wb[b].y < e.y;
+            out[rank] = e;
+        }
+        wave_lds_handover();
     }
+    // the block's large sets, one after another
     __syncthreads();
-    sort_records(v, n);
-    if (in_lds)
-        for (int i = threadIdx.x; i < n; i += blockDim.x) out[i] = buf[i];
+    const int nd = min(n_defer, kEmitDefer);
+    for (int d = 0; d < nd; d++) {
+        const int jd = defer[d];
+        const EmitMeta c = emit_meta(p, ly, jd, Tp);
+        const int n = static_cast<int>(c.o1 - c.o0);
+        int4 *out = p.lat_out + ly.lo0 + c.o0;
+        int4 *v = n <= kEmitW * kEmitK ? buf : out;
+        if (threadIdx.x == 0) sh_n = 0;
+        __syncthreads();
+        const int ne = static_cast<int>(c.ne);
+        const int nr = ne + static_cast<int>(c.nx);
+        for (int i = threadIdx.x; i < nr; i += blockDim.x) {
+            const float x = i < ne ? p.ex_e[c.e0 + i] : p.ex_x[c.x0 + (i - ne)];
+            if (x <= lb) {
+                const int slot = atomicAdd(&sh_n, 1);
+                const int4 r = i < ne ? p.lat_e[c.e0 + i] : p.lat_x[c.x0 + (i - ne)];
+                if (slot < n) v[slot] = make_int4(jd, r.z, r.w, __float_as_int(x));
+            }
+        }
+        __syncthreads();
+        sort_records(v, n);
+        if (v == buf)
+            for (int i = threadIdx.x; i < n; i += blockDim.x) out[i] = buf[i];
+        __syncthreads();
+    }
 }
 
 // The best paths of all utterances packed one after another (utterance
@@ -1361,7 +1471,10 @@ hipError_t launch_finish(const Params &p, hipStream_t s)
 
 hipError_t launch_lattice_emit(const Params &p, int max_frames, hipStream_t s)
 {
-    hipLaunchKernelGGL(lattice_emit_kernel, dim3(max_frames + 1, p.U), dim3(256), 0, s, p);
+    // about 1,024 blocks over the batch, no more waves per utterance than sets
+    const int sets = max_frames + 1;
+    const int g = std::max(1, std::min((1024 + p.U - 1) / p.U, (sets + kEmitW - 1) / kEmitW));
+    hipLaunchKernelGGL(lattice_emit_kernel, dim3(g, p.U), dim3(kEmitW * kWave), 0, s, p);
     return hipGetLastError();
 }
 

@@ -246,6 +246,18 @@ def test_lattice_streamed_pass(dec, torch_mod, oracle_mod, cfg2, mode):
         parity.assert_same(ro, rg, lattice=True, tag="streamed pass %d seed %d" % (mode, seed))
 
 
+def test_lattice_output_large_sets(dec, torch_mod, oracle_mod):
+    # token sets with more kept arcs than the output pass sorts in LDS (512
+    # per set): every raw record kept (infinite beams) on a graph with
+    # thousands of arcs per set, against the oracle
+    g = W.random_small_graph(1400, 1500, mean_deg=3.0, eps_frac=0.2, num_labels=5, weights="int")
+    ll = W.random_small_loglikes(1400, 12, 5, kind="int")
+    ro, rg = both(dec, torch_mod, oracle_mod, g, ll, beam=INF, lattice_beam=INF)
+    parity.assert_same(ro, rg, lattice=True, tag="large kept sets")
+    per_set = np.bincount(np.asarray(rg.lat_frame))
+    assert per_set.max() > 512 and per_set.min() >= 0
+
+
 @pytest.mark.parametrize("fill,big", [(1, 1), (900, 1), (1, 1 << 20), (900, 1500)])
 def test_record_large_set_path(dec, torch_mod, oracle_mod, cfg2, fill, big):
     # token sets of more than `fill` survivors get their back-pointers and
