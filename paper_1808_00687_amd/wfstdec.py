@@ -66,6 +66,9 @@ class _Stats(C.Structure):
                 ("workspace_bytes", C.c_int64)]
 
 
+_STAT_FIELDS = tuple(f for f, _ in _Stats._fields_ if f != "search_phase_ms")
+
+
 class _DebugOpts(C.Structure):
     _fields_ = [("lds_fill", C.c_int32), ("queue_cap", C.c_int32), ("record_fill", C.c_int32),
                 ("record_big_fill", C.c_int32), ("lattice_lds", C.c_int32), ("permute", C.c_int32),
@@ -271,9 +274,13 @@ class WfstResult:
 
 
 def _arr(ptr, n, dt):
+    """Copy of n elements of type dt at a library pointer (one memmove: a
+    ctypes array view per call costs more than the copy)."""
     if n <= 0 or not ptr:
         return np.zeros(0, dtype=dt)
-    return np.ctypeslib.as_array(ptr, shape=(n,)).astype(dt, copy=True)
+    a = np.empty(n, dtype=dt)
+    C.memmove(a.ctypes.data, ptr, a.nbytes)
+    return a
 
 
 def _lattice_views(outs) -> list:
@@ -309,7 +316,7 @@ def _collect(h, lattice: bool, tokens: bool, lat=None, words: bool = False) -> W
     r.kept = _arr(kp, nd.value, np.int32)
     s = _Stats()
     _check(_lib.wfst_result_stats(h, C.byref(s)), "wfst_result_stats")
-    r.stats = {f: getattr(s, f) for f, _ in _Stats._fields_}
+    r.stats = {f: getattr(s, f) for f in _STAT_FIELDS}
     r.stats["search_phase_ms"] = list(s.search_phase_ms)
     if st != WFST_OK:
         return r
