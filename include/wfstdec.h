@@ -424,6 +424,10 @@ int wfst_decode_noalloc(const wfst_graph *g, const float *loglikes, int32_t T, i
  *                      sets are too large for the one-wave pass): -1 never
  *                      (the block pass instead), 0 where the utterance's
  *                      sets hold few records on average, 1 wherever it fits
+ *   lattice_spin       polls of one hand-over flag before the one-wave or
+ *                      streamed lattice pass gives up (0: the library's own,
+ *                      seconds); a tiny count makes the pass fail as a stuck
+ *                      hand-over would: WFST_EDEVICE, every kernel ending
  *
  * opts == NULL restores every default.  Takes effect for decodes started
  * after the call returns.  Errors: WFST_EINVAL for a negative field other
@@ -443,6 +447,7 @@ typedef struct wfst_debug_opts {
     int32_t record_groups;
     int32_t record_publish;
     int32_t lattice_pipe;
+    int32_t lattice_spin;
 } wfst_debug_opts;
 
 int wfst_set_debug_opts(const wfst_debug_opts *opts);

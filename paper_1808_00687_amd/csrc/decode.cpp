@@ -609,6 +609,7 @@ void set_params(Params &p, const Graph &G, int U, int L, const wfst_decode_opts 
     p.rec_big_fill = limit_or(dbg.record_big_fill, 1 << 30);
     p.lat_lds = dbg.lattice_lds < 0 ? 0 : limit_or(dbg.lattice_lds, 1 << 30);
     p.lat_pipe = dbg.lattice_pipe < 0 ? -1 : (dbg.lattice_pipe > 0 ? 1 : 0);
+    p.lat_spin = dbg.lattice_spin;
     p.hash_mul = dbg.permute ? kHashMulAlt : kHashMul;
     p.reverse = dbg.permute ? 1 : 0;
     p.capG = 8192;
@@ -1088,7 +1089,7 @@ int run_batch(const Graph &G, int U, const float *const *ll_in, const int32_t *T
         if (st[u].status == kStatusStreamTimeout)
             return fail(WFST_EDEVICE, "decode: internal error, a pass beside the search stopped waiting for it");
         if (st[u].status == kStatusLatticeWait)
-            return fail(WFST_EDEVICE, "decode: internal error, the one-wave lattice pass stopped waiting");
+            return fail(WFST_EDEVICE, "decode: internal error, a lattice pass stopped waiting for its other waves");
     }
 
     std::shared_ptr<LatBuf> lat_buf;
@@ -1574,7 +1575,8 @@ extern "C" int wfst_set_debug_opts(const wfst_debug_opts *opts)
         o = *opts;
         if (o.lds_fill < 0 || o.queue_cap < 0 || o.record_fill < 0 || o.record_big_fill < 0 ||
             o.lattice_lds < -1 || o.permute < 0 || o.fail_lattice_alloc < 0 || o.lattice_chunk < -1 ||
-            o.lattice_ring < 0 || o.record_groups < -1 || o.record_publish < 0 || o.lattice_pipe < -1)
+            o.lattice_ring < 0 || o.record_groups < -1 || o.record_publish < 0 || o.lattice_pipe < -1 ||
+            o.lattice_spin < 0)
             return fail(WFST_EINVAL, "wfst_set_debug_opts: negative field");
     }
     DebugState &d = debug_state();
@@ -1748,7 +1750,7 @@ int noalloc_impl(const wfst_graph *gh, const float *ll, int32_t T, int32_t L, co
     if (st.status == kStatusNoBackPointer)
         return fail(WFST_EDEVICE, "wfst_decode_noalloc: internal error, a surviving token without a back-pointer");
     if (st.status == kStatusLatticeWait)
-        return fail(WFST_EDEVICE, "wfst_decode_noalloc: internal error, the one-wave lattice pass stopped waiting");
+        return fail(WFST_EDEVICE, "wfst_decode_noalloc: internal error, a lattice pass stopped waiting for its other waves");
     if (st.status == WFST_ECAPACITY) {
         set_error("wfst_decode_noalloc: the decode overflowed the fixed workspace");
         return WFST_ECAPACITY;

@@ -505,7 +505,7 @@ __device__ void lattice_sets(const Params &p, int u, uint32_t *s_e, float *s_c, 
 // ---------------------------------------------------------------------------
 constexpr int kSmallSet = 64;                 // survivors and records per set (one per lane)
 constexpr int kRing = 16;                     // sets in flight between the loading waves and wave 0
-constexpr long long kSmallSpin = 1LL << 24;   // polls of one flag before the pass gives up
+constexpr long long kSmallSpin = 1LL << 24;   // polls of one flag before a pass gives up (unless lat_spin sets it)
 
 struct SmallSlot {
     int b0;                   // the set's first survivor (utterance-relative)
@@ -520,13 +520,16 @@ struct SmallSlot {
 };
 static_assert(kRing * sizeof(SmallSlot) <= 2 * kLatLds * sizeof(float), "the ring fits the cost half of the LDS");
 
+// Polls of one flag before a pass gives up.
+__device__ __forceinline__ long long lat_spin(const Params &p) { return p.lat_spin > 0 ? p.lat_spin : kSmallSpin; }
+
 // Wait until *f >= v (every lane reads the same LDS word); false if the pass
 // has failed or the wait gave up (then it marks the pass failed).
-__device__ __forceinline__ bool small_wait(int *f, int v, int *fail)
+__device__ __forceinline__ bool small_wait(int *f, int v, int *fail, long long spin)
 {
     for (long long i = 0;; i++) {
         if (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= v) break;
-        if (__hip_atomic_load(fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= kSmallSpin) {
+        if (__hip_atomic_load(fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= spin) {
             __hip_atomic_store(fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             return false;
         }
@@ -579,6 +582,7 @@ __device__ void lattice_records(const Params &p, const UttLayout &ly, int Tp)
 // survivors, emitting records and epsilon records.
 __device__ void lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c)
 {
+    const long long spin = lat_spin(p);
     UttState &st = p.st[u];
     const UttLayout ly = p.lay[u];
     const int tid = threadIdx.x;
@@ -612,7 +616,7 @@ __device__ void lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c)
         // ---- the loading waves: set n (the n-th from the last) into slot n mod kRing ----
         for (int n = wid - 1; n <= Tp; n += nw - 1) {
             const int slot = n % kRing;
-            if (n >= kRing && !small_wait(done, n - kRing + 1, fail)) break;
+            if (n >= kRing && !small_wait(done, n - kRing + 1, fail, spin)) break;
             const int j = Tp - n;
             const int b0 = static_cast<int>(so[j]);
             const int nB = static_cast<int>(so[j + 1] - so[j]);
@@ -647,7 +651,7 @@ __device__ void lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c)
         for (int n = 0; n <= Tp; n++) {
             const int j = Tp - n;
             const SmallSlot &sl = ring[n % kRing];
-            if (!small_wait(filled + n % kRing, n + 1, fail)) break;
+            if (!small_wait(filled + n % kRing, n + 1, fail, spin)) break;
             const int b0 = sl.b0, nB = sl.nB, ne = sl.ne, nx = sl.nx;
             const int hB = hA ^ 1;
             uint32_t *eA = se + hA * kSmallSet, *eB = se + hB * kSmallSet;
@@ -757,11 +761,11 @@ struct LatCtl {
 // Wait until *f >= v; LDS-only ordering (the waiting wave's device-memory
 // stores are not waited for).  False if the pass has failed or the wait gave
 // up (then it marks the pass failed).
-__device__ __forceinline__ bool pipe_wait(const int *f, int v, int *fail)
+__device__ __forceinline__ bool pipe_wait(const int *f, int v, int *fail, long long spin)
 {
     for (long long i = 0;; i++) {
         if (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= v) break;
-        if (__hip_atomic_load(fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= kSmallSpin) {
+        if (__hip_atomic_load(fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= spin) {
             __hip_atomic_store(fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             return false;
         }
@@ -782,6 +786,7 @@ __device__ __forceinline__ void pipe_publish(int *f, int v)
 __device__ void pipe_load(const Params &p, const UttLayout &ly, const UttState &st, LatCtl *ctl, uint2 *ring,
                           int pw, int np)
 {
+    const long long spin = lat_spin(p);
     const int lane = lane_id();
     const int Tp = st.Tp;
     const float B = st.final_cost;
@@ -801,7 +806,7 @@ __device__ void pipe_load(const Params &p, const UttLayout &ly, const UttState &
         const int64_t re = ly.le0 + (j < Tp ? p.le_off[ly.fo0 + j] : 0);
         const int64_t rx = ly.lx0 + p.lx_off[ly.fo0 + j];
         const int start = static_cast<int>(ld_relaxed(start_of + j));
-        if (n >= kPipeSlots && !pipe_wait(&ctl->done, n - kPipeSlots + 1, &ctl->fail)) return;
+        if (n >= kPipeSlots && !pipe_wait(&ctl->done, n - kPipeSlots + 1, &ctl->fail, spin)) return;
         if (lane == 0) {
             PipeMeta &m = ctl->meta[slot];
             m.re = re;
@@ -830,7 +835,7 @@ __device__ void pipe_load(const Params &p, const UttLayout &ly, const UttState &
                     }
                 }
                 const int end = start + min(i0 + kPipePiece, nB);
-                if (!pipe_wait(&ctl->consumed, end - kPipeCap, &ctl->fail)) return;
+                if (!pipe_wait(&ctl->consumed, end - kPipeCap, &ctl->fail, spin)) return;
 #pragma unroll
                 for (int q = 0; q < kQ; q++) {
                     const int i = i0 + q * kWave + lane;
@@ -864,7 +869,7 @@ __device__ void pipe_load(const Params &p, const UttLayout &ly, const UttState &
                 }
             }
             const int end = pos + min(i0 + kPipePiece, nr);
-            if (!pipe_wait(&ctl->consumed, end - kPipeCap, &ctl->fail)) return;
+            if (!pipe_wait(&ctl->consumed, end - kPipeCap, &ctl->fail, spin)) return;
 #pragma unroll
             for (int q = 0; q < kQ; q++) {
                 const int i = i0 + q * kWave + lane;
@@ -878,7 +883,7 @@ __device__ void pipe_load(const Params &p, const UttLayout &ly, const UttState &
 // Wave 0's wait for stream position `end` of the set in `slot`: `have` is
 // the position it last saw written.  Before it blocks it reports what it has
 // read (up to `cur`), which the loaders may be waiting for.
-__device__ __forceinline__ bool pipe_need(LatCtl *ctl, int slot, int end, int &have, int cur)
+__device__ __forceinline__ bool pipe_need(LatCtl *ctl, int slot, int end, int &have, int cur, long long spin)
 {
     if (have >= end) return true;
     pipe_publish(&ctl->consumed, cur);
@@ -888,7 +893,7 @@ __device__ __forceinline__ bool pipe_need(LatCtl *ctl, int slot, int end, int &h
             have = v;
             break;
         }
-        if (__hip_atomic_load(&ctl->fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= kSmallSpin) {
+        if (__hip_atomic_load(&ctl->fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) || i >= spin) {
             __hip_atomic_store(&ctl->fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             return false;
         }
@@ -971,6 +976,7 @@ __device__ __forceinline__ int64_t uniform64(int64_t v)
 __device__ void pipe_chain(const Params &p, const UttLayout &ly, int Tp, LatCtl *ctl, const uint2 *ring,
                            uint32_t *se)
 {
+    const long long spin = lat_spin(p);
     const int lane = lane_id();
     const float lb = p.lattice_beam;
     const uint32_t kinf = okey(__int_as_float(0x7F800000));
@@ -980,7 +986,7 @@ __device__ void pipe_chain(const Params &p, const UttLayout &ly, int Tp, LatCtl 
     for (int n = 0; n <= Tp; n++) {
         const int j = Tp - n;
         const int slot = n % kPipeSlots;
-        if (!pipe_wait(ctl->filled + slot, n + 1, &ctl->fail)) return;
+        if (!pipe_wait(ctl->filled + slot, n + 1, &ctl->fail, spin)) return;
         const PipeMeta &mm = ctl->meta[slot];
         const int nB = __builtin_amdgcn_readfirstlane(mm.nB);
         const int ne = __builtin_amdgcn_readfirstlane(mm.ne);
@@ -995,7 +1001,7 @@ __device__ void pipe_chain(const Params &p, const UttLayout &ly, int Tp, LatCtl 
         int have = start;
         if (n == 0) {
             for (int i0 = 0; i0 < nB; i0 += kPipePiece) {
-                if (!pipe_need(ctl, slot, pos + min(i0 + kPipePiece, nB), have, pos + i0)) return;
+                if (!pipe_need(ctl, slot, pos + min(i0 + kPipePiece, nB), have, pos + i0, spin)) return;
                 uint32_t v[kQ];
 #pragma unroll
                 for (int q = 0; q < kQ; q++) v[q] = ring[(pos + min(i0 + q * kWave + lane, nB - 1)) & (kPipeCap - 1)].x;
@@ -1014,7 +1020,7 @@ __device__ void pipe_chain(const Params &p, const UttLayout &ly, int Tp, LatCtl 
         // emitting arcs into S_j+1
         for (int i0 = 0; i0 < ne; i0 += kPipePiece) {
             const int left = ne - i0;
-            if (!pipe_need(ctl, slot, pos + min(i0 + kPipePiece, ne), have, pos + i0)) return;
+            if (!pipe_need(ctl, slot, pos + min(i0 + kPipePiece, ne), have, pos + i0, spin)) return;
             if (left >= kPipePiece) pipe_emit<true, kQ>(ring, pos, i0, ne, eA, eB, exe, lb, kept);
             else if (left > 4 * kWave) pipe_emit<false, kQ>(ring, pos, i0, ne, eA, eB, exe, lb, kept);
             else if (left > 2 * kWave) pipe_emit<false, 4>(ring, pos, i0, ne, eA, eB, exe, lb, kept);
@@ -1029,7 +1035,7 @@ __device__ void pipe_chain(const Params &p, const UttLayout &ly, int Tp, LatCtl 
         // epsilon arcs inside S_j, to their fixed point; the round that
         // changes nothing stores the final extra costs last
         if (nx > 0) {
-            if (!pipe_need(ctl, slot, pos + nx, have, pos)) return;
+            if (!pipe_need(ctl, slot, pos + nx, have, pos, spin)) return;
             int kx = 0;
             for (;;) {
                 bool changed = false;

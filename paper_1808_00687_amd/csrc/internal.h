@@ -247,6 +247,7 @@ struct Params {
     int32_t *rec_next;
     int32_t lat_pipe;         // the lattice backward pass's streamed form: -1 never, 0 where sets are
                               // small on average, 1 wherever it fits
+    int32_t lat_spin;         // > 0: polls of one flag before a lattice pass's wait gives up (else its own)
 };
 
 // Workspace of the word-level lattice pass (word_kernel.hip), uniform

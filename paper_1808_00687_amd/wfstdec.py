@@ -74,7 +74,7 @@ class _DebugOpts(C.Structure):
                 ("record_big_fill", C.c_int32), ("lattice_lds", C.c_int32), ("permute", C.c_int32),
                 ("fail_lattice_alloc", C.c_int32), ("lattice_chunk", C.c_int32), ("lattice_ring", C.c_int32),
                 ("record_groups", C.c_int32), ("record_publish", C.c_int32),
-                ("lattice_pipe", C.c_int32)]
+                ("lattice_pipe", C.c_int32), ("lattice_spin", C.c_int32)]
 
 
 class _LatArc(C.Structure):

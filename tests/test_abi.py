@@ -124,7 +124,7 @@ def test_debug_opts_validation():
     wfstdec.wfst_set_debug_opts(lds_fill=5, lattice_lds=-1, permute=1, lattice_pipe=-1)
     wfstdec.wfst_set_debug_opts(lattice_pipe=1)
     for bad in (dict(lds_fill=-1), dict(lattice_lds=-2), dict(permute=-3), dict(fail_lattice_alloc=-1),
-                dict(lattice_pipe=-2)):
+                dict(lattice_pipe=-2), dict(lattice_spin=-1)):
         with pytest.raises(wfstdec.WfstError) as e:
             wfstdec.wfst_set_debug_opts(**bad)
         assert e.value.code == wfstdec.WFST_EINVAL

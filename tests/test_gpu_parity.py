@@ -246,6 +246,36 @@ def test_lattice_streamed_pass(dec, torch_mod, oracle_mod, cfg2, mode):
         parity.assert_same(ro, rg, lattice=True, tag="streamed pass %d seed %d" % (mode, seed))
 
 
+@pytest.mark.parametrize("form", ["one-wave", "streamed"])
+def test_lattice_pass_gives_up(dec, torch_mod, oracle_mod, cfg2, form):
+    # the lattice passes' hand-over waits are bounded: with one poll allowed
+    # (set from the host) the pass gives up, every kernel ends and the call
+    # reports a device error; the next call, with the library's own limit,
+    # decodes as before
+    if form == "one-wave":
+        g = W.random_small_graph(1500, 40, mean_deg=2.0, eps_frac=0.2, num_labels=5, weights="int")
+        ll = W.random_small_loglikes(1500, 30, 5, kind="int")
+        gh, kw = None, dict(beam=INF, lattice_beam=INF)
+        opts = dict()
+    else:
+        wl, gh = cfg2
+        g, ll = wl.graph, wl.loglikes[0][:60]
+        kw = dict(beam=13.0, max_active=7000, lattice_beam=8.0)
+        opts = dict(lattice_pipe=1)
+    own = gh is None
+    if own:
+        gh = dec.load_graph(g)
+    with dec.debug_opts(lattice_spin=1, **opts):
+        with pytest.raises(dec.WfstError) as e:
+            dec.wfst_decode(gh, to_dev(torch_mod, ll), kw["beam"], kw.get("max_active", 0), kw["lattice_beam"])
+    assert e.value.code == dec.WFST_EDEVICE and "lattice pass stopped waiting" in str(e.value)
+    with dec.debug_opts(**opts):
+        ro, rg = both(dec, torch_mod, oracle_mod, g, ll, gh=gh, **kw)
+    parity.assert_same(ro, rg, lattice=True, tag="after a pass that gave up (%s)" % form)
+    if own:
+        gh.free()
+
+
 def test_lattice_output_large_sets(dec, torch_mod, oracle_mod):
     # token sets with more kept arcs than the output pass sorts in LDS (512
     # per set): every raw record kept (infinite beams) on a graph with
