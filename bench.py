@@ -15,6 +15,7 @@ one GPU; batches of utterances would shard across GPUs with no per-frame
 communication, which this build does not do.
 """
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -448,6 +449,12 @@ def main():
         log("warmup %d done" % i)
     torch.cuda.synchronize()
     profile = not args.no_profile
+    # the process's long-lived objects (torch's, the workload's) go to the
+    # permanent generation: a full collection over them would otherwise land
+    # inside a step now and then (tens of ms); each step's own garbage is
+    # still collected
+    gc.collect()
+    gc.freeze()
     t0 = time.perf_counter()
     res = None
     for i in range(args.steps):
