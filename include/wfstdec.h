@@ -315,6 +315,38 @@ int wfst_result_words(const wfst_result *r, int64_t *n, const int64_t **offsets,
    Eq. 3: decoded frames, tokens and arcs expanded).  Errors: WFST_EINVAL. */
 int wfst_result_stats(const wfst_result *r, wfst_stats *stats);
 
+/*
+ * For callers that pay per call (language bindings): what
+ * wfst_result_status, wfst_result_frames, wfst_result_best,
+ * wfst_result_stats and, with want_lattice nonzero, wfst_result_lattice
+ * return, for n results at once, one summary each.  The pointers are the
+ * ones those calls give (host memory owned by the result, or the batch's
+ * shared host copy of the lattices, made by this call when needed).  A
+ * result without a path has path_len = 0, NULL path pointers and a NaN
+ * cost; without want_lattice (or without a lattice) lattice_n = 0 and
+ * lattice = NULL.  Errors: WFST_EINVAL (a NULL argument or result, n < 0),
+ * WFST_EDEVICE (the lattice copy failed).
+ */
+typedef struct wfst_result_summary {
+    int32_t status;
+    int32_t num_frames;
+    int32_t num_decoded;
+    int32_t path_len;
+    float cost;
+    int32_t final_state;
+    int32_t reached_final;
+    int32_t reserved;
+    const int32_t *orig_frame;     /* num_decoded entries */
+    const int32_t *path_arcs;      /* path_len entries */
+    const int32_t *path_frames;    /* path_len entries */
+    int64_t lattice_n;
+    const wfst_lat_arc *lattice;   /* lattice_n entries */
+    wfst_stats stats;
+} wfst_result_summary;
+
+int wfst_result_summaries(const wfst_result *const *results, int32_t n, int32_t want_lattice,
+                          wfst_result_summary *out);
+
 /* Release a result (NULL is allowed). */
 void wfst_result_free(wfst_result *r);
 

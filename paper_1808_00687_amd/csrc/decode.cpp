@@ -1489,10 +1489,11 @@ extern "C" int wfst_result_frames(const wfst_result *r, int32_t *num_frames, int
     return WFST_OK;
 }
 
-extern "C" int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs)
+namespace {
+
+// The result's lattice in the batch's host copy, made on first use.
+int lattice_host(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs, const char *who)
 {
-    clear_error();
-    if (!r) return fail(WFST_EINVAL, "wfst_result_lattice: NULL result");
     if (!r->lat_host) {
         if (n) *n = 0;
         if (arcs) *arcs = nullptr;
@@ -1507,7 +1508,7 @@ extern "C" int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_
                 DeviceGuard dg(r->lat_dev->device);
                 hipError_t e = hipMemcpy(h.arcs.data(), r->lat_dev->p, h.total * sizeof(wfst_lat_arc),
                                          hipMemcpyDeviceToHost);
-                if (e != hipSuccess) return hip_fail(e, "wfst_result_lattice: copy");
+                if (e != hipSuccess) return hip_fail(e, who);
             }
             h.loaded = true;
         }
@@ -1515,6 +1516,15 @@ extern "C" int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_
     if (n) *n = r->lat_n;
     if (arcs) *arcs = h.arcs.data() + r->lat_off;
     return WFST_OK;
+}
+
+}  // namespace
+
+extern "C" int wfst_result_lattice(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs)
+{
+    clear_error();
+    if (!r) return fail(WFST_EINVAL, "wfst_result_lattice: NULL result");
+    return lattice_host(r, n, arcs, "wfst_result_lattice: copy");
 }
 
 extern "C" int wfst_result_lattice_device(const wfst_result *r, int64_t *n, const wfst_lat_arc **arcs)
@@ -1562,6 +1572,39 @@ extern "C" int wfst_result_stats(const wfst_result *r, wfst_stats *stats)
     clear_error();
     if (!r || !stats) return fail(WFST_EINVAL, "wfst_result_stats: NULL argument");
     *stats = r->stats;
+    return WFST_OK;
+}
+
+extern "C" int wfst_result_summaries(const wfst_result *const *results, int32_t n, int32_t want_lattice,
+                                     wfst_result_summary *out)
+{
+    clear_error();
+    if (n < 0 || (n > 0 && (!results || !out))) return fail(WFST_EINVAL, "wfst_result_summaries: bad arguments");
+    for (int32_t i = 0; i < n; i++)
+        if (!results[i]) return fail(WFST_EINVAL, "wfst_result_summaries: NULL result");
+    for (int32_t i = 0; i < n; i++) {
+        const wfst_result *r = results[i];
+        wfst_result_summary &s = out[i];
+        s = wfst_result_summary{};
+        s.status = r->status;
+        s.num_frames = r->T;
+        s.num_decoded = r->Tp;
+        s.orig_frame = r->kept.data();
+        s.cost = std::numeric_limits<float>::quiet_NaN();
+        if (r->status == WFST_OK) {
+            s.cost = r->cost;
+            s.final_state = r->final_state;
+            s.reached_final = r->reached_final;
+            s.path_len = static_cast<int32_t>(r->path_arcs.size());
+            s.path_arcs = r->path_arcs.data();
+            s.path_frames = r->path_frames.data();
+        }
+        s.stats = r->stats;
+        if (want_lattice) {
+            const int rc = lattice_host(r, &s.lattice_n, &s.lattice, "wfst_result_summaries: lattice copy");
+            if (rc != WFST_OK) return rc;
+        }
+    }
     return WFST_OK;
 }
 

@@ -81,6 +81,15 @@ class _LatArc(C.Structure):
     _fields_ = [("frame", C.c_int32), ("arc", C.c_int32), ("cost", C.c_float), ("extra", C.c_float)]
 
 
+class _Summary(C.Structure):
+    _fields_ = [("status", C.c_int32), ("num_frames", C.c_int32), ("num_decoded", C.c_int32),
+                ("path_len", C.c_int32), ("cost", C.c_float), ("final_state", C.c_int32),
+                ("reached_final", C.c_int32), ("reserved", C.c_int32),
+                ("orig_frame", C.POINTER(C.c_int32)), ("path_arcs", C.POINTER(C.c_int32)),
+                ("path_frames", C.POINTER(C.c_int32)), ("lattice_n", C.c_int64),
+                ("lattice", C.POINTER(_LatArc)), ("stats", _Stats)]
+
+
 class _NoallocOut(C.Structure):
     _fields_ = [("path_arcs", C.c_void_p), ("path_frames", C.c_void_p), ("path_cap", C.c_int32),
                 ("lattice", C.c_void_p), ("lattice_cap", C.c_int64), ("kept", C.c_void_p), ("kept_cap", C.c_int32),
@@ -128,6 +137,8 @@ def _load_lib():
     lib.wfst_result_words.restype = C.c_int
     lib.wfst_result_stats.argtypes = [vp, C.POINTER(_Stats)]
     lib.wfst_result_stats.restype = C.c_int
+    lib.wfst_result_summaries.argtypes = [C.POINTER(vp), C.c_int32, C.c_int32, C.POINTER(_Summary)]
+    lib.wfst_result_summaries.restype = C.c_int
     lib.wfst_result_free.argtypes = [vp]
     lib.wfst_result_free.restype = None
     lib.wfst_decode_noalloc.argtypes = [vp, vp, C.c_int32, C.c_int32, C.POINTER(_Opts), vp, C.POINTER(_NoallocOut)]
@@ -283,16 +294,18 @@ def _arr(ptr, n, dt):
     return a
 
 
-def _lattice_views(outs) -> list:
+def _lattice_views(outs, spans=None) -> list:
     """Each result's lattice as an [n x 4] int32 view of one host copy: the
     lattices of a batch lie in one host buffer the results share, copied here
-    once instead of once per result."""
-    spans = []
-    for h in outs:
-        ln = C.c_int64()
-        la = C.POINTER(_LatArc)()
-        _check(_lib.wfst_result_lattice(h, C.byref(ln), C.byref(la)), "wfst_result_lattice")
-        spans.append((C.cast(la, C.c_void_p).value or 0, ln.value))
+    once instead of once per result.  spans: (address, arcs) of each result's
+    lattice when the caller has them already."""
+    if spans is None:
+        spans = []
+        for h in outs:
+            ln = C.c_int64()
+            la = C.POINTER(_LatArc)()
+            _check(_lib.wfst_result_lattice(h, C.byref(ln), C.byref(la)), "wfst_result_lattice")
+            spans.append((C.cast(la, C.c_void_p).value or 0, ln.value))
     live = [(p, m) for p, m in spans if m > 0 and p]
     if not live:
         return [np.zeros((0, 4), np.int32)] * len(spans)
@@ -306,27 +319,37 @@ def _lattice_views(outs) -> list:
     return views
 
 
-def _collect(h, lattice: bool, tokens: bool, lat=None, words: bool = False) -> WfstResult:
-    st = _lib.wfst_result_status(h)
+def _collect(h, lattice: bool, tokens: bool, lat=None, words: bool = False, sm=None) -> WfstResult:
+    """The result behind handle h; sm: its wfst_result_summaries entry, when
+    the caller has fetched those for the batch (else per-result calls)."""
+    if sm is None:
+        st = _lib.wfst_result_status(h)
+        nf, nd = C.c_int32(), C.c_int32()
+        kp = C.POINTER(C.c_int32)()
+        _check(_lib.wfst_result_frames(h, C.byref(nf), C.byref(nd), C.byref(kp)), "wfst_result_frames")
+        num_frames, num_decoded = nf.value, nd.value
+        s = _Stats()
+        _check(_lib.wfst_result_stats(h, C.byref(s)), "wfst_result_stats")
+    else:
+        st, num_frames, num_decoded, kp, s = sm.status, sm.num_frames, sm.num_decoded, sm.orig_frame, sm.stats
     r = WfstResult(status=st)
-    nf, nd = C.c_int32(), C.c_int32()
-    kp = C.POINTER(C.c_int32)()
-    _check(_lib.wfst_result_frames(h, C.byref(nf), C.byref(nd), C.byref(kp)), "wfst_result_frames")
-    r.num_frames, r.num_decoded = nf.value, nd.value
-    r.kept = _arr(kp, nd.value, np.int32)
-    s = _Stats()
-    _check(_lib.wfst_result_stats(h, C.byref(s)), "wfst_result_stats")
+    r.num_frames, r.num_decoded = num_frames, num_decoded
+    r.kept = _arr(kp, num_decoded, np.int32)
     r.stats = {f: getattr(s, f) for f in _STAT_FIELDS}
     r.stats["search_phase_ms"] = list(s.search_phase_ms)
     if st != WFST_OK:
         return r
-    cost, fs, rf, n = C.c_float(), C.c_int32(), C.c_int32(), C.c_int32()
-    pa, pf = C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)()
-    _check(_lib.wfst_result_best(h, C.byref(cost), C.byref(fs), C.byref(rf), C.byref(n),
-                                 C.byref(pa), C.byref(pf)), "wfst_result_best")
-    r.cost, r.final_state, r.reached_final = float(np.float32(cost.value)), fs.value, rf.value
-    r.path_arcs = _arr(pa, n.value, np.int32)
-    r.path_frames = _arr(pf, n.value, np.int32)
+    if sm is None:
+        cost, fs, rf, n = C.c_float(), C.c_int32(), C.c_int32(), C.c_int32()
+        pa, pf = C.POINTER(C.c_int32)(), C.POINTER(C.c_int32)()
+        _check(_lib.wfst_result_best(h, C.byref(cost), C.byref(fs), C.byref(rf), C.byref(n),
+                                     C.byref(pa), C.byref(pf)), "wfst_result_best")
+        cost, fs, rf, n = cost.value, fs.value, rf.value, n.value
+    else:
+        cost, fs, rf, n, pa, pf = sm.cost, sm.final_state, sm.reached_final, sm.path_len, sm.path_arcs, sm.path_frames
+    r.cost, r.final_state, r.reached_final = float(np.float32(cost)), fs, rf
+    r.path_arcs = _arr(pa, n, np.int32)
+    r.path_frames = _arr(pf, n, np.int32)
     if lattice:
         if lat is None:
             lat = _lattice_views([h])[0]
@@ -449,9 +472,18 @@ def wfst_decode_batch(graph: WfstGraph, loglikes: Sequence, beam: float, max_act
     _check(rc, "wfst_decode_batch")
     res = []
     try:
-        lats = _lattice_views(outs) if lattice_beam >= 0 else [None] * n
-        for h, lat in zip(outs, lats):
-            res.append(_collect(h, lattice_beam >= 0, record_tokens, lat, word_lattice))
+        # the results' fields in one call (per-result calls cost more than
+        # their work for a batch of short results)
+        summ = (_Summary * n)()
+        want_lat = lattice_beam >= 0
+        _check(_lib.wfst_result_summaries(outs, n, 1 if want_lat else 0, summ), "wfst_result_summaries")
+        sms = list(summ)
+        if want_lat:
+            lats = _lattice_views(outs, [(C.cast(sm.lattice, C.c_void_p).value or 0, sm.lattice_n) for sm in sms])
+        else:
+            lats = [None] * n
+        for h, lat, sm in zip(outs, lats, sms):
+            res.append(_collect(h, want_lat, record_tokens, lat, word_lattice, sm))
     finally:
         for h in outs:
             _lib.wfst_result_free(h)

@@ -97,7 +97,8 @@ def test_ctypes_structs_match_the_header(tmp_path):
     from paper_1808_00687_amd import wfstdec
     mirrors = {"wfst_decode_opts": wfstdec._Opts, "wfst_stats": wfstdec._Stats,
                "wfst_graph_info": wfstdec._Info, "wfst_lat_arc": wfstdec._LatArc,
-               "wfst_debug_opts": wfstdec._DebugOpts, "wfst_noalloc_out": wfstdec._NoallocOut}
+               "wfst_debug_opts": wfstdec._DebugOpts, "wfst_noalloc_out": wfstdec._NoallocOut,
+               "wfst_result_summary": wfstdec._Summary}
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "wfstdec.h"', "int main(void) {"]
     for cname, py in mirrors.items():
         lines.append('printf("%s size %%zu\\n", sizeof(%s));' % (cname, cname))
@@ -141,3 +142,16 @@ def test_noalloc_rejects_bad_arguments_on_the_host():
     d = wfstdec._NoallocOut()
     assert lib.wfst_decode_noalloc(None, None, 0, 1, ctypes.byref(o), None, ctypes.byref(d)) == wfstdec.WFST_EINVAL
     assert lib.wfst_decode_noalloc(None, None, 0, 1, None, None, None) == wfstdec.WFST_EINVAL
+
+
+def test_result_summaries_reject_bad_arguments_on_the_host():
+    # the batched result accessor checks its arguments before touching a result
+    import ctypes
+    from paper_1808_00687_amd import wfstdec
+    s = (wfstdec._Summary * 1)()
+    lib = wfstdec._lib
+    assert lib.wfst_result_summaries(None, 1, 0, s) == wfstdec.WFST_EINVAL
+    outs = (ctypes.c_void_p * 1)()
+    assert lib.wfst_result_summaries(outs, 1, 0, s) == wfstdec.WFST_EINVAL
+    assert lib.wfst_result_summaries(outs, -1, 0, s) == wfstdec.WFST_EINVAL
+    assert lib.wfst_result_summaries(outs, 0, 1, None) == wfstdec.WFST_OK
