@@ -246,6 +246,28 @@ def test_lattice_streamed_pass(dec, torch_mod, oracle_mod, cfg2, mode):
         parity.assert_same(ro, rg, lattice=True, tag="streamed pass %d seed %d" % (mode, seed))
 
 
+@pytest.mark.parametrize("seed", range(30))
+def test_lattice_passes_on_random_graphs(dec, torch_mod, oracle_mod, seed):
+    # random graphs of 40-2,500 states with up to 45% epsilon arcs, finite
+    # and infinite beams: the streamed lattice pass forced wherever it fits,
+    # and the passes the rules pick otherwise, against the oracle
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(40, 2500))
+    g = W.random_small_graph(5000 + seed, n, mean_deg=float(rng.uniform(1.5, 4.0)),
+                             eps_frac=float(rng.uniform(0.0, 0.45)), num_labels=5,
+                             weights=["int", "exp", "dyadic"][seed % 3], final=bool(seed % 4 == 1))
+    ll = W.random_small_loglikes(5000 + seed, int(rng.integers(1, 60)), 5,
+                                 kind={0: "int", 1: "gauss", 2: "dyadic"}[seed % 3])
+    kw = dict(beam=[INF, 6.0, 10.0, 14.0][seed % 4], max_active=[0, 0, 50, 400][(seed // 4) % 4],
+              lattice_beam=[2.0, 5.0, INF][seed % 3])
+    gh = dec.load_graph(g)
+    for mode in (1, 0):
+        with dec.debug_opts(lattice_pipe=mode):
+            ro, rg = both(dec, torch_mod, oracle_mod, g, ll, gh=gh, **kw)
+        parity.assert_same(ro, rg, lattice=True, tag="seed %d lattice_pipe %d" % (seed, mode))
+    gh.free()
+
+
 @pytest.mark.parametrize("form", ["one-wave", "streamed"])
 def test_lattice_pass_gives_up(dec, torch_mod, oracle_mod, cfg2, form):
     # the lattice passes' hand-over waits are bounded: with one poll allowed
