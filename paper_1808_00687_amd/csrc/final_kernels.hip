@@ -124,10 +124,10 @@ __device__ void backtrace_block(const Params &p, int u, int *sh)
 // s_waitcnt immediate: vmcnt(0), the other counters left free
 constexpr int kWaitVm0 = 0x0F70;
 constexpr int kLatLds = 8192;   // survivors per token set kept in LDS by the backward pass
-constexpr int kLatT = 768;      // threads of a finish block
-constexpr int kRE = 3;          // emitting records per thread held in registers
-constexpr int kRX = 2;          // epsilon records per thread held in registers
-constexpr int kRC = 4;          // survivors per thread held in registers
+constexpr int kLatT = 1024;     // threads of a finish block
+constexpr int kRE = 1;          // emitting records per thread held in registers
+constexpr int kRX = 1;          // epsilon records per thread held in registers
+constexpr int kRC = 1;          // survivors per thread held in registers
 
 // Where the records and survivors of one token set j lie.
 struct LatMeta {
@@ -491,8 +491,8 @@ __device__ void lattice_sets(const Params &p, int u, uint32_t *s_e, float *s_c, 
 // ---------------------------------------------------------------------------
 // The backward pass of an utterance whose token sets all hold at most
 // kSmallSet survivors, emitting records and epsilon records (the CTC-style
-// configurations).  The block pass spends a set's time mostly on a dozen
-// waves' bookkeeping and barriers, whatever the set's size.  Here one wave
+// configurations).  The block pass spends a set's time mostly on its waves'
+// bookkeeping and barriers, whatever the set's size.  Here one wave
 // (wave 0) computes the nodes' extra costs set after set from LDS alone,
 // while the block's other waves load the coming sets into a ring of LDS
 // slots; each slot is handed over with a workgroup-scope flag, filled after
@@ -718,8 +718,8 @@ __device__ void lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c)
 // 8-byte entry: the source's and destination's offsets in their sets and the
 // record's first difference fl(p - c(d)), which the loading waves compute
 // from device memory.  Every set's place in the stream is the prefix of the
-// sizes before it, computed up front, so the loading waves (wave w takes the
-// sets w-1, w-1+11, ...) write side by side into a ring of LDS entries, 512
+// sizes before it, computed up front, so the loading waves (wave w of W takes
+// the sets w-1, w-1+(W-1), ...) write side by side into a ring of LDS entries, 512
 // at a time, each piece once wave 0 has read what those ring positions held
 // before.  Wave 0 takes the sets in order and the pieces as they arrive; it
 // computes the nodes' extra costs as the block pass does and, on the way,
@@ -735,7 +735,7 @@ __device__ void lattice_small(const Params &p, int u, uint32_t *s_e, float *s_c)
 constexpr int kPipeCap = 8192;     // ring entries (8 bytes each): the cost half of the LDS
 constexpr int kPipePiece = 512;    // entries per hand-over (8 per lane)
 constexpr int kPipeSlots = 32;     // sets described ahead of wave 0
-constexpr int kPipeAvg = 640;      // stream entries per set up to which the pass beats the block pass
+constexpr int kPipeAvg = 480;      // stream entries per set up to which the pass beats the block pass
 static_assert(kPipeCap * sizeof(uint2) == 2 * kLatLds * sizeof(float), "the ring is the cost half of the LDS");
 static_assert(kLatLds <= 65536, "a survivor's offset in its set fits 16 bits");
 
